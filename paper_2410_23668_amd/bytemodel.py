@@ -1,0 +1,56 @@
+"""Bytes and FLOPs of one decode step (the roofline model of the bench).
+
+Two conventions:
+
+* ``paper_table1`` is the paper's operation-intensity model (Sec. 1,
+  Table 1): every parameter and every cached KV value is read once per
+  token step; parameters are counted from the nominal model size at 2 bytes
+  each and reported in GiB; FLOPs are 2 per parameter plus 4 per
+  (layer, query head, head dim, cached position) for attention, times the
+  batch.
+* ``step_bytes`` / ``step_flops`` are the exact algorithmic counts of the
+  step this library runs: all layer weights and norm gains, the final norm
+  and LM head, one embedding row per sequence, the KV read over the cached
+  positions, the KV write of the new slot and the fp32 logits.  The unread
+  rows of the embedding table are not counted.  ``step_bytes`` divided by the
+  step time is the achieved HBM bandwidth the bench reports against the
+  8 TB/s peak (the "% of peak" form of Sec. 4.4).
+"""
+from __future__ import annotations
+
+GIB = float(1 << 30)
+
+
+def paper_table1(n_params: float, n_layers: int, n_kv_heads: int, head_dim: int,
+                 n_heads: int, batch: int, context: int) -> dict:
+    params_gib = n_params * 2 / GIB
+    kv_gib = batch * n_layers * 2 * n_kv_heads * head_dim * 2 * context / GIB
+    gflops = batch * (2 * n_params + 4 * n_layers * n_heads * head_dim * context) / 1e9
+    gbytes = params_gib + kv_gib
+    return dict(params_gib=params_gib, kv_gib=kv_gib, gflops=gflops, gbytes=gbytes,
+                flops_per_byte=gflops / gbytes)
+
+
+def layer_weight_bytes(cfg) -> int:
+    H, nq, nkv, d, F = (cfg[k] for k in ("hidden", "n_heads", "n_kv_heads", "head_dim", "ffn_dim"))
+    return 2 * (H * nq * d + 2 * H * nkv * d + nq * d * H + 3 * H * F + 2 * H)
+
+
+def step_bytes(cfg, batch: int, context: int) -> int:
+    """Algorithmic HBM bytes of one step; ``context`` cached positions per sequence."""
+    L, H, nkv, d, V = (cfg[k] for k in ("n_layers", "hidden", "n_kv_heads", "head_dim", "vocab"))
+    weights = L * layer_weight_bytes(cfg) + 2 * (V * H + H)
+    embed_rows = batch * 2 * H
+    kv_read = batch * L * 2 * nkv * d * 2 * context
+    kv_write = batch * L * 2 * nkv * d * 2
+    logits = batch * V * 4
+    return weights + embed_rows + kv_read + kv_write + logits
+
+
+def step_flops(cfg, batch: int, context: int) -> int:
+    """2 FLOPs per weight MAC per sequence plus 4 * n_heads * d * (context + 1) per layer."""
+    L, H, nq, nkv, d, F, V = (cfg[k] for k in ("n_layers", "hidden", "n_heads", "n_kv_heads",
+                                                 "head_dim", "ffn_dim", "vocab"))
+    macs = L * (H * nq * d + 2 * H * nkv * d + nq * d * H + 3 * H * F) + V * H
+    attn = L * 4 * nq * d * (context + 1)
+    return batch * (2 * macs + attn)

@@ -1,0 +1,32 @@
+"""The decode-step workloads, by name, with their shapes and seeds.
+
+Shapes are Llama-style decoder-only models (the paper evaluates Llama 3.1
+8B/70B decode, Table 1 and Table 2).  Weights are seeded synthetic stand-ins
+for trained checkpoints; decode cost does not depend on the values.
+"""
+from __future__ import annotations
+
+TINY = dict(n_layers=4, hidden=256, n_heads=4, n_kv_heads=2, head_dim=64, ffn_dim=688,
+            vocab=1024, rope_theta=10000.0, rms_eps=1e-5)
+LLAMA8B = dict(n_layers=32, hidden=4096, n_heads=32, n_kv_heads=8, head_dim=128, ffn_dim=14336,
+               vocab=128256, rope_theta=500000.0, rms_eps=1e-5)
+LLAMA70B = dict(n_layers=80, hidden=8192, n_heads=64, n_kv_heads=8, head_dim=128, ffn_dim=28672,
+                vocab=128256, rope_theta=500000.0, rms_eps=1e-5)
+
+
+def _wl(name, model, batch, context, index):
+    return dict(name=name, model=dict(model), batch=batch, context=context,
+                # new token sits at position = context; capacity rounded up to 64
+                capacity=((context + 1 + 63) // 64) * 64,
+                seed_weights=1 + 1000 * index, seed_kv=2 + 1000 * index,
+                seed_tokens=3 + 1000 * index)
+
+
+WORKLOADS = {
+    "tiny-b1-ctx128": _wl("tiny-b1-ctx128", TINY, 1, 128, 0),
+    "llama8b-b1-ctx4096": _wl("llama8b-b1-ctx4096", LLAMA8B, 1, 4096, 1),
+    "llama8b-b32-ctx4096": _wl("llama8b-b32-ctx4096", LLAMA8B, 32, 4096, 2),
+    "llama8b-b1-ctx65536": _wl("llama8b-b1-ctx65536", LLAMA8B, 1, 65536, 3),
+    "llama70b-b1-ctx4096": _wl("llama70b-b1-ctx4096", LLAMA70B, 1, 4096, 4),
+    "llama70b-b32-ctx4096": _wl("llama70b-b32-ctx4096", LLAMA70B, 32, 4096, 4),
+}

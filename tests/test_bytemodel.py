@@ -1,0 +1,54 @@
+"""The bench's byte/FLOP model against the paper's Table 1 (CPU only)."""
+import json
+import os
+
+import pytest
+
+from paper_2410_23668_amd import bytemodel as bm
+from synth.workloads import WORKLOADS
+
+GOLD = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "paper_table1.json")))
+
+
+@pytest.mark.parametrize("row", GOLD["rows"], ids=lambda r: f"{r[0]}-b{r[1]}-{r[2]}")
+def test_table1_parameters_kv_and_bytes(row):
+    name, batch, ctx, params, kv, gflops, gbytes, fpb = row
+    m = GOLD["models"][name]
+    t = bm.paper_table1(m["n_params"], m["n_layers"], m["n_kv_heads"], m["head_dim"],
+                        m["n_heads"], batch, ctx)
+    assert t["params_gib"] == pytest.approx(params, rel=5e-3)
+    assert t["kv_gib"] == pytest.approx(kv, rel=5e-3)
+    assert t["gbytes"] == pytest.approx(gbytes, rel=5e-3)
+    # GFLOPs are printed after rounding (batch-32 rows are 32x the rounded
+    # batch-1 value); the 8B batch-1 4K cell prints 20 where the formula gives 18.1
+    assert t["gflops"] == pytest.approx(gflops, rel=0.11 if name == "8B" and ctx == 4096 else 0.02)
+    assert gflops / gbytes == pytest.approx(fpb, abs=0.051)
+
+
+def test_batch32_gflops_are_32x_batch1_as_printed():
+    rows = {(r[0], r[1], r[2]): r for r in GOLD["rows"]}
+    for (name, b, ctx), r in rows.items():
+        if b == 32:
+            assert r[5] == 32 * rows[(name, 1, ctx)][5]
+
+
+def test_step_bytes_decomposition_8b():
+    cfg = WORKLOADS["llama8b-b1-ctx4096"]["model"]
+    # per-layer weights: qkv 50.3 MB, o 33.5 MB, gate/up 234.9 MB, down 117.4 MB, norms
+    assert bm.layer_weight_bytes(cfg) == 2 * (4096 * 6144 + 4096 * 4096 + 3 * 4096 * 14336 + 2 * 4096)
+    b = bm.step_bytes(cfg, 1, 4096)
+    assert b == 15_547_372_544
+    # the paper's all-parameters convention (Sec. 1) also counts the unread
+    # embedding rows and leaves out the KV write and the logits
+    paper = 32 * bm.layer_weight_bytes(cfg) + 2 * (2 * 128256 * 4096 + 4096) + 32 * 2 * 8 * 128 * 2 * 4096
+    assert paper == 16_597_393_408
+    assert b == paper - 2 * 128256 * 4096 + 2 * 4096 + 32 * 2 * 8 * 128 * 2 + 4 * 128256
+    assert bm.step_bytes(cfg, 32, 4096) == 32_210_591_744
+    assert bm.step_bytes(cfg, 1, 65536) == 23_600_436_224
+
+
+def test_step_flops_counts_two_per_mac():
+    cfg = dict(n_layers=1, hidden=2, n_heads=1, n_kv_heads=1, head_dim=2, ffn_dim=3, vocab=5)
+    macs = 2 * 2 + 2 * 2 * 2 + 2 * 2 + 3 * 2 * 3 + 5 * 2
+    assert bm.step_flops(cfg, 1, 0) == 2 * macs + 4 * 2 * 1
+    assert bm.step_flops(cfg, 3, 4) == 3 * (2 * macs + 4 * 2 * 5)

@@ -1,0 +1,276 @@
+"""Pins of the CPU oracle to the mathematics (CPU only).
+
+Each test checks the oracle against something other than itself: a library
+routine for a special case, a closed form, an invariant, or an independent
+brute-force evaluation on tiny inputs.  They are chosen so that a plausible
+slip (a dropped term, a wrong sign or index, a transposed operand, a wrong
+head group) fails at least one of them.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from tests import bruteforce
+
+RNG = np.random.default_rng(1234)
+
+
+def bf(x):
+    return bruteforce.bf16_encode(np.asarray(x, dtype=np.float64))
+
+
+# ---------------------------------------------------------------- bf16 format
+
+def test_bf16_decode_matches_torch():
+    h = RNG.integers(0, 1 << 16, size=20000, dtype=np.uint16)
+    h = h[(h & 0x7F80) != 0x7F80]                      # finite patterns only
+    np.testing.assert_array_equal(oracle.bf16_to_f64(h), bruteforce.bf16_decode(h))
+
+
+def test_bf16_encode_matches_torch_on_float32_values():
+    # float32 inputs are exact in double, so torch's RNE conversion is the reference
+    x = np.concatenate([
+        RNG.standard_normal(20000).astype(np.float32),
+        (RNG.standard_normal(2000) * 1e-39).astype(np.float32),     # subnormals
+        (RNG.standard_normal(2000) * 1e30).astype(np.float32),
+        np.array([1.0 + 1 / 256, 1.0 + 3 / 256, -(1.0 + 1 / 256), 2.0 ** -133, 0.0, -0.0,
+                  3.3895313892515355e38], dtype=np.float32),          # ties, tiny, max
+    ]).astype(np.float64)
+    ref = torch.from_numpy(x.astype(np.float32)).to(torch.bfloat16).view(torch.int16)
+    np.testing.assert_array_equal(oracle.f64_to_bf16(x), ref.numpy().view(np.uint16))
+
+
+def test_bf16_ties_go_to_even():
+    assert oracle.f64_to_bf16(np.array([1.0 + 1 / 256]))[0] == 0x3F80   # down to even
+    assert oracle.f64_to_bf16(np.array([1.0 + 3 / 256]))[0] == 0x3F82   # up to even
+    # just above a tie rounds up (a float-first conversion would lose this)
+    assert oracle.f64_to_bf16(np.array([1.0 + 1 / 256 + 2.0 ** -40]))[0] == 0x3F81
+
+
+# ---------------------------------------------------------------- RMSNorm
+
+def test_rmsnorm_constant_vector_closed_form():
+    n, c, eps = 64, -1.7, 1e-5
+    g = bf(1.0 + 0.1 * RNG.standard_normal(n))
+    u = oracle.rmsnorm(np.full(n, c), g, eps)
+    expect = c / math.sqrt(c * c + eps) * bruteforce.bf16_decode(g)
+    np.testing.assert_allclose(u, expect, rtol=1e-14, atol=0)
+
+
+def test_rmsnorm_one_hot_depends_on_length():
+    n, a, eps = 48, 3.0, 1e-2
+    x = np.zeros(n)
+    x[5] = a
+    u = oracle.rmsnorm(x, bf(np.ones(n)), eps)
+    assert u[5] == pytest.approx(a / math.sqrt(a * a / n + eps), rel=1e-14)
+    assert np.count_nonzero(u) == 1
+
+
+def test_rmsnorm_scale_invariant_without_eps():
+    x = RNG.standard_normal(100)
+    g = bf(1 + 0.01 * RNG.standard_normal(100))
+    np.testing.assert_allclose(oracle.rmsnorm(7.5 * x, g, 0.0), oracle.rmsnorm(x, g, 0.0),
+                               rtol=1e-13)
+
+
+# ---------------------------------------------------------------- GEMV
+
+def test_gemv_one_hot_selects_column_of_nonsquare_matrix():
+    w = bf(RNG.standard_normal((5, 7)))
+    wd = bruteforce.bf16_decode(w)
+    for j in range(7):
+        e = np.zeros(7)
+        e[j] = 1.0
+        np.testing.assert_array_equal(oracle.gemv(w, e), wd[:, j])
+
+
+def test_gemv_matches_library_matmul():
+    w = bf(RNG.standard_normal((33, 70)) * 0.02)
+    u = RNG.standard_normal(70)
+    np.testing.assert_allclose(oracle.gemv(w, u), bruteforce.bf16_decode(w) @ u, rtol=1e-12,
+                               atol=1e-15)
+    np.testing.assert_array_equal(oracle.gemv(w, u, nthreads=4), oracle.gemv(w, u, nthreads=1))
+
+
+# ---------------------------------------------------------------- RoPE
+
+@pytest.mark.parametrize("d,theta", [(64, 10000.0), (128, 500000.0)])
+def test_rope_identity_at_position_zero(d, theta):
+    y = RNG.standard_normal(d)
+    np.testing.assert_array_equal(oracle.rope(y, theta, 0), y)
+
+
+@pytest.mark.parametrize("d,theta,pos", [(64, 10000.0, 1), (64, 10000.0, 127),
+                                         (128, 500000.0, 4096), (128, 500000.0, 65536)])
+def test_rope_is_complex_rotation(d, theta, pos):
+    y = RNG.standard_normal(d)
+    ref = bruteforce.rotate(y[None, :], pos, theta)[0]
+    np.testing.assert_allclose(oracle.rope(y, theta, pos), ref, rtol=1e-12, atol=1e-12)
+
+
+def test_rope_preserves_norm_and_relative_position():
+    d, theta = 128, 10000.0
+    q, k = RNG.standard_normal(d), RNG.standard_normal(d)
+    for p in (3, 100, 5000):
+        assert np.linalg.norm(oracle.rope(q, theta, p)) == pytest.approx(np.linalg.norm(q), rel=1e-13)
+    for p, s in ((10, 3), (700, 699), (4096, 1)):
+        lhs = oracle.rope(q, theta, p) @ oracle.rope(k, theta, s)
+        rhs = oracle.rope(q, theta, p - s) @ k
+        assert lhs == pytest.approx(rhs, rel=1e-10, abs=1e-10)
+
+
+# ---------------------------------------------------------------- softmax / attention
+
+def test_softmax_closed_form_and_sum():
+    a = oracle.softmax(np.array([0.0, math.log(3.0)]))
+    np.testing.assert_allclose(a, [0.25, 0.75], rtol=1e-15)
+    s = RNG.standard_normal(1000) * 30
+    assert oracle.softmax(s).sum() == pytest.approx(1.0, abs=1e-14)
+    np.testing.assert_allclose(oracle.softmax(s + 1234.5), oracle.softmax(s), rtol=1e-12)
+
+
+def _cache(nkv, cap, d, scale=1.0):
+    return bf(RNG.standard_normal((nkv, cap, d)) * scale), bf(RNG.standard_normal((nkv, cap, d)))
+
+
+def test_attention_single_key_returns_value_of_group():
+    nq, nkv, d, cap = 8, 2, 16, 4
+    K, V = _cache(nkv, cap, d)
+    o = oracle.attention(RNG.standard_normal((nq, d)), K, V, pos=0)
+    Vd = bruteforce.bf16_decode(V)
+    for h in range(nq):
+        np.testing.assert_array_equal(o[h], Vd[h // (nq // nkv), 0])
+
+
+def test_attention_zero_query_is_mean_of_values():
+    nq, nkv, d, cap, pos = 4, 4, 8, 16, 9
+    K, V = _cache(nkv, cap, d)
+    o = oracle.attention(np.zeros((nq, d)), K, V, pos)
+    np.testing.assert_allclose(o, bruteforce.bf16_decode(V)[:, : pos + 1].mean(axis=1),
+                               rtol=1e-13)
+
+
+def test_attention_two_keys_closed_form_with_scale():
+    d = 4
+    K = np.zeros((1, 2, d), dtype=np.uint16)
+    K[0, 1, 0] = bf(np.array([2.0]))[0]
+    V = bf(np.array([[[1.0, 0, 0, 0], [0, 1.0, 0, 0]]]))
+    q = np.array([[1.5, 0, 0, 0]])
+    s1 = 1.5 * 2.0 / math.sqrt(d)                # scaled score of key 1; key 0 scores 0
+    w1 = math.exp(s1) / (1 + math.exp(s1))
+    o = oracle.attention(q, K, V, pos=1)
+    np.testing.assert_allclose(o[0], [1 - w1, w1, 0, 0], rtol=1e-14)
+
+
+def test_attention_gqa_equals_mha_with_repeated_kv():
+    nq, nkv, d, cap, pos = 8, 2, 16, 12, 10
+    K, V = _cache(nkv, cap, d, scale=0.5)
+    q = RNG.standard_normal((nq, d))
+    grp = nq // nkv
+    o_gqa = oracle.attention(q, K, V, pos)
+    o_mha = oracle.attention(q, np.repeat(K, grp, axis=0), np.repeat(V, grp, axis=0), pos)
+    np.testing.assert_array_equal(o_gqa, o_mha)
+
+
+def test_attention_ignores_slots_after_pos_and_order_of_slots():
+    nq, nkv, d, cap, pos = 4, 2, 8, 20, 11
+    K, V = _cache(nkv, cap, d)
+    q = RNG.standard_normal((nq, d))
+    o = oracle.attention(q, K, V, pos)
+    K2, V2 = K.copy(), V.copy()
+    K2[:, pos + 1:] = bf(np.full(1, 1e30))[0]
+    V2[:, pos + 1:] = bf(np.full(1, -1e30))[0]
+    np.testing.assert_array_equal(oracle.attention(q, K2, V2, pos), o)
+    perm = RNG.permutation(pos + 1)
+    K3, V3 = K.copy(), V.copy()
+    K3[:, : pos + 1] = K[:, perm]
+    V3[:, : pos + 1] = V[:, perm]
+    np.testing.assert_allclose(oracle.attention(q, K3, V3, pos), o, rtol=1e-12, atol=1e-14)
+
+
+# ---------------------------------------------------------------- SwiGLU
+
+def test_swiglu_closed_forms():
+    np.testing.assert_array_equal(oracle.swiglu(np.zeros(5), RNG.standard_normal(5)), np.zeros(5))
+    m = oracle.swiglu(np.array([1.0, 2.0, -3.0]), np.array([2.0, 1.0, 0.5]))
+    silu = lambda z: z / (1 + math.exp(-z))
+    np.testing.assert_allclose(m, [silu(1.0) * 2.0, silu(2.0) * 1.0, silu(-3.0) * 0.5],
+                               rtol=1e-15)
+    assert m[0] != m[1]                          # gate and up are not interchangeable
+
+
+# ---------------------------------------------------------------- whole step
+
+SMALL = dict(n_layers=2, hidden=16, n_heads=4, n_kv_heads=2, head_dim=4, ffn_dim=24, vocab=32,
+             rope_theta=10000.0, rms_eps=1e-5)
+
+
+def _small_inputs(cfg, batch, cap, positions, seed=7):
+    model = synth.model_host(cfg, seed, nthreads=1)
+    K, V = synth.kv_cache_host(cfg, seed + 1, batch, cap, positions, nthreads=1)
+    toks = synth.tokens(cfg, seed + 2, batch)
+    return model, K, V, toks
+
+
+def test_step_with_zero_updates_keeps_embedding_and_closed_form_logits():
+    cfg = dict(SMALL)
+    model, K, V, toks = _small_inputs(cfg, 2, 8, [3, 5])
+    for lay in model["layers"]:
+        lay["wo"][:] = 0
+        lay["w_down"][:] = 0
+    logits, hidden = oracle.decode_step(cfg, model, toks, [3, 5], K, V)
+    E = bruteforce.bf16_decode(model["embed"])
+    for b, t in enumerate(toks):
+        np.testing.assert_array_equal(hidden[b], E[t])
+        u = bruteforce.rms_normalise(E[t], bruteforce.bf16_decode(model["final_norm"]),
+                                     cfg["rms_eps"])
+        np.testing.assert_allclose(logits[b], bruteforce.bf16_decode(model["lm_head"]) @ u,
+                                   rtol=1e-12, atol=1e-15)
+
+
+@pytest.mark.parametrize("cfg_over,positions,cap", [
+    ({}, [3, 5], 8),
+    ({"n_heads": 4, "n_kv_heads": 4}, [0, 7], 8),
+    ({"n_heads": 6, "n_kv_heads": 2, "head_dim": 8, "hidden": 24, "n_layers": 3}, [1, 2], 4),
+])
+def test_step_matches_independent_brute_force(cfg_over, positions, cap):
+    cfg = dict(SMALL, **cfg_over)
+    model, K, V, toks = _small_inputs(cfg, len(positions), cap, positions)
+    K2, V2 = K.copy(), V.copy()
+    logits, hidden = oracle.decode_step(cfg, model, toks, positions, K, V)
+    lref, href = bruteforce.decode_step(cfg, model, toks, positions, K2, V2)
+    assert oracle.rel_l2(logits, lref) < 1e-12
+    assert oracle.rel_l2(hidden, href) < 1e-12
+    np.testing.assert_array_equal(K, K2)
+    np.testing.assert_array_equal(V, V2)
+
+
+def test_step_sequences_are_independent_and_thread_count_free():
+    cfg = dict(SMALL)
+    model, K, V, toks = _small_inputs(cfg, 2, 8, [3, 6])
+    Kb, Vb = K.copy(), V.copy()
+    logits, hidden = oracle.decode_step(cfg, model, toks, [3, 6], K, V, nthreads=3)
+    for b, p in enumerate([3, 6]):
+        Ks, Vs = Kb[:, b:b + 1].copy(), Vb[:, b:b + 1].copy()
+        ls, hs = oracle.decode_step(cfg, model, toks[b:b + 1], [p], Ks, Vs, nthreads=1)
+        np.testing.assert_array_equal(ls[0], logits[b])
+        np.testing.assert_array_equal(hs[0], hidden[b])
+        np.testing.assert_array_equal(Ks[:, 0], K[:, b])
+
+
+def test_step_is_idempotent_and_rejects_bad_token():
+    cfg = dict(SMALL)
+    model, K, V, toks = _small_inputs(cfg, 1, 8, [4])
+    l1, h1 = oracle.decode_step(cfg, model, toks, [4], K, V)
+    K1, V1 = K.copy(), V.copy()
+    l2, h2 = oracle.decode_step(cfg, model, toks, [4], K, V)
+    np.testing.assert_array_equal(l1, l2)
+    np.testing.assert_array_equal(K1, K)
+    with pytest.raises(ValueError):
+        oracle.decode_step(cfg, model, np.array([cfg["vocab"]]), [4], K, V)
+    with pytest.raises(ValueError):
+        oracle.decode_step(cfg, model, toks, [8], K, V)
