@@ -1,0 +1,158 @@
+#!/usr/bin/env python3
+"""Decode-step benchmark on one MI355X.
+
+One step = one decode step of the whole model (embedding, all decoder layers,
+final norm + LM head) for every sequence of the batch, on seeded synthetic
+weights and KV cache already resident in HBM.  The headline is the looped
+(kernel-looping) schedule; the per-layer schedule is timed beside it.
+
+Prints ONE JSON line with tokens/s, step latency, achieved HBM bandwidth of
+the step kernel (algorithmic bytes / mean launch duration, HIP events on the
+launch stream) against the 8 TB/s peak, and the CPU oracle timed on a
+bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "decode tok/s + achieved HBM TB/s vs peak, 8B-shape batch 1 ctx 4096"
+PEAK_HBM_GBS = 8000.0
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def time_mode(model, toks, pos, kv, logits, mode, steps, warmup):
+    import torch
+    for _ in range(warmup):
+        model.step(toks, pos, kv, logits, None, mode)
+    torch.cuda.synchronize()
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        starts[i].record()
+        model.step(toks, pos, kv, logits, None, mode)
+        ends[i].record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per = sorted(s.elapsed_time(e) for s, e in zip(starts, ends))   # ms
+    mean = sum(per) / len(per)
+    return dict(mean_ms=mean, median_ms=per[len(per) // 2], p10_ms=per[len(per) // 10],
+                p90_ms=per[(9 * len(per)) // 10], wall_ms_per_step=1e3 * wall / steps)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="llama8b-b1-ctx4096")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--modes", default="looped,per_layer",
+                    help="schedules to time; the first is the headline")
+    ap.add_argument("--threads", type=int, default=0, help="host threads for input generation")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2410_23668_amd import binding as kb
+    from paper_2410_23668_amd import bytemodel
+    from paper_2410_23668_amd.device import GpuModel, KvCache
+    from synth.workloads import WORKLOADS
+
+    wl = WORKLOADS[args.workload]
+    cfg, B, P, cap = wl["model"], wl["batch"], wl["context"], wl["capacity"]
+    nthr = args.threads or synth.default_threads()
+    torch.cuda.set_device(0)
+
+    log(f"workload {args.workload}: generating weights ({nthr} threads)")
+    t = time.perf_counter()
+    weights = synth.model_host(cfg, wl["seed_weights"], nthr)
+    K0, V0 = synth.kv_cache_host(cfg, wl["seed_kv"], B, cap, [P] * B, nthr)
+    tokens = synth.tokens(cfg, wl["seed_tokens"], B)
+    log(f"inputs ready in {time.perf_counter() - t:.1f}s; loading model")
+    model = GpuModel(cfg, weights, B, cap)
+    kv = KvCache(cfg, B, cap, k_host=K0, v_host=V0)
+    toks = torch.from_numpy(tokens).cuda()
+    pos = torch.full((B,), P, dtype=torch.int32, device="cuda")
+    logits = torch.empty((B, cfg["vocab"]), dtype=torch.float32, device="cuda")
+    info = model.info()
+
+    modes = [m.strip() for m in args.modes.split(",") if m.strip()]
+    res = {}
+    for m in modes:
+        log(f"timing mode {m}: {args.warmup} warmup + {args.steps} steps")
+        res[m] = time_mode(model, toks, pos, kv, logits, kb.MODES[m], args.steps, args.warmup)
+        log(f"  {m}: mean {res[m]['mean_ms']:.3f} ms/step")
+    err = model.device_error()
+    if err:
+        log(f"device error word {err:#x}")
+        sys.exit(1)
+
+    head = modes[0]
+    step_ms = res[head]["mean_ms"]
+    nbytes = bytemodel.step_bytes(cfg, B, P)
+    achieved = nbytes / (step_ms * 1e-3) / 1e9      # GB/s
+    out = {
+        "metric": METRIC,
+        "value": B / (step_ms * 1e-3),
+        "unit": "tok/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": step_ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "accum_dtype": "f32",
+        "data": "synthetic (seeded N(0,0.02) weights, N(0,1) KV)",
+        "config": {"workload": args.workload, "batch": B, "context": P, "mode": head},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": achieved / PEAK_HBM_GBS, "traffic": None,
+                     "algorithmic_bytes_per_launch": nbytes,
+                     "kernel": "kl_step_kernel (one launch per step)"},
+        "modes": {m: r for m, r in res.items()},
+        "dispatches_per_step": {"looped": 1, "per_layer": cfg["n_layers"] + 2,
+                                "per_op": 5 * cfg["n_layers"] + 2},
+        "grid": {"workgroups": info.n_workgroups, "threads": info.threads_per_group,
+                 "lds_bytes": info.lds_bytes},
+    }
+    if "per_layer" in res and head != "per_layer":
+        out["speedup_vs_per_layer"] = res["per_layer"]["mean_ms"] / step_ms
+
+    # parity of the timed output, and the oracle's own time on the host
+    if not args.no_cpu_baseline:
+        import oracle
+        log("oracle (1 thread) on the same inputs")
+        Kr, Vr = K0.copy(), V0.copy()
+        t = time.perf_counter()
+        ref_logits, _ = oracle.decode_step(cfg, weights, tokens, [P] * B, Kr, Vr, nthreads=1)
+        cpu_s = time.perf_counter() - t
+        got = logits.cpu().numpy()
+        out["parity_rel_l2_logits"] = max(oracle.rel_l2(got[b], ref_logits[b]) for b in range(B))
+        out["cpu_baseline"] = {"value": B / cpu_s, "unit": "tok/s", "cores": 1, "kind": "oracle",
+                               "sample": f"one full decode step of {args.workload}, fp64 oracle, "
+                                         f"1 thread, {cpu_s:.1f} s"}
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,158 @@
+/*
+ * kl — one decode step of a Llama-style decoder-only transformer on one
+ * AMD MI355X (gfx950), with kernel looping (arXiv 2410.23668).
+ *
+ * The paper's token step is Embedding -> L x Decoder -> Classifier (Sec. 2).
+ * Each decoder layer is RMSNorm, the Q/K/V projections, RoPE, GQA attention
+ * over the KV cache, the O projection with a residual add, RMSNorm, a SwiGLU
+ * MLP and a second residual add.  The step runs in one of three schedules:
+ *
+ *   KL_MODE_PER_LAYER  one kernel launch per decoder layer (the layer-level
+ *                      fusion baseline of Sec. 2, K0 called L times), plus one
+ *                      launch for the embedding and one for the classifier:
+ *                      L + 2 dispatches.
+ *   KL_MODE_LOOPED     kernel looping (Sec. 2 and Sec. 3.2): the L chained
+ *                      layer calls become one call of a kernel with an outer
+ *                      loop over layers; the embedding and classifier run in
+ *                      the same launch: 1 dispatch.  Kernel boundaries are
+ *                      replaced by device-scope counters.
+ *   KL_MODE_PER_OP     one launch per operator group of a layer (the many-
+ *                      kernels-per-layer GPU schedule of Sec. 2, Fig. 3 (i)):
+ *                      5 L + 2 dispatches.
+ *
+ * All modes run the same device code with the same work partition, so for the
+ * same inputs they produce bit-identical logits, hidden states and KV writes.
+ *
+ * Conventions.  All tensors are row-major.  "dev" pointers are device memory
+ * of the current HIP device; "host" pointers are host memory.  bf16 values are
+ * passed as their 16-bit patterns.  Streams are hipStream_t passed as void*
+ * (NULL = the default stream).  Functions returning kl_status return KL_OK or
+ * a negative code; on a negative code nothing was enqueued and kl_last_error()
+ * describes the problem.  The library is built for gfx950 only.
+ */
+#ifndef KL_H
+#define KL_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    KL_OK = 0,
+    KL_ERR_INVALID_ARGUMENT = -1,  /* null / misaligned pointer, bad size, bad mode  */
+    KL_ERR_UNSUPPORTED = -2,       /* a shape this build does not implement           */
+    KL_ERR_OUT_OF_MEMORY = -3,     /* device allocation failed                        */
+    KL_ERR_HIP = -4,               /* a HIP runtime call failed (message has details) */
+    KL_ERR_DEVICE_FAULT = -5       /* reported by kl_get_device_error                 */
+} kl_status;
+
+typedef enum {
+    KL_MODE_PER_LAYER = 0,
+    KL_MODE_LOOPED = 1,
+    KL_MODE_PER_OP = 2
+} kl_mode;
+
+/* Bits of the device error word (kl_get_device_error). */
+#define KL_DEVERR_TOKEN    1   /* a token id outside [0, vocab): row 0 was used instead      */
+#define KL_DEVERR_POSITION 2   /* a position outside [0, capacity) or >= max_seq: clamped    */
+#define KL_DEVERR_BARRIER  4   /* a grid barrier waited longer than its watchdog allows      */
+
+/* Model shape.  Supported: head_dim 64 or 128, n_heads a multiple of
+ * n_kv_heads with n_heads / n_kv_heads <= 8, every dimension >= 1 and
+ * hidden, ffn_dim multiples of 8.  max_batch bounds the batch of a step;
+ * max_seq bounds positions (the RoPE table covers [0, max_seq)). */
+typedef struct {
+    int32_t n_layers, hidden, n_heads, n_kv_heads, head_dim, ffn_dim, vocab;
+    float rope_theta, rms_eps;
+    int32_t max_batch, max_seq;
+} kl_config;
+
+/* One decoder layer's weights: dev bf16, nn.Linear layout [out][in].
+ *   attn_norm, ffn_norm [hidden]
+ *   wq [n_heads*head_dim][hidden], wk, wv [n_kv_heads*head_dim][hidden]
+ *   wo [hidden][n_heads*head_dim]
+ *   w_gate, w_up [ffn_dim][hidden], w_down [hidden][ffn_dim]            */
+typedef struct {
+    const void *attn_norm, *wq, *wk, *wv, *wo, *ffn_norm, *w_gate, *w_up, *w_down;
+} kl_layer_ptrs;
+
+/* Whole model: dev bf16 embed [vocab][hidden], final_norm [hidden],
+ * lm_head [vocab][hidden] (untied); layers is a host array of n_layers. */
+typedef struct {
+    const void *embed, *final_norm, *lm_head;
+    const kl_layer_ptrs *layers;
+} kl_weight_ptrs;
+
+/* Caller-owned KV cache: dev bf16 k and v, each
+ * [n_layers][batch][n_kv_heads][capacity][head_dim], holding post-RoPE keys.
+ * 'batch' is the allocated batch extent (>= the step's batch), 'capacity'
+ * the allocated positions per sequence.  16-byte aligned. */
+typedef struct {
+    void *k, *v;
+    int32_t batch, capacity;
+} kl_kv_cache;
+
+typedef struct kl_state kl_state;
+
+/* Read-only facts about a loaded model (for benches and tests). */
+typedef struct {
+    int32_t n_workgroups;       /* persistent grid size used by every mode        */
+    int32_t threads_per_group;
+    int32_t lds_bytes;          /* dynamic LDS per workgroup                       */
+    int32_t attn_chunks_b1;     /* KV chunks per (sequence, KV head) at batch 1    */
+    int64_t arena_bytes;        /* packed weights + gains                          */
+    int64_t scratch_bytes;      /* activations, partials, counters                 */
+} kl_info;
+
+/* Load a model: validates cfg, allocates the packed weight arena, the RoPE
+ * table and the step scratch on the current device, and repacks the caller's
+ * weights into the gfx950 layout with kernels on 'stream'.  Returns after the
+ * stream has finished the packing, so the caller may free the source weights.
+ * The grouped weights of all layers are laid out linearly in one arena (the
+ * grouping rule of Sec. 3.2, Eq. 3, with the linear layout it suggests).
+ * On success *out owns every allocation; release with kl_free_model. */
+kl_status kl_load_model(const kl_config *cfg, const kl_weight_ptrs *weights, void *stream,
+                        kl_state **out);
+
+/* Enqueue one decode step on 'stream' (asynchronous).
+ *   token_ids  dev int32 [batch]   token of each sequence
+ *   positions  dev int32 [batch]   position p of the new token; the step writes
+ *                                  K/V slot p of every layer and attends over
+ *                                  slots 0..p
+ *   batch      1 <= batch <= min(max_batch, kv->batch)
+ *   kv         caller's cache (layout above); capacity <= max_seq
+ *   logits_out dev fp32 [batch][vocab]
+ *   hidden_out dev fp32 [batch][hidden] or NULL: the residual stream after the
+ *              last layer (before the final norm)
+ *   mode       a kl_mode
+ * Out-of-range token ids or positions cannot be checked on the host; they set
+ * bits in the device error word and are replaced by in-range values.  One step
+ * may be in flight per state; the caller's buffers are borrowed until the step
+ * completes in stream order. */
+kl_status kl_decode_step(kl_state *st, const int32_t *token_ids, const int32_t *positions,
+                         int32_t batch, const kl_kv_cache *kv, float *logits_out,
+                         float *hidden_out, void *stream, int32_t mode);
+
+/* Bytes of ONE of the K or V buffers for the given batch and capacity
+ * (0 if cfg is invalid). */
+size_t kl_kv_cache_bytes(const kl_config *cfg, int32_t batch, int32_t capacity);
+
+/* Synchronizes the device, returns the device error word in *code (KL_DEVERR_*
+ * bits, 0 = none) and clears it.  Returns KL_ERR_DEVICE_FAULT when *code != 0. */
+kl_status kl_get_device_error(kl_state *st, int32_t *code);
+
+kl_status kl_get_info(const kl_state *st, kl_info *info);
+
+/* Frees everything the state owns (synchronizes the device first). NULL is a no-op. */
+void kl_free_model(kl_state *st);
+
+/* Message describing the last failing call on this thread ("" if none). */
+const char *kl_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* KL_H */

@@ -1,0 +1,440 @@
+// Host runtime behind the C ABI in include/kl.h: argument validation, the
+// packed weight arena, the RoPE table, step scratch and the launch plans of
+// the three schedules.
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "kl.h"
+#include "kl_internal.h"
+
+using namespace kl;
+
+struct kl_state {
+    kl_config cfg;
+    int device;
+    int Hp, Ap, Fp, qkv_rg, o_rg, gu_rg, down_rg, head_rg;
+    size_t layer_stride, off_attn_norm, off_ffn_norm, off_qkv, off_o, off_gu, off_down;
+    size_t off_final_norm, off_lm_head, off_embed;
+    uint8_t *arena;
+    size_t arena_bytes;
+    float2 *rope;
+    uint8_t *scratch;
+    size_t scratch_bytes;
+    float *x, *q, *o, *m, *part;
+    unsigned *bar, *cnt;
+    int *err;
+    int nwg, lds_bytes;
+};
+
+namespace {
+
+thread_local std::string g_last_error;
+
+kl_status fail(kl_status s, const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return s;
+}
+
+#define HIP_TRY(expr)                                                                      \
+    do {                                                                                   \
+        hipError_t e_ = (expr);                                                            \
+        if (e_ != hipSuccess)                                                              \
+            return fail(e_ == hipErrorOutOfMemory ? KL_ERR_OUT_OF_MEMORY : KL_ERR_HIP,     \
+                        "%s failed: %s", #expr, hipGetErrorString(e_));                    \
+    } while (0)
+
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+int pad_k(int v) { return (v + kTileK - 1) / kTileK * kTileK; }
+
+bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+kl_status validate_config(const kl_config *c) {
+    if (!c) return fail(KL_ERR_INVALID_ARGUMENT, "config is NULL");
+    if (c->n_layers < 1 || c->hidden < 1 || c->n_heads < 1 || c->n_kv_heads < 1 ||
+        c->head_dim < 1 || c->ffn_dim < 1 || c->vocab < 1 || c->max_batch < 1 || c->max_seq < 1)
+        return fail(KL_ERR_INVALID_ARGUMENT, "every config dimension must be >= 1");
+    if (!(c->rms_eps > 0.f) || !std::isfinite(c->rms_eps))
+        return fail(KL_ERR_INVALID_ARGUMENT, "rms_eps must be a positive finite number");
+    if (!(c->rope_theta > 1.f) || !std::isfinite(c->rope_theta))
+        return fail(KL_ERR_INVALID_ARGUMENT, "rope_theta must be a finite number > 1");
+    if (c->head_dim != 64 && c->head_dim != 128)
+        return fail(KL_ERR_UNSUPPORTED, "head_dim %d unsupported (64 or 128)", c->head_dim);
+    if (c->n_heads % c->n_kv_heads != 0)
+        return fail(KL_ERR_UNSUPPORTED, "n_heads %d is not a multiple of n_kv_heads %d",
+                    c->n_heads, c->n_kv_heads);
+    const int g = c->n_heads / c->n_kv_heads;
+    if (g != 1 && g != 2 && g != 4 && g != 8)
+        return fail(KL_ERR_UNSUPPORTED, "query heads per KV head must be 1, 2, 4 or 8 (got %d)", g);
+    if (c->hidden % 8 != 0 || c->ffn_dim % 8 != 0)
+        return fail(KL_ERR_UNSUPPORTED, "hidden and ffn_dim must be multiples of 8");
+    if (c->max_batch > 4096) return fail(KL_ERR_UNSUPPORTED, "max_batch above 4096");
+    if ((int64_t)c->vocab >= (1 << 28) || (int64_t)c->ffn_dim >= (1 << 27))
+        return fail(KL_ERR_UNSUPPORTED, "vocab or ffn_dim too large");
+    return KL_OK;
+}
+
+// Packed-row -> source-row maps, encoded (source id << 28) | row, -1 = zero row.
+std::vector<int32_t> qkv_rowmap(const kl_config &c) {
+    const int d = c.head_dim, half = d / 2, qd = c.n_heads * d, kd = c.n_kv_heads * d;
+    std::vector<int32_t> m(qd + 2 * kd);
+    for (int pr = 0; pr < qd + kd; ++pr) {
+        const int sid = pr < qd ? 0 : 1, r = pr < qd ? pr : pr - qd;
+        const int h = r / d, j = r % d;
+        m[pr] = (sid << 28) | (h * d + j / 2 + (j % 2) * half);   // rotation pairs adjacent
+    }
+    for (int r = 0; r < kd; ++r) m[qd + kd + r] = (2 << 28) | r;
+    return m;
+}
+
+std::vector<int32_t> identity_rowmap(int rows, int padded_rows) {
+    std::vector<int32_t> m(padded_rows, -1);
+    for (int r = 0; r < rows; ++r) m[r] = r;
+    return m;
+}
+
+std::vector<int32_t> gateup_rowmap(int F) {
+    std::vector<int32_t> m(2 * F);
+    for (int i = 0; i < F; ++i) {
+        m[2 * i] = i;                  // gate row i
+        m[2 * i + 1] = (1 << 28) | i;  // up row i
+    }
+    return m;
+}
+
+int lds_bytes_for(const kl_state &s) {
+    const kl_config &c = s.cfg;
+    const int g = c.n_heads / c.n_kv_heads;
+    int amax = std::max(std::max(s.Hp, s.Ap), s.Fp);
+    const int attn = g * c.head_dim + g * kAttnSub + g * 4 + kWaves * g * c.head_dim;
+    amax = std::max(amax, attn);
+    amax = (amax + 63) & ~63;
+    return (amax + kWaves * kRgBatch * kTileRows + 64) * (int)sizeof(float);
+}
+
+void free_state(kl_state *s) {
+    if (!s) return;
+    if (s->arena) (void)hipFree(s->arena);
+    if (s->rope) (void)hipFree(s->rope);
+    if (s->scratch) (void)hipFree(s->scratch);
+    delete s;
+}
+
+StepParams base_params(const kl_state &s) {
+    const kl_config &c = s.cfg;
+    StepParams P{};
+    P.L = c.n_layers; P.H = c.hidden; P.nq = c.n_heads; P.nkv = c.n_kv_heads; P.d = c.head_dim;
+    P.F = c.ffn_dim; P.V = c.vocab; P.group = c.n_heads / c.n_kv_heads;
+    P.Hp = s.Hp; P.Ap = s.Ap; P.Fp = s.Fp;
+    P.qkv_rg = s.qkv_rg; P.o_rg = s.o_rg; P.gu_rg = s.gu_rg; P.down_rg = s.down_rg;
+    P.head_rg = s.head_rg;
+    P.eps = c.rms_eps; P.max_seq = c.max_seq;
+    P.arena = s.arena; P.layer_stride = s.layer_stride;
+    P.off_attn_norm = s.off_attn_norm; P.off_ffn_norm = s.off_ffn_norm; P.off_qkv = s.off_qkv;
+    P.off_o = s.off_o; P.off_gu = s.off_gu; P.off_down = s.off_down;
+    P.embed = reinterpret_cast<const uint16_t *>(s.arena + s.off_embed);
+    P.final_norm = reinterpret_cast<const float *>(s.arena + s.off_final_norm);
+    P.lm_head = reinterpret_cast<const uint16_t *>(s.arena + s.off_lm_head);
+    P.rope = s.rope;
+    P.x = s.x; P.q = s.q; P.o = s.o; P.m = s.m; P.part = s.part;
+    P.bar = s.bar; P.cnt = s.cnt; P.err = s.err;
+    P.nwg = s.nwg;
+    return P;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *kl_last_error(void) { return g_last_error.c_str(); }
+
+size_t kl_kv_cache_bytes(const kl_config *cfg, int32_t batch, int32_t capacity) {
+    if (!cfg || validate_config(cfg) != KL_OK || batch < 1 || capacity < 1) return 0;
+    return (size_t)cfg->n_layers * batch * cfg->n_kv_heads * (size_t)capacity * cfg->head_dim *
+           sizeof(uint16_t);
+}
+
+kl_status kl_load_model(const kl_config *cfg, const kl_weight_ptrs *w, void *stream,
+                        kl_state **out) {
+    g_last_error.clear();
+    if (!out) return fail(KL_ERR_INVALID_ARGUMENT, "out is NULL");
+    *out = nullptr;
+    kl_status st = validate_config(cfg);
+    if (st != KL_OK) return st;
+    if (!w || !w->embed || !w->final_norm || !w->lm_head || !w->layers)
+        return fail(KL_ERR_INVALID_ARGUMENT, "weight pointers must not be NULL");
+    if (!aligned(w->embed, 2) || !aligned(w->final_norm, 2) || !aligned(w->lm_head, 2))
+        return fail(KL_ERR_INVALID_ARGUMENT, "weight pointers must be 2-byte aligned");
+    for (int l = 0; l < cfg->n_layers; ++l) {
+        const kl_layer_ptrs &L = w->layers[l];
+        const void *ps[] = {L.attn_norm, L.wq, L.wk, L.wv, L.wo, L.ffn_norm, L.w_gate, L.w_up,
+                            L.w_down};
+        for (const void *p : ps) {
+            if (!p) return fail(KL_ERR_INVALID_ARGUMENT, "layer %d has a NULL weight pointer", l);
+            if (!aligned(p, 2))
+                return fail(KL_ERR_INVALID_ARGUMENT, "layer %d weight not 2-byte aligned", l);
+        }
+    }
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+
+    kl_state *S = new kl_state();
+    S->cfg = *cfg;
+    const kl_config &c = S->cfg;
+    auto bail = [&](kl_status code) { free_state(S); return code; };
+#define TRY(expr)                                                                          \
+    do {                                                                                   \
+        hipError_t e_ = (expr);                                                            \
+        if (e_ != hipSuccess)                                                              \
+            return bail(fail(e_ == hipErrorOutOfMemory ? KL_ERR_OUT_OF_MEMORY : KL_ERR_HIP,  \
+                             "%s failed: %s", #expr, hipGetErrorString(e_)));              \
+    } while (0)
+
+    TRY(hipGetDevice(&S->device));
+    int ncu = 0, coop = 0;
+    TRY(hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, S->device));
+    TRY(hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, S->device));
+    if (!coop) return bail(fail(KL_ERR_UNSUPPORTED, "device lacks cooperative launch"));
+
+    const int d = c.head_dim, g = c.n_heads / c.n_kv_heads;
+    S->Hp = pad_k(c.hidden);
+    S->Ap = pad_k(c.n_heads * d);
+    S->Fp = pad_k(c.ffn_dim);
+    const int qkv_rows = (c.n_heads + 2 * c.n_kv_heads) * d;
+    const int vrows = (c.vocab + kTileRows - 1) / kTileRows * kTileRows;
+    S->qkv_rg = qkv_rows / kTileRows;
+    S->o_rg = c.hidden / kTileRows;
+    S->gu_rg = 2 * c.ffn_dim / kTileRows;
+    S->down_rg = c.hidden / kTileRows;
+    S->head_rg = vrows / kTileRows;
+    const int KTH = S->Hp / kTileK, KTA = S->Ap / kTileK, KTF = S->Fp / kTileK;
+
+    // arena: [layer 0 .. L-1][final_norm][lm_head][embed]
+    const size_t A = 4096;
+    size_t off = 0;
+    S->off_attn_norm = off; off = align_up(off + S->Hp * 4, A);
+    S->off_ffn_norm = off;  off = align_up(off + S->Hp * 4, A);
+    S->off_qkv = off;  off = align_up(off + (size_t)S->qkv_rg * KTH * kTileBytes, A);
+    S->off_o = off;    off = align_up(off + (size_t)S->o_rg * KTA * kTileBytes, A);
+    S->off_gu = off;   off = align_up(off + (size_t)S->gu_rg * KTH * kTileBytes, A);
+    S->off_down = off; off = align_up(off + (size_t)S->down_rg * KTF * kTileBytes, A);
+    S->layer_stride = off;
+    off = S->layer_stride * c.n_layers;
+    S->off_final_norm = off; off = align_up(off + S->Hp * 4, A);
+    S->off_lm_head = off;    off = align_up(off + (size_t)S->head_rg * KTH * kTileBytes, A);
+    S->off_embed = off;      off = align_up(off + (size_t)c.vocab * c.hidden * 2, A);
+    S->arena_bytes = off;
+    TRY(hipMalloc(&S->arena, S->arena_bytes));
+
+    // grid: one persistent workgroup per CU
+    S->lds_bytes = lds_bytes_for(*S);
+    if (S->lds_bytes > 160 * 1024)
+        return bail(fail(KL_ERR_UNSUPPORTED, "LDS need %d bytes exceeds 160 KiB", S->lds_bytes));
+    int per_cu = 0;
+    TRY(step_kernel_setup(S->lds_bytes, &per_cu));
+    if (per_cu < 1) return bail(fail(KL_ERR_UNSUPPORTED, "step kernel does not fit on a CU"));
+    S->nwg = ncu;
+
+    // scratch
+    const int B = c.max_batch, nkv = c.n_kv_heads;
+    const int Cmax = std::max(1, S->nwg / nkv);
+    const size_t part_items = (size_t)std::max(S->nwg, B * nkv);   // >= B * nkv * C
+    size_t so = 0;
+    const size_t off_x = so;    so = align_up(so + (size_t)B * S->Hp * 4, 256);
+    const size_t off_q = so;    so = align_up(so + (size_t)B * c.n_heads * d * 4, 256);
+    const size_t off_o = so;    so = align_up(so + (size_t)B * S->Ap * 4, 256);
+    const size_t off_m = so;    so = align_up(so + (size_t)B * S->Fp * 4, 256);
+    const size_t off_p = so;
+    so = align_up(so + std::max(part_items, (size_t)nkv * Cmax) * g * (d + 2) * 4, 256);
+    (void)Cmax;
+    const size_t off_bar = so;  so = align_up(so + 1024, 256);
+    const size_t off_cnt = so;  so = align_up(so + (size_t)B * nkv * 4, 256);
+    const size_t off_err = so;  so = align_up(so + 256, 256);
+    S->scratch_bytes = so;
+    TRY(hipMalloc(&S->scratch, S->scratch_bytes));
+    TRY(hipMemsetAsync(S->scratch, 0, S->scratch_bytes, s));
+    S->x = reinterpret_cast<float *>(S->scratch + off_x);
+    S->q = reinterpret_cast<float *>(S->scratch + off_q);
+    S->o = reinterpret_cast<float *>(S->scratch + off_o);
+    S->m = reinterpret_cast<float *>(S->scratch + off_m);
+    S->part = reinterpret_cast<float *>(S->scratch + off_p);
+    S->bar = reinterpret_cast<unsigned *>(S->scratch + off_bar);
+    S->cnt = reinterpret_cast<unsigned *>(S->scratch + off_cnt);
+    S->err = reinterpret_cast<int *>(S->scratch + off_err);
+
+    // RoPE table (cos, sin) of pos * theta^(-2i/d), computed in double
+    {
+        const int half = d / 2;
+        std::vector<float2> tab((size_t)c.max_seq * half);
+        for (int p = 0; p < c.max_seq; ++p)
+            for (int i = 0; i < half; ++i) {
+                const double w = std::pow((double)c.rope_theta, -2.0 * i / (double)d);
+                const double phi = (double)p * w;
+                tab[(size_t)p * half + i] = make_float2((float)std::cos(phi), (float)std::sin(phi));
+            }
+        TRY(hipMalloc(&S->rope, tab.size() * sizeof(float2)));
+        TRY(hipMemcpyAsync(S->rope, tab.data(), tab.size() * sizeof(float2),
+                           hipMemcpyHostToDevice, s));
+        TRY(hipStreamSynchronize(s));
+    }
+
+    // row maps (the same for every layer)
+    const std::vector<int32_t> m_qkv = qkv_rowmap(c), m_h = identity_rowmap(c.hidden, c.hidden),
+                               m_gu = gateup_rowmap(c.ffn_dim),
+                               m_head = identity_rowmap(c.vocab, vrows);
+    int32_t *dmaps = nullptr;
+    const size_t nmap = m_qkv.size() + m_h.size() + m_gu.size() + m_head.size();
+    TRY(hipMalloc(&dmaps, nmap * sizeof(int32_t)));
+    std::vector<int32_t> all;
+    all.reserve(nmap);
+    all.insert(all.end(), m_qkv.begin(), m_qkv.end());
+    all.insert(all.end(), m_h.begin(), m_h.end());
+    all.insert(all.end(), m_gu.begin(), m_gu.end());
+    all.insert(all.end(), m_head.begin(), m_head.end());
+    hipError_t pe = hipMemcpyAsync(dmaps, all.data(), nmap * sizeof(int32_t),
+                                   hipMemcpyHostToDevice, s);
+    const int32_t *d_qkv = dmaps, *d_h = d_qkv + m_qkv.size(), *d_gu = d_h + m_h.size(),
+                  *d_head = d_gu + m_gu.size();
+    for (int l = 0; l < c.n_layers && pe == hipSuccess; ++l) {
+        const kl_layer_ptrs &Lw = w->layers[l];
+        uint8_t *Lb = S->arena + (size_t)l * S->layer_stride;
+        const auto u16 = [](const void *p) { return reinterpret_cast<const uint16_t *>(p); };
+        pe = launch_gain_to_f32(reinterpret_cast<float *>(Lb + S->off_attn_norm), u16(Lw.attn_norm),
+                                c.hidden, S->Hp, s);
+        if (pe == hipSuccess)
+            pe = launch_gain_to_f32(reinterpret_cast<float *>(Lb + S->off_ffn_norm),
+                                    u16(Lw.ffn_norm), c.hidden, S->Hp, s);
+        if (pe == hipSuccess)
+            pe = launch_pack_rows(reinterpret_cast<uint16_t *>(Lb + S->off_qkv), S->qkv_rg, KTH,
+                                  c.hidden, d_qkv, u16(Lw.wq), u16(Lw.wk), u16(Lw.wv), s);
+        if (pe == hipSuccess)
+            pe = launch_pack_rows(reinterpret_cast<uint16_t *>(Lb + S->off_o), S->o_rg, KTA,
+                                  c.n_heads * d, d_h, u16(Lw.wo), nullptr, nullptr, s);
+        if (pe == hipSuccess)
+            pe = launch_pack_rows(reinterpret_cast<uint16_t *>(Lb + S->off_gu), S->gu_rg, KTH,
+                                  c.hidden, d_gu, u16(Lw.w_gate), u16(Lw.w_up), nullptr, s);
+        if (pe == hipSuccess)
+            pe = launch_pack_rows(reinterpret_cast<uint16_t *>(Lb + S->off_down), S->down_rg, KTF,
+                                  c.ffn_dim, d_h, u16(Lw.w_down), nullptr, nullptr, s);
+    }
+    if (pe == hipSuccess)
+        pe = launch_gain_to_f32(reinterpret_cast<float *>(S->arena + S->off_final_norm),
+                                reinterpret_cast<const uint16_t *>(w->final_norm), c.hidden, S->Hp,
+                                s);
+    if (pe == hipSuccess)
+        pe = launch_pack_rows(reinterpret_cast<uint16_t *>(S->arena + S->off_lm_head), S->head_rg,
+                              KTH, c.hidden, d_head,
+                              reinterpret_cast<const uint16_t *>(w->lm_head), nullptr, nullptr, s);
+    if (pe == hipSuccess)
+        pe = hipMemcpyAsync(S->arena + S->off_embed, w->embed, (size_t)c.vocab * c.hidden * 2,
+                            hipMemcpyDeviceToDevice, s);
+    hipError_t se = hipStreamSynchronize(s);
+    (void)hipFree(dmaps);
+    if (pe != hipSuccess) TRY(pe);
+    TRY(se);
+#undef TRY
+    *out = S;
+    return KL_OK;
+}
+
+kl_status kl_decode_step(kl_state *st, const int32_t *token_ids, const int32_t *positions,
+                         int32_t batch, const kl_kv_cache *kv, float *logits_out,
+                         float *hidden_out, void *stream, int32_t mode) {
+    g_last_error.clear();
+    if (!st) return fail(KL_ERR_INVALID_ARGUMENT, "state is NULL");
+    if (!token_ids || !positions || !logits_out || !kv || !kv->k || !kv->v)
+        return fail(KL_ERR_INVALID_ARGUMENT, "token_ids, positions, kv, kv->k, kv->v and "
+                                             "logits_out must not be NULL");
+    if (!aligned(token_ids, 4) || !aligned(positions, 4) || !aligned(logits_out, 4) ||
+        (hidden_out && !aligned(hidden_out, 4)))
+        return fail(KL_ERR_INVALID_ARGUMENT, "int32/fp32 buffers must be 4-byte aligned");
+    if (!aligned(kv->k, 16) || !aligned(kv->v, 16))
+        return fail(KL_ERR_INVALID_ARGUMENT, "KV cache buffers must be 16-byte aligned");
+    const kl_config &c = st->cfg;
+    if (batch < 1 || batch > c.max_batch)
+        return fail(KL_ERR_INVALID_ARGUMENT, "batch %d outside [1, max_batch=%d]", batch,
+                    c.max_batch);
+    if (kv->batch < batch)
+        return fail(KL_ERR_INVALID_ARGUMENT, "kv batch extent %d < batch %d", kv->batch, batch);
+    if (kv->capacity < 1 || kv->capacity > c.max_seq)
+        return fail(KL_ERR_INVALID_ARGUMENT, "kv capacity %d outside [1, max_seq=%d]",
+                    kv->capacity, c.max_seq);
+    if (mode != KL_MODE_PER_LAYER && mode != KL_MODE_LOOPED && mode != KL_MODE_PER_OP)
+        return fail(KL_ERR_INVALID_ARGUMENT, "unknown mode %d", mode);
+    int dev = -1;
+    HIP_TRY(hipGetDevice(&dev));
+    if (dev != st->device)
+        return fail(KL_ERR_INVALID_ARGUMENT, "current device %d is not the model's device %d",
+                    dev, st->device);
+
+    StepParams P = base_params(*st);
+    P.tokens = token_ids; P.positions = positions; P.B = batch;
+    P.kc = reinterpret_cast<uint16_t *>(kv->k); P.vc = reinterpret_cast<uint16_t *>(kv->v);
+    P.kv_batch = kv->batch; P.cap = kv->capacity;
+    P.logits = logits_out; P.hidden_out = hidden_out;
+    P.C = std::max(1, st->nwg / (batch * c.n_kv_heads));
+
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    const int L = c.n_layers, lds = st->lds_bytes;
+    if (mode == KL_MODE_LOOPED) {
+        HIP_TRY(launch_step(P, 0, L, kPhEmbed | kPhLayer | kPhHead, true, lds, s));
+    } else if (mode == KL_MODE_PER_LAYER) {
+        HIP_TRY(launch_step(P, 0, 0, kPhEmbed, false, lds, s));
+        for (int l = 0; l < L; ++l) HIP_TRY(launch_step(P, l, l + 1, kPhLayer, true, lds, s));
+        HIP_TRY(launch_step(P, 0, 0, kPhHead, false, lds, s));
+    } else {
+        HIP_TRY(launch_step(P, 0, 0, kPhEmbed, false, lds, s));
+        const int ops[] = {kPhQkv, kPhAttn, kPhOproj, kPhGateUp, kPhDown};
+        for (int l = 0; l < L; ++l)
+            for (int ph : ops) HIP_TRY(launch_step(P, l, l + 1, ph, false, lds, s));
+        HIP_TRY(launch_step(P, 0, 0, kPhHead, false, lds, s));
+    }
+    return KL_OK;
+}
+
+kl_status kl_get_device_error(kl_state *st, int32_t *code) {
+    g_last_error.clear();
+    if (!st || !code) return fail(KL_ERR_INVALID_ARGUMENT, "state and code must not be NULL");
+    HIP_TRY(hipDeviceSynchronize());
+    int32_t v = 0;
+    HIP_TRY(hipMemcpy(&v, st->err, sizeof v, hipMemcpyDeviceToHost));
+    *code = v;
+    if (v == 0) return KL_OK;
+    HIP_TRY(hipMemset(st->err, 0, sizeof(int32_t)));
+    if (v & KL_DEVERR_BARRIER) {
+        // a timed-out barrier leaves its counters mid-count: start them afresh
+        HIP_TRY(hipMemset(st->bar, 0, 1024));
+        HIP_TRY(hipMemset(st->cnt, 0, (size_t)st->cfg.max_batch * st->cfg.n_kv_heads * 4));
+    }
+    return fail(KL_ERR_DEVICE_FAULT, "device error word 0x%x", v);
+}
+
+kl_status kl_get_info(const kl_state *st, kl_info *info) {
+    if (!st || !info) return fail(KL_ERR_INVALID_ARGUMENT, "state and info must not be NULL");
+    info->n_workgroups = st->nwg;
+    info->threads_per_group = kThreads;
+    info->lds_bytes = st->lds_bytes;
+    info->attn_chunks_b1 = std::max(1, st->nwg / st->cfg.n_kv_heads);
+    info->arena_bytes = (int64_t)st->arena_bytes;
+    info->scratch_bytes = (int64_t)st->scratch_bytes;
+    return KL_OK;
+}
+
+void kl_free_model(kl_state *st) {
+    if (!st) return;
+    (void)hipDeviceSynchronize();
+    free_state(st);
+}
+
+}  // extern "C"

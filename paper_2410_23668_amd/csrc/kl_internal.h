@@ -1,0 +1,73 @@
+// Internal interface between the host runtime (kl_host.cpp) and the device
+// code (kl_device.hip).  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace kl {
+
+// Work geometry shared by host and device.
+constexpr int kWaves = 8;                 // waves per workgroup
+constexpr int kThreads = kWaves * 64;     // threads per workgroup
+constexpr int kTileRows = 8;              // rows of one packed weight tile
+constexpr int kTileK = 64;                // columns of one packed weight tile
+constexpr int kTileBytes = kTileRows * kTileK * 2;   // 1 KiB: one 16-byte load per lane
+constexpr int kRgBatch = 16;              // row groups reduced per LDS round
+constexpr int kAttnSub = 256;             // positions per attention sub-chunk
+constexpr int kMaxGroup = 8;              // max query heads per KV head
+
+// Phase selection bits of one launch of the step kernel.
+enum : int {
+    kPhEmbed = 1, kPhQkv = 2, kPhAttn = 4, kPhOproj = 8, kPhGateUp = 16, kPhDown = 32,
+    kPhHead = 64,
+    kPhLayer = kPhQkv | kPhAttn | kPhOproj | kPhGateUp | kPhDown,
+};
+
+// Everything one step needs, passed by value as the kernel argument.
+struct StepParams {
+    // shape
+    int L, H, nq, nkv, d, F, V, group;
+    int Hp, Ap, Fp;            // K extents padded to kTileK: hidden, n_heads*d, ffn
+    int qkv_rg, o_rg, gu_rg, down_rg, head_rg;   // row groups (kTileRows rows) per matrix
+    float eps;
+    int max_seq;
+    // packed weights
+    const uint8_t *arena;      // layer 0 base
+    size_t layer_stride;       // bytes between consecutive layers
+    size_t off_attn_norm, off_ffn_norm, off_qkv, off_o, off_gu, off_down;
+    const uint16_t *embed;     // [V][H] bf16, row-major
+    const float *final_norm;   // [Hp]
+    const uint16_t *lm_head;   // packed tiles
+    const float2 *rope;        // [max_seq][d/2] (cos, sin)
+    // step arguments
+    const int32_t *tokens, *positions;
+    int B;
+    uint16_t *kc, *vc;         // [L][kv_batch][nkv][cap][d]
+    int kv_batch, cap;
+    float *logits, *hidden_out;
+    // scratch
+    float *x;                  // [max_batch][Hp]   residual stream
+    float *q;                  // [max_batch][nq*d] rotated queries
+    float *o;                  // [max_batch][Ap]   attention output (padding stays 0)
+    float *m;                  // [max_batch][Fp]   SwiGLU output (padding stays 0)
+    float *part;               // attention partials [max_batch*nkv*C][group][d+2]
+    unsigned *bar;             // grid barrier: [0] arrivals, [64] generation
+    unsigned *cnt;             // [max_batch*nkv] attention chunk arrivals
+    int *err;                  // device error word
+    int nwg;                   // grid size; the work partition depends only on it
+    int C;                     // attention chunks per (sequence, KV head)
+};
+
+hipError_t launch_step(const StepParams &p, int first_layer, int last_layer, int phases,
+                       bool cooperative, int lds_bytes, hipStream_t stream);
+hipError_t step_kernel_setup(int lds_bytes, int *max_blocks_per_cu);
+
+hipError_t launch_pack_rows(uint16_t *dst, int n_rg, int kt, int K, const int32_t *rowmap,
+                            const uint16_t *src0, const uint16_t *src1, const uint16_t *src2,
+                            hipStream_t stream);
+hipError_t launch_gain_to_f32(float *dst, const uint16_t *src, int n, int npad,
+                              hipStream_t stream);
+
+}  // namespace kl

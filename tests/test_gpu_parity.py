@@ -1,0 +1,135 @@
+"""Parity of the HIP decode step against the CPU oracle, through the C ABI.
+
+Bar: per-sequence rel L2 <= 1e-2 on logits, hidden state and the written KV
+slots (bf16 weights and KV, fp32 accumulation), every other KV slot
+untouched, and all three schedules bit-identical with each other.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_2410_23668_amd import binding as kb
+from paper_2410_23668_amd.device import KvCache
+from synth.workloads import TINY, WORKLOADS
+from tests.gpu_cases import MODES, Case, assert_bit_exact, check_against_oracle, say
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def tiny():
+    w = WORKLOADS["tiny-b1-ctx128"]
+    say(f"[tiny] building case capacity={w['capacity']} P={w['context']}")
+    return Case(w["model"], 1, w["capacity"], [w["context"]], seed=w["seed_weights"])
+
+
+def test_tiny_all_modes_match_oracle_and_each_other(tiny):
+    ref = tiny.oracle_step()
+    outs = {}
+    for name, mode in MODES:
+        say(f"[tiny] mode={name}")
+        outs[name] = tiny.gpu_step(mode)
+        check_against_oracle(tiny, outs[name], ref)
+    assert_bit_exact(outs["per_layer"], outs["looped"], "per_layer vs looped")
+    assert_bit_exact(outs["per_op"], outs["looped"], "per_op vs looped")
+
+
+def test_tiny_repeated_steps_are_deterministic(tiny):
+    say("[tiny] repeat looped x3")
+    a = tiny.gpu_step(kb.KL_MODE_LOOPED)
+    for _ in range(2):
+        assert_bit_exact(a, tiny.gpu_step(kb.KL_MODE_LOOPED), "repeat")
+
+
+def test_tiny_reports_dispatch_geometry(tiny):
+    info = tiny.model.info()
+    assert info.n_workgroups == torch.cuda.get_device_properties(0).multi_processor_count
+    assert info.threads_per_group == 512
+    assert info.lds_bytes <= 160 * 1024
+    assert tiny.model.device_error() == 0
+
+
+@pytest.mark.parametrize("positions", [[0], [1], [127], [190], [191]])
+def test_tiny_edge_positions(positions):
+    # position 0 attends to one key; 191 is the last slot of the 192-slot cache
+    say(f"[tiny-edge] positions={positions}")
+    c = Case(TINY, 1, 192, positions, seed=21)
+    ref = c.oracle_step()
+    outs = [c.gpu_step(mode) for _, mode in MODES]
+    check_against_oracle(c, outs[1], ref)
+    assert_bit_exact(outs[0], outs[1], "per_layer vs looped")
+    assert_bit_exact(outs[2], outs[1], "per_op vs looped")
+
+
+def test_tiny_batch_with_ragged_positions():
+    say("[tiny-batch] batch=5 ragged positions")
+    c = Case(TINY, 5, 320, [0, 63, 64, 257, 319], seed=31)
+    ref = c.oracle_step()
+    outs = [c.gpu_step(mode) for _, mode in MODES]
+    check_against_oracle(c, outs[1], ref)
+    assert_bit_exact(outs[0], outs[1], "per_layer vs looped")
+    assert_bit_exact(outs[2], outs[1], "per_op vs looped")
+
+
+def test_tiny_batch_smaller_than_allocated():
+    # the step's batch may be below max_batch and below the cache's batch extent
+    say("[tiny-batch] batch 2 of max 4")
+    c = Case(TINY, 4, 128, [5, 100, 17, 60], seed=41, max_batch=4)
+    ref = c.oracle_step()
+    kv = KvCache(c.cfg, 4, 128, k_host=c.K0, v_host=c.V0)
+    toks = torch.from_numpy(c.tokens[:2]).cuda()
+    pos = torch.from_numpy(c.positions[:2]).cuda()
+    logits = torch.zeros((2, c.cfg["vocab"]), device="cuda")
+    c.model.step(toks, pos, kv, logits, None, kb.KL_MODE_LOOPED)
+    torch.cuda.synchronize()
+    lg = logits.cpu().numpy()
+    import oracle
+    for b in range(2):
+        assert oracle.rel_l2(lg[b], ref[0][b]) <= 1e-2
+    K, _ = kv.host()
+    assert np.array_equal(K[:, 2:], c.K0[:, 2:]), "sequences beyond the step's batch were written"
+
+
+def test_device_error_bits_for_bad_token_and_position(tiny):
+    say("[tiny] bad token and position")
+    V = tiny.cfg["vocab"]
+    lg, _, _, _ = tiny.gpu_step(kb.KL_MODE_LOOPED, tokens=np.array([V], dtype=np.int32))
+    assert tiny.model.device_error() == kb.KL_DEVERR_TOKEN
+    assert np.isfinite(lg).all()
+    lg, _, _, _ = tiny.gpu_step(kb.KL_MODE_PER_LAYER,
+                                positions=np.array([tiny.capacity], dtype=np.int32))
+    assert tiny.model.device_error() == kb.KL_DEVERR_POSITION
+    assert np.isfinite(lg).all()
+    assert tiny.model.device_error() == 0          # cleared
+    ref = tiny.oracle_step()
+    check_against_oracle(tiny, tiny.gpu_step(kb.KL_MODE_LOOPED), ref)
+
+
+def test_host_validation_enqueues_nothing(tiny):
+    kv = KvCache(tiny.cfg, 1, tiny.capacity)
+    toks = torch.zeros(1, dtype=torch.int32, device="cuda")
+    logits = torch.zeros((1, tiny.cfg["vocab"]), device="cuda")
+    with pytest.raises(kb.KlError) as e:
+        tiny.model.step(toks, toks, kv, logits, None, 7)
+    assert e.value.status == kb.KL_ERR_INVALID_ARGUMENT
+    with pytest.raises(kb.KlError):
+        kb.kl_decode_step(tiny.model.state, toks.data_ptr(), toks.data_ptr(), 2, kv.k.data_ptr(),
+                          kv.v.data_ptr(), 1, tiny.capacity, logits.data_ptr(), None, 0,
+                          kb.KL_MODE_LOOPED)
+
+
+def test_llama8b_width_two_layers_long_cache():
+    # the 8B layer shapes (d 128, 4 query heads per KV head, K 4096 and 14336,
+    # 128256-row LM head) over a 4096-position cache, with 2 layers
+    cfg = dict(WORKLOADS["llama8b-b1-ctx4096"]["model"], n_layers=2)
+    say("[8b-width L=2] building")
+    c = Case(cfg, 1, 4160, [4096], seed=51)
+    say("[8b-width L=2] oracle")
+    ref = c.oracle_step(nthreads=8)
+    outs = []
+    for name, mode in MODES:
+        say(f"[8b-width L=2] mode={name}")
+        outs.append(c.gpu_step(mode))
+    check_against_oracle(c, outs[1], ref)
+    assert_bit_exact(outs[0], outs[1], "per_layer vs looped")
+    assert_bit_exact(outs[2], outs[1], "per_op vs looped")
