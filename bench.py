@@ -152,6 +152,10 @@ def main():
                                "sample": f"one full decode step of {args.workload}, fp64 oracle, "
                                          f"1 thread, {cpu_s:.1f} s"}
     print(json.dumps(out), flush=True)
+    # release device memory before interpreter shutdown
+    model.close()
+    del kv, toks, pos, logits
+    torch.cuda.synchronize()
 
 
 if __name__ == "__main__":

@@ -12,6 +12,14 @@
 // The work partition depends only on StepParams::nwg, so every schedule
 // performs the same arithmetic in the same order: results are bit-identical.
 //
+// Pipelining across phases (the "pipelined outer loop" of Sec. 3.2): a phase
+// issues the first loads of its weight tiles before it waits for the barrier
+// that publishes its input activations, so HBM keeps streaming while the
+// grid synchronises.  Data that crosses workgroups (activations, partials,
+// the new KV slot) is written and read with device-coherent (agent-scope)
+// accesses, so a barrier needs no cache write-back or invalidation: only the
+// completion of the stores before the arrival.
+//
 // Weights are pre-packed into 1 KiB tiles of 8 rows x 64 columns (bf16,
 // row-major inside the tile); the tiles of one 8-row group are contiguous
 // along K.  A wave reads one tile per 16-byte-per-lane load: lane l holds row
@@ -104,41 +112,103 @@ __device__ __forceinline__ size_t kv_row(const StepParams &P, int l, int b, int 
     return (((size_t)l * P.kv_batch + b) * P.nkv + g) * (size_t)P.cap;
 }
 
+// ---------------------------------------------------------------- coherent accesses
+//
+// Relaxed agent-scope atomic loads and stores compile to ordinary vector
+// memory instructions with the device-coherence bit (sc1): they see, and are
+// seen by, every XCD without flushing or invalidating the XCD-private L2.
+
+__device__ __forceinline__ void st_dev(float *p, float v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_dev_u16(uint16_t *p, uint16_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_dev_u32(unsigned *p, unsigned v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ld_dev(const float *p) {
+    return __hip_atomic_load(const_cast<float *>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ unsigned long long ld_dev_u64(const void *p) {
+    return __hip_atomic_load(reinterpret_cast<unsigned long long *>(const_cast<void *>(p)),
+                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ u32x4 ld_dev_16B(const void *p) {
+    const unsigned long long a = ld_dev_u64(p);
+    const unsigned long long b = ld_dev_u64(reinterpret_cast<const char *>(p) + 8);
+    return u32x4{(unsigned)a, (unsigned)(a >> 32), (unsigned)b, (unsigned)(b >> 32)};
+}
+__device__ __forceinline__ u32x4 ld_stream_16B(const void *p) {
+    return __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
+}
+
+// s_waitcnt vmcnt(0): this wave's stores have completed at their coherence point.
+__device__ __forceinline__ void wait_stores() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
 // ---------------------------------------------------------------- grid barrier
 //
-// A generation barrier over the nwg co-resident workgroups.  Arrivals count
-// up one word; the last arrival resets it and bumps the generation word that
-// the others poll.  Release/acquire at agent scope makes every workgroup's
-// global writes before the barrier visible to every workgroup after it,
-// across XCDs.  The wait is bounded: after ~2 s it raises KL_DEVERR_BARRIER,
-// and any later wait returns at once once that bit is set, so a broken
-// barrier ends the kernel instead of hanging it.
+// Two-level arrival counting on monotonically increasing 64-bit counters:
+// workgroup w arrives on group counter w % ng; the last arrival of a group
+// bumps the root counter; waiters poll the root for its target value.  The
+// counters are never reset: at launch start each workgroup rounds the
+// current values down to whole barriers (every launch ends with all
+// counters at a multiple of their group size, and no group can complete the
+// first barrier before every member has read its base).  Barrier k of a
+// launch is complete when root reaches base + (k + 1) * ng.  The wait is
+// bounded: after ~2 s it raises KL_DEVERR_BARRIER and every later wait
+// returns at once, so a broken barrier ends the kernel instead of hanging it.
 constexpr long long kBarrierTicks = 200000000LL;   // s_memrealtime runs at 100 MHz
 
-__device__ __forceinline__ void grid_sync(const StepParams &P) {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+__shared__ unsigned long long kl_bar_base[2];      // root base, group base (this launch)
+
+__device__ __forceinline__ void bar_geometry(const StepParams &P, int &ng, int &g,
+                                             unsigned &gsize) {
+    ng = min(kBarGroups, P.nwg);
+    g = blockIdx.x % ng;
+    gsize = (unsigned)(P.nwg / ng + (g < P.nwg % ng ? 1 : 0));
+}
+
+__device__ void bar_init(const StepParams &P) {
+    if (threadIdx.x == 0) {
+        int ng, g;
+        unsigned gsize;
+        bar_geometry(P, ng, g, gsize);
+        const unsigned long long r = ld_dev_u64(P.bar);
+        const unsigned long long c = ld_dev_u64(P.bar + 32 * (g + 1));
+        kl_bar_base[0] = r - r % (unsigned long long)ng;
+        kl_bar_base[1] = c - c % gsize;
+    }
+    __syncthreads();
+}
+
+__device__ __forceinline__ void bar_arrive(const StepParams &P, int k) {
+    wait_stores();
     __syncthreads();
     if (threadIdx.x == 0) {
-        unsigned *arrive = P.bar;
-        unsigned *gen = P.bar + 64;
-        const unsigned g0 = __hip_atomic_load(gen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        const unsigned old = __hip_atomic_fetch_add(arrive, 1u, __ATOMIC_ACQ_REL,
-                                                    __HIP_MEMORY_SCOPE_AGENT);
-        if (old == (unsigned)P.nwg - 1u) {
-            __hip_atomic_store(arrive, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            __hip_atomic_fetch_add(gen, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-        } else {
-            const long long t0 = wall_clock64();
-            while (__hip_atomic_load(gen, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) == g0) {
-                if (__hip_atomic_load(P.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) &
-                    KL_DEVERR_BARRIER)
-                    break;
-                if (wall_clock64() - t0 > kBarrierTicks) {
-                    __hip_atomic_fetch_or(P.err, KL_DEVERR_BARRIER, __ATOMIC_RELAXED,
-                                          __HIP_MEMORY_SCOPE_AGENT);
-                    break;
-                }
-                __builtin_amdgcn_s_sleep(1);
+        int ng, g;
+        unsigned gsize;
+        bar_geometry(P, ng, g, gsize);
+        const unsigned long long old = __hip_atomic_fetch_add(
+            P.bar + 32 * (g + 1), 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (old == kl_bar_base[1] + (unsigned long long)(k + 1) * gsize - 1ull)
+            __hip_atomic_fetch_add(P.bar, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+}
+
+__device__ __forceinline__ void bar_wait(const StepParams &P, int k) {
+    if (threadIdx.x == 0) {
+        const int ng = min(kBarGroups, P.nwg);
+        const unsigned long long target = kl_bar_base[0] + (unsigned long long)(k + 1) * ng;
+        const long long t0 = wall_clock64();
+        while ((long long)(ld_dev_u64(P.bar) - target) < 0) {
+            if (__hip_atomic_load(P.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) &
+                KL_DEVERR_BARRIER)
+                break;
+            if (wall_clock64() - t0 > kBarrierTicks) {
+                __hip_atomic_fetch_or(P.err, KL_DEVERR_BARRIER, __ATOMIC_RELAXED,
+                                      __HIP_MEMORY_SCOPE_AGENT);
+                break;
             }
         }
     }
@@ -188,10 +258,13 @@ struct Lds {
     float *sm;    // small reductions and flags
 };
 
+__device__ __forceinline__ int attn_cmax(const StepParams &P) { return max(1, P.nwg / P.nkv); }
+
 __device__ __forceinline__ Lds lds_layout(char *smem, const StepParams &P) {
     Lds s;
     int amax = max(max(P.Hp, P.Ap), P.Fp);
-    const int attn = P.group * P.d + P.group * kAttnSub + P.group * 4 + kWaves * P.group * P.d;
+    const int attn = P.group * P.d + P.group * kAttnSub + P.group * 4 + kWaves * P.group * P.d +
+                     3 * attn_cmax(P) * P.group + P.group;
     amax = max(amax, attn);
     amax = (amax + 63) & ~63;
     s.a = reinterpret_cast<float *>(smem);
@@ -202,133 +275,161 @@ __device__ __forceinline__ Lds lds_layout(char *smem, const StepParams &P) {
 
 // ---------------------------------------------------------------- activations
 
-// a[i] = x[i] * rsqrt(mean(x^2) + eps) * gain[i] for i < n, 0 up to npad.
-__device__ __forceinline__ void rmsnorm_to_lds(const float *__restrict__ x, const float *__restrict__ gain,
-                               int n, int npad, float eps, float *a, float *sm) {
-    float ss = 0.f;
-    for (int i = threadIdx.x; i < n; i += kThreads) {
-        const float v = x[i];
-        ss = fmaf(v, v, ss);
+// Copy a device-coherent fp32 vector of n (even) values into LDS, zero up to npad.
+__device__ __forceinline__ void stage_vec(const float *__restrict__ src, int n, int npad,
+                                          float *a) {
+    for (int i = threadIdx.x; 2 * i < npad; i += kThreads) {
+        float lo = 0.f, hi = 0.f;
+        if (2 * i < n) {
+            const unsigned long long v = ld_dev_u64(src + 2 * i);
+            lo = __uint_as_float((unsigned)v);
+            hi = __uint_as_float((unsigned)(v >> 32));
+        }
+        a[2 * i] = lo;
+        a[2 * i + 1] = hi;
     }
-    ss = block_sum(ss, sm);
-    const float r = 1.0f / sqrtf(ss / (float)n + eps);
-    for (int i = threadIdx.x; i < npad; i += kThreads) a[i] = (i < n) ? x[i] * r * gain[i] : 0.f;
     __syncthreads();
 }
 
-__device__ __forceinline__ void vec_to_lds(const float *__restrict__ src, int n, float *a) {
-    for (int i = threadIdx.x; i < n; i += kThreads) a[i] = src[i];
+// a[i] = x[i] * rsqrt(mean(x^2) + eps) * gain[i] for i < n, 0 up to npad.
+__device__ __forceinline__ void stage_rmsnorm(const float *__restrict__ x,
+                                              const float *__restrict__ gain, int n, int npad,
+                                              float eps, float *a, float *sm) {
+    stage_vec(x, n, npad, a);
+    float ss = 0.f;
+    for (int i = threadIdx.x; i < n; i += kThreads) ss = fmaf(a[i], a[i], ss);
+    ss = block_sum(ss, sm);
+    const float r = 1.0f / sqrtf(ss / (float)n + eps);
+    for (int i = threadIdx.x; i < n; i += kThreads) a[i] = a[i] * r * gain[i];
     __syncthreads();
 }
 
 // ---------------------------------------------------------------- GEMV engine
 //
-// y[r] = sum_k W[r][k] a[k] for the rows of row groups [rg0, rg1) of a packed
-// matrix with KT k-tiles per row group.  Each wave takes a fixed slice of the
-// k-tiles of every row group (split-K inside the workgroup), keeps U tile
-// loads in flight, and reduces its partial dot products over the 8 lanes of a
-// row with DPP.  The slices are summed in wave order through LDS, and epi is
-// called once per row pair (r even, r + 1).
-template <class Epi>
-__device__ __forceinline__ void gemv_rows(const uint8_t *__restrict__ W, int KT, int rg0, int rg1,
-                                          const float *__restrict__ a, float *red, Epi &&epi) {
-    constexpr int U = 8;
+// y_b[r] = sum_k W[r][k] a_b[k] for the rows of row groups [rg0, rg1) of a
+// packed matrix with KT k-tiles per row group, for each sequence b.  Each
+// wave takes a fixed slice of the k-tiles of every row group (split-K inside
+// the workgroup), keeps U tile loads in flight, and reduces its partial dot
+// products over the 8 lanes of a row with DPP.  The slices are summed in wave
+// order through LDS, and epi(b, r, y_r, y_r+1) is called once per row pair.
+// Row groups are processed in batches of kRgBatch.  The first loads are
+// issued before wait() (the grid barrier that publishes the activations) and
+// before stage(b) (which fills a with sequence b's activation vector); each
+// next batch's first loads are issued before the previous batch's reduction.
+constexpr int kGemvDepth = 16;   // tile loads in flight per wave (16 KiB)
+
+// The ring of tile loads must stay in flight across loop iterations, the
+// grid barrier and the activation staging, and the compiler only places a
+// precise "wait for the oldest load" (vmcnt(U-1)) when every path issues the
+// same loads.  So the ring is refilled unconditionally: once the batch's real
+// tiles are exhausted, a slot is refilled from a 16-byte dummy line that all
+// lanes share (one cache line per wave), and only the consumption of a slot
+// is conditional.
+template <class Wait, class Stage, class Epi>
+__device__ __forceinline__ void gemv_phase(const uint8_t *__restrict__ W, int KT, int rg0,
+                                           int rg1, int B, const float *__restrict__ a,
+                                           float *red, const uint8_t *dummy, Wait &&wait,
+                                           Stage &&stage, Epi &&epi) {
+    constexpr int U = kGemvDepth;
     // wave-uniform values live in scalar registers, so every branch below is
-    // a scalar branch and the loads of the main loop are unconditional
+    // a scalar branch
     const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
-    const int kt0 = (wid * KT) / kWaves, kt1 = ((wid + 1) * KT) / kWaves;
-    const int nk = kt1 - kt0;
     const int row = lane >> 3, sub = lane & 7;
+    const int kt0 = (wid * KT) / kWaves;
+    const int nk = ((wid + 1) * KT) / kWaves - kt0;
     const uint8_t *base = W + (size_t)lane * 16;
     const float *abase = a + sub * 8;
-    for (int rb0 = rg0; rb0 < rg1; rb0 += kRgBatch) {
-        const int nrg = min(kRgBatch, rg1 - rb0);
-        const int n = nk * nrg;
-        if (n > 0) {
-            u32x4 buf[U];
-            int lr = 0, lk = 0;        // next tile to load
-            int cr = 0, ck = 0;        // next tile to consume
+    u32x4 buf[U];
+    int n = 0, ltile = 0, lk = 0, left = 0;   // batch items; next tile, its k index; tiles left
+
+    // load the next tile of the batch, or the dummy line (branch-free)
+    auto load_next = [&]() {
+        const int t = __builtin_amdgcn_readfirstlane(ltile);
+        const bool real = left > 0;
+        const u32x4 v = ld_stream_16B(real ? base + (size_t)t * kTileBytes : dummy);
+        const bool wrap = lk + 1 == nk;
+        ltile = real ? ltile + (wrap ? KT - nk + 1 : 1) : ltile;
+        lk = real ? (wrap ? 0 : lk + 1) : lk;
+        left = real ? left - 1 : left;
+        return v;
+    };
+    auto start = [&](int rb) {
+        n = nk * min(kRgBatch, rg1 - rb);
+        left = n;
+        ltile = rb * KT + kt0;
+        lk = 0;
+#pragma unroll
+        for (int s = 0; s < U; ++s) buf[s] = load_next();
+    };
+
+    const bool has_rows = rg0 < rg1;
+    if (has_rows) start(rg0);
+    wait();
+    if (!has_rows) return;
+    for (int b = 0; b < B; ++b) {
+        for (int rb = rg0; rb < rg1; rb += kRgBatch) {
+            if (b > 0 || rb > rg0) start(rb);
+            if (rb == rg0) stage(b);
+            const int nrg = min(kRgBatch, rg1 - rb);
+            int cr = 0, ck = 0;
             float acc = 0.f;
-            auto load_next = [&]() {
-                const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(
-                    base + ((size_t)(rb0 + lr) * KT + kt0 + lk) * kTileBytes));
-                if (++lk == nk) { lk = 0; ++lr; }
-                return v;
-            };
-            auto consume = [&](const u32x4 wv) {
-                const float *ap = abase + (kt0 + ck) * kTileK;
-                const float4 a0 = *reinterpret_cast<const float4 *>(ap);
-                const float4 a1 = *reinterpret_cast<const float4 *>(ap + 4);
-                acc = fmaf(bf_lo(wv.x), a0.x, acc);
-                acc = fmaf(bf_hi(wv.x), a0.y, acc);
-                acc = fmaf(bf_lo(wv.y), a0.z, acc);
-                acc = fmaf(bf_hi(wv.y), a0.w, acc);
-                acc = fmaf(bf_lo(wv.z), a1.x, acc);
-                acc = fmaf(bf_hi(wv.z), a1.y, acc);
-                acc = fmaf(bf_lo(wv.w), a1.z, acc);
-                acc = fmaf(bf_hi(wv.w), a1.w, acc);
-                if (++ck == nk) {
-                    const float t = sum8(acc);
-                    if (sub == 0) red[(wid * kRgBatch + cr) * kTileRows + row] = t;
-                    acc = 0.f;
-                    ck = 0;
-                    ++cr;
-                }
-            };
-            if (n >= U) {
-                // every path into the main loop has exactly U loads in flight, so
-                // the compiler can wait for the oldest one only (vmcnt(U-1))
-#pragma unroll
-                for (int s = 0; s < U; ++s) buf[s] = load_next();
-                int i0 = 0;
-                for (; i0 + 2 * U <= n; i0 += U) {
-#pragma unroll
-                    for (int s = 0; s < U; ++s) {
-                        // consume before refilling: the refill reuses the slot's registers
-                        consume(buf[s]);
-                        buf[s] = load_next();
-                    }
-                }
-                const int rem = n - i0;   // in [U, 2U): U items in buf, rem - U still to load
+            // item i sits in slot i % U and is refilled with item i + U (or
+            // the dummy line) right after it is consumed
+            for (int i0 = 0; i0 < n; i0 += U) {
 #pragma unroll
                 for (int s = 0; s < U; ++s) {
-                    consume(buf[s]);
-                    if (s + U < rem) buf[s] = load_next();
+                    if (i0 + s < n) {
+                        const u32x4 wv = buf[s];
+                        const float *ap = abase + (kt0 + ck) * kTileK;
+                        const float4 a0 = *reinterpret_cast<const float4 *>(ap);
+                        const float4 a1 = *reinterpret_cast<const float4 *>(ap + 4);
+                        acc = fmaf(bf_lo(wv.x), a0.x, acc);
+                        acc = fmaf(bf_hi(wv.x), a0.y, acc);
+                        acc = fmaf(bf_lo(wv.y), a0.z, acc);
+                        acc = fmaf(bf_hi(wv.y), a0.w, acc);
+                        acc = fmaf(bf_lo(wv.z), a1.x, acc);
+                        acc = fmaf(bf_hi(wv.z), a1.y, acc);
+                        acc = fmaf(bf_lo(wv.w), a1.z, acc);
+                        acc = fmaf(bf_hi(wv.w), a1.w, acc);
+                        if (++ck == nk) {
+                            const float t = sum8(acc);
+                            if (sub == 0) red[(wid * kRgBatch + cr) * kTileRows + row] = t;
+                            acc = 0.f;
+                            ck = 0;
+                            ++cr;
+                        }
+                    }
+                    buf[s] = load_next();
                 }
-#pragma unroll
-                for (int s = 0; s < U; ++s)
-                    if (s + U < rem) consume(buf[s]);
-            } else {
-#pragma unroll
-                for (int s = 0; s < U; ++s)
-                    if (s < n) buf[s] = load_next();
-#pragma unroll
-                for (int s = 0; s < U; ++s)
-                    if (s < n) consume(buf[s]);
             }
-        }
-        __syncthreads();
-        for (int t = threadIdx.x; t < nrg * (kTileRows / 2); t += kThreads) {
-            const int rgi = t / (kTileRows / 2), pr = (t % (kTileRows / 2)) * 2;
-            float y0 = 0.f, y1 = 0.f;
-            for (int w = 0; w < kWaves; ++w) {
-                if (((w + 1) * KT) / kWaves == (w * KT) / kWaves) continue;   // empty slice
-                y0 += red[(w * kRgBatch + rgi) * kTileRows + pr];
-                y1 += red[(w * kRgBatch + rgi) * kTileRows + pr + 1];
+            __syncthreads();
+            for (int t = threadIdx.x; t < nrg * (kTileRows / 2); t += kThreads) {
+                const int rgi = t / (kTileRows / 2), pr = (t % (kTileRows / 2)) * 2;
+                float y0 = 0.f, y1 = 0.f;
+                for (int w = 0; w < kWaves; ++w) {
+                    if (((w + 1) * KT) / kWaves == (w * KT) / kWaves) continue;   // empty slice
+                    y0 += red[(w * kRgBatch + rgi) * kTileRows + pr];
+                    y1 += red[(w * kRgBatch + rgi) * kTileRows + pr + 1];
+                }
+                epi(b, (rb + rgi) * kTileRows + pr, y0, y1);
             }
-            epi((rb0 + rgi) * kTileRows + pr, y0, y1);
+            __syncthreads();
         }
-        __syncthreads();
     }
 }
 
 // ---------------------------------------------------------------- phases
+//
+// Every phase takes (wait, arrive): the barrier index to wait on before its
+// inputs are read (-1: none, the inputs come from an earlier launch) and the
+// barrier index to arrive on after its outputs are written (-1: none).
 
 // Embedding block (Sec. 2): x = f32(E[token]).  Workgroup 0 records bad
 // token ids and positions in the device error word.
-__device__ __noinline__ void phase_embed(KArg ka) {
+__device__ __noinline__ void phase_embed(KArg ka, int wait, int arrive) {
     const StepParams P = load_params(ka);
+    if (wait >= 0) bar_wait(P, wait);
     if (blockIdx.x == 0) {
         for (int b = threadIdx.x; b < P.B; b += kThreads) {
             const int t = P.tokens[b], p = P.positions[b];
@@ -341,58 +442,59 @@ __device__ __noinline__ void phase_embed(KArg ka) {
     const int total = P.B * P.Hp;
     for (int idx = blockIdx.x * kThreads + threadIdx.x; idx < total; idx += P.nwg * kThreads) {
         const int b = idx / P.Hp, i = idx % P.Hp;
-        P.x[idx] = (i < P.H) ? bf2f(P.embed[(size_t)eff_tok(P, b) * P.H + i]) : 0.f;
+        st_dev(P.x + idx, (i < P.H) ? bf2f(P.embed[(size_t)eff_tok(P, b) * P.H + i]) : 0.f);
     }
+    if (arrive >= 0) bar_arrive(P, arrive);
 }
 
 // RMSNorm + fused Q/K/V projection + RoPE + KV-cache append.  Q/K rows are
 // packed in rotation pairs (dims i and i + d/2 adjacent), V rows in order.
-__device__ __noinline__ void phase_qkv(KArg ka, int l) {
+__device__ __noinline__ void phase_qkv(KArg ka, int l, int wait, int arrive) {
     const StepParams P = load_params(ka);
     const Lds S = lds_layout(kl_smem, P);
     int rg0, rg1;
     split_range(P.qkv_rg, P.nwg, blockIdx.x, rg0, rg1);
-    if (rg0 == rg1) return;
     const uint8_t *Lb = P.arena + (size_t)l * P.layer_stride;
     const float *gain = reinterpret_cast<const float *>(Lb + P.off_attn_norm);
     const int d = P.d, half = P.d / 2, qd = P.nq * P.d, kd = P.nkv * P.d;
-    for (int b = 0; b < P.B; ++b) {
-        rmsnorm_to_lds(P.x + (size_t)b * P.Hp, gain, P.H, P.Hp, P.eps, S.a, S.sm);
-        const int p = eff_pos(P, b);
-        const float2 *rp = P.rope + (size_t)p * half;
-        gemv_rows(Lb + P.off_qkv, P.Hp / kTileK, rg0, rg1, S.a, S.red,
-                  [&](int r, float y0, float y1) {
-                      if (r < qd + kd) {
-                          const int h = r / d, i = (r % d) >> 1;
-                          const float2 cs = rp[i];
-                          const float u0 = y0 * cs.x - y1 * cs.y;
-                          const float u1 = y0 * cs.y + y1 * cs.x;
-                          if (r < qd) {
-                              float *qq = P.q + (size_t)b * qd + (size_t)h * d;
-                              qq[i] = u0;
-                              qq[i + half] = u1;
-                          } else {
-                              uint16_t *kk = P.kc + (kv_row(P, l, b, h - P.nq) + p) * d;
-                              kk[i] = f2bf(u0);
-                              kk[i + half] = f2bf(u1);
-                          }
-                      } else {
-                          const int rr = r - qd - kd, g = rr / d, j = rr % d;
-                          uint16_t *vv = P.vc + (kv_row(P, l, b, g) + p) * d;
-                          vv[j] = f2bf(y0);
-                          vv[j + 1] = f2bf(y1);
-                      }
-                  });
-    }
+    gemv_phase(
+        Lb + P.off_qkv, P.Hp / kTileK, rg0, rg1, P.B, S.a, S.red, P.dummy,
+        [&]() { if (wait >= 0) bar_wait(P, wait); },
+        [&](int b) { stage_rmsnorm(P.x + (size_t)b * P.Hp, gain, P.H, P.Hp, P.eps, S.a, S.sm); },
+        [&](int b, int r, float y0, float y1) {
+            const int p = eff_pos(P, b);
+            if (r < qd + kd) {
+                const int h = r / d, i = (r % d) >> 1;
+                const float2 cs = P.rope[(size_t)p * half + i];
+                const float u0 = y0 * cs.x - y1 * cs.y;
+                const float u1 = y0 * cs.y + y1 * cs.x;
+                if (r < qd) {
+                    float *qq = P.q + (size_t)b * qd + (size_t)h * d;
+                    st_dev(qq + i, u0);
+                    st_dev(qq + i + half, u1);
+                } else {
+                    uint16_t *kk = P.kc + (kv_row(P, l, b, h - P.nq) + p) * d;
+                    st_dev_u16(kk + i, f2bf(u0));
+                    st_dev_u16(kk + i + half, f2bf(u1));
+                }
+            } else {
+                const int rr = r - qd - kd, g = rr / d, j = rr % d;
+                uint16_t *vv = P.vc + (kv_row(P, l, b, g) + p) * d;
+                st_dev_u32(reinterpret_cast<unsigned *>(vv + j),
+                           (unsigned)f2bf(y0) | ((unsigned)f2bf(y1) << 16));
+            }
+        });
+    if (arrive >= 0) bar_arrive(P, arrive);
 }
 
 // One attention work item: the positions of chunk c of sequence b against KV
 // head g, for the G query heads of that group.  Scores and probabilities are
 // fp32; the chunk result is (running max, running sum, unnormalised output)
 // per head.  The last workgroup to finish a (b, g) combines all chunks in
-// chunk order and writes o.
+// chunk order and writes o.  The KV tiles of the first sub-chunk are loaded
+// before the barrier wait, except the new slot, which the QKV phase writes.
 template <int D, int G>
-__device__ __noinline__ void attn_item(KArg ka, int l, int b, int g, int c) {
+__device__ __noinline__ void attn_item(KArg ka, int l, int b, int g, int c, int wait) {
     const StepParams P = load_params(ka);
     const Lds S = lds_layout(kl_smem, P);
     constexpr int LP = D / 8;                       // lanes per position
@@ -401,7 +503,7 @@ __device__ __noinline__ void attn_item(KArg ka, int l, int b, int g, int c) {
     const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
     const int pi = lane / LP, ds = (lane % LP) * 8;
-    const int n = eff_pos(P, b) + 1;
+    const int pnew = eff_pos(P, b), n = pnew + 1;
     const int cs = (n + P.C - 1) / P.C;
     const int j0 = min(n, c * cs), j1 = min(n, j0 + cs);
 
@@ -409,13 +511,47 @@ __device__ __noinline__ void attn_item(KArg ka, int l, int b, int g, int c) {
     float *sp = qs + G * D;             // [G][kAttnSub]
     float *st = sp + G * kAttnSub;      // [G][4]
     float *red = st + G * 4;            // [kWaves][G][D]
+    float *cst = red + kWaves * G * D;  // combine: [3][Cmax][G] + [G]
     const size_t row0 = kv_row(P, l, b, g);
     const uint16_t *Kb = P.kc + row0 * D;
     const uint16_t *Vb = P.vc + row0 * D;
     const float scale = 1.0f / sqrtf((float)D);
 
+    u32x4 kr[NG], vr[NG];
+    // pre: true before the barrier, when the new slot is not written yet
+    auto issue = [&](int js, int len, bool pre) {
+#pragma unroll
+        for (int t = 0; t < NG; ++t) {
+            const int jl = (wid * NG + t) * PP + pi;
+            const int pos = js + jl;
+            if (jl < len && pos != pnew) {
+                kr[t] = ld_stream_16B(Kb + (size_t)pos * D + ds);
+                vr[t] = ld_stream_16B(Vb + (size_t)pos * D + ds);
+            } else if (jl < len && !pre) {
+                kr[t] = ld_dev_16B(Kb + (size_t)pos * D + ds);
+                vr[t] = ld_dev_16B(Vb + (size_t)pos * D + ds);
+            } else {
+                kr[t] = u32x4{0u, 0u, 0u, 0u};
+                vr[t] = u32x4{0u, 0u, 0u, 0u};
+            }
+        }
+    };
+    const int len0 = min(kAttnSub, j1 - j0);
+    if (j0 < j1) issue(j0, len0, true);
+    if (wait >= 0) bar_wait(P, wait);
+    if (j0 < j1 && pnew >= j0 && pnew < j0 + len0) {
+        // the new slot lies in the first sub-chunk: fetch it now, coherently
+#pragma unroll
+        for (int t = 0; t < NG; ++t) {
+            const int pos = j0 + (wid * NG + t) * PP + pi;
+            if (pos == pnew) {
+                kr[t] = ld_dev_16B(Kb + (size_t)pos * D + ds);
+                vr[t] = ld_dev_16B(Vb + (size_t)pos * D + ds);
+            }
+        }
+    }
     for (int t = threadIdx.x; t < G * D; t += kThreads)
-        qs[t] = P.q[(size_t)b * P.nq * D + (size_t)g * G * D + t];
+        qs[t] = ld_dev(P.q + (size_t)b * P.nq * D + (size_t)g * G * D + t);
     if (threadIdx.x < G) {
         st[threadIdx.x * 4 + 0] = -INFINITY;
         st[threadIdx.x * 4 + 1] = 0.f;
@@ -429,20 +565,13 @@ __device__ __noinline__ void attn_item(KArg ka, int l, int b, int g, int c) {
 
     for (int js = j0; js < j1; js += kAttnSub) {
         const int len = min(kAttnSub, j1 - js);
-        u32x4 kv[NG];
-#pragma unroll
-        for (int t = 0; t < NG; ++t) {
-            const int jl = (wid * NG + t) * PP + pi;
-            kv[t] = (jl < len) ? __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(
-                                     Kb + (size_t)(js + jl) * D + ds))
-                               : u32x4{0u, 0u, 0u, 0u};
-        }
+        if (js != j0) issue(js, len, false);
         // scores (q is read from LDS; all lanes take part in the lane sums)
 #pragma unroll
         for (int t = 0; t < NG; ++t) {
             const int jl = (wid * NG + t) * PP + pi;
-            const float kf[8] = {bf_lo(kv[t].x), bf_hi(kv[t].x), bf_lo(kv[t].y), bf_hi(kv[t].y),
-                                 bf_lo(kv[t].z), bf_hi(kv[t].z), bf_lo(kv[t].w), bf_hi(kv[t].w)};
+            const float kf[8] = {bf_lo(kr[t].x), bf_hi(kr[t].x), bf_lo(kr[t].y), bf_hi(kr[t].y),
+                                 bf_lo(kr[t].z), bf_hi(kr[t].z), bf_lo(kr[t].w), bf_hi(kr[t].w)};
 #pragma unroll
             for (int h = 0; h < G; ++h) {
                 const float4 q0 = *reinterpret_cast<const float4 *>(qs + h * D + ds);
@@ -459,14 +588,6 @@ __device__ __noinline__ void attn_item(KArg ka, int l, int b, int g, int c) {
                 s = sum_lanes<LP>(s);
                 if (jl < len && (lane % LP) == 0) sp[h * kAttnSub + jl] = s * scale;
             }
-        }
-        // V loads go out now and land during the softmax step
-#pragma unroll
-        for (int t = 0; t < NG; ++t) {
-            const int jl = (wid * NG + t) * PP + pi;
-            kv[t] = (jl < len) ? __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(
-                                     Vb + (size_t)(js + jl) * D + ds))
-                               : u32x4{0u, 0u, 0u, 0u};
         }
         __syncthreads();
         // softmax statistics: wave h owns head h
@@ -502,9 +623,9 @@ __device__ __noinline__ void attn_item(KArg ka, int l, int b, int g, int c) {
         for (int t = 0; t < NG; ++t) {
             const int jl = (wid * NG + t) * PP + pi;
             if (jl < len) {
-                const float vf[8] = {bf_lo(kv[t].x), bf_hi(kv[t].x), bf_lo(kv[t].y),
-                                     bf_hi(kv[t].y), bf_lo(kv[t].z), bf_hi(kv[t].z),
-                                     bf_lo(kv[t].w), bf_hi(kv[t].w)};
+                const float vf[8] = {bf_lo(vr[t].x), bf_hi(vr[t].x), bf_lo(vr[t].y),
+                                     bf_hi(vr[t].y), bf_lo(vr[t].z), bf_hi(vr[t].z),
+                                     bf_lo(vr[t].w), bf_hi(vr[t].w)};
 #pragma unroll
                 for (int h = 0; h < G; ++h) {
                     const float pr = sp[h * kAttnSub + jl];
@@ -538,19 +659,19 @@ __device__ __noinline__ void attn_item(KArg ka, int l, int b, int g, int c) {
         const int h = t / D, dd = t % D;
         float s = 0.f;
         for (int w = 0; w < kWaves; ++w) s += red[(w * G + h) * D + dd];
-        out[h * (D + 2) + dd] = s;
+        st_dev(out + h * (D + 2) + dd, s);
     }
     if (threadIdx.x < G) {
-        out[threadIdx.x * (D + 2) + D] = st[threadIdx.x * 4 + 0];
-        out[threadIdx.x * (D + 2) + D + 1] = st[threadIdx.x * 4 + 1];
+        st_dev(out + threadIdx.x * (D + 2) + D, st[threadIdx.x * 4 + 0]);
+        st_dev(out + threadIdx.x * (D + 2) + D + 1, st[threadIdx.x * 4 + 1]);
     }
     // publish this chunk; the last arrival for (b, g) combines
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    wait_stores();
     __syncthreads();
     int *flag = reinterpret_cast<int *>(S.sm);
     if (threadIdx.x == 0) {
         unsigned *cnt = P.cnt + b * P.nkv + g;
-        const unsigned old = __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_ACQ_REL,
+        const unsigned old = __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED,
                                                     __HIP_MEMORY_SCOPE_AGENT);
         const int last = old == (unsigned)(P.C - 1);
         if (last) __hip_atomic_store(cnt, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -558,121 +679,155 @@ __device__ __noinline__ void attn_item(KArg ka, int l, int b, int g, int c) {
     }
     __syncthreads();
     if (flag[0]) {
+        const int C = P.C;
+        float *cM = cst, *cL = cst + C * G, *cW = cst + 2 * C * G, *cT = cst + 3 * C * G;
+        for (int t = threadIdx.x; t < C * G; t += kThreads) {
+            const float *pc = part_bg + (size_t)t * (D + 2);   // t = cc * G + h
+            cM[t] = ld_dev(pc + D);
+            cL[t] = ld_dev(pc + D + 1);
+        }
+        __syncthreads();
+        for (int t = threadIdx.x; t < C * G; t += kThreads) {
+            const int h = t % G;
+            float M = -INFINITY;
+            for (int cc = 0; cc < C; ++cc) M = fmaxf(M, cM[cc * G + h]);
+            cW[t] = (cM[t] == -INFINITY) ? 0.f : expf(cM[t] - M);
+        }
+        __syncthreads();
+        if (threadIdx.x < G) {
+            float lsum = 0.f;
+            for (int cc = 0; cc < C; ++cc)
+                lsum = fmaf(cL[cc * G + threadIdx.x], cW[cc * G + threadIdx.x], lsum);
+            cT[threadIdx.x] = lsum;
+        }
+        __syncthreads();
         for (int t = threadIdx.x; t < G * D; t += kThreads) {
             const int h = t / D, dd = t % D;
-            float M = -INFINITY;
-            for (int cc = 0; cc < P.C; ++cc) M = fmaxf(M, part_bg[((size_t)cc * G + h) * (D + 2) + D]);
-            float lsum = 0.f, num = 0.f;
-            for (int cc = 0; cc < P.C; ++cc) {
-                const float *pc = part_bg + ((size_t)cc * G + h) * (D + 2);
-                const float mc = pc[D];
-                if (mc == -INFINITY) continue;
-                const float w = expf(mc - M);
-                lsum = fmaf(pc[D + 1], w, lsum);
-                num = fmaf(pc[dd], w, num);
+            float num = 0.f;
+            for (int c0 = 0; c0 < C; c0 += 8) {
+                float v[8];
+#pragma unroll
+                for (int i = 0; i < 8; ++i)
+                    v[i] = (c0 + i < C) ? ld_dev(part_bg + ((size_t)(c0 + i) * G + h) * (D + 2) + dd)
+                                        : 0.f;
+#pragma unroll
+                for (int i = 0; i < 8; ++i)
+                    if (c0 + i < C) num = fmaf(v[i], cW[(c0 + i) * G + h], num);
             }
-            P.o[(size_t)b * P.Ap + (size_t)(g * G + h) * D + dd] = num / lsum;
+            st_dev(P.o + (size_t)b * P.Ap + (size_t)(g * G + h) * D + dd, num / cT[h]);
         }
     }
     __syncthreads();
 }
 
 template <int D>
-__device__ __forceinline__ void attn_dispatch_g(KArg ka, int group, int l, int b, int g, int c) {
+__device__ __forceinline__ void attn_dispatch_g(KArg ka, int group, int l, int b, int g, int c,
+                                                int wait) {
     switch (group) {
-        case 1: attn_item<D, 1>(ka, l, b, g, c); break;
-        case 2: attn_item<D, 2>(ka, l, b, g, c); break;
-        case 4: attn_item<D, 4>(ka, l, b, g, c); break;
-        default: attn_item<D, 8>(ka, l, b, g, c); break;
+        case 1: attn_item<D, 1>(ka, l, b, g, c, wait); break;
+        case 2: attn_item<D, 2>(ka, l, b, g, c, wait); break;
+        case 4: attn_item<D, 4>(ka, l, b, g, c, wait); break;
+        default: attn_item<D, 8>(ka, l, b, g, c, wait); break;
     }
 }
 
-__device__ __noinline__ void phase_attn(KArg ka, int l) {
+__device__ __noinline__ void phase_attn(KArg ka, int l, int wait, int arrive) {
     const StepParams P = load_params(ka);
     const int items = P.B * P.nkv * P.C;
+    bool waited = wait < 0;
     for (int it = blockIdx.x; it < items; it += P.nwg) {
         const int c = it % P.C, bg = it / P.C, g = bg % P.nkv, b = bg / P.nkv;
-        if (P.d == 64) attn_dispatch_g<64>(ka, P.group, l, b, g, c);
-        else attn_dispatch_g<128>(ka, P.group, l, b, g, c);
+        if (P.d == 64) attn_dispatch_g<64>(ka, P.group, l, b, g, c, waited ? -1 : wait);
+        else attn_dispatch_g<128>(ka, P.group, l, b, g, c, waited ? -1 : wait);
+        waited = true;
     }
+    if (!waited) bar_wait(P, wait);
+    if (arrive >= 0) bar_arrive(P, arrive);
 }
 
 // O projection + residual: x += Wo o (each row has one owner; no atomics).
-__device__ __noinline__ void phase_oproj(KArg ka, int l) {
+__device__ __noinline__ void phase_oproj(KArg ka, int l, int wait, int arrive) {
     const StepParams P = load_params(ka);
     const Lds S = lds_layout(kl_smem, P);
     int rg0, rg1;
     split_range(P.o_rg, P.nwg, blockIdx.x, rg0, rg1);
-    if (rg0 == rg1) return;
     const uint8_t *Lb = P.arena + (size_t)l * P.layer_stride;
-    for (int b = 0; b < P.B; ++b) {
-        vec_to_lds(P.o + (size_t)b * P.Ap, P.Ap, S.a);
-        float *x = P.x + (size_t)b * P.Hp;
-        gemv_rows(Lb + P.off_o, P.Ap / kTileK, rg0, rg1, S.a, S.red,
-                  [&](int r, float y0, float y1) {
-                      x[r] += y0;
-                      x[r + 1] += y1;
-                  });
-    }
+    gemv_phase(
+        Lb + P.off_o, P.Ap / kTileK, rg0, rg1, P.B, S.a, S.red, P.dummy,
+        [&]() { if (wait >= 0) bar_wait(P, wait); },
+        [&](int b) { stage_vec(P.o + (size_t)b * P.Ap, P.Ap, P.Ap, S.a); },
+        [&](int b, int r, float y0, float y1) {
+            float *x = P.x + (size_t)b * P.Hp;
+            st_dev(x + r, ld_dev(x + r) + y0);
+            st_dev(x + r + 1, ld_dev(x + r + 1) + y1);
+        });
+    if (arrive >= 0) bar_arrive(P, arrive);
 }
 
 // RMSNorm + fused gate/up projection + SwiGLU: m = silu(Wg u) * (Wu u).
 // Packed rows alternate gate i, up i.
-__device__ __noinline__ void phase_gateup(KArg ka, int l) {
+__device__ __noinline__ void phase_gateup(KArg ka, int l, int wait, int arrive) {
     const StepParams P = load_params(ka);
     const Lds S = lds_layout(kl_smem, P);
     int rg0, rg1;
     split_range(P.gu_rg, P.nwg, blockIdx.x, rg0, rg1);
-    if (rg0 == rg1) return;
     const uint8_t *Lb = P.arena + (size_t)l * P.layer_stride;
     const float *gain = reinterpret_cast<const float *>(Lb + P.off_ffn_norm);
-    for (int b = 0; b < P.B; ++b) {
-        rmsnorm_to_lds(P.x + (size_t)b * P.Hp, gain, P.H, P.Hp, P.eps, S.a, S.sm);
-        float *m = P.m + (size_t)b * P.Fp;
-        gemv_rows(Lb + P.off_gu, P.Hp / kTileK, rg0, rg1, S.a, S.red,
-                  [&](int r, float g, float u) { m[r >> 1] = g / (1.0f + expf(-g)) * u; });
-    }
+    gemv_phase(
+        Lb + P.off_gu, P.Hp / kTileK, rg0, rg1, P.B, S.a, S.red, P.dummy,
+        [&]() { if (wait >= 0) bar_wait(P, wait); },
+        [&](int b) { stage_rmsnorm(P.x + (size_t)b * P.Hp, gain, P.H, P.Hp, P.eps, S.a, S.sm); },
+        [&](int b, int r, float gt, float up) {
+            st_dev(P.m + (size_t)b * P.Fp + (r >> 1), gt / (1.0f + expf(-gt)) * up);
+        });
+    if (arrive >= 0) bar_arrive(P, arrive);
 }
 
 // Down projection + residual: x += Wd m.
-__device__ __noinline__ void phase_down(KArg ka, int l) {
+__device__ __noinline__ void phase_down(KArg ka, int l, int wait, int arrive) {
     const StepParams P = load_params(ka);
     const Lds S = lds_layout(kl_smem, P);
     int rg0, rg1;
     split_range(P.down_rg, P.nwg, blockIdx.x, rg0, rg1);
-    if (rg0 == rg1) return;
     const uint8_t *Lb = P.arena + (size_t)l * P.layer_stride;
-    for (int b = 0; b < P.B; ++b) {
-        vec_to_lds(P.m + (size_t)b * P.Fp, P.Fp, S.a);
-        float *x = P.x + (size_t)b * P.Hp;
-        gemv_rows(Lb + P.off_down, P.Fp / kTileK, rg0, rg1, S.a, S.red,
-                  [&](int r, float y0, float y1) {
-                      x[r] += y0;
-                      x[r + 1] += y1;
-                  });
-    }
+    gemv_phase(
+        Lb + P.off_down, P.Fp / kTileK, rg0, rg1, P.B, S.a, S.red, P.dummy,
+        [&]() { if (wait >= 0) bar_wait(P, wait); },
+        [&](int b) { stage_vec(P.m + (size_t)b * P.Fp, P.Fp, P.Fp, S.a); },
+        [&](int b, int r, float y0, float y1) {
+            float *x = P.x + (size_t)b * P.Hp;
+            st_dev(x + r, ld_dev(x + r) + y0);
+            st_dev(x + r + 1, ld_dev(x + r + 1) + y1);
+        });
+    if (arrive >= 0) bar_arrive(P, arrive);
 }
 
 // Classifier block (Sec. 2): final RMSNorm + LM head -> fp32 logits.
-__device__ __noinline__ void phase_head(KArg ka) {
+__device__ __noinline__ void phase_head(KArg ka, int wait, int arrive) {
     const StepParams P = load_params(ka);
     const Lds S = lds_layout(kl_smem, P);
-    if (blockIdx.x == 0 && P.hidden_out) {
-        for (int idx = threadIdx.x; idx < P.B * P.H; idx += kThreads)
-            P.hidden_out[idx] = P.x[(size_t)(idx / P.H) * P.Hp + idx % P.H];
-    }
     int rg0, rg1;
     split_range(P.head_rg, P.nwg, blockIdx.x, rg0, rg1);
-    if (rg0 == rg1) return;
-    for (int b = 0; b < P.B; ++b) {
-        rmsnorm_to_lds(P.x + (size_t)b * P.Hp, P.final_norm, P.H, P.Hp, P.eps, S.a, S.sm);
-        float *lg = P.logits + (size_t)b * P.V;
-        const int V = P.V;
-        gemv_rows(reinterpret_cast<const uint8_t *>(P.lm_head), P.Hp / kTileK, rg0, rg1, S.a, S.red, [&](int r, float y0, float y1) {
+    const int V = P.V;
+    gemv_phase(
+        reinterpret_cast<const uint8_t *>(P.lm_head), P.Hp / kTileK, rg0, rg1, P.B, S.a, S.red,
+        P.dummy,
+        [&]() {
+            if (wait >= 0) bar_wait(P, wait);
+            if (blockIdx.x == 0 && P.hidden_out) {
+                for (int idx = threadIdx.x; idx < P.B * P.H; idx += kThreads)
+                    P.hidden_out[idx] = ld_dev(P.x + (size_t)(idx / P.H) * P.Hp + idx % P.H);
+            }
+        },
+        [&](int b) {
+            stage_rmsnorm(P.x + (size_t)b * P.Hp, P.final_norm, P.H, P.Hp, P.eps, S.a, S.sm);
+        },
+        [&](int b, int r, float y0, float y1) {
+            float *lg = P.logits + (size_t)b * V;
             if (r < V) lg[r] = y0;
             if (r + 1 < V) lg[r + 1] = y1;
         });
-    }
+    if (arrive >= 0) bar_arrive(P, arrive);
 }
 
 // ---------------------------------------------------------------- kernels
@@ -680,20 +835,22 @@ __device__ __noinline__ void phase_head(KArg ka) {
 __global__ __launch_bounds__(kThreads) void kl_step_kernel(StepParams P, int l0, int l1,
                                                           int phases) {
     const KArg ka = kernarg_address();
-    bool started = false;
-    auto next = [&]() {
-        if (started) grid_sync(P);
-        started = true;
-    };
-    if (phases & kPhEmbed) { next(); phase_embed(ka); }
+    const int per_layer = __builtin_popcount(phases & kPhLayer);
+    const int total = ((phases & kPhEmbed) ? 1 : 0) + (l1 - l0) * per_layer +
+                      ((phases & kPhHead) ? 1 : 0);
+    if (total > 1) bar_init(P);
+    int i = 0;   // index of the phase within this launch: waits on i - 1, arrives on i
+    auto wt = [&]() { return i - 1; };
+    auto ar = [&]() { return i + 1 < total ? i : -1; };
+    if (phases & kPhEmbed) { phase_embed(ka, wt(), ar()); ++i; }
     for (int l = l0; l < l1; ++l) {
-        if (phases & kPhQkv) { next(); phase_qkv(ka, l); }
-        if (phases & kPhAttn) { next(); phase_attn(ka, l); }
-        if (phases & kPhOproj) { next(); phase_oproj(ka, l); }
-        if (phases & kPhGateUp) { next(); phase_gateup(ka, l); }
-        if (phases & kPhDown) { next(); phase_down(ka, l); }
+        if (phases & kPhQkv) { phase_qkv(ka, l, wt(), ar()); ++i; }
+        if (phases & kPhAttn) { phase_attn(ka, l, wt(), ar()); ++i; }
+        if (phases & kPhOproj) { phase_oproj(ka, l, wt(), ar()); ++i; }
+        if (phases & kPhGateUp) { phase_gateup(ka, l, wt(), ar()); ++i; }
+        if (phases & kPhDown) { phase_down(ka, l, wt(), ar()); ++i; }
     }
-    if (phases & kPhHead) { next(); phase_head(ka); }
+    if (phases & kPhHead) { phase_head(ka, wt(), ar()); ++i; }
 }
 
 // Repack row-major bf16 matrices into 8x64 tiles.  rowmap[packed row] =

@@ -29,8 +29,10 @@ struct kl_state {
     uint8_t *scratch;
     size_t scratch_bytes;
     float *x, *q, *o, *m, *part;
-    unsigned *bar, *cnt;
+    unsigned long long *bar;
+    unsigned *cnt;
     int *err;
+    uint8_t *dummy;
     int nwg, lds_bytes;
 };
 
@@ -118,7 +120,9 @@ int lds_bytes_for(const kl_state &s) {
     const kl_config &c = s.cfg;
     const int g = c.n_heads / c.n_kv_heads;
     int amax = std::max(std::max(s.Hp, s.Ap), s.Fp);
-    const int attn = g * c.head_dim + g * kAttnSub + g * 4 + kWaves * g * c.head_dim;
+    const int cmax = std::max(1, s.nwg / c.n_kv_heads);
+    const int attn = g * c.head_dim + g * kAttnSub + g * 4 + kWaves * g * c.head_dim +
+                     3 * cmax * g + g;
     amax = std::max(amax, attn);
     amax = (amax + 63) & ~63;
     return (amax + kWaves * kRgBatch * kTileRows + 64) * (int)sizeof(float);
@@ -149,7 +153,7 @@ StepParams base_params(const kl_state &s) {
     P.lm_head = reinterpret_cast<const uint16_t *>(s.arena + s.off_lm_head);
     P.rope = s.rope;
     P.x = s.x; P.q = s.q; P.o = s.o; P.m = s.m; P.part = s.part;
-    P.bar = s.bar; P.cnt = s.cnt; P.err = s.err;
+    P.bar = s.bar; P.cnt = s.cnt; P.err = s.err; P.dummy = s.dummy;
     P.nwg = s.nwg;
     return P;
 }
@@ -238,13 +242,13 @@ kl_status kl_load_model(const kl_config *cfg, const kl_weight_ptrs *w, void *str
     TRY(hipMalloc(&S->arena, S->arena_bytes));
 
     // grid: one persistent workgroup per CU
+    S->nwg = ncu;
     S->lds_bytes = lds_bytes_for(*S);
-    if (S->lds_bytes > 160 * 1024)
+    if (S->lds_bytes > 160 * 1024 - 256)
         return bail(fail(KL_ERR_UNSUPPORTED, "LDS need %d bytes exceeds 160 KiB", S->lds_bytes));
     int per_cu = 0;
     TRY(step_kernel_setup(S->lds_bytes, &per_cu));
     if (per_cu < 1) return bail(fail(KL_ERR_UNSUPPORTED, "step kernel does not fit on a CU"));
-    S->nwg = ncu;
 
     // scratch
     const int B = c.max_batch, nkv = c.n_kv_heads;
@@ -258,9 +262,10 @@ kl_status kl_load_model(const kl_config *cfg, const kl_weight_ptrs *w, void *str
     const size_t off_p = so;
     so = align_up(so + std::max(part_items, (size_t)nkv * Cmax) * g * (d + 2) * 4, 256);
     (void)Cmax;
-    const size_t off_bar = so;  so = align_up(so + 1024, 256);
+    const size_t off_bar = so;  so = align_up(so + kBarBytes, 256);
     const size_t off_cnt = so;  so = align_up(so + (size_t)B * nkv * 4, 256);
     const size_t off_err = so;  so = align_up(so + 256, 256);
+    const size_t off_dummy = so; so = align_up(so + kTileBytes, 256);
     S->scratch_bytes = so;
     TRY(hipMalloc(&S->scratch, S->scratch_bytes));
     TRY(hipMemsetAsync(S->scratch, 0, S->scratch_bytes, s));
@@ -269,9 +274,10 @@ kl_status kl_load_model(const kl_config *cfg, const kl_weight_ptrs *w, void *str
     S->o = reinterpret_cast<float *>(S->scratch + off_o);
     S->m = reinterpret_cast<float *>(S->scratch + off_m);
     S->part = reinterpret_cast<float *>(S->scratch + off_p);
-    S->bar = reinterpret_cast<unsigned *>(S->scratch + off_bar);
+    S->bar = reinterpret_cast<unsigned long long *>(S->scratch + off_bar);
     S->cnt = reinterpret_cast<unsigned *>(S->scratch + off_cnt);
     S->err = reinterpret_cast<int *>(S->scratch + off_err);
+    S->dummy = S->scratch + off_dummy;
 
     // RoPE table (cos, sin) of pos * theta^(-2i/d), computed in double
     {
@@ -414,7 +420,7 @@ kl_status kl_get_device_error(kl_state *st, int32_t *code) {
     HIP_TRY(hipMemset(st->err, 0, sizeof(int32_t)));
     if (v & KL_DEVERR_BARRIER) {
         // a timed-out barrier leaves its counters mid-count: start them afresh
-        HIP_TRY(hipMemset(st->bar, 0, 1024));
+        HIP_TRY(hipMemset(st->bar, 0, kBarBytes));
         HIP_TRY(hipMemset(st->cnt, 0, (size_t)st->cfg.max_batch * st->cfg.n_kv_heads * 4));
     }
     return fail(KL_ERR_DEVICE_FAULT, "device error word 0x%x", v);

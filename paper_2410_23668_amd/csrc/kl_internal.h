@@ -14,9 +14,11 @@ constexpr int kThreads = kWaves * 64;     // threads per workgroup
 constexpr int kTileRows = 8;              // rows of one packed weight tile
 constexpr int kTileK = 64;                // columns of one packed weight tile
 constexpr int kTileBytes = kTileRows * kTileK * 2;   // 1 KiB: one 16-byte load per lane
-constexpr int kRgBatch = 16;              // row groups reduced per LDS round
+constexpr int kRgBatch = 64;              // row groups reduced per LDS round
 constexpr int kAttnSub = 256;             // positions per attention sub-chunk
 constexpr int kMaxGroup = 8;              // max query heads per KV head
+constexpr int kBarGroups = 16;            // first level of the grid barrier
+constexpr int kBarBytes = 8192;           // barrier counters: root + kBarGroups lines of 256 B
 
 // Phase selection bits of one launch of the step kernel.
 enum : int {
@@ -53,9 +55,10 @@ struct StepParams {
     float *o;                  // [max_batch][Ap]   attention output (padding stays 0)
     float *m;                  // [max_batch][Fp]   SwiGLU output (padding stays 0)
     float *part;               // attention partials [max_batch*nkv*C][group][d+2]
-    unsigned *bar;             // grid barrier: [0] arrivals, [64] generation
+    unsigned long long *bar;   // grid barrier counters (monotonic): root at [0], group g at [32 (g + 1)]
     unsigned *cnt;             // [max_batch*nkv] attention chunk arrivals
     int *err;                  // device error word
+    const uint8_t *dummy;      // 16 readable bytes: target of the GEMV ring's spare loads
     int nwg;                   // grid size; the work partition depends only on it
     int C;                     // attention chunks per (sequence, KV head)
 };
