@@ -30,7 +30,7 @@ KL_DEVERR_POSITION = 2
 KL_DEVERR_BARRIER = 4
 
 EXPORTED = ["kl_load_model", "kl_decode_step", "kl_kv_cache_bytes", "kl_get_device_error",
-            "kl_get_info", "kl_free_model", "kl_last_error"]
+            "kl_get_info", "kl_set_trace", "kl_free_model", "kl_last_error"]
 
 
 class kl_config(ctypes.Structure):
@@ -95,6 +95,8 @@ def lib():
     L.kl_get_device_error.restype = i32
     L.kl_get_info.argtypes = [vp, ctypes.POINTER(kl_info)]
     L.kl_get_info.restype = i32
+    L.kl_set_trace.argtypes = [vp, vp, i32]
+    L.kl_set_trace.restype = i32
     L.kl_free_model.argtypes = [vp]
     L.kl_free_model.restype = None
     L.kl_last_error.argtypes = []
@@ -157,6 +159,10 @@ def kl_get_info(state: int) -> kl_info:
     info = kl_info()
     _check(lib().kl_get_info(state, ctypes.byref(info)))
     return info
+
+
+def kl_set_trace(state: int, dev_buffer: int | None, max_barriers: int) -> None:
+    _check(lib().kl_set_trace(state, dev_buffer, max_barriers))
 
 
 def kl_free_model(state: int) -> None:

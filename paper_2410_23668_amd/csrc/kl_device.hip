@@ -182,7 +182,15 @@ __device__ void bar_init(const StepParams &P) {
     __syncthreads();
 }
 
+// Optional timeline: thread 0 of every workgroup stamps (s_memrealtime, 100 MHz)
+// its arrival at barrier k, the start of its wait on k and the end of that wait.
+__device__ __forceinline__ void trace_stamp(const StepParams &P, int k, int what) {
+    if (P.trace && k < P.trace_max)
+        P.trace[((size_t)k * P.nwg + blockIdx.x) * 4 + what] = wall_clock64();
+}
+
 __device__ __forceinline__ void bar_arrive(const StepParams &P, int k) {
+    if (threadIdx.x == 0) trace_stamp(P, k, 0);
     wait_stores();
     __syncthreads();
     if (threadIdx.x == 0) {
@@ -200,6 +208,7 @@ __device__ __forceinline__ void bar_wait(const StepParams &P, int k) {
     if (threadIdx.x == 0) {
         const int ng = min(kBarGroups, P.nwg);
         const unsigned long long target = kl_bar_base[0] + (unsigned long long)(k + 1) * ng;
+        trace_stamp(P, k, 1);
         const long long t0 = wall_clock64();
         while ((long long)(ld_dev_u64(P.bar) - target) < 0) {
             if (__hip_atomic_load(P.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) &
@@ -211,6 +220,7 @@ __device__ __forceinline__ void bar_wait(const StepParams &P, int k) {
                 break;
             }
         }
+        trace_stamp(P, k, 2);
     }
     __syncthreads();
 }
@@ -264,7 +274,7 @@ __device__ __forceinline__ Lds lds_layout(char *smem, const StepParams &P) {
     Lds s;
     int amax = max(max(P.Hp, P.Ap), P.Fp);
     const int attn = P.group * P.d + P.group * kAttnSub + P.group * 4 + kWaves * P.group * P.d +
-                     3 * attn_cmax(P) * P.group + P.group;
+                     3 * attn_cmax(P) * P.group + P.group + P.group * P.d + attn_cmax(P);
     amax = max(amax, attn);
     amax = (amax + 63) & ~63;
     s.a = reinterpret_cast<float *>(smem);
@@ -439,6 +449,10 @@ __device__ __noinline__ void phase_embed(KArg ka, int wait, int arrive) {
             if (bits) atomicOr(P.err, bits);
         }
     }
+    if (blockIdx.x == 0) {
+        for (int i = threadIdx.x; i < P.B * P.nkv; i += kThreads)
+            __hip_atomic_store(P.cnt + i, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
     const int total = P.B * P.Hp;
     for (int idx = blockIdx.x * kThreads + threadIdx.x; idx < total; idx += P.nwg * kThreads) {
         const int b = idx / P.Hp, i = idx % P.Hp;
@@ -511,7 +525,7 @@ __device__ __noinline__ void attn_item(KArg ka, int l, int b, int g, int c, int 
     float *sp = qs + G * D;             // [G][kAttnSub]
     float *st = sp + G * kAttnSub;      // [G][4]
     float *red = st + G * 4;            // [kWaves][G][D]
-    float *cst = red + kWaves * G * D;  // combine: [3][Cmax][G] + [G]
+    float *cst = red + kWaves * G * D;  // combine: [3][Cmax][G] + [G] + [Cmax][nout]
     const size_t row0 = kv_row(P, l, b, g);
     const uint16_t *Kb = P.kc + row0 * D;
     const uint16_t *Vb = P.vc + row0 * D;
@@ -665,57 +679,86 @@ __device__ __noinline__ void attn_item(KArg ka, int l, int b, int g, int c, int 
         st_dev(out + threadIdx.x * (D + 2) + D, st[threadIdx.x * 4 + 0]);
         st_dev(out + threadIdx.x * (D + 2) + D + 1, st[threadIdx.x * 4 + 1]);
     }
-    // publish this chunk; the last arrival for (b, g) combines
+    // Publish this chunk, then combine: once all C chunks of (b, g) are in,
+    // each of the C workgroups finalises its own slice of the G*D outputs,
+    // reading every chunk's statistics and its slice of their outputs (all
+    // loads in one round trip) and merging them in chunk order.  The per-(b, g)
+    // counter is zeroed by the embedding phase and grows by C per layer.
+    if (threadIdx.x == 0 && wait >= 0) trace_stamp(P, wait + 1, 3);
     wait_stores();
     __syncthreads();
-    int *flag = reinterpret_cast<int *>(S.sm);
+    const int C = P.C;
     if (threadIdx.x == 0) {
         unsigned *cnt = P.cnt + b * P.nkv + g;
-        const unsigned old = __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED,
-                                                    __HIP_MEMORY_SCOPE_AGENT);
-        const int last = old == (unsigned)(P.C - 1);
-        if (last) __hip_atomic_store(cnt, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        flag[0] = last;
+        __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const unsigned target = (unsigned)(l + 1) * (unsigned)C;
+        const long long t0 = wall_clock64();
+        while ((int)(__hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) - target) < 0) {
+            if (__hip_atomic_load(P.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) &
+                KL_DEVERR_BARRIER)
+                break;
+            if (wall_clock64() - t0 > kBarrierTicks) {
+                __hip_atomic_fetch_or(P.err, KL_DEVERR_BARRIER, __ATOMIC_RELAXED,
+                                      __HIP_MEMORY_SCOPE_AGENT);
+                break;
+            }
+        }
     }
     __syncthreads();
-    if (flag[0]) {
-        const int C = P.C;
-        float *cM = cst, *cL = cst + C * G, *cW = cst + 2 * C * G, *cT = cst + 3 * C * G;
-        for (int t = threadIdx.x; t < C * G; t += kThreads) {
-            const float *pc = part_bg + (size_t)t * (D + 2);   // t = cc * G + h
-            cM[t] = ld_dev(pc + D);
-            cL[t] = ld_dev(pc + D + 1);
-        }
-        __syncthreads();
-        for (int t = threadIdx.x; t < C * G; t += kThreads) {
-            const int h = t % G;
-            float M = -INFINITY;
-            for (int cc = 0; cc < C; ++cc) M = fmaxf(M, cM[cc * G + h]);
-            cW[t] = (cM[t] == -INFINITY) ? 0.f : expf(cM[t] - M);
-        }
-        __syncthreads();
-        if (threadIdx.x < G) {
-            float lsum = 0.f;
-            for (int cc = 0; cc < C; ++cc)
-                lsum = fmaf(cL[cc * G + threadIdx.x], cW[cc * G + threadIdx.x], lsum);
-            cT[threadIdx.x] = lsum;
-        }
-        __syncthreads();
-        for (int t = threadIdx.x; t < G * D; t += kThreads) {
-            const int h = t / D, dd = t % D;
-            float num = 0.f;
-            for (int c0 = 0; c0 < C; c0 += 8) {
-                float v[8];
+    const int nout = (G * D + C - 1) / C;              // outputs finalised per chunk
+    const int o0 = c * nout, o1 = min(G * D, o0 + nout);
+    const int no = max(0, o1 - o0);
+    float *cM = cst, *cL = cst + C * G, *cW = cst + 2 * C * G, *cT = cst + 3 * C * G;
+    float *cA = cT + G;                                // [C][nout]
+    // gather: up to 4 loads per thread issued together, then stored to LDS
+    const int ngather = C * G + C * no;
+    for (int t0 = 0; t0 < ngather; t0 += 4 * kThreads) {
+        float v0[4], v1[4];
 #pragma unroll
-                for (int i = 0; i < 8; ++i)
-                    v[i] = (c0 + i < C) ? ld_dev(part_bg + ((size_t)(c0 + i) * G + h) * (D + 2) + dd)
-                                        : 0.f;
-#pragma unroll
-                for (int i = 0; i < 8; ++i)
-                    if (c0 + i < C) num = fmaf(v[i], cW[(c0 + i) * G + h], num);
+        for (int k = 0; k < 4; ++k) {
+            const int t = t0 + k * kThreads + threadIdx.x;
+            v0[k] = v1[k] = 0.f;
+            if (t < C * G) {
+                const float *pc = part_bg + (size_t)t * (D + 2);   // t = cc * G + h
+                v0[k] = ld_dev(pc + D);
+                v1[k] = ld_dev(pc + D + 1);
+            } else if (t < ngather) {
+                const int u = t - C * G, cc = u / no, j = o0 + u % no;
+                v0[k] = ld_dev(part_bg + ((size_t)cc * G + j / D) * (D + 2) + j % D);
             }
-            st_dev(P.o + (size_t)b * P.Ap + (size_t)(g * G + h) * D + dd, num / cT[h]);
         }
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int t = t0 + k * kThreads + threadIdx.x;
+            if (t < C * G) {
+                cM[t] = v0[k];
+                cL[t] = v1[k];
+            } else if (t < ngather) {
+                const int u = t - C * G;
+                cA[(u / no) * nout + u % no] = v0[k];
+            }
+        }
+    }
+    __syncthreads();
+    for (int t = threadIdx.x; t < C * G; t += kThreads) {
+        const int h = t % G;
+        float M = -INFINITY;
+        for (int cc = 0; cc < C; ++cc) M = fmaxf(M, cM[cc * G + h]);
+        cW[t] = (cM[t] == -INFINITY) ? 0.f : expf(cM[t] - M);
+    }
+    __syncthreads();
+    if (threadIdx.x < G) {
+        float lsum = 0.f;
+        for (int cc = 0; cc < C; ++cc)
+            lsum = fmaf(cL[cc * G + threadIdx.x], cW[cc * G + threadIdx.x], lsum);
+        cT[threadIdx.x] = lsum;
+    }
+    __syncthreads();
+    for (int t = threadIdx.x; t < no; t += kThreads) {
+        const int j = o0 + t, h = j / D;
+        float num = 0.f;
+        for (int cc = 0; cc < C; ++cc) num = fmaf(cA[cc * nout + t], cW[cc * G + h], num);
+        st_dev(P.o + (size_t)b * P.Ap + (size_t)g * G * D + j, num / cT[h]);
     }
     __syncthreads();
 }

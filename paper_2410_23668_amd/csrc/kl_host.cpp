@@ -33,6 +33,8 @@ struct kl_state {
     unsigned *cnt;
     int *err;
     uint8_t *dummy;
+    unsigned long long *trace;
+    int trace_max;
     int nwg, lds_bytes;
 };
 
@@ -122,7 +124,7 @@ int lds_bytes_for(const kl_state &s) {
     int amax = std::max(std::max(s.Hp, s.Ap), s.Fp);
     const int cmax = std::max(1, s.nwg / c.n_kv_heads);
     const int attn = g * c.head_dim + g * kAttnSub + g * 4 + kWaves * g * c.head_dim +
-                     3 * cmax * g + g;
+                     3 * cmax * g + g + g * c.head_dim + cmax;
     amax = std::max(amax, attn);
     amax = (amax + 63) & ~63;
     return (amax + kWaves * kRgBatch * kTileRows + 64) * (int)sizeof(float);
@@ -155,6 +157,8 @@ StepParams base_params(const kl_state &s) {
     P.x = s.x; P.q = s.q; P.o = s.o; P.m = s.m; P.part = s.part;
     P.bar = s.bar; P.cnt = s.cnt; P.err = s.err; P.dummy = s.dummy;
     P.nwg = s.nwg;
+    P.trace = s.trace;
+    P.trace_max = s.trace_max;
     return P;
 }
 
@@ -424,6 +428,16 @@ kl_status kl_get_device_error(kl_state *st, int32_t *code) {
         HIP_TRY(hipMemset(st->cnt, 0, (size_t)st->cfg.max_batch * st->cfg.n_kv_heads * 4));
     }
     return fail(KL_ERR_DEVICE_FAULT, "device error word 0x%x", v);
+}
+
+kl_status kl_set_trace(kl_state *st, uint64_t *dev_buffer, int32_t max_barriers) {
+    g_last_error.clear();
+    if (!st) return fail(KL_ERR_INVALID_ARGUMENT, "state is NULL");
+    if (dev_buffer && (max_barriers < 1 || !aligned(dev_buffer, 8)))
+        return fail(KL_ERR_INVALID_ARGUMENT, "trace buffer needs max_barriers >= 1, 8-byte alignment");
+    st->trace = reinterpret_cast<unsigned long long *>(dev_buffer);
+    st->trace_max = dev_buffer ? max_barriers : 0;
+    return KL_OK;
 }
 
 kl_status kl_get_info(const kl_state *st, kl_info *info) {

@@ -61,6 +61,8 @@ struct StepParams {
     const uint8_t *dummy;      // 16 readable bytes: target of the GEMV ring's spare loads
     int nwg;                   // grid size; the work partition depends only on it
     int C;                     // attention chunks per (sequence, KV head)
+    unsigned long long *trace; // optional barrier timestamps (see kl_set_trace), or null
+    int trace_max;             // barriers recorded per launch
 };
 
 hipError_t launch_step(const StepParams &p, int first_layer, int last_layer, int phases,
