@@ -148,36 +148,46 @@ __device__ __forceinline__ void wait_stores() { __builtin_amdgcn_s_waitcnt(0x0F7
 
 // ---------------------------------------------------------------- grid barrier
 //
-// Two-level arrival counting on monotonically increasing 64-bit counters:
-// workgroup w arrives on group counter w % ng; the last arrival of a group
-// bumps the root counter; waiters poll the root for its target value.  The
-// counters are never reset: at launch start each workgroup rounds the
-// current values down to whole barriers (every launch ends with all
-// counters at a multiple of their group size, and no group can complete the
-// first barrier before every member has read its base).  Barrier k of a
-// launch is complete when root reaches base + (k + 1) * ng.  The wait is
-// bounded: after ~2 s it raises KL_DEVERR_BARRIER and every later wait
-// returns at once, so a broken barrier ends the kernel instead of hanging it.
-constexpr long long kBarrierTicks = 200000000LL;   // s_memrealtime runs at 100 MHz
+// Arrival counting on monotonically increasing 64-bit counters, one per
+// group of workgroups: workgroup w arrives on counter w % ng (one atomic
+// add), and a waiter's wave 0 polls all ng counters at once, one per lane.
+// Spreading arrivals over ng counters keeps the atomics on any one address
+// few; polling them directly saves a second atomic hop.  The counters are
+// never reset: every launch ends with counter g at E * size_g, E being the
+// number of barriers completed so far, and at launch start each workgroup
+// recovers E from its own group's counter.  Barrier k of a launch is complete
+// when counter g reaches base_g + (k + 1) * size_g for every group g.  The
+// wait is bounded by a poll count: past it, KL_DEVERR_BARRIER is raised and every
+// later wait returns at once, so a broken barrier ends the kernel instead of
+// hanging it.
+constexpr int kSpinLimit = 1 << 22;   // polls before a wait gives up (well over a second)
 
-__shared__ unsigned long long kl_bar_base[2];      // root base, group base (this launch)
+// The per-group bases of the current launch live in the dynamic LDS area (a
+// fixed slot after everything else; see lds_layout), which every phase
+// function addresses the same way.
+extern __shared__ __align__(16) char kl_smem[];
+__device__ __forceinline__ unsigned long long *bar_bases(const StepParams &P);
 
-__device__ __forceinline__ void bar_geometry(const StepParams &P, int &ng, int &g,
-                                             unsigned &gsize) {
-    ng = min(kBarGroups, P.nwg);
-    g = blockIdx.x % ng;
-    gsize = (unsigned)(P.nwg / ng + (g < P.nwg % ng ? 1 : 0));
+__device__ __forceinline__ int bar_groups(const StepParams &P) { return min(kBarGroups, P.nwg); }
+__device__ __forceinline__ unsigned bar_gsize(const StepParams &P, int ng, int g) {
+    return (unsigned)(P.nwg / ng + (g < P.nwg % ng ? 1 : 0));
+}
+__device__ __forceinline__ unsigned long long *bar_counter(const StepParams &P, int g) {
+    return P.bar + 32 * (g + 1);   // 256 bytes apart
 }
 
 __device__ void bar_init(const StepParams &P) {
-    if (threadIdx.x == 0) {
-        int ng, g;
-        unsigned gsize;
-        bar_geometry(P, ng, g, gsize);
-        const unsigned long long r = ld_dev_u64(P.bar);
-        const unsigned long long c = ld_dev_u64(P.bar + 32 * (g + 1));
-        kl_bar_base[0] = r - r % (unsigned long long)ng;
-        kl_bar_base[1] = c - c % gsize;
+    // Only this workgroup's own group counter is read: that group cannot
+    // complete barrier 0 before this workgroup arrives, so the value rounds
+    // down to the number E of whole barriers done by earlier launches.  Any
+    // other group may already be one barrier further, so its base is E times
+    // its size, not its current value rounded down.
+    const int ng = bar_groups(P);
+    if (threadIdx.x < ng) {
+        const int own = blockIdx.x % ng;
+        const unsigned long long c = ld_dev_u64(bar_counter(P, own));
+        const unsigned long long epoch = c / bar_gsize(P, ng, own);
+        bar_bases(P)[threadIdx.x] = epoch * bar_gsize(P, ng, threadIdx.x);
     }
     __syncthreads();
 }
@@ -193,34 +203,33 @@ __device__ __forceinline__ void bar_arrive(const StepParams &P, int k) {
     if (threadIdx.x == 0) trace_stamp(P, k, 0);
     wait_stores();
     __syncthreads();
-    if (threadIdx.x == 0) {
-        int ng, g;
-        unsigned gsize;
-        bar_geometry(P, ng, g, gsize);
-        const unsigned long long old = __hip_atomic_fetch_add(
-            P.bar + 32 * (g + 1), 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (old == kl_bar_base[1] + (unsigned long long)(k + 1) * gsize - 1ull)
-            __hip_atomic_fetch_add(P.bar, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
+    if (threadIdx.x == 0)
+        __hip_atomic_fetch_add(bar_counter(P, blockIdx.x % bar_groups(P)), 1ull,
+                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 __device__ __forceinline__ void bar_wait(const StepParams &P, int k) {
-    if (threadIdx.x == 0) {
-        const int ng = min(kBarGroups, P.nwg);
-        const unsigned long long target = kl_bar_base[0] + (unsigned long long)(k + 1) * ng;
-        trace_stamp(P, k, 1);
-        const long long t0 = wall_clock64();
-        while ((long long)(ld_dev_u64(P.bar) - target) < 0) {
+    if (threadIdx.x < 64) {
+        const int lane = threadIdx.x, ng = bar_groups(P);
+        const bool mine = lane < ng;
+        const unsigned long long target =
+            mine ? bar_bases(P)[lane] + (unsigned long long)(k + 1) * bar_gsize(P, ng, lane) : 0ull;
+        if (lane == 0) trace_stamp(P, k, 1);
+        for (int spins = 0;; ++spins) {
+            const bool done =
+                !mine || (long long)(ld_dev_u64(bar_counter(P, lane)) - target) >= 0;
+            if (__all(done)) break;
             if (__hip_atomic_load(P.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) &
                 KL_DEVERR_BARRIER)
                 break;
-            if (wall_clock64() - t0 > kBarrierTicks) {
-                __hip_atomic_fetch_or(P.err, KL_DEVERR_BARRIER, __ATOMIC_RELAXED,
-                                      __HIP_MEMORY_SCOPE_AGENT);
+            if (spins >= kSpinLimit) {
+                if (lane == 0)
+                    __hip_atomic_fetch_or(P.err, KL_DEVERR_BARRIER, __ATOMIC_RELAXED,
+                                          __HIP_MEMORY_SCOPE_AGENT);
                 break;
             }
         }
-        trace_stamp(P, k, 2);
+        if (lane == 0) trace_stamp(P, k, 2);
     }
     __syncthreads();
 }
@@ -258,14 +267,13 @@ __device__ __forceinline__ StepParams load_params(KArg ka) {
 #endif
 }
 
-extern __shared__ __align__(16) char kl_smem[];
-
 // ---------------------------------------------------------------- LDS layout
 
 struct Lds {
     float *a;     // activation vector (max K extent), or the attention area
     float *red;   // [kWaves][kRgBatch][kTileRows] GEMV partial sums
-    float *sm;    // small reductions and flags
+    float *sm;    // small reductions and flags (64 floats)
+    unsigned long long *bar;   // [kBarGroups] barrier bases of this launch
 };
 
 __device__ __forceinline__ int attn_cmax(const StepParams &P) { return max(1, P.nwg / P.nkv); }
@@ -280,7 +288,12 @@ __device__ __forceinline__ Lds lds_layout(char *smem, const StepParams &P) {
     s.a = reinterpret_cast<float *>(smem);
     s.red = s.a + amax;
     s.sm = s.red + kWaves * kRgBatch * kTileRows;
+    s.bar = reinterpret_cast<unsigned long long *>(s.sm + 64);
     return s;
+}
+
+__device__ __forceinline__ unsigned long long *bar_bases(const StepParams &P) {
+    return lds_layout(kl_smem, P).bar;
 }
 
 // ---------------------------------------------------------------- activations
@@ -692,12 +705,13 @@ __device__ __noinline__ void attn_item(KArg ka, int l, int b, int g, int c, int 
         unsigned *cnt = P.cnt + b * P.nkv + g;
         __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         const unsigned target = (unsigned)(l + 1) * (unsigned)C;
-        const long long t0 = wall_clock64();
-        while ((int)(__hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) - target) < 0) {
+        for (int spins = 0;
+             (int)(__hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) - target) < 0;
+             ++spins) {
             if (__hip_atomic_load(P.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) &
                 KL_DEVERR_BARRIER)
                 break;
-            if (wall_clock64() - t0 > kBarrierTicks) {
+            if (spins >= kSpinLimit) {
                 __hip_atomic_fetch_or(P.err, KL_DEVERR_BARRIER, __ATOMIC_RELAXED,
                                       __HIP_MEMORY_SCOPE_AGENT);
                 break;

@@ -127,7 +127,8 @@ int lds_bytes_for(const kl_state &s) {
                      3 * cmax * g + g + g * c.head_dim + cmax;
     amax = std::max(amax, attn);
     amax = (amax + 63) & ~63;
-    return (amax + kWaves * kRgBatch * kTileRows + 64) * (int)sizeof(float);
+    return (amax + kWaves * kRgBatch * kTileRows + 64) * (int)sizeof(float) +
+           kBarGroups * (int)sizeof(unsigned long long);
 }
 
 void free_state(kl_state *s) {

@@ -14,11 +14,11 @@ constexpr int kThreads = kWaves * 64;     // threads per workgroup
 constexpr int kTileRows = 8;              // rows of one packed weight tile
 constexpr int kTileK = 64;                // columns of one packed weight tile
 constexpr int kTileBytes = kTileRows * kTileK * 2;   // 1 KiB: one 16-byte load per lane
-constexpr int kRgBatch = 64;              // row groups reduced per LDS round
+constexpr int kRgBatch = 16;              // row groups reduced per LDS round
 constexpr int kAttnSub = 256;             // positions per attention sub-chunk
 constexpr int kMaxGroup = 8;              // max query heads per KV head
 constexpr int kBarGroups = 16;            // first level of the grid barrier
-constexpr int kBarBytes = 8192;           // barrier counters: root + kBarGroups lines of 256 B
+constexpr int kBarBytes = 8192;           // barrier counters: kBarGroups lines of 256 B
 
 // Phase selection bits of one launch of the step kernel.
 enum : int {
@@ -55,7 +55,7 @@ struct StepParams {
     float *o;                  // [max_batch][Ap]   attention output (padding stays 0)
     float *m;                  // [max_batch][Fp]   SwiGLU output (padding stays 0)
     float *part;               // attention partials [max_batch*nkv*C][group][d+2]
-    unsigned long long *bar;   // grid barrier counters (monotonic): root at [0], group g at [32 (g + 1)]
+    unsigned long long *bar;   // grid barrier counters (monotonic): group g at [32 (g + 1)]
     unsigned *cnt;             // [max_batch*nkv] attention chunk arrivals
     int *err;                  // device error word
     const uint8_t *dummy;      // 16 readable bytes: target of the GEMV ring's spare loads
