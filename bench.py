@@ -24,10 +24,54 @@ sys.path.insert(0, ROOT)
 
 METRIC = "decode tok/s + achieved HBM TB/s vs peak, 8B-shape batch 1 ctx 4096"
 PEAK_HBM_GBS = 8000.0
+# Measured HBM traffic of the step kernel (rocprofv3 FETCH_SIZE / WRITE_SIZE,
+# scaled by a plain copy kernel), with the hash of the device source it was
+# taken on: reported only while that source is unchanged.
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "kl_step_kernel_traffic.md")
+DEVICE_SRC = [os.path.join(ROOT, "paper_2410_23668_amd", "csrc", f)
+              for f in ("kl_device.hip", "kl_internal.h")]
 
 
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def device_source_sha() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in DEVICE_SRC:
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload: str):
+    """Bytes per launch from the committed counter summary, or None when it
+    is missing, for another workload, or taken on other device code."""
+    try:
+        with open(TRAFFIC_FILE) as fh:
+            text = fh.read()
+        t = json.loads(text.split("```json", 1)[1].split("```", 1)[0])
+    except (OSError, ValueError, IndexError):
+        return None
+    w = t.get("workloads", {}).get(workload)
+    if not w or t.get("device_source_sha256") != device_source_sha():
+        return None
+    return w["fetch_bytes"] + w["write_bytes"]
+
+
+def copy_probe(mib: int, reps: int = 3):
+    """Plain copy kernel of known size for scaling the HBM counters: reads and
+    writes mib MiB per launch (torch's elementwise negation, fp32)."""
+    import torch
+    n = mib * (1 << 20) // 4
+    x = torch.ones(n, dtype=torch.float32, device="cuda")
+    y = torch.empty_like(x)
+    for _ in range(reps):
+        torch.neg(x, out=y)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe": {"read_bytes": 4 * n, "write_bytes": 4 * n, "launches": reps,
+                                     "kernel": "torch.neg fp32 (elementwise)"}}), flush=True)
 
 
 def time_mode(model, toks, pos, kv, logits, mode, steps, warmup):
@@ -61,6 +105,8 @@ def main():
     ap.add_argument("--modes", default="looped,per_layer",
                     help="schedules to time; the first is the headline")
     ap.add_argument("--threads", type=int, default=0, help="host threads for input generation")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="only run the copy kernel used to scale HBM counters, then exit")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -68,8 +114,11 @@ def main():
               "(run with --gpus 1)", file=sys.stderr)
         sys.exit(2)
 
-    import numpy as np
     import torch
+    if args.copy_probe_mib:
+        torch.cuda.set_device(0)
+        copy_probe(args.copy_probe_mib)
+        return
 
     import synth
     from paper_2410_23668_amd import binding as kb
@@ -126,7 +175,8 @@ def main():
         "data": "synthetic (seeded N(0,0.02) weights, N(0,1) KV)",
         "config": {"workload": args.workload, "batch": B, "context": P, "mode": head},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                     "frac": achieved / PEAK_HBM_GBS, "traffic": None,
+                     "frac": achieved / PEAK_HBM_GBS,
+                     "traffic": measured_traffic(args.workload) if head == "looped" else None,
                      "algorithmic_bytes_per_launch": nbytes,
                      "kernel": "kl_step_kernel (one launch per step)"},
         "modes": {m: r for m, r in res.items()},
