@@ -88,7 +88,7 @@ __device__ __forceinline__ float block_sum(float v, float *sm) {
     __syncthreads();
     float t = 0.f;
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) t += sm[w];
+    for (int w = 0; w < kThreads / 64; ++w) t += sm[w];
     __syncthreads();
     return t;
 }
@@ -126,6 +126,13 @@ __device__ __forceinline__ void st_dev_u16(uint16_t *p, uint16_t v) {
 }
 __device__ __forceinline__ void st_dev_u32(unsigned *p, unsigned v) {
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// x += v performed at the device-coherent level, without returning the old
+// value (nothing waits for it until the store drain before a barrier
+// arrival).  Each residual element has exactly one adder per phase, so the
+// result is x + v rounded once, independent of timing.
+__device__ __forceinline__ void add_dev(float *p, float v) {
+    __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 __device__ __forceinline__ float ld_dev(const float *p) {
     return __hip_atomic_load(const_cast<float *>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -183,7 +190,7 @@ __device__ void bar_init(const StepParams &P) {
     // other group may already be one barrier further, so its base is E times
     // its size, not its current value rounded down.
     const int ng = bar_groups(P);
-    if (threadIdx.x < ng) {
+    if (threadIdx.x < ng) {   // (before any wait; any wave may do it)
         const int own = blockIdx.x % ng;
         const unsigned long long c = ld_dev_u64(bar_counter(P, own));
         const unsigned long long epoch = c / bar_gsize(P, ng, own);
@@ -199,36 +206,50 @@ __device__ __forceinline__ void trace_stamp(const StepParams &P, int k, int what
         P.trace[((size_t)k * P.nwg + blockIdx.x) * 4 + what] = wall_clock64();
 }
 
+// The control wave (kCtlWave) does all of a workgroup's barrier traffic.  It
+// never has weight or KV loads in flight, so its polls are not queued behind
+// the compute waves' prefetches (a wave's loads complete in issue order).
+__device__ __forceinline__ bool is_ctl_lane0() { return threadIdx.x == kCtlWave * 64; }
+
 __device__ __forceinline__ void bar_arrive(const StepParams &P, int k) {
-    if (threadIdx.x == 0) trace_stamp(P, k, 0);
+    if (is_ctl_lane0()) trace_stamp(P, k, 0);
     wait_stores();
     __syncthreads();
-    if (threadIdx.x == 0)
+    if (is_ctl_lane0())
         __hip_atomic_fetch_add(bar_counter(P, blockIdx.x % bar_groups(P)), 1ull,
                                __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// Spin until *flag_fn() says done; gives up (raising KL_DEVERR_BARRIER) after
+// kSpinLimit polls or as soon as another wait has given up.
+template <class Done>
+__device__ __forceinline__ void spin_until(const StepParams &P, Done &&done) {
+    for (int spins = 1;; ++spins) {
+        if (done()) return;
+        if ((spins & 63) == 0 &&
+            (__hip_atomic_load(P.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) &
+             KL_DEVERR_BARRIER))
+            return;
+        if (spins >= kSpinLimit) {
+            if ((threadIdx.x & 63) == 0)
+                __hip_atomic_fetch_or(P.err, KL_DEVERR_BARRIER, __ATOMIC_RELAXED,
+                                      __HIP_MEMORY_SCOPE_AGENT);
+            return;
+        }
+    }
+}
+
 __device__ __forceinline__ void bar_wait(const StepParams &P, int k) {
-    if (threadIdx.x < 64) {
-        const int lane = threadIdx.x, ng = bar_groups(P);
+    if ((threadIdx.x >> 6) == kCtlWave) {
+        const int lane = threadIdx.x & 63, ng = bar_groups(P);
         const bool mine = lane < ng;
         const unsigned long long target =
             mine ? bar_bases(P)[lane] + (unsigned long long)(k + 1) * bar_gsize(P, ng, lane) : 0ull;
         if (lane == 0) trace_stamp(P, k, 1);
-        for (int spins = 0;; ++spins) {
-            const bool done =
-                !mine || (long long)(ld_dev_u64(bar_counter(P, lane)) - target) >= 0;
-            if (__all(done)) break;
-            if (__hip_atomic_load(P.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) &
-                KL_DEVERR_BARRIER)
-                break;
-            if (spins >= kSpinLimit) {
-                if (lane == 0)
-                    __hip_atomic_fetch_or(P.err, KL_DEVERR_BARRIER, __ATOMIC_RELAXED,
-                                          __HIP_MEMORY_SCOPE_AGENT);
-                break;
-            }
-        }
+        spin_until(P, [&]() {
+            const bool d = !mine || (long long)(ld_dev_u64(bar_counter(P, lane)) - target) >= 0;
+            return __all(d) != 0;
+        });
         if (lane == 0) trace_stamp(P, k, 2);
     }
     __syncthreads();
@@ -269,26 +290,23 @@ __device__ __forceinline__ StepParams load_params(KArg ka) {
 
 // ---------------------------------------------------------------- LDS layout
 
+// Offsets (in floats) come from the host, which sizes the allocation.
 struct Lds {
-    float *a;     // activation vector (max K extent), or the attention area
+    float *a;     // activation vector (max K extent); aliased by the attention area
+    float *attn;  // attention scratch (same storage as a)
     float *red;   // [kWaves][kRgBatch][kTileRows] GEMV partial sums
     float *sm;    // small reductions and flags (64 floats)
     unsigned long long *bar;   // [kBarGroups] barrier bases of this launch
 };
 
-__device__ __forceinline__ int attn_cmax(const StepParams &P) { return max(1, P.nwg / P.nkv); }
-
 __device__ __forceinline__ Lds lds_layout(char *smem, const StepParams &P) {
     Lds s;
-    int amax = max(max(P.Hp, P.Ap), P.Fp);
-    const int attn = P.group * P.d + P.group * kAttnSub + P.group * 4 + kWaves * P.group * P.d +
-                     3 * attn_cmax(P) * P.group + P.group + P.group * P.d + attn_cmax(P);
-    amax = max(amax, attn);
-    amax = (amax + 63) & ~63;
-    s.a = reinterpret_cast<float *>(smem);
-    s.red = s.a + amax;
-    s.sm = s.red + kWaves * kRgBatch * kTileRows;
-    s.bar = reinterpret_cast<unsigned long long *>(s.sm + 64);
+    float *f = reinterpret_cast<float *>(smem);
+    s.a = f;
+    s.attn = f;
+    s.red = f + P.lds_red;
+    s.sm = f + P.lds_sm;
+    s.bar = reinterpret_cast<unsigned long long *>(f + P.lds_bar);
     return s;
 }
 
@@ -329,7 +347,7 @@ __device__ __forceinline__ void stage_rmsnorm(const float *__restrict__ x,
 
 // ---------------------------------------------------------------- GEMV engine
 //
-// y_b[r] = sum_k W[r][k] a_b[k] for the rows of row groups [rg0, rg1) of a
+// y_b[r] = sum_k W[r][k] a_b[k] for the rows of the row groups a workgroup owns in a
 // packed matrix with KT k-tiles per row group, for each sequence b.  Each
 // wave takes a fixed slice of the k-tiles of every row group (split-K inside
 // the workgroup), keeps U tile loads in flight, and reduces its partial dot
@@ -348,11 +366,23 @@ constexpr int kGemvDepth = 16;   // tile loads in flight per wave (16 KiB)
 // tiles are exhausted, a slot is refilled from a 16-byte dummy line that all
 // lanes share (one cache line per wave), and only the consumption of a slot
 // is conditional.
+//
+// A workgroup owns the row groups first, first + stride, ... (count of
+// them).  The phases use stride 1 (a contiguous block per workgroup): a
+// strided assignment (stride = grid size) was measured no faster.
+struct RgRange { int first, count; };
+__device__ __forceinline__ RgRange own_rgs(int nrg, const StepParams &P) {
+    int a, b;
+    split_range(nrg, P.nwg, blockIdx.x, a, b);
+    return RgRange{a, b - a};
+}
+
 template <class Wait, class Stage, class Epi>
-__device__ __forceinline__ void gemv_phase(const uint8_t *__restrict__ W, int KT, int rg0,
-                                           int rg1, int B, const float *__restrict__ a,
-                                           float *red, const uint8_t *dummy, Wait &&wait,
-                                           Stage &&stage, Epi &&epi) {
+__device__ __forceinline__ void gemv_phase(const uint8_t *__restrict__ W, int KT, int first,
+                                           int count, int stride, int B,
+                                           const float *__restrict__ a, float *red,
+                                           const uint8_t *dummy, Wait &&wait, Stage &&stage,
+                                           Epi &&epi) {
     constexpr int U = kGemvDepth;
     // wave-uniform values live in scalar registers, so every branch below is
     // a scalar branch
@@ -366,39 +396,44 @@ __device__ __forceinline__ void gemv_phase(const uint8_t *__restrict__ W, int KT
     u32x4 buf[U];
     int n = 0, ltile = 0, lk = 0, left = 0;   // batch items; next tile, its k index; tiles left
 
+    // from a wave's last tile of one row group to its first of the next
+    const int jump = (stride - 1) * KT + (KT - nk) + 1;
     // load the next tile of the batch, or the dummy line (branch-free)
     auto load_next = [&]() {
         const int t = __builtin_amdgcn_readfirstlane(ltile);
         const bool real = left > 0;
         const u32x4 v = ld_stream_16B(real ? base + (size_t)t * kTileBytes : dummy);
         const bool wrap = lk + 1 == nk;
-        ltile = real ? ltile + (wrap ? KT - nk + 1 : 1) : ltile;
+        ltile = real ? ltile + (wrap ? jump : 1) : ltile;
         lk = real ? (wrap ? 0 : lk + 1) : lk;
         left = real ? left - 1 : left;
         return v;
     };
-    auto start = [&](int rb) {
-        n = nk * min(kRgBatch, rg1 - rb);
+    auto start = [&](int ib) {   // batch of items ib .. ib + kRgBatch - 1
+        n = nk * min(kRgBatch, count - ib);
         left = n;
-        ltile = rb * KT + kt0;
+        ltile = (first + ib * stride) * KT + kt0;
         lk = 0;
 #pragma unroll
         for (int s = 0; s < U; ++s) buf[s] = load_next();
     };
 
-    const bool has_rows = rg0 < rg1;
-    if (has_rows) start(rg0);
+    // the control wave takes part in the staging and the epilogue only
+    const bool compute = wid < kWaves;
+    const bool has_rows = count > 0;
+    if (has_rows && compute) start(0);
     wait();
     if (!has_rows) return;
     for (int b = 0; b < B; ++b) {
-        for (int rb = rg0; rb < rg1; rb += kRgBatch) {
-            if (b > 0 || rb > rg0) start(rb);
-            if (rb == rg0) stage(b);
-            const int nrg = min(kRgBatch, rg1 - rb);
+        for (int ib = 0; ib < count; ib += kRgBatch) {
+            if ((b > 0 || ib > 0) && compute) start(ib);
+            if (ib == 0) stage(b);
+            const int nrg = min(kRgBatch, count - ib);
             int cr = 0, ck = 0;
             float acc = 0.f;
             // item i sits in slot i % U and is refilled with item i + U (or
             // the dummy line) right after it is consumed
+            if (compute)
             for (int i0 = 0; i0 < n; i0 += U) {
 #pragma unroll
                 for (int s = 0; s < U; ++s) {
@@ -435,7 +470,7 @@ __device__ __forceinline__ void gemv_phase(const uint8_t *__restrict__ W, int KT
                     y0 += red[(w * kRgBatch + rgi) * kTileRows + pr];
                     y1 += red[(w * kRgBatch + rgi) * kTileRows + pr + 1];
                 }
-                epi(b, (rb + rgi) * kTileRows + pr, y0, y1);
+                epi(b, (first + (ib + rgi) * stride) * kTileRows + pr, y0, y1);
             }
             __syncthreads();
         }
@@ -479,13 +514,12 @@ __device__ __noinline__ void phase_embed(KArg ka, int wait, int arrive) {
 __device__ __noinline__ void phase_qkv(KArg ka, int l, int wait, int arrive) {
     const StepParams P = load_params(ka);
     const Lds S = lds_layout(kl_smem, P);
-    int rg0, rg1;
-    split_range(P.qkv_rg, P.nwg, blockIdx.x, rg0, rg1);
+    const RgRange R = own_rgs(P.qkv_rg, P);
     const uint8_t *Lb = P.arena + (size_t)l * P.layer_stride;
     const float *gain = reinterpret_cast<const float *>(Lb + P.off_attn_norm);
     const int d = P.d, half = P.d / 2, qd = P.nq * P.d, kd = P.nkv * P.d;
     gemv_phase(
-        Lb + P.off_qkv, P.Hp / kTileK, rg0, rg1, P.B, S.a, S.red, P.dummy,
+        Lb + P.off_qkv, P.Hp / kTileK, R.first, R.count, 1, P.B, S.a, S.red, P.dummy,
         [&]() { if (wait >= 0) bar_wait(P, wait); },
         [&](int b) { stage_rmsnorm(P.x + (size_t)b * P.Hp, gain, P.H, P.Hp, P.eps, S.a, S.sm); },
         [&](int b, int r, float y0, float y1) {
@@ -514,69 +548,76 @@ __device__ __noinline__ void phase_qkv(KArg ka, int l, int wait, int arrive) {
     if (arrive >= 0) bar_arrive(P, arrive);
 }
 
-// One attention work item: the positions of chunk c of sequence b against KV
-// head g, for the G query heads of that group.  Scores and probabilities are
-// fp32; the chunk result is (running max, running sum, unnormalised output)
-// per head.  The last workgroup to finish a (b, g) combines all chunks in
-// chunk order and writes o.  The KV tiles of the first sub-chunk are loaded
-// before the barrier wait, except the new slot, which the QKV phase writes.
+// One attention work item: chunk c of sequence b against KV head g, for the
+// G query heads of that group (split-K flash decoding).  Positions are
+// grouped in slabs of PP positions (one 16-byte load per lane covers a slab);
+// chunk c owns a contiguous range of slabs, and inside a sub-chunk slab q is
+// held by wave q % kWaves, so every compute wave takes part even when a
+// chunk is short.  Scores and probabilities are fp32.  The chunk result is
+// (running max, running sum, unnormalised output) per head; the last chunk
+// of (b, g) to finish merges all chunks in chunk order and writes o.  The
+// first sub-chunk's K/V vectors are loaded before the barrier wait, except
+// the new slot, which the QKV phase writes and which is read after the wait
+// with device-coherent loads.  Loads are unconditional (spare ones target a
+// shared 16-byte line) and masked when consumed.
+template <int D>
+constexpr int attn_sub() { return kWaves * kAttnLoads * (64 / (D / 8)); }
+
 template <int D, int G>
 __device__ __noinline__ void attn_item(KArg ka, int l, int b, int g, int c, int wait) {
     const StepParams P = load_params(ka);
     const Lds S = lds_layout(kl_smem, P);
     constexpr int LP = D / 8;                       // lanes per position
-    constexpr int PP = 64 / LP;                     // positions per wave load
-    constexpr int NG = kAttnSub / PP / kWaves;      // loads per wave per sub-chunk
+    constexpr int PP = 64 / LP;                     // positions per slab
+    constexpr int NG = kAttnLoads;                  // slabs per wave per sub-chunk
+    constexpr int SUB = attn_sub<D>();              // positions per sub-chunk
     const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
     const int pi = lane / LP, ds = (lane % LP) * 8;
     const int pnew = eff_pos(P, b), n = pnew + 1;
-    const int cs = (n + P.C - 1) / P.C;
-    const int j0 = min(n, c * cs), j1 = min(n, j0 + cs);
+    int s0, s1;
+    split_range((n + PP - 1) / PP, P.C, c, s0, s1);
+    const int j0 = min(n, s0 * PP), j1 = min(n, s1 * PP);
+    const bool compute = wid < kWaves;
 
-    float *qs = S.a;                    // [G][D]
-    float *sp = qs + G * D;             // [G][kAttnSub]
-    float *st = sp + G * kAttnSub;      // [G][4]
+    float *qs = S.attn;                 // [G][D]
+    float *sp = qs + G * D;             // [G][SUB]
+    float *st = sp + G * SUB;           // [G][4]: max, sum, rescale
     float *red = st + G * 4;            // [kWaves][G][D]
-    float *cst = red + kWaves * G * D;  // combine: [3][Cmax][G] + [G] + [Cmax][nout]
     const size_t row0 = kv_row(P, l, b, g);
     const uint16_t *Kb = P.kc + row0 * D;
     const uint16_t *Vb = P.vc + row0 * D;
     const float scale = 1.0f / sqrtf((float)D);
 
+    // local position of (wave, load t) in a sub-chunk
+    auto jloc = [&](int t) { return (t * kWaves + wid) * PP + pi; };
     u32x4 kr[NG], vr[NG];
-    // pre: true before the barrier, when the new slot is not written yet
-    auto issue = [&](int js, int len, bool pre) {
+    auto issue = [&](int js, int len) {
+        if (!compute) return;   // the control wave keeps its load queue empty for the barrier
 #pragma unroll
         for (int t = 0; t < NG; ++t) {
-            const int jl = (wid * NG + t) * PP + pi;
-            const int pos = js + jl;
-            if (jl < len && pos != pnew) {
-                kr[t] = ld_stream_16B(Kb + (size_t)pos * D + ds);
-                vr[t] = ld_stream_16B(Vb + (size_t)pos * D + ds);
-            } else if (jl < len && !pre) {
-                kr[t] = ld_dev_16B(Kb + (size_t)pos * D + ds);
-                vr[t] = ld_dev_16B(Vb + (size_t)pos * D + ds);
-            } else {
-                kr[t] = u32x4{0u, 0u, 0u, 0u};
-                vr[t] = u32x4{0u, 0u, 0u, 0u};
+            const int jl = jloc(t), pos = js + jl;
+            const bool real = compute && jl < len && pos != pnew;
+            kr[t] = ld_stream_16B(real ? (const void *)(Kb + (size_t)pos * D + ds) : P.dummy);
+            vr[t] = ld_stream_16B(real ? (const void *)(Vb + (size_t)pos * D + ds) : P.dummy);
+        }
+    };
+    // the new slot (written during this step by another workgroup) is read
+    // with device-coherent loads, after the wait
+    auto fetch_new = [&](int js, int len) {
+        if (compute && pnew >= js && pnew < js + len) {
+#pragma unroll
+            for (int t = 0; t < NG; ++t) {
+                if (js + jloc(t) == pnew) {
+                    kr[t] = ld_dev_16B(Kb + (size_t)pnew * D + ds);
+                    vr[t] = ld_dev_16B(Vb + (size_t)pnew * D + ds);
+                }
             }
         }
     };
-    const int len0 = min(kAttnSub, j1 - j0);
-    if (j0 < j1) issue(j0, len0, true);
+    issue(j0, min(SUB, j1 - j0));
     if (wait >= 0) bar_wait(P, wait);
-    if (j0 < j1 && pnew >= j0 && pnew < j0 + len0) {
-        // the new slot lies in the first sub-chunk: fetch it now, coherently
-#pragma unroll
-        for (int t = 0; t < NG; ++t) {
-            const int pos = j0 + (wid * NG + t) * PP + pi;
-            if (pos == pnew) {
-                kr[t] = ld_dev_16B(Kb + (size_t)pos * D + ds);
-                vr[t] = ld_dev_16B(Vb + (size_t)pos * D + ds);
-            }
-        }
-    }
+    fetch_new(j0, min(SUB, j1 - j0));
     for (int t = threadIdx.x; t < G * D; t += kThreads)
         qs[t] = ld_dev(P.q + (size_t)b * P.nq * D + (size_t)g * G * D + t);
     if (threadIdx.x < G) {
@@ -590,30 +631,36 @@ __device__ __noinline__ void attn_item(KArg ka, int l, int b, int g, int c, int 
 #pragma unroll
         for (int e = 0; e < 8; ++e) acc[h][e] = 0.f;
 
-    for (int js = j0; js < j1; js += kAttnSub) {
-        const int len = min(kAttnSub, j1 - js);
-        if (js != j0) issue(js, len, false);
+    for (int js = j0; js < j1; js += SUB) {
+        const int len = min(SUB, j1 - js);
+        if (js != j0) {
+            issue(js, len);
+            fetch_new(js, len);
+        }
         // scores (q is read from LDS; all lanes take part in the lane sums)
+        if (compute) {
 #pragma unroll
-        for (int t = 0; t < NG; ++t) {
-            const int jl = (wid * NG + t) * PP + pi;
-            const float kf[8] = {bf_lo(kr[t].x), bf_hi(kr[t].x), bf_lo(kr[t].y), bf_hi(kr[t].y),
-                                 bf_lo(kr[t].z), bf_hi(kr[t].z), bf_lo(kr[t].w), bf_hi(kr[t].w)};
+            for (int t = 0; t < NG; ++t) {
+                const int jl = jloc(t);
+                const float kf[8] = {bf_lo(kr[t].x), bf_hi(kr[t].x), bf_lo(kr[t].y),
+                                     bf_hi(kr[t].y), bf_lo(kr[t].z), bf_hi(kr[t].z),
+                                     bf_lo(kr[t].w), bf_hi(kr[t].w)};
 #pragma unroll
-            for (int h = 0; h < G; ++h) {
-                const float4 q0 = *reinterpret_cast<const float4 *>(qs + h * D + ds);
-                const float4 q1 = *reinterpret_cast<const float4 *>(qs + h * D + ds + 4);
-                float s = 0.f;
-                s = fmaf(q0.x, kf[0], s);
-                s = fmaf(q0.y, kf[1], s);
-                s = fmaf(q0.z, kf[2], s);
-                s = fmaf(q0.w, kf[3], s);
-                s = fmaf(q1.x, kf[4], s);
-                s = fmaf(q1.y, kf[5], s);
-                s = fmaf(q1.z, kf[6], s);
-                s = fmaf(q1.w, kf[7], s);
-                s = sum_lanes<LP>(s);
-                if (jl < len && (lane % LP) == 0) sp[h * kAttnSub + jl] = s * scale;
+                for (int h = 0; h < G; ++h) {
+                    const float4 q0 = *reinterpret_cast<const float4 *>(qs + h * D + ds);
+                    const float4 q1 = *reinterpret_cast<const float4 *>(qs + h * D + ds + 4);
+                    float s = 0.f;
+                    s = fmaf(q0.x, kf[0], s);
+                    s = fmaf(q0.y, kf[1], s);
+                    s = fmaf(q0.z, kf[2], s);
+                    s = fmaf(q0.w, kf[3], s);
+                    s = fmaf(q1.x, kf[4], s);
+                    s = fmaf(q1.y, kf[5], s);
+                    s = fmaf(q1.z, kf[6], s);
+                    s = fmaf(q1.w, kf[7], s);
+                    s = sum_lanes<LP>(s);
+                    if (jl < len && (lane % LP) == 0) sp[h * SUB + jl] = s * scale;
+                }
             }
         }
         __syncthreads();
@@ -621,14 +668,14 @@ __device__ __noinline__ void attn_item(KArg ka, int l, int b, int g, int c, int 
         if (wid < G) {
             const int h = wid;
             float mx = -INFINITY;
-            for (int j = lane; j < len; j += 64) mx = fmaxf(mx, sp[h * kAttnSub + j]);
+            for (int j = lane; j < len; j += 64) mx = fmaxf(mx, sp[h * SUB + j]);
             mx = wave_max(mx);
             const float mold = st[h * 4], mnew = fmaxf(mold, mx);
             const float resc = (mold == -INFINITY) ? 0.f : expf(mold - mnew);
             float sum = 0.f;
             for (int j = lane; j < len; j += 64) {
-                const float e = expf(sp[h * kAttnSub + j] - mnew);
-                sp[h * kAttnSub + j] = e;
+                const float e = expf(sp[h * SUB + j] - mnew);
+                sp[h * SUB + j] = e;
                 sum += e;
             }
             sum = wave_sum(sum);
@@ -640,47 +687,65 @@ __device__ __noinline__ void attn_item(KArg ka, int l, int b, int g, int c, int 
         }
         __syncthreads();
         // values
+        if (compute) {
 #pragma unroll
-        for (int h = 0; h < G; ++h) {
-            const float r = st[h * 4 + 2];
+            for (int h = 0; h < G; ++h) {
+                const float r = st[h * 4 + 2];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) acc[h][e] *= r;
-        }
+                for (int e = 0; e < 8; ++e) acc[h][e] *= r;
+            }
 #pragma unroll
-        for (int t = 0; t < NG; ++t) {
-            const int jl = (wid * NG + t) * PP + pi;
-            if (jl < len) {
-                const float vf[8] = {bf_lo(vr[t].x), bf_hi(vr[t].x), bf_lo(vr[t].y),
-                                     bf_hi(vr[t].y), bf_lo(vr[t].z), bf_hi(vr[t].z),
-                                     bf_lo(vr[t].w), bf_hi(vr[t].w)};
+            for (int t = 0; t < NG; ++t) {
+                const int jl = jloc(t);
+                if (jl < len) {
+                    const float vf[8] = {bf_lo(vr[t].x), bf_hi(vr[t].x), bf_lo(vr[t].y),
+                                         bf_hi(vr[t].y), bf_lo(vr[t].z), bf_hi(vr[t].z),
+                                         bf_lo(vr[t].w), bf_hi(vr[t].w)};
 #pragma unroll
-                for (int h = 0; h < G; ++h) {
-                    const float pr = sp[h * kAttnSub + jl];
+                    for (int h = 0; h < G; ++h) {
+                        const float pr = sp[h * SUB + jl];
 #pragma unroll
-                    for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(pr, vf[e], acc[h][e]);
+                        for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(pr, vf[e], acc[h][e]);
+                    }
                 }
             }
         }
         __syncthreads();
     }
     // reduce the PP position slots of each wave, then the waves in order
-#pragma unroll
-    for (int h = 0; h < G; ++h)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            float v = acc[h][e];
-#pragma unroll
-            for (int off = LP; off < 64; off <<= 1) v += __shfl_xor(v, off);
-            acc[h][e] = v;
-        }
-    if (pi == 0) {
+    if (compute) {
 #pragma unroll
         for (int h = 0; h < G; ++h)
 #pragma unroll
-            for (int e = 0; e < 8; ++e) red[(wid * G + h) * D + ds + e] = acc[h][e];
+            for (int e = 0; e < 8; ++e) {
+                float v = acc[h][e];
+#pragma unroll
+                for (int off = LP; off < 64; off <<= 1) v += __shfl_xor(v, off);
+                acc[h][e] = v;
+            }
+        if (pi == 0) {
+#pragma unroll
+            for (int h = 0; h < G; ++h)
+#pragma unroll
+                for (int e = 0; e < 8; ++e) red[(wid * G + h) * D + ds + e] = acc[h][e];
+        }
     }
     __syncthreads();
-    float *part_bg = P.part + (size_t)(b * P.nkv + g) * P.C * G * (D + 2);
+    float *o_bg = P.o + (size_t)b * P.Ap + (size_t)g * G * D;
+    const int C = P.C;
+    if (C == 1) {
+        // a single chunk: normalise and write o directly
+        for (int t = threadIdx.x; t < G * D; t += kThreads) {
+            const int h = t / D, dd = t % D;
+            float s = 0.f;
+            for (int w = 0; w < kWaves; ++w) s += red[(w * G + h) * D + dd];
+            st_dev(o_bg + t, s / st[h * 4 + 1]);
+        }
+        if (is_ctl_lane0() && wait >= 0) trace_stamp(P, wait + 1, 3);
+        __syncthreads();
+        return;
+    }
+    float *part_bg = P.part + (size_t)(b * P.nkv + g) * C * G * (D + 2);
     float *out = part_bg + (size_t)c * G * (D + 2);
     for (int t = threadIdx.x; t < G * D; t += kThreads) {
         const int h = t / D, dd = t % D;
@@ -692,87 +757,61 @@ __device__ __noinline__ void attn_item(KArg ka, int l, int b, int g, int c, int 
         st_dev(out + threadIdx.x * (D + 2) + D, st[threadIdx.x * 4 + 0]);
         st_dev(out + threadIdx.x * (D + 2) + D + 1, st[threadIdx.x * 4 + 1]);
     }
-    // Publish this chunk, then combine: once all C chunks of (b, g) are in,
-    // each of the C workgroups finalises its own slice of the G*D outputs,
-    // reading every chunk's statistics and its slice of their outputs (all
-    // loads in one round trip) and merging them in chunk order.  The per-(b, g)
-    // counter is zeroed by the embedding phase and grows by C per layer.
-    if (threadIdx.x == 0 && wait >= 0) trace_stamp(P, wait + 1, 3);
+    // Publish this chunk; the workgroup whose arrival completes the count
+    // merges all chunks.  The per-(b, g) counter is zeroed by the embedding
+    // phase and grows by C per layer.
+    if (is_ctl_lane0() && wait >= 0) trace_stamp(P, wait + 1, 3);
     wait_stores();
     __syncthreads();
-    const int C = P.C;
-    if (threadIdx.x == 0) {
-        unsigned *cnt = P.cnt + b * P.nkv + g;
-        __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        const unsigned target = (unsigned)(l + 1) * (unsigned)C;
-        for (int spins = 0;
-             (int)(__hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) - target) < 0;
-             ++spins) {
-            if (__hip_atomic_load(P.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) &
-                KL_DEVERR_BARRIER)
-                break;
-            if (spins >= kSpinLimit) {
-                __hip_atomic_fetch_or(P.err, KL_DEVERR_BARRIER, __ATOMIC_RELAXED,
-                                      __HIP_MEMORY_SCOPE_AGENT);
-                break;
-            }
-        }
+    int *flag = reinterpret_cast<int *>(S.sm);
+    if (is_ctl_lane0()) {
+        const unsigned old = __hip_atomic_fetch_add(P.cnt + b * P.nkv + g, 1u, __ATOMIC_RELAXED,
+                                                    __HIP_MEMORY_SCOPE_AGENT);
+        flag[0] = (old == (unsigned)(l + 1) * (unsigned)C - 1u) ? 1 : 0;
     }
     __syncthreads();
-    const int nout = (G * D + C - 1) / C;              // outputs finalised per chunk
-    const int o0 = c * nout, o1 = min(G * D, o0 + nout);
-    const int no = max(0, o1 - o0);
-    float *cM = cst, *cL = cst + C * G, *cW = cst + 2 * C * G, *cT = cst + 3 * C * G;
-    float *cA = cT + G;                                // [C][nout]
-    // gather: up to 4 loads per thread issued together, then stored to LDS
-    const int ngather = C * G + C * no;
-    for (int t0 = 0; t0 < ngather; t0 += 4 * kThreads) {
-        float v0[4], v1[4];
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const int t = t0 + k * kThreads + threadIdx.x;
-            v0[k] = v1[k] = 0.f;
-            if (t < C * G) {
-                const float *pc = part_bg + (size_t)t * (D + 2);   // t = cc * G + h
-                v0[k] = ld_dev(pc + D);
-                v1[k] = ld_dev(pc + D + 1);
-            } else if (t < ngather) {
-                const int u = t - C * G, cc = u / no, j = o0 + u % no;
-                v0[k] = ld_dev(part_bg + ((size_t)cc * G + j / D) * (D + 2) + j % D);
-            }
-        }
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const int t = t0 + k * kThreads + threadIdx.x;
-            if (t < C * G) {
-                cM[t] = v0[k];
-                cL[t] = v1[k];
-            } else if (t < ngather) {
-                const int u = t - C * G;
-                cA[(u / no) * nout + u % no] = v0[k];
-            }
-        }
-    }
-    __syncthreads();
-    for (int t = threadIdx.x; t < C * G; t += kThreads) {
-        const int h = t % G;
-        float M = -INFINITY;
-        for (int cc = 0; cc < C; ++cc) M = fmaxf(M, cM[cc * G + h]);
-        cW[t] = (cM[t] == -INFINITY) ? 0.f : expf(cM[t] - M);
-    }
-    __syncthreads();
-    if (threadIdx.x < G) {
-        float lsum = 0.f;
-        for (int cc = 0; cc < C; ++cc)
-            lsum = fmaf(cL[cc * G + threadIdx.x], cW[cc * G + threadIdx.x], lsum);
-        cT[threadIdx.x] = lsum;
-    }
-    __syncthreads();
-    for (int t = threadIdx.x; t < no; t += kThreads) {
-        const int j = o0 + t, h = j / D;
+    if (!flag[0]) return;
+    // merge: every thread owns outputs j (of G*D); its loads of all chunks'
+    // partial outputs are issued together with the statistics loads
+    float *cM = S.attn, *cL = cM + C * G, *cW = cL + C * G, *cT = cW + C * G;
+    for (int j = threadIdx.x; j - (int)threadIdx.x < G * D; j += kThreads) {
+        const bool jv = j < G * D;
+        const int h = jv ? j / D : 0, dd = jv ? j % D : 0;
         float num = 0.f;
-        for (int cc = 0; cc < C; ++cc) num = fmaf(cA[cc * nout + t], cW[cc * G + h], num);
-        st_dev(P.o + (size_t)b * P.Ap + (size_t)g * G * D + j, num / cT[h]);
+        for (int c0 = 0; c0 < C; c0 += kCombBatch) {
+            float av[kCombBatch];
+#pragma unroll
+            for (int k = 0; k < kCombBatch; ++k)
+                av[k] = (jv && c0 + k < C)
+                            ? ld_dev(part_bg + ((size_t)(c0 + k) * G + h) * (D + 2) + dd)
+                            : 0.f;
+            if (j == (int)threadIdx.x && c0 == 0) {
+                // (first pass only, uniform across the block)
+                for (int t = threadIdx.x; t < C * G; t += kThreads) {
+                    cM[t] = ld_dev(part_bg + (size_t)t * (D + 2) + D);
+                    cL[t] = ld_dev(part_bg + (size_t)t * (D + 2) + D + 1);
+                }
+                __syncthreads();
+                for (int t = threadIdx.x; t < C * G; t += kThreads) {
+                    const int hh = t % G;
+                    float M = -INFINITY;
+                    for (int cc = 0; cc < C; ++cc) M = fmaxf(M, cM[cc * G + hh]);
+                    cW[t] = (cM[t] == -INFINITY) ? 0.f : expf(cM[t] - M);
+                }
+                __syncthreads();
+                if (threadIdx.x < G) {
+                    float lsum = 0.f;
+                    for (int cc = 0; cc < C; ++cc)
+                        lsum = fmaf(cL[cc * G + threadIdx.x], cW[cc * G + threadIdx.x], lsum);
+                    cT[threadIdx.x] = lsum;
+                }
+                __syncthreads();
+            }
+#pragma unroll
+            for (int k = 0; k < kCombBatch; ++k)
+                if (c0 + k < C) num = fmaf(av[k], cW[(c0 + k) * G + h], num);
+        }
+        if (jv) st_dev(o_bg + j, num / cT[h]);
     }
     __syncthreads();
 }
@@ -802,21 +841,20 @@ __device__ __noinline__ void phase_attn(KArg ka, int l, int wait, int arrive) {
     if (arrive >= 0) bar_arrive(P, arrive);
 }
 
-// O projection + residual: x += Wo o (each row has one owner; no atomics).
+// O projection + residual: x += Wo o (each row has one owner).
 __device__ __noinline__ void phase_oproj(KArg ka, int l, int wait, int arrive) {
     const StepParams P = load_params(ka);
     const Lds S = lds_layout(kl_smem, P);
-    int rg0, rg1;
-    split_range(P.o_rg, P.nwg, blockIdx.x, rg0, rg1);
+    const RgRange R = own_rgs(P.o_rg, P);
     const uint8_t *Lb = P.arena + (size_t)l * P.layer_stride;
     gemv_phase(
-        Lb + P.off_o, P.Ap / kTileK, rg0, rg1, P.B, S.a, S.red, P.dummy,
+        Lb + P.off_o, P.Ap / kTileK, R.first, R.count, 1, P.B, S.a, S.red, P.dummy,
         [&]() { if (wait >= 0) bar_wait(P, wait); },
         [&](int b) { stage_vec(P.o + (size_t)b * P.Ap, P.Ap, P.Ap, S.a); },
         [&](int b, int r, float y0, float y1) {
             float *x = P.x + (size_t)b * P.Hp;
-            st_dev(x + r, ld_dev(x + r) + y0);
-            st_dev(x + r + 1, ld_dev(x + r + 1) + y1);
+            add_dev(x + r, y0);
+            add_dev(x + r + 1, y1);
         });
     if (arrive >= 0) bar_arrive(P, arrive);
 }
@@ -826,12 +864,11 @@ __device__ __noinline__ void phase_oproj(KArg ka, int l, int wait, int arrive) {
 __device__ __noinline__ void phase_gateup(KArg ka, int l, int wait, int arrive) {
     const StepParams P = load_params(ka);
     const Lds S = lds_layout(kl_smem, P);
-    int rg0, rg1;
-    split_range(P.gu_rg, P.nwg, blockIdx.x, rg0, rg1);
+    const RgRange R = own_rgs(P.gu_rg, P);
     const uint8_t *Lb = P.arena + (size_t)l * P.layer_stride;
     const float *gain = reinterpret_cast<const float *>(Lb + P.off_ffn_norm);
     gemv_phase(
-        Lb + P.off_gu, P.Hp / kTileK, rg0, rg1, P.B, S.a, S.red, P.dummy,
+        Lb + P.off_gu, P.Hp / kTileK, R.first, R.count, 1, P.B, S.a, S.red, P.dummy,
         [&]() { if (wait >= 0) bar_wait(P, wait); },
         [&](int b) { stage_rmsnorm(P.x + (size_t)b * P.Hp, gain, P.H, P.Hp, P.eps, S.a, S.sm); },
         [&](int b, int r, float gt, float up) {
@@ -844,17 +881,17 @@ __device__ __noinline__ void phase_gateup(KArg ka, int l, int wait, int arrive) 
 __device__ __noinline__ void phase_down(KArg ka, int l, int wait, int arrive) {
     const StepParams P = load_params(ka);
     const Lds S = lds_layout(kl_smem, P);
-    int rg0, rg1;
-    split_range(P.down_rg, P.nwg, blockIdx.x, rg0, rg1);
+    const RgRange R = own_rgs(P.down_rg, P);
     const uint8_t *Lb = P.arena + (size_t)l * P.layer_stride;
     gemv_phase(
-        Lb + P.off_down, P.Fp / kTileK, rg0, rg1, P.B, S.a, S.red, P.dummy,
+        Lb + P.off_down, P.Fp / kTileK, R.first, R.count, 1,
+        P.B, S.a, S.red, P.dummy,
         [&]() { if (wait >= 0) bar_wait(P, wait); },
         [&](int b) { stage_vec(P.m + (size_t)b * P.Fp, P.Fp, P.Fp, S.a); },
         [&](int b, int r, float y0, float y1) {
             float *x = P.x + (size_t)b * P.Hp;
-            st_dev(x + r, ld_dev(x + r) + y0);
-            st_dev(x + r + 1, ld_dev(x + r + 1) + y1);
+            add_dev(x + r, y0);
+            add_dev(x + r + 1, y1);
         });
     if (arrive >= 0) bar_arrive(P, arrive);
 }
@@ -863,11 +900,10 @@ __device__ __noinline__ void phase_down(KArg ka, int l, int wait, int arrive) {
 __device__ __noinline__ void phase_head(KArg ka, int wait, int arrive) {
     const StepParams P = load_params(ka);
     const Lds S = lds_layout(kl_smem, P);
-    int rg0, rg1;
-    split_range(P.head_rg, P.nwg, blockIdx.x, rg0, rg1);
+    const RgRange R = own_rgs(P.head_rg, P);
     const int V = P.V;
     gemv_phase(
-        reinterpret_cast<const uint8_t *>(P.lm_head), P.Hp / kTileK, rg0, rg1, P.B, S.a, S.red,
+        reinterpret_cast<const uint8_t *>(P.lm_head), P.Hp / kTileK, R.first, R.count, 1, P.B, S.a, S.red,
         P.dummy,
         [&]() {
             if (wait >= 0) bar_wait(P, wait);

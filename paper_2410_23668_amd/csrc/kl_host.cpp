@@ -36,6 +36,7 @@ struct kl_state {
     unsigned long long *trace;
     int trace_max;
     int nwg, lds_bytes;
+    int lds_red, lds_sm, lds_bar;
 };
 
 namespace {
@@ -118,17 +119,23 @@ std::vector<int32_t> gateup_rowmap(int F) {
     return m;
 }
 
-int lds_bytes_for(const kl_state &s) {
+// Dynamic LDS layout of the step kernel (offsets in floats): the activation
+// vector / attention area, the GEMV wave partials, 64 floats of small
+// reductions and flags, then the barrier bases.
+void lds_layout_for(kl_state &s) {
     const kl_config &c = s.cfg;
-    const int g = c.n_heads / c.n_kv_heads;
-    int amax = std::max(std::max(s.Hp, s.Ap), s.Fp);
+    const int g = c.n_heads / c.n_kv_heads, d = c.head_dim;
     const int cmax = std::max(1, s.nwg / c.n_kv_heads);
-    const int attn = g * c.head_dim + g * kAttnSub + g * 4 + kWaves * g * c.head_dim +
-                     3 * cmax * g + g + g * c.head_dim + cmax;
-    amax = std::max(amax, attn);
+    const int sub = kWaves * kAttnLoads * (64 / (d / 8));      // positions per sub-chunk
+    const int attn_main = g * d + g * sub + g * 4 + kWaves * g * d;
+    const int attn_merge = 3 * cmax * g + g;
+    int amax = std::max(std::max(s.Hp, s.Ap), s.Fp);
+    amax = std::max(amax, std::max(attn_main, attn_merge));
     amax = (amax + 63) & ~63;
-    return (amax + kWaves * kRgBatch * kTileRows + 64) * (int)sizeof(float) +
-           kBarGroups * (int)sizeof(unsigned long long);
+    s.lds_red = amax;
+    s.lds_sm = s.lds_red + kWaves * kRgBatch * kTileRows;
+    s.lds_bar = s.lds_sm + 64;
+    s.lds_bytes = (s.lds_bar + 2 * kBarGroups) * (int)sizeof(float);
 }
 
 void free_state(kl_state *s) {
@@ -158,6 +165,7 @@ StepParams base_params(const kl_state &s) {
     P.x = s.x; P.q = s.q; P.o = s.o; P.m = s.m; P.part = s.part;
     P.bar = s.bar; P.cnt = s.cnt; P.err = s.err; P.dummy = s.dummy;
     P.nwg = s.nwg;
+    P.lds_red = s.lds_red; P.lds_sm = s.lds_sm; P.lds_bar = s.lds_bar;
     P.trace = s.trace;
     P.trace_max = s.trace_max;
     return P;
@@ -248,7 +256,7 @@ kl_status kl_load_model(const kl_config *cfg, const kl_weight_ptrs *w, void *str
 
     // grid: one persistent workgroup per CU
     S->nwg = ncu;
-    S->lds_bytes = lds_bytes_for(*S);
+    lds_layout_for(*S);
     if (S->lds_bytes > 160 * 1024 - 256)
         return bail(fail(KL_ERR_UNSUPPORTED, "LDS need %d bytes exceeds 160 KiB", S->lds_bytes));
     int per_cu = 0;

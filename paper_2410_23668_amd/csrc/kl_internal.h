@@ -9,13 +9,15 @@
 namespace kl {
 
 // Work geometry shared by host and device.
-constexpr int kWaves = 8;                 // waves per workgroup
-constexpr int kThreads = kWaves * 64;     // threads per workgroup
+constexpr int kWaves = 8;                 // compute waves per workgroup
+constexpr int kCtlWave = kWaves;          // the control wave: barriers and counters only
+constexpr int kThreads = (kWaves + 1) * 64;   // threads per workgroup
 constexpr int kTileRows = 8;              // rows of one packed weight tile
 constexpr int kTileK = 64;                // columns of one packed weight tile
 constexpr int kTileBytes = kTileRows * kTileK * 2;   // 1 KiB: one 16-byte load per lane
 constexpr int kRgBatch = 16;              // row groups reduced per LDS round
-constexpr int kAttnSub = 256;             // positions per attention sub-chunk
+constexpr int kAttnLoads = 5;             // K (and V) loads per lane per attention sub-chunk
+constexpr int kCombBatch = 32;            // chunk partials loaded together when merging
 constexpr int kMaxGroup = 8;              // max query heads per KV head
 constexpr int kBarGroups = 16;            // first level of the grid barrier
 constexpr int kBarBytes = 8192;           // barrier counters: kBarGroups lines of 256 B
@@ -60,6 +62,7 @@ struct StepParams {
     int *err;                  // device error word
     const uint8_t *dummy;      // 16 readable bytes: target of the GEMV ring's spare loads
     int nwg;                   // grid size; the work partition depends only on it
+    int lds_red, lds_sm, lds_bar;   // dynamic LDS layout (float offsets)
     int C;                     // attention chunks per (sequence, KV head)
     unsigned long long *trace; // optional barrier timestamps (see kl_set_trace), or null
     int trace_max;             // barriers recorded per launch
