@@ -183,7 +183,7 @@ __device__ __forceinline__ unsigned long long *bar_counter(const StepParams &P, 
     return P.bar + 32 * (g + 1);   // 256 bytes apart
 }
 
-__device__ void bar_init(const StepParams &P) {
+__device__ __forceinline__ void bar_init(const StepParams &P) {
     // Only this workgroup's own group counter is read: that group cannot
     // complete barrier 0 before this workgroup arrives, so the value rounds
     // down to the number E of whole barriers done by earlier launches.  Any
@@ -257,14 +257,13 @@ __device__ __forceinline__ void bar_wait(const StepParams &P, int k) {
 
 // ---------------------------------------------------------------- params
 //
-// Each phase is a separate (non-inlined) function that reads the step
-// parameters from the kernel-argument segment itself.  Inlining all phases
-// into the layer loop would let the compiler hoist every phase's address
-// arithmetic out of the loop and keep it live across all phases, which
-// exhausts registers; separate functions keep each phase's registers local.
-// The kernel passes the address of its argument segment down as an integer
-// (the segment-pointer builtin is only valid inside the kernel itself), and
-// the callee makes it wave-uniform again so the fields load with s_load.
+// The step kernel is one function per (head_dim, group size), with every
+// phase inlined (no calls: a call would save and restore callee-saved
+// registers through scratch memory on every phase).  Each phase reads the
+// step parameters from the kernel-argument segment itself, through an
+// address the compiler cannot see through, so the loads stay inside the
+// phase instead of being hoisted out of the layer loop, where the values of
+// all phases together would exhaust the registers.
 #define KL_KARG __attribute__((address_space(4)))
 
 typedef uint64_t KArg;
@@ -279,8 +278,9 @@ __device__ __forceinline__ KArg kernarg_address() {
 
 __device__ __forceinline__ StepParams load_params(KArg ka) {
 #if defined(__HIP_DEVICE_COMPILE__)
-    const unsigned lo = __builtin_amdgcn_readfirstlane((unsigned)ka);
-    const unsigned hi = __builtin_amdgcn_readfirstlane((unsigned)(ka >> 32));
+    unsigned lo = __builtin_amdgcn_readfirstlane((unsigned)ka);
+    unsigned hi = __builtin_amdgcn_readfirstlane((unsigned)(ka >> 32));
+    asm volatile("" : "+s"(lo), "+s"(hi));
     const KL_KARG StepParams *p = (const KL_KARG StepParams *)(((KArg)hi << 32) | lo);
     return *p;
 #else
@@ -485,7 +485,7 @@ __device__ __forceinline__ void gemv_phase(const uint8_t *__restrict__ W, int KT
 
 // Embedding block (Sec. 2): x = f32(E[token]).  Workgroup 0 records bad
 // token ids and positions in the device error word.
-__device__ __noinline__ void phase_embed(KArg ka, int wait, int arrive) {
+__device__ __forceinline__ void phase_embed(KArg ka, int wait, int arrive) {
     const StepParams P = load_params(ka);
     if (wait >= 0) bar_wait(P, wait);
     if (blockIdx.x == 0) {
@@ -511,7 +511,7 @@ __device__ __noinline__ void phase_embed(KArg ka, int wait, int arrive) {
 
 // RMSNorm + fused Q/K/V projection + RoPE + KV-cache append.  Q/K rows are
 // packed in rotation pairs (dims i and i + d/2 adjacent), V rows in order.
-__device__ __noinline__ void phase_qkv(KArg ka, int l, int wait, int arrive) {
+__device__ __forceinline__ void phase_qkv(KArg ka, int l, int wait, int arrive) {
     const StepParams P = load_params(ka);
     const Lds S = lds_layout(kl_smem, P);
     const RgRange R = own_rgs(P.qkv_rg, P);
@@ -564,7 +564,7 @@ template <int D>
 constexpr int attn_sub() { return kWaves * kAttnLoads * (64 / (D / 8)); }
 
 template <int D, int G>
-__device__ __noinline__ void attn_item(KArg ka, int l, int b, int g, int c, int wait) {
+__device__ __forceinline__ void attn_item(KArg ka, int l, int b, int g, int c, int wait) {
     const StepParams P = load_params(ka);
     const Lds S = lds_layout(kl_smem, P);
     constexpr int LP = D / 8;                       // lanes per position
@@ -816,25 +816,14 @@ __device__ __noinline__ void attn_item(KArg ka, int l, int b, int g, int c, int 
     __syncthreads();
 }
 
-template <int D>
-__device__ __forceinline__ void attn_dispatch_g(KArg ka, int group, int l, int b, int g, int c,
-                                                int wait) {
-    switch (group) {
-        case 1: attn_item<D, 1>(ka, l, b, g, c, wait); break;
-        case 2: attn_item<D, 2>(ka, l, b, g, c, wait); break;
-        case 4: attn_item<D, 4>(ka, l, b, g, c, wait); break;
-        default: attn_item<D, 8>(ka, l, b, g, c, wait); break;
-    }
-}
-
-__device__ __noinline__ void phase_attn(KArg ka, int l, int wait, int arrive) {
+template <int D, int G>
+__device__ __forceinline__ void phase_attn(KArg ka, int l, int wait, int arrive) {
     const StepParams P = load_params(ka);
     const int items = P.B * P.nkv * P.C;
     bool waited = wait < 0;
     for (int it = blockIdx.x; it < items; it += P.nwg) {
         const int c = it % P.C, bg = it / P.C, g = bg % P.nkv, b = bg / P.nkv;
-        if (P.d == 64) attn_dispatch_g<64>(ka, P.group, l, b, g, c, waited ? -1 : wait);
-        else attn_dispatch_g<128>(ka, P.group, l, b, g, c, waited ? -1 : wait);
+        attn_item<D, G>(ka, l, b, g, c, waited ? -1 : wait);
         waited = true;
     }
     if (!waited) bar_wait(P, wait);
@@ -842,7 +831,7 @@ __device__ __noinline__ void phase_attn(KArg ka, int l, int wait, int arrive) {
 }
 
 // O projection + residual: x += Wo o (each row has one owner).
-__device__ __noinline__ void phase_oproj(KArg ka, int l, int wait, int arrive) {
+__device__ __forceinline__ void phase_oproj(KArg ka, int l, int wait, int arrive) {
     const StepParams P = load_params(ka);
     const Lds S = lds_layout(kl_smem, P);
     const RgRange R = own_rgs(P.o_rg, P);
@@ -861,7 +850,7 @@ __device__ __noinline__ void phase_oproj(KArg ka, int l, int wait, int arrive) {
 
 // RMSNorm + fused gate/up projection + SwiGLU: m = silu(Wg u) * (Wu u).
 // Packed rows alternate gate i, up i.
-__device__ __noinline__ void phase_gateup(KArg ka, int l, int wait, int arrive) {
+__device__ __forceinline__ void phase_gateup(KArg ka, int l, int wait, int arrive) {
     const StepParams P = load_params(ka);
     const Lds S = lds_layout(kl_smem, P);
     const RgRange R = own_rgs(P.gu_rg, P);
@@ -878,7 +867,7 @@ __device__ __noinline__ void phase_gateup(KArg ka, int l, int wait, int arrive) 
 }
 
 // Down projection + residual: x += Wd m.
-__device__ __noinline__ void phase_down(KArg ka, int l, int wait, int arrive) {
+__device__ __forceinline__ void phase_down(KArg ka, int l, int wait, int arrive) {
     const StepParams P = load_params(ka);
     const Lds S = lds_layout(kl_smem, P);
     const RgRange R = own_rgs(P.down_rg, P);
@@ -897,7 +886,7 @@ __device__ __noinline__ void phase_down(KArg ka, int l, int wait, int arrive) {
 }
 
 // Classifier block (Sec. 2): final RMSNorm + LM head -> fp32 logits.
-__device__ __noinline__ void phase_head(KArg ka, int wait, int arrive) {
+__device__ __forceinline__ void phase_head(KArg ka, int wait, int arrive) {
     const StepParams P = load_params(ka);
     const Lds S = lds_layout(kl_smem, P);
     const RgRange R = own_rgs(P.head_rg, P);
@@ -925,25 +914,46 @@ __device__ __noinline__ void phase_head(KArg ka, int wait, int arrive) {
 
 // ---------------------------------------------------------------- kernels
 
+template <int D, int G>
 __global__ __launch_bounds__(kThreads) void kl_step_kernel(StepParams P, int l0, int l1,
                                                           int phases) {
+    (void)P;   // read through the kernel-argument segment (see load_params)
     const KArg ka = kernarg_address();
     const int per_layer = __builtin_popcount(phases & kPhLayer);
     const int total = ((phases & kPhEmbed) ? 1 : 0) + (l1 - l0) * per_layer +
                       ((phases & kPhHead) ? 1 : 0);
-    if (total > 1) bar_init(P);
+    if (total > 1) bar_init(load_params(ka));
     int i = 0;   // index of the phase within this launch: waits on i - 1, arrives on i
     auto wt = [&]() { return i - 1; };
     auto ar = [&]() { return i + 1 < total ? i : -1; };
     if (phases & kPhEmbed) { phase_embed(ka, wt(), ar()); ++i; }
     for (int l = l0; l < l1; ++l) {
         if (phases & kPhQkv) { phase_qkv(ka, l, wt(), ar()); ++i; }
-        if (phases & kPhAttn) { phase_attn(ka, l, wt(), ar()); ++i; }
+        if (phases & kPhAttn) { phase_attn<D, G>(ka, l, wt(), ar()); ++i; }
         if (phases & kPhOproj) { phase_oproj(ka, l, wt(), ar()); ++i; }
         if (phases & kPhGateUp) { phase_gateup(ka, l, wt(), ar()); ++i; }
         if (phases & kPhDown) { phase_down(ka, l, wt(), ar()); ++i; }
     }
     if (phases & kPhHead) { phase_head(ka, wt(), ar()); ++i; }
+}
+
+typedef void (*StepKernel)(StepParams, int, int, int);
+
+// The instance for a model's head_dim and query heads per KV head (the host
+// has validated both).
+StepKernel step_kernel_for(int d, int group) {
+#define KL_INST(DD)                                      \
+    switch (group) {                                     \
+        case 1: return kl_step_kernel<DD, 1>;            \
+        case 2: return kl_step_kernel<DD, 2>;            \
+        case 4: return kl_step_kernel<DD, 4>;            \
+        case 8: return kl_step_kernel<DD, 8>;            \
+        default: return nullptr;                         \
+    }
+    if (d == 64) { KL_INST(64) }
+    if (d == 128) { KL_INST(128) }
+#undef KL_INST
+    return nullptr;
 }
 
 // Repack row-major bf16 matrices into 8x64 tiles.  rowmap[packed row] =
@@ -982,24 +992,28 @@ __global__ void kl_gain_to_f32_kernel(float *dst, const uint16_t *src, int n, in
 
 // ---------------------------------------------------------------- launchers
 
-hipError_t step_kernel_setup(int lds_bytes, int *max_blocks_per_cu) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kl_step_kernel),
+hipError_t step_kernel_setup(int d, int group, int lds_bytes, int *max_blocks_per_cu) {
+    const StepKernel k = step_kernel_for(d, group);
+    if (!k) return hipErrorInvalidValue;
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(k),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes);
     if (e != hipSuccess) return e;
-    return hipOccupancyMaxActiveBlocksPerMultiprocessor(max_blocks_per_cu, kl_step_kernel,
-                                                         kThreads, lds_bytes);
+    return hipOccupancyMaxActiveBlocksPerMultiprocessor(max_blocks_per_cu, k, kThreads,
+                                                         lds_bytes);
 }
 
 hipError_t launch_step(const StepParams &p, int first_layer, int last_layer, int phases,
                        bool cooperative, int lds_bytes, hipStream_t stream) {
+    const StepKernel k = step_kernel_for(p.d, p.group);
+    if (!k) return hipErrorInvalidValue;
     StepParams pc = p;
     if (cooperative) {
         void *args[] = {&pc, &first_layer, &last_layer, &phases};
-        return hipLaunchCooperativeKernel(reinterpret_cast<const void *>(kl_step_kernel),
-                                          dim3(p.nwg), dim3(kThreads), args, lds_bytes, stream);
+        return hipLaunchCooperativeKernel(reinterpret_cast<const void *>(k), dim3(p.nwg),
+                                          dim3(kThreads), args, lds_bytes, stream);
     }
-    hipLaunchKernelGGL(kl_step_kernel, dim3(p.nwg), dim3(kThreads), lds_bytes, stream, pc,
-                       first_layer, last_layer, phases);
+    hipLaunchKernelGGL(k, dim3(p.nwg), dim3(kThreads), lds_bytes, stream, pc, first_layer,
+                       last_layer, phases);
     return hipGetLastError();
 }
 

@@ -260,7 +260,7 @@ kl_status kl_load_model(const kl_config *cfg, const kl_weight_ptrs *w, void *str
     if (S->lds_bytes > 160 * 1024 - 256)
         return bail(fail(KL_ERR_UNSUPPORTED, "LDS need %d bytes exceeds 160 KiB", S->lds_bytes));
     int per_cu = 0;
-    TRY(step_kernel_setup(S->lds_bytes, &per_cu));
+    TRY(step_kernel_setup(c.head_dim, c.n_heads / c.n_kv_heads, S->lds_bytes, &per_cu));
     if (per_cu < 1) return bail(fail(KL_ERR_UNSUPPORTED, "step kernel does not fit on a CU"));
 
     // scratch

@@ -70,7 +70,7 @@ struct StepParams {
 
 hipError_t launch_step(const StepParams &p, int first_layer, int last_layer, int phases,
                        bool cooperative, int lds_bytes, hipStream_t stream);
-hipError_t step_kernel_setup(int lds_bytes, int *max_blocks_per_cu);
+hipError_t step_kernel_setup(int d, int group, int lds_bytes, int *max_blocks_per_cu);
 
 hipError_t launch_pack_rows(uint16_t *dst, int n_rg, int kt, int K, const int32_t *rowmap,
                             const uint16_t *src0, const uint16_t *src1, const uint16_t *src2,
