@@ -146,17 +146,18 @@ kl_status kl_get_device_error(kl_state *st, int32_t *code);
 
 kl_status kl_get_info(const kl_state *st, kl_info *info);
 
-/* Timeline of the grid barriers, for profiling the schedules (the kind of
+/* Timeline of the phases, for profiling the schedules (the kind of
  * synchronization-cost breakdown of Sec. 2, Fig. 5).  While a buffer is set,
- * every later step writes, for barrier k < max_barriers of each launch and
- * workgroup w, three s_memrealtime stamps (100 MHz ticks) into
- *   dev_buffer[(k * n_workgroups + w) * 4 + {0: arrival, 1: wait start, 2: wait end}]
- * and, for an attention phase arriving on barrier k, slot 3 = the moment its
- * chunk result is ready, before the chunks are combined (a launch overwrites
- * the previous launch's entries).  The
- * buffer (dev, uint64, max_barriers * n_workgroups * 4 entries) stays owned by
- * the caller; pass NULL to stop tracing. */
-kl_status kl_set_trace(kl_state *st, uint64_t *dev_buffer, int32_t max_barriers);
+ * every later launch writes, for phase i < max_phases of the launch (in the
+ * order embed, then qkv, attn, oproj, gateup, down per layer, then head) and
+ * workgroup w, s_memrealtime stamps (100 MHz ticks) into
+ *   dev_buffer[(i * n_workgroups + w) * 4 + {0: phase end, 1: start of the
+ *   wait for its inputs, 2: end of that wait, 3: attention result published}]
+ * (slots a workgroup does not reach keep their old contents; a launch
+ * overwrites the previous launch's entries).  The buffer (dev, uint64,
+ * max_phases * n_workgroups * 4 entries) stays owned by the caller; pass NULL
+ * to stop tracing. */
+kl_status kl_set_trace(kl_state *st, uint64_t *dev_buffer, int32_t max_phases);
 
 /* Frees everything the state owns (synchronizes the device first). NULL is a no-op. */
 void kl_free_model(kl_state *st);

@@ -161,8 +161,8 @@ def kl_get_info(state: int) -> kl_info:
     return info
 
 
-def kl_set_trace(state: int, dev_buffer: int | None, max_barriers: int) -> None:
-    _check(lib().kl_set_trace(state, dev_buffer, max_barriers))
+def kl_set_trace(state: int, dev_buffer: int | None, max_phases: int) -> None:
+    _check(lib().kl_set_trace(state, dev_buffer, max_phases))
 
 
 def kl_free_model(state: int) -> None:

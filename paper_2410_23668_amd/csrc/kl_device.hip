@@ -127,12 +127,26 @@ __device__ __forceinline__ void st_dev_u16(uint16_t *p, uint16_t v) {
 __device__ __forceinline__ void st_dev_u32(unsigned *p, unsigned v) {
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-// x += v performed at the device-coherent level, without returning the old
-// value (nothing waits for it until the store drain before a barrier
-// arrival).  Each residual element has exactly one adder per phase, so the
-// result is x + v rounded once, independent of timing.
-__device__ __forceinline__ void add_dev(float *p, float v) {
-    __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+// The residual stream is kept in fixed point: int64 in units of 2^-32.  Every
+// contribution (the embedding, each O-projection partial, each
+// down-projection partial) is rounded once to that grid and added with an
+// integer atomic, so the sum is exact and independent of the order in which
+// workgroups add: results are reproducible however the work is split.  The
+// range (+-2^31) and resolution (2^-32) are far beyond fp32 activations'.
+constexpr double kFixScale = 4294967296.0;   // 2^32
+__device__ __forceinline__ long long to_fix(float v) {
+    return __double2ll_rn((double)v * kFixScale);
+}
+__device__ __forceinline__ float from_fix(long long v) {
+    return (float)v * (1.0f / 4294967296.0f);
+}
+__device__ __forceinline__ void add_fix(long long *p, float v) {
+    __hip_atomic_fetch_add(reinterpret_cast<unsigned long long *>(p),
+                           (unsigned long long)to_fix(v), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_dev_u64(unsigned long long *p, unsigned long long v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 __device__ __forceinline__ float ld_dev(const float *p) {
     return __hip_atomic_load(const_cast<float *>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -199,11 +213,13 @@ __device__ __forceinline__ void bar_init(const StepParams &P) {
     __syncthreads();
 }
 
-// Optional timeline: thread 0 of every workgroup stamps (s_memrealtime, 100 MHz)
-// its arrival at barrier k, the start of its wait on k and the end of that wait.
-__device__ __forceinline__ void trace_stamp(const StepParams &P, int k, int what) {
-    if (P.trace && k < P.trace_max)
-        P.trace[((size_t)k * P.nwg + blockIdx.x) * 4 + what] = wall_clock64();
+// Optional timeline: the control wave of every workgroup stamps
+// (s_memrealtime, 100 MHz) the end of phase i of the launch (slot 0), the
+// start and end of phase i's wait for its inputs (slots 1, 2) and, for an
+// attention phase, the moment its last chunk result is published (slot 3).
+__device__ __forceinline__ void trace_stamp(const StepParams &P, int i, int what) {
+    if (P.trace && i >= 0 && i < P.trace_max)
+        P.trace[((size_t)i * P.nwg + blockIdx.x) * 4 + what] = wall_clock64();
 }
 
 // The control wave (kCtlWave) does all of a workgroup's barrier traffic.  It
@@ -211,13 +227,28 @@ __device__ __forceinline__ void trace_stamp(const StepParams &P, int k, int what
 // the compute waves' prefetches (a wave's loads complete in issue order).
 __device__ __forceinline__ bool is_ctl_lane0() { return threadIdx.x == kCtlWave * 64; }
 
-__device__ __forceinline__ void bar_arrive(const StepParams &P, int k) {
-    if (is_ctl_lane0()) trace_stamp(P, k, 0);
+// Every wave drains its stores (they must be visible before the signal),
+// then the control wave signals.
+__device__ __forceinline__ void drain_all() {
     wait_stores();
     __syncthreads();
+}
+
+// Arrival on grid barrier k after phase ti.
+__device__ __forceinline__ void bar_arrive(const StepParams &P, int k, int ti) {
+    if (is_ctl_lane0()) trace_stamp(P, ti, 0);
+    drain_all();
     if (is_ctl_lane0())
         __hip_atomic_fetch_add(bar_counter(P, blockIdx.x % bar_groups(P)), 1ull,
                                __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Arrival on a local counter (one add per arriving workgroup) after phase ti.
+__device__ __forceinline__ void local_arrive(const StepParams &P, unsigned *cnt, int ti) {
+    if (is_ctl_lane0()) trace_stamp(P, ti, 0);
+    drain_all();
+    if (is_ctl_lane0())
+        __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Spin until *flag_fn() says done; gives up (raising KL_DEVERR_BARRIER) after
@@ -239,18 +270,33 @@ __device__ __forceinline__ void spin_until(const StepParams &P, Done &&done) {
     }
 }
 
-__device__ __forceinline__ void bar_wait(const StepParams &P, int k) {
+__device__ __forceinline__ void bar_wait(const StepParams &P, int k, int ti) {
     if ((threadIdx.x >> 6) == kCtlWave) {
         const int lane = threadIdx.x & 63, ng = bar_groups(P);
         const bool mine = lane < ng;
         const unsigned long long target =
             mine ? bar_bases(P)[lane] + (unsigned long long)(k + 1) * bar_gsize(P, ng, lane) : 0ull;
-        if (lane == 0) trace_stamp(P, k, 1);
+        if (lane == 0) trace_stamp(P, ti, 1);
         spin_until(P, [&]() {
             const bool d = !mine || (long long)(ld_dev_u64(bar_counter(P, lane)) - target) >= 0;
             return __all(d) != 0;
         });
-        if (lane == 0) trace_stamp(P, k, 2);
+        if (lane == 0) trace_stamp(P, ti, 2);
+    }
+    __syncthreads();
+}
+
+// Wait until a local counter (monotonic within a step; zeroed by the
+// embedding phase) reaches target.
+__device__ __forceinline__ void local_wait(const StepParams &P, const unsigned *cnt,
+                                           unsigned target, int ti) {
+    if (is_ctl_lane0()) {
+        trace_stamp(P, ti, 1);
+        spin_until(P, [&]() {
+            return (int)(__hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) -
+                         target) >= 0;
+        });
+        trace_stamp(P, ti, 2);
     }
     __syncthreads();
 }
@@ -316,27 +362,46 @@ __device__ __forceinline__ unsigned long long *bar_bases(const StepParams &P) {
 
 // ---------------------------------------------------------------- activations
 
-// Copy a device-coherent fp32 vector of n (even) values into LDS, zero up to npad.
+// Copy a device-coherent fp32 vector of n values into LDS, zero up to npad
+// (loads are issued in batches of kStageBatch per thread before any is used).
+constexpr int kStageBatch = 8;
 __device__ __forceinline__ void stage_vec(const float *__restrict__ src, int n, int npad,
                                           float *a) {
-    for (int i = threadIdx.x; 2 * i < npad; i += kThreads) {
-        float lo = 0.f, hi = 0.f;
-        if (2 * i < n) {
-            const unsigned long long v = ld_dev_u64(src + 2 * i);
-            lo = __uint_as_float((unsigned)v);
-            hi = __uint_as_float((unsigned)(v >> 32));
+    for (int i0 = threadIdx.x; i0 < npad; i0 += kStageBatch * kThreads) {
+        float v[kStageBatch];
+#pragma unroll
+        for (int k = 0; k < kStageBatch; ++k) {
+            const int i = i0 + k * kThreads;
+            v[k] = i < n ? ld_dev(src + i) : 0.f;
         }
-        a[2 * i] = lo;
-        a[2 * i + 1] = hi;
+#pragma unroll
+        for (int k = 0; k < kStageBatch; ++k) {
+            const int i = i0 + k * kThreads;
+            if (i < npad) a[i] = v[k];
+        }
     }
     __syncthreads();
 }
 
-// a[i] = x[i] * rsqrt(mean(x^2) + eps) * gain[i] for i < n, 0 up to npad.
-__device__ __forceinline__ void stage_rmsnorm(const float *__restrict__ x,
+// a[i] = x[i] * rsqrt(mean(x^2) + eps) * gain[i] for i < n, 0 up to npad,
+// x read from the fixed-point residual stream.
+__device__ __forceinline__ void stage_rmsnorm(const long long *__restrict__ xf,
                                               const float *__restrict__ gain, int n, int npad,
                                               float eps, float *a, float *sm) {
-    stage_vec(x, n, npad, a);
+    for (int i0 = threadIdx.x; i0 < npad; i0 += kStageBatch * kThreads) {
+        long long v[kStageBatch];
+#pragma unroll
+        for (int k = 0; k < kStageBatch; ++k) {
+            const int i = i0 + k * kThreads;
+            v[k] = i < n ? (long long)ld_dev_u64(xf + i) : 0ll;
+        }
+#pragma unroll
+        for (int k = 0; k < kStageBatch; ++k) {
+            const int i = i0 + k * kThreads;
+            if (i < npad) a[i] = from_fix(v[k]);
+        }
+    }
+    __syncthreads();
     float ss = 0.f;
     for (int i = threadIdx.x; i < n; i += kThreads) ss = fmaf(a[i], a[i], ss);
     ss = block_sum(ss, sm);
@@ -377,27 +442,36 @@ __device__ __forceinline__ RgRange own_rgs(int nrg, const StepParams &P) {
     return RgRange{a, b - a};
 }
 
-template <class Wait, class Stage, class Epi>
-__device__ __forceinline__ void gemv_phase(const uint8_t *__restrict__ W, int KT, int first,
-                                           int count, int stride, int B,
-                                           const float *__restrict__ a, float *red,
-                                           const uint8_t *dummy, Wait &&wait, Stage &&stage,
-                                           Epi &&epi) {
+// Two ways to share a row group's tiles among the waves:
+//   split-K   (long rows, KT >= 2 kWaves): wave w takes the k-tiles
+//             [w KT / kWaves, (w + 1) KT / kWaves) of every row group; the
+//             wave partial sums are added in wave order through LDS;
+//   row-split (short rows): wave w takes whole row groups w, w + kWaves, ...
+//             of the batch and needs no cross-wave sum.
+// Both orders are fixed by the partition alone.
+template <bool RowSplit, class Wait, class Stage, class Epi>
+__device__ __forceinline__ void gemv_rows(const uint8_t *__restrict__ W, int KT, int first,
+                                          int count, int stride, int B,
+                                          const float *__restrict__ a, float *red,
+                                          const uint8_t *dummy, Wait &&wait, Stage &&stage,
+                                          Epi &&epi) {
     constexpr int U = kGemvDepth;
+    constexpr int BATCH = RowSplit ? kWaves * kRgBatch : kRgBatch;   // row groups per LDS round
     // wave-uniform values live in scalar registers, so every branch below is
     // a scalar branch
     const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
     const int row = lane >> 3, sub = lane & 7;
-    const int kt0 = (wid * KT) / kWaves;
-    const int nk = ((wid + 1) * KT) / kWaves - kt0;
+    const int kt0 = RowSplit ? 0 : (wid * KT) / kWaves;
+    const int nk = RowSplit ? KT : ((wid + 1) * KT) / kWaves - kt0;
+    const int rstep = RowSplit ? kWaves : 1;   // a wave's next row group, in batch items
     const uint8_t *base = W + (size_t)lane * 16;
     const float *abase = a + sub * 8;
     u32x4 buf[U];
     int n = 0, ltile = 0, lk = 0, left = 0;   // batch items; next tile, its k index; tiles left
 
     // from a wave's last tile of one row group to its first of the next
-    const int jump = (stride - 1) * KT + (KT - nk) + 1;
+    const int jump = (rstep * stride - 1) * KT + (KT - nk) + 1;
     // load the next tile of the batch, or the dummy line (branch-free)
     auto load_next = [&]() {
         const int t = __builtin_amdgcn_readfirstlane(ltile);
@@ -409,10 +483,12 @@ __device__ __forceinline__ void gemv_phase(const uint8_t *__restrict__ W, int KT
         left = real ? left - 1 : left;
         return v;
     };
-    auto start = [&](int ib) {   // batch of items ib .. ib + kRgBatch - 1
-        n = nk * min(kRgBatch, count - ib);
+    auto start = [&](int ib) {   // batch of row groups ib .. ib + BATCH - 1
+        const int nb = min(BATCH, count - ib);
+        const int mine = RowSplit ? (nb > wid ? (nb - wid + kWaves - 1) / kWaves : 0) : nb;
+        n = nk * mine;
         left = n;
-        ltile = (first + ib * stride) * KT + kt0;
+        ltile = (first + (ib + (RowSplit ? wid : 0)) * stride) * KT + kt0;
         lk = 0;
 #pragma unroll
         for (int s = 0; s < U; ++s) buf[s] = load_next();
@@ -425,11 +501,11 @@ __device__ __forceinline__ void gemv_phase(const uint8_t *__restrict__ W, int KT
     wait();
     if (!has_rows) return;
     for (int b = 0; b < B; ++b) {
-        for (int ib = 0; ib < count; ib += kRgBatch) {
+        for (int ib = 0; ib < count; ib += BATCH) {
             if ((b > 0 || ib > 0) && compute) start(ib);
             if (ib == 0) stage(b);
-            const int nrg = min(kRgBatch, count - ib);
-            int cr = 0, ck = 0;
+            const int nrg = min(BATCH, count - ib);
+            int cr = RowSplit ? wid : 0, ck = 0;   // batch item of the row group in progress
             float acc = 0.f;
             // item i sits in slot i % U and is refilled with item i + U (or
             // the dummy line) right after it is consumed
@@ -452,10 +528,13 @@ __device__ __forceinline__ void gemv_phase(const uint8_t *__restrict__ W, int KT
                         acc = fmaf(bf_hi(wv.w), a1.w, acc);
                         if (++ck == nk) {
                             const float t = sum8(acc);
-                            if (sub == 0) red[(wid * kRgBatch + cr) * kTileRows + row] = t;
+                            if (sub == 0) {
+                                if (RowSplit) red[cr * kTileRows + row] = t;
+                                else red[(wid * kRgBatch + cr) * kTileRows + row] = t;
+                            }
                             acc = 0.f;
                             ck = 0;
-                            ++cr;
+                            cr += rstep;
                         }
                     }
                     buf[s] = load_next();
@@ -465,10 +544,15 @@ __device__ __forceinline__ void gemv_phase(const uint8_t *__restrict__ W, int KT
             for (int t = threadIdx.x; t < nrg * (kTileRows / 2); t += kThreads) {
                 const int rgi = t / (kTileRows / 2), pr = (t % (kTileRows / 2)) * 2;
                 float y0 = 0.f, y1 = 0.f;
-                for (int w = 0; w < kWaves; ++w) {
-                    if (((w + 1) * KT) / kWaves == (w * KT) / kWaves) continue;   // empty slice
-                    y0 += red[(w * kRgBatch + rgi) * kTileRows + pr];
-                    y1 += red[(w * kRgBatch + rgi) * kTileRows + pr + 1];
+                if (RowSplit) {
+                    y0 = red[rgi * kTileRows + pr];
+                    y1 = red[rgi * kTileRows + pr + 1];
+                } else {
+                    for (int w = 0; w < kWaves; ++w) {
+                        if (((w + 1) * KT) / kWaves == (w * KT) / kWaves) continue;   // empty slice
+                        y0 += red[(w * kRgBatch + rgi) * kTileRows + pr];
+                        y1 += red[(w * kRgBatch + rgi) * kTileRows + pr + 1];
+                    }
                 }
                 epi(b, (first + (ib + rgi) * stride) * kTileRows + pr, y0, y1);
             }
@@ -477,17 +561,43 @@ __device__ __forceinline__ void gemv_phase(const uint8_t *__restrict__ W, int KT
     }
 }
 
+// Row groups are shared split-K when they are long enough for every wave to
+// hold two or more tiles, else row-split.
+template <class Wait, class Stage, class Epi>
+__device__ __forceinline__ void gemv_phase(const uint8_t *__restrict__ W, int KT, int first,
+                                           int count, int stride, int B,
+                                           const float *__restrict__ a, float *red,
+                                           const uint8_t *dummy, Wait &&wait, Stage &&stage,
+                                           Epi &&epi) {
+    if (KT >= 2 * kWaves)
+        gemv_rows<false>(W, KT, first, count, stride, B, a, red, dummy, wait, stage, epi);
+    else
+        gemv_rows<true>(W, KT, first, count, stride, B, a, red, dummy, wait, stage, epi);
+}
+
 // ---------------------------------------------------------------- phases
 //
-// Every phase takes (wait, arrive): the barrier index to wait on before its
-// inputs are read (-1: none, the inputs come from an earlier launch) and the
-// barrier index to arrive on after its outputs are written (-1: none).
+// Synchronization between the phases of a layer (l):
+//   grid barrier   after embed, oproj and down: the residual stream is
+//                  complete; qkv, gateup and head wait on it.
+//   cnt_qkv[g]     qkv -> attn: the workgroups of KV head g compute exactly
+//                  the q/k/v rows of that head, so the attention of head g
+//                  waits only for them (Sg arrivals per layer).
+//   cnt_attn[g]    attn -> oproj: the chunk results of KV head g (B * C per
+//                  layer); the same workgroups then merge them and apply the
+//                  O-projection columns of head g, adding into the residual.
+//   cnt_gu[j]      gateup -> down: column block j of the FFN (Rc workgroups
+//                  compute its SwiGLU values; the same Rc workgroups then
+//                  apply the matching columns of the down projection).
+// Local counters grow monotonically within a step (zeroed by the embedding
+// phase); their targets are (l + 1) times the arrivals per layer.
+// Every workgroup arrives on, and waits on, every grid barrier.
 
-// Embedding block (Sec. 2): x = f32(E[token]).  Workgroup 0 records bad
-// token ids and positions in the device error word.
-__device__ __forceinline__ void phase_embed(KArg ka, int wait, int arrive) {
+// Embedding block (Sec. 2): x = E[token] (exact in fixed point).  Workgroup 0
+// records bad token ids and positions, and zeroes the local counters.
+__device__ __forceinline__ void phase_embed(KArg ka, int gwait, int garrive, int ti) {
     const StepParams P = load_params(ka);
-    if (wait >= 0) bar_wait(P, wait);
+    if (gwait >= 0) bar_wait(P, gwait, ti);
     if (blockIdx.x == 0) {
         for (int b = threadIdx.x; b < P.B; b += kThreads) {
             const int t = P.tokens[b], p = P.positions[b];
@@ -496,56 +606,62 @@ __device__ __forceinline__ void phase_embed(KArg ka, int wait, int arrive) {
             if (p < 0 || p >= P.cap || p >= P.max_seq) bits |= KL_DEVERR_POSITION;
             if (bits) atomicOr(P.err, bits);
         }
-    }
-    if (blockIdx.x == 0) {
-        for (int i = threadIdx.x; i < P.B * P.nkv; i += kThreads)
+        for (int i = threadIdx.x; i < 2 * P.nkv + P.Sc; i += kThreads)
             __hip_atomic_store(P.cnt + i, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
     const int total = P.B * P.Hp;
     for (int idx = blockIdx.x * kThreads + threadIdx.x; idx < total; idx += P.nwg * kThreads) {
         const int b = idx / P.Hp, i = idx % P.Hp;
-        st_dev(P.x + idx, (i < P.H) ? bf2f(P.embed[(size_t)eff_tok(P, b) * P.H + i]) : 0.f);
+        const float e = (i < P.H) ? bf2f(P.embed[(size_t)eff_tok(P, b) * P.H + i]) : 0.f;
+        st_dev_u64(reinterpret_cast<unsigned long long *>(P.xf + idx),
+                   (unsigned long long)to_fix(e));
     }
-    if (arrive >= 0) bar_arrive(P, arrive);
+    if (garrive >= 0) bar_arrive(P, garrive, ti);
 }
 
-// RMSNorm + fused Q/K/V projection + RoPE + KV-cache append.  Q/K rows are
-// packed in rotation pairs (dims i and i + d/2 adjacent), V rows in order.
-__device__ __forceinline__ void phase_qkv(KArg ka, int l, int wait, int arrive) {
+// RMSNorm + Q/K/V projection of KV head g + RoPE + KV-cache append.  The rows
+// of head g's block are: its G query heads, then its key, then its value
+// head; query and key rows are packed in rotation pairs (dims i, i + d/2).
+__device__ __forceinline__ void phase_qkv(KArg ka, int l, int gwait, int ti) {
     const StepParams P = load_params(ka);
     const Lds S = lds_layout(kl_smem, P);
-    const RgRange R = own_rgs(P.qkv_rg, P);
+    const int g = blockIdx.x / P.Sg, part = blockIdx.x % P.Sg;
+    const bool member = g < P.nkv;
+    int a0 = 0, a1 = 0;
+    if (member) split_range(P.qkv_rg, P.Sg, part, a0, a1);
     const uint8_t *Lb = P.arena + (size_t)l * P.layer_stride;
     const float *gain = reinterpret_cast<const float *>(Lb + P.off_attn_norm);
-    const int d = P.d, half = P.d / 2, qd = P.nq * P.d, kd = P.nkv * P.d;
+    const int d = P.d, half = P.d / 2, G = P.group;
+    const int row0 = g * P.qkv_rg * kTileRows;   // first packed row of head g's block
     gemv_phase(
-        Lb + P.off_qkv, P.Hp / kTileK, R.first, R.count, 1, P.B, S.a, S.red, P.dummy,
-        [&]() { if (wait >= 0) bar_wait(P, wait); },
-        [&](int b) { stage_rmsnorm(P.x + (size_t)b * P.Hp, gain, P.H, P.Hp, P.eps, S.a, S.sm); },
+        Lb + P.off_qkv, P.Hp / kTileK, g * P.qkv_rg + a0, a1 - a0, 1, P.B, S.a, S.red, P.dummy,
+        [&]() { if (gwait >= 0) bar_wait(P, gwait, ti); },
+        [&](int b) { stage_rmsnorm(P.xf + (size_t)b * P.Hp, gain, P.H, P.Hp, P.eps, S.a, S.sm); },
         [&](int b, int r, float y0, float y1) {
             const int p = eff_pos(P, b);
-            if (r < qd + kd) {
-                const int h = r / d, i = (r % d) >> 1;
+            const int lr = r - row0;
+            if (lr < (G + 1) * d) {
+                const int i = (lr % d) >> 1;
                 const float2 cs = P.rope[(size_t)p * half + i];
                 const float u0 = y0 * cs.x - y1 * cs.y;
                 const float u1 = y0 * cs.y + y1 * cs.x;
-                if (r < qd) {
-                    float *qq = P.q + (size_t)b * qd + (size_t)h * d;
+                if (lr < G * d) {
+                    float *qq = P.q + (size_t)b * P.nq * d + (size_t)(g * G + lr / d) * d;
                     st_dev(qq + i, u0);
                     st_dev(qq + i + half, u1);
                 } else {
-                    uint16_t *kk = P.kc + (kv_row(P, l, b, h - P.nq) + p) * d;
+                    uint16_t *kk = P.kc + (kv_row(P, l, b, g) + p) * d;
                     st_dev_u16(kk + i, f2bf(u0));
                     st_dev_u16(kk + i + half, f2bf(u1));
                 }
             } else {
-                const int rr = r - qd - kd, g = rr / d, j = rr % d;
+                const int j = lr - (G + 1) * d;
                 uint16_t *vv = P.vc + (kv_row(P, l, b, g) + p) * d;
                 st_dev_u32(reinterpret_cast<unsigned *>(vv + j),
                            (unsigned)f2bf(y0) | ((unsigned)f2bf(y1) << 16));
             }
         });
-    if (arrive >= 0) bar_arrive(P, arrive);
+    if (member) local_arrive(P, P.cnt + g, ti);
 }
 
 // One attention work item: chunk c of sequence b against KV head g, for the
@@ -564,7 +680,8 @@ template <int D>
 constexpr int attn_sub() { return kWaves * kAttnLoads * (64 / (D / 8)); }
 
 template <int D, int G>
-__device__ __forceinline__ void attn_item(KArg ka, int l, int b, int g, int c, int wait) {
+__device__ __forceinline__ void attn_item(KArg ka, int l, int b, int g, int c, bool first,
+                                          int ti) {
     const StepParams P = load_params(ka);
     const Lds S = lds_layout(kl_smem, P);
     constexpr int LP = D / 8;                       // lanes per position
@@ -616,7 +733,7 @@ __device__ __forceinline__ void attn_item(KArg ka, int l, int b, int g, int c, i
         }
     };
     issue(j0, min(SUB, j1 - j0));
-    if (wait >= 0) bar_wait(P, wait);
+    if (first) local_wait(P, P.cnt + g, (unsigned)(l + 1) * (unsigned)P.Sg, ti);
     fetch_new(j0, min(SUB, j1 - j0));
     for (int t = threadIdx.x; t < G * D; t += kThreads)
         qs[t] = ld_dev(P.q + (size_t)b * P.nq * D + (size_t)g * G * D + t);
@@ -731,65 +848,66 @@ __device__ __forceinline__ void attn_item(KArg ka, int l, int b, int g, int c, i
         }
     }
     __syncthreads();
-    float *o_bg = P.o + (size_t)b * P.Ap + (size_t)g * G * D;
-    const int C = P.C;
-    if (C == 1) {
-        // a single chunk: normalise and write o directly
-        for (int t = threadIdx.x; t < G * D; t += kThreads) {
-            const int h = t / D, dd = t % D;
-            float s = 0.f;
-            for (int w = 0; w < kWaves; ++w) s += red[(w * G + h) * D + dd];
-            st_dev(o_bg + t, s / st[h * 4 + 1]);
-        }
-        if (is_ctl_lane0() && wait >= 0) trace_stamp(P, wait + 1, 3);
-        __syncthreads();
-        return;
-    }
-    float *part_bg = P.part + (size_t)(b * P.nkv + g) * C * G * (D + 2);
-    float *out = part_bg + (size_t)c * G * (D + 2);
+    // publish: unnormalised outputs [G][D] and (max, sum) per head
+    const size_t item = ((size_t)b * P.nkv + g) * P.C + c;
+    float *out = P.part_o + item * G * D;
+    float *sts = P.part_s + item * G * 2;
     for (int t = threadIdx.x; t < G * D; t += kThreads) {
         const int h = t / D, dd = t % D;
         float s = 0.f;
         for (int w = 0; w < kWaves; ++w) s += red[(w * G + h) * D + dd];
-        st_dev(out + h * (D + 2) + dd, s);
+        st_dev(out + t, s);
     }
     if (threadIdx.x < G) {
-        st_dev(out + threadIdx.x * (D + 2) + D, st[threadIdx.x * 4 + 0]);
-        st_dev(out + threadIdx.x * (D + 2) + D + 1, st[threadIdx.x * 4 + 1]);
+        st_dev(sts + threadIdx.x * 2, st[threadIdx.x * 4 + 0]);
+        st_dev(sts + threadIdx.x * 2 + 1, st[threadIdx.x * 4 + 1]);
     }
-    // Publish this chunk; the workgroup whose arrival completes the count
-    // merges all chunks.  The per-(b, g) counter is zeroed by the embedding
-    // phase and grows by C per layer.
-    if (is_ctl_lane0() && wait >= 0) trace_stamp(P, wait + 1, 3);
-    wait_stores();
-    __syncthreads();
-    int *flag = reinterpret_cast<int *>(S.sm);
-    if (is_ctl_lane0()) {
-        const unsigned old = __hip_atomic_fetch_add(P.cnt + b * P.nkv + g, 1u, __ATOMIC_RELAXED,
-                                                    __HIP_MEMORY_SCOPE_AGENT);
-        flag[0] = (old == (unsigned)(l + 1) * (unsigned)C - 1u) ? 1 : 0;
-    }
-    __syncthreads();
-    if (!flag[0]) return;
-    // merge: every thread owns outputs j (of G*D); its loads of all chunks'
-    // partial outputs are issued together with the statistics loads
-    float *cM = S.attn, *cL = cM + C * G, *cW = cL + C * G, *cT = cW + C * G;
+    if (is_ctl_lane0()) trace_stamp(P, ti, 3);
+    drain_all();
+    if (is_ctl_lane0())
+        __hip_atomic_fetch_add(P.cnt + P.nkv + g, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Attention of KV head g: the workgroups of head g take its items (sequence b,
+// chunk c) round-robin.
+template <int D, int G>
+__device__ __forceinline__ void phase_attn(KArg ka, int l, int ti) {
+    const StepParams P = load_params(ka);
+    const int g = blockIdx.x / P.Sg, part = blockIdx.x % P.Sg;
+    if (g >= P.nkv) return;
+    const int items = P.B * P.C;
+    for (int it = part; it < items; it += P.Sg)
+        attn_item<D, G>(ka, l, it / P.C, g, it % P.C, it == part, ti);
+    if (is_ctl_lane0()) trace_stamp(P, ti, 0);
+}
+
+// Merge the C chunk results of (sequence b, KV head g) in chunk order into
+// o[G * D] (LDS): o_h = sum_c w_ch A_ch / sum_c w_ch L_ch, w_ch = exp(M_ch - M_h).
+// Every thread owns outputs j; its loads of all chunks' values for j are
+// issued together (batches of kCombBatch) with the statistics loads.
+template <int D, int G>
+__device__ __forceinline__ void merge_chunks(const StepParams &P, int b, int g, float *o,
+                                             float *scratch) {
+    const int C = P.C;
+    const size_t item0 = ((size_t)b * P.nkv + g) * C;
+    const float *po = P.part_o + item0 * G * D;
+    const float *ps = P.part_s + item0 * G * 2;
+    float *cM = scratch, *cL = cM + C * G, *cW = cL + C * G, *cT = cW + C * G;
     for (int j = threadIdx.x; j - (int)threadIdx.x < G * D; j += kThreads) {
         const bool jv = j < G * D;
-        const int h = jv ? j / D : 0, dd = jv ? j % D : 0;
+        const int h = jv ? j / D : 0;
         float num = 0.f;
         for (int c0 = 0; c0 < C; c0 += kCombBatch) {
             float av[kCombBatch];
 #pragma unroll
             for (int k = 0; k < kCombBatch; ++k)
-                av[k] = (jv && c0 + k < C)
-                            ? ld_dev(part_bg + ((size_t)(c0 + k) * G + h) * (D + 2) + dd)
-                            : 0.f;
+                av[k] = (jv && c0 + k < C) ? ld_dev(po + (size_t)(c0 + k) * G * D + j) : 0.f;
             if (j == (int)threadIdx.x && c0 == 0) {
                 // (first pass only, uniform across the block)
                 for (int t = threadIdx.x; t < C * G; t += kThreads) {
-                    cM[t] = ld_dev(part_bg + (size_t)t * (D + 2) + D);
-                    cL[t] = ld_dev(part_bg + (size_t)t * (D + 2) + D + 1);
+                    const unsigned long long v = ld_dev_u64(ps + (size_t)t * 2);
+                    cM[t] = __uint_as_float((unsigned)v);
+                    cL[t] = __uint_as_float((unsigned)(v >> 32));
                 }
                 __syncthreads();
                 for (int t = threadIdx.x; t < C * G; t += kThreads) {
@@ -811,130 +929,151 @@ __device__ __forceinline__ void attn_item(KArg ka, int l, int b, int g, int c, i
             for (int k = 0; k < kCombBatch; ++k)
                 if (c0 + k < C) num = fmaf(av[k], cW[(c0 + k) * G + h], num);
         }
-        if (jv) st_dev(o_bg + j, num / cT[h]);
+        if (jv) o[j] = num / cT[h];
     }
     __syncthreads();
 }
 
+// O projection of KV head g: x += Wo[:, columns of head g] o_g, for the rows
+// this workgroup owns among head g's workgroups, added into the fixed-point
+// residual.  The chunk merge is the activation staging of this GEMV.
 template <int D, int G>
-__device__ __forceinline__ void phase_attn(KArg ka, int l, int wait, int arrive) {
+__device__ __forceinline__ void phase_oproj(KArg ka, int l, int garrive, int ti) {
     const StepParams P = load_params(ka);
-    const int items = P.B * P.nkv * P.C;
-    bool waited = wait < 0;
-    for (int it = blockIdx.x; it < items; it += P.nwg) {
-        const int c = it % P.C, bg = it / P.C, g = bg % P.nkv, b = bg / P.nkv;
-        attn_item<D, G>(ka, l, b, g, c, waited ? -1 : wait);
-        waited = true;
+    const Lds S = lds_layout(kl_smem, P);
+    const int g = blockIdx.x / P.Sg, part = blockIdx.x % P.Sg;
+    if (g < P.nkv) {
+        int a0, a1;
+        split_range(P.o_rg, P.Sg, part, a0, a1);
+        const int KT = G * D / kTileK;
+        const uint8_t *W = P.arena + (size_t)l * P.layer_stride + P.off_o +
+                           (size_t)g * P.o_rg * KT * kTileBytes;
+        const unsigned target = (unsigned)(l + 1) * (unsigned)(P.B * P.C);
+        gemv_phase(
+            W, KT, a0, a1 - a0, 1, P.B, S.a, S.red, P.dummy,
+            [&]() { local_wait(P, P.cnt + P.nkv + g, target, ti); },
+            [&](int b) { merge_chunks<D, G>(P, b, g, S.a, S.a + G * D); },
+            [&](int b, int r, float y0, float y1) {
+                long long *x = P.xf + (size_t)b * P.Hp;
+                add_fix(x + r, y0);
+                add_fix(x + r + 1, y1);
+            });
     }
-    if (!waited) bar_wait(P, wait);
-    if (arrive >= 0) bar_arrive(P, arrive);
+    if (garrive >= 0) bar_arrive(P, garrive, ti);
 }
 
-// O projection + residual: x += Wo o (each row has one owner).
-__device__ __forceinline__ void phase_oproj(KArg ka, int l, int wait, int arrive) {
+// RMSNorm + gate/up projection + SwiGLU for FFN column block j = w / Rc:
+// m = silu(Wg u) * (Wu u).  Packed rows alternate gate i, up i.
+__device__ __forceinline__ void phase_gateup(KArg ka, int l, int gwait, int ti) {
     const StepParams P = load_params(ka);
     const Lds S = lds_layout(kl_smem, P);
-    const RgRange R = own_rgs(P.o_rg, P);
-    const uint8_t *Lb = P.arena + (size_t)l * P.layer_stride;
-    gemv_phase(
-        Lb + P.off_o, P.Ap / kTileK, R.first, R.count, 1, P.B, S.a, S.red, P.dummy,
-        [&]() { if (wait >= 0) bar_wait(P, wait); },
-        [&](int b) { stage_vec(P.o + (size_t)b * P.Ap, P.Ap, P.Ap, S.a); },
-        [&](int b, int r, float y0, float y1) {
-            float *x = P.x + (size_t)b * P.Hp;
-            add_dev(x + r, y0);
-            add_dev(x + r + 1, y1);
-        });
-    if (arrive >= 0) bar_arrive(P, arrive);
-}
-
-// RMSNorm + fused gate/up projection + SwiGLU: m = silu(Wg u) * (Wu u).
-// Packed rows alternate gate i, up i.
-__device__ __forceinline__ void phase_gateup(KArg ka, int l, int wait, int arrive) {
-    const StepParams P = load_params(ka);
-    const Lds S = lds_layout(kl_smem, P);
-    const RgRange R = own_rgs(P.gu_rg, P);
+    const int j = blockIdx.x / P.Rc, part = blockIdx.x % P.Rc;
+    const bool member = j < P.Sc;
+    int first = 0, count = 0;
+    if (member) {
+        // block j covers SwiGLU outputs [j KTc 64, (j + 1) KTc 64): 2 packed rows each
+        const int r0 = min(P.gu_rg, j * P.KTc * 2 * kTileK / kTileRows);
+        const int r1 = min(P.gu_rg, (j + 1) * P.KTc * 2 * kTileK / kTileRows);
+        int a0, a1;
+        split_range(r1 - r0, P.Rc, part, a0, a1);
+        first = r0 + a0;
+        count = a1 - a0;
+    }
     const uint8_t *Lb = P.arena + (size_t)l * P.layer_stride;
     const float *gain = reinterpret_cast<const float *>(Lb + P.off_ffn_norm);
     gemv_phase(
-        Lb + P.off_gu, P.Hp / kTileK, R.first, R.count, 1, P.B, S.a, S.red, P.dummy,
-        [&]() { if (wait >= 0) bar_wait(P, wait); },
-        [&](int b) { stage_rmsnorm(P.x + (size_t)b * P.Hp, gain, P.H, P.Hp, P.eps, S.a, S.sm); },
+        Lb + P.off_gu, P.Hp / kTileK, first, count, 1, P.B, S.a, S.red, P.dummy,
+        [&]() { if (gwait >= 0) bar_wait(P, gwait, ti); },
+        [&](int b) { stage_rmsnorm(P.xf + (size_t)b * P.Hp, gain, P.H, P.Hp, P.eps, S.a, S.sm); },
         [&](int b, int r, float gt, float up) {
             st_dev(P.m + (size_t)b * P.Fp + (r >> 1), gt / (1.0f + expf(-gt)) * up);
         });
-    if (arrive >= 0) bar_arrive(P, arrive);
+    if (member) local_arrive(P, P.cnt + 2 * P.nkv + j, ti);
 }
 
-// Down projection + residual: x += Wd m.
-__device__ __forceinline__ void phase_down(KArg ka, int l, int wait, int arrive) {
+// Down projection of FFN column block j: x += Wd[:, block j] m[block j], for
+// the rows this workgroup owns among block j's workgroups.
+__device__ __forceinline__ void phase_down(KArg ka, int l, int garrive, int ti) {
     const StepParams P = load_params(ka);
     const Lds S = lds_layout(kl_smem, P);
-    const RgRange R = own_rgs(P.down_rg, P);
-    const uint8_t *Lb = P.arena + (size_t)l * P.layer_stride;
-    gemv_phase(
-        Lb + P.off_down, P.Fp / kTileK, R.first, R.count, 1,
-        P.B, S.a, S.red, P.dummy,
-        [&]() { if (wait >= 0) bar_wait(P, wait); },
-        [&](int b) { stage_vec(P.m + (size_t)b * P.Fp, P.Fp, P.Fp, S.a); },
-        [&](int b, int r, float y0, float y1) {
-            float *x = P.x + (size_t)b * P.Hp;
-            add_dev(x + r, y0);
-            add_dev(x + r + 1, y1);
-        });
-    if (arrive >= 0) bar_arrive(P, arrive);
+    const int j = blockIdx.x / P.Rc, part = blockIdx.x % P.Rc;
+    if (j < P.Sc) {
+        int a0, a1;
+        split_range(P.down_rg, P.Rc, part, a0, a1);
+        const uint8_t *W = P.arena + (size_t)l * P.layer_stride + P.off_down +
+                           (size_t)j * P.down_rg * P.KTc * kTileBytes;
+        const int kw = P.KTc * kTileK;
+        gemv_phase(
+            W, P.KTc, a0, a1 - a0, 1, P.B, S.a, S.red, P.dummy,
+            [&]() { local_wait(P, P.cnt + 2 * P.nkv + j, (unsigned)(l + 1) * (unsigned)P.Rc, ti); },
+            [&](int b) { stage_vec(P.m + (size_t)b * P.Fp + (size_t)j * kw, kw, kw, S.a); },
+            [&](int b, int r, float y0, float y1) {
+                long long *x = P.xf + (size_t)b * P.Hp;
+                add_fix(x + r, y0);
+                add_fix(x + r + 1, y1);
+            });
+    }
+    if (garrive >= 0) bar_arrive(P, garrive, ti);
 }
 
 // Classifier block (Sec. 2): final RMSNorm + LM head -> fp32 logits.
-__device__ __forceinline__ void phase_head(KArg ka, int wait, int arrive) {
+__device__ __forceinline__ void phase_head(KArg ka, int gwait, int ti) {
     const StepParams P = load_params(ka);
     const Lds S = lds_layout(kl_smem, P);
     const RgRange R = own_rgs(P.head_rg, P);
     const int V = P.V;
     gemv_phase(
-        reinterpret_cast<const uint8_t *>(P.lm_head), P.Hp / kTileK, R.first, R.count, 1, P.B, S.a, S.red,
-        P.dummy,
+        reinterpret_cast<const uint8_t *>(P.lm_head), P.Hp / kTileK, R.first, R.count, 1, P.B,
+        S.a, S.red, P.dummy,
         [&]() {
-            if (wait >= 0) bar_wait(P, wait);
+            if (gwait >= 0) bar_wait(P, gwait, ti);
             if (blockIdx.x == 0 && P.hidden_out) {
                 for (int idx = threadIdx.x; idx < P.B * P.H; idx += kThreads)
-                    P.hidden_out[idx] = ld_dev(P.x + (size_t)(idx / P.H) * P.Hp + idx % P.H);
+                    P.hidden_out[idx] = from_fix((long long)ld_dev_u64(
+                        P.xf + (size_t)(idx / P.H) * P.Hp + idx % P.H));
             }
         },
         [&](int b) {
-            stage_rmsnorm(P.x + (size_t)b * P.Hp, P.final_norm, P.H, P.Hp, P.eps, S.a, S.sm);
+            stage_rmsnorm(P.xf + (size_t)b * P.Hp, P.final_norm, P.H, P.Hp, P.eps, S.a, S.sm);
         },
         [&](int b, int r, float y0, float y1) {
             float *lg = P.logits + (size_t)b * V;
             if (r < V) lg[r] = y0;
             if (r + 1 < V) lg[r + 1] = y1;
         });
-    if (arrive >= 0) bar_arrive(P, arrive);
+    if (is_ctl_lane0()) trace_stamp(P, ti, 0);
 }
 
 // ---------------------------------------------------------------- kernels
 
+// Runs the phases selected by 'phases' for layers [l0, l1) in order:
+// embed, (qkv, attn, oproj, gateup, down) per layer, head.  Grid barrier k is
+// the k-th arrival of the launch; a phase that needs the residual stream waits
+// on the latest one, and an arriving phase arrives only if a later phase of
+// the same launch waits (a launch boundary already orders the rest).
 template <int D, int G>
 __global__ __launch_bounds__(kThreads) void kl_step_kernel(StepParams P, int l0, int l1,
                                                           int phases) {
     (void)P;   // read through the kernel-argument segment (see load_params)
     const KArg ka = kernarg_address();
-    const int per_layer = __builtin_popcount(phases & kPhLayer);
-    const int total = ((phases & kPhEmbed) ? 1 : 0) + (l1 - l0) * per_layer +
-                      ((phases & kPhHead) ? 1 : 0);
-    if (total > 1) bar_init(load_params(ka));
-    int i = 0;   // index of the phase within this launch: waits on i - 1, arrives on i
-    auto wt = [&]() { return i - 1; };
-    auto ar = [&]() { return i + 1 < total ? i : -1; };
-    if (phases & kPhEmbed) { phase_embed(ka, wt(), ar()); ++i; }
-    for (int l = l0; l < l1; ++l) {
-        if (phases & kPhQkv) { phase_qkv(ka, l, wt(), ar()); ++i; }
-        if (phases & kPhAttn) { phase_attn<D, G>(ka, l, wt(), ar()); ++i; }
-        if (phases & kPhOproj) { phase_oproj(ka, l, wt(), ar()); ++i; }
-        if (phases & kPhGateUp) { phase_gateup(ka, l, wt(), ar()); ++i; }
-        if (phases & kPhDown) { phase_down(ka, l, wt(), ar()); ++i; }
+    const bool has_qkv = phases & kPhQkv, has_gu = phases & kPhGateUp, has_head = phases & kPhHead;
+    const int nlay = (phases & kPhLayer) ? l1 - l0 : 0;
+    if ((phases & kPhEmbed) + nlay * 2 + (has_head ? 1 : 0) > 1) bar_init(load_params(ka));
+    int na = 0, ti = 0;   // grid arrivals so far; phase index (for the trace)
+    auto gw = [&]() { return na - 1; };                 // barrier to wait on (-1: none)
+    auto ga = [&](bool waited_later) { return waited_later ? na++ : -1; };
+    if (phases & kPhEmbed) {
+        phase_embed(ka, -1, ga((has_qkv && nlay > 0) || has_head), ti++);
     }
-    if (phases & kPhHead) { phase_head(ka, wt(), ar()); ++i; }
+    for (int l = l0; l < l1; ++l) {
+        if (phases & kPhQkv) phase_qkv(ka, l, gw(), ti++);
+        if (phases & kPhAttn) phase_attn<D, G>(ka, l, ti++);
+        if (phases & kPhOproj) phase_oproj<D, G>(ka, l, ga(has_gu), ti++);
+        if (phases & kPhGateUp) phase_gateup(ka, l, gw(), ti++);
+        if (phases & kPhDown)
+            phase_down(ka, l, ga((has_qkv && l + 1 < l1) || has_head), ti++);
+    }
+    if (has_head) phase_head(ka, gw(), ti++);
 }
 
 typedef void (*StepKernel)(StepParams, int, int, int);
@@ -956,9 +1095,10 @@ StepKernel step_kernel_for(int d, int group) {
     return nullptr;
 }
 
-// Repack row-major bf16 matrices into 8x64 tiles.  rowmap[packed row] =
-// (source id << 28) | source row, or -1 for a zero row; columns >= K are zero.
-__global__ void kl_pack_rows_kernel(uint16_t *__restrict__ dst, int n_rg, int KT, int K,
+// Repack row-major bf16 matrices (row stride ld elements) into 8x64 tiles of
+// their first K columns.  rowmap[packed row] = (source id << 28) | source
+// row, or -1 for a zero row; columns >= K are zero.
+__global__ void kl_pack_rows_kernel(uint16_t *__restrict__ dst, int n_rg, int KT, int K, int ld,
                                     const int32_t *__restrict__ rowmap,
                                     const uint16_t *__restrict__ s0,
                                     const uint16_t *__restrict__ s1,
@@ -974,7 +1114,7 @@ __global__ void kl_pack_rows_kernel(uint16_t *__restrict__ dst, int n_rg, int KT
         unsigned w[4] = {0u, 0u, 0u, 0u};
         if (m >= 0) {
             const int sid = m >> 28, row = m & 0x0fffffff;
-            const uint16_t *src = (sid == 0 ? s0 : (sid == 1 ? s1 : s2)) + (size_t)row * K;
+            const uint16_t *src = (sid == 0 ? s0 : (sid == 1 ? s1 : s2)) + (size_t)row * ld;
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
                 const unsigned v = (k + e < K) ? src[k + e] : 0u;
@@ -1017,13 +1157,13 @@ hipError_t launch_step(const StepParams &p, int first_layer, int last_layer, int
     return hipGetLastError();
 }
 
-hipError_t launch_pack_rows(uint16_t *dst, int n_rg, int kt, int K, const int32_t *rowmap,
+hipError_t launch_pack_rows(uint16_t *dst, int n_rg, int kt, int K, int ld, const int32_t *rowmap,
                             const uint16_t *src0, const uint16_t *src1, const uint16_t *src2,
                             hipStream_t stream) {
     const size_t chunks = (size_t)n_rg * kt * 64;
     const int blocks = (int)std::min<size_t>((chunks + 255) / 256, 65536);
     hipLaunchKernelGGL(kl_pack_rows_kernel, dim3(blocks), dim3(256), 0, stream, dst, n_rg, kt, K,
-                       rowmap, src0, src1, src2);
+                       ld, rowmap, src0, src1, src2);
     return hipGetLastError();
 }
 

@@ -28,7 +28,9 @@ struct kl_state {
     float2 *rope;
     uint8_t *scratch;
     size_t scratch_bytes;
-    float *x, *q, *o, *m, *part;
+    long long *xf;
+    float *q, *m, *part_o, *part_s;
+    int Sg, Sc, Rc, KTc;
     unsigned long long *bar;
     unsigned *cnt;
     int *err;
@@ -92,16 +94,29 @@ kl_status validate_config(const kl_config *c) {
 }
 
 // Packed-row -> source-row maps, encoded (source id << 28) | row, -1 = zero row.
+// Q/K/V rows grouped by KV head g: the G query heads of g, then key head g,
+// then value head g; query and key rows in rotation pairs (i, i + d/2).
 std::vector<int32_t> qkv_rowmap(const kl_config &c) {
-    const int d = c.head_dim, half = d / 2, qd = c.n_heads * d, kd = c.n_kv_heads * d;
-    std::vector<int32_t> m(qd + 2 * kd);
-    for (int pr = 0; pr < qd + kd; ++pr) {
-        const int sid = pr < qd ? 0 : 1, r = pr < qd ? pr : pr - qd;
-        const int h = r / d, j = r % d;
-        m[pr] = (sid << 28) | (h * d + j / 2 + (j % 2) * half);   // rotation pairs adjacent
+    const int d = c.head_dim, half = d / 2, G = c.n_heads / c.n_kv_heads;
+    const auto pair = [&](int j) { return j / 2 + (j % 2) * half; };
+    std::vector<int32_t> m;
+    m.reserve((size_t)(c.n_heads + 2 * c.n_kv_heads) * d);
+    for (int g = 0; g < c.n_kv_heads; ++g) {
+        for (int h = g * G; h < (g + 1) * G; ++h)
+            for (int j = 0; j < d; ++j) m.push_back((0 << 28) | (h * d + pair(j)));
+        for (int j = 0; j < d; ++j) m.push_back((1 << 28) | (g * d + pair(j)));
+        for (int j = 0; j < d; ++j) m.push_back((2 << 28) | (g * d + j));
     }
-    for (int r = 0; r < kd; ++r) m[qd + kd + r] = (2 << 28) | r;
     return m;
+}
+
+// FFN column blocks: the largest divisor of the k-tile count of ffn_dim that
+// is at most 32 (and at most the grid).
+int ffn_column_blocks(int ktf, int nwg) {
+    int best = 1;
+    for (int s = 1; s <= std::min(32, std::min(ktf, nwg)); ++s)
+        if (ktf % s == 0) best = s;
+    return best;
 }
 
 std::vector<int32_t> identity_rowmap(int rows, int padded_rows) {
@@ -125,12 +140,12 @@ std::vector<int32_t> gateup_rowmap(int F) {
 void lds_layout_for(kl_state &s) {
     const kl_config &c = s.cfg;
     const int g = c.n_heads / c.n_kv_heads, d = c.head_dim;
-    const int cmax = std::max(1, s.nwg / c.n_kv_heads);
+    const int cmax = std::max(1, s.Sg);                        // chunks at batch 1
     const int sub = kWaves * kAttnLoads * (64 / (d / 8));      // positions per sub-chunk
     const int attn_main = g * d + g * sub + g * 4 + kWaves * g * d;
-    const int attn_merge = 3 * cmax * g + g;
-    int amax = std::max(std::max(s.Hp, s.Ap), s.Fp);
-    amax = std::max(amax, std::max(attn_main, attn_merge));
+    const int oproj_stage = g * d + 3 * cmax * g + g;          // o + merge statistics
+    int amax = std::max(s.Hp, s.KTc * kTileK);
+    amax = std::max(amax, std::max(attn_main, oproj_stage));
     amax = (amax + 63) & ~63;
     s.lds_red = amax;
     s.lds_sm = s.lds_red + kWaves * kRgBatch * kTileRows;
@@ -154,6 +169,7 @@ StepParams base_params(const kl_state &s) {
     P.Hp = s.Hp; P.Ap = s.Ap; P.Fp = s.Fp;
     P.qkv_rg = s.qkv_rg; P.o_rg = s.o_rg; P.gu_rg = s.gu_rg; P.down_rg = s.down_rg;
     P.head_rg = s.head_rg;
+    P.Sg = s.Sg; P.Sc = s.Sc; P.Rc = s.Rc; P.KTc = s.KTc;
     P.eps = c.rms_eps; P.max_seq = c.max_seq;
     P.arena = s.arena; P.layer_stride = s.layer_stride;
     P.off_attn_norm = s.off_attn_norm; P.off_ffn_norm = s.off_ffn_norm; P.off_qkv = s.off_qkv;
@@ -162,7 +178,7 @@ StepParams base_params(const kl_state &s) {
     P.final_norm = reinterpret_cast<const float *>(s.arena + s.off_final_norm);
     P.lm_head = reinterpret_cast<const uint16_t *>(s.arena + s.off_lm_head);
     P.rope = s.rope;
-    P.x = s.x; P.q = s.q; P.o = s.o; P.m = s.m; P.part = s.part;
+    P.xf = s.xf; P.q = s.q; P.m = s.m; P.part_o = s.part_o; P.part_s = s.part_s;
     P.bar = s.bar; P.cnt = s.cnt; P.err = s.err; P.dummy = s.dummy;
     P.nwg = s.nwg;
     P.lds_red = s.lds_red; P.lds_sm = s.lds_sm; P.lds_bar = s.lds_bar;
@@ -225,27 +241,39 @@ kl_status kl_load_model(const kl_config *cfg, const kl_weight_ptrs *w, void *str
     if (!coop) return bail(fail(KL_ERR_UNSUPPORTED, "device lacks cooperative launch"));
 
     const int d = c.head_dim, g = c.n_heads / c.n_kv_heads;
+    if (ncu < c.n_kv_heads)
+        return bail(fail(KL_ERR_UNSUPPORTED, "n_kv_heads %d exceeds the %d compute units",
+                         c.n_kv_heads, ncu));
+    S->nwg = ncu;
     S->Hp = pad_k(c.hidden);
     S->Ap = pad_k(c.n_heads * d);
     S->Fp = pad_k(c.ffn_dim);
-    const int qkv_rows = (c.n_heads + 2 * c.n_kv_heads) * d;
     const int vrows = (c.vocab + kTileRows - 1) / kTileRows * kTileRows;
-    S->qkv_rg = qkv_rows / kTileRows;
+    const int KTH = S->Hp / kTileK, KTF = S->Fp / kTileK, KTO = g * d / kTileK;
+    S->Sg = S->nwg / c.n_kv_heads;
+    S->Sc = ffn_column_blocks(KTF, S->nwg);
+    S->Rc = S->nwg / S->Sc;
+    S->KTc = KTF / S->Sc;
+    S->qkv_rg = (g + 2) * d / kTileRows;
     S->o_rg = c.hidden / kTileRows;
     S->gu_rg = 2 * c.ffn_dim / kTileRows;
     S->down_rg = c.hidden / kTileRows;
     S->head_rg = vrows / kTileRows;
-    const int KTH = S->Hp / kTileK, KTA = S->Ap / kTileK, KTF = S->Fp / kTileK;
 
-    // arena: [layer 0 .. L-1][final_norm][lm_head][embed]
+    // arena: [layer 0 .. L-1][final_norm][lm_head][embed]; per layer the O
+    // projection is stored per KV head (its columns) and the down projection
+    // per FFN column block
     const size_t A = 4096;
     size_t off = 0;
     S->off_attn_norm = off; off = align_up(off + S->Hp * 4, A);
     S->off_ffn_norm = off;  off = align_up(off + S->Hp * 4, A);
-    S->off_qkv = off;  off = align_up(off + (size_t)S->qkv_rg * KTH * kTileBytes, A);
-    S->off_o = off;    off = align_up(off + (size_t)S->o_rg * KTA * kTileBytes, A);
+    S->off_qkv = off;
+    off = align_up(off + (size_t)c.n_kv_heads * S->qkv_rg * KTH * kTileBytes, A);
+    S->off_o = off;
+    off = align_up(off + (size_t)c.n_kv_heads * S->o_rg * KTO * kTileBytes, A);
     S->off_gu = off;   off = align_up(off + (size_t)S->gu_rg * KTH * kTileBytes, A);
-    S->off_down = off; off = align_up(off + (size_t)S->down_rg * KTF * kTileBytes, A);
+    S->off_down = off;
+    off = align_up(off + (size_t)S->Sc * S->down_rg * S->KTc * kTileBytes, A);
     S->layer_stride = off;
     off = S->layer_stride * c.n_layers;
     S->off_final_norm = off; off = align_up(off + S->Hp * 4, A);
@@ -255,7 +283,6 @@ kl_status kl_load_model(const kl_config *cfg, const kl_weight_ptrs *w, void *str
     TRY(hipMalloc(&S->arena, S->arena_bytes));
 
     // grid: one persistent workgroup per CU
-    S->nwg = ncu;
     lds_layout_for(*S);
     if (S->lds_bytes > 160 * 1024 - 256)
         return bail(fail(KL_ERR_UNSUPPORTED, "LDS need %d bytes exceeds 160 KiB", S->lds_bytes));
@@ -265,28 +292,25 @@ kl_status kl_load_model(const kl_config *cfg, const kl_weight_ptrs *w, void *str
 
     // scratch
     const int B = c.max_batch, nkv = c.n_kv_heads;
-    const int Cmax = std::max(1, S->nwg / nkv);
-    const size_t part_items = (size_t)std::max(S->nwg, B * nkv);   // >= B * nkv * C
+    const size_t items = (size_t)nkv * std::max(B, S->Sg);   // >= B * nkv * C for every batch
     size_t so = 0;
-    const size_t off_x = so;    so = align_up(so + (size_t)B * S->Hp * 4, 256);
+    const size_t off_x = so;    so = align_up(so + (size_t)B * S->Hp * 8, 256);
     const size_t off_q = so;    so = align_up(so + (size_t)B * c.n_heads * d * 4, 256);
-    const size_t off_o = so;    so = align_up(so + (size_t)B * S->Ap * 4, 256);
     const size_t off_m = so;    so = align_up(so + (size_t)B * S->Fp * 4, 256);
-    const size_t off_p = so;
-    so = align_up(so + std::max(part_items, (size_t)nkv * Cmax) * g * (d + 2) * 4, 256);
-    (void)Cmax;
+    const size_t off_po = so;   so = align_up(so + items * g * d * 4, 256);
+    const size_t off_ps = so;   so = align_up(so + items * g * 2 * 4, 256);
     const size_t off_bar = so;  so = align_up(so + kBarBytes, 256);
-    const size_t off_cnt = so;  so = align_up(so + (size_t)B * nkv * 4, 256);
+    const size_t off_cnt = so;  so = align_up(so + (size_t)(2 * nkv + S->Sc) * 4, 256);
     const size_t off_err = so;  so = align_up(so + 256, 256);
     const size_t off_dummy = so; so = align_up(so + kTileBytes, 256);
     S->scratch_bytes = so;
     TRY(hipMalloc(&S->scratch, S->scratch_bytes));
     TRY(hipMemsetAsync(S->scratch, 0, S->scratch_bytes, s));
-    S->x = reinterpret_cast<float *>(S->scratch + off_x);
+    S->xf = reinterpret_cast<long long *>(S->scratch + off_x);
     S->q = reinterpret_cast<float *>(S->scratch + off_q);
-    S->o = reinterpret_cast<float *>(S->scratch + off_o);
     S->m = reinterpret_cast<float *>(S->scratch + off_m);
-    S->part = reinterpret_cast<float *>(S->scratch + off_p);
+    S->part_o = reinterpret_cast<float *>(S->scratch + off_po);
+    S->part_s = reinterpret_cast<float *>(S->scratch + off_ps);
     S->bar = reinterpret_cast<unsigned long long *>(S->scratch + off_bar);
     S->cnt = reinterpret_cast<unsigned *>(S->scratch + off_cnt);
     S->err = reinterpret_cast<int *>(S->scratch + off_err);
@@ -335,17 +359,26 @@ kl_status kl_load_model(const kl_config *cfg, const kl_weight_ptrs *w, void *str
             pe = launch_gain_to_f32(reinterpret_cast<float *>(Lb + S->off_ffn_norm),
                                     u16(Lw.ffn_norm), c.hidden, S->Hp, s);
         if (pe == hipSuccess)
-            pe = launch_pack_rows(reinterpret_cast<uint16_t *>(Lb + S->off_qkv), S->qkv_rg, KTH,
-                                  c.hidden, d_qkv, u16(Lw.wq), u16(Lw.wk), u16(Lw.wv), s);
-        if (pe == hipSuccess)
-            pe = launch_pack_rows(reinterpret_cast<uint16_t *>(Lb + S->off_o), S->o_rg, KTA,
-                                  c.n_heads * d, d_h, u16(Lw.wo), nullptr, nullptr, s);
+            pe = launch_pack_rows(reinterpret_cast<uint16_t *>(Lb + S->off_qkv),
+                                  c.n_kv_heads * S->qkv_rg, KTH, c.hidden, c.hidden, d_qkv,
+                                  u16(Lw.wq), u16(Lw.wk), u16(Lw.wv), s);
+        for (int kv = 0; kv < c.n_kv_heads && pe == hipSuccess; ++kv)   // Wo[:, head kv]
+            pe = launch_pack_rows(reinterpret_cast<uint16_t *>(Lb + S->off_o) +
+                                      (size_t)kv * S->o_rg * KTO * kTileBytes / 2,
+                                  S->o_rg, KTO, g * d, c.n_heads * d, d_h,
+                                  u16(Lw.wo) + (size_t)kv * g * d, nullptr, nullptr, s);
         if (pe == hipSuccess)
             pe = launch_pack_rows(reinterpret_cast<uint16_t *>(Lb + S->off_gu), S->gu_rg, KTH,
-                                  c.hidden, d_gu, u16(Lw.w_gate), u16(Lw.w_up), nullptr, s);
-        if (pe == hipSuccess)
-            pe = launch_pack_rows(reinterpret_cast<uint16_t *>(Lb + S->off_down), S->down_rg, KTF,
-                                  c.ffn_dim, d_h, u16(Lw.w_down), nullptr, nullptr, s);
+                                  c.hidden, c.hidden, d_gu, u16(Lw.w_gate), u16(Lw.w_up),
+                                  nullptr, s);
+        for (int j = 0; j < S->Sc && pe == hipSuccess; ++j) {   // Wd[:, column block j]
+            const int c0 = j * S->KTc * kTileK;
+            pe = launch_pack_rows(reinterpret_cast<uint16_t *>(Lb + S->off_down) +
+                                      (size_t)j * S->down_rg * S->KTc * kTileBytes / 2,
+                                  S->down_rg, S->KTc, std::max(0, std::min(c.ffn_dim - c0,
+                                                                           S->KTc * kTileK)),
+                                  c.ffn_dim, d_h, u16(Lw.w_down) + c0, nullptr, nullptr, s);
+        }
     }
     if (pe == hipSuccess)
         pe = launch_gain_to_f32(reinterpret_cast<float *>(S->arena + S->off_final_norm),
@@ -353,7 +386,7 @@ kl_status kl_load_model(const kl_config *cfg, const kl_weight_ptrs *w, void *str
                                 s);
     if (pe == hipSuccess)
         pe = launch_pack_rows(reinterpret_cast<uint16_t *>(S->arena + S->off_lm_head), S->head_rg,
-                              KTH, c.hidden, d_head,
+                              KTH, c.hidden, c.hidden, d_head,
                               reinterpret_cast<const uint16_t *>(w->lm_head), nullptr, nullptr, s);
     if (pe == hipSuccess)
         pe = hipMemcpyAsync(S->arena + S->off_embed, w->embed, (size_t)c.vocab * c.hidden * 2,
@@ -402,7 +435,7 @@ kl_status kl_decode_step(kl_state *st, const int32_t *token_ids, const int32_t *
     P.kc = reinterpret_cast<uint16_t *>(kv->k); P.vc = reinterpret_cast<uint16_t *>(kv->v);
     P.kv_batch = kv->batch; P.cap = kv->capacity;
     P.logits = logits_out; P.hidden_out = hidden_out;
-    P.C = std::max(1, st->nwg / (batch * c.n_kv_heads));
+    P.C = std::max(1, st->Sg / batch);
 
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     const int L = c.n_layers, lds = st->lds_bytes;
@@ -434,18 +467,18 @@ kl_status kl_get_device_error(kl_state *st, int32_t *code) {
     if (v & KL_DEVERR_BARRIER) {
         // a timed-out barrier leaves its counters mid-count: start them afresh
         HIP_TRY(hipMemset(st->bar, 0, kBarBytes));
-        HIP_TRY(hipMemset(st->cnt, 0, (size_t)st->cfg.max_batch * st->cfg.n_kv_heads * 4));
+        HIP_TRY(hipMemset(st->cnt, 0, (size_t)(2 * st->cfg.n_kv_heads + st->Sc) * 4));
     }
     return fail(KL_ERR_DEVICE_FAULT, "device error word 0x%x", v);
 }
 
-kl_status kl_set_trace(kl_state *st, uint64_t *dev_buffer, int32_t max_barriers) {
+kl_status kl_set_trace(kl_state *st, uint64_t *dev_buffer, int32_t max_phases) {
     g_last_error.clear();
     if (!st) return fail(KL_ERR_INVALID_ARGUMENT, "state is NULL");
-    if (dev_buffer && (max_barriers < 1 || !aligned(dev_buffer, 8)))
-        return fail(KL_ERR_INVALID_ARGUMENT, "trace buffer needs max_barriers >= 1, 8-byte alignment");
+    if (dev_buffer && (max_phases < 1 || !aligned(dev_buffer, 8)))
+        return fail(KL_ERR_INVALID_ARGUMENT, "trace buffer needs max_phases >= 1, 8-byte alignment");
     st->trace = reinterpret_cast<unsigned long long *>(dev_buffer);
-    st->trace_max = dev_buffer ? max_barriers : 0;
+    st->trace_max = dev_buffer ? max_phases : 0;
     return KL_OK;
 }
 
@@ -454,7 +487,7 @@ kl_status kl_get_info(const kl_state *st, kl_info *info) {
     info->n_workgroups = st->nwg;
     info->threads_per_group = kThreads;
     info->lds_bytes = st->lds_bytes;
-    info->attn_chunks_b1 = std::max(1, st->nwg / st->cfg.n_kv_heads);
+    info->attn_chunks_b1 = std::max(1, st->Sg);
     info->arena_bytes = (int64_t)st->arena_bytes;
     info->scratch_bytes = (int64_t)st->scratch_bytes;
     return KL_OK;

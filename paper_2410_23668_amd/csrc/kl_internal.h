@@ -34,9 +34,16 @@ struct StepParams {
     // shape
     int L, H, nq, nkv, d, F, V, group;
     int Hp, Ap, Fp;            // K extents padded to kTileK: hidden, n_heads*d, ffn
-    int qkv_rg, o_rg, gu_rg, down_rg, head_rg;   // row groups (kTileRows rows) per matrix
+    int qkv_rg;                // row groups of one KV head's q/k/v block
+    int o_rg;                  // row groups of one KV head's O-projection block (H / 8)
+    int gu_rg;                 // row groups of the gate/up matrix (2 F / 8)
+    int down_rg;               // row groups of one FFN column block of the down matrix
+    int head_rg;               // row groups of the LM head
     float eps;
     int max_seq;
+    // work partition (depends only on nwg and the shape)
+    int Sg;                    // workgroups per KV head: w / Sg is the head
+    int Sc, Rc, KTc;           // FFN column blocks, workgroups per block, k-tiles per block
     // packed weights
     const uint8_t *arena;      // layer 0 base
     size_t layer_stride;       // bytes between consecutive layers
@@ -52,27 +59,27 @@ struct StepParams {
     int kv_batch, cap;
     float *logits, *hidden_out;
     // scratch
-    float *x;                  // [max_batch][Hp]   residual stream
+    long long *xf;             // [max_batch][Hp] residual stream, fixed point (2^-32 units)
     float *q;                  // [max_batch][nq*d] rotated queries
-    float *o;                  // [max_batch][Ap]   attention output (padding stays 0)
-    float *m;                  // [max_batch][Fp]   SwiGLU output (padding stays 0)
-    float *part;               // attention partials [max_batch*nkv*C][group][d+2]
+    float *m;                  // [max_batch][Fp] SwiGLU output (padding stays 0)
+    float *part_o;             // attention chunk outputs [B*nkv*C][group*d]
+    float *part_s;             // attention chunk (max, sum) [B*nkv*C][group][2]
     unsigned long long *bar;   // grid barrier counters (monotonic): group g at [32 (g + 1)]
-    unsigned *cnt;             // [max_batch*nkv] attention chunk arrivals
+    unsigned *cnt;             // local counters: [nkv] qkv, [nkv] attention, [Sc] gate/up
     int *err;                  // device error word
     const uint8_t *dummy;      // 16 readable bytes: target of the GEMV ring's spare loads
-    int nwg;                   // grid size; the work partition depends only on it
+    int nwg;                   // grid size
     int lds_red, lds_sm, lds_bar;   // dynamic LDS layout (float offsets)
     int C;                     // attention chunks per (sequence, KV head)
-    unsigned long long *trace; // optional barrier timestamps (see kl_set_trace), or null
-    int trace_max;             // barriers recorded per launch
+    unsigned long long *trace; // optional phase timestamps (see kl_set_trace), or null
+    int trace_max;             // phases recorded per launch
 };
 
 hipError_t launch_step(const StepParams &p, int first_layer, int last_layer, int phases,
                        bool cooperative, int lds_bytes, hipStream_t stream);
 hipError_t step_kernel_setup(int d, int group, int lds_bytes, int *max_blocks_per_cu);
 
-hipError_t launch_pack_rows(uint16_t *dst, int n_rg, int kt, int K, const int32_t *rowmap,
+hipError_t launch_pack_rows(uint16_t *dst, int n_rg, int kt, int K, int ld, const int32_t *rowmap,
                             const uint16_t *src0, const uint16_t *src1, const uint16_t *src2,
                             hipStream_t stream);
 hipError_t launch_gain_to_f32(float *dst, const uint16_t *src, int n, int npad,
