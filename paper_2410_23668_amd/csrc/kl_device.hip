@@ -384,29 +384,43 @@ __device__ __forceinline__ void stage_vec(const float *__restrict__ src, int n, 
 }
 
 // a[i] = x[i] * rsqrt(mean(x^2) + eps) * gain[i] for i < n, 0 up to npad,
-// x read from the fixed-point residual stream.
+// x read from the fixed-point residual stream.  The gain is loaded in the
+// same batch as x (a dependent second batch would cost a second memory round
+// trip, ~2 us when HBM is saturated), and so are the ne floats of an optional
+// extra vector (esrc -> edst in LDS), e.g. the RoPE row the epilogue needs.
 __device__ __forceinline__ void stage_rmsnorm(const long long *__restrict__ xf,
                                               const float *__restrict__ gain, int n, int npad,
-                                              float eps, float *a, float *sm) {
+                                              float eps, float *a, float *sm,
+                                              const float *esrc = nullptr, float *edst = nullptr,
+                                              int ne = 0) {
     for (int i0 = threadIdx.x; i0 < npad; i0 += kStageBatch * kThreads) {
         long long v[kStageBatch];
+        float gv[kStageBatch];
+        float ev = 0.f;
+        const bool first = i0 == (int)threadIdx.x;
 #pragma unroll
         for (int k = 0; k < kStageBatch; ++k) {
             const int i = i0 + k * kThreads;
             v[k] = i < n ? (long long)ld_dev_u64(xf + i) : 0ll;
+            gv[k] = i < n ? gain[i] : 0.f;
         }
+        if (first && (int)threadIdx.x < ne) ev = esrc[threadIdx.x];
 #pragma unroll
         for (int k = 0; k < kStageBatch; ++k) {
             const int i = i0 + k * kThreads;
-            if (i < npad) a[i] = from_fix(v[k]);
+            if (i < npad) {
+                a[i] = from_fix(v[k]);
+                a[npad + i] = gv[k];
+            }
         }
+        if (first && (int)threadIdx.x < ne) edst[threadIdx.x] = ev;
     }
     __syncthreads();
     float ss = 0.f;
     for (int i = threadIdx.x; i < n; i += kThreads) ss = fmaf(a[i], a[i], ss);
     ss = block_sum(ss, sm);
     const float r = 1.0f / sqrtf(ss / (float)n + eps);
-    for (int i = threadIdx.x; i < n; i += kThreads) a[i] = a[i] * r * gain[i];
+    for (int i = threadIdx.x; i < n; i += kThreads) a[i] = a[i] * r * a[npad + i];
     __syncthreads();
 }
 
@@ -636,13 +650,19 @@ __device__ __forceinline__ void phase_qkv(KArg ka, int l, int gwait, int ti) {
     gemv_phase(
         Lb + P.off_qkv, P.Hp / kTileK, g * P.qkv_rg + a0, a1 - a0, 1, P.B, S.a, S.red, P.dummy,
         [&]() { if (gwait >= 0) bar_wait(P, gwait, ti); },
-        [&](int b) { stage_rmsnorm(P.xf + (size_t)b * P.Hp, gain, P.H, P.Hp, P.eps, S.a, S.sm); },
+        [&](int b) {
+            // the RoPE row of this sequence's position rides along (a + 2 Hp)
+            stage_rmsnorm(P.xf + (size_t)b * P.Hp, gain, P.H, P.Hp, P.eps, S.a, S.sm,
+                          reinterpret_cast<const float *>(P.rope + (size_t)eff_pos(P, b) * half),
+                          S.a + 2 * P.Hp, 2 * half);
+            if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 3);
+        },
         [&](int b, int r, float y0, float y1) {
             const int p = eff_pos(P, b);
             const int lr = r - row0;
             if (lr < (G + 1) * d) {
                 const int i = (lr % d) >> 1;
-                const float2 cs = P.rope[(size_t)p * half + i];
+                const float2 cs = reinterpret_cast<const float2 *>(S.a + 2 * P.Hp)[i];
                 const float u0 = y0 * cs.x - y1 * cs.y;
                 const float u1 = y0 * cs.y + y1 * cs.x;
                 if (lr < G * d) {
@@ -952,7 +972,10 @@ __device__ __forceinline__ void phase_oproj(KArg ka, int l, int garrive, int ti)
         gemv_phase(
             W, KT, a0, a1 - a0, 1, P.B, S.a, S.red, P.dummy,
             [&]() { local_wait(P, P.cnt + P.nkv + g, target, ti); },
-            [&](int b) { merge_chunks<D, G>(P, b, g, S.a, S.a + G * D); },
+            [&](int b) {
+                merge_chunks<D, G>(P, b, g, S.a, S.a + G * D);
+                if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 3);
+            },
             [&](int b, int r, float y0, float y1) {
                 long long *x = P.xf + (size_t)b * P.Hp;
                 add_fix(x + r, y0);
@@ -984,7 +1007,10 @@ __device__ __forceinline__ void phase_gateup(KArg ka, int l, int gwait, int ti) 
     gemv_phase(
         Lb + P.off_gu, P.Hp / kTileK, first, count, 1, P.B, S.a, S.red, P.dummy,
         [&]() { if (gwait >= 0) bar_wait(P, gwait, ti); },
-        [&](int b) { stage_rmsnorm(P.xf + (size_t)b * P.Hp, gain, P.H, P.Hp, P.eps, S.a, S.sm); },
+        [&](int b) {
+            stage_rmsnorm(P.xf + (size_t)b * P.Hp, gain, P.H, P.Hp, P.eps, S.a, S.sm);
+            if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 3);
+        },
         [&](int b, int r, float gt, float up) {
             st_dev(P.m + (size_t)b * P.Fp + (r >> 1), gt / (1.0f + expf(-gt)) * up);
         });
@@ -1006,7 +1032,10 @@ __device__ __forceinline__ void phase_down(KArg ka, int l, int garrive, int ti) 
         gemv_phase(
             W, P.KTc, a0, a1 - a0, 1, P.B, S.a, S.red, P.dummy,
             [&]() { local_wait(P, P.cnt + 2 * P.nkv + j, (unsigned)(l + 1) * (unsigned)P.Rc, ti); },
-            [&](int b) { stage_vec(P.m + (size_t)b * P.Fp + (size_t)j * kw, kw, kw, S.a); },
+            [&](int b) {
+                stage_vec(P.m + (size_t)b * P.Fp + (size_t)j * kw, kw, kw, S.a);
+                if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 3);
+            },
             [&](int b, int r, float y0, float y1) {
                 long long *x = P.xf + (size_t)b * P.Hp;
                 add_fix(x + r, y0);
@@ -1035,6 +1064,7 @@ __device__ __forceinline__ void phase_head(KArg ka, int gwait, int ti) {
         },
         [&](int b) {
             stage_rmsnorm(P.xf + (size_t)b * P.Hp, P.final_norm, P.H, P.Hp, P.eps, S.a, S.sm);
+            if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 3);
         },
         [&](int b, int r, float y0, float y1) {
             float *lg = P.logits + (size_t)b * V;

@@ -144,7 +144,7 @@ void lds_layout_for(kl_state &s) {
     const int sub = kWaves * kAttnLoads * (64 / (d / 8));      // positions per sub-chunk
     const int attn_main = g * d + g * sub + g * 4 + kWaves * g * d;
     const int oproj_stage = g * d + 3 * cmax * g + g;          // o + merge statistics
-    int amax = std::max(s.Hp, s.KTc * kTileK);
+    int amax = std::max(2 * s.Hp + d, s.KTc * kTileK);   // activations, gain, RoPE row
     amax = std::max(amax, std::max(attn_main, oproj_stage));
     amax = (amax + 63) & ~63;
     s.lds_red = amax;
