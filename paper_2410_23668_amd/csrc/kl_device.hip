@@ -362,6 +362,23 @@ __device__ __forceinline__ unsigned long long *bar_bases(const StepParams &P) {
 
 // ---------------------------------------------------------------- activations
 
+// Control wave only: copy 'bytes' (a multiple of 16; src and dst 16-byte
+// aligned) from device memory straight to LDS (global_load_lds, 16 bytes per
+// lane, device-coherent: cache-policy bits sc1), then wait for the copy.  The
+// control wave has no weight loads in flight, so the copy does not queue
+// behind them.
+constexpr int kLdsCoherent = 16;
+__device__ __forceinline__ void ctl_copy_to_lds(const void *src, void *dst, int bytes) {
+    const int lane = threadIdx.x & 63;
+    const char *s = static_cast<const char *>(src);
+    char *d = static_cast<char *>(dst);
+    for (int off = 0; off < bytes; off += 64 * 16) {
+        if (off + lane * 16 < bytes)
+            __builtin_amdgcn_global_load_lds(s + off + lane * 16, d + off, 16, 0, kLdsCoherent);
+    }
+}
+__device__ __forceinline__ void ctl_copy_wait() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
 // Copy a device-coherent fp32 vector of n values into LDS, zero up to npad
 // (loads are issued in batches of kStageBatch per thread before any is used).
 constexpr int kStageBatch = 8;
@@ -589,6 +606,204 @@ __device__ __forceinline__ void gemv_phase(const uint8_t *__restrict__ W, int KT
         gemv_rows<true>(W, KT, first, count, stride, B, a, red, dummy, wait, stage, epi);
 }
 
+// ---------------------------------------------------------------- batched engine
+//
+// Y[r][b] = sum_k W[r][k] X[b][k] on the matrix cores (v_mfma_f32_16x16x32_bf16:
+// D[16x16] += A[16x32] B[32x16]) for the row groups first .. first + count - 1
+// and up to kGemmBatch sequences b0 .. b0 + nb - 1.  A block is 16 weight
+// rows (2 row groups); A = W[16 rows][32 k], B = X[32 k][16 sequences], two
+// products per 32 columns cover 32 sequences.  Operand layouts: A lane l holds
+// A[l % 16][8 (l / 16) .. +7], B lane l holds B[8 (l / 16) .. +7][l % 16], D
+// lane l holds D[4 (l / 16) + v][l % 16].  Weight tiles arrive through the
+// same ring of 16-byte loads as the GEMV path and are re-laid out through a
+// per-wave LDS slot (2 KiB: the two tiles of a block at one k-tile).  X is
+// staged in LDS in chunks of kGemmChunkK columns (bf16, kActStride per row),
+// double-buffered: stage(c, buf) fills chunk c.  Waves share blocks and
+// k-tiles: with nblk >= 8 blocks each wave takes whole blocks, else
+// ksplit = 8 / nblk waves share a block's k-tiles and their partial products
+// are added in wave order.
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+struct GemmLds {
+    uint16_t *act[2];   // [kGemmBatch][kActStride] bf16
+    uint8_t *wslot;     // [kWaves][2048]
+    float *cred;        // [kWaves][16][32]
+};
+
+__device__ __forceinline__ GemmLds gemm_lds(char *smem) {
+    GemmLds g;
+    g.act[0] = reinterpret_cast<uint16_t *>(smem);
+    g.act[1] = reinterpret_cast<uint16_t *>(smem + kGemmActBytes);
+    g.wslot = reinterpret_cast<uint8_t *>(smem + 2 * kGemmActBytes);
+    g.cred = reinterpret_cast<float *>(smem + 2 * kGemmActBytes + kWaves * 2048);
+    return g;
+}
+
+//
+// The K extent may be split over several packed matrices of ktg k-tiles each
+// (the O projection per KV head, the down projection per FFN column block),
+// gstride tiles apart: k-tile kt of row group r is tile
+// (kt / ktg) gstride + r ktg + kt % ktg.
+template <class Stage, class Epi>
+__device__ __forceinline__ void gemm_rows(const uint8_t *__restrict__ W, int KT, int first,
+                                          int count, int ktg, size_t gstride, int b0, int nb,
+                                          const uint8_t *dummy, const GemmLds &L,
+                                          bool async_stage, Stage &&stage, Epi &&epi) {
+    constexpr int U = kGemvDepth;
+    constexpr int CT = kGemmChunkK / kTileK;   // k-tiles per chunk
+    const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    const bool compute = wid < kWaves;
+    const int nblk = (count + 1) / 2;
+    const int nkc = (KT + CT - 1) / CT;
+    const int ksplit = nblk >= 8 ? 1 : (nblk >= 4 ? 2 : (nblk >= 2 ? 4 : 8));
+    const int slots = kWaves / ksplit;            // blocks worked on at once
+    const int slot = wid / ksplit, kpart = wid % ksplit;
+    uint8_t *ws = L.wslot + (size_t)wid * 2048;
+    const uint8_t *tbase = W + (size_t)lane * 16;
+    const uint8_t *zbase = dummy + (size_t)lane * 16;   // 1 KiB of zeros
+
+    // zero the padding sequences of both activation buffers once
+    for (int t = threadIdx.x; t < 2 * (kGemmBatch - nb) * kActStride / 8; t += kThreads) {
+        const int half = (kGemmBatch - nb) * kActStride / 8;
+        uint16_t *buf = L.act[t / half];
+        reinterpret_cast<u32x4 *>(buf + nb * kActStride)[t % half] = u32x4{0u, 0u, 0u, 0u};
+    }
+
+    for (int bg0 = 0; bg0 < nblk; bg0 += slots * kGemmMaxBlk) {
+        // my blocks in this group: bg0 + slot + i * slots, i < nbw
+        const int left_blk = min(nblk - bg0, slots * kGemmMaxBlk);
+        const int nbw = left_blk > slot ? (left_blk - slot + slots - 1) / slots : 0;
+        auto nkw_of = [&](int c) {   // my k-tiles in chunk c
+            const int lim = min(CT, KT - c * CT);
+            return lim > kpart ? (lim - kpart + ksplit - 1) / ksplit : 0;
+        };
+        // items of chunk c: (block i, k-tile q, row group t), padded with
+        // zero-tile items to a multiple of U so that every chunk starts at
+        // ring slot 0 (the slot of an item is then known at compile time)
+        auto items_of = [&](int c) { return compute ? nbw * nkw_of(c) * 2 : 0; };
+        auto padded = [&](int n) { return (n + U - 1) / U * U; };
+        // load generator: chunk gc, item gj of the chunk
+        int gc = 0, gj = 0, gn = items_of(0), gnk = max(1, nkw_of(0));
+        auto load_next = [&]() {
+            const bool real = gc < nkc && gj < gn;
+            int tile = 0;
+            bool inb = false;
+            if (real) {
+                const int t = gj & 1, q = (gj >> 1) % gnk, i = (gj >> 1) / gnk;
+                const int rgl = 2 * (bg0 + slot + i * slots) + t;   // row group in this range
+                const int kt = gc * CT + kpart + q * ksplit;
+                inb = rgl < count;
+                tile = __builtin_amdgcn_readfirstlane(
+                    (int)((kt / ktg) * gstride) + (first + rgl) * ktg + kt % ktg);
+            }
+            const u32x4 v = ld_stream_16B(inb ? tbase + (size_t)tile * kTileBytes : zbase);
+            if (gc < nkc && ++gj >= padded(gn)) {
+                gj = 0;
+                do {   // (chunks without items of this wave take no ring slots)
+                    ++gc;
+                    gn = gc < nkc ? items_of(gc) : 0;
+                    gnk = gc < nkc ? max(1, nkw_of(gc)) : 1;
+                } while (gc < nkc && gn == 0);
+            }
+            return v;
+        };
+        while (gc < nkc && gn == 0) {
+            ++gc;
+            gn = gc < nkc ? items_of(gc) : 0;
+            gnk = gc < nkc ? max(1, nkw_of(gc)) : 1;
+        }
+        u32x4 buf[U];
+        if (compute) {   // (the control wave keeps its load queue empty)
+#pragma unroll
+            for (int s = 0; s < U; ++s) buf[s] = load_next();
+        }
+
+        f32x4 acc[kGemmMaxBlk][2];
+#pragma unroll
+        for (int i = 0; i < kGemmMaxBlk; ++i)
+            acc[i][0] = acc[i][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+        stage(0, L.act[0]);
+        __syncthreads();
+        for (int c = 0; c < nkc; ++c) {
+            const uint16_t *act = L.act[c & 1];
+            if (async_stage && c + 1 < nkc) stage(c + 1, L.act[(c + 1) & 1]);
+            const int n = items_of(c), nkw = nkw_of(c);
+            for (int j0 = 0; j0 < padded(n); j0 += U) {
+#pragma unroll
+                for (int s = 0; s < U; ++s) {
+                    const int j = j0 + s;
+                    if (j < n) {
+                        // tile of row group (j & 1) of the block -> the wave's slot
+                        *reinterpret_cast<u32x4 *>(ws + (s & 1) * 1024 + lane * 16) = buf[s];
+                        if (s & 1) {
+                            const int i = (j >> 1) / nkw, ktl = kpart + ((j >> 1) % nkw) * ksplit;
+#pragma unroll
+                            for (int st = 0; st < 2; ++st) {
+                                const int r16 = lane & 15, ko = 4 * st + (lane >> 4);
+                                const bf16x8 a = *reinterpret_cast<const bf16x8 *>(
+                                    ws + (r16 >> 3) * 1024 + ((r16 & 7) * 8 + ko) * 16);
+#pragma unroll
+                                for (int h = 0; h < 2; ++h) {
+                                    const int b = h * 16 + (lane & 15);
+                                    const int k = ktl * kTileK + 32 * st + 8 * (lane >> 4);
+                                    const bf16x8 x = *reinterpret_cast<const bf16x8 *>(
+                                        act + b * kActStride + k);
+#pragma unroll
+                                    for (int ii = 0; ii < kGemmMaxBlk; ++ii)
+                                        if (ii == i)
+                                            acc[ii][h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                                                a, x, acc[ii][h], 0, 0, 0);
+                                }
+                            }
+                        }
+                    }
+                    buf[s] = load_next();
+                }
+            }
+            __syncthreads();   // chunk c consumed by every wave; chunk c + 1 staged
+            if (!async_stage && c + 1 < nkc) {
+                stage(c + 1, L.act[(c + 1) & 1]);
+                __syncthreads();
+            }
+        }
+        // partial products of each block -> LDS, summed over the sharing waves
+        for (int i = 0; i < kGemmMaxBlk; ++i) {
+            if (bg0 + i * slots >= nblk) break;   // (uniform)
+            if (compute) {
+#pragma unroll
+                for (int ii = 0; ii < kGemmMaxBlk; ++ii) {
+                    if (ii != i) continue;
+#pragma unroll
+                    for (int h = 0; h < 2; ++h)
+#pragma unroll
+                        for (int v = 0; v < 4; ++v)
+                            L.cred[(wid * 16 + 4 * (lane >> 4) + v) * 32 + h * 16 + (lane & 15)] =
+                                acc[ii][h][v];
+                }
+            }
+            __syncthreads();
+            // blocks bg0 + i * slots + s, s < slots; rows in pairs, sequences b < nb
+            for (int t = threadIdx.x; t < slots * 8 * nb; t += kThreads) {
+                const int s = t / (8 * nb), rem = t % (8 * nb), pr = (rem / nb) * 2, b = rem % nb;
+                const int blk = bg0 + i * slots + s;
+                if (blk >= nblk || 2 * blk * kTileRows + pr >= count * kTileRows) continue;
+                float y0 = 0.f, y1 = 0.f;
+                for (int kp = 0; kp < ksplit; ++kp) {
+                    const int w = s * ksplit + kp;
+                    y0 += L.cred[(w * 16 + pr) * 32 + b];
+                    y1 += L.cred[(w * 16 + pr + 1) * 32 + b];
+                }
+                epi(b0 + b, (first + 2 * blk) * kTileRows + pr, y0, y1);
+            }
+            __syncthreads();
+        }
+    }
+}
+
+
 // ---------------------------------------------------------------- phases
 //
 // Synchronization between the phases of a layer (l):
@@ -606,6 +821,223 @@ __device__ __forceinline__ void gemv_phase(const uint8_t *__restrict__ W, int KT
 // Local counters grow monotonically within a step (zeroed by the embedding
 // phase); their targets are (l + 1) times the arrivals per layer.
 // Every workgroup arrives on, and waits on, every grid barrier.
+
+// ---------------------------------------------------------------- batched phases
+//
+// A weight phase runs the GEMV engine for batches below kMfmaBatch and the
+// matrix-core engine otherwise (sequences in groups of kGemmBatch; the
+// weights stream once per group).  In the batched path every input is staged
+// as bf16 chunks: prep() runs once after wait(), stageb(c, b0, nb, buf) fills
+// chunk c for sequences b0 .. b0 + nb - 1 (async: the control wave copies it
+// while the compute waves work on the previous chunk).
+template <bool BAT, class Wait, class Prep, class Stage1, class StageB, class Epi>
+__device__ __forceinline__ void weight_phase(const StepParams &P, const Lds &S,
+                                             const uint8_t *W, int KT, int first, int count,
+                                             Wait &&wait, Prep &&prep, Stage1 &&stage1,
+                                             bool async, StageB &&stageb, Epi &&epi,
+                                             int ktg = 0, size_t gstride = 0) {
+    if constexpr (!BAT) {
+        gemv_phase(W, KT, first, count, 1, P.B, S.a, S.red, P.dummy, wait, stage1, epi);
+        return;
+    }
+    wait();
+    prep();
+    const GemmLds L = gemm_lds(kl_smem);
+    for (int b0 = 0; b0 < P.B; b0 += kGemmBatch) {
+        const int nb = min(kGemmBatch, P.B - b0);
+        gemm_rows(W, KT, first, count, ktg ? ktg : KT, gstride, b0, nb, P.dummy, L, async,
+                  [&](int c, uint16_t *buf) { stageb(c, b0, nb, buf); }, epi);
+    }
+}
+
+// Batched RMSNorm: act[b][k] = bf16(x_b[k] r_b gain[k]) for every sequence,
+// the (sequence, kGemmChunkK-column slice) items spread over the grid; ends
+// with grid barrier k, after which any workgroup may stage any slice.
+__device__ __forceinline__ void norm_batched(const StepParams &P, const Lds &S,
+                                             const float *gain, int k) {
+    const int ns = (P.Hp + kGemmChunkK - 1) / kGemmChunkK;
+    for (int it = blockIdx.x; it < P.B * ns; it += P.nwg) {
+        const int b = it / ns, c0 = (it % ns) * kGemmChunkK;
+        const int c1 = min(P.Hp, c0 + kGemmChunkK);
+        stage_rmsnorm(P.xf + (size_t)b * P.Hp, gain, P.H, P.Hp, P.eps, S.a, S.sm);
+        for (int kk = c0 + 2 * (int)threadIdx.x; kk < c1; kk += 2 * kThreads)
+            st_dev_u32(reinterpret_cast<unsigned *>(P.act + (size_t)b * P.Hp + kk),
+                       (unsigned)f2bf(S.a[kk]) | ((unsigned)f2bf(S.a[kk + 1]) << 16));
+        __syncthreads();   // (S.a is restaged by the next item)
+    }
+    bar_arrive(P, k, -1);
+    bar_wait(P, k, -1);
+}
+
+// Chunk c of the normalised activations (control wave: memory-to-LDS copies).
+__device__ __forceinline__ void stage_act_chunk(const StepParams &P, int c, int b0, int nb,
+                                                uint16_t *buf) {
+    if ((threadIdx.x >> 6) != kCtlWave) return;
+    const int k0 = c * kGemmChunkK, kc = min(kGemmChunkK, P.Hp - k0);
+    for (int b = 0; b < nb; ++b)
+        ctl_copy_to_lds(P.act + (size_t)(b0 + b) * P.Hp + k0, buf + b * kActStride, kc * 2);
+    ctl_copy_wait();
+}
+
+// Chunk c of a bf16 matrix src[b][ld] with K columns (control wave: memory-to-
+// LDS copies, so the compute waves keep working on the previous chunk).
+__device__ __forceinline__ void stage_bf16_chunk(const uint16_t *src, int ld, int K, int c, int b0,
+                                                 int nb, uint16_t *buf) {
+    if ((threadIdx.x >> 6) != kCtlWave) return;
+    const int k0 = c * kGemmChunkK, kc = min(kGemmChunkK, K - k0);
+    for (int b = 0; b < nb; ++b)
+        ctl_copy_to_lds(src + (size_t)(b0 + b) * ld + k0, buf + b * kActStride, kc * 2);
+    ctl_copy_wait();
+}
+
+// Chunk c of the merged attention output of KV head g, as bf16.  With one
+// chunk per (sequence, head), o = A / L: every thread loads four outputs
+// (16 bytes) and their head's sum in one batch; otherwise the chunk results
+// are merged as in merge_chunks.
+template <int D, int G>
+__device__ __forceinline__ void stage_o_chunk(const StepParams &P, int g, int c, int b0, int nb,
+                                              uint16_t *buf) {
+    const int C = P.C, k0 = c * kGemmChunkK, kc = min(kGemmChunkK, G * D - k0);
+    if (C == 1) {
+        constexpr int NB = 8;   // float4 loads per thread in flight
+        const int n4 = nb * kc / 4;
+        for (int t0 = threadIdx.x; t0 < n4; t0 += NB * kThreads) {
+            float4 v[NB];
+            float den[NB];
+#pragma unroll
+            for (int q = 0; q < NB; ++q) {
+                const int t = t0 + q * kThreads;
+                v[q] = make_float4(0.f, 0.f, 0.f, 0.f);
+                den[q] = 1.f;
+                if (t < n4) {
+                    const int b = t / (kc / 4), j = k0 + (t % (kc / 4)) * 4;
+                    const size_t item = (size_t)(b0 + b) * P.nkv + g;
+                    const u32x4 u = ld_dev_16B(P.part_o + item * G * D + j);
+                    v[q] = make_float4(__uint_as_float(u.x), __uint_as_float(u.y),
+                                       __uint_as_float(u.z), __uint_as_float(u.w));
+                    den[q] = ld_dev(P.part_s + (item * G + j / D) * 2 + 1);
+                }
+            }
+#pragma unroll
+            for (int q = 0; q < NB; ++q) {
+                const int t = t0 + q * kThreads;
+                if (t < n4) {
+                    const int b = t / (kc / 4), jj = (t % (kc / 4)) * 4;
+                    const float r = 1.0f / den[q];
+                    unsigned *dst = reinterpret_cast<unsigned *>(buf + b * kActStride + jj);
+                    dst[0] = (unsigned)f2bf(v[q].x * r) | ((unsigned)f2bf(v[q].y * r) << 16);
+                    dst[1] = (unsigned)f2bf(v[q].z * r) | ((unsigned)f2bf(v[q].w * r) << 16);
+                }
+            }
+        }
+        return;
+    }
+    for (int t = threadIdx.x; t < nb * kc; t += kThreads) {
+        const int b = t / kc, j = k0 + t % kc, h = j / D;
+        const size_t item0 = ((size_t)(b0 + b) * P.nkv + g) * C;
+        float M = -INFINITY;
+        for (int cc = 0; cc < C; ++cc) M = fmaxf(M, ld_dev(P.part_s + ((item0 + cc) * G + h) * 2));
+        float num = 0.f, den = 0.f;
+        for (int cc = 0; cc < C; ++cc) {
+            const float m = ld_dev(P.part_s + ((item0 + cc) * G + h) * 2);
+            const float w = (m == -INFINITY) ? 0.f : expf(m - M);
+            num = fmaf(ld_dev(P.part_o + (item0 + cc) * G * D + j), w, num);
+            den = fmaf(ld_dev(P.part_s + ((item0 + cc) * G + h) * 2 + 1), w, den);
+        }
+        buf[b * kActStride + (j - k0)] = f2bf(num / den);
+    }
+}
+
+// Chunk c of the merged attention output of all heads (K = n_heads d), as
+// bf16; same scheme as stage_o_chunk.
+template <int D, int G>
+__device__ __forceinline__ void stage_o_full(const StepParams &P, int c, int b0, int nb,
+                                             uint16_t *buf) {
+    const int C = P.C, A = P.nq * D, k0 = c * kGemmChunkK, kc = min(kGemmChunkK, A - k0);
+    if (C == 1) {   // item (b, g) holds heads g G .. g G + G - 1 contiguously: index b A + j
+        constexpr int NB = 8;
+        const int n4 = nb * kc / 4;
+        for (int t0 = threadIdx.x; t0 < n4; t0 += NB * kThreads) {
+            float4 v[NB];
+            float den[NB];
+#pragma unroll
+            for (int q = 0; q < NB; ++q) {
+                const int t = t0 + q * kThreads;
+                v[q] = make_float4(0.f, 0.f, 0.f, 0.f);
+                den[q] = 1.f;
+                if (t < n4) {
+                    const int b = t / (kc / 4), j = k0 + (t % (kc / 4)) * 4;
+                    const u32x4 u = ld_dev_16B(P.part_o + (size_t)(b0 + b) * A + j);
+                    v[q] = make_float4(__uint_as_float(u.x), __uint_as_float(u.y),
+                                       __uint_as_float(u.z), __uint_as_float(u.w));
+                    den[q] = ld_dev(P.part_s + ((size_t)(b0 + b) * P.nq + j / D) * 2 + 1);
+                }
+            }
+#pragma unroll
+            for (int q = 0; q < NB; ++q) {
+                const int t = t0 + q * kThreads;
+                if (t < n4) {
+                    const int b = t / (kc / 4), jj = (t % (kc / 4)) * 4;
+                    const float r = 1.0f / den[q];
+                    unsigned *dst = reinterpret_cast<unsigned *>(buf + b * kActStride + jj);
+                    dst[0] = (unsigned)f2bf(v[q].x * r) | ((unsigned)f2bf(v[q].y * r) << 16);
+                    dst[1] = (unsigned)f2bf(v[q].z * r) | ((unsigned)f2bf(v[q].w * r) << 16);
+                }
+            }
+        }
+        return;
+    }
+    for (int t = threadIdx.x; t < nb * kc; t += kThreads) {
+        const int b = t / kc, j = k0 + t % kc, h = j / D, g = h / G, hl = h % G, dd = j % D;
+        const size_t item0 = ((size_t)(b0 + b) * P.nkv + g) * C;
+        float M = -INFINITY;
+        for (int cc = 0; cc < C; ++cc)
+            M = fmaxf(M, ld_dev(P.part_s + ((item0 + cc) * G + hl) * 2));
+        float num = 0.f, den = 0.f;
+        for (int cc = 0; cc < C; ++cc) {
+            const float m = ld_dev(P.part_s + ((item0 + cc) * G + hl) * 2);
+            const float w = (m == -INFINITY) ? 0.f : expf(m - M);
+            num = fmaf(ld_dev(P.part_o + (item0 + cc) * G * D + hl * D + dd), w, num);
+            den = fmaf(ld_dev(P.part_s + ((item0 + cc) * G + hl) * 2 + 1), w, den);
+        }
+        buf[b * kActStride + (j - k0)] = f2bf(num / den);
+    }
+}
+
+// Chunk c of FFN column block j's SwiGLU values, as bf16 (16-byte loads, in
+// one batch per thread); j < 0: chunk c of all columns.
+__device__ __forceinline__ void stage_m_chunk(const StepParams &P, int j, int c, int b0, int nb,
+                                              uint16_t *buf) {
+    constexpr int NB = 8;
+    const int kw = j < 0 ? P.Fp : P.KTc * kTileK, k0 = c * kGemmChunkK;
+    const int kc = min(kGemmChunkK, kw - k0);
+    const size_t col0 = j < 0 ? 0 : (size_t)j * kw;
+    const int n4 = nb * kc / 4;
+    for (int t0 = threadIdx.x; t0 < n4; t0 += NB * kThreads) {
+        u32x4 v[NB];
+#pragma unroll
+        for (int q = 0; q < NB; ++q) {
+            const int t = t0 + q * kThreads;
+            v[q] = u32x4{0u, 0u, 0u, 0u};
+            if (t < n4) {
+                const int b = t / (kc / 4), k = (t % (kc / 4)) * 4;
+                v[q] = ld_dev_16B(P.m + (size_t)(b0 + b) * P.Fp + col0 + k0 + k);
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < NB; ++q) {
+            const int t = t0 + q * kThreads;
+            if (t < n4) {
+                const int b = t / (kc / 4), k = (t % (kc / 4)) * 4;
+                unsigned *dst = reinterpret_cast<unsigned *>(buf + b * kActStride + k);
+                dst[0] = (unsigned)f2bf(__uint_as_float(v[q].x)) |
+                         ((unsigned)f2bf(__uint_as_float(v[q].y)) << 16);
+                dst[1] = (unsigned)f2bf(__uint_as_float(v[q].z)) |
+                         ((unsigned)f2bf(__uint_as_float(v[q].w)) << 16);
+            }
+        }
+    }
+}
 
 // Embedding block (Sec. 2): x = E[token] (exact in fixed point).  Workgroup 0
 // records bad token ids and positions, and zeroes the local counters.
@@ -636,7 +1068,8 @@ __device__ __forceinline__ void phase_embed(KArg ka, int gwait, int garrive, int
 // RMSNorm + Q/K/V projection of KV head g + RoPE + KV-cache append.  The rows
 // of head g's block are: its G query heads, then its key, then its value
 // head; query and key rows are packed in rotation pairs (dims i, i + d/2).
-__device__ __forceinline__ void phase_qkv(KArg ka, int l, int gwait, int ti) {
+template <bool BAT>
+__device__ __forceinline__ void phase_qkv(KArg ka, int l, int gwait, int xbar, int ti) {
     const StepParams P = load_params(ka);
     const Lds S = lds_layout(kl_smem, P);
     const int g = blockIdx.x / P.Sg, part = blockIdx.x % P.Sg;
@@ -647,9 +1080,11 @@ __device__ __forceinline__ void phase_qkv(KArg ka, int l, int gwait, int ti) {
     const float *gain = reinterpret_cast<const float *>(Lb + P.off_attn_norm);
     const int d = P.d, half = P.d / 2, G = P.group;
     const int row0 = g * P.qkv_rg * kTileRows;   // first packed row of head g's block
-    gemv_phase(
-        Lb + P.off_qkv, P.Hp / kTileK, g * P.qkv_rg + a0, a1 - a0, 1, P.B, S.a, S.red, P.dummy,
+    constexpr bool batched = BAT;
+    weight_phase<BAT>(
+        P, S, Lb + P.off_qkv, P.Hp / kTileK, g * P.qkv_rg + a0, a1 - a0,
         [&]() { if (gwait >= 0) bar_wait(P, gwait, ti); },
+        [&]() { norm_batched(P, S, gain, xbar); },
         [&](int b) {
             // the RoPE row of this sequence's position rides along (a + 2 Hp)
             stage_rmsnorm(P.xf + (size_t)b * P.Hp, gain, P.H, P.Hp, P.eps, S.a, S.sm,
@@ -657,12 +1092,14 @@ __device__ __forceinline__ void phase_qkv(KArg ka, int l, int gwait, int ti) {
                           S.a + 2 * P.Hp, 2 * half);
             if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 3);
         },
+        true, [&](int c, int b0, int nb, uint16_t *buf) { stage_act_chunk(P, c, b0, nb, buf); },
         [&](int b, int r, float y0, float y1) {
             const int p = eff_pos(P, b);
             const int lr = r - row0;
             if (lr < (G + 1) * d) {
                 const int i = (lr % d) >> 1;
-                const float2 cs = reinterpret_cast<const float2 *>(S.a + 2 * P.Hp)[i];
+                const float2 cs = batched ? P.rope[(size_t)p * half + i]
+                                          : reinterpret_cast<const float2 *>(S.a + 2 * P.Hp)[i];
                 const float u0 = y0 * cs.x - y1 * cs.y;
                 const float u1 = y0 * cs.y + y1 * cs.x;
                 if (lr < G * d) {
@@ -729,32 +1166,32 @@ __device__ __forceinline__ void attn_item(KArg ka, int l, int b, int g, int c, b
     // local position of (wave, load t) in a sub-chunk
     auto jloc = [&](int t) { return (t * kWaves + wid) * PP + pi; };
     u32x4 kr[NG], vr[NG];
-    auto issue = [&](int js, int len) {
+    // K (or V) vectors of a sub-chunk; the next sub-chunk's K is issued once
+    // the scores have used this one's, and its V once the values have (the
+    // loop is software-pipelined over sub-chunks)
+    auto issue_one = [&](u32x4 *r, const uint16_t *base, int js, int len) {
         if (!compute) return;   // the control wave keeps its load queue empty for the barrier
 #pragma unroll
         for (int t = 0; t < NG; ++t) {
             const int jl = jloc(t), pos = js + jl;
-            const bool real = compute && jl < len && pos != pnew;
-            kr[t] = ld_stream_16B(real ? (const void *)(Kb + (size_t)pos * D + ds) : P.dummy);
-            vr[t] = ld_stream_16B(real ? (const void *)(Vb + (size_t)pos * D + ds) : P.dummy);
+            const bool real = jl < len && pos != pnew;
+            r[t] = ld_stream_16B(real ? (const void *)(base + (size_t)pos * D + ds) : P.dummy);
         }
     };
     // the new slot (written during this step by another workgroup) is read
     // with device-coherent loads, after the wait
-    auto fetch_new = [&](int js, int len) {
+    auto fetch_new = [&](u32x4 *r, const uint16_t *base, int js, int len) {
         if (compute && pnew >= js && pnew < js + len) {
 #pragma unroll
-            for (int t = 0; t < NG; ++t) {
-                if (js + jloc(t) == pnew) {
-                    kr[t] = ld_dev_16B(Kb + (size_t)pnew * D + ds);
-                    vr[t] = ld_dev_16B(Vb + (size_t)pnew * D + ds);
-                }
-            }
+            for (int t = 0; t < NG; ++t)
+                if (js + jloc(t) == pnew) r[t] = ld_dev_16B(base + (size_t)pnew * D + ds);
         }
     };
-    issue(j0, min(SUB, j1 - j0));
+    issue_one(kr, Kb, j0, min(SUB, j1 - j0));
+    issue_one(vr, Vb, j0, min(SUB, j1 - j0));
     if (first) local_wait(P, P.cnt + g, (unsigned)(l + 1) * (unsigned)P.Sg, ti);
-    fetch_new(j0, min(SUB, j1 - j0));
+    fetch_new(kr, Kb, j0, min(SUB, j1 - j0));
+    fetch_new(vr, Vb, j0, min(SUB, j1 - j0));
     for (int t = threadIdx.x; t < G * D; t += kThreads)
         qs[t] = ld_dev(P.q + (size_t)b * P.nq * D + (size_t)g * G * D + t);
     if (threadIdx.x < G) {
@@ -770,10 +1207,7 @@ __device__ __forceinline__ void attn_item(KArg ka, int l, int b, int g, int c, b
 
     for (int js = j0; js < j1; js += SUB) {
         const int len = min(SUB, j1 - js);
-        if (js != j0) {
-            issue(js, len);
-            fetch_new(js, len);
-        }
+        const int jn = js + SUB, lenn = min(SUB, j1 - jn);   // the next sub-chunk
         // scores (q is read from LDS; all lanes take part in the lane sums)
         if (compute) {
 #pragma unroll
@@ -799,6 +1233,10 @@ __device__ __forceinline__ void attn_item(KArg ka, int l, int b, int g, int c, b
                     if (jl < len && (lane % LP) == 0) sp[h * SUB + jl] = s * scale;
                 }
             }
+        }
+        if (jn < j1) {
+            issue_one(kr, Kb, jn, lenn);
+            fetch_new(kr, Kb, jn, lenn);
         }
         __syncthreads();
         // softmax statistics: wave h owns head h
@@ -847,6 +1285,10 @@ __device__ __forceinline__ void attn_item(KArg ka, int l, int b, int g, int c, b
                 }
             }
         }
+        if (jn < j1) {
+            issue_one(vr, Vb, jn, lenn);
+            fetch_new(vr, Vb, jn, lenn);
+        }
         __syncthreads();
     }
     // reduce the PP position slots of each wave, then the waves in order
@@ -877,6 +1319,8 @@ __device__ __forceinline__ void attn_item(KArg ka, int l, int b, int g, int c, b
         float s = 0.f;
         for (int w = 0; w < kWaves; ++w) s += red[(w * G + h) * D + dd];
         st_dev(out + t, s);
+        if (P.C == 1)   // (one chunk: the merged output is final; the batched O projection copies it)
+            st_dev_u16(P.acto + (size_t)b * P.nq * D + (size_t)g * G * D + t, f2bf(s / st[h * 4 + 1]));
     }
     if (threadIdx.x < G) {
         st_dev(sts + threadIdx.x * 2, st[threadIdx.x * 4 + 0]);
@@ -891,14 +1335,17 @@ __device__ __forceinline__ void attn_item(KArg ka, int l, int b, int g, int c, b
 // Attention of KV head g: the workgroups of head g take its items (sequence b,
 // chunk c) round-robin.
 template <int D, int G>
-__device__ __forceinline__ void phase_attn(KArg ka, int l, int ti) {
+__device__ __forceinline__ void phase_attn(KArg ka, int l, int garrive, int ti) {
     const StepParams P = load_params(ka);
     const int g = blockIdx.x / P.Sg, part = blockIdx.x % P.Sg;
-    if (g >= P.nkv) return;
-    const int items = P.B * P.C;
-    for (int it = part; it < items; it += P.Sg)
-        attn_item<D, G>(ka, l, it / P.C, g, it % P.C, it == part, ti);
-    if (is_ctl_lane0()) trace_stamp(P, ti, 0);
+    if (g < P.nkv) {
+        const int items = P.B * P.C;
+        for (int it = part; it < items; it += P.Sg)
+            attn_item<D, G>(ka, l, it / P.C, g, it % P.C, it == part, ti);
+    }
+    // (batched steps: the O projection takes all heads and waits on the grid)
+    if (garrive >= 0) bar_arrive(P, garrive, ti);
+    else if (is_ctl_lane0()) trace_stamp(P, ti, 0);
 }
 
 // Merge the C chunk results of (sequence b, KV head g) in chunk order into
@@ -957,37 +1404,53 @@ __device__ __forceinline__ void merge_chunks(const StepParams &P, int b, int g, 
 // O projection of KV head g: x += Wo[:, columns of head g] o_g, for the rows
 // this workgroup owns among head g's workgroups, added into the fixed-point
 // residual.  The chunk merge is the activation staging of this GEMV.
-template <int D, int G>
-__device__ __forceinline__ void phase_oproj(KArg ka, int l, int garrive, int ti) {
+template <int D, int G, bool BAT>
+__device__ __forceinline__ void phase_oproj(KArg ka, int l, int gwait, int garrive, int ti) {
     const StepParams P = load_params(ka);
     const Lds S = lds_layout(kl_smem, P);
-    const int g = blockIdx.x / P.Sg, part = blockIdx.x % P.Sg;
-    if (g < P.nkv) {
+    const int KTO = G * D / kTileK;
+    const uint8_t *Wo = P.arena + (size_t)l * P.layer_stride + P.off_o;
+    auto epi = [&](int b, int r, float y0, float y1) {
+        long long *x = P.xf + (size_t)b * P.Hp;
+        add_fix(x + r, y0);
+        add_fix(x + r + 1, y1);
+    };
+    if constexpr (BAT) {
+        // all heads at once (K = n_heads d): one writer per residual element
         int a0, a1;
-        split_range(P.o_rg, P.Sg, part, a0, a1);
-        const int KT = G * D / kTileK;
-        const uint8_t *W = P.arena + (size_t)l * P.layer_stride + P.off_o +
-                           (size_t)g * P.o_rg * KT * kTileBytes;
-        const unsigned target = (unsigned)(l + 1) * (unsigned)(P.B * P.C);
-        gemv_phase(
-            W, KT, a0, a1 - a0, 1, P.B, S.a, S.red, P.dummy,
-            [&]() { local_wait(P, P.cnt + P.nkv + g, target, ti); },
-            [&](int b) {
-                merge_chunks<D, G>(P, b, g, S.a, S.a + G * D);
-                if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 3);
+        split_range(P.o_rg, P.nwg, blockIdx.x, a0, a1);
+        weight_phase<true>(
+            P, S, Wo, P.nkv * KTO, a0, a1 - a0,
+            [&]() { if (gwait >= 0) bar_wait(P, gwait, ti); }, [&]() {}, [&](int) {}, P.C == 1,
+            [&](int c, int b0, int nb, uint16_t *buf) {
+                if (P.C == 1) stage_bf16_chunk(P.acto, P.nq * D, P.nq * D, c, b0, nb, buf);
+                else stage_o_full<D, G>(P, c, b0, nb, buf);
             },
-            [&](int b, int r, float y0, float y1) {
-                long long *x = P.xf + (size_t)b * P.Hp;
-                add_fix(x + r, y0);
-                add_fix(x + r + 1, y1);
-            });
+            epi, KTO, (size_t)P.o_rg * KTO);
+    } else {
+        const int g = blockIdx.x / P.Sg, part = blockIdx.x % P.Sg;
+        if (g < P.nkv) {
+            int a0, a1;
+            split_range(P.o_rg, P.Sg, part, a0, a1);
+            const unsigned target = (unsigned)(l + 1) * (unsigned)(P.B * P.C);
+            weight_phase<false>(
+                P, S, Wo + (size_t)g * P.o_rg * KTO * kTileBytes, KTO, a0, a1 - a0,
+                [&]() { local_wait(P, P.cnt + P.nkv + g, target, ti); }, [&]() {},
+                [&](int b) {
+                    merge_chunks<D, G>(P, b, g, S.a, S.a + G * D);
+                    if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 3);
+                },
+                false, [&](int, int, int, uint16_t *) {}, epi);
+        }
     }
     if (garrive >= 0) bar_arrive(P, garrive, ti);
 }
 
 // RMSNorm + gate/up projection + SwiGLU for FFN column block j = w / Rc:
 // m = silu(Wg u) * (Wu u).  Packed rows alternate gate i, up i.
-__device__ __forceinline__ void phase_gateup(KArg ka, int l, int gwait, int ti) {
+template <bool BAT>
+__device__ __forceinline__ void phase_gateup(KArg ka, int l, int gwait, int xbar, int garrive,
+                                             int ti) {
     const StepParams P = load_params(ka);
     const Lds S = lds_layout(kl_smem, P);
     const int j = blockIdx.x / P.Rc, part = blockIdx.x % P.Rc;
@@ -1004,56 +1467,81 @@ __device__ __forceinline__ void phase_gateup(KArg ka, int l, int gwait, int ti) 
     }
     const uint8_t *Lb = P.arena + (size_t)l * P.layer_stride;
     const float *gain = reinterpret_cast<const float *>(Lb + P.off_ffn_norm);
-    gemv_phase(
-        Lb + P.off_gu, P.Hp / kTileK, first, count, 1, P.B, S.a, S.red, P.dummy,
+    weight_phase<BAT>(
+        P, S, Lb + P.off_gu, P.Hp / kTileK, first, count,
         [&]() { if (gwait >= 0) bar_wait(P, gwait, ti); },
+        [&]() { norm_batched(P, S, gain, xbar); },
         [&](int b) {
             stage_rmsnorm(P.xf + (size_t)b * P.Hp, gain, P.H, P.Hp, P.eps, S.a, S.sm);
             if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 3);
         },
+        true, [&](int c, int b0, int nb, uint16_t *buf) { stage_act_chunk(P, c, b0, nb, buf); },
         [&](int b, int r, float gt, float up) {
-            st_dev(P.m + (size_t)b * P.Fp + (r >> 1), gt / (1.0f + expf(-gt)) * up);
+            const float mv = gt / (1.0f + expf(-gt)) * up;
+            if constexpr (BAT) st_dev_u16(P.actm + (size_t)b * P.Fp + (r >> 1), f2bf(mv));
+            else st_dev(P.m + (size_t)b * P.Fp + (r >> 1), mv);
         });
-    if (member) local_arrive(P, P.cnt + 2 * P.nkv + j, ti);
+    if constexpr (BAT) {
+        if (garrive >= 0) bar_arrive(P, garrive, ti);
+    } else {
+        if (member) local_arrive(P, P.cnt + 2 * P.nkv + j, ti);
+    }
 }
 
 // Down projection of FFN column block j: x += Wd[:, block j] m[block j], for
 // the rows this workgroup owns among block j's workgroups.
-__device__ __forceinline__ void phase_down(KArg ka, int l, int garrive, int ti) {
+template <bool BAT>
+__device__ __forceinline__ void phase_down(KArg ka, int l, int gwait, int garrive, int ti) {
     const StepParams P = load_params(ka);
     const Lds S = lds_layout(kl_smem, P);
-    const int j = blockIdx.x / P.Rc, part = blockIdx.x % P.Rc;
-    if (j < P.Sc) {
+    const uint8_t *Wd = P.arena + (size_t)l * P.layer_stride + P.off_down;
+    auto epi = [&](int b, int r, float y0, float y1) {
+        long long *x = P.xf + (size_t)b * P.Hp;
+        add_fix(x + r, y0);
+        add_fix(x + r + 1, y1);
+    };
+    if constexpr (BAT) {
+        // all FFN columns at once: one writer per residual element
         int a0, a1;
-        split_range(P.down_rg, P.Rc, part, a0, a1);
-        const uint8_t *W = P.arena + (size_t)l * P.layer_stride + P.off_down +
-                           (size_t)j * P.down_rg * P.KTc * kTileBytes;
-        const int kw = P.KTc * kTileK;
-        gemv_phase(
-            W, P.KTc, a0, a1 - a0, 1, P.B, S.a, S.red, P.dummy,
-            [&]() { local_wait(P, P.cnt + 2 * P.nkv + j, (unsigned)(l + 1) * (unsigned)P.Rc, ti); },
-            [&](int b) {
-                stage_vec(P.m + (size_t)b * P.Fp + (size_t)j * kw, kw, kw, S.a);
-                if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 3);
+        split_range(P.down_rg, P.nwg, blockIdx.x, a0, a1);
+        weight_phase<true>(
+            P, S, Wd, P.Sc * P.KTc, a0, a1 - a0,
+            [&]() { if (gwait >= 0) bar_wait(P, gwait, ti); }, [&]() {}, [&](int) {}, true,
+            [&](int c, int b0, int nb, uint16_t *buf) {
+                stage_bf16_chunk(P.actm, P.Fp, P.Fp, c, b0, nb, buf);
             },
-            [&](int b, int r, float y0, float y1) {
-                long long *x = P.xf + (size_t)b * P.Hp;
-                add_fix(x + r, y0);
-                add_fix(x + r + 1, y1);
-            });
+            epi, P.KTc, (size_t)P.down_rg * P.KTc);
+    } else {
+        const int j = blockIdx.x / P.Rc, part = blockIdx.x % P.Rc;
+        if (j < P.Sc) {
+            int a0, a1;
+            split_range(P.down_rg, P.Rc, part, a0, a1);
+            const int kw = P.KTc * kTileK;
+            weight_phase<false>(
+                P, S, Wd + (size_t)j * P.down_rg * P.KTc * kTileBytes, P.KTc, a0, a1 - a0,
+                [&]() {
+                    local_wait(P, P.cnt + 2 * P.nkv + j, (unsigned)(l + 1) * (unsigned)P.Rc, ti);
+                },
+                [&]() {},
+                [&](int b) {
+                    stage_vec(P.m + (size_t)b * P.Fp + (size_t)j * kw, kw, kw, S.a);
+                    if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 3);
+                },
+                false, [&](int, int, int, uint16_t *) {}, epi);
+        }
     }
     if (garrive >= 0) bar_arrive(P, garrive, ti);
 }
 
 // Classifier block (Sec. 2): final RMSNorm + LM head -> fp32 logits.
-__device__ __forceinline__ void phase_head(KArg ka, int gwait, int ti) {
+template <bool BAT>
+__device__ __forceinline__ void phase_head(KArg ka, int gwait, int xbar, int ti) {
     const StepParams P = load_params(ka);
     const Lds S = lds_layout(kl_smem, P);
     const RgRange R = own_rgs(P.head_rg, P);
     const int V = P.V;
-    gemv_phase(
-        reinterpret_cast<const uint8_t *>(P.lm_head), P.Hp / kTileK, R.first, R.count, 1, P.B,
-        S.a, S.red, P.dummy,
+    weight_phase<BAT>(
+        P, S, reinterpret_cast<const uint8_t *>(P.lm_head), P.Hp / kTileK, R.first, R.count,
         [&]() {
             if (gwait >= 0) bar_wait(P, gwait, ti);
             if (blockIdx.x == 0 && P.hidden_out) {
@@ -1062,10 +1550,12 @@ __device__ __forceinline__ void phase_head(KArg ka, int gwait, int ti) {
                         P.xf + (size_t)(idx / P.H) * P.Hp + idx % P.H));
             }
         },
+        [&]() { norm_batched(P, S, P.final_norm, xbar); },
         [&](int b) {
             stage_rmsnorm(P.xf + (size_t)b * P.Hp, P.final_norm, P.H, P.Hp, P.eps, S.a, S.sm);
             if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 3);
         },
+        true, [&](int c, int b0, int nb, uint16_t *buf) { stage_act_chunk(P, c, b0, nb, buf); },
         [&](int b, int r, float y0, float y1) {
             float *lg = P.logits + (size_t)b * V;
             if (r < V) lg[r] = y0;
@@ -1081,46 +1571,69 @@ __device__ __forceinline__ void phase_head(KArg ka, int gwait, int ti) {
 // the k-th arrival of the launch; a phase that needs the residual stream waits
 // on the latest one, and an arriving phase arrives only if a later phase of
 // the same launch waits (a launch boundary already orders the rest).
-template <int D, int G>
+template <int D, int G, bool BAT>
 __global__ __launch_bounds__(kThreads) void kl_step_kernel(StepParams P, int l0, int l1,
                                                           int phases) {
     (void)P;   // read through the kernel-argument segment (see load_params)
     const KArg ka = kernarg_address();
     const bool has_qkv = phases & kPhQkv, has_gu = phases & kPhGateUp, has_head = phases & kPhHead;
     const int nlay = (phases & kPhLayer) ? l1 - l0 : 0;
-    if ((phases & kPhEmbed) + nlay * 2 + (has_head ? 1 : 0) > 1) bar_init(load_params(ka));
+    // batched steps add a grid barrier inside each RMSNorm phase (norm_batched)
+    constexpr bool batched = BAT;
+    bar_init(load_params(ka));
     int na = 0, ti = 0;   // grid arrivals so far; phase index (for the trace)
     auto gw = [&]() { return na - 1; };                 // barrier to wait on (-1: none)
     auto ga = [&](bool waited_later) { return waited_later ? na++ : -1; };
+    auto xb = [&]() { return batched ? na++ : -1; };    // the phase's own barrier
+    const bool has_attn = phases & kPhAttn, has_op = phases & kPhOproj;
+    const bool has_down = phases & kPhDown;
     if (phases & kPhEmbed) {
         phase_embed(ka, -1, ga((has_qkv && nlay > 0) || has_head), ti++);
     }
     for (int l = l0; l < l1; ++l) {
-        if (phases & kPhQkv) phase_qkv(ka, l, gw(), ti++);
-        if (phases & kPhAttn) phase_attn<D, G>(ka, l, ti++);
-        if (phases & kPhOproj) phase_oproj<D, G>(ka, l, ga(has_gu), ti++);
-        if (phases & kPhGateUp) phase_gateup(ka, l, gw(), ti++);
-        if (phases & kPhDown)
-            phase_down(ka, l, ga((has_qkv && l + 1 < l1) || has_head), ti++);
+        // batched steps: attn -> oproj and gateup -> down are grid barriers
+        // too (full-K products with one writer per output)
+        if (phases & kPhQkv) {
+            const int w = gw(), x = xb();
+            phase_qkv<BAT>(ka, l, w, x, ti++);
+        }
+        if (phases & kPhAttn) phase_attn<D, G>(ka, l, BAT ? ga(has_op) : -1, ti++);
+        if (phases & kPhOproj) {
+            const int w = BAT && has_attn ? gw() : -1, a = ga(has_gu);
+            phase_oproj<D, G, BAT>(ka, l, w, a, ti++);
+        }
+        if (phases & kPhGateUp) {
+            const int w = gw(), x = xb(), a = BAT ? ga(has_down) : -1;
+            phase_gateup<BAT>(ka, l, w, x, a, ti++);
+        }
+        if (phases & kPhDown) {
+            const int w = BAT && has_gu ? gw() : -1;
+            phase_down<BAT>(ka, l, w, ga((has_qkv && l + 1 < l1) || has_head), ti++);
+        }
     }
-    if (has_head) phase_head(ka, gw(), ti++);
+    if (has_head) {
+        const int w = gw(), x = xb();
+        phase_head<BAT>(ka, w, x, ti++);
+    }
 }
 
 typedef void (*StepKernel)(StepParams, int, int, int);
 
-// The instance for a model's head_dim and query heads per KV head (the host
-// has validated both).
-StepKernel step_kernel_for(int d, int group) {
-#define KL_INST(DD)                                      \
-    switch (group) {                                     \
-        case 1: return kl_step_kernel<DD, 1>;            \
-        case 2: return kl_step_kernel<DD, 2>;            \
-        case 4: return kl_step_kernel<DD, 4>;            \
-        case 8: return kl_step_kernel<DD, 8>;            \
-        default: return nullptr;                         \
+// The instance for a model's head_dim, query heads per KV head (the host has
+// validated both) and the batch regime (matrix cores at batch >= kMfmaBatch).
+StepKernel step_kernel_for(int d, int group, bool batched) {
+#define KL_INST(DD, BB)                                    \
+    switch (group) {                                       \
+        case 1: return kl_step_kernel<DD, 1, BB>;          \
+        case 2: return kl_step_kernel<DD, 2, BB>;          \
+        case 4: return kl_step_kernel<DD, 4, BB>;          \
+        case 8: return kl_step_kernel<DD, 8, BB>;          \
+        default: return nullptr;                           \
     }
-    if (d == 64) { KL_INST(64) }
-    if (d == 128) { KL_INST(128) }
+    if (d == 64 && !batched) { KL_INST(64, false) }
+    if (d == 64 && batched) { KL_INST(64, true) }
+    if (d == 128 && !batched) { KL_INST(128, false) }
+    if (d == 128 && batched) { KL_INST(128, true) }
 #undef KL_INST
     return nullptr;
 }
@@ -1163,18 +1676,24 @@ __global__ void kl_gain_to_f32_kernel(float *dst, const uint16_t *src, int n, in
 // ---------------------------------------------------------------- launchers
 
 hipError_t step_kernel_setup(int d, int group, int lds_bytes, int *max_blocks_per_cu) {
-    const StepKernel k = step_kernel_for(d, group);
-    if (!k) return hipErrorInvalidValue;
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(k),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes);
-    if (e != hipSuccess) return e;
-    return hipOccupancyMaxActiveBlocksPerMultiprocessor(max_blocks_per_cu, k, kThreads,
-                                                         lds_bytes);
+    *max_blocks_per_cu = 1 << 30;
+    for (int bat = 0; bat < 2; ++bat) {
+        const StepKernel k = step_kernel_for(d, group, bat != 0);
+        if (!k) return hipErrorInvalidValue;
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(k),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes);
+        if (e != hipSuccess) return e;
+        int n = 0;
+        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k, kThreads, lds_bytes);
+        if (e != hipSuccess) return e;
+        *max_blocks_per_cu = std::min(*max_blocks_per_cu, n);
+    }
+    return hipSuccess;
 }
 
 hipError_t launch_step(const StepParams &p, int first_layer, int last_layer, int phases,
                        bool cooperative, int lds_bytes, hipStream_t stream) {
-    const StepKernel k = step_kernel_for(p.d, p.group);
+    const StepKernel k = step_kernel_for(p.d, p.group, p.B >= kMfmaBatch);
     if (!k) return hipErrorInvalidValue;
     StepParams pc = p;
     if (cooperative) {

@@ -30,6 +30,7 @@ struct kl_state {
     size_t scratch_bytes;
     long long *xf;
     float *q, *m, *part_o, *part_s;
+    uint16_t *act, *actm, *acto;
     int Sg, Sc, Rc, KTc;
     unsigned long long *bar;
     unsigned *cnt;
@@ -146,6 +147,7 @@ void lds_layout_for(kl_state &s) {
     const int oproj_stage = g * d + 3 * cmax * g + g;          // o + merge statistics
     int amax = std::max(2 * s.Hp + d, s.KTc * kTileK);   // activations, gain, RoPE row
     amax = std::max(amax, std::max(attn_main, oproj_stage));
+    if (c.max_batch >= kMfmaBatch) amax = std::max(amax, kGemmLdsBytes / 4);   // batched path
     amax = (amax + 63) & ~63;
     s.lds_red = amax;
     s.lds_sm = s.lds_red + kWaves * kRgBatch * kTileRows;
@@ -178,7 +180,8 @@ StepParams base_params(const kl_state &s) {
     P.final_norm = reinterpret_cast<const float *>(s.arena + s.off_final_norm);
     P.lm_head = reinterpret_cast<const uint16_t *>(s.arena + s.off_lm_head);
     P.rope = s.rope;
-    P.xf = s.xf; P.q = s.q; P.m = s.m; P.part_o = s.part_o; P.part_s = s.part_s;
+    P.xf = s.xf; P.q = s.q; P.m = s.m; P.part_o = s.part_o; P.part_s = s.part_s; P.act = s.act;
+    P.actm = s.actm; P.acto = s.acto;
     P.bar = s.bar; P.cnt = s.cnt; P.err = s.err; P.dummy = s.dummy;
     P.nwg = s.nwg;
     P.lds_red = s.lds_red; P.lds_sm = s.lds_sm; P.lds_bar = s.lds_bar;
@@ -299,6 +302,9 @@ kl_status kl_load_model(const kl_config *cfg, const kl_weight_ptrs *w, void *str
     const size_t off_m = so;    so = align_up(so + (size_t)B * S->Fp * 4, 256);
     const size_t off_po = so;   so = align_up(so + items * g * d * 4, 256);
     const size_t off_ps = so;   so = align_up(so + items * g * 2 * 4, 256);
+    const size_t off_act = so;  so = align_up(so + (size_t)B * S->Hp * 2, 256);
+    const size_t off_actm = so; so = align_up(so + (size_t)B * S->Fp * 2, 256);
+    const size_t off_acto = so; so = align_up(so + (size_t)B * S->Ap * 2, 256);
     const size_t off_bar = so;  so = align_up(so + kBarBytes, 256);
     const size_t off_cnt = so;  so = align_up(so + (size_t)(2 * nkv + S->Sc) * 4, 256);
     const size_t off_err = so;  so = align_up(so + 256, 256);
@@ -311,6 +317,9 @@ kl_status kl_load_model(const kl_config *cfg, const kl_weight_ptrs *w, void *str
     S->m = reinterpret_cast<float *>(S->scratch + off_m);
     S->part_o = reinterpret_cast<float *>(S->scratch + off_po);
     S->part_s = reinterpret_cast<float *>(S->scratch + off_ps);
+    S->act = reinterpret_cast<uint16_t *>(S->scratch + off_act);
+    S->actm = reinterpret_cast<uint16_t *>(S->scratch + off_actm);
+    S->acto = reinterpret_cast<uint16_t *>(S->scratch + off_acto);
     S->bar = reinterpret_cast<unsigned long long *>(S->scratch + off_bar);
     S->cnt = reinterpret_cast<unsigned *>(S->scratch + off_cnt);
     S->err = reinterpret_cast<int *>(S->scratch + off_err);
@@ -439,18 +448,24 @@ kl_status kl_decode_step(kl_state *st, const int32_t *token_ids, const int32_t *
 
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     const int L = c.n_layers, lds = st->lds_bytes;
+    // a launch whose workgroups wait for each other must be cooperative (all
+    // resident): every multi-phase launch, and at batch >= kMfmaBatch also
+    // the single RMSNorm phases (their batched normalisation has a barrier)
+    const bool bat = batch >= kMfmaBatch;
     if (mode == KL_MODE_LOOPED) {
         HIP_TRY(launch_step(P, 0, L, kPhEmbed | kPhLayer | kPhHead, true, lds, s));
     } else if (mode == KL_MODE_PER_LAYER) {
         HIP_TRY(launch_step(P, 0, 0, kPhEmbed, false, lds, s));
         for (int l = 0; l < L; ++l) HIP_TRY(launch_step(P, l, l + 1, kPhLayer, true, lds, s));
-        HIP_TRY(launch_step(P, 0, 0, kPhHead, false, lds, s));
+        HIP_TRY(launch_step(P, 0, 0, kPhHead, bat, lds, s));
     } else {
         HIP_TRY(launch_step(P, 0, 0, kPhEmbed, false, lds, s));
         const int ops[] = {kPhQkv, kPhAttn, kPhOproj, kPhGateUp, kPhDown};
         for (int l = 0; l < L; ++l)
-            for (int ph : ops) HIP_TRY(launch_step(P, l, l + 1, ph, false, lds, s));
-        HIP_TRY(launch_step(P, 0, 0, kPhHead, false, lds, s));
+            for (int ph : ops)
+                HIP_TRY(launch_step(P, l, l + 1, ph, bat && (ph == kPhQkv || ph == kPhGateUp),
+                                    lds, s));
+        HIP_TRY(launch_step(P, 0, 0, kPhHead, bat, lds, s));
     }
     return KL_OK;
 }

@@ -133,3 +133,44 @@ def test_llama8b_width_two_layers_long_cache():
     check_against_oracle(c, outs[1], ref)
     assert_bit_exact(outs[0], outs[1], "per_layer vs looped")
     assert_bit_exact(outs[2], outs[1], "per_op vs looped")
+
+
+@pytest.mark.parametrize("batch", [8, 16, 32])
+def test_tiny_batched_matrix_core_path(batch):
+    # batches >= 8 run the weight products on the matrix cores (bf16
+    # activations); ragged positions, all schedules bit-identical
+    say(f"[tiny-batched] batch={batch}")
+    rng = np.random.default_rng(batch)
+    filled = rng.integers(0, 190, size=batch).astype(np.int32)
+    c = Case(TINY, batch, 192, filled, seed=61 + batch)
+    ref = c.oracle_step(nthreads=8)
+    outs = [c.gpu_step(mode) for _, mode in MODES]
+    check_against_oracle(c, outs[1], ref)
+    assert_bit_exact(outs[0], outs[1], "per_layer vs looped")
+    assert_bit_exact(outs[2], outs[1], "per_op vs looped")
+
+
+def test_batched_path_with_batch_above_one_group():
+    # 40 sequences: two groups of the matrix-core path (32 + 8)
+    say("[tiny-batched] batch=40")
+    filled = (np.arange(40, dtype=np.int32) * 7) % 150
+    c = Case(TINY, 40, 192, filled, seed=71)
+    ref = c.oracle_step(nthreads=8)
+    check_against_oracle(c, c.gpu_step(kb.KL_MODE_LOOPED), ref)
+
+
+def test_llama8b_width_two_layers_batch32():
+    # the 8B layer shapes at batch 32 (matrix-core path), 256-position caches
+    cfg = dict(WORKLOADS["llama8b-b32-ctx4096"]["model"], n_layers=2)
+    say("[8b-width L=2 B=32] building")
+    filled = (np.arange(32, dtype=np.int32) * 37) % 250
+    c = Case(cfg, 32, 256, filled, seed=81)
+    say("[8b-width L=2 B=32] oracle")
+    ref = c.oracle_step(nthreads=8)
+    outs = []
+    for name, mode in MODES:
+        say(f"[8b-width L=2 B=32] mode={name}")
+        outs.append(c.gpu_step(mode))
+    check_against_oracle(c, outs[1], ref)
+    assert_bit_exact(outs[0], outs[1], "per_layer vs looped")
+    assert_bit_exact(outs[2], outs[1], "per_op vs looped")
