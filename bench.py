@@ -131,13 +131,26 @@ def main():
     nthr = args.threads or synth.default_threads()
     torch.cuda.set_device(0)
 
-    log(f"workload {args.workload}: generating weights ({nthr} threads)")
     t = time.perf_counter()
-    weights = synth.model_host(cfg, wl["seed_weights"], nthr)
+    # models whose weights would not fit twice in device memory (the 70B
+    # shape) are generated and loaded one layer at a time
+    big = bytemodel.step_bytes(cfg, 1, 0) > 40e9
+    weights = None
+    if big:
+        log(f"workload {args.workload}: generating and loading layer by layer ({nthr} threads)")
+        seed = wl["seed_weights"]
+        model = GpuModel.from_layers(
+            cfg, lambda l: {k: synth.layer_tensor(cfg, seed, l, k, nthr) for k in kb.LAYER_FIELDS},
+            lambda: {k: synth.global_tensor(cfg, seed, k, nthr)
+                     for k in ("embed", "final_norm", "lm_head")}, B, cap)
+    else:
+        log(f"workload {args.workload}: generating weights ({nthr} threads)")
+        weights = synth.model_host(cfg, wl["seed_weights"], nthr)
     K0, V0 = synth.kv_cache_host(cfg, wl["seed_kv"], B, cap, [P] * B, nthr)
     tokens = synth.tokens(cfg, wl["seed_tokens"], B)
     log(f"inputs ready in {time.perf_counter() - t:.1f}s; loading model")
-    model = GpuModel(cfg, weights, B, cap)
+    if not big:
+        model = GpuModel(cfg, weights, B, cap)
     kv = KvCache(cfg, B, cap, k_host=K0, v_host=V0)
     toks = torch.from_numpy(tokens).cuda()
     pos = torch.full((B,), P, dtype=torch.int32, device="cuda")
@@ -189,7 +202,7 @@ def main():
         out["speedup_vs_per_layer"] = res["per_layer"]["mean_ms"] / step_ms
 
     # parity of the timed output, and the oracle's own time on the host
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and weights is not None:
         import oracle
         log("oracle (1 thread) on the same inputs")
         Kr, Vr = K0.copy(), V0.copy()

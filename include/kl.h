@@ -117,6 +117,26 @@ typedef struct {
 kl_status kl_load_model(const kl_config *cfg, const kl_weight_ptrs *weights, void *stream,
                         kl_state **out);
 
+/* Incremental loading, for models whose source weights cannot sit in device
+ * memory beside the packed copy (e.g. the 70B shape on one GPU): the same
+ * result as kl_load_model, one layer at a time.
+ *   kl_model_create      validates cfg and allocates everything kl_load_model
+ *                        allocates; the weights start as zeros.
+ *   kl_model_set_layer   packs layer 'layer' (0 <= layer < n_layers) from the
+ *                        caller's device pointers (layout of kl_layer_ptrs);
+ *                        returns after the packing finished on 'stream', so
+ *                        the caller may free the source right away.
+ *   kl_model_set_globals packs the embedding, final norm and LM head (layouts
+ *                        of kl_weight_ptrs), likewise synchronously.
+ * Steps may run once every layer and the globals are set (earlier steps
+ * compute with zero weights).  Errors as for kl_load_model; a failed set call
+ * leaves the model usable for another attempt. */
+kl_status kl_model_create(const kl_config *cfg, kl_state **out);
+kl_status kl_model_set_layer(kl_state *st, int32_t layer, const kl_layer_ptrs *weights,
+                             void *stream);
+kl_status kl_model_set_globals(kl_state *st, const void *embed, const void *final_norm,
+                               const void *lm_head, void *stream);
+
 /* Enqueue one decode step on 'stream' (asynchronous).
  *   token_ids  dev int32 [batch]   token of each sequence
  *   positions  dev int32 [batch]   position p of the new token; the step writes

@@ -29,7 +29,8 @@ KL_DEVERR_TOKEN = 1
 KL_DEVERR_POSITION = 2
 KL_DEVERR_BARRIER = 4
 
-EXPORTED = ["kl_load_model", "kl_decode_step", "kl_kv_cache_bytes", "kl_get_device_error",
+EXPORTED = ["kl_load_model", "kl_model_create", "kl_model_set_layer", "kl_model_set_globals",
+            "kl_decode_step", "kl_kv_cache_bytes", "kl_get_device_error",
             "kl_get_info", "kl_set_trace", "kl_free_model", "kl_last_error"]
 
 
@@ -87,6 +88,12 @@ def lib():
     L.kl_load_model.argtypes = [ctypes.POINTER(kl_config), ctypes.POINTER(kl_weight_ptrs), vp,
                                 ctypes.POINTER(vp)]
     L.kl_load_model.restype = i32
+    L.kl_model_create.argtypes = [ctypes.POINTER(kl_config), ctypes.POINTER(vp)]
+    L.kl_model_create.restype = i32
+    L.kl_model_set_layer.argtypes = [vp, i32, ctypes.POINTER(kl_layer_ptrs), vp]
+    L.kl_model_set_layer.restype = i32
+    L.kl_model_set_globals.argtypes = [vp, vp, vp, vp, vp]
+    L.kl_model_set_globals.restype = i32
     L.kl_decode_step.argtypes = [vp, vp, vp, i32, ctypes.POINTER(kl_kv_cache), vp, vp, vp, i32]
     L.kl_decode_step.restype = i32
     L.kl_kv_cache_bytes.argtypes = [ctypes.POINTER(kl_config), i32, i32]
@@ -132,6 +139,22 @@ def kl_load_model(cfg: kl_config, embed: int, final_norm: int, lm_head: int, lay
     out = ctypes.c_void_p()
     _check(lib().kl_load_model(ctypes.byref(cfg), ctypes.byref(w), stream, ctypes.byref(out)))
     return out.value
+
+
+def kl_model_create(cfg: kl_config) -> int:
+    out = ctypes.c_void_p()
+    _check(lib().kl_model_create(ctypes.byref(cfg), ctypes.byref(out)))
+    return out.value
+
+
+def kl_model_set_layer(state: int, layer: int, ptrs: dict, stream: int = 0) -> None:
+    lp = kl_layer_ptrs(*[ptrs[n] for n in LAYER_FIELDS])
+    _check(lib().kl_model_set_layer(state, layer, ctypes.byref(lp), stream))
+
+
+def kl_model_set_globals(state: int, embed: int, final_norm: int, lm_head: int,
+                         stream: int = 0) -> None:
+    _check(lib().kl_model_set_globals(state, embed, final_norm, lm_head, stream))
 
 
 def kl_decode_step(state: int, token_ids: int, positions: int, batch: int, k: int, v: int,

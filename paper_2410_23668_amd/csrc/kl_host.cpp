@@ -38,6 +38,8 @@ struct kl_state {
     uint8_t *dummy;
     unsigned long long *trace;
     int trace_max;
+    int32_t *rowmaps;                 // device row maps used by set_layer / set_globals
+    const int32_t *map_qkv, *map_h, *map_gu, *map_head;
     int nwg, lds_bytes;
     int lds_red, lds_sm, lds_bar;
 };
@@ -160,6 +162,7 @@ void free_state(kl_state *s) {
     if (s->arena) (void)hipFree(s->arena);
     if (s->rope) (void)hipFree(s->rope);
     if (s->scratch) (void)hipFree(s->scratch);
+    if (s->rowmaps) (void)hipFree(s->rowmaps);
     delete s;
 }
 
@@ -202,28 +205,25 @@ size_t kl_kv_cache_bytes(const kl_config *cfg, int32_t batch, int32_t capacity) 
            sizeof(uint16_t);
 }
 
-kl_status kl_load_model(const kl_config *cfg, const kl_weight_ptrs *w, void *stream,
-                        kl_state **out) {
+// Validates one layer's pointers.
+kl_status check_layer_ptrs(const kl_layer_ptrs &L, int l) {
+    const void *ps[] = {L.attn_norm, L.wq, L.wk, L.wv, L.wo, L.ffn_norm, L.w_gate, L.w_up,
+                        L.w_down};
+    for (const void *p : ps) {
+        if (!p) return fail(KL_ERR_INVALID_ARGUMENT, "layer %d has a NULL weight pointer", l);
+        if (!aligned(p, 2))
+            return fail(KL_ERR_INVALID_ARGUMENT, "layer %d weight not 2-byte aligned", l);
+    }
+    return KL_OK;
+}
+
+kl_status kl_model_create(const kl_config *cfg, kl_state **out) {
     g_last_error.clear();
     if (!out) return fail(KL_ERR_INVALID_ARGUMENT, "out is NULL");
     *out = nullptr;
     kl_status st = validate_config(cfg);
     if (st != KL_OK) return st;
-    if (!w || !w->embed || !w->final_norm || !w->lm_head || !w->layers)
-        return fail(KL_ERR_INVALID_ARGUMENT, "weight pointers must not be NULL");
-    if (!aligned(w->embed, 2) || !aligned(w->final_norm, 2) || !aligned(w->lm_head, 2))
-        return fail(KL_ERR_INVALID_ARGUMENT, "weight pointers must be 2-byte aligned");
-    for (int l = 0; l < cfg->n_layers; ++l) {
-        const kl_layer_ptrs &L = w->layers[l];
-        const void *ps[] = {L.attn_norm, L.wq, L.wk, L.wv, L.wo, L.ffn_norm, L.w_gate, L.w_up,
-                            L.w_down};
-        for (const void *p : ps) {
-            if (!p) return fail(KL_ERR_INVALID_ARGUMENT, "layer %d has a NULL weight pointer", l);
-            if (!aligned(p, 2))
-                return fail(KL_ERR_INVALID_ARGUMENT, "layer %d weight not 2-byte aligned", l);
-        }
-    }
-    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    hipStream_t s = nullptr;
 
     kl_state *S = new kl_state();
     S->cfg = *cfg;
@@ -341,70 +341,135 @@ kl_status kl_load_model(const kl_config *cfg, const kl_weight_ptrs *w, void *str
         TRY(hipStreamSynchronize(s));
     }
 
-    // row maps (the same for every layer)
-    const std::vector<int32_t> m_qkv = qkv_rowmap(c), m_h = identity_rowmap(c.hidden, c.hidden),
-                               m_gu = gateup_rowmap(c.ffn_dim),
-                               m_head = identity_rowmap(c.vocab, vrows);
-    int32_t *dmaps = nullptr;
-    const size_t nmap = m_qkv.size() + m_h.size() + m_gu.size() + m_head.size();
-    TRY(hipMalloc(&dmaps, nmap * sizeof(int32_t)));
-    std::vector<int32_t> all;
-    all.reserve(nmap);
-    all.insert(all.end(), m_qkv.begin(), m_qkv.end());
-    all.insert(all.end(), m_h.begin(), m_h.end());
-    all.insert(all.end(), m_gu.begin(), m_gu.end());
-    all.insert(all.end(), m_head.begin(), m_head.end());
-    hipError_t pe = hipMemcpyAsync(dmaps, all.data(), nmap * sizeof(int32_t),
-                                   hipMemcpyHostToDevice, s);
-    const int32_t *d_qkv = dmaps, *d_h = d_qkv + m_qkv.size(), *d_gu = d_h + m_h.size(),
-                  *d_head = d_gu + m_gu.size();
-    for (int l = 0; l < c.n_layers && pe == hipSuccess; ++l) {
-        const kl_layer_ptrs &Lw = w->layers[l];
-        uint8_t *Lb = S->arena + (size_t)l * S->layer_stride;
-        const auto u16 = [](const void *p) { return reinterpret_cast<const uint16_t *>(p); };
-        pe = launch_gain_to_f32(reinterpret_cast<float *>(Lb + S->off_attn_norm), u16(Lw.attn_norm),
-                                c.hidden, S->Hp, s);
-        if (pe == hipSuccess)
-            pe = launch_gain_to_f32(reinterpret_cast<float *>(Lb + S->off_ffn_norm),
-                                    u16(Lw.ffn_norm), c.hidden, S->Hp, s);
-        if (pe == hipSuccess)
-            pe = launch_pack_rows(reinterpret_cast<uint16_t *>(Lb + S->off_qkv),
-                                  c.n_kv_heads * S->qkv_rg, KTH, c.hidden, c.hidden, d_qkv,
-                                  u16(Lw.wq), u16(Lw.wk), u16(Lw.wv), s);
-        for (int kv = 0; kv < c.n_kv_heads && pe == hipSuccess; ++kv)   // Wo[:, head kv]
-            pe = launch_pack_rows(reinterpret_cast<uint16_t *>(Lb + S->off_o) +
-                                      (size_t)kv * S->o_rg * KTO * kTileBytes / 2,
-                                  S->o_rg, KTO, g * d, c.n_heads * d, d_h,
-                                  u16(Lw.wo) + (size_t)kv * g * d, nullptr, nullptr, s);
-        if (pe == hipSuccess)
-            pe = launch_pack_rows(reinterpret_cast<uint16_t *>(Lb + S->off_gu), S->gu_rg, KTH,
-                                  c.hidden, c.hidden, d_gu, u16(Lw.w_gate), u16(Lw.w_up),
-                                  nullptr, s);
-        for (int j = 0; j < S->Sc && pe == hipSuccess; ++j) {   // Wd[:, column block j]
-            const int c0 = j * S->KTc * kTileK;
-            pe = launch_pack_rows(reinterpret_cast<uint16_t *>(Lb + S->off_down) +
-                                      (size_t)j * S->down_rg * S->KTc * kTileBytes / 2,
-                                  S->down_rg, S->KTc, std::max(0, std::min(c.ffn_dim - c0,
-                                                                           S->KTc * kTileK)),
-                                  c.ffn_dim, d_h, u16(Lw.w_down) + c0, nullptr, nullptr, s);
-        }
+    // the arena starts zeroed: weights not set yet read as zero
+    TRY(hipMemsetAsync(S->arena, 0, S->arena_bytes, s));
+
+    // row maps (the same for every layer), kept on the device for set_layer
+    {
+        const int vrows = (c.vocab + kTileRows - 1) / kTileRows * kTileRows;
+        const std::vector<int32_t> m_qkv = qkv_rowmap(c),
+                                   m_h = identity_rowmap(c.hidden, c.hidden),
+                                   m_gu = gateup_rowmap(c.ffn_dim),
+                                   m_head = identity_rowmap(c.vocab, vrows);
+        const size_t nmap = m_qkv.size() + m_h.size() + m_gu.size() + m_head.size();
+        TRY(hipMalloc(&S->rowmaps, nmap * sizeof(int32_t)));
+        std::vector<int32_t> all;
+        all.reserve(nmap);
+        all.insert(all.end(), m_qkv.begin(), m_qkv.end());
+        all.insert(all.end(), m_h.begin(), m_h.end());
+        all.insert(all.end(), m_gu.begin(), m_gu.end());
+        all.insert(all.end(), m_head.begin(), m_head.end());
+        TRY(hipMemcpy(S->rowmaps, all.data(), nmap * sizeof(int32_t), hipMemcpyHostToDevice));
+        S->map_qkv = S->rowmaps;
+        S->map_h = S->map_qkv + m_qkv.size();
+        S->map_gu = S->map_h + m_h.size();
+        S->map_head = S->map_gu + m_gu.size();
     }
-    if (pe == hipSuccess)
-        pe = launch_gain_to_f32(reinterpret_cast<float *>(S->arena + S->off_final_norm),
-                                reinterpret_cast<const uint16_t *>(w->final_norm), c.hidden, S->Hp,
-                                s);
-    if (pe == hipSuccess)
-        pe = launch_pack_rows(reinterpret_cast<uint16_t *>(S->arena + S->off_lm_head), S->head_rg,
-                              KTH, c.hidden, c.hidden, d_head,
-                              reinterpret_cast<const uint16_t *>(w->lm_head), nullptr, nullptr, s);
-    if (pe == hipSuccess)
-        pe = hipMemcpyAsync(S->arena + S->off_embed, w->embed, (size_t)c.vocab * c.hidden * 2,
-                            hipMemcpyDeviceToDevice, s);
-    hipError_t se = hipStreamSynchronize(s);
-    (void)hipFree(dmaps);
-    if (pe != hipSuccess) TRY(pe);
-    TRY(se);
+    TRY(hipDeviceSynchronize());
 #undef TRY
+    *out = S;
+    return KL_OK;
+}
+
+kl_status kl_model_set_layer(kl_state *S, int32_t l, const kl_layer_ptrs *w, void *stream) {
+    g_last_error.clear();
+    if (!S || !w) return fail(KL_ERR_INVALID_ARGUMENT, "state and weights must not be NULL");
+    const kl_config &c = S->cfg;
+    if (l < 0 || l >= c.n_layers)
+        return fail(KL_ERR_INVALID_ARGUMENT, "layer %d outside [0, %d)", l, c.n_layers);
+    kl_status st = check_layer_ptrs(*w, l);
+    if (st != KL_OK) return st;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    const int d = c.head_dim, g = c.n_heads / c.n_kv_heads;
+    const int KTH = S->Hp / kTileK, KTO = g * d / kTileK;
+    const kl_layer_ptrs &Lw = *w;
+    uint8_t *Lb = S->arena + (size_t)l * S->layer_stride;
+    const auto u16 = [](const void *p) { return reinterpret_cast<const uint16_t *>(p); };
+    hipError_t pe = launch_gain_to_f32(reinterpret_cast<float *>(Lb + S->off_attn_norm),
+                                       u16(Lw.attn_norm), c.hidden, S->Hp, s);
+    if (pe == hipSuccess)
+        pe = launch_gain_to_f32(reinterpret_cast<float *>(Lb + S->off_ffn_norm),
+                                u16(Lw.ffn_norm), c.hidden, S->Hp, s);
+    if (pe == hipSuccess)
+        pe = launch_pack_rows(reinterpret_cast<uint16_t *>(Lb + S->off_qkv),
+                              c.n_kv_heads * S->qkv_rg, KTH, c.hidden, c.hidden, S->map_qkv,
+                              u16(Lw.wq), u16(Lw.wk), u16(Lw.wv), s);
+    for (int kv = 0; kv < c.n_kv_heads && pe == hipSuccess; ++kv)   // Wo[:, head kv]
+        pe = launch_pack_rows(reinterpret_cast<uint16_t *>(Lb + S->off_o) +
+                                  (size_t)kv * S->o_rg * KTO * kTileBytes / 2,
+                              S->o_rg, KTO, g * d, c.n_heads * d, S->map_h,
+                              u16(Lw.wo) + (size_t)kv * g * d, nullptr, nullptr, s);
+    if (pe == hipSuccess)
+        pe = launch_pack_rows(reinterpret_cast<uint16_t *>(Lb + S->off_gu), S->gu_rg, KTH,
+                              c.hidden, c.hidden, S->map_gu, u16(Lw.w_gate), u16(Lw.w_up),
+                              nullptr, s);
+    for (int j = 0; j < S->Sc && pe == hipSuccess; ++j) {   // Wd[:, column block j]
+        const int c0 = j * S->KTc * kTileK;
+        pe = launch_pack_rows(reinterpret_cast<uint16_t *>(Lb + S->off_down) +
+                                  (size_t)j * S->down_rg * S->KTc * kTileBytes / 2,
+                              S->down_rg, S->KTc,
+                              std::max(0, std::min(c.ffn_dim - c0, S->KTc * kTileK)), c.ffn_dim,
+                              S->map_h, u16(Lw.w_down) + c0, nullptr, nullptr, s);
+    }
+    if (pe != hipSuccess)
+        return fail(KL_ERR_HIP, "packing layer %d failed: %s", l, hipGetErrorString(pe));
+    HIP_TRY(hipStreamSynchronize(s));
+    return KL_OK;
+}
+
+kl_status kl_model_set_globals(kl_state *S, const void *embed, const void *final_norm,
+                               const void *lm_head, void *stream) {
+    g_last_error.clear();
+    if (!S || !embed || !final_norm || !lm_head)
+        return fail(KL_ERR_INVALID_ARGUMENT, "state and weight pointers must not be NULL");
+    if (!aligned(embed, 2) || !aligned(final_norm, 2) || !aligned(lm_head, 2))
+        return fail(KL_ERR_INVALID_ARGUMENT, "weight pointers must be 2-byte aligned");
+    const kl_config &c = S->cfg;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    const int KTH = S->Hp / kTileK;
+    hipError_t pe = launch_gain_to_f32(reinterpret_cast<float *>(S->arena + S->off_final_norm),
+                                       reinterpret_cast<const uint16_t *>(final_norm), c.hidden,
+                                       S->Hp, s);
+    if (pe == hipSuccess)
+        pe = launch_pack_rows(reinterpret_cast<uint16_t *>(S->arena + S->off_lm_head),
+                              S->head_rg, KTH, c.hidden, c.hidden, S->map_head,
+                              reinterpret_cast<const uint16_t *>(lm_head), nullptr, nullptr, s);
+    if (pe == hipSuccess)
+        pe = hipMemcpyAsync(S->arena + S->off_embed, embed, (size_t)c.vocab * c.hidden * 2,
+                            hipMemcpyDeviceToDevice, s);
+    if (pe != hipSuccess)
+        return fail(KL_ERR_HIP, "packing the globals failed: %s", hipGetErrorString(pe));
+    HIP_TRY(hipStreamSynchronize(s));
+    return KL_OK;
+}
+
+kl_status kl_load_model(const kl_config *cfg, const kl_weight_ptrs *w, void *stream,
+                        kl_state **out) {
+    g_last_error.clear();
+    if (!out) return fail(KL_ERR_INVALID_ARGUMENT, "out is NULL");
+    *out = nullptr;
+    kl_status st = validate_config(cfg);
+    if (st != KL_OK) return st;
+    if (!w || !w->embed || !w->final_norm || !w->lm_head || !w->layers)
+        return fail(KL_ERR_INVALID_ARGUMENT, "weight pointers must not be NULL");
+    if (!aligned(w->embed, 2) || !aligned(w->final_norm, 2) || !aligned(w->lm_head, 2))
+        return fail(KL_ERR_INVALID_ARGUMENT, "weight pointers must be 2-byte aligned");
+    for (int l = 0; l < cfg->n_layers; ++l) {
+        st = check_layer_ptrs(w->layers[l], l);
+        if (st != KL_OK) return st;
+    }
+    kl_state *S = nullptr;
+    st = kl_model_create(cfg, &S);
+    if (st != KL_OK) return st;
+    for (int l = 0; l < cfg->n_layers && st == KL_OK; ++l)
+        st = kl_model_set_layer(S, l, &w->layers[l], stream);
+    if (st == KL_OK) st = kl_model_set_globals(S, w->embed, w->final_norm, w->lm_head, stream);
+    if (st != KL_OK) {
+        const std::string msg = g_last_error;
+        free_state(S);
+        g_last_error = msg;
+        return st;
+    }
     *out = S;
     return KL_OK;
 }

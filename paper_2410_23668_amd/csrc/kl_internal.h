@@ -90,6 +90,12 @@ struct StepParams {
     int trace_max;             // phases recorded per launch
 };
 
+typedef void (*StepKernel)(StepParams, int, int, int);
+StepKernel step_kernel_d64(int group);
+StepKernel step_kernel_d64_batched(int group);
+StepKernel step_kernel_d128(int group);
+StepKernel step_kernel_d128_batched(int group);
+
 hipError_t launch_step(const StepParams &p, int first_layer, int last_layer, int phases,
                        bool cooperative, int lds_bytes, hipStream_t stream);
 hipError_t step_kernel_setup(int d, int group, int lds_bytes, int *max_blocks_per_cu);

@@ -1,0 +1,1623 @@
+// Device code of the decode step for gfx950 (CDNA4), included by the
+// translation units that instantiate the step kernel (kl_step_*.hip).
+//
+// One kernel, kl_step_kernel, runs any contiguous run of the step's phases:
+//   embed | for each layer: qkv, attn, oproj, gateup, down | head
+// The three schedules differ only in how many launches cover the run:
+//   looped     one cooperative launch for everything (kernel looping, Sec. 2
+//              and Sec. 3.2 of arXiv 2410.23668: the L chained layer calls
+//              become one call with an outer loop; kernel boundaries become
+//              device-scope grid barriers),
+//   per-layer  one launch per layer (the fused-layer kernel K0 of Sec. 2),
+//   per-op     one launch per phase.
+// The work partition depends only on StepParams::nwg, so every schedule
+// performs the same arithmetic in the same order: results are bit-identical.
+//
+// Pipelining across phases (the "pipelined outer loop" of Sec. 3.2): a phase
+// issues the first loads of its weight tiles before it waits for the barrier
+// that publishes its input activations, so HBM keeps streaming while the
+// grid synchronises.  Data that crosses workgroups (activations, partials,
+// the new KV slot) is written and read with device-coherent (agent-scope)
+// accesses, so a barrier needs no cache write-back or invalidation: only the
+// completion of the stores before the arrival.
+//
+// Weights are pre-packed into 1 KiB tiles of 8 rows x 64 columns (bf16,
+// row-major inside the tile); the tiles of one 8-row group are contiguous
+// along K.  A wave reads one tile per 16-byte-per-lane load: lane l holds row
+// l/8, columns 8*(l%8) .. +7.  Activations are fp32 in LDS; accumulation is
+// fp32 with a fixed order.
+
+#pragma once
+
+#include "kl_internal.h"
+#include "kl.h"
+
+namespace kl {
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// ---------------------------------------------------------------- helpers
+
+__device__ __forceinline__ float bf_lo(unsigned u) { return __uint_as_float(u << 16); }
+__device__ __forceinline__ float bf_hi(unsigned u) { return __uint_as_float(u & 0xffff0000u); }
+__device__ __forceinline__ float bf2f(uint16_t h) { return __uint_as_float((unsigned)h << 16); }
+
+// fp32 -> bf16, round to nearest even (NaN stays NaN).
+__device__ __forceinline__ uint16_t f2bf(float f) {
+    unsigned u = __float_as_uint(f);
+    if ((u & 0x7f800000u) == 0x7f800000u) return (uint16_t)((u >> 16) | ((u & 0xffffu) ? 0x40u : 0u));
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v),
+                                                                 CTRL, 0xF, 0xF, false));
+}
+// DPP controls: quad_perm [1,0,3,2] = 0xB1, [2,3,0,1] = 0x4E,
+// row_half_mirror = 0x141, row_mirror = 0x140.
+// Sum over aligned groups of 8 lanes; every lane of the group gets the sum.
+__device__ __forceinline__ float sum8(float v) {
+    v += dpp<0xB1>(v);
+    v += dpp<0x4E>(v);
+    v += dpp<0x141>(v);
+    return v;
+}
+__device__ __forceinline__ float sum16(float v) { v = sum8(v); return v + dpp<0x140>(v); }
+
+template <int LP>
+__device__ __forceinline__ float sum_lanes(float v) {
+    if constexpr (LP == 8) return sum8(v);
+    else return sum16(v);
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+    v = sum16(v);
+    v += __shfl_xor(v, 16);
+    v += __shfl_xor(v, 32);
+    return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+    for (int off = 1; off < 64; off <<= 1) v = fmaxf(v, __shfl_xor(v, off));
+    return v;
+}
+
+// Sum over the workgroup; every thread gets the same value (fixed order).
+__device__ __forceinline__ float block_sum(float v, float *sm) {
+    v = wave_sum(v);
+    const int wid = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) sm[wid] = v;
+    __syncthreads();
+    float t = 0.f;
+#pragma unroll
+    for (int w = 0; w < kThreads / 64; ++w) t += sm[w];
+    __syncthreads();
+    return t;
+}
+
+__device__ __forceinline__ void split_range(int n, int parts, int i, int &a, int &b) {
+    a = (int)((long long)n * i / parts);
+    b = (int)((long long)n * (i + 1) / parts);
+}
+
+__device__ __forceinline__ int eff_pos(const StepParams &P, int b) {
+    const int p = P.positions[b];
+    const int lim = min(P.cap, P.max_seq);
+    return p < 0 ? 0 : (p >= lim ? lim - 1 : p);
+}
+__device__ __forceinline__ int eff_tok(const StepParams &P, int b) {
+    const int t = P.tokens[b];
+    return (t < 0 || t >= P.V) ? 0 : t;
+}
+
+__device__ __forceinline__ size_t kv_row(const StepParams &P, int l, int b, int g) {
+    return (((size_t)l * P.kv_batch + b) * P.nkv + g) * (size_t)P.cap;
+}
+
+// ---------------------------------------------------------------- coherent accesses
+//
+// Relaxed agent-scope atomic loads and stores compile to ordinary vector
+// memory instructions with the device-coherence bit (sc1): they see, and are
+// seen by, every XCD without flushing or invalidating the XCD-private L2.
+
+__device__ __forceinline__ void st_dev(float *p, float v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_dev_u16(uint16_t *p, uint16_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_dev_u32(unsigned *p, unsigned v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// The residual stream is kept in fixed point: int64 in units of 2^-32.  Every
+// contribution (the embedding, each O-projection partial, each
+// down-projection partial) is rounded once to that grid and added with an
+// integer atomic, so the sum is exact and independent of the order in which
+// workgroups add: results are reproducible however the work is split.  The
+// range (+-2^31) and resolution (2^-32) are far beyond fp32 activations'.
+constexpr double kFixScale = 4294967296.0;   // 2^32
+__device__ __forceinline__ long long to_fix(float v) {
+    return __double2ll_rn((double)v * kFixScale);
+}
+__device__ __forceinline__ float from_fix(long long v) {
+    return (float)v * (1.0f / 4294967296.0f);
+}
+__device__ __forceinline__ void add_fix(long long *p, float v) {
+    __hip_atomic_fetch_add(reinterpret_cast<unsigned long long *>(p),
+                           (unsigned long long)to_fix(v), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_dev_u64(unsigned long long *p, unsigned long long v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ld_dev(const float *p) {
+    return __hip_atomic_load(const_cast<float *>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ unsigned long long ld_dev_u64(const void *p) {
+    return __hip_atomic_load(reinterpret_cast<unsigned long long *>(const_cast<void *>(p)),
+                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ u32x4 ld_dev_16B(const void *p) {
+    const unsigned long long a = ld_dev_u64(p);
+    const unsigned long long b = ld_dev_u64(reinterpret_cast<const char *>(p) + 8);
+    return u32x4{(unsigned)a, (unsigned)(a >> 32), (unsigned)b, (unsigned)(b >> 32)};
+}
+__device__ __forceinline__ u32x4 ld_stream_16B(const void *p) {
+    return __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
+}
+
+// s_waitcnt vmcnt(0): this wave's stores have completed at their coherence point.
+__device__ __forceinline__ void wait_stores() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+// ---------------------------------------------------------------- grid barrier
+//
+// Arrival counting on monotonically increasing 64-bit counters, one per
+// group of workgroups: workgroup w arrives on counter w % ng (one atomic
+// add), and a waiter's wave 0 polls all ng counters at once, one per lane.
+// Spreading arrivals over ng counters keeps the atomics on any one address
+// few; polling them directly saves a second atomic hop.  The counters are
+// never reset: every launch ends with counter g at E * size_g, E being the
+// number of barriers completed so far, and at launch start each workgroup
+// recovers E from its own group's counter.  Barrier k of a launch is complete
+// when counter g reaches base_g + (k + 1) * size_g for every group g.  The
+// wait is bounded by a poll count: past it, KL_DEVERR_BARRIER is raised and every
+// later wait returns at once, so a broken barrier ends the kernel instead of
+// hanging it.
+constexpr int kSpinLimit = 1 << 22;   // polls before a wait gives up (well over a second)
+
+// The per-group bases of the current launch live in the dynamic LDS area (a
+// fixed slot after everything else; see lds_layout), which every phase
+// function addresses the same way.
+extern __shared__ __align__(16) char kl_smem[];
+__device__ __forceinline__ unsigned long long *bar_bases(const StepParams &P);
+
+__device__ __forceinline__ int bar_groups(const StepParams &P) { return min(kBarGroups, P.nwg); }
+__device__ __forceinline__ unsigned bar_gsize(const StepParams &P, int ng, int g) {
+    return (unsigned)(P.nwg / ng + (g < P.nwg % ng ? 1 : 0));
+}
+__device__ __forceinline__ unsigned long long *bar_counter(const StepParams &P, int g) {
+    return P.bar + 32 * (g + 1);   // 256 bytes apart
+}
+
+__device__ __forceinline__ void bar_init(const StepParams &P) {
+    // Only this workgroup's own group counter is read: that group cannot
+    // complete barrier 0 before this workgroup arrives, so the value rounds
+    // down to the number E of whole barriers done by earlier launches.  Any
+    // other group may already be one barrier further, so its base is E times
+    // its size, not its current value rounded down.
+    const int ng = bar_groups(P);
+    if (threadIdx.x < ng) {   // (before any wait; any wave may do it)
+        const int own = blockIdx.x % ng;
+        const unsigned long long c = ld_dev_u64(bar_counter(P, own));
+        const unsigned long long epoch = c / bar_gsize(P, ng, own);
+        bar_bases(P)[threadIdx.x] = epoch * bar_gsize(P, ng, threadIdx.x);
+    }
+    __syncthreads();
+}
+
+// Optional timeline: the control wave of every workgroup stamps
+// (s_memrealtime, 100 MHz) the end of phase i of the launch (slot 0), the
+// start and end of phase i's wait for its inputs (slots 1, 2) and, for an
+// attention phase, the moment its last chunk result is published (slot 3).
+__device__ __forceinline__ void trace_stamp(const StepParams &P, int i, int what) {
+    if (P.trace && i >= 0 && i < P.trace_max)
+        P.trace[((size_t)i * P.nwg + blockIdx.x) * 4 + what] = wall_clock64();
+}
+
+// The control wave (kCtlWave) does all of a workgroup's barrier traffic.  It
+// never has weight or KV loads in flight, so its polls are not queued behind
+// the compute waves' prefetches (a wave's loads complete in issue order).
+__device__ __forceinline__ bool is_ctl_lane0() { return threadIdx.x == kCtlWave * 64; }
+
+// Every wave drains its stores (they must be visible before the signal),
+// then the control wave signals.
+__device__ __forceinline__ void drain_all() {
+    wait_stores();
+    __syncthreads();
+}
+
+// Arrival on grid barrier k after phase ti.
+__device__ __forceinline__ void bar_arrive(const StepParams &P, int k, int ti) {
+    if (is_ctl_lane0()) trace_stamp(P, ti, 0);
+    drain_all();
+    if (is_ctl_lane0())
+        __hip_atomic_fetch_add(bar_counter(P, blockIdx.x % bar_groups(P)), 1ull,
+                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Arrival on a local counter (one add per arriving workgroup) after phase ti.
+__device__ __forceinline__ void local_arrive(const StepParams &P, unsigned *cnt, int ti) {
+    if (is_ctl_lane0()) trace_stamp(P, ti, 0);
+    drain_all();
+    if (is_ctl_lane0())
+        __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Spin until *flag_fn() says done; gives up (raising KL_DEVERR_BARRIER) after
+// kSpinLimit polls or as soon as another wait has given up.
+template <class Done>
+__device__ __forceinline__ void spin_until(const StepParams &P, Done &&done) {
+    for (int spins = 1;; ++spins) {
+        if (done()) return;
+        if ((spins & 63) == 0 &&
+            (__hip_atomic_load(P.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) &
+             KL_DEVERR_BARRIER))
+            return;
+        if (spins >= kSpinLimit) {
+            if ((threadIdx.x & 63) == 0)
+                __hip_atomic_fetch_or(P.err, KL_DEVERR_BARRIER, __ATOMIC_RELAXED,
+                                      __HIP_MEMORY_SCOPE_AGENT);
+            return;
+        }
+    }
+}
+
+__device__ __forceinline__ void bar_wait(const StepParams &P, int k, int ti) {
+    if ((threadIdx.x >> 6) == kCtlWave) {
+        const int lane = threadIdx.x & 63, ng = bar_groups(P);
+        const bool mine = lane < ng;
+        const unsigned long long target =
+            mine ? bar_bases(P)[lane] + (unsigned long long)(k + 1) * bar_gsize(P, ng, lane) : 0ull;
+        if (lane == 0) trace_stamp(P, ti, 1);
+        spin_until(P, [&]() {
+            const bool d = !mine || (long long)(ld_dev_u64(bar_counter(P, lane)) - target) >= 0;
+            return __all(d) != 0;
+        });
+        if (lane == 0) trace_stamp(P, ti, 2);
+    }
+    __syncthreads();
+}
+
+// Wait until a local counter (monotonic within a step; zeroed by the
+// embedding phase) reaches target.
+__device__ __forceinline__ void local_wait(const StepParams &P, const unsigned *cnt,
+                                           unsigned target, int ti) {
+    if (is_ctl_lane0()) {
+        trace_stamp(P, ti, 1);
+        spin_until(P, [&]() {
+            return (int)(__hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) -
+                         target) >= 0;
+        });
+        trace_stamp(P, ti, 2);
+    }
+    __syncthreads();
+}
+
+// ---------------------------------------------------------------- params
+//
+// The step kernel is one function per (head_dim, group size), with every
+// phase inlined (no calls: a call would save and restore callee-saved
+// registers through scratch memory on every phase).  Each phase reads the
+// step parameters from the kernel-argument segment itself, through an
+// address the compiler cannot see through, so the loads stay inside the
+// phase instead of being hoisted out of the layer loop, where the values of
+// all phases together would exhaust the registers.
+#define KL_KARG __attribute__((address_space(4)))
+
+typedef uint64_t KArg;
+
+__device__ __forceinline__ KArg kernarg_address() {
+#if defined(__HIP_DEVICE_COMPILE__)
+    return (KArg)(const KL_KARG char *)__builtin_amdgcn_kernarg_segment_ptr();
+#else
+    return 0;
+#endif
+}
+
+__device__ __forceinline__ StepParams load_params(KArg ka) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    unsigned lo = __builtin_amdgcn_readfirstlane((unsigned)ka);
+    unsigned hi = __builtin_amdgcn_readfirstlane((unsigned)(ka >> 32));
+    asm volatile("" : "+s"(lo), "+s"(hi));
+    const KL_KARG StepParams *p = (const KL_KARG StepParams *)(((KArg)hi << 32) | lo);
+    return *p;
+#else
+    return StepParams{};   // the host pass only type-checks device code
+#endif
+}
+
+// ---------------------------------------------------------------- LDS layout
+
+// Offsets (in floats) come from the host, which sizes the allocation.
+struct Lds {
+    float *a;     // activation vector (max K extent); aliased by the attention area
+    float *attn;  // attention scratch (same storage as a)
+    float *red;   // [kWaves][kRgBatch][kTileRows] GEMV partial sums
+    float *sm;    // small reductions and flags (64 floats)
+    unsigned long long *bar;   // [kBarGroups] barrier bases of this launch
+};
+
+__device__ __forceinline__ Lds lds_layout(char *smem, const StepParams &P) {
+    Lds s;
+    float *f = reinterpret_cast<float *>(smem);
+    s.a = f;
+    s.attn = f;
+    s.red = f + P.lds_red;
+    s.sm = f + P.lds_sm;
+    s.bar = reinterpret_cast<unsigned long long *>(f + P.lds_bar);
+    return s;
+}
+
+__device__ __forceinline__ unsigned long long *bar_bases(const StepParams &P) {
+    return lds_layout(kl_smem, P).bar;
+}
+
+// ---------------------------------------------------------------- activations
+
+// Control wave only: copy 'bytes' (a multiple of 16; src and dst 16-byte
+// aligned) from device memory straight to LDS (global_load_lds, 16 bytes per
+// lane, device-coherent: cache-policy bits sc1), then wait for the copy.  The
+// control wave has no weight loads in flight, so the copy does not queue
+// behind them.
+constexpr int kLdsCoherent = 16;
+__device__ __forceinline__ void ctl_copy_to_lds(const void *src, void *dst, int bytes) {
+    const int lane = threadIdx.x & 63;
+    const char *s = static_cast<const char *>(src);
+    char *d = static_cast<char *>(dst);
+    for (int off = 0; off < bytes; off += 64 * 16) {
+        if (off + lane * 16 < bytes)
+            __builtin_amdgcn_global_load_lds(s + off + lane * 16, d + off, 16, 0, kLdsCoherent);
+    }
+}
+__device__ __forceinline__ void ctl_copy_wait() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+// Copy a device-coherent fp32 vector of n values into LDS, zero up to npad
+// (loads are issued in batches of kStageBatch per thread before any is used).
+constexpr int kStageBatch = 8;
+__device__ __forceinline__ void stage_vec(const float *__restrict__ src, int n, int npad,
+                                          float *a) {
+    for (int i0 = threadIdx.x; i0 < npad; i0 += kStageBatch * kThreads) {
+        float v[kStageBatch];
+#pragma unroll
+        for (int k = 0; k < kStageBatch; ++k) {
+            const int i = i0 + k * kThreads;
+            v[k] = i < n ? ld_dev(src + i) : 0.f;
+        }
+#pragma unroll
+        for (int k = 0; k < kStageBatch; ++k) {
+            const int i = i0 + k * kThreads;
+            if (i < npad) a[i] = v[k];
+        }
+    }
+    __syncthreads();
+}
+
+// a[i] = x[i] * rsqrt(mean(x^2) + eps) * gain[i] for i < n, 0 up to npad,
+// x read from the fixed-point residual stream.  The gain is loaded in the
+// same batch as x (a dependent second batch would cost a second memory round
+// trip, ~2 us when HBM is saturated), and so are the ne floats of an optional
+// extra vector (esrc -> edst in LDS), e.g. the RoPE row the epilogue needs.
+__device__ __forceinline__ void stage_rmsnorm(const long long *__restrict__ xf,
+                                              const float *__restrict__ gain, int n, int npad,
+                                              float eps, float *a, float *sm,
+                                              const float *esrc = nullptr, float *edst = nullptr,
+                                              int ne = 0) {
+    for (int i0 = threadIdx.x; i0 < npad; i0 += kStageBatch * kThreads) {
+        long long v[kStageBatch];
+        float gv[kStageBatch];
+        float ev = 0.f;
+        const bool first = i0 == (int)threadIdx.x;
+#pragma unroll
+        for (int k = 0; k < kStageBatch; ++k) {
+            const int i = i0 + k * kThreads;
+            v[k] = i < n ? (long long)ld_dev_u64(xf + i) : 0ll;
+            gv[k] = i < n ? gain[i] : 0.f;
+        }
+        if (first && (int)threadIdx.x < ne) ev = esrc[threadIdx.x];
+#pragma unroll
+        for (int k = 0; k < kStageBatch; ++k) {
+            const int i = i0 + k * kThreads;
+            if (i < npad) {
+                a[i] = from_fix(v[k]);
+                a[npad + i] = gv[k];
+            }
+        }
+        if (first && (int)threadIdx.x < ne) edst[threadIdx.x] = ev;
+    }
+    __syncthreads();
+    float ss = 0.f;
+    for (int i = threadIdx.x; i < n; i += kThreads) ss = fmaf(a[i], a[i], ss);
+    ss = block_sum(ss, sm);
+    const float r = 1.0f / sqrtf(ss / (float)n + eps);
+    for (int i = threadIdx.x; i < n; i += kThreads) a[i] = a[i] * r * a[npad + i];
+    __syncthreads();
+}
+
+// ---------------------------------------------------------------- GEMV engine
+//
+// y_b[r] = sum_k W[r][k] a_b[k] for the rows of the row groups a workgroup owns in a
+// packed matrix with KT k-tiles per row group, for each sequence b.  Each
+// wave takes a fixed slice of the k-tiles of every row group (split-K inside
+// the workgroup), keeps U tile loads in flight, and reduces its partial dot
+// products over the 8 lanes of a row with DPP.  The slices are summed in wave
+// order through LDS, and epi(b, r, y_r, y_r+1) is called once per row pair.
+// Row groups are processed in batches of kRgBatch.  The first loads are
+// issued before wait() (the grid barrier that publishes the activations) and
+// before stage(b) (which fills a with sequence b's activation vector); each
+// next batch's first loads are issued before the previous batch's reduction.
+constexpr int kGemvDepth = 16;   // tile loads in flight per wave (16 KiB)
+
+// The ring of tile loads must stay in flight across loop iterations, the
+// grid barrier and the activation staging, and the compiler only places a
+// precise "wait for the oldest load" (vmcnt(U-1)) when every path issues the
+// same loads.  So the ring is refilled unconditionally: once the batch's real
+// tiles are exhausted, a slot is refilled from a 16-byte dummy line that all
+// lanes share (one cache line per wave), and only the consumption of a slot
+// is conditional.
+//
+// A workgroup owns the row groups first, first + stride, ... (count of
+// them).  The phases use stride 1 (a contiguous block per workgroup): a
+// strided assignment (stride = grid size) was measured no faster.
+struct RgRange { int first, count; };
+__device__ __forceinline__ RgRange own_rgs(int nrg, const StepParams &P) {
+    int a, b;
+    split_range(nrg, P.nwg, blockIdx.x, a, b);
+    return RgRange{a, b - a};
+}
+
+// Two ways to share a row group's tiles among the waves:
+//   split-K   (long rows, KT >= 2 kWaves): wave w takes the k-tiles
+//             [w KT / kWaves, (w + 1) KT / kWaves) of every row group; the
+//             wave partial sums are added in wave order through LDS;
+//   row-split (short rows): wave w takes whole row groups w, w + kWaves, ...
+//             of the batch and needs no cross-wave sum.
+// Both orders are fixed by the partition alone.
+template <bool RowSplit, class Wait, class Stage, class Epi>
+__device__ __forceinline__ void gemv_rows(const uint8_t *__restrict__ W, int KT, int first,
+                                          int count, int stride, int B,
+                                          const float *__restrict__ a, float *red,
+                                          const uint8_t *dummy, Wait &&wait, Stage &&stage,
+                                          Epi &&epi) {
+    constexpr int U = kGemvDepth;
+    constexpr int BATCH = RowSplit ? kWaves * kRgBatch : kRgBatch;   // row groups per LDS round
+    // wave-uniform values live in scalar registers, so every branch below is
+    // a scalar branch
+    const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    const int row = lane >> 3, sub = lane & 7;
+    const int kt0 = RowSplit ? 0 : (wid * KT) / kWaves;
+    const int nk = RowSplit ? KT : ((wid + 1) * KT) / kWaves - kt0;
+    const int rstep = RowSplit ? kWaves : 1;   // a wave's next row group, in batch items
+    const uint8_t *base = W + (size_t)lane * 16;
+    const float *abase = a + sub * 8;
+    u32x4 buf[U];
+    int n = 0, ltile = 0, lk = 0, left = 0;   // batch items; next tile, its k index; tiles left
+
+    // from a wave's last tile of one row group to its first of the next
+    const int jump = (rstep * stride - 1) * KT + (KT - nk) + 1;
+    // load the next tile of the batch, or the dummy line (branch-free)
+    auto load_next = [&]() {
+        const int t = __builtin_amdgcn_readfirstlane(ltile);
+        const bool real = left > 0;
+        const u32x4 v = ld_stream_16B(real ? base + (size_t)t * kTileBytes : dummy);
+        const bool wrap = lk + 1 == nk;
+        ltile = real ? ltile + (wrap ? jump : 1) : ltile;
+        lk = real ? (wrap ? 0 : lk + 1) : lk;
+        left = real ? left - 1 : left;
+        return v;
+    };
+    auto start = [&](int ib) {   // batch of row groups ib .. ib + BATCH - 1
+        const int nb = min(BATCH, count - ib);
+        const int mine = RowSplit ? (nb > wid ? (nb - wid + kWaves - 1) / kWaves : 0) : nb;
+        n = nk * mine;
+        left = n;
+        ltile = (first + (ib + (RowSplit ? wid : 0)) * stride) * KT + kt0;
+        lk = 0;
+#pragma unroll
+        for (int s = 0; s < U; ++s) buf[s] = load_next();
+    };
+
+    // the control wave takes part in the staging and the epilogue only
+    const bool compute = wid < kWaves;
+    const bool has_rows = count > 0;
+    if (has_rows && compute) start(0);
+    wait();
+    if (!has_rows) return;
+    for (int b = 0; b < B; ++b) {
+        for (int ib = 0; ib < count; ib += BATCH) {
+            if ((b > 0 || ib > 0) && compute) start(ib);
+            if (ib == 0) stage(b);
+            const int nrg = min(BATCH, count - ib);
+            int cr = RowSplit ? wid : 0, ck = 0;   // batch item of the row group in progress
+            float acc = 0.f;
+            // item i sits in slot i % U and is refilled with item i + U (or
+            // the dummy line) right after it is consumed
+            if (compute)
+            for (int i0 = 0; i0 < n; i0 += U) {
+#pragma unroll
+                for (int s = 0; s < U; ++s) {
+                    if (i0 + s < n) {
+                        const u32x4 wv = buf[s];
+                        const float *ap = abase + (kt0 + ck) * kTileK;
+                        const float4 a0 = *reinterpret_cast<const float4 *>(ap);
+                        const float4 a1 = *reinterpret_cast<const float4 *>(ap + 4);
+                        acc = fmaf(bf_lo(wv.x), a0.x, acc);
+                        acc = fmaf(bf_hi(wv.x), a0.y, acc);
+                        acc = fmaf(bf_lo(wv.y), a0.z, acc);
+                        acc = fmaf(bf_hi(wv.y), a0.w, acc);
+                        acc = fmaf(bf_lo(wv.z), a1.x, acc);
+                        acc = fmaf(bf_hi(wv.z), a1.y, acc);
+                        acc = fmaf(bf_lo(wv.w), a1.z, acc);
+                        acc = fmaf(bf_hi(wv.w), a1.w, acc);
+                        if (++ck == nk) {
+                            const float t = sum8(acc);
+                            if (sub == 0) {
+                                if (RowSplit) red[cr * kTileRows + row] = t;
+                                else red[(wid * kRgBatch + cr) * kTileRows + row] = t;
+                            }
+                            acc = 0.f;
+                            ck = 0;
+                            cr += rstep;
+                        }
+                    }
+                    buf[s] = load_next();
+                }
+            }
+            __syncthreads();
+            for (int t = threadIdx.x; t < nrg * (kTileRows / 2); t += kThreads) {
+                const int rgi = t / (kTileRows / 2), pr = (t % (kTileRows / 2)) * 2;
+                float y0 = 0.f, y1 = 0.f;
+                if (RowSplit) {
+                    y0 = red[rgi * kTileRows + pr];
+                    y1 = red[rgi * kTileRows + pr + 1];
+                } else {
+                    for (int w = 0; w < kWaves; ++w) {
+                        if (((w + 1) * KT) / kWaves == (w * KT) / kWaves) continue;   // empty slice
+                        y0 += red[(w * kRgBatch + rgi) * kTileRows + pr];
+                        y1 += red[(w * kRgBatch + rgi) * kTileRows + pr + 1];
+                    }
+                }
+                epi(b, (first + (ib + rgi) * stride) * kTileRows + pr, y0, y1);
+            }
+            __syncthreads();
+        }
+    }
+}
+
+// Row groups are shared split-K when they are long enough for every wave to
+// hold two or more tiles, else row-split.
+template <class Wait, class Stage, class Epi>
+__device__ __forceinline__ void gemv_phase(const uint8_t *__restrict__ W, int KT, int first,
+                                           int count, int stride, int B,
+                                           const float *__restrict__ a, float *red,
+                                           const uint8_t *dummy, Wait &&wait, Stage &&stage,
+                                           Epi &&epi) {
+    if (KT >= 2 * kWaves)
+        gemv_rows<false>(W, KT, first, count, stride, B, a, red, dummy, wait, stage, epi);
+    else
+        gemv_rows<true>(W, KT, first, count, stride, B, a, red, dummy, wait, stage, epi);
+}
+
+// ---------------------------------------------------------------- batched engine
+//
+// Y[r][b] = sum_k W[r][k] X[b][k] on the matrix cores (v_mfma_f32_16x16x32_bf16:
+// D[16x16] += A[16x32] B[32x16]) for the row groups first .. first + count - 1
+// and up to kGemmBatch sequences b0 .. b0 + nb - 1.  A block is 16 weight
+// rows (2 row groups); A = W[16 rows][32 k], B = X[32 k][16 sequences], two
+// products per 32 columns cover 32 sequences.  Operand layouts: A lane l holds
+// A[l % 16][8 (l / 16) .. +7], B lane l holds B[8 (l / 16) .. +7][l % 16], D
+// lane l holds D[4 (l / 16) + v][l % 16].  Weight tiles arrive through the
+// same ring of 16-byte loads as the GEMV path and are re-laid out through a
+// per-wave LDS slot (2 KiB: the two tiles of a block at one k-tile).  X is
+// staged in LDS in chunks of kGemmChunkK columns (bf16, kActStride per row),
+// double-buffered: stage(c, buf) fills chunk c.  Waves share blocks and
+// k-tiles: with nblk >= 8 blocks each wave takes whole blocks, else
+// ksplit = 8 / nblk waves share a block's k-tiles and their partial products
+// are added in wave order.
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+struct GemmLds {
+    uint16_t *act[2];   // [kGemmBatch][kActStride] bf16
+    uint8_t *wslot;     // [kWaves][2048]
+    float *cred;        // [kWaves][16][32]
+};
+
+__device__ __forceinline__ GemmLds gemm_lds(char *smem) {
+    GemmLds g;
+    g.act[0] = reinterpret_cast<uint16_t *>(smem);
+    g.act[1] = reinterpret_cast<uint16_t *>(smem + kGemmActBytes);
+    g.wslot = reinterpret_cast<uint8_t *>(smem + 2 * kGemmActBytes);
+    g.cred = reinterpret_cast<float *>(smem + 2 * kGemmActBytes + kWaves * 2048);
+    return g;
+}
+
+//
+// The K extent may be split over several packed matrices of ktg k-tiles each
+// (the O projection per KV head, the down projection per FFN column block),
+// gstride tiles apart: k-tile kt of row group r is tile
+// (kt / ktg) gstride + r ktg + kt % ktg.
+template <class Stage, class Epi>
+__device__ __forceinline__ void gemm_rows(const uint8_t *__restrict__ W, int KT, int first,
+                                          int count, int ktg, size_t gstride, int b0, int nb,
+                                          const uint8_t *dummy, const GemmLds &L,
+                                          bool async_stage, Stage &&stage, Epi &&epi) {
+    constexpr int U = kGemvDepth;
+    constexpr int CT = kGemmChunkK / kTileK;   // k-tiles per chunk
+    const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    const bool compute = wid < kWaves;
+    const int nblk = (count + 1) / 2;
+    const int nkc = (KT + CT - 1) / CT;
+    const int ksplit = nblk >= 8 ? 1 : (nblk >= 4 ? 2 : (nblk >= 2 ? 4 : 8));
+    const int slots = kWaves / ksplit;            // blocks worked on at once
+    const int slot = wid / ksplit, kpart = wid % ksplit;
+    uint8_t *ws = L.wslot + (size_t)wid * 2048;
+    const uint8_t *tbase = W + (size_t)lane * 16;
+    const uint8_t *zbase = dummy + (size_t)lane * 16;   // 1 KiB of zeros
+
+    // zero the padding sequences of both activation buffers once
+    for (int t = threadIdx.x; t < 2 * (kGemmBatch - nb) * kActStride / 8; t += kThreads) {
+        const int half = (kGemmBatch - nb) * kActStride / 8;
+        uint16_t *buf = L.act[t / half];
+        reinterpret_cast<u32x4 *>(buf + nb * kActStride)[t % half] = u32x4{0u, 0u, 0u, 0u};
+    }
+
+    for (int bg0 = 0; bg0 < nblk; bg0 += slots * kGemmMaxBlk) {
+        // my blocks in this group: bg0 + slot + i * slots, i < nbw
+        const int left_blk = min(nblk - bg0, slots * kGemmMaxBlk);
+        const int nbw = left_blk > slot ? (left_blk - slot + slots - 1) / slots : 0;
+        auto nkw_of = [&](int c) {   // my k-tiles in chunk c
+            const int lim = min(CT, KT - c * CT);
+            return lim > kpart ? (lim - kpart + ksplit - 1) / ksplit : 0;
+        };
+        // items of chunk c: (block i, k-tile q, row group t), padded with
+        // zero-tile items to a multiple of U so that every chunk starts at
+        // ring slot 0 (the slot of an item is then known at compile time)
+        auto items_of = [&](int c) { return compute ? nbw * nkw_of(c) * 2 : 0; };
+        auto padded = [&](int n) { return (n + U - 1) / U * U; };
+        // load generator: chunk gc, item gj of the chunk
+        int gc = 0, gj = 0, gn = items_of(0), gnk = max(1, nkw_of(0));
+        auto load_next = [&]() {
+            const bool real = gc < nkc && gj < gn;
+            int tile = 0;
+            bool inb = false;
+            if (real) {
+                const int t = gj & 1, q = (gj >> 1) % gnk, i = (gj >> 1) / gnk;
+                const int rgl = 2 * (bg0 + slot + i * slots) + t;   // row group in this range
+                const int kt = gc * CT + kpart + q * ksplit;
+                inb = rgl < count;
+                tile = __builtin_amdgcn_readfirstlane(
+                    (int)((kt / ktg) * gstride) + (first + rgl) * ktg + kt % ktg);
+            }
+            const u32x4 v = ld_stream_16B(inb ? tbase + (size_t)tile * kTileBytes : zbase);
+            if (gc < nkc && ++gj >= padded(gn)) {
+                gj = 0;
+                do {   // (chunks without items of this wave take no ring slots)
+                    ++gc;
+                    gn = gc < nkc ? items_of(gc) : 0;
+                    gnk = gc < nkc ? max(1, nkw_of(gc)) : 1;
+                } while (gc < nkc && gn == 0);
+            }
+            return v;
+        };
+        while (gc < nkc && gn == 0) {
+            ++gc;
+            gn = gc < nkc ? items_of(gc) : 0;
+            gnk = gc < nkc ? max(1, nkw_of(gc)) : 1;
+        }
+        u32x4 buf[U];
+        if (compute) {   // (the control wave keeps its load queue empty)
+#pragma unroll
+            for (int s = 0; s < U; ++s) buf[s] = load_next();
+        }
+
+        f32x4 acc[kGemmMaxBlk][2];
+#pragma unroll
+        for (int i = 0; i < kGemmMaxBlk; ++i)
+            acc[i][0] = acc[i][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+        stage(0, L.act[0]);
+        __syncthreads();
+        for (int c = 0; c < nkc; ++c) {
+            const uint16_t *act = L.act[c & 1];
+            if (async_stage && c + 1 < nkc) stage(c + 1, L.act[(c + 1) & 1]);
+            const int n = items_of(c), nkw = nkw_of(c);
+            for (int j0 = 0; j0 < padded(n); j0 += U) {
+#pragma unroll
+                for (int s = 0; s < U; ++s) {
+                    const int j = j0 + s;
+                    if (j < n) {
+                        // tile of row group (j & 1) of the block -> the wave's slot
+                        *reinterpret_cast<u32x4 *>(ws + (s & 1) * 1024 + lane * 16) = buf[s];
+                        if (s & 1) {
+                            const int i = (j >> 1) / nkw, ktl = kpart + ((j >> 1) % nkw) * ksplit;
+#pragma unroll
+                            for (int st = 0; st < 2; ++st) {
+                                const int r16 = lane & 15, ko = 4 * st + (lane >> 4);
+                                const bf16x8 a = *reinterpret_cast<const bf16x8 *>(
+                                    ws + (r16 >> 3) * 1024 + ((r16 & 7) * 8 + ko) * 16);
+#pragma unroll
+                                for (int h = 0; h < 2; ++h) {
+                                    const int b = h * 16 + (lane & 15);
+                                    const int k = ktl * kTileK + 32 * st + 8 * (lane >> 4);
+                                    const bf16x8 x = *reinterpret_cast<const bf16x8 *>(
+                                        act + b * kActStride + k);
+#pragma unroll
+                                    for (int ii = 0; ii < kGemmMaxBlk; ++ii)
+                                        if (ii == i)
+                                            acc[ii][h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                                                a, x, acc[ii][h], 0, 0, 0);
+                                }
+                            }
+                        }
+                    }
+                    buf[s] = load_next();
+                }
+            }
+            __syncthreads();   // chunk c consumed by every wave; chunk c + 1 staged
+            if (!async_stage && c + 1 < nkc) {
+                stage(c + 1, L.act[(c + 1) & 1]);
+                __syncthreads();
+            }
+        }
+        // partial products of each block -> LDS, summed over the sharing waves
+        for (int i = 0; i < kGemmMaxBlk; ++i) {
+            if (bg0 + i * slots >= nblk) break;   // (uniform)
+            if (compute) {
+#pragma unroll
+                for (int ii = 0; ii < kGemmMaxBlk; ++ii) {
+                    if (ii != i) continue;
+#pragma unroll
+                    for (int h = 0; h < 2; ++h)
+#pragma unroll
+                        for (int v = 0; v < 4; ++v)
+                            L.cred[(wid * 16 + 4 * (lane >> 4) + v) * 32 + h * 16 + (lane & 15)] =
+                                acc[ii][h][v];
+                }
+            }
+            __syncthreads();
+            // blocks bg0 + i * slots + s, s < slots; rows in pairs, sequences b < nb
+            for (int t = threadIdx.x; t < slots * 8 * nb; t += kThreads) {
+                const int s = t / (8 * nb), rem = t % (8 * nb), pr = (rem / nb) * 2, b = rem % nb;
+                const int blk = bg0 + i * slots + s;
+                if (blk >= nblk || 2 * blk * kTileRows + pr >= count * kTileRows) continue;
+                float y0 = 0.f, y1 = 0.f;
+                for (int kp = 0; kp < ksplit; ++kp) {
+                    const int w = s * ksplit + kp;
+                    y0 += L.cred[(w * 16 + pr) * 32 + b];
+                    y1 += L.cred[(w * 16 + pr + 1) * 32 + b];
+                }
+                epi(b0 + b, (first + 2 * blk) * kTileRows + pr, y0, y1);
+            }
+            __syncthreads();
+        }
+    }
+}
+
+
+// ---------------------------------------------------------------- phases
+//
+// Synchronization between the phases of a layer (l):
+//   grid barrier   after embed, oproj and down: the residual stream is
+//                  complete; qkv, gateup and head wait on it.
+//   cnt_qkv[g]     qkv -> attn: the workgroups of KV head g compute exactly
+//                  the q/k/v rows of that head, so the attention of head g
+//                  waits only for them (Sg arrivals per layer).
+//   cnt_attn[g]    attn -> oproj: the chunk results of KV head g (B * C per
+//                  layer); the same workgroups then merge them and apply the
+//                  O-projection columns of head g, adding into the residual.
+//   cnt_gu[j]      gateup -> down: column block j of the FFN (Rc workgroups
+//                  compute its SwiGLU values; the same Rc workgroups then
+//                  apply the matching columns of the down projection).
+// Local counters grow monotonically within a step (zeroed by the embedding
+// phase); their targets are (l + 1) times the arrivals per layer.
+// Every workgroup arrives on, and waits on, every grid barrier.
+
+// ---------------------------------------------------------------- batched phases
+//
+// A weight phase runs the GEMV engine for batches below kMfmaBatch and the
+// matrix-core engine otherwise (sequences in groups of kGemmBatch; the
+// weights stream once per group).  In the batched path every input is staged
+// as bf16 chunks: prep() runs once after wait(), stageb(c, b0, nb, buf) fills
+// chunk c for sequences b0 .. b0 + nb - 1 (async: the control wave copies it
+// while the compute waves work on the previous chunk).
+template <bool BAT, class Wait, class Prep, class Stage1, class StageB, class Epi>
+__device__ __forceinline__ void weight_phase(const StepParams &P, const Lds &S,
+                                             const uint8_t *W, int KT, int first, int count,
+                                             Wait &&wait, Prep &&prep, Stage1 &&stage1,
+                                             bool async, StageB &&stageb, Epi &&epi,
+                                             int ktg = 0, size_t gstride = 0) {
+    if constexpr (!BAT) {
+        gemv_phase(W, KT, first, count, 1, P.B, S.a, S.red, P.dummy, wait, stage1, epi);
+        return;
+    }
+    wait();
+    prep();
+    const GemmLds L = gemm_lds(kl_smem);
+    for (int b0 = 0; b0 < P.B; b0 += kGemmBatch) {
+        const int nb = min(kGemmBatch, P.B - b0);
+        gemm_rows(W, KT, first, count, ktg ? ktg : KT, gstride, b0, nb, P.dummy, L, async,
+                  [&](int c, uint16_t *buf) { stageb(c, b0, nb, buf); }, epi);
+    }
+}
+
+// Batched RMSNorm: act[b][k] = bf16(x_b[k] r_b gain[k]) for every sequence,
+// the (sequence, kGemmChunkK-column slice) items spread over the grid; ends
+// with grid barrier k, after which any workgroup may stage any slice.
+__device__ __forceinline__ void norm_batched(const StepParams &P, const Lds &S,
+                                             const float *gain, int k) {
+    const int ns = (P.Hp + kGemmChunkK - 1) / kGemmChunkK;
+    for (int it = blockIdx.x; it < P.B * ns; it += P.nwg) {
+        const int b = it / ns, c0 = (it % ns) * kGemmChunkK;
+        const int c1 = min(P.Hp, c0 + kGemmChunkK);
+        stage_rmsnorm(P.xf + (size_t)b * P.Hp, gain, P.H, P.Hp, P.eps, S.a, S.sm);
+        for (int kk = c0 + 2 * (int)threadIdx.x; kk < c1; kk += 2 * kThreads)
+            st_dev_u32(reinterpret_cast<unsigned *>(P.act + (size_t)b * P.Hp + kk),
+                       (unsigned)f2bf(S.a[kk]) | ((unsigned)f2bf(S.a[kk + 1]) << 16));
+        __syncthreads();   // (S.a is restaged by the next item)
+    }
+    bar_arrive(P, k, -1);
+    bar_wait(P, k, -1);
+}
+
+// Chunk c of the normalised activations (control wave: memory-to-LDS copies).
+__device__ __forceinline__ void stage_act_chunk(const StepParams &P, int c, int b0, int nb,
+                                                uint16_t *buf) {
+    if ((threadIdx.x >> 6) != kCtlWave) return;
+    const int k0 = c * kGemmChunkK, kc = min(kGemmChunkK, P.Hp - k0);
+    for (int b = 0; b < nb; ++b)
+        ctl_copy_to_lds(P.act + (size_t)(b0 + b) * P.Hp + k0, buf + b * kActStride, kc * 2);
+    ctl_copy_wait();
+}
+
+// Chunk c of a bf16 matrix src[b][ld] with K columns (control wave: memory-to-
+// LDS copies, so the compute waves keep working on the previous chunk).
+__device__ __forceinline__ void stage_bf16_chunk(const uint16_t *src, int ld, int K, int c, int b0,
+                                                 int nb, uint16_t *buf) {
+    if ((threadIdx.x >> 6) != kCtlWave) return;
+    const int k0 = c * kGemmChunkK, kc = min(kGemmChunkK, K - k0);
+    for (int b = 0; b < nb; ++b)
+        ctl_copy_to_lds(src + (size_t)(b0 + b) * ld + k0, buf + b * kActStride, kc * 2);
+    ctl_copy_wait();
+}
+
+// Chunk c of the merged attention output of KV head g, as bf16.  With one
+// chunk per (sequence, head), o = A / L: every thread loads four outputs
+// (16 bytes) and their head's sum in one batch; otherwise the chunk results
+// are merged as in merge_chunks.
+template <int D, int G>
+__device__ __forceinline__ void stage_o_chunk(const StepParams &P, int g, int c, int b0, int nb,
+                                              uint16_t *buf) {
+    const int C = P.C, k0 = c * kGemmChunkK, kc = min(kGemmChunkK, G * D - k0);
+    if (C == 1) {
+        constexpr int NB = 8;   // float4 loads per thread in flight
+        const int n4 = nb * kc / 4;
+        for (int t0 = threadIdx.x; t0 < n4; t0 += NB * kThreads) {
+            float4 v[NB];
+            float den[NB];
+#pragma unroll
+            for (int q = 0; q < NB; ++q) {
+                const int t = t0 + q * kThreads;
+                v[q] = make_float4(0.f, 0.f, 0.f, 0.f);
+                den[q] = 1.f;
+                if (t < n4) {
+                    const int b = t / (kc / 4), j = k0 + (t % (kc / 4)) * 4;
+                    const size_t item = (size_t)(b0 + b) * P.nkv + g;
+                    const u32x4 u = ld_dev_16B(P.part_o + item * G * D + j);
+                    v[q] = make_float4(__uint_as_float(u.x), __uint_as_float(u.y),
+                                       __uint_as_float(u.z), __uint_as_float(u.w));
+                    den[q] = ld_dev(P.part_s + (item * G + j / D) * 2 + 1);
+                }
+            }
+#pragma unroll
+            for (int q = 0; q < NB; ++q) {
+                const int t = t0 + q * kThreads;
+                if (t < n4) {
+                    const int b = t / (kc / 4), jj = (t % (kc / 4)) * 4;
+                    const float r = 1.0f / den[q];
+                    unsigned *dst = reinterpret_cast<unsigned *>(buf + b * kActStride + jj);
+                    dst[0] = (unsigned)f2bf(v[q].x * r) | ((unsigned)f2bf(v[q].y * r) << 16);
+                    dst[1] = (unsigned)f2bf(v[q].z * r) | ((unsigned)f2bf(v[q].w * r) << 16);
+                }
+            }
+        }
+        return;
+    }
+    for (int t = threadIdx.x; t < nb * kc; t += kThreads) {
+        const int b = t / kc, j = k0 + t % kc, h = j / D;
+        const size_t item0 = ((size_t)(b0 + b) * P.nkv + g) * C;
+        float M = -INFINITY;
+        for (int cc = 0; cc < C; ++cc) M = fmaxf(M, ld_dev(P.part_s + ((item0 + cc) * G + h) * 2));
+        float num = 0.f, den = 0.f;
+        for (int cc = 0; cc < C; ++cc) {
+            const float m = ld_dev(P.part_s + ((item0 + cc) * G + h) * 2);
+            const float w = (m == -INFINITY) ? 0.f : expf(m - M);
+            num = fmaf(ld_dev(P.part_o + (item0 + cc) * G * D + j), w, num);
+            den = fmaf(ld_dev(P.part_s + ((item0 + cc) * G + h) * 2 + 1), w, den);
+        }
+        buf[b * kActStride + (j - k0)] = f2bf(num / den);
+    }
+}
+
+// Chunk c of the merged attention output of all heads (K = n_heads d), as
+// bf16; same scheme as stage_o_chunk.
+template <int D, int G>
+__device__ __forceinline__ void stage_o_full(const StepParams &P, int c, int b0, int nb,
+                                             uint16_t *buf) {
+    const int C = P.C, A = P.nq * D, k0 = c * kGemmChunkK, kc = min(kGemmChunkK, A - k0);
+    if (C == 1) {   // item (b, g) holds heads g G .. g G + G - 1 contiguously: index b A + j
+        constexpr int NB = 8;
+        const int n4 = nb * kc / 4;
+        for (int t0 = threadIdx.x; t0 < n4; t0 += NB * kThreads) {
+            float4 v[NB];
+            float den[NB];
+#pragma unroll
+            for (int q = 0; q < NB; ++q) {
+                const int t = t0 + q * kThreads;
+                v[q] = make_float4(0.f, 0.f, 0.f, 0.f);
+                den[q] = 1.f;
+                if (t < n4) {
+                    const int b = t / (kc / 4), j = k0 + (t % (kc / 4)) * 4;
+                    const u32x4 u = ld_dev_16B(P.part_o + (size_t)(b0 + b) * A + j);
+                    v[q] = make_float4(__uint_as_float(u.x), __uint_as_float(u.y),
+                                       __uint_as_float(u.z), __uint_as_float(u.w));
+                    den[q] = ld_dev(P.part_s + ((size_t)(b0 + b) * P.nq + j / D) * 2 + 1);
+                }
+            }
+#pragma unroll
+            for (int q = 0; q < NB; ++q) {
+                const int t = t0 + q * kThreads;
+                if (t < n4) {
+                    const int b = t / (kc / 4), jj = (t % (kc / 4)) * 4;
+                    const float r = 1.0f / den[q];
+                    unsigned *dst = reinterpret_cast<unsigned *>(buf + b * kActStride + jj);
+                    dst[0] = (unsigned)f2bf(v[q].x * r) | ((unsigned)f2bf(v[q].y * r) << 16);
+                    dst[1] = (unsigned)f2bf(v[q].z * r) | ((unsigned)f2bf(v[q].w * r) << 16);
+                }
+            }
+        }
+        return;
+    }
+    for (int t = threadIdx.x; t < nb * kc; t += kThreads) {
+        const int b = t / kc, j = k0 + t % kc, h = j / D, g = h / G, hl = h % G, dd = j % D;
+        const size_t item0 = ((size_t)(b0 + b) * P.nkv + g) * C;
+        float M = -INFINITY;
+        for (int cc = 0; cc < C; ++cc)
+            M = fmaxf(M, ld_dev(P.part_s + ((item0 + cc) * G + hl) * 2));
+        float num = 0.f, den = 0.f;
+        for (int cc = 0; cc < C; ++cc) {
+            const float m = ld_dev(P.part_s + ((item0 + cc) * G + hl) * 2);
+            const float w = (m == -INFINITY) ? 0.f : expf(m - M);
+            num = fmaf(ld_dev(P.part_o + (item0 + cc) * G * D + hl * D + dd), w, num);
+            den = fmaf(ld_dev(P.part_s + ((item0 + cc) * G + hl) * 2 + 1), w, den);
+        }
+        buf[b * kActStride + (j - k0)] = f2bf(num / den);
+    }
+}
+
+// Chunk c of FFN column block j's SwiGLU values, as bf16 (16-byte loads, in
+// one batch per thread); j < 0: chunk c of all columns.
+__device__ __forceinline__ void stage_m_chunk(const StepParams &P, int j, int c, int b0, int nb,
+                                              uint16_t *buf) {
+    constexpr int NB = 8;
+    const int kw = j < 0 ? P.Fp : P.KTc * kTileK, k0 = c * kGemmChunkK;
+    const int kc = min(kGemmChunkK, kw - k0);
+    const size_t col0 = j < 0 ? 0 : (size_t)j * kw;
+    const int n4 = nb * kc / 4;
+    for (int t0 = threadIdx.x; t0 < n4; t0 += NB * kThreads) {
+        u32x4 v[NB];
+#pragma unroll
+        for (int q = 0; q < NB; ++q) {
+            const int t = t0 + q * kThreads;
+            v[q] = u32x4{0u, 0u, 0u, 0u};
+            if (t < n4) {
+                const int b = t / (kc / 4), k = (t % (kc / 4)) * 4;
+                v[q] = ld_dev_16B(P.m + (size_t)(b0 + b) * P.Fp + col0 + k0 + k);
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < NB; ++q) {
+            const int t = t0 + q * kThreads;
+            if (t < n4) {
+                const int b = t / (kc / 4), k = (t % (kc / 4)) * 4;
+                unsigned *dst = reinterpret_cast<unsigned *>(buf + b * kActStride + k);
+                dst[0] = (unsigned)f2bf(__uint_as_float(v[q].x)) |
+                         ((unsigned)f2bf(__uint_as_float(v[q].y)) << 16);
+                dst[1] = (unsigned)f2bf(__uint_as_float(v[q].z)) |
+                         ((unsigned)f2bf(__uint_as_float(v[q].w)) << 16);
+            }
+        }
+    }
+}
+
+// Embedding block (Sec. 2): x = E[token] (exact in fixed point).  Workgroup 0
+// records bad token ids and positions, and zeroes the local counters.
+__device__ __forceinline__ void phase_embed(KArg ka, int gwait, int garrive, int ti) {
+    const StepParams P = load_params(ka);
+    if (gwait >= 0) bar_wait(P, gwait, ti);
+    if (blockIdx.x == 0) {
+        for (int b = threadIdx.x; b < P.B; b += kThreads) {
+            const int t = P.tokens[b], p = P.positions[b];
+            int bits = 0;
+            if (t < 0 || t >= P.V) bits |= KL_DEVERR_TOKEN;
+            if (p < 0 || p >= P.cap || p >= P.max_seq) bits |= KL_DEVERR_POSITION;
+            if (bits) atomicOr(P.err, bits);
+        }
+        for (int i = threadIdx.x; i < 2 * P.nkv + P.Sc; i += kThreads)
+            __hip_atomic_store(P.cnt + i, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    const int total = P.B * P.Hp;
+    for (int idx = blockIdx.x * kThreads + threadIdx.x; idx < total; idx += P.nwg * kThreads) {
+        const int b = idx / P.Hp, i = idx % P.Hp;
+        const float e = (i < P.H) ? bf2f(P.embed[(size_t)eff_tok(P, b) * P.H + i]) : 0.f;
+        st_dev_u64(reinterpret_cast<unsigned long long *>(P.xf + idx),
+                   (unsigned long long)to_fix(e));
+    }
+    if (garrive >= 0) bar_arrive(P, garrive, ti);
+}
+
+// RMSNorm + Q/K/V projection of KV head g + RoPE + KV-cache append.  The rows
+// of head g's block are: its G query heads, then its key, then its value
+// head; query and key rows are packed in rotation pairs (dims i, i + d/2).
+template <bool BAT>
+__device__ __forceinline__ void phase_qkv(KArg ka, int l, int gwait, int xbar, int ti) {
+    const StepParams P = load_params(ka);
+    const Lds S = lds_layout(kl_smem, P);
+    const int g = blockIdx.x / P.Sg, part = blockIdx.x % P.Sg;
+    const bool member = g < P.nkv;
+    int a0 = 0, a1 = 0;
+    if (member) split_range(P.qkv_rg, P.Sg, part, a0, a1);
+    const uint8_t *Lb = P.arena + (size_t)l * P.layer_stride;
+    const float *gain = reinterpret_cast<const float *>(Lb + P.off_attn_norm);
+    const int d = P.d, half = P.d / 2, G = P.group;
+    const int row0 = g * P.qkv_rg * kTileRows;   // first packed row of head g's block
+    constexpr bool batched = BAT;
+    weight_phase<BAT>(
+        P, S, Lb + P.off_qkv, P.Hp / kTileK, g * P.qkv_rg + a0, a1 - a0,
+        [&]() { if (gwait >= 0) bar_wait(P, gwait, ti); },
+        [&]() { norm_batched(P, S, gain, xbar); },
+        [&](int b) {
+            // the RoPE row of this sequence's position rides along (a + 2 Hp)
+            stage_rmsnorm(P.xf + (size_t)b * P.Hp, gain, P.H, P.Hp, P.eps, S.a, S.sm,
+                          reinterpret_cast<const float *>(P.rope + (size_t)eff_pos(P, b) * half),
+                          S.a + 2 * P.Hp, 2 * half);
+            if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 3);
+        },
+        true, [&](int c, int b0, int nb, uint16_t *buf) { stage_act_chunk(P, c, b0, nb, buf); },
+        [&](int b, int r, float y0, float y1) {
+            const int p = eff_pos(P, b);
+            const int lr = r - row0;
+            if (lr < (G + 1) * d) {
+                const int i = (lr % d) >> 1;
+                const float2 cs = batched ? P.rope[(size_t)p * half + i]
+                                          : reinterpret_cast<const float2 *>(S.a + 2 * P.Hp)[i];
+                const float u0 = y0 * cs.x - y1 * cs.y;
+                const float u1 = y0 * cs.y + y1 * cs.x;
+                if (lr < G * d) {
+                    float *qq = P.q + (size_t)b * P.nq * d + (size_t)(g * G + lr / d) * d;
+                    st_dev(qq + i, u0);
+                    st_dev(qq + i + half, u1);
+                } else {
+                    uint16_t *kk = P.kc + (kv_row(P, l, b, g) + p) * d;
+                    st_dev_u16(kk + i, f2bf(u0));
+                    st_dev_u16(kk + i + half, f2bf(u1));
+                }
+            } else {
+                const int j = lr - (G + 1) * d;
+                uint16_t *vv = P.vc + (kv_row(P, l, b, g) + p) * d;
+                st_dev_u32(reinterpret_cast<unsigned *>(vv + j),
+                           (unsigned)f2bf(y0) | ((unsigned)f2bf(y1) << 16));
+            }
+        });
+    if (member) local_arrive(P, P.cnt + g, ti);
+}
+
+// One attention work item: chunk c of sequence b against KV head g, for the
+// G query heads of that group (split-K flash decoding).  Positions are
+// grouped in slabs of PP positions (one 16-byte load per lane covers a slab);
+// chunk c owns a contiguous range of slabs, and inside a sub-chunk slab q is
+// held by wave q % kWaves, so every compute wave takes part even when a
+// chunk is short.  Scores and probabilities are fp32.  The chunk result is
+// (running max, running sum, unnormalised output) per head; the last chunk
+// of (b, g) to finish merges all chunks in chunk order and writes o.  The
+// first sub-chunk's K/V vectors are loaded before the barrier wait, except
+// the new slot, which the QKV phase writes and which is read after the wait
+// with device-coherent loads.  Loads are unconditional (spare ones target a
+// shared 16-byte line) and masked when consumed.
+template <int D>
+constexpr int attn_sub() { return kWaves * kAttnLoads * (64 / (D / 8)); }
+
+template <int D, int G>
+__device__ __forceinline__ void attn_item(KArg ka, int l, int b, int g, int c, bool first,
+                                          int ti) {
+    const StepParams P = load_params(ka);
+    const Lds S = lds_layout(kl_smem, P);
+    constexpr int LP = D / 8;                       // lanes per position
+    constexpr int PP = 64 / LP;                     // positions per slab
+    constexpr int NG = kAttnLoads;                  // slabs per wave per sub-chunk
+    constexpr int SUB = attn_sub<D>();              // positions per sub-chunk
+    const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    const int pi = lane / LP, ds = (lane % LP) * 8;
+    const int pnew = eff_pos(P, b), n = pnew + 1;
+    int s0, s1;
+    split_range((n + PP - 1) / PP, P.C, c, s0, s1);
+    const int j0 = min(n, s0 * PP), j1 = min(n, s1 * PP);
+    const bool compute = wid < kWaves;
+
+    float *qs = S.attn;                 // [G][D]
+    float *sp = qs + G * D;             // [G][SUB]
+    float *st = sp + G * SUB;           // [G][4]: max, sum, rescale
+    float *red = st + G * 4;            // [kWaves][G][D]
+    const size_t row0 = kv_row(P, l, b, g);
+    const uint16_t *Kb = P.kc + row0 * D;
+    const uint16_t *Vb = P.vc + row0 * D;
+    const float scale = 1.0f / sqrtf((float)D);
+
+    // local position of (wave, load t) in a sub-chunk
+    auto jloc = [&](int t) { return (t * kWaves + wid) * PP + pi; };
+    u32x4 kr[NG], vr[NG];
+    // K (or V) vectors of a sub-chunk; the next sub-chunk's K is issued once
+    // the scores have used this one's, and its V once the values have (the
+    // loop is software-pipelined over sub-chunks)
+    auto issue_one = [&](u32x4 *r, const uint16_t *base, int js, int len) {
+        if (!compute) return;   // the control wave keeps its load queue empty for the barrier
+#pragma unroll
+        for (int t = 0; t < NG; ++t) {
+            const int jl = jloc(t), pos = js + jl;
+            const bool real = jl < len && pos != pnew;
+            r[t] = ld_stream_16B(real ? (const void *)(base + (size_t)pos * D + ds) : P.dummy);
+        }
+    };
+    // the new slot (written during this step by another workgroup) is read
+    // with device-coherent loads, after the wait
+    auto fetch_new = [&](u32x4 *r, const uint16_t *base, int js, int len) {
+        if (compute && pnew >= js && pnew < js + len) {
+#pragma unroll
+            for (int t = 0; t < NG; ++t)
+                if (js + jloc(t) == pnew) r[t] = ld_dev_16B(base + (size_t)pnew * D + ds);
+        }
+    };
+    issue_one(kr, Kb, j0, min(SUB, j1 - j0));
+    issue_one(vr, Vb, j0, min(SUB, j1 - j0));
+    if (first) local_wait(P, P.cnt + g, (unsigned)(l + 1) * (unsigned)P.Sg, ti);
+    fetch_new(kr, Kb, j0, min(SUB, j1 - j0));
+    fetch_new(vr, Vb, j0, min(SUB, j1 - j0));
+    for (int t = threadIdx.x; t < G * D; t += kThreads)
+        qs[t] = ld_dev(P.q + (size_t)b * P.nq * D + (size_t)g * G * D + t);
+    if (threadIdx.x < G) {
+        st[threadIdx.x * 4 + 0] = -INFINITY;
+        st[threadIdx.x * 4 + 1] = 0.f;
+    }
+    __syncthreads();
+    float acc[G][8];
+#pragma unroll
+    for (int h = 0; h < G; ++h)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[h][e] = 0.f;
+
+    for (int js = j0; js < j1; js += SUB) {
+        const int len = min(SUB, j1 - js);
+        const int jn = js + SUB, lenn = min(SUB, j1 - jn);   // the next sub-chunk
+        // scores (q is read from LDS; all lanes take part in the lane sums)
+        if (compute) {
+#pragma unroll
+            for (int t = 0; t < NG; ++t) {
+                const int jl = jloc(t);
+                const float kf[8] = {bf_lo(kr[t].x), bf_hi(kr[t].x), bf_lo(kr[t].y),
+                                     bf_hi(kr[t].y), bf_lo(kr[t].z), bf_hi(kr[t].z),
+                                     bf_lo(kr[t].w), bf_hi(kr[t].w)};
+#pragma unroll
+                for (int h = 0; h < G; ++h) {
+                    const float4 q0 = *reinterpret_cast<const float4 *>(qs + h * D + ds);
+                    const float4 q1 = *reinterpret_cast<const float4 *>(qs + h * D + ds + 4);
+                    float s = 0.f;
+                    s = fmaf(q0.x, kf[0], s);
+                    s = fmaf(q0.y, kf[1], s);
+                    s = fmaf(q0.z, kf[2], s);
+                    s = fmaf(q0.w, kf[3], s);
+                    s = fmaf(q1.x, kf[4], s);
+                    s = fmaf(q1.y, kf[5], s);
+                    s = fmaf(q1.z, kf[6], s);
+                    s = fmaf(q1.w, kf[7], s);
+                    s = sum_lanes<LP>(s);
+                    if (jl < len && (lane % LP) == 0) sp[h * SUB + jl] = s * scale;
+                }
+            }
+        }
+        if (jn < j1) {
+            issue_one(kr, Kb, jn, lenn);
+            fetch_new(kr, Kb, jn, lenn);
+        }
+        __syncthreads();
+        // softmax statistics: wave h owns head h
+        if (wid < G) {
+            const int h = wid;
+            float mx = -INFINITY;
+            for (int j = lane; j < len; j += 64) mx = fmaxf(mx, sp[h * SUB + j]);
+            mx = wave_max(mx);
+            const float mold = st[h * 4], mnew = fmaxf(mold, mx);
+            const float resc = (mold == -INFINITY) ? 0.f : expf(mold - mnew);
+            float sum = 0.f;
+            for (int j = lane; j < len; j += 64) {
+                const float e = expf(sp[h * SUB + j] - mnew);
+                sp[h * SUB + j] = e;
+                sum += e;
+            }
+            sum = wave_sum(sum);
+            if (lane == 0) {
+                st[h * 4 + 0] = mnew;
+                st[h * 4 + 1] = st[h * 4 + 1] * resc + sum;
+                st[h * 4 + 2] = resc;
+            }
+        }
+        __syncthreads();
+        // values
+        if (compute) {
+#pragma unroll
+            for (int h = 0; h < G; ++h) {
+                const float r = st[h * 4 + 2];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) acc[h][e] *= r;
+            }
+#pragma unroll
+            for (int t = 0; t < NG; ++t) {
+                const int jl = jloc(t);
+                if (jl < len) {
+                    const float vf[8] = {bf_lo(vr[t].x), bf_hi(vr[t].x), bf_lo(vr[t].y),
+                                         bf_hi(vr[t].y), bf_lo(vr[t].z), bf_hi(vr[t].z),
+                                         bf_lo(vr[t].w), bf_hi(vr[t].w)};
+#pragma unroll
+                    for (int h = 0; h < G; ++h) {
+                        const float pr = sp[h * SUB + jl];
+#pragma unroll
+                        for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(pr, vf[e], acc[h][e]);
+                    }
+                }
+            }
+        }
+        if (jn < j1) {
+            issue_one(vr, Vb, jn, lenn);
+            fetch_new(vr, Vb, jn, lenn);
+        }
+        __syncthreads();
+    }
+    // reduce the PP position slots of each wave, then the waves in order
+    if (compute) {
+#pragma unroll
+        for (int h = 0; h < G; ++h)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                float v = acc[h][e];
+#pragma unroll
+                for (int off = LP; off < 64; off <<= 1) v += __shfl_xor(v, off);
+                acc[h][e] = v;
+            }
+        if (pi == 0) {
+#pragma unroll
+            for (int h = 0; h < G; ++h)
+#pragma unroll
+                for (int e = 0; e < 8; ++e) red[(wid * G + h) * D + ds + e] = acc[h][e];
+        }
+    }
+    __syncthreads();
+    // publish: unnormalised outputs [G][D] and (max, sum) per head
+    const size_t item = ((size_t)b * P.nkv + g) * P.C + c;
+    float *out = P.part_o + item * G * D;
+    float *sts = P.part_s + item * G * 2;
+    for (int t = threadIdx.x; t < G * D; t += kThreads) {
+        const int h = t / D, dd = t % D;
+        float s = 0.f;
+        for (int w = 0; w < kWaves; ++w) s += red[(w * G + h) * D + dd];
+        st_dev(out + t, s);
+        if (P.C == 1)   // (one chunk: the merged output is final; the batched O projection copies it)
+            st_dev_u16(P.acto + (size_t)b * P.nq * D + (size_t)g * G * D + t, f2bf(s / st[h * 4 + 1]));
+    }
+    if (threadIdx.x < G) {
+        st_dev(sts + threadIdx.x * 2, st[threadIdx.x * 4 + 0]);
+        st_dev(sts + threadIdx.x * 2 + 1, st[threadIdx.x * 4 + 1]);
+    }
+    if (is_ctl_lane0()) trace_stamp(P, ti, 3);
+    drain_all();
+    if (is_ctl_lane0())
+        __hip_atomic_fetch_add(P.cnt + P.nkv + g, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Attention of KV head g: the workgroups of head g take its items (sequence b,
+// chunk c) round-robin.
+template <int D, int G>
+__device__ __forceinline__ void phase_attn(KArg ka, int l, int garrive, int ti) {
+    const StepParams P = load_params(ka);
+    const int g = blockIdx.x / P.Sg, part = blockIdx.x % P.Sg;
+    if (g < P.nkv) {
+        const int items = P.B * P.C;
+        for (int it = part; it < items; it += P.Sg)
+            attn_item<D, G>(ka, l, it / P.C, g, it % P.C, it == part, ti);
+    }
+    // (batched steps: the O projection takes all heads and waits on the grid)
+    if (garrive >= 0) bar_arrive(P, garrive, ti);
+    else if (is_ctl_lane0()) trace_stamp(P, ti, 0);
+}
+
+// Merge the C chunk results of (sequence b, KV head g) in chunk order into
+// o[G * D] (LDS): o_h = sum_c w_ch A_ch / sum_c w_ch L_ch, w_ch = exp(M_ch - M_h).
+// Every thread owns outputs j; its loads of all chunks' values for j are
+// issued together (batches of kCombBatch) with the statistics loads.
+template <int D, int G>
+__device__ __forceinline__ void merge_chunks(const StepParams &P, int b, int g, float *o,
+                                             float *scratch) {
+    const int C = P.C;
+    const size_t item0 = ((size_t)b * P.nkv + g) * C;
+    const float *po = P.part_o + item0 * G * D;
+    const float *ps = P.part_s + item0 * G * 2;
+    float *cM = scratch, *cL = cM + C * G, *cW = cL + C * G, *cT = cW + C * G;
+    for (int j = threadIdx.x; j - (int)threadIdx.x < G * D; j += kThreads) {
+        const bool jv = j < G * D;
+        const int h = jv ? j / D : 0;
+        float num = 0.f;
+        for (int c0 = 0; c0 < C; c0 += kCombBatch) {
+            float av[kCombBatch];
+#pragma unroll
+            for (int k = 0; k < kCombBatch; ++k)
+                av[k] = (jv && c0 + k < C) ? ld_dev(po + (size_t)(c0 + k) * G * D + j) : 0.f;
+            if (j == (int)threadIdx.x && c0 == 0) {
+                // (first pass only, uniform across the block)
+                for (int t = threadIdx.x; t < C * G; t += kThreads) {
+                    const unsigned long long v = ld_dev_u64(ps + (size_t)t * 2);
+                    cM[t] = __uint_as_float((unsigned)v);
+                    cL[t] = __uint_as_float((unsigned)(v >> 32));
+                }
+                __syncthreads();
+                for (int t = threadIdx.x; t < C * G; t += kThreads) {
+                    const int hh = t % G;
+                    float M = -INFINITY;
+                    for (int cc = 0; cc < C; ++cc) M = fmaxf(M, cM[cc * G + hh]);
+                    cW[t] = (cM[t] == -INFINITY) ? 0.f : expf(cM[t] - M);
+                }
+                __syncthreads();
+                if (threadIdx.x < G) {
+                    float lsum = 0.f;
+                    for (int cc = 0; cc < C; ++cc)
+                        lsum = fmaf(cL[cc * G + threadIdx.x], cW[cc * G + threadIdx.x], lsum);
+                    cT[threadIdx.x] = lsum;
+                }
+                __syncthreads();
+            }
+#pragma unroll
+            for (int k = 0; k < kCombBatch; ++k)
+                if (c0 + k < C) num = fmaf(av[k], cW[(c0 + k) * G + h], num);
+        }
+        if (jv) o[j] = num / cT[h];
+    }
+    __syncthreads();
+}
+
+// O projection of KV head g: x += Wo[:, columns of head g] o_g, for the rows
+// this workgroup owns among head g's workgroups, added into the fixed-point
+// residual.  The chunk merge is the activation staging of this GEMV.
+template <int D, int G, bool BAT>
+__device__ __forceinline__ void phase_oproj(KArg ka, int l, int gwait, int garrive, int ti) {
+    const StepParams P = load_params(ka);
+    const Lds S = lds_layout(kl_smem, P);
+    const int KTO = G * D / kTileK;
+    const uint8_t *Wo = P.arena + (size_t)l * P.layer_stride + P.off_o;
+    auto epi = [&](int b, int r, float y0, float y1) {
+        long long *x = P.xf + (size_t)b * P.Hp;
+        add_fix(x + r, y0);
+        add_fix(x + r + 1, y1);
+    };
+    if constexpr (BAT) {
+        // all heads at once (K = n_heads d): one writer per residual element
+        int a0, a1;
+        split_range(P.o_rg, P.nwg, blockIdx.x, a0, a1);
+        weight_phase<true>(
+            P, S, Wo, P.nkv * KTO, a0, a1 - a0,
+            [&]() { if (gwait >= 0) bar_wait(P, gwait, ti); }, [&]() {}, [&](int) {}, P.C == 1,
+            [&](int c, int b0, int nb, uint16_t *buf) {
+                if (P.C == 1) stage_bf16_chunk(P.acto, P.nq * D, P.nq * D, c, b0, nb, buf);
+                else stage_o_full<D, G>(P, c, b0, nb, buf);
+            },
+            epi, KTO, (size_t)P.o_rg * KTO);
+    } else {
+        const int g = blockIdx.x / P.Sg, part = blockIdx.x % P.Sg;
+        if (g < P.nkv) {
+            int a0, a1;
+            split_range(P.o_rg, P.Sg, part, a0, a1);
+            const unsigned target = (unsigned)(l + 1) * (unsigned)(P.B * P.C);
+            weight_phase<false>(
+                P, S, Wo + (size_t)g * P.o_rg * KTO * kTileBytes, KTO, a0, a1 - a0,
+                [&]() { local_wait(P, P.cnt + P.nkv + g, target, ti); }, [&]() {},
+                [&](int b) {
+                    merge_chunks<D, G>(P, b, g, S.a, S.a + G * D);
+                    if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 3);
+                },
+                false, [&](int, int, int, uint16_t *) {}, epi);
+        }
+    }
+    if (garrive >= 0) bar_arrive(P, garrive, ti);
+}
+
+// RMSNorm + gate/up projection + SwiGLU for FFN column block j = w / Rc:
+// m = silu(Wg u) * (Wu u).  Packed rows alternate gate i, up i.
+template <bool BAT>
+__device__ __forceinline__ void phase_gateup(KArg ka, int l, int gwait, int xbar, int garrive,
+                                             int ti) {
+    const StepParams P = load_params(ka);
+    const Lds S = lds_layout(kl_smem, P);
+    const int j = blockIdx.x / P.Rc, part = blockIdx.x % P.Rc;
+    const bool member = j < P.Sc;
+    int first = 0, count = 0;
+    if (member) {
+        // block j covers SwiGLU outputs [j KTc 64, (j + 1) KTc 64): 2 packed rows each
+        const int r0 = min(P.gu_rg, j * P.KTc * 2 * kTileK / kTileRows);
+        const int r1 = min(P.gu_rg, (j + 1) * P.KTc * 2 * kTileK / kTileRows);
+        int a0, a1;
+        split_range(r1 - r0, P.Rc, part, a0, a1);
+        first = r0 + a0;
+        count = a1 - a0;
+    }
+    const uint8_t *Lb = P.arena + (size_t)l * P.layer_stride;
+    const float *gain = reinterpret_cast<const float *>(Lb + P.off_ffn_norm);
+    weight_phase<BAT>(
+        P, S, Lb + P.off_gu, P.Hp / kTileK, first, count,
+        [&]() { if (gwait >= 0) bar_wait(P, gwait, ti); },
+        [&]() { norm_batched(P, S, gain, xbar); },
+        [&](int b) {
+            stage_rmsnorm(P.xf + (size_t)b * P.Hp, gain, P.H, P.Hp, P.eps, S.a, S.sm);
+            if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 3);
+        },
+        true, [&](int c, int b0, int nb, uint16_t *buf) { stage_act_chunk(P, c, b0, nb, buf); },
+        [&](int b, int r, float gt, float up) {
+            const float mv = gt / (1.0f + expf(-gt)) * up;
+            if constexpr (BAT) st_dev_u16(P.actm + (size_t)b * P.Fp + (r >> 1), f2bf(mv));
+            else st_dev(P.m + (size_t)b * P.Fp + (r >> 1), mv);
+        });
+    if constexpr (BAT) {
+        if (garrive >= 0) bar_arrive(P, garrive, ti);
+    } else {
+        if (member) local_arrive(P, P.cnt + 2 * P.nkv + j, ti);
+    }
+}
+
+// Down projection of FFN column block j: x += Wd[:, block j] m[block j], for
+// the rows this workgroup owns among block j's workgroups.
+template <bool BAT>
+__device__ __forceinline__ void phase_down(KArg ka, int l, int gwait, int garrive, int ti) {
+    const StepParams P = load_params(ka);
+    const Lds S = lds_layout(kl_smem, P);
+    const uint8_t *Wd = P.arena + (size_t)l * P.layer_stride + P.off_down;
+    auto epi = [&](int b, int r, float y0, float y1) {
+        long long *x = P.xf + (size_t)b * P.Hp;
+        add_fix(x + r, y0);
+        add_fix(x + r + 1, y1);
+    };
+    if constexpr (BAT) {
+        // all FFN columns at once: one writer per residual element
+        int a0, a1;
+        split_range(P.down_rg, P.nwg, blockIdx.x, a0, a1);
+        weight_phase<true>(
+            P, S, Wd, P.Sc * P.KTc, a0, a1 - a0,
+            [&]() { if (gwait >= 0) bar_wait(P, gwait, ti); }, [&]() {}, [&](int) {}, true,
+            [&](int c, int b0, int nb, uint16_t *buf) {
+                stage_bf16_chunk(P.actm, P.Fp, P.Fp, c, b0, nb, buf);
+            },
+            epi, P.KTc, (size_t)P.down_rg * P.KTc);
+    } else {
+        const int j = blockIdx.x / P.Rc, part = blockIdx.x % P.Rc;
+        if (j < P.Sc) {
+            int a0, a1;
+            split_range(P.down_rg, P.Rc, part, a0, a1);
+            const int kw = P.KTc * kTileK;
+            weight_phase<false>(
+                P, S, Wd + (size_t)j * P.down_rg * P.KTc * kTileBytes, P.KTc, a0, a1 - a0,
+                [&]() {
+                    local_wait(P, P.cnt + 2 * P.nkv + j, (unsigned)(l + 1) * (unsigned)P.Rc, ti);
+                },
+                [&]() {},
+                [&](int b) {
+                    stage_vec(P.m + (size_t)b * P.Fp + (size_t)j * kw, kw, kw, S.a);
+                    if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 3);
+                },
+                false, [&](int, int, int, uint16_t *) {}, epi);
+        }
+    }
+    if (garrive >= 0) bar_arrive(P, garrive, ti);
+}
+
+// Classifier block (Sec. 2): final RMSNorm + LM head -> fp32 logits.
+template <bool BAT>
+__device__ __forceinline__ void phase_head(KArg ka, int gwait, int xbar, int ti) {
+    const StepParams P = load_params(ka);
+    const Lds S = lds_layout(kl_smem, P);
+    const RgRange R = own_rgs(P.head_rg, P);
+    const int V = P.V;
+    weight_phase<BAT>(
+        P, S, reinterpret_cast<const uint8_t *>(P.lm_head), P.Hp / kTileK, R.first, R.count,
+        [&]() {
+            if (gwait >= 0) bar_wait(P, gwait, ti);
+            if (blockIdx.x == 0 && P.hidden_out) {
+                for (int idx = threadIdx.x; idx < P.B * P.H; idx += kThreads)
+                    P.hidden_out[idx] = from_fix((long long)ld_dev_u64(
+                        P.xf + (size_t)(idx / P.H) * P.Hp + idx % P.H));
+            }
+        },
+        [&]() { norm_batched(P, S, P.final_norm, xbar); },
+        [&](int b) {
+            stage_rmsnorm(P.xf + (size_t)b * P.Hp, P.final_norm, P.H, P.Hp, P.eps, S.a, S.sm);
+            if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 3);
+        },
+        true, [&](int c, int b0, int nb, uint16_t *buf) { stage_act_chunk(P, c, b0, nb, buf); },
+        [&](int b, int r, float y0, float y1) {
+            float *lg = P.logits + (size_t)b * V;
+            if (r < V) lg[r] = y0;
+            if (r + 1 < V) lg[r + 1] = y1;
+        });
+    if (is_ctl_lane0()) trace_stamp(P, ti, 0);
+}
+
+// ---------------------------------------------------------------- kernels
+
+// Runs the phases selected by 'phases' for layers [l0, l1) in order:
+// embed, (qkv, attn, oproj, gateup, down) per layer, head.  Grid barrier k is
+// the k-th arrival of the launch; a phase that needs the residual stream waits
+// on the latest one, and an arriving phase arrives only if a later phase of
+// the same launch waits (a launch boundary already orders the rest).
+template <int D, int G, bool BAT>
+__global__ __launch_bounds__(kThreads) void kl_step_kernel(StepParams P, int l0, int l1,
+                                                          int phases) {
+    (void)P;   // read through the kernel-argument segment (see load_params)
+    const KArg ka = kernarg_address();
+    const bool has_qkv = phases & kPhQkv, has_gu = phases & kPhGateUp, has_head = phases & kPhHead;
+    const int nlay = (phases & kPhLayer) ? l1 - l0 : 0;
+    // batched steps add a grid barrier inside each RMSNorm phase (norm_batched)
+    constexpr bool batched = BAT;
+    bar_init(load_params(ka));
+    int na = 0, ti = 0;   // grid arrivals so far; phase index (for the trace)
+    auto gw = [&]() { return na - 1; };                 // barrier to wait on (-1: none)
+    auto ga = [&](bool waited_later) { return waited_later ? na++ : -1; };
+    auto xb = [&]() { return batched ? na++ : -1; };    // the phase's own barrier
+    const bool has_attn = phases & kPhAttn, has_op = phases & kPhOproj;
+    const bool has_down = phases & kPhDown;
+    if (phases & kPhEmbed) {
+        phase_embed(ka, -1, ga((has_qkv && nlay > 0) || has_head), ti++);
+    }
+    for (int l = l0; l < l1; ++l) {
+        // batched steps: attn -> oproj and gateup -> down are grid barriers
+        // too (full-K products with one writer per output)
+        if (phases & kPhQkv) {
+            const int w = gw(), x = xb();
+            phase_qkv<BAT>(ka, l, w, x, ti++);
+        }
+        if (phases & kPhAttn) phase_attn<D, G>(ka, l, BAT ? ga(has_op) : -1, ti++);
+        if (phases & kPhOproj) {
+            const int w = BAT && has_attn ? gw() : -1, a = ga(has_gu);
+            phase_oproj<D, G, BAT>(ka, l, w, a, ti++);
+        }
+        if (phases & kPhGateUp) {
+            const int w = gw(), x = xb(), a = BAT ? ga(has_down) : -1;
+            phase_gateup<BAT>(ka, l, w, x, a, ti++);
+        }
+        if (phases & kPhDown) {
+            const int w = BAT && has_gu ? gw() : -1;
+            phase_down<BAT>(ka, l, w, ga((has_qkv && l + 1 < l1) || has_head), ti++);
+        }
+    }
+    if (has_head) {
+        const int w = gw(), x = xb();
+        phase_head<BAT>(ka, w, x, ti++);
+    }
+}
+
+}  // namespace kl

@@ -45,6 +45,35 @@ class GpuModel:
                                       g["lm_head"].data_ptr(), layers, stream_handle(stream))
         del src, g   # kl_load_model copied and repacked everything
 
+    @classmethod
+    def from_layers(cls, model_cfg: dict, layer_fn, globals_fn, max_batch: int, max_seq: int,
+                    device="cuda", stream: torch.cuda.Stream | None = None) -> "GpuModel":
+        """Load one layer at a time (kl_model_create + kl_model_set_layer): only
+        one layer's source weights are on the device at once.  layer_fn(l) and
+        globals_fn() return host bf16 arrays by name (as in model_host)."""
+        if not torch.cuda.is_available():
+            raise RuntimeError("GpuModel needs a GPU")
+        self = cls.__new__(cls)
+        self.model_cfg = dict(model_cfg)
+        self.device = torch.device(device)
+        self.cfg = kb.make_config(model_cfg, max_batch, max_seq)
+        self.max_batch, self.max_seq = max_batch, max_seq
+        self.state = kb.kl_model_create(self.cfg)
+        h = stream_handle(stream)
+        for l in range(model_cfg["n_layers"]):
+            lay = layer_fn(l)
+            src = {n: _dev_u16(lay[n], self.device) for n in kb.LAYER_FIELDS}
+            torch.cuda.synchronize(self.device)
+            kb.kl_model_set_layer(self.state, l, {n: t.data_ptr() for n, t in src.items()}, h)
+            del src, lay
+        g = globals_fn()
+        src = {n: _dev_u16(g[n], self.device) for n in ("embed", "final_norm", "lm_head")}
+        torch.cuda.synchronize(self.device)
+        kb.kl_model_set_globals(self.state, src["embed"].data_ptr(), src["final_norm"].data_ptr(),
+                                src["lm_head"].data_ptr(), h)
+        del src, g
+        return self
+
     def info(self) -> kb.kl_info:
         return kb.kl_get_info(self.state)
 

@@ -174,3 +174,28 @@ def test_llama8b_width_two_layers_batch32():
     check_against_oracle(c, outs[1], ref)
     assert_bit_exact(outs[0], outs[1], "per_layer vs looped")
     assert_bit_exact(outs[2], outs[1], "per_op vs looped")
+
+
+@pytest.mark.parametrize("batch", [1, 8])
+def test_llama70b_width_two_layers(batch):
+    # the 70B layer shapes (hidden 8192, 64 query / 8 KV heads: 8 query heads
+    # per KV head, FFN 28672) with 2 layers, loaded one layer at a time
+    import synth
+    from paper_2410_23668_amd.device import GpuModel
+    cfg = dict(WORKLOADS["llama70b-b1-ctx4096"]["model"], n_layers=2)
+    say(f"[70b-width L=2 B={batch}] building")
+    filled = (np.arange(batch, dtype=np.int32) * 53 + 200) % 250
+    c = Case(cfg, batch, 256, filled, seed=91)
+    inc = GpuModel.from_layers(cfg, lambda l: c.weights["layers"][l], lambda: c.weights,
+                               batch, 256)
+    say(f"[70b-width L=2 B={batch}] oracle")
+    ref = c.oracle_step(nthreads=8)
+    outs = [c.gpu_step(mode) for _, mode in MODES]
+    check_against_oracle(c, outs[1], ref)
+    assert_bit_exact(outs[0], outs[1], "per_layer vs looped")
+    assert_bit_exact(outs[2], outs[1], "per_op vs looped")
+    # the incrementally loaded copy computes the same bits
+    c.model, full = inc, c.model
+    assert_bit_exact(c.gpu_step(kb.KL_MODE_LOOPED), outs[1], "incremental vs whole load")
+    c.model = full
+    inc.close()
