@@ -30,7 +30,7 @@ struct kl_state {
     size_t scratch_bytes;
     long long *xf;
     float *q, *m, *part_o, *part_s;
-    uint16_t *act, *actm, *acto;
+    uint16_t *act, *act_lo, *actm, *actm_lo, *acto, *acto_lo;
     int Sg, Sc, Rc, KTc;
     unsigned long long *bar;
     unsigned *cnt;
@@ -184,7 +184,8 @@ StepParams base_params(const kl_state &s) {
     P.lm_head = reinterpret_cast<const uint16_t *>(s.arena + s.off_lm_head);
     P.rope = s.rope;
     P.xf = s.xf; P.q = s.q; P.m = s.m; P.part_o = s.part_o; P.part_s = s.part_s; P.act = s.act;
-    P.actm = s.actm; P.acto = s.acto;
+    P.act_lo = s.act_lo; P.actm = s.actm; P.actm_lo = s.actm_lo; P.acto = s.acto;
+    P.acto_lo = s.acto_lo;
     P.bar = s.bar; P.cnt = s.cnt; P.err = s.err; P.dummy = s.dummy;
     P.nwg = s.nwg;
     P.lds_red = s.lds_red; P.lds_sm = s.lds_sm; P.lds_bar = s.lds_bar;
@@ -302,9 +303,9 @@ kl_status kl_model_create(const kl_config *cfg, kl_state **out) {
     const size_t off_m = so;    so = align_up(so + (size_t)B * S->Fp * 4, 256);
     const size_t off_po = so;   so = align_up(so + items * g * d * 4, 256);
     const size_t off_ps = so;   so = align_up(so + items * g * 2 * 4, 256);
-    const size_t off_act = so;  so = align_up(so + (size_t)B * S->Hp * 2, 256);
-    const size_t off_actm = so; so = align_up(so + (size_t)B * S->Fp * 2, 256);
-    const size_t off_acto = so; so = align_up(so + (size_t)B * S->Ap * 2, 256);
+    const size_t off_act = so;  so = align_up(so + (size_t)B * S->Hp * 2 * 2, 256);
+    const size_t off_actm = so; so = align_up(so + (size_t)B * S->Fp * 2 * 2, 256);
+    const size_t off_acto = so; so = align_up(so + (size_t)B * S->Ap * 2 * 2, 256);
     const size_t off_bar = so;  so = align_up(so + kBarBytes, 256);
     const size_t off_cnt = so;  so = align_up(so + (size_t)(2 * nkv + S->Sc) * 4, 256);
     const size_t off_err = so;  so = align_up(so + 256, 256);
@@ -318,8 +319,11 @@ kl_status kl_model_create(const kl_config *cfg, kl_state **out) {
     S->part_o = reinterpret_cast<float *>(S->scratch + off_po);
     S->part_s = reinterpret_cast<float *>(S->scratch + off_ps);
     S->act = reinterpret_cast<uint16_t *>(S->scratch + off_act);
+    S->act_lo = S->act + (size_t)B * S->Hp;
     S->actm = reinterpret_cast<uint16_t *>(S->scratch + off_actm);
+    S->actm_lo = S->actm + (size_t)B * S->Fp;
     S->acto = reinterpret_cast<uint16_t *>(S->scratch + off_acto);
+    S->acto_lo = S->acto + (size_t)B * S->Ap;
     S->bar = reinterpret_cast<unsigned long long *>(S->scratch + off_bar);
     S->cnt = reinterpret_cast<unsigned *>(S->scratch + off_cnt);
     S->err = reinterpret_cast<int *>(S->scratch + off_err);

@@ -19,17 +19,21 @@ constexpr int kRgBatch = 16;              // row groups reduced per LDS round
 constexpr int kAttnLoads = 5;             // K (and V) loads per lane per attention sub-chunk
 constexpr int kCombBatch = 32;            // chunk partials loaded together when merging
 // Batched steps (batch >= kMfmaBatch) run the weight products on the matrix
-// cores: activations in bf16, staged in LDS in chunks of kGemmChunkK columns
-// for up to kGemmBatch sequences at a time, weight rows in blocks of 16.
+// cores.  An activation x enters them as two bf16 terms, hi = bf16(x) and
+// lo = bf16(x - hi), both multiplied into the same fp32 accumulators (about
+// 16 significant bits of x instead of 8).  Activations are staged in LDS in
+// chunks of kGemmChunkK columns for up to kGemmBatch sequences at a time,
+// weight rows in blocks of 16.
 constexpr int kMfmaBatch = 8;
 constexpr int kGemmBatch = 32;
 constexpr int kGemmChunkK = 512;
 constexpr int kActStride = kGemmChunkK + 8;   // bf16 per staged activation row (bank spread)
 constexpr int kGemmMaxBlk = 4;            // 16-row blocks per wave per pass over the weights
-// LDS of the batched path (bytes): two activation chunks, per-wave weight
-// re-layout slots (2 KiB), per-wave partial products of one block (2 KiB)
-constexpr int kGemmActBytes = kGemmBatch * kActStride * 2;
-constexpr int kGemmLdsBytes = 2 * kGemmActBytes + kWaves * 2048 + kWaves * 2048;
+// LDS of the batched path (bytes): two activation chunks of both terms, and
+// per-wave weight re-layout slots (2 KiB; after the chunk loop they hold the
+// partial products of one block)
+constexpr int kGemmActBytes = kGemmBatch * kActStride * 2;   // one term of one chunk
+constexpr int kGemmLdsBytes = 4 * kGemmActBytes + kWaves * 2048;
 constexpr int kMaxGroup = 8;              // max query heads per KV head
 constexpr int kBarGroups = 16;            // first level of the grid barrier
 constexpr int kBarBytes = 8192;           // barrier counters: kBarGroups lines of 256 B
@@ -76,9 +80,10 @@ struct StepParams {
     float *m;                  // [max_batch][Fp] SwiGLU output (padding stays 0)
     float *part_o;             // attention chunk outputs [B*nkv*C][group*d]
     float *part_s;             // attention chunk (max, sum) [B*nkv*C][group][2]
-    uint16_t *act;             // [max_batch][Hp] bf16 normalised activations (batched path)
-    uint16_t *actm;            // [max_batch][Fp] bf16 SwiGLU output (batched path)
-    uint16_t *acto;            // [max_batch][nq*d] bf16 attention output, when C == 1
+    // batched path: activations as bf16 hi and lo terms (hi + lo ~ the fp32 value)
+    uint16_t *act, *act_lo;    // [max_batch][Hp] normalised activations
+    uint16_t *actm, *actm_lo;  // [max_batch][Fp] SwiGLU output
+    uint16_t *acto, *acto_lo;  // [max_batch][nq*d] attention output, when C == 1
     unsigned long long *bar;   // grid barrier counters (monotonic): group g at [32 (g + 1)]
     unsigned *cnt;             // local counters: [nkv] qkv, [nkv] attention, [Sc] gate/up
     int *err;                  // device error word

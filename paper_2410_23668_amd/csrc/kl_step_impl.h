@@ -50,6 +50,19 @@ __device__ __forceinline__ uint16_t f2bf(float f) {
     return (uint16_t)(u >> 16);
 }
 
+// The two bf16 terms of a matrix-core activation: hi = bf16(x), lo =
+// bf16(x - hi) (x - hi is exact in fp32), so hi + lo = x (1 + O(2^-17)).
+// Two values per call, packed as (x0 | x1 << 16).
+__device__ __forceinline__ void split_bf16x2(float x0, float x1, unsigned &hi, unsigned &lo) {
+    const uint16_t h0 = f2bf(x0), h1 = f2bf(x1);
+    hi = (unsigned)h0 | ((unsigned)h1 << 16);
+    lo = (unsigned)f2bf(x0 - bf2f(h0)) | ((unsigned)f2bf(x1 - bf2f(h1)) << 16);
+}
+__device__ __forceinline__ void split_bf16(float x, uint16_t &hi, uint16_t &lo) {
+    hi = f2bf(x);
+    lo = f2bf(x - bf2f(hi));
+}
+
 template <int CTRL>
 __device__ __forceinline__ float dpp(float v) {
     return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v),
@@ -615,31 +628,35 @@ __device__ __forceinline__ void gemv_phase(const uint8_t *__restrict__ W, int KT
 // D[16x16] += A[16x32] B[32x16]) for the row groups first .. first + count - 1
 // and up to kGemmBatch sequences b0 .. b0 + nb - 1.  A block is 16 weight
 // rows (2 row groups); A = W[16 rows][32 k], B = X[32 k][16 sequences], two
-// products per 32 columns cover 32 sequences.  Operand layouts: A lane l holds
-// A[l % 16][8 (l / 16) .. +7], B lane l holds B[8 (l / 16) .. +7][l % 16], D
-// lane l holds D[4 (l / 16) + v][l % 16].  Weight tiles arrive through the
-// same ring of 16-byte loads as the GEMV path and are re-laid out through a
-// per-wave LDS slot (2 KiB: the two tiles of a block at one k-tile).  X is
-// staged in LDS in chunks of kGemmChunkK columns (bf16, kActStride per row),
-// double-buffered: stage(c, buf) fills chunk c.  Waves share blocks and
+// products per 32 columns cover 32 sequences, each product taken for both
+// bf16 terms of X (hi, then lo, into the same accumulators).  Operand layouts:
+// A lane l holds A[l % 16][8 (l / 16) .. +7], B lane l holds
+// B[8 (l / 16) .. +7][l % 16], D lane l holds D[4 (l / 16) + v][l % 16].
+// Weight tiles arrive through the same ring of 16-byte loads as the GEMV path
+// and are re-laid out through a per-wave LDS slot (2 KiB: the two tiles of a
+// block at one k-tile).  X is staged in LDS in chunks of kGemmChunkK columns
+// (kActStride bf16 per row; the hi rows, then kLoOff elements further the lo
+// rows), double-buffered: stage(c, buf) fills chunk c.  Waves share blocks and
 // k-tiles: with nblk >= 8 blocks each wave takes whole blocks, else
 // ksplit = 8 / nblk waves share a block's k-tiles and their partial products
 // are added in wave order.
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
+constexpr int kLoOff = kGemmBatch * kActStride;   // elements from a chunk's hi rows to its lo rows
+
 struct GemmLds {
-    uint16_t *act[2];   // [kGemmBatch][kActStride] bf16
+    uint16_t *act[2];   // [2 terms][kGemmBatch][kActStride] bf16
     uint8_t *wslot;     // [kWaves][2048]
-    float *cred;        // [kWaves][16][32]
+    float *cred;        // [kWaves][16][32], the same memory as wslot (used after the chunk loop)
 };
 
 __device__ __forceinline__ GemmLds gemm_lds(char *smem) {
     GemmLds g;
     g.act[0] = reinterpret_cast<uint16_t *>(smem);
-    g.act[1] = reinterpret_cast<uint16_t *>(smem + kGemmActBytes);
-    g.wslot = reinterpret_cast<uint8_t *>(smem + 2 * kGemmActBytes);
-    g.cred = reinterpret_cast<float *>(smem + 2 * kGemmActBytes + kWaves * 2048);
+    g.act[1] = reinterpret_cast<uint16_t *>(smem + 2 * kGemmActBytes);
+    g.wslot = reinterpret_cast<uint8_t *>(smem + 4 * kGemmActBytes);
+    g.cred = reinterpret_cast<float *>(g.wslot);
     return g;
 }
 
@@ -667,11 +684,11 @@ __device__ __forceinline__ void gemm_rows(const uint8_t *__restrict__ W, int KT,
     const uint8_t *tbase = W + (size_t)lane * 16;
     const uint8_t *zbase = dummy + (size_t)lane * 16;   // 1 KiB of zeros
 
-    // zero the padding sequences of both activation buffers once
-    for (int t = threadIdx.x; t < 2 * (kGemmBatch - nb) * kActStride / 8; t += kThreads) {
-        const int half = (kGemmBatch - nb) * kActStride / 8;
-        uint16_t *buf = L.act[t / half];
-        reinterpret_cast<u32x4 *>(buf + nb * kActStride)[t % half] = u32x4{0u, 0u, 0u, 0u};
+    // zero the padding sequences of both terms of both activation buffers once
+    const int pad16 = (kGemmBatch - nb) * kActStride / 8;   // 16-byte words per term
+    for (int t = threadIdx.x; t < 4 * pad16; t += kThreads) {
+        uint16_t *buf = L.act[t / (2 * pad16)] + ((t / pad16) & 1) * kLoOff;
+        reinterpret_cast<u32x4 *>(buf + nb * kActStride)[t % pad16] = u32x4{0u, 0u, 0u, 0u};
     }
 
     for (int bg0 = 0; bg0 < nblk; bg0 += slots * kGemmMaxBlk) {
@@ -754,11 +771,16 @@ __device__ __forceinline__ void gemm_rows(const uint8_t *__restrict__ W, int KT,
                                     const int k = ktl * kTileK + 32 * st + 8 * (lane >> 4);
                                     const bf16x8 x = *reinterpret_cast<const bf16x8 *>(
                                         act + b * kActStride + k);
+                                    const bf16x8 xl = *reinterpret_cast<const bf16x8 *>(
+                                        act + kLoOff + b * kActStride + k);
 #pragma unroll
                                     for (int ii = 0; ii < kGemmMaxBlk; ++ii)
-                                        if (ii == i)
+                                        if (ii == i) {
                                             acc[ii][h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
                                                 a, x, acc[ii][h], 0, 0, 0);
+                                            acc[ii][h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                                                a, xl, acc[ii][h], 0, 0, 0);
+                                        }
                                 }
                             }
                         }
@@ -853,7 +875,8 @@ __device__ __forceinline__ void weight_phase(const StepParams &P, const Lds &S,
     }
 }
 
-// Batched RMSNorm: act[b][k] = bf16(x_b[k] r_b gain[k]) for every sequence,
+// Batched RMSNorm: act / act_lo [b][k] = the two bf16 terms of x_b[k] r_b gain[k]
+// for every sequence,
 // the (sequence, kGemmChunkK-column slice) items spread over the grid; ends
 // with grid barrier k, after which any workgroup may stage any slice.
 __device__ __forceinline__ void norm_batched(const StepParams &P, const Lds &S,
@@ -863,9 +886,12 @@ __device__ __forceinline__ void norm_batched(const StepParams &P, const Lds &S,
         const int b = it / ns, c0 = (it % ns) * kGemmChunkK;
         const int c1 = min(P.Hp, c0 + kGemmChunkK);
         stage_rmsnorm(P.xf + (size_t)b * P.Hp, gain, P.H, P.Hp, P.eps, S.a, S.sm);
-        for (int kk = c0 + 2 * (int)threadIdx.x; kk < c1; kk += 2 * kThreads)
-            st_dev_u32(reinterpret_cast<unsigned *>(P.act + (size_t)b * P.Hp + kk),
-                       (unsigned)f2bf(S.a[kk]) | ((unsigned)f2bf(S.a[kk + 1]) << 16));
+        for (int kk = c0 + 2 * (int)threadIdx.x; kk < c1; kk += 2 * kThreads) {
+            unsigned hi, lo;
+            split_bf16x2(S.a[kk], S.a[kk + 1], hi, lo);
+            st_dev_u32(reinterpret_cast<unsigned *>(P.act + (size_t)b * P.Hp + kk), hi);
+            st_dev_u32(reinterpret_cast<unsigned *>(P.act_lo + (size_t)b * P.Hp + kk), lo);
+        }
         __syncthreads();   // (S.a is restaged by the next item)
     }
     bar_arrive(P, k, -1);
@@ -877,119 +903,37 @@ __device__ __forceinline__ void stage_act_chunk(const StepParams &P, int c, int 
                                                 uint16_t *buf) {
     if ((threadIdx.x >> 6) != kCtlWave) return;
     const int k0 = c * kGemmChunkK, kc = min(kGemmChunkK, P.Hp - k0);
-    for (int b = 0; b < nb; ++b)
-        ctl_copy_to_lds(P.act + (size_t)(b0 + b) * P.Hp + k0, buf + b * kActStride, kc * 2);
+    for (int b = 0; b < nb; ++b) {
+        const size_t o = (size_t)(b0 + b) * P.Hp + k0;
+        ctl_copy_to_lds(P.act + o, buf + b * kActStride, kc * 2);
+        ctl_copy_to_lds(P.act_lo + o, buf + kLoOff + b * kActStride, kc * 2);
+    }
     ctl_copy_wait();
 }
 
-// Chunk c of a bf16 matrix src[b][ld] with K columns (control wave: memory-to-
-// LDS copies, so the compute waves keep working on the previous chunk).
-__device__ __forceinline__ void stage_bf16_chunk(const uint16_t *src, int ld, int K, int c, int b0,
-                                                 int nb, uint16_t *buf) {
+// Chunk c of a two-term bf16 matrix src / src_lo [b][ld] with K columns
+// (control wave: memory-to-LDS copies, so the compute waves keep working on
+// the previous chunk).
+__device__ __forceinline__ void stage_bf16_chunk(const uint16_t *src, const uint16_t *src_lo,
+                                                 int ld, int K, int c, int b0, int nb,
+                                                 uint16_t *buf) {
     if ((threadIdx.x >> 6) != kCtlWave) return;
     const int k0 = c * kGemmChunkK, kc = min(kGemmChunkK, K - k0);
-    for (int b = 0; b < nb; ++b)
-        ctl_copy_to_lds(src + (size_t)(b0 + b) * ld + k0, buf + b * kActStride, kc * 2);
+    for (int b = 0; b < nb; ++b) {
+        const size_t o = (size_t)(b0 + b) * ld + k0;
+        ctl_copy_to_lds(src + o, buf + b * kActStride, kc * 2);
+        ctl_copy_to_lds(src_lo + o, buf + kLoOff + b * kActStride, kc * 2);
+    }
     ctl_copy_wait();
-}
-
-// Chunk c of the merged attention output of KV head g, as bf16.  With one
-// chunk per (sequence, head), o = A / L: every thread loads four outputs
-// (16 bytes) and their head's sum in one batch; otherwise the chunk results
-// are merged as in merge_chunks.
-template <int D, int G>
-__device__ __forceinline__ void stage_o_chunk(const StepParams &P, int g, int c, int b0, int nb,
-                                              uint16_t *buf) {
-    const int C = P.C, k0 = c * kGemmChunkK, kc = min(kGemmChunkK, G * D - k0);
-    if (C == 1) {
-        constexpr int NB = 8;   // float4 loads per thread in flight
-        const int n4 = nb * kc / 4;
-        for (int t0 = threadIdx.x; t0 < n4; t0 += NB * kThreads) {
-            float4 v[NB];
-            float den[NB];
-#pragma unroll
-            for (int q = 0; q < NB; ++q) {
-                const int t = t0 + q * kThreads;
-                v[q] = make_float4(0.f, 0.f, 0.f, 0.f);
-                den[q] = 1.f;
-                if (t < n4) {
-                    const int b = t / (kc / 4), j = k0 + (t % (kc / 4)) * 4;
-                    const size_t item = (size_t)(b0 + b) * P.nkv + g;
-                    const u32x4 u = ld_dev_16B(P.part_o + item * G * D + j);
-                    v[q] = make_float4(__uint_as_float(u.x), __uint_as_float(u.y),
-                                       __uint_as_float(u.z), __uint_as_float(u.w));
-                    den[q] = ld_dev(P.part_s + (item * G + j / D) * 2 + 1);
-                }
-            }
-#pragma unroll
-            for (int q = 0; q < NB; ++q) {
-                const int t = t0 + q * kThreads;
-                if (t < n4) {
-                    const int b = t / (kc / 4), jj = (t % (kc / 4)) * 4;
-                    const float r = 1.0f / den[q];
-                    unsigned *dst = reinterpret_cast<unsigned *>(buf + b * kActStride + jj);
-                    dst[0] = (unsigned)f2bf(v[q].x * r) | ((unsigned)f2bf(v[q].y * r) << 16);
-                    dst[1] = (unsigned)f2bf(v[q].z * r) | ((unsigned)f2bf(v[q].w * r) << 16);
-                }
-            }
-        }
-        return;
-    }
-    for (int t = threadIdx.x; t < nb * kc; t += kThreads) {
-        const int b = t / kc, j = k0 + t % kc, h = j / D;
-        const size_t item0 = ((size_t)(b0 + b) * P.nkv + g) * C;
-        float M = -INFINITY;
-        for (int cc = 0; cc < C; ++cc) M = fmaxf(M, ld_dev(P.part_s + ((item0 + cc) * G + h) * 2));
-        float num = 0.f, den = 0.f;
-        for (int cc = 0; cc < C; ++cc) {
-            const float m = ld_dev(P.part_s + ((item0 + cc) * G + h) * 2);
-            const float w = (m == -INFINITY) ? 0.f : expf(m - M);
-            num = fmaf(ld_dev(P.part_o + (item0 + cc) * G * D + j), w, num);
-            den = fmaf(ld_dev(P.part_s + ((item0 + cc) * G + h) * 2 + 1), w, den);
-        }
-        buf[b * kActStride + (j - k0)] = f2bf(num / den);
-    }
 }
 
 // Chunk c of the merged attention output of all heads (K = n_heads d), as
-// bf16; same scheme as stage_o_chunk.
+// two bf16 terms, when there are several chunk results per (sequence, KV
+// head): o_h = sum_c w_ch A_ch / sum_c w_ch L_ch, w_ch = exp(M_ch - M_h).
 template <int D, int G>
 __device__ __forceinline__ void stage_o_full(const StepParams &P, int c, int b0, int nb,
                                              uint16_t *buf) {
     const int C = P.C, A = P.nq * D, k0 = c * kGemmChunkK, kc = min(kGemmChunkK, A - k0);
-    if (C == 1) {   // item (b, g) holds heads g G .. g G + G - 1 contiguously: index b A + j
-        constexpr int NB = 8;
-        const int n4 = nb * kc / 4;
-        for (int t0 = threadIdx.x; t0 < n4; t0 += NB * kThreads) {
-            float4 v[NB];
-            float den[NB];
-#pragma unroll
-            for (int q = 0; q < NB; ++q) {
-                const int t = t0 + q * kThreads;
-                v[q] = make_float4(0.f, 0.f, 0.f, 0.f);
-                den[q] = 1.f;
-                if (t < n4) {
-                    const int b = t / (kc / 4), j = k0 + (t % (kc / 4)) * 4;
-                    const u32x4 u = ld_dev_16B(P.part_o + (size_t)(b0 + b) * A + j);
-                    v[q] = make_float4(__uint_as_float(u.x), __uint_as_float(u.y),
-                                       __uint_as_float(u.z), __uint_as_float(u.w));
-                    den[q] = ld_dev(P.part_s + ((size_t)(b0 + b) * P.nq + j / D) * 2 + 1);
-                }
-            }
-#pragma unroll
-            for (int q = 0; q < NB; ++q) {
-                const int t = t0 + q * kThreads;
-                if (t < n4) {
-                    const int b = t / (kc / 4), jj = (t % (kc / 4)) * 4;
-                    const float r = 1.0f / den[q];
-                    unsigned *dst = reinterpret_cast<unsigned *>(buf + b * kActStride + jj);
-                    dst[0] = (unsigned)f2bf(v[q].x * r) | ((unsigned)f2bf(v[q].y * r) << 16);
-                    dst[1] = (unsigned)f2bf(v[q].z * r) | ((unsigned)f2bf(v[q].w * r) << 16);
-                }
-            }
-        }
-        return;
-    }
     for (int t = threadIdx.x; t < nb * kc; t += kThreads) {
         const int b = t / kc, j = k0 + t % kc, h = j / D, g = h / G, hl = h % G, dd = j % D;
         const size_t item0 = ((size_t)(b0 + b) * P.nkv + g) * C;
@@ -1003,42 +947,7 @@ __device__ __forceinline__ void stage_o_full(const StepParams &P, int c, int b0,
             num = fmaf(ld_dev(P.part_o + (item0 + cc) * G * D + hl * D + dd), w, num);
             den = fmaf(ld_dev(P.part_s + ((item0 + cc) * G + hl) * 2 + 1), w, den);
         }
-        buf[b * kActStride + (j - k0)] = f2bf(num / den);
-    }
-}
-
-// Chunk c of FFN column block j's SwiGLU values, as bf16 (16-byte loads, in
-// one batch per thread); j < 0: chunk c of all columns.
-__device__ __forceinline__ void stage_m_chunk(const StepParams &P, int j, int c, int b0, int nb,
-                                              uint16_t *buf) {
-    constexpr int NB = 8;
-    const int kw = j < 0 ? P.Fp : P.KTc * kTileK, k0 = c * kGemmChunkK;
-    const int kc = min(kGemmChunkK, kw - k0);
-    const size_t col0 = j < 0 ? 0 : (size_t)j * kw;
-    const int n4 = nb * kc / 4;
-    for (int t0 = threadIdx.x; t0 < n4; t0 += NB * kThreads) {
-        u32x4 v[NB];
-#pragma unroll
-        for (int q = 0; q < NB; ++q) {
-            const int t = t0 + q * kThreads;
-            v[q] = u32x4{0u, 0u, 0u, 0u};
-            if (t < n4) {
-                const int b = t / (kc / 4), k = (t % (kc / 4)) * 4;
-                v[q] = ld_dev_16B(P.m + (size_t)(b0 + b) * P.Fp + col0 + k0 + k);
-            }
-        }
-#pragma unroll
-        for (int q = 0; q < NB; ++q) {
-            const int t = t0 + q * kThreads;
-            if (t < n4) {
-                const int b = t / (kc / 4), k = (t % (kc / 4)) * 4;
-                unsigned *dst = reinterpret_cast<unsigned *>(buf + b * kActStride + k);
-                dst[0] = (unsigned)f2bf(__uint_as_float(v[q].x)) |
-                         ((unsigned)f2bf(__uint_as_float(v[q].y)) << 16);
-                dst[1] = (unsigned)f2bf(__uint_as_float(v[q].z)) |
-                         ((unsigned)f2bf(__uint_as_float(v[q].w)) << 16);
-            }
-        }
+        split_bf16(num / den, buf[b * kActStride + (j - k0)], buf[kLoOff + b * kActStride + (j - k0)]);
     }
 }
 
@@ -1322,8 +1231,13 @@ __device__ __forceinline__ void attn_item(KArg ka, int l, int b, int g, int c, b
         float s = 0.f;
         for (int w = 0; w < kWaves; ++w) s += red[(w * G + h) * D + dd];
         st_dev(out + t, s);
-        if (P.C == 1)   // (one chunk: the merged output is final; the batched O projection copies it)
-            st_dev_u16(P.acto + (size_t)b * P.nq * D + (size_t)g * G * D + t, f2bf(s / st[h * 4 + 1]));
+        if (P.C == 1) {   // (one chunk: the merged output is final; the batched O projection copies it)
+            uint16_t hi, lo;
+            split_bf16(s / st[h * 4 + 1], hi, lo);
+            const size_t o = (size_t)b * P.nq * D + (size_t)g * G * D + t;
+            st_dev_u16(P.acto + o, hi);
+            st_dev_u16(P.acto_lo + o, lo);
+        }
     }
     if (threadIdx.x < G) {
         st_dev(sts + threadIdx.x * 2, st[threadIdx.x * 4 + 0]);
@@ -1426,7 +1340,8 @@ __device__ __forceinline__ void phase_oproj(KArg ka, int l, int gwait, int garri
             P, S, Wo, P.nkv * KTO, a0, a1 - a0,
             [&]() { if (gwait >= 0) bar_wait(P, gwait, ti); }, [&]() {}, [&](int) {}, P.C == 1,
             [&](int c, int b0, int nb, uint16_t *buf) {
-                if (P.C == 1) stage_bf16_chunk(P.acto, P.nq * D, P.nq * D, c, b0, nb, buf);
+                if (P.C == 1)
+                    stage_bf16_chunk(P.acto, P.acto_lo, P.nq * D, P.nq * D, c, b0, nb, buf);
                 else stage_o_full<D, G>(P, c, b0, nb, buf);
             },
             epi, KTO, (size_t)P.o_rg * KTO);
@@ -1481,8 +1396,14 @@ __device__ __forceinline__ void phase_gateup(KArg ka, int l, int gwait, int xbar
         true, [&](int c, int b0, int nb, uint16_t *buf) { stage_act_chunk(P, c, b0, nb, buf); },
         [&](int b, int r, float gt, float up) {
             const float mv = gt / (1.0f + expf(-gt)) * up;
-            if constexpr (BAT) st_dev_u16(P.actm + (size_t)b * P.Fp + (r >> 1), f2bf(mv));
-            else st_dev(P.m + (size_t)b * P.Fp + (r >> 1), mv);
+            if constexpr (BAT) {
+                uint16_t hi, lo;
+                split_bf16(mv, hi, lo);
+                st_dev_u16(P.actm + (size_t)b * P.Fp + (r >> 1), hi);
+                st_dev_u16(P.actm_lo + (size_t)b * P.Fp + (r >> 1), lo);
+            } else {
+                st_dev(P.m + (size_t)b * P.Fp + (r >> 1), mv);
+            }
         });
     if constexpr (BAT) {
         if (garrive >= 0) bar_arrive(P, garrive, ti);
@@ -1511,7 +1432,7 @@ __device__ __forceinline__ void phase_down(KArg ka, int l, int gwait, int garriv
             P, S, Wd, P.Sc * P.KTc, a0, a1 - a0,
             [&]() { if (gwait >= 0) bar_wait(P, gwait, ti); }, [&]() {}, [&](int) {}, true,
             [&](int c, int b0, int nb, uint16_t *buf) {
-                stage_bf16_chunk(P.actm, P.Fp, P.Fp, c, b0, nb, buf);
+                stage_bf16_chunk(P.actm, P.actm_lo, P.Fp, P.Fp, c, b0, nb, buf);
             },
             epi, P.KTc, (size_t)P.down_rg * P.KTc);
     } else {
