@@ -28,8 +28,9 @@ PEAK_HBM_GBS = 8000.0
 # scaled by a plain copy kernel), with the hash of the device source it was
 # taken on: reported only while that source is unchanged.
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "kl_step_kernel_traffic.md")
-DEVICE_SRC = [os.path.join(ROOT, "paper_2410_23668_amd", "csrc", f)
-              for f in ("kl_device.hip", "kl_internal.h")]
+CSRC = os.path.join(ROOT, "paper_2410_23668_amd", "csrc")
+DEVICE_SRC = sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC)
+                    if f.endswith((".hip", ".h", ".cpp")))
 
 
 def log(msg):
