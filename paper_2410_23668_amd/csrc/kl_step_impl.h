@@ -421,6 +421,55 @@ __device__ __forceinline__ void stage_vec(const float *__restrict__ src, int n, 
 // same batch as x (a dependent second batch would cost a second memory round
 // trip, ~2 us when HBM is saturated), and so are the ne floats of an optional
 // extra vector (esrc -> edst in LDS), e.g. the RoPE row the epilogue needs.
+// RMSNorm staging for the GEMV path, with the normalisation deferred: the
+// weight product is linear, so W (x r g) = r (W (x g)) with the per-sequence
+// scale r = 1 / sqrt(mean(x^2) + eps) applied in the epilogue (rms_scale).
+// Stages a = x g (and the gain at a + npad, zero padding) and leaves each
+// wave's partial sum of x^2 in sm[wave]; the weight stream starts as soon as
+// a is in LDS, without waiting for a block-wide reduction.
+__device__ __forceinline__ void stage_rms_deferred(const long long *__restrict__ xf,
+                                                   const float *__restrict__ gain, int n, int npad,
+                                                   float *a, float *sm,
+                                                   const float *esrc = nullptr,
+                                                   float *edst = nullptr, int ne = 0) {
+    float ss = 0.f;
+    for (int i0 = threadIdx.x; i0 < npad; i0 += kStageBatch * kThreads) {
+        long long v[kStageBatch];
+        float gv[kStageBatch];
+        float ev = 0.f;
+        const bool first = i0 == (int)threadIdx.x;
+#pragma unroll
+        for (int k = 0; k < kStageBatch; ++k) {
+            const int i = i0 + k * kThreads;
+            v[k] = i < n ? (long long)ld_dev_u64(xf + i) : 0ll;
+            gv[k] = i < n ? gain[i] : 0.f;
+        }
+        if (first && (int)threadIdx.x < ne) ev = esrc[threadIdx.x];
+#pragma unroll
+        for (int k = 0; k < kStageBatch; ++k) {
+            const int i = i0 + k * kThreads;
+            const float x = from_fix(v[k]);
+            ss = fmaf(x, x, ss);
+            if (i < npad) {
+                a[i] = x * gv[k];
+                a[npad + i] = gv[k];
+            }
+        }
+        if (first && (int)threadIdx.x < ne) edst[threadIdx.x] = ev;
+    }
+    ss = wave_sum(ss);
+    if ((threadIdx.x & 63) == 0) sm[threadIdx.x >> 6] = ss;
+    __syncthreads();
+}
+// The scale r of the sequence staged last by stage_rms_deferred (the wave
+// partials are added in wave order: the same value in every thread).
+__device__ __forceinline__ float rms_scale(const float *sm, int n, float eps) {
+    float ss = 0.f;
+#pragma unroll
+    for (int w = 0; w < kThreads / 64; ++w) ss += sm[w];
+    return 1.0f / sqrtf(ss / (float)n + eps);
+}
+
 __device__ __forceinline__ void stage_rmsnorm(const long long *__restrict__ xf,
                                               const float *__restrict__ gain, int n, int npad,
                                               float eps, float *a, float *sm,
@@ -999,13 +1048,18 @@ __device__ __forceinline__ void phase_qkv(KArg ka, int l, int gwait, int xbar, i
         [&]() { norm_batched(P, S, gain, xbar); },
         [&](int b) {
             // the RoPE row of this sequence's position rides along (a + 2 Hp)
-            stage_rmsnorm(P.xf + (size_t)b * P.Hp, gain, P.H, P.Hp, P.eps, S.a, S.sm,
-                          reinterpret_cast<const float *>(P.rope + (size_t)eff_pos(P, b) * half),
-                          S.a + 2 * P.Hp, 2 * half);
+            stage_rms_deferred(P.xf + (size_t)b * P.Hp, gain, P.H, P.Hp, S.a, S.sm,
+                               reinterpret_cast<const float *>(P.rope + (size_t)eff_pos(P, b) * half),
+                               S.a + 2 * P.Hp, 2 * half);
             if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 3);
         },
         true, [&](int c, int b0, int nb, uint16_t *buf) { stage_act_chunk(P, c, b0, nb, buf); },
         [&](int b, int r, float y0, float y1) {
+            if (!batched) {   // the deferred RMSNorm scale
+                const float rs = rms_scale(S.sm, P.H, P.eps);
+                y0 *= rs;
+                y1 *= rs;
+            }
             const int p = eff_pos(P, b);
             const int lr = r - row0;
             if (lr < (G + 1) * d) {
@@ -1390,11 +1444,16 @@ __device__ __forceinline__ void phase_gateup(KArg ka, int l, int gwait, int xbar
         [&]() { if (gwait >= 0) bar_wait(P, gwait, ti); },
         [&]() { norm_batched(P, S, gain, xbar); },
         [&](int b) {
-            stage_rmsnorm(P.xf + (size_t)b * P.Hp, gain, P.H, P.Hp, P.eps, S.a, S.sm);
+            stage_rms_deferred(P.xf + (size_t)b * P.Hp, gain, P.H, P.Hp, S.a, S.sm);
             if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 3);
         },
         true, [&](int c, int b0, int nb, uint16_t *buf) { stage_act_chunk(P, c, b0, nb, buf); },
         [&](int b, int r, float gt, float up) {
+            if constexpr (!BAT) {   // the deferred RMSNorm scale
+                const float rs = rms_scale(S.sm, P.H, P.eps);
+                gt *= rs;
+                up *= rs;
+            }
             const float mv = gt / (1.0f + expf(-gt)) * up;
             if constexpr (BAT) {
                 uint16_t hi, lo;
@@ -1476,11 +1535,16 @@ __device__ __forceinline__ void phase_head(KArg ka, int gwait, int xbar, int ti)
         },
         [&]() { norm_batched(P, S, P.final_norm, xbar); },
         [&](int b) {
-            stage_rmsnorm(P.xf + (size_t)b * P.Hp, P.final_norm, P.H, P.Hp, P.eps, S.a, S.sm);
+            stage_rms_deferred(P.xf + (size_t)b * P.Hp, P.final_norm, P.H, P.Hp, S.a, S.sm);
             if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 3);
         },
         true, [&](int c, int b0, int nb, uint16_t *buf) { stage_act_chunk(P, c, b0, nb, buf); },
         [&](int b, int r, float y0, float y1) {
+            if constexpr (!BAT) {   // the deferred RMSNorm scale
+                const float rs = rms_scale(S.sm, P.H, P.eps);
+                y0 *= rs;
+                y1 *= rs;
+            }
             float *lg = P.logits + (size_t)b * V;
             if (r < V) lg[r] = y0;
             if (r + 1 < V) lg[r + 1] = y1;
