@@ -353,6 +353,8 @@ __device__ __forceinline__ StepParams load_params(KArg ka) {
 // ---------------------------------------------------------------- LDS layout
 
 // Offsets (in floats) come from the host, which sizes the allocation.
+constexpr int kSmLastFlag = 32;   // sm slot: this workgroup's attention result arrived last
+
 struct Lds {
     float *a;     // activation vector (max K extent); aliased by the attention area
     float *attn;  // attention scratch (same storage as a)
@@ -887,8 +889,10 @@ __device__ __forceinline__ void gemm_rows(const uint8_t *__restrict__ W, int KT,
 //                  the q/k/v rows of that head, so the attention of head g
 //                  waits only for them (Sg arrivals per layer).
 //   cnt_attn[g]    attn -> oproj: the chunk results of KV head g (B * C per
-//                  layer); the same workgroups then merge them and apply the
-//                  O-projection columns of head g, adding into the residual.
+//                  layer), then (GEMV path) one more arrival once the
+//                  workgroup that delivered the last of them has merged them;
+//                  head g's workgroups then apply the O-projection columns of
+//                  head g to the merged output, adding into the residual.
 //   cnt_gu[j]      gateup -> down: column block j of the FFN (Rc workgroups
 //                  compute its SwiGLU values; the same Rc workgroups then
 //                  apply the matching columns of the down projection).
@@ -1087,6 +1091,65 @@ __device__ __forceinline__ void phase_qkv(KArg ka, int l, int gwait, int xbar, i
     if (member) local_arrive(P, P.cnt + g, ti);
 }
 
+// Merge the C chunk results of (sequence b, KV head g) in chunk order into
+// o[G * D] (LDS): o_h = sum_c w_ch A_ch / sum_c w_ch L_ch, w_ch = exp(M_ch - M_h).
+// Every thread owns outputs j; its loads of all chunks' values for j are
+// issued together (batches of kCombBatch) with the statistics loads.
+template <int D, int G>
+__device__ __forceinline__ void merge_chunks(const StepParams &P, int b, int g, float *o,
+                                             float *scratch) {
+    const int C = P.C;
+    const size_t item0 = ((size_t)b * P.nkv + g) * C;
+    const float *po = P.part_o + item0 * G * D;
+    const float *ps = P.part_s + item0 * G * 2;
+    float *cM = scratch, *cL = cM + C * G, *cW = cL + C * G, *cT = cW + C * G;
+    for (int j = threadIdx.x; j - (int)threadIdx.x < G * D; j += kThreads) {
+        const bool jv = j < G * D;
+        const int h = jv ? j / D : 0;
+        float num = 0.f;
+        for (int c0 = 0; c0 < C; c0 += kCombBatch) {
+            float av[kCombBatch];
+            // (unconditional loads from in-range addresses, masked when used: a
+            // load under a per-lane condition would be waited for on its own)
+#pragma unroll
+            for (int k = 0; k < kCombBatch; ++k)
+                av[k] = ld_dev(po + (size_t)min(c0 + k, C - 1) * G * D + (jv ? j : 0));
+            if (j == (int)threadIdx.x && c0 == 0) {
+                // (first pass only, uniform across the block) statistics:
+                // wave h takes head h, lane c chunk c (strided): the chunk
+                // weights w_ch = exp(M_ch - M_h) and their sum, by wave
+                // reductions instead of a per-thread pass over the chunks
+                const int wid = threadIdx.x >> 6, lane = threadIdx.x & 63;
+                if (wid < G) {
+                    float mx = -INFINITY;
+                    for (int cc = lane; cc < C; cc += 64) {
+                        const unsigned long long v = ld_dev_u64(ps + ((size_t)cc * G + wid) * 2);
+                        cM[cc * G + wid] = __uint_as_float((unsigned)v);
+                        cL[cc * G + wid] = __uint_as_float((unsigned)(v >> 32));
+                        mx = fmaxf(mx, __uint_as_float((unsigned)v));
+                    }
+                    mx = wave_max(mx);
+                    float tot = 0.f;
+                    for (int cc = lane; cc < C; cc += 64) {
+                        const float m = cM[cc * G + wid];
+                        const float w = (m == -INFINITY) ? 0.f : expf(m - mx);
+                        cW[cc * G + wid] = w;
+                        tot = fmaf(cL[cc * G + wid], w, tot);
+                    }
+                    tot = wave_sum(tot);
+                    if (lane == 0) cT[wid] = tot;
+                }
+                __syncthreads();
+            }
+#pragma unroll
+            for (int k = 0; k < kCombBatch; ++k)
+                if (c0 + k < C) num = fmaf(av[k], cW[(c0 + k) * G + h], num);
+        }
+        if (jv) o[j] = num / cT[h];
+    }
+    __syncthreads();
+}
+
 // One attention work item: chunk c of sequence b against KV head g, for the
 // G query heads of that group (split-K flash decoding).  Positions are
 // grouped in slabs of PP positions (one 16-byte load per lane covers a slab);
@@ -1102,7 +1165,7 @@ __device__ __forceinline__ void phase_qkv(KArg ka, int l, int gwait, int xbar, i
 template <int D>
 constexpr int attn_sub() { return kWaves * kAttnLoads * (64 / (D / 8)); }
 
-template <int D, int G>
+template <int D, int G, bool LAST>
 __device__ __forceinline__ void attn_item(KArg ka, int l, int b, int g, int c, bool first,
                                           int ti) {
     const StepParams P = load_params(ka);
@@ -1299,82 +1362,64 @@ __device__ __forceinline__ void attn_item(KArg ka, int l, int b, int g, int c, b
     }
     if (is_ctl_lane0()) trace_stamp(P, ti, 3);
     drain_all();
-    if (is_ctl_lane0())
-        __hip_atomic_fetch_add(P.cnt + P.nkv + g, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (is_ctl_lane0()) {
+        if (LAST) {
+            const unsigned old = __hip_atomic_fetch_add(P.cnt + P.nkv + g, 1u, __ATOMIC_RELAXED,
+                                                        __HIP_MEMORY_SCOPE_AGENT);
+            // the last chunk result of head g in layer l (per layer: B C
+            // results, then the merged output)
+            const unsigned per_layer = (unsigned)(P.B * P.C) + 1u;
+            S.sm[kSmLastFlag] = (old == (unsigned)l * per_layer + per_layer - 2u) ? 1.f : 0.f;
+        } else {
+            __hip_atomic_fetch_add(P.cnt + P.nkv + g, 1u, __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+        }
+    }
 }
 
 // Attention of KV head g: the workgroups of head g take its items (sequence b,
-// chunk c) round-robin.
-template <int D, int G>
+// chunk c) round-robin.  GEMV path: the workgroup whose chunk result of head
+// g arrives last merges the chunk results of every sequence (in chunk order)
+// and publishes o_g in place of the queries (no longer needed in this layer);
+// the O projection then stages G d values instead of merging C chunks in each
+// of its workgroups.
+template <int D, int G, bool BAT>
 __device__ __forceinline__ void phase_attn(KArg ka, int l, int garrive, int ti) {
     const StepParams P = load_params(ka);
+    const Lds S = lds_layout(kl_smem, P);
     const int g = blockIdx.x / P.Sg, part = blockIdx.x % P.Sg;
     if (g < P.nkv) {
         const int items = P.B * P.C;
-        for (int it = part; it < items; it += P.Sg)
-            attn_item<D, G>(ka, l, it / P.C, g, it % P.C, it == part, ti);
+        bool last = false;
+        for (int it = part; it < items; it += P.Sg) {
+            attn_item<D, G, !BAT>(ka, l, it / P.C, g, it % P.C, it == part, ti);
+            if (!BAT) {
+                __syncthreads();
+                last = last || S.sm[kSmLastFlag] != 0.f;
+            }
+        }
+        if (!BAT && last) {
+            for (int b = 0; b < P.B; ++b) {
+                merge_chunks<D, G>(P, b, g, S.a, S.a + G * D);
+                float *o = P.q + (size_t)b * P.nq * D + (size_t)g * G * D;
+                for (int t = threadIdx.x; t < G * D; t += kThreads) st_dev(o + t, S.a[t]);
+                __syncthreads();   // (S.a is the next sequence's merge area)
+            }
+            drain_all();
+            if (is_ctl_lane0())
+                __hip_atomic_fetch_add(P.cnt + P.nkv + g, 1u, __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+        }
     }
     // (batched steps: the O projection takes all heads and waits on the grid)
     if (garrive >= 0) bar_arrive(P, garrive, ti);
     else if (is_ctl_lane0()) trace_stamp(P, ti, 0);
 }
 
-// Merge the C chunk results of (sequence b, KV head g) in chunk order into
-// o[G * D] (LDS): o_h = sum_c w_ch A_ch / sum_c w_ch L_ch, w_ch = exp(M_ch - M_h).
-// Every thread owns outputs j; its loads of all chunks' values for j are
-// issued together (batches of kCombBatch) with the statistics loads.
-template <int D, int G>
-__device__ __forceinline__ void merge_chunks(const StepParams &P, int b, int g, float *o,
-                                             float *scratch) {
-    const int C = P.C;
-    const size_t item0 = ((size_t)b * P.nkv + g) * C;
-    const float *po = P.part_o + item0 * G * D;
-    const float *ps = P.part_s + item0 * G * 2;
-    float *cM = scratch, *cL = cM + C * G, *cW = cL + C * G, *cT = cW + C * G;
-    for (int j = threadIdx.x; j - (int)threadIdx.x < G * D; j += kThreads) {
-        const bool jv = j < G * D;
-        const int h = jv ? j / D : 0;
-        float num = 0.f;
-        for (int c0 = 0; c0 < C; c0 += kCombBatch) {
-            float av[kCombBatch];
-#pragma unroll
-            for (int k = 0; k < kCombBatch; ++k)
-                av[k] = (jv && c0 + k < C) ? ld_dev(po + (size_t)(c0 + k) * G * D + j) : 0.f;
-            if (j == (int)threadIdx.x && c0 == 0) {
-                // (first pass only, uniform across the block)
-                for (int t = threadIdx.x; t < C * G; t += kThreads) {
-                    const unsigned long long v = ld_dev_u64(ps + (size_t)t * 2);
-                    cM[t] = __uint_as_float((unsigned)v);
-                    cL[t] = __uint_as_float((unsigned)(v >> 32));
-                }
-                __syncthreads();
-                for (int t = threadIdx.x; t < C * G; t += kThreads) {
-                    const int hh = t % G;
-                    float M = -INFINITY;
-                    for (int cc = 0; cc < C; ++cc) M = fmaxf(M, cM[cc * G + hh]);
-                    cW[t] = (cM[t] == -INFINITY) ? 0.f : expf(cM[t] - M);
-                }
-                __syncthreads();
-                if (threadIdx.x < G) {
-                    float lsum = 0.f;
-                    for (int cc = 0; cc < C; ++cc)
-                        lsum = fmaf(cL[cc * G + threadIdx.x], cW[cc * G + threadIdx.x], lsum);
-                    cT[threadIdx.x] = lsum;
-                }
-                __syncthreads();
-            }
-#pragma unroll
-            for (int k = 0; k < kCombBatch; ++k)
-                if (c0 + k < C) num = fmaf(av[k], cW[(c0 + k) * G + h], num);
-        }
-        if (jv) o[j] = num / cT[h];
-    }
-    __syncthreads();
-}
-
 // O projection of KV head g: x += Wo[:, columns of head g] o_g, for the rows
 // this workgroup owns among head g's workgroups, added into the fixed-point
-// residual.  The chunk merge is the activation staging of this GEMV.
+// residual.  GEMV path: the staged input is head g's merged attention output,
+// published by the attention phase.
 template <int D, int G, bool BAT>
 __device__ __forceinline__ void phase_oproj(KArg ka, int l, int gwait, int garrive, int ti) {
     const StepParams P = load_params(ka);
@@ -1404,12 +1449,13 @@ __device__ __forceinline__ void phase_oproj(KArg ka, int l, int gwait, int garri
         if (g < P.nkv) {
             int a0, a1;
             split_range(P.o_rg, P.Sg, part, a0, a1);
-            const unsigned target = (unsigned)(l + 1) * (unsigned)(P.B * P.C);
+            // head g's merged outputs are published: B C chunk results + 1 per layer
+            const unsigned target = (unsigned)(l + 1) * (unsigned)(P.B * P.C + 1);
             weight_phase<false>(
                 P, S, Wo + (size_t)g * P.o_rg * KTO * kTileBytes, KTO, a0, a1 - a0,
                 [&]() { local_wait(P, P.cnt + P.nkv + g, target, ti); }, [&]() {},
                 [&](int b) {
-                    merge_chunks<D, G>(P, b, g, S.a, S.a + G * D);
+                    stage_vec(P.q + (size_t)b * P.nq * D + (size_t)g * G * D, G * D, G * D, S.a);
                     if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 3);
                 },
                 false, [&](int, int, int, uint16_t *) {}, epi);
@@ -1585,7 +1631,7 @@ __global__ __launch_bounds__(kThreads) void kl_step_kernel(StepParams P, int l0,
             const int w = gw(), x = xb();
             phase_qkv<BAT>(ka, l, w, x, ti++);
         }
-        if (phases & kPhAttn) phase_attn<D, G>(ka, l, BAT ? ga(has_op) : -1, ti++);
+        if (phases & kPhAttn) phase_attn<D, G, BAT>(ka, l, BAT ? ga(has_op) : -1, ti++);
         if (phases & kPhOproj) {
             const int w = BAT && has_attn ? gw() : -1, a = ga(has_gu);
             phase_oproj<D, G, BAT>(ka, l, w, a, ti++);
