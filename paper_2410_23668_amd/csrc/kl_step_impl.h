@@ -952,16 +952,41 @@ __device__ __forceinline__ void norm_batched(const StepParams &P, const Lds &S,
 }
 
 // Chunk c of the normalised activations (control wave: memory-to-LDS copies).
-__device__ __forceinline__ void stage_act_chunk(const StepParams &P, int c, int b0, int nb,
-                                                uint16_t *buf) {
+//
+// Rows k0 .. k0 + kc - 1 (kc <= kGemmChunkK: one 16-byte copy per lane and row)
+// of both terms of sequences b0 .. b0 + nb - 1 of a two-term bf16 matrix with
+// row stride ld.  The copies are straight-line code without branches: a
+// branch or loop between two copies makes the compiler wait for the first
+// before issuing the second (it cannot tell that their LDS ranges are
+// disjoint).  So every padding row (b >= nb) receives a copy of row nb - 1,
+// and lanes past kc copy a clamped in-row address: the matrix-core loop
+// reads neither (outputs of padding sequences are discarded, columns past
+// kc are never consumed).
+__device__ __forceinline__ void ctl_copy_rows(const uint16_t *hi, const uint16_t *lo, int ld,
+                                              int k0, int kc, int b0, int nb, uint16_t *buf) {
     if ((threadIdx.x >> 6) != kCtlWave) return;
-    const int k0 = c * kGemmChunkK, kc = min(kGemmChunkK, P.Hp - k0);
-    for (int b = 0; b < nb; ++b) {
-        const size_t o = (size_t)(b0 + b) * P.Hp + k0;
-        ctl_copy_to_lds(P.act + o, buf + b * kActStride, kc * 2);
-        ctl_copy_to_lds(P.act_lo + o, buf + kLoOff + b * kActStride, kc * 2);
+    const int lane = threadIdx.x & 63;
+    const uint64_t col = (uint64_t)(k0 + min(lane * 8, kc - 8));
+    // (the row offset is opaque to the compiler at each step, so that the
+    // addresses are formed right before their copies instead of all at once)
+    uint64_t row = (uint64_t)b0 * ld;
+    const uint64_t last = (uint64_t)(b0 + nb - 1) * ld;
+#pragma unroll
+    for (int b = 0; b < kGemmBatch; ++b) {
+        const uint64_t o = min(row, last) + col;
+        __builtin_amdgcn_global_load_lds(hi + o, buf + b * kActStride, 16, 0, kLdsCoherent);
+        __builtin_amdgcn_global_load_lds(lo + o, buf + kLoOff + b * kActStride, 16, 0,
+                                         kLdsCoherent);
+        row += (uint64_t)ld;
+        asm volatile("" : "+v"(row));
     }
     ctl_copy_wait();
+}
+
+__device__ __forceinline__ void stage_act_chunk(const StepParams &P, int c, int b0, int nb,
+                                                uint16_t *buf) {
+    const int k0 = c * kGemmChunkK;
+    ctl_copy_rows(P.act, P.act_lo, P.Hp, k0, min(kGemmChunkK, P.Hp - k0), b0, nb, buf);
 }
 
 // Chunk c of a two-term bf16 matrix src / src_lo [b][ld] with K columns
@@ -970,14 +995,8 @@ __device__ __forceinline__ void stage_act_chunk(const StepParams &P, int c, int 
 __device__ __forceinline__ void stage_bf16_chunk(const uint16_t *src, const uint16_t *src_lo,
                                                  int ld, int K, int c, int b0, int nb,
                                                  uint16_t *buf) {
-    if ((threadIdx.x >> 6) != kCtlWave) return;
-    const int k0 = c * kGemmChunkK, kc = min(kGemmChunkK, K - k0);
-    for (int b = 0; b < nb; ++b) {
-        const size_t o = (size_t)(b0 + b) * ld + k0;
-        ctl_copy_to_lds(src + o, buf + b * kActStride, kc * 2);
-        ctl_copy_to_lds(src_lo + o, buf + kLoOff + b * kActStride, kc * 2);
-    }
-    ctl_copy_wait();
+    const int k0 = c * kGemmChunkK;
+    ctl_copy_rows(src, src_lo, ld, k0, min(kGemmChunkK, K - k0), b0, nb, buf);
 }
 
 // Chunk c of the merged attention output of all heads (K = n_heads d), as
