@@ -889,8 +889,9 @@ __device__ __forceinline__ void gemm_rows(const uint8_t *__restrict__ W, int KT,
 //                  the q/k/v rows of that head, so the attention of head g
 //                  waits only for them (Sg arrivals per layer).
 //   cnt_attn[g]    attn -> oproj: the chunk results of KV head g (B * C per
-//                  layer), then (GEMV path) one more arrival once the
-//                  workgroup that delivered the last of them has merged them;
+//                  layer), then (GEMV path, up to 4 query heads per KV head)
+//                  one more arrival once the workgroup that delivered the
+//                  last of them has merged them;
 //                  head g's workgroups then apply the O-projection columns of
 //                  head g to the merged output, adding into the residual.
 //   cnt_gu[j]      gateup -> down: column block j of the FFN (Rc workgroups
@@ -1128,11 +1129,9 @@ __device__ __forceinline__ void merge_chunks(const StepParams &P, int b, int g, 
         float num = 0.f;
         for (int c0 = 0; c0 < C; c0 += kCombBatch) {
             float av[kCombBatch];
-            // (unconditional loads from in-range addresses, masked when used: a
-            // load under a per-lane condition would be waited for on its own)
 #pragma unroll
             for (int k = 0; k < kCombBatch; ++k)
-                av[k] = ld_dev(po + (size_t)min(c0 + k, C - 1) * G * D + (jv ? j : 0));
+                av[k] = (jv && c0 + k < C) ? ld_dev(po + (size_t)(c0 + k) * G * D + j) : 0.f;
             if (j == (int)threadIdx.x && c0 == 0) {
                 // (first pass only, uniform across the block) statistics:
                 // wave h takes head h, lane c chunk c (strided): the chunk
@@ -1397,11 +1396,16 @@ __device__ __forceinline__ void attn_item(KArg ka, int l, int b, int g, int c, b
 }
 
 // Attention of KV head g: the workgroups of head g take its items (sequence b,
-// chunk c) round-robin.  GEMV path: the workgroup whose chunk result of head
-// g arrives last merges the chunk results of every sequence (in chunk order)
-// and publishes o_g in place of the queries (no longer needed in this layer);
-// the O projection then stages G d values instead of merging C chunks in each
-// of its workgroups.
+// chunk c) round-robin.  GEMV path with up to 4 query heads per KV head: the
+// workgroup whose chunk result of head g arrives last merges the chunk
+// results of every sequence (in chunk order) and publishes o_g in place of
+// the queries (no longer needed in this layer); the O projection then stages
+// G d values instead of merging C chunks in each of its workgroups.  (With 8
+// query heads per KV head the attention already needs every register, and
+// the merge is left to the O projection's workgroups.)
+template <int D, int G, bool BAT>
+constexpr bool merge_last() { return !BAT && G <= 4; }
+
 template <int D, int G, bool BAT>
 __device__ __forceinline__ void phase_attn(KArg ka, int l, int garrive, int ti) {
     const StepParams P = load_params(ka);
@@ -1411,13 +1415,13 @@ __device__ __forceinline__ void phase_attn(KArg ka, int l, int garrive, int ti) 
         const int items = P.B * P.C;
         bool last = false;
         for (int it = part; it < items; it += P.Sg) {
-            attn_item<D, G, !BAT>(ka, l, it / P.C, g, it % P.C, it == part, ti);
-            if (!BAT) {
+            attn_item<D, G, merge_last<D, G, BAT>()>(ka, l, it / P.C, g, it % P.C, it == part, ti);
+            if (merge_last<D, G, BAT>()) {
                 __syncthreads();
                 last = last || S.sm[kSmLastFlag] != 0.f;
             }
         }
-        if (!BAT && last) {
+        if (merge_last<D, G, BAT>() && last) {
             for (int b = 0; b < P.B; ++b) {
                 merge_chunks<D, G>(P, b, g, S.a, S.a + G * D);
                 float *o = P.q + (size_t)b * P.nq * D + (size_t)g * G * D;
@@ -1468,13 +1472,18 @@ __device__ __forceinline__ void phase_oproj(KArg ka, int l, int gwait, int garri
         if (g < P.nkv) {
             int a0, a1;
             split_range(P.o_rg, P.Sg, part, a0, a1);
-            // head g's merged outputs are published: B C chunk results + 1 per layer
-            const unsigned target = (unsigned)(l + 1) * (unsigned)(P.B * P.C + 1);
+            // head g's chunk results (and, when the attention phase merges
+            // them, the merged output: one more arrival per layer)
+            constexpr bool merged = merge_last<D, G, false>();
+            const unsigned target = (unsigned)(l + 1) * (unsigned)(P.B * P.C + (merged ? 1 : 0));
             weight_phase<false>(
                 P, S, Wo + (size_t)g * P.o_rg * KTO * kTileBytes, KTO, a0, a1 - a0,
                 [&]() { local_wait(P, P.cnt + P.nkv + g, target, ti); }, [&]() {},
                 [&](int b) {
-                    stage_vec(P.q + (size_t)b * P.nq * D + (size_t)g * G * D, G * D, G * D, S.a);
+                    if (merged)
+                        stage_vec(P.q + (size_t)b * P.nq * D + (size_t)g * G * D, G * D, G * D, S.a);
+                    else
+                        merge_chunks<D, G>(P, b, g, S.a, S.a + G * D);
                     if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 3);
                 },
                 false, [&](int, int, int, uint16_t *) {}, epi);
