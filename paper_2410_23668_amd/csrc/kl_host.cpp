@@ -28,8 +28,9 @@ struct kl_state {
     float2 *rope;
     uint8_t *scratch;
     size_t scratch_bytes;
-    long long *xf;
-    float *q, *m, *part_o, *part_s;
+    long long *xf, *xf2;
+    float *q, *m, *part_o, *part_s, *xpart;
+    int KSo, KSd;                     // K slices of the batched O and down projections
     uint16_t *act, *act_lo, *actm, *actm_lo, *acto, *acto_lo;
     int Sg, Sc, Rc, KTc;
     unsigned long long *bar;
@@ -115,6 +116,12 @@ std::vector<int32_t> qkv_rowmap(const kl_config &c) {
 
 // FFN column blocks: the largest divisor of the k-tile count of ffn_dim that
 // is at most 32 (and at most the grid).
+int largest_divisor_at_most(int n, int cap) {
+    for (int k = std::min(n, cap); k > 1; --k)
+        if (n % k == 0) return k;
+    return 1;
+}
+
 int ffn_column_blocks(int ktf, int nwg) {
     int best = 1;
     for (int s = 1; s <= std::min(32, std::min(ktf, nwg)); ++s)
@@ -183,7 +190,9 @@ StepParams base_params(const kl_state &s) {
     P.final_norm = reinterpret_cast<const float *>(s.arena + s.off_final_norm);
     P.lm_head = reinterpret_cast<const uint16_t *>(s.arena + s.off_lm_head);
     P.rope = s.rope;
-    P.xf = s.xf; P.q = s.q; P.m = s.m; P.part_o = s.part_o; P.part_s = s.part_s; P.act = s.act;
+    P.xf = s.xf; P.xf2 = s.xf2; P.xpart = s.xpart; P.xpart_stride = c.max_batch * s.Hp;
+    P.KSo = s.KSo; P.KSd = s.KSd;
+    P.q = s.q; P.m = s.m; P.part_o = s.part_o; P.part_s = s.part_s; P.act = s.act;
     P.act_lo = s.act_lo; P.actm = s.actm; P.actm_lo = s.actm_lo; P.acto = s.acto;
     P.acto_lo = s.acto_lo;
     P.bar = s.bar; P.cnt = s.cnt; P.err = s.err; P.dummy = s.dummy;
@@ -310,6 +319,15 @@ kl_status kl_model_create(const kl_config *cfg, kl_state **out) {
     const size_t off_cnt = so;  so = align_up(so + (size_t)(2 * nkv + S->Sc) * 4, 256);
     const size_t off_err = so;  so = align_up(so + 256, 256);
     const size_t off_dummy = so; so = align_up(so + kTileBytes, 256);
+    // batched path: the second residual buffer and the K-slice partial sums
+    // of the O and down projections (folded by the next RMSNorm step)
+    S->KSo = largest_divisor_at_most(nkv, kMaxKSlices);
+    S->KSd = largest_divisor_at_most(S->Sc, kMaxKSlices);
+    const bool batched = B >= kMfmaBatch;
+    const size_t off_x2 = so;
+    if (batched) so = align_up(so + (size_t)B * S->Hp * 8, 256);
+    const size_t off_xp = so;
+    if (batched) so = align_up(so + (size_t)std::max(S->KSo, S->KSd) * B * S->Hp * 4, 256);
     S->scratch_bytes = so;
     TRY(hipMalloc(&S->scratch, S->scratch_bytes));
     TRY(hipMemsetAsync(S->scratch, 0, S->scratch_bytes, s));
@@ -328,6 +346,8 @@ kl_status kl_model_create(const kl_config *cfg, kl_state **out) {
     S->cnt = reinterpret_cast<unsigned *>(S->scratch + off_cnt);
     S->err = reinterpret_cast<int *>(S->scratch + off_err);
     S->dummy = S->scratch + off_dummy;
+    S->xf2 = batched ? reinterpret_cast<long long *>(S->scratch + off_x2) : nullptr;
+    S->xpart = batched ? reinterpret_cast<float *>(S->scratch + off_xp) : nullptr;
 
     // RoPE table (cos, sin) of pos * theta^(-2i/d), computed in double
     {

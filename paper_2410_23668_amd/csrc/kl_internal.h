@@ -29,6 +29,7 @@ constexpr int kGemmBatch = 32;
 constexpr int kGemmChunkK = 512;
 constexpr int kActStride = kGemmChunkK + 8;   // bf16 per staged activation row (bank spread)
 constexpr int kGemmMaxBlk = 4;            // 16-row blocks per wave per pass over the weights
+constexpr int kMaxKSlices = 8;            // K slices of the batched O and down projections
 // LDS of the batched path (bytes): two activation chunks of both terms, and
 // per-wave weight re-layout slots (2 KiB; after the chunk loop they hold the
 // partial products of one block)
@@ -76,6 +77,10 @@ struct StepParams {
     float *logits, *hidden_out;
     // scratch
     long long *xf;             // [max_batch][Hp] residual stream, fixed point (2^-32 units)
+    long long *xf2;            // batched path: the other residual buffer (the folds alternate)
+    float *xpart;              // batched path: K-slice partials [ks][max_batch][Hp] (O, down)
+    int xpart_stride;          // floats between consecutive K-slice partials
+    int KSo, KSd;              // K slices of the batched O and down projections
     float *q;                  // [max_batch][nq*d] rotated queries
     float *m;                  // [max_batch][Fp] SwiGLU output (padding stays 0)
     float *part_o;             // attention chunk outputs [B*nkv*C][group*d]

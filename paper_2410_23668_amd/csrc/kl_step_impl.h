@@ -929,20 +929,60 @@ __device__ __forceinline__ void weight_phase(const StepParams &P, const Lds &S,
     }
 }
 
-// Batched RMSNorm: act / act_lo [b][k] = the two bf16 terms of x_b[k] r_b gain[k]
-// for every sequence,
-// the (sequence, kGemmChunkK-column slice) items spread over the grid; ends
-// with grid barrier k, after which any workgroup may stage any slice.
+// Batched RMSNorm.  The K-slice partial sums of the last O or down
+// projection (nparts of them) are first folded into the residual,
+// x = x_in + sum_s fix(part_s) (exact integer adds, so the order is
+// immaterial), and this item's slice of x is written to x_out; then
+// act / act_lo = the two bf16 terms of x r gain.  Items (sequence,
+// kGemmChunkK-column slice) are spread over the grid; each reads its
+// sequence's whole row (the norm needs all of it).  Ends with grid barrier
+// k, after which any workgroup may stage any slice.
 __device__ __forceinline__ void norm_batched(const StepParams &P, const Lds &S,
-                                             const float *gain, int k) {
+                                             const float *gain, int k, const long long *xin,
+                                             long long *xout, int nparts) {
+    constexpr int E = 4;   // elements per thread per batch of loads
     const int ns = (P.Hp + kGemmChunkK - 1) / kGemmChunkK;
+    const int plast = max(nparts - 1, 0);
     for (int it = blockIdx.x; it < P.B * ns; it += P.nwg) {
         const int b = it / ns, c0 = (it % ns) * kGemmChunkK;
         const int c1 = min(P.Hp, c0 + kGemmChunkK);
-        stage_rmsnorm(P.xf + (size_t)b * P.Hp, gain, P.H, P.Hp, P.eps, S.a, S.sm);
+        const long long *xr = xin + (size_t)b * P.Hp;
+        const float *pr = P.xpart + (size_t)b * P.Hp;
+        float ss = 0.f;
+        for (int i0 = threadIdx.x; i0 < P.Hp; i0 += E * kThreads) {
+            // (unconditional loads from in-range addresses, masked when used)
+            long long v[E];
+            float pv[E][kMaxKSlices];
+#pragma unroll
+            for (int e = 0; e < E; ++e) {
+                const int i = min(i0 + e * kThreads, P.Hp - 1);
+                v[e] = (long long)ld_dev_u64(xr + i);
+#pragma unroll
+                for (int q = 0; q < kMaxKSlices; ++q)
+                    pv[e][q] = ld_dev(pr + (size_t)min(q, plast) * P.xpart_stride + i);
+            }
+#pragma unroll
+            for (int e = 0; e < E; ++e) {
+                const int i = i0 + e * kThreads;
+                long long x = v[e];
+#pragma unroll
+                for (int q = 0; q < kMaxKSlices; ++q)
+                    if (q < nparts) x += to_fix(pv[e][q]);
+                if (i < P.Hp) {
+                    const float xv = from_fix(x);
+                    S.a[i] = xv;
+                    ss = fmaf(xv, xv, ss);   // (padding columns hold zero)
+                    if (nparts > 0 && i >= c0 && i < c1)
+                        st_dev_u64(reinterpret_cast<unsigned long long *>(xout + (size_t)b * P.Hp + i),
+                                   (unsigned long long)x);
+                }
+            }
+        }
+        ss = block_sum(ss, S.sm);
+        const float r = 1.0f / sqrtf(ss / (float)P.H + P.eps);
         for (int kk = c0 + 2 * (int)threadIdx.x; kk < c1; kk += 2 * kThreads) {
             unsigned hi, lo;
-            split_bf16x2(S.a[kk], S.a[kk + 1], hi, lo);
+            split_bf16x2(S.a[kk] * r * gain[kk], S.a[kk + 1] * r * gain[kk + 1], hi, lo);
             st_dev_u32(reinterpret_cast<unsigned *>(P.act + (size_t)b * P.Hp + kk), hi);
             st_dev_u32(reinterpret_cast<unsigned *>(P.act_lo + (size_t)b * P.Hp + kk), lo);
         }
@@ -1000,15 +1040,16 @@ __device__ __forceinline__ void stage_bf16_chunk(const uint16_t *src, const uint
     ctl_copy_rows(src, src_lo, ld, k0, min(kGemmChunkK, K - k0), b0, nb, buf);
 }
 
-// Chunk c of the merged attention output of all heads (K = n_heads d), as
-// two bf16 terms, when there are several chunk results per (sequence, KV
-// head): o_h = sum_c w_ch A_ch / sum_c w_ch L_ch, w_ch = exp(M_ch - M_h).
+// Chunk c of the merged attention output in columns col0 .. col0 + width - 1
+// (of n_heads d), as two bf16 terms, when there are several chunk results per
+// (sequence, KV head): o_h = sum_c w_ch A_ch / sum_c w_ch L_ch,
+// w_ch = exp(M_ch - M_h).
 template <int D, int G>
-__device__ __forceinline__ void stage_o_full(const StepParams &P, int c, int b0, int nb,
-                                             uint16_t *buf) {
-    const int C = P.C, A = P.nq * D, k0 = c * kGemmChunkK, kc = min(kGemmChunkK, A - k0);
+__device__ __forceinline__ void stage_o_full(const StepParams &P, int col0, int width, int c,
+                                             int b0, int nb, uint16_t *buf) {
+    const int C = P.C, k0 = c * kGemmChunkK, kc = min(kGemmChunkK, width - k0);
     for (int t = threadIdx.x; t < nb * kc; t += kThreads) {
-        const int b = t / kc, j = k0 + t % kc, h = j / D, g = h / G, hl = h % G, dd = j % D;
+        const int b = t / kc, j = col0 + k0 + t % kc, h = j / D, g = h / G, hl = h % G, dd = j % D;
         const size_t item0 = ((size_t)(b0 + b) * P.nkv + g) * C;
         float M = -INFINITY;
         for (int cc = 0; cc < C; ++cc)
@@ -1020,7 +1061,8 @@ __device__ __forceinline__ void stage_o_full(const StepParams &P, int c, int b0,
             num = fmaf(ld_dev(P.part_o + (item0 + cc) * G * D + hl * D + dd), w, num);
             den = fmaf(ld_dev(P.part_s + ((item0 + cc) * G + hl) * 2 + 1), w, den);
         }
-        split_bf16(num / den, buf[b * kActStride + (j - k0)], buf[kLoOff + b * kActStride + (j - k0)]);
+        const int jl = j - col0 - k0;
+        split_bf16(num / den, buf[b * kActStride + jl], buf[kLoOff + b * kActStride + jl]);
     }
 }
 
@@ -1069,7 +1111,9 @@ __device__ __forceinline__ void phase_qkv(KArg ka, int l, int gwait, int xbar, i
     weight_phase<BAT>(
         P, S, Lb + P.off_qkv, P.Hp / kTileK, g * P.qkv_rg + a0, a1 - a0,
         [&]() { if (gwait >= 0) bar_wait(P, gwait, ti); },
-        [&]() { norm_batched(P, S, gain, xbar); },
+        // (layer 0 reads the embedding; later layers fold the down projection's
+        // partials, x: xf2 -> xf)
+        [&]() { norm_batched(P, S, gain, xbar, l == 0 ? P.xf : P.xf2, P.xf, l == 0 ? 0 : P.KSd); },
         [&](int b) {
             // the RoPE row of this sequence's position rides along (a + 2 Hp)
             stage_rms_deferred(P.xf + (size_t)b * P.Hp, gain, P.H, P.Hp, S.a, S.sm,
@@ -1455,18 +1499,31 @@ __device__ __forceinline__ void phase_oproj(KArg ka, int l, int gwait, int garri
         add_fix(x + r + 1, y1);
     };
     if constexpr (BAT) {
-        // all heads at once (K = n_heads d): one writer per residual element
-        int a0, a1;
-        split_range(P.o_rg, P.nwg, blockIdx.x, a0, a1);
+        // 2-D partition: KSo K slices (the columns of nkv / KSo KV heads
+        // each) x row groups; a workgroup writes its slice's partial sums,
+        // which the next RMSNorm step folds into the residual.  Every wave
+        // gets whole 16-row blocks and the activation staging is one slice.
+        const int KS = P.KSo, RB = P.nwg / KS;
+        const int ks = blockIdx.x / RB, rb = blockIdx.x % RB, ksc = min(ks, KS - 1);
+        const int gps = P.nkv / KS, width = gps * G * D;   // KV heads and columns per slice
+        int a0 = 0, a1 = 0;
+        if (ks < KS) split_range(P.o_rg, RB, rb, a0, a1);
+        const int col0 = ksc * width;
+        float *part = P.xpart + (size_t)ksc * P.xpart_stride;
         weight_phase<true>(
-            P, S, Wo, P.nkv * KTO, a0, a1 - a0,
+            P, S, Wo + (size_t)ksc * gps * P.o_rg * KTO * kTileBytes, gps * KTO, a0, a1 - a0,
             [&]() { if (gwait >= 0) bar_wait(P, gwait, ti); }, [&]() {}, [&](int) {}, P.C == 1,
             [&](int c, int b0, int nb, uint16_t *buf) {
                 if (P.C == 1)
-                    stage_bf16_chunk(P.acto, P.acto_lo, P.nq * D, P.nq * D, c, b0, nb, buf);
-                else stage_o_full<D, G>(P, c, b0, nb, buf);
+                    stage_bf16_chunk(P.acto + col0, P.acto_lo + col0, P.nq * D, width, c, b0, nb,
+                                     buf);
+                else stage_o_full<D, G>(P, col0, width, c, b0, nb, buf);
             },
-            epi, KTO, (size_t)P.o_rg * KTO);
+            [&](int b, int r, float y0, float y1) {
+                st_dev(part + (size_t)b * P.Hp + r, y0);
+                st_dev(part + (size_t)b * P.Hp + r + 1, y1);
+            },
+            KTO, (size_t)P.o_rg * KTO);
     } else {
         const int g = blockIdx.x / P.Sg, part = blockIdx.x % P.Sg;
         if (g < P.nkv) {
@@ -1516,7 +1573,8 @@ __device__ __forceinline__ void phase_gateup(KArg ka, int l, int gwait, int xbar
     weight_phase<BAT>(
         P, S, Lb + P.off_gu, P.Hp / kTileK, first, count,
         [&]() { if (gwait >= 0) bar_wait(P, gwait, ti); },
-        [&]() { norm_batched(P, S, gain, xbar); },
+        // (folds the O projection's partials, x: xf -> xf2)
+        [&]() { norm_batched(P, S, gain, xbar, P.xf, P.xf2, P.KSo); },
         [&](int b) {
             stage_rms_deferred(P.xf + (size_t)b * P.Hp, gain, P.H, P.Hp, S.a, S.sm);
             if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 3);
@@ -1558,16 +1616,28 @@ __device__ __forceinline__ void phase_down(KArg ka, int l, int gwait, int garriv
         add_fix(x + r + 1, y1);
     };
     if constexpr (BAT) {
-        // all FFN columns at once: one writer per residual element
-        int a0, a1;
-        split_range(P.down_rg, P.nwg, blockIdx.x, a0, a1);
+        // 2-D partition: KSd K slices (Sc / KSd FFN column blocks each) x row
+        // groups, partial sums folded by the next RMSNorm step (as for the O
+        // projection)
+        const int KS = P.KSd, RB = P.nwg / KS;
+        const int ks = blockIdx.x / RB, rb = blockIdx.x % RB, ksc = min(ks, KS - 1);
+        const int gps = P.Sc / KS, width = gps * P.KTc * kTileK;
+        int a0 = 0, a1 = 0;
+        if (ks < KS) split_range(P.down_rg, RB, rb, a0, a1);
+        const size_t col0 = (size_t)ksc * width;
+        float *part = P.xpart + (size_t)ksc * P.xpart_stride;
         weight_phase<true>(
-            P, S, Wd, P.Sc * P.KTc, a0, a1 - a0,
-            [&]() { if (gwait >= 0) bar_wait(P, gwait, ti); }, [&]() {}, [&](int) {}, true,
+            P, S, Wd + (size_t)ksc * gps * P.down_rg * P.KTc * kTileBytes, gps * P.KTc, a0,
+            a1 - a0, [&]() { if (gwait >= 0) bar_wait(P, gwait, ti); }, [&]() {}, [&](int) {},
+            true,
             [&](int c, int b0, int nb, uint16_t *buf) {
-                stage_bf16_chunk(P.actm, P.actm_lo, P.Fp, P.Fp, c, b0, nb, buf);
+                stage_bf16_chunk(P.actm + col0, P.actm_lo + col0, P.Fp, width, c, b0, nb, buf);
             },
-            epi, P.KTc, (size_t)P.down_rg * P.KTc);
+            [&](int b, int r, float y0, float y1) {
+                st_dev(part + (size_t)b * P.Hp + r, y0);
+                st_dev(part + (size_t)b * P.Hp + r + 1, y1);
+            },
+            P.KTc, (size_t)P.down_rg * P.KTc);
     } else {
         const int j = blockIdx.x / P.Rc, part = blockIdx.x % P.Rc;
         if (j < P.Sc) {
@@ -1590,6 +1660,12 @@ __device__ __forceinline__ void phase_down(KArg ka, int l, int gwait, int garriv
     if (garrive >= 0) bar_arrive(P, garrive, ti);
 }
 
+// The final residual stream -> hidden_out (fp32).
+__device__ __forceinline__ void copy_hidden(const StepParams &P) {
+    for (int idx = threadIdx.x; idx < P.B * P.H; idx += kThreads)
+        P.hidden_out[idx] = from_fix((long long)ld_dev_u64(P.xf + (size_t)(idx / P.H) * P.Hp + idx % P.H));
+}
+
 // Classifier block (Sec. 2): final RMSNorm + LM head -> fp32 logits.
 template <bool BAT>
 __device__ __forceinline__ void phase_head(KArg ka, int gwait, int xbar, int ti) {
@@ -1601,13 +1677,13 @@ __device__ __forceinline__ void phase_head(KArg ka, int gwait, int xbar, int ti)
         P, S, reinterpret_cast<const uint8_t *>(P.lm_head), P.Hp / kTileK, R.first, R.count,
         [&]() {
             if (gwait >= 0) bar_wait(P, gwait, ti);
-            if (blockIdx.x == 0 && P.hidden_out) {
-                for (int idx = threadIdx.x; idx < P.B * P.H; idx += kThreads)
-                    P.hidden_out[idx] = from_fix((long long)ld_dev_u64(
-                        P.xf + (size_t)(idx / P.H) * P.Hp + idx % P.H));
-            }
+            if (!BAT && blockIdx.x == 0 && P.hidden_out) copy_hidden(P);
         },
-        [&]() { norm_batched(P, S, P.final_norm, xbar); },
+        [&]() {
+            // (folds the last down projection's partials, x: xf2 -> xf)
+            norm_batched(P, S, P.final_norm, xbar, P.xf2, P.xf, P.KSd);
+            if (blockIdx.x == 0 && P.hidden_out) copy_hidden(P);
+        },
         [&](int b) {
             stage_rms_deferred(P.xf + (size_t)b * P.Hp, P.final_norm, P.H, P.Hp, S.a, S.sm);
             if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 3);
