@@ -231,8 +231,10 @@ __device__ __forceinline__ void bar_init(const StepParams &P) {
 
 // Optional timeline: the control wave of every workgroup stamps
 // (s_memrealtime, 100 MHz) the end of phase i of the launch (slot 0), the
-// start and end of phase i's wait for its inputs (slots 1, 2) and, for an
-// attention phase, the moment its last chunk result is published (slot 3).
+// start and end of phase i's wait for its inputs (slots 1, 2) and the moment
+// its inputs are staged (slot 3: the GEMV path's first activation vector in
+// LDS, the batched path's normalised activations written by the whole grid,
+// an attention phase's last chunk result published).
 __device__ __forceinline__ void trace_stamp(const StepParams &P, int i, int what) {
     if (P.trace && i >= 0 && i < P.trace_max)
         P.trace[((size_t)i * P.nwg + blockIdx.x) * 4 + what] = wall_clock64();
@@ -716,11 +718,16 @@ __device__ __forceinline__ GemmLds gemm_lds(char *smem) {
 // (the O projection per KV head, the down projection per FFN column block),
 // gstride tiles apart: k-tile kt of row group r is tile
 // (kt / ktg) gstride + r ktg + kt % ktg.
-template <class Stage, class Epi>
+//
+// pre() runs once, after the first ring of weight loads is issued (so the
+// weight stream overlaps whatever pre() waits for), before anything touches
+// the activation buffers; it runs even when there are no rows.
+template <class Pre, class Stage, class Epi>
 __device__ __forceinline__ void gemm_rows(const uint8_t *__restrict__ W, int KT, int first,
                                           int count, int ktg, size_t gstride, int b0, int nb,
                                           const uint8_t *dummy, const GemmLds &L,
-                                          bool async_stage, Stage &&stage, Epi &&epi) {
+                                          bool async_stage, Pre &&pre, Stage &&stage,
+                                          Epi &&epi) {
     constexpr int U = kGemvDepth;
     constexpr int CT = kGemmChunkK / kTileK;   // k-tiles per chunk
     const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -735,13 +742,10 @@ __device__ __forceinline__ void gemm_rows(const uint8_t *__restrict__ W, int KT,
     const uint8_t *tbase = W + (size_t)lane * 16;
     const uint8_t *zbase = dummy + (size_t)lane * 16;   // 1 KiB of zeros
 
-    // zero the padding sequences of both terms of both activation buffers once
-    const int pad16 = (kGemmBatch - nb) * kActStride / 8;   // 16-byte words per term
-    for (int t = threadIdx.x; t < 4 * pad16; t += kThreads) {
-        uint16_t *buf = L.act[t / (2 * pad16)] + ((t / pad16) & 1) * kLoOff;
-        reinterpret_cast<u32x4 *>(buf + nb * kActStride)[t % pad16] = u32x4{0u, 0u, 0u, 0u};
-    }
-
+    // (padding sequences: their rows of the activation buffers may hold any
+    // finite values; a product's columns are independent, and the outputs of
+    // padding sequences are never stored)
+    if (nblk == 0) pre();
     for (int bg0 = 0; bg0 < nblk; bg0 += slots * kGemmMaxBlk) {
         // my blocks in this group: bg0 + slot + i * slots, i < nbw
         const int left_blk = min(nblk - bg0, slots * kGemmMaxBlk);
@@ -791,6 +795,7 @@ __device__ __forceinline__ void gemm_rows(const uint8_t *__restrict__ W, int KT,
             for (int s = 0; s < U; ++s) buf[s] = load_next();
         }
 
+        if (bg0 == 0) pre();
         f32x4 acc[kGemmMaxBlk][2];
 #pragma unroll
         for (int i = 0; i < kGemmMaxBlk; ++i)
@@ -906,7 +911,8 @@ __device__ __forceinline__ void gemm_rows(const uint8_t *__restrict__ W, int KT,
 // A weight phase runs the GEMV engine for batches below kMfmaBatch and the
 // matrix-core engine otherwise (sequences in groups of kGemmBatch; the
 // weights stream once per group).  In the batched path every input is staged
-// as bf16 chunks: prep() runs once after wait(), stageb(c, b0, nb, buf) fills
+// as bf16 chunks: prep() runs once after wait(), both once the first weight
+// loads are in flight; stageb(c, b0, nb, buf) fills
 // chunk c for sequences b0 .. b0 + nb - 1 (async: the control wave copies it
 // while the compute waves work on the previous chunk).
 template <bool BAT, class Wait, class Prep, class Stage1, class StageB, class Epi>
@@ -919,12 +925,16 @@ __device__ __forceinline__ void weight_phase(const StepParams &P, const Lds &S,
         gemv_phase(W, KT, first, count, 1, P.B, S.a, S.red, P.dummy, wait, stage1, epi);
         return;
     }
-    wait();
-    prep();
     const GemmLds L = gemm_lds(kl_smem);
     for (int b0 = 0; b0 < P.B; b0 += kGemmBatch) {
         const int nb = min(kGemmBatch, P.B - b0);
         gemm_rows(W, KT, first, count, ktg ? ktg : KT, gstride, b0, nb, P.dummy, L, async,
+                  [&]() {   // (first group only: the inputs' wait and the grid-wide prologue)
+                      if (b0 == 0) {
+                          wait();
+                          prep();
+                      }
+                  },
                   [&](int c, uint16_t *buf) { stageb(c, b0, nb, buf); }, epi);
     }
 }
@@ -1113,7 +1123,10 @@ __device__ __forceinline__ void phase_qkv(KArg ka, int l, int gwait, int xbar, i
         [&]() { if (gwait >= 0) bar_wait(P, gwait, ti); },
         // (layer 0 reads the embedding; later layers fold the down projection's
         // partials, x: xf2 -> xf)
-        [&]() { norm_batched(P, S, gain, xbar, l == 0 ? P.xf : P.xf2, P.xf, l == 0 ? 0 : P.KSd); },
+        [&]() {
+            norm_batched(P, S, gain, xbar, l == 0 ? P.xf : P.xf2, P.xf, l == 0 ? 0 : P.KSd);
+            if (is_ctl_lane0()) trace_stamp(P, ti, 3);
+        },
         [&](int b) {
             // the RoPE row of this sequence's position rides along (a + 2 Hp)
             stage_rms_deferred(P.xf + (size_t)b * P.Hp, gain, P.H, P.Hp, S.a, S.sm,
@@ -1574,7 +1587,10 @@ __device__ __forceinline__ void phase_gateup(KArg ka, int l, int gwait, int xbar
         P, S, Lb + P.off_gu, P.Hp / kTileK, first, count,
         [&]() { if (gwait >= 0) bar_wait(P, gwait, ti); },
         // (folds the O projection's partials, x: xf -> xf2)
-        [&]() { norm_batched(P, S, gain, xbar, P.xf, P.xf2, P.KSo); },
+        [&]() {
+            norm_batched(P, S, gain, xbar, P.xf, P.xf2, P.KSo);
+            if (is_ctl_lane0()) trace_stamp(P, ti, 3);
+        },
         [&](int b) {
             stage_rms_deferred(P.xf + (size_t)b * P.Hp, gain, P.H, P.Hp, S.a, S.sm);
             if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 3);
@@ -1682,6 +1698,7 @@ __device__ __forceinline__ void phase_head(KArg ka, int gwait, int xbar, int ti)
         [&]() {
             // (folds the last down projection's partials, x: xf2 -> xf)
             norm_batched(P, S, P.final_norm, xbar, P.xf2, P.xf, P.KSd);
+            if (is_ctl_lane0()) trace_stamp(P, ti, 3);
             if (blockIdx.x == 0 && P.hidden_out) copy_hidden(P);
         },
         [&](int b) {
