@@ -29,8 +29,8 @@ struct kl_state {
     uint8_t *scratch;
     size_t scratch_bytes;
     long long *xf, *xf2;
-    float *q, *m, *part_o, *part_s, *xpart;
-    int KSo, KSd;                     // K slices of the batched O and down projections
+    float *q, *m, *part_o, *part_s, *xpart, *gpart, *ssp;
+    int KSo, KSd, KSg, KSq;           // K slices of the batched O, down, gate/up, q/k/v products
     uint16_t *act, *act_lo, *actm, *actm_lo, *acto, *acto_lo;
     int Sg, Sc, Rc, KTc;
     unsigned long long *bar;
@@ -122,6 +122,22 @@ int largest_divisor_at_most(int n, int cap) {
     return 1;
 }
 
+// K slices of a batched product over n K units of t k-tiles each, for a
+// matrix of nblk 16-row blocks: the fewest slices (a divisor of n, at most
+// kMaxKSlices) whose K range stays resident in LDS and that give every
+// workgroup kWaves blocks or more; failing that, the resident choice with the
+// most blocks per workgroup; if no slice fits in LDS, the most slices (the
+// activations then stream through LDS in chunks).
+int batched_k_slices(int n, int t, int nblk, int nwg) {
+    int best = -1;
+    for (int s = 1; s <= std::min(n, kMaxKSlices); ++s) {
+        if (n % s || (n / s) * t * kTileK > kGemmResidentK) continue;
+        best = s;
+        if ((long long)nblk * s >= (long long)kWaves * nwg) break;
+    }
+    return best > 0 ? best : largest_divisor_at_most(n, kMaxKSlices);
+}
+
 int ffn_column_blocks(int ktf, int nwg) {
     int best = 1;
     for (int s = 1; s <= std::min(32, std::min(ktf, nwg)); ++s)
@@ -191,7 +207,10 @@ StepParams base_params(const kl_state &s) {
     P.lm_head = reinterpret_cast<const uint16_t *>(s.arena + s.off_lm_head);
     P.rope = s.rope;
     P.xf = s.xf; P.xf2 = s.xf2; P.xpart = s.xpart; P.xpart_stride = c.max_batch * s.Hp;
-    P.KSo = s.KSo; P.KSd = s.KSd;
+    P.KSo = s.KSo; P.KSd = s.KSd; P.KSg = s.KSg; P.KSq = s.KSq;
+    P.gpart = s.gpart; P.gpart_stride = c.max_batch * s.gu_rg * kTileRows;
+    P.qpart_stride = c.max_batch * c.n_kv_heads * s.qkv_rg * kTileRows;
+    P.ssp = s.ssp;
     P.q = s.q; P.m = s.m; P.part_o = s.part_o; P.part_s = s.part_s; P.act = s.act;
     P.act_lo = s.act_lo; P.actm = s.actm; P.actm_lo = s.actm_lo; P.acto = s.acto;
     P.acto_lo = s.acto_lo;
@@ -320,14 +339,26 @@ kl_status kl_model_create(const kl_config *cfg, kl_state **out) {
     const size_t off_err = so;  so = align_up(so + 256, 256);
     const size_t off_dummy = so; so = align_up(so + kTileBytes, 256);
     // batched path: the second residual buffer and the K-slice partial sums
-    // of the O and down projections (folded by the next RMSNorm step)
-    S->KSo = largest_divisor_at_most(nkv, kMaxKSlices);
-    S->KSd = largest_divisor_at_most(S->Sc, kMaxKSlices);
+    // of the O and down projections (folded by the next RMSNorm step), of the
+    // gate/up product (folded by the SwiGLU step) and of the q/k/v product
+    // (folded with the RoPE and the KV-cache append)
+    const int qkv_rows = nkv * S->qkv_rg * kTileRows;
+    S->KSo = batched_k_slices(nkv, KTO, S->o_rg / 2, S->nwg);
+    S->KSd = batched_k_slices(S->Sc, S->KTc, S->down_rg / 2, S->nwg);
+    S->KSg = batched_k_slices(KTH, 1, S->gu_rg / 2, S->nwg);
+    S->KSq = batched_k_slices(KTH, 1, qkv_rows / 16, S->nwg);
     const bool batched = B >= kMfmaBatch;
     const size_t off_x2 = so;
     if (batched) so = align_up(so + (size_t)B * S->Hp * 8, 256);
     const size_t off_xp = so;
     if (batched) so = align_up(so + (size_t)std::max(S->KSo, S->KSd) * B * S->Hp * 4, 256);
+    const size_t off_gp = so;
+    if (batched)
+        so = align_up(so + std::max((size_t)S->KSg * B * S->gu_rg * kTileRows,
+                                    (size_t)S->KSq * B * qkv_rows) * 4, 256);
+    const size_t off_ss = so;
+    if (batched)
+        so = align_up(so + (size_t)B * ((S->Hp + kGemmChunkK - 1) / kGemmChunkK) * 4, 256);
     S->scratch_bytes = so;
     TRY(hipMalloc(&S->scratch, S->scratch_bytes));
     TRY(hipMemsetAsync(S->scratch, 0, S->scratch_bytes, s));
@@ -348,6 +379,8 @@ kl_status kl_model_create(const kl_config *cfg, kl_state **out) {
     S->dummy = S->scratch + off_dummy;
     S->xf2 = batched ? reinterpret_cast<long long *>(S->scratch + off_x2) : nullptr;
     S->xpart = batched ? reinterpret_cast<float *>(S->scratch + off_xp) : nullptr;
+    S->gpart = batched ? reinterpret_cast<float *>(S->scratch + off_gp) : nullptr;
+    S->ssp = batched ? reinterpret_cast<float *>(S->scratch + off_ss) : nullptr;
 
     // RoPE table (cos, sin) of pos * theta^(-2i/d), computed in double
     {

@@ -29,10 +29,10 @@ constexpr int kGemmBatch = 32;
 constexpr int kGemmChunkK = 512;
 constexpr int kActStride = kGemmChunkK + 8;   // bf16 per staged activation row (bank spread)
 constexpr int kGemmMaxBlk = 4;            // 16-row blocks per wave per pass over the weights
-constexpr int kMaxKSlices = 8;            // K slices of the batched O and down projections
+constexpr int kMaxKSlices = 16;           // K slices of a batched product (partial sums)
+constexpr int kGemmResidentK = 2 * kGemmChunkK;   // K columns a workgroup keeps resident
 // LDS of the batched path (bytes): two activation chunks of both terms, and
-// per-wave weight re-layout slots (2 KiB; after the chunk loop they hold the
-// partial products of one block)
+// per-wave weight re-layout slots (2 KiB)
 constexpr int kGemmActBytes = kGemmBatch * kActStride * 2;   // one term of one chunk
 constexpr int kGemmLdsBytes = 4 * kGemmActBytes + kWaves * 2048;
 constexpr int kMaxGroup = 8;              // max query heads per KV head
@@ -81,6 +81,14 @@ struct StepParams {
     float *xpart;              // batched path: K-slice partials [ks][max_batch][Hp] (O, down)
     int xpart_stride;          // floats between consecutive K-slice partials
     int KSo, KSd;              // K slices of the batched O and down projections
+    float *gpart;              // batched path: K-slice partials of the gate/up product
+                               // [ks][max_batch][2F rows] and, at other times, of the
+                               // q/k/v product [ks][max_batch][nkv * qkv_rg * 8 rows]
+    int gpart_stride;          // floats between consecutive gate/up K-slice partials
+    int qpart_stride;          // floats between consecutive q/k/v K-slice partials
+    int KSg, KSq;              // K slices of the batched gate/up and q/k/v products
+    float *ssp;                // batched path: sums of squares of the last RMSNorm step's
+                               // rows per kGemmChunkK columns [max_batch][ceil(Hp / chunk)]
     float *q;                  // [max_batch][nq*d] rotated queries
     float *m;                  // [max_batch][Fp] SwiGLU output (padding stays 0)
     float *part_o;             // attention chunk outputs [B*nkv*C][group*d]

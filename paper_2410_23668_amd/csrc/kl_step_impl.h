@@ -253,20 +253,23 @@ __device__ __forceinline__ void drain_all() {
 }
 
 // Arrival on grid barrier k after phase ti.
+// (the phase's end is stamped once every wave of the workgroup is done)
 __device__ __forceinline__ void bar_arrive(const StepParams &P, int k, int ti) {
-    if (is_ctl_lane0()) trace_stamp(P, ti, 0);
     drain_all();
-    if (is_ctl_lane0())
+    if (is_ctl_lane0()) {
+        trace_stamp(P, ti, 0);
         __hip_atomic_fetch_add(bar_counter(P, blockIdx.x % bar_groups(P)), 1ull,
                                __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
 }
 
 // Arrival on a local counter (one add per arriving workgroup) after phase ti.
 __device__ __forceinline__ void local_arrive(const StepParams &P, unsigned *cnt, int ti) {
-    if (is_ctl_lane0()) trace_stamp(P, ti, 0);
     drain_all();
-    if (is_ctl_lane0())
+    if (is_ctl_lane0()) {
+        trace_stamp(P, ti, 0);
         __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
 }
 
 // Spin until *flag_fn() says done; gives up (raising KL_DEVERR_BARRIER) after
@@ -701,7 +704,6 @@ constexpr int kLoOff = kGemmBatch * kActStride;   // elements from a chunk's hi 
 struct GemmLds {
     uint16_t *act[2];   // [2 terms][kGemmBatch][kActStride] bf16
     uint8_t *wslot;     // [kWaves][2048]
-    float *cred;        // [kWaves][16][32], the same memory as wslot (used after the chunk loop)
 };
 
 __device__ __forceinline__ GemmLds gemm_lds(char *smem) {
@@ -709,179 +711,211 @@ __device__ __forceinline__ GemmLds gemm_lds(char *smem) {
     g.act[0] = reinterpret_cast<uint16_t *>(smem);
     g.act[1] = reinterpret_cast<uint16_t *>(smem + 2 * kGemmActBytes);
     g.wslot = reinterpret_cast<uint8_t *>(smem + 4 * kGemmActBytes);
-    g.cred = reinterpret_cast<float *>(g.wslot);
     return g;
 }
 
 //
-// The K extent may be split over several packed matrices of ktg k-tiles each
-// (the O projection per KV head, the down projection per FFN column block),
-// gstride tiles apart: k-tile kt of row group r is tile
-// (kt / ktg) gstride + r ktg + kt % ktg.
+// A workgroup's products cover the row groups first .. first + count - 1 and
+// the K range of W (KT k-tiles).  The K range may span several packed
+// matrices of ktg k-tiles each, gstride tiles apart: k-tile kt of row group
+// r is tile (kt / ktg) gstride + r ktg + kt % ktg.
+//
+// Work split: wave w owns the 16-row blocks w, w + kWaves, ... and takes
+// them in groups of up to kGemmMaxBlk; for each group it runs through the
+// chunks of K, and within a chunk through its blocks, one ring pass (U = 16
+// tile loads: the 8 k-tiles of the chunk x the block's 2 row groups) per
+// block.  Slot s of a pass is always (k-tile s / 2, row group s % 2), so
+// that the consuming code is the same straight-line code for every pass; the
+// loads run ahead through the same sequence across blocks, chunks and
+// groups, and every slot is refilled unconditionally (with the zero tile
+// once the wave's work is exhausted, or for a row group or k-tile past the
+// range), so the compiler keeps the whole ring in flight.
+//
+// Activations: with up to two chunks (1024 columns) the whole K range is
+// staged once and stays resident, and the waves then run without any
+// workgroup barrier; longer K ranges stream through the two chunk buffers
+// (the control wave copies chunk f + 1 while the compute waves work on chunk
+// f; one barrier per chunk, every wave taking part in every chunk's
+// barrier).  stage(c, buf) fills chunk c with the control wave's
+// memory-to-LDS copies (a no-op in the other waves).
+//
+// Each block's products go straight from the accumulators to epi(b, r,
+// y_r, y_r+1), for its row pairs and sequences b < nb.
 //
 // pre() runs once, after the first ring of weight loads is issued (so the
 // weight stream overlaps whatever pre() waits for), before anything touches
 // the activation buffers; it runs even when there are no rows.
-template <class Pre, class Stage, class Epi>
-__device__ __forceinline__ void gemm_rows(const uint8_t *__restrict__ W, int KT, int first,
-                                          int count, int ktg, size_t gstride, int b0, int nb,
-                                          const uint8_t *dummy, const GemmLds &L,
-                                          bool async_stage, Pre &&pre, Stage &&stage,
-                                          Epi &&epi) {
+//
+// Memory-to-LDS copies issued inside the compute loop would make the
+// compiler wait for all outstanding loads before each of the loop's LDS
+// accesses (draining the ring once per pass), so the two modes are separate
+// instances and the streaming copies run in a loop of the control wave's own.
+template <bool resident, class Pre, class Stage, class Epi>
+__device__ __forceinline__ void gemm_rows_mode(const uint8_t *__restrict__ W, int KT, int first,
+                                               int count, int ktg, size_t gstride, int b0,
+                                               int nb, const uint8_t *dummy, const GemmLds &L,
+                                               Pre &&pre, Stage &&stage, Epi &&epi) {
     constexpr int U = kGemvDepth;
     constexpr int CT = kGemmChunkK / kTileK;   // k-tiles per chunk
+    constexpr int MB = kGemmMaxBlk;
+    static_assert(U == 2 * CT, "a ring pass is one chunk of one 16-row block");
     const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
     const bool compute = wid < kWaves;
+    const int nkc = resident ? min((KT + CT - 1) / CT, 2) : (KT + CT - 1) / CT;
     const int nblk = (count + 1) / 2;
-    const int nkc = (KT + CT - 1) / CT;
-    const int ksplit = nblk >= 8 ? 1 : (nblk >= 4 ? 2 : (nblk >= 2 ? 4 : 8));
-    const int slots = kWaves / ksplit;            // blocks worked on at once
-    const int slot = wid / ksplit, kpart = wid % ksplit;
-    uint8_t *ws = L.wslot + (size_t)wid * 2048;
-    const uint8_t *tbase = W + (size_t)lane * 16;
-    const uint8_t *zbase = dummy + (size_t)lane * 16;   // 1 KiB of zeros
+    const int mine = (compute && nblk > wid) ? (nblk - wid + kWaves - 1) / kWaves : 0;
+    const int ngrp = (mine + MB - 1) / MB;
+    const int ngrp_wg = ((nblk + kWaves - 1) / kWaves + MB - 1) / MB;   // wave 0's
+    const int last_rg = first + count;
+    // (LDS addresses are formed from the shared array itself: a pointer taken
+    // out of GemmLds by a run-time index is a generic pointer, and generic
+    // loads would make every wait for an operand a wait for the whole ring)
+    uint8_t *ws = reinterpret_cast<uint8_t *>(kl_smem + 4 * kGemmActBytes + wid * 2048);
+    const int lo16 = lane * 16;
 
-    // (padding sequences: their rows of the activation buffers may hold any
+    // load generator: group gi, chunk gc, block gb of the group, slot gs;
+    // (kg, kr) = (k-tile / ktg, k-tile % ktg) of the next load, and (kg0,
+    // kr0) of the current chunk's first k-tile (wave-uniform scalars,
+    // advanced by selects)
+    int gi = 0, gc = 0, gb = 0, gs = 0, kg = 0, kr = 0, kg0 = 0, kr0 = 0;
+    auto load_next = [&]() {
+        const int blk = wid + kWaves * (MB * gi + gb);
+        const int rg = first + 2 * blk + (gs & 1);
+        const int kt = gc * CT + (gs >> 1);
+        const bool inb = gi < ngrp && rg < last_rg && kt < KT;
+        const size_t tile = (size_t)kg * gstride + (size_t)rg * ktg + kr;
+        const uint8_t *src = inb ? W + tile * kTileBytes : dummy;
+        const u32x4 v = ld_stream_16B(src + lo16);
+        int nkr = kr + (gs & 1), nkg = kg;
+        nkg = nkr == ktg ? nkg + 1 : nkg;
+        nkr = nkr == ktg ? 0 : nkr;
+        const bool pass_end = gs == U - 1;
+        const bool blk_next = pass_end && gb + 1 < min(MB, mine - MB * gi);
+        const bool chunk_end = pass_end && !blk_next;
+        const bool grp_end = chunk_end && gc + 1 >= nkc;
+        gs = pass_end ? 0 : gs + 1;
+        gb = blk_next ? gb + 1 : (chunk_end ? 0 : gb);
+        gc = grp_end ? 0 : (chunk_end ? gc + 1 : gc);
+        gi = grp_end ? gi + 1 : gi;
+        kg = grp_end ? 0 : (blk_next ? kg0 : nkg);
+        kr = grp_end ? 0 : (blk_next ? kr0 : nkr);
+        kg0 = grp_end ? 0 : (chunk_end ? nkg : kg0);
+        kr0 = grp_end ? 0 : (chunk_end ? nkr : kr0);
+        return v;
+    };
+
+    // (padding sequences: their rows of the activation buffers hold copies of
     // finite values; a product's columns are independent, and the outputs of
     // padding sequences are never stored)
-    if (nblk == 0) pre();
-    for (int bg0 = 0; bg0 < nblk; bg0 += slots * kGemmMaxBlk) {
-        // my blocks in this group: bg0 + slot + i * slots, i < nbw
-        const int left_blk = min(nblk - bg0, slots * kGemmMaxBlk);
-        const int nbw = left_blk > slot ? (left_blk - slot + slots - 1) / slots : 0;
-        auto nkw_of = [&](int c) {   // my k-tiles in chunk c
-            const int lim = min(CT, KT - c * CT);
-            return lim > kpart ? (lim - kpart + ksplit - 1) / ksplit : 0;
-        };
-        // items of chunk c: (block i, k-tile q, row group t), padded with
-        // zero-tile items to a multiple of U so that every chunk starts at
-        // ring slot 0 (the slot of an item is then known at compile time)
-        auto items_of = [&](int c) { return compute ? nbw * nkw_of(c) * 2 : 0; };
-        auto padded = [&](int n) { return (n + U - 1) / U * U; };
-        // load generator: chunk gc, item gj of the chunk
-        int gc = 0, gj = 0, gn = items_of(0), gnk = max(1, nkw_of(0));
-        auto load_next = [&]() {
-            const bool real = gc < nkc && gj < gn;
-            int tile = 0;
-            bool inb = false;
-            if (real) {
-                const int t = gj & 1, q = (gj >> 1) % gnk, i = (gj >> 1) / gnk;
-                const int rgl = 2 * (bg0 + slot + i * slots) + t;   // row group in this range
-                const int kt = gc * CT + kpart + q * ksplit;
-                inb = rgl < count;
-                tile = __builtin_amdgcn_readfirstlane(
-                    (int)((kt / ktg) * gstride) + (first + rgl) * ktg + kt % ktg);
-            }
-            const u32x4 v = ld_stream_16B(inb ? tbase + (size_t)tile * kTileBytes : zbase);
-            if (gc < nkc && ++gj >= padded(gn)) {
-                gj = 0;
-                do {   // (chunks without items of this wave take no ring slots)
-                    ++gc;
-                    gn = gc < nkc ? items_of(gc) : 0;
-                    gnk = gc < nkc ? max(1, nkw_of(gc)) : 1;
-                } while (gc < nkc && gn == 0);
-            }
-            return v;
-        };
-        while (gc < nkc && gn == 0) {
-            ++gc;
-            gn = gc < nkc ? items_of(gc) : 0;
-            gnk = gc < nkc ? max(1, nkw_of(gc)) : 1;
-        }
-        u32x4 buf[U];
-        if (compute) {   // (the control wave keeps its load queue empty)
+    u32x4 buf[U];
+    if (compute) {   // (the control wave keeps its load queue empty)
 #pragma unroll
-            for (int s = 0; s < U; ++s) buf[s] = load_next();
+        for (int s = 0; s < U; ++s) buf[s] = load_next();
+    }
+    pre();
+    if (count <= 0) return;
+    __syncthreads();   // (the buffers may still hold the previous sequence group)
+    stage(0, L.act[0]);
+    if (resident && nkc > 1) stage(1, L.act[1]);
+    __syncthreads();
+
+    if constexpr (!resident) {
+        if (!compute) {
+            // chunk f + 1 into buffer (f + 1) % 2 while the compute waves work on chunk f
+            const int total = ngrp_wg * nkc;
+            for (int f = 0; f < total; ++f) {
+                if (f + 1 < total) stage((f + 1) % nkc, L.act[(f + 1) & 1]);
+                __syncthreads();
+            }
+            return;
         }
-
-        if (bg0 == 0) pre();
-        f32x4 acc[kGemmMaxBlk][2];
+    }
+    f32x4 acc[MB][2];
 #pragma unroll
-        for (int i = 0; i < kGemmMaxBlk; ++i)
-            acc[i][0] = acc[i][1] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-        stage(0, L.act[0]);
-        __syncthreads();
-        for (int c = 0; c < nkc; ++c) {
-            const uint16_t *act = L.act[c & 1];
-            if (async_stage && c + 1 < nkc) stage(c + 1, L.act[(c + 1) & 1]);
-            const int n = items_of(c), nkw = nkw_of(c);
-            for (int j0 = 0; j0 < padded(n); j0 += U) {
+    for (int i = 0; i < MB; ++i) acc[i][0] = acc[i][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const int ngl = resident ? ngrp : ngrp_wg;
+    int f = 0;   // chunks consumed (streaming: chunk f sits in buffer f % 2)
+    for (int g = 0; g < ngl; ++g) {
+        const int nbg = min(MB, mine - MB * g);
+        for (int c = 0; c < nkc; ++c, ++f) {
+            const uint16_t *act = reinterpret_cast<const uint16_t *>(
+                kl_smem + ((resident ? c : f) & 1) * (2 * kGemmActBytes));
+#pragma unroll
+            for (int i = 0; i < MB; ++i) {
+                if (i >= nbg) continue;   // (uniform)
 #pragma unroll
                 for (int s = 0; s < U; ++s) {
-                    const int j = j0 + s;
-                    if (j < n) {
-                        // tile of row group (j & 1) of the block -> the wave's slot
-                        *reinterpret_cast<u32x4 *>(ws + (s & 1) * 1024 + lane * 16) = buf[s];
-                        if (s & 1) {
-                            const int i = (j >> 1) / nkw, ktl = kpart + ((j >> 1) % nkw) * ksplit;
+                    // tile (s % 2) of the block -> the wave's slot; the 16-byte
+                    // column c of row r of tile t sits at column c ^ ((r + t) & 7),
+                    // so that both these writes and the operand reads below (16
+                    // rows at a time) are free of LDS bank conflicts
+                    {
+                        const int wr = lane >> 3, wc = lane & 7, tt = s & 1;
+                        *reinterpret_cast<u32x4 *>(
+                            ws + tt * 1024 + (wr * 8 + (wc ^ ((wr + tt) & 7))) * 16) = buf[s];
+                    }
+                    if (s & 1) {
+                        const int ktl = s >> 1;
 #pragma unroll
-                            for (int st = 0; st < 2; ++st) {
-                                const int r16 = lane & 15, ko = 4 * st + (lane >> 4);
-                                const bf16x8 a = *reinterpret_cast<const bf16x8 *>(
-                                    ws + (r16 >> 3) * 1024 + ((r16 & 7) * 8 + ko) * 16);
+                        for (int st = 0; st < 2; ++st) {
+                            const int r16 = lane & 15, ko = 4 * st + (lane >> 4);
+                            const int at = r16 >> 3, ar = r16 & 7;
+                            const bf16x8 a = *reinterpret_cast<const bf16x8 *>(
+                                ws + at * 1024 + (ar * 8 + (ko ^ ((ar + at) & 7))) * 16);
 #pragma unroll
-                                for (int h = 0; h < 2; ++h) {
-                                    const int b = h * 16 + (lane & 15);
-                                    const int k = ktl * kTileK + 32 * st + 8 * (lane >> 4);
-                                    const bf16x8 x = *reinterpret_cast<const bf16x8 *>(
-                                        act + b * kActStride + k);
-                                    const bf16x8 xl = *reinterpret_cast<const bf16x8 *>(
-                                        act + kLoOff + b * kActStride + k);
-#pragma unroll
-                                    for (int ii = 0; ii < kGemmMaxBlk; ++ii)
-                                        if (ii == i) {
-                                            acc[ii][h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                                                a, x, acc[ii][h], 0, 0, 0);
-                                            acc[ii][h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                                                a, xl, acc[ii][h], 0, 0, 0);
-                                        }
-                                }
+                            for (int h = 0; h < 2; ++h) {
+                                const int b = h * 16 + (lane & 15);
+                                const int k = ktl * kTileK + 32 * st + 8 * (lane >> 4);
+                                const bf16x8 x = *reinterpret_cast<const bf16x8 *>(
+                                    act + b * kActStride + k);
+                                const bf16x8 xl = *reinterpret_cast<const bf16x8 *>(
+                                    act + kLoOff + b * kActStride + k);
+                                acc[i][h] =
+                                    __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, x, acc[i][h], 0, 0, 0);
+                                acc[i][h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, xl, acc[i][h],
+                                                                                   0, 0, 0);
                             }
                         }
                     }
                     buf[s] = load_next();
                 }
             }
-            __syncthreads();   // chunk c consumed by every wave; chunk c + 1 staged
-            if (!async_stage && c + 1 < nkc) {
-                stage(c + 1, L.act[(c + 1) & 1]);
-                __syncthreads();
-            }
+            if (!resident) __syncthreads();   // chunk f consumed by every wave; f + 1 staged
         }
-        // partial products of each block -> LDS, summed over the sharing waves
-        for (int i = 0; i < kGemmMaxBlk; ++i) {
-            if (bg0 + i * slots >= nblk) break;   // (uniform)
-            if (compute) {
+        // the group's products: lane l holds rows 4 (l / 16) .. + 3 of the
+        // block for sequence h 16 + l % 16
 #pragma unroll
-                for (int ii = 0; ii < kGemmMaxBlk; ++ii) {
-                    if (ii != i) continue;
+        for (int i = 0; i < MB; ++i) {
+            if (i >= nbg) continue;   // (uniform)
+            const int blk = wid + kWaves * (MB * g + i);
+            const int r4 = 4 * (lane >> 4);
+            const bool rv = first + 2 * blk + (r4 >> 3) < last_rg;
+            const int r = (first + 2 * blk) * kTileRows + r4;
 #pragma unroll
-                    for (int h = 0; h < 2; ++h)
-#pragma unroll
-                        for (int v = 0; v < 4; ++v)
-                            L.cred[(wid * 16 + 4 * (lane >> 4) + v) * 32 + h * 16 + (lane & 15)] =
-                                acc[ii][h][v];
+            for (int h = 0; h < 2; ++h) {
+                const int b = h * 16 + (lane & 15);
+                if (rv && b < nb) {
+                    epi(b0 + b, r, acc[i][h][0], acc[i][h][1]);
+                    epi(b0 + b, r + 2, acc[i][h][2], acc[i][h][3]);
                 }
+                acc[i][h] = f32x4{0.f, 0.f, 0.f, 0.f};
             }
-            __syncthreads();
-            // blocks bg0 + i * slots + s, s < slots; rows in pairs, sequences b < nb
-            for (int t = threadIdx.x; t < slots * 8 * nb; t += kThreads) {
-                const int s = t / (8 * nb), rem = t % (8 * nb), pr = (rem / nb) * 2, b = rem % nb;
-                const int blk = bg0 + i * slots + s;
-                if (blk >= nblk || 2 * blk * kTileRows + pr >= count * kTileRows) continue;
-                float y0 = 0.f, y1 = 0.f;
-                for (int kp = 0; kp < ksplit; ++kp) {
-                    const int w = s * ksplit + kp;
-                    y0 += L.cred[(w * 16 + pr) * 32 + b];
-                    y1 += L.cred[(w * 16 + pr + 1) * 32 + b];
-                }
-                epi(b0 + b, (first + 2 * blk) * kTileRows + pr, y0, y1);
-            }
-            __syncthreads();
         }
     }
+}
+
+template <class Pre, class Stage, class Epi>
+__device__ __forceinline__ void gemm_rows(const uint8_t *__restrict__ W, int KT, int first,
+                                          int count, int ktg, size_t gstride, int b0, int nb,
+                                          const uint8_t *dummy, const GemmLds &L, Pre &&pre,
+                                          Stage &&stage, Epi &&epi) {
+    if (KT <= 2 * (kGemmChunkK / kTileK))
+        gemm_rows_mode<true>(W, KT, first, count, ktg, gstride, b0, nb, dummy, L, pre, stage,
+                             epi);
+    else
+        gemm_rows_mode<false>(W, KT, first, count, ktg, gstride, b0, nb, dummy, L, pre, stage,
+                              epi);
 }
 
 
@@ -912,15 +946,14 @@ __device__ __forceinline__ void gemm_rows(const uint8_t *__restrict__ W, int KT,
 // matrix-core engine otherwise (sequences in groups of kGemmBatch; the
 // weights stream once per group).  In the batched path every input is staged
 // as bf16 chunks: prep() runs once after wait(), both once the first weight
-// loads are in flight; stageb(c, b0, nb, buf) fills
-// chunk c for sequences b0 .. b0 + nb - 1 (async: the control wave copies it
-// while the compute waves work on the previous chunk).
+// loads are in flight; stageb(c, b0, nb, buf) fills chunk c for sequences
+// b0 .. b0 + nb - 1 (the control wave's memory-to-LDS copies).
 template <bool BAT, class Wait, class Prep, class Stage1, class StageB, class Epi>
 __device__ __forceinline__ void weight_phase(const StepParams &P, const Lds &S,
                                              const uint8_t *W, int KT, int first, int count,
                                              Wait &&wait, Prep &&prep, Stage1 &&stage1,
-                                             bool async, StageB &&stageb, Epi &&epi,
-                                             int ktg = 0, size_t gstride = 0) {
+                                             StageB &&stageb, Epi &&epi, int ktg = 0,
+                                             size_t gstride = 0) {
     if constexpr (!BAT) {
         gemv_phase(W, KT, first, count, 1, P.B, S.a, S.red, P.dummy, wait, stage1, epi);
         return;
@@ -928,7 +961,7 @@ __device__ __forceinline__ void weight_phase(const StepParams &P, const Lds &S,
     const GemmLds L = gemm_lds(kl_smem);
     for (int b0 = 0; b0 < P.B; b0 += kGemmBatch) {
         const int nb = min(kGemmBatch, P.B - b0);
-        gemm_rows(W, KT, first, count, ktg ? ktg : KT, gstride, b0, nb, P.dummy, L, async,
+        gemm_rows(W, KT, first, count, ktg ? ktg : KT, gstride, b0, nb, P.dummy, L,
                   [&]() {   // (first group only: the inputs' wait and the grid-wide prologue)
                       if (b0 == 0) {
                           wait();
@@ -939,67 +972,85 @@ __device__ __forceinline__ void weight_phase(const StepParams &P, const Lds &S,
     }
 }
 
-// Batched RMSNorm.  The K-slice partial sums of the last O or down
-// projection (nparts of them) are first folded into the residual,
-// x = x_in + sum_s fix(part_s) (exact integer adds, so the order is
-// immaterial), and this item's slice of x is written to x_out; then
-// act / act_lo = the two bf16 terms of x r gain.  Items (sequence,
-// kGemmChunkK-column slice) are spread over the grid; each reads its
-// sequence's whole row (the norm needs all of it).  Ends with grid barrier
-// k, after which any workgroup may stage any slice.
+// Batched RMSNorm (Sec. 2), deferred scale.  The K-slice partial sums of
+// the last O or down projection (nparts of them) are first folded into the
+// residual, x = x_in + sum_s fix(part_s) (exact integer adds, so the order is
+// immaterial), and x is written to x_out; act / act_lo = the two bf16 terms
+// of x gain, and the row's sum of squares goes to P.ssp per kGemmChunkK
+// columns.  The consumers apply r = 1 / rms(x) to the products (rms_r).
+// Items (sequence, kGemmChunkK-column slice) are spread over the grid, one
+// column per thread.  Ends with grid barrier k.
 __device__ __forceinline__ void norm_batched(const StepParams &P, const Lds &S,
                                              const float *gain, int k, const long long *xin,
                                              long long *xout, int nparts) {
-    constexpr int E = 4;   // elements per thread per batch of loads
+    static_assert(kGemmChunkK <= kThreads, "one column per thread");
     const int ns = (P.Hp + kGemmChunkK - 1) / kGemmChunkK;
     const int plast = max(nparts - 1, 0);
     for (int it = blockIdx.x; it < P.B * ns; it += P.nwg) {
-        const int b = it / ns, c0 = (it % ns) * kGemmChunkK;
-        const int c1 = min(P.Hp, c0 + kGemmChunkK);
-        const long long *xr = xin + (size_t)b * P.Hp;
-        const float *pr = P.xpart + (size_t)b * P.Hp;
+        const int b = it / ns, sl = it % ns;
+        const int i = sl * kGemmChunkK + (int)threadIdx.x;
+        const bool live = (int)threadIdx.x < kGemmChunkK && i < P.Hp;
+        const int ic = min(i, P.Hp - 1);
+        // (unconditional loads from in-range addresses, masked when used)
+        long long x = (long long)ld_dev_u64(xin + (size_t)b * P.Hp + ic);
+        const float *pr = P.xpart + (size_t)b * P.Hp + ic;
+        float pv[kMaxKSlices];
+#pragma unroll
+        for (int q = 0; q < kMaxKSlices; ++q)
+            pv[q] = ld_dev(pr + (size_t)min(q, plast) * P.xpart_stride);
+#pragma unroll
+        for (int q = 0; q < kMaxKSlices; ++q)
+            if (q < nparts) x += to_fix(pv[q]);
         float ss = 0.f;
-        for (int i0 = threadIdx.x; i0 < P.Hp; i0 += E * kThreads) {
-            // (unconditional loads from in-range addresses, masked when used)
-            long long v[E];
-            float pv[E][kMaxKSlices];
-#pragma unroll
-            for (int e = 0; e < E; ++e) {
-                const int i = min(i0 + e * kThreads, P.Hp - 1);
-                v[e] = (long long)ld_dev_u64(xr + i);
-#pragma unroll
-                for (int q = 0; q < kMaxKSlices; ++q)
-                    pv[e][q] = ld_dev(pr + (size_t)min(q, plast) * P.xpart_stride + i);
-            }
-#pragma unroll
-            for (int e = 0; e < E; ++e) {
-                const int i = i0 + e * kThreads;
-                long long x = v[e];
-#pragma unroll
-                for (int q = 0; q < kMaxKSlices; ++q)
-                    if (q < nparts) x += to_fix(pv[e][q]);
-                if (i < P.Hp) {
-                    const float xv = from_fix(x);
-                    S.a[i] = xv;
-                    ss = fmaf(xv, xv, ss);   // (padding columns hold zero)
-                    if (nparts > 0 && i >= c0 && i < c1)
-                        st_dev_u64(reinterpret_cast<unsigned long long *>(xout + (size_t)b * P.Hp + i),
-                                   (unsigned long long)x);
-                }
-            }
+        if (live) {
+            const float xv = from_fix(x);
+            ss = xv * xv;   // (padding columns hold zero)
+            if (nparts > 0)
+                st_dev_u64(reinterpret_cast<unsigned long long *>(xout + (size_t)b * P.Hp + i),
+                           (unsigned long long)x);
+            uint16_t hi, lo;
+            split_bf16(xv * gain[i], hi, lo);
+            st_dev_u16(P.act + (size_t)b * P.Hp + i, hi);
+            st_dev_u16(P.act_lo + (size_t)b * P.Hp + i, lo);
         }
         ss = block_sum(ss, S.sm);
-        const float r = 1.0f / sqrtf(ss / (float)P.H + P.eps);
-        for (int kk = c0 + 2 * (int)threadIdx.x; kk < c1; kk += 2 * kThreads) {
-            unsigned hi, lo;
-            split_bf16x2(S.a[kk] * r * gain[kk], S.a[kk + 1] * r * gain[kk + 1], hi, lo);
-            st_dev_u32(reinterpret_cast<unsigned *>(P.act + (size_t)b * P.Hp + kk), hi);
-            st_dev_u32(reinterpret_cast<unsigned *>(P.act_lo + (size_t)b * P.Hp + kk), lo);
-        }
-        __syncthreads();   // (S.a is restaged by the next item)
+        if (threadIdx.x == 0) st_dev(P.ssp + (size_t)b * ns + sl, ss);
+        __syncthreads();   // (S.sm is reused by the next item)
     }
     bar_arrive(P, k, -1);
     bar_wait(P, k, -1);
+}
+
+// (the steps that apply the scales keep those of sequences below
+// kRScaleTable in LDS, in the area of the GEMV partial sums, which the
+// batched path does not use)
+constexpr int kRScaleTable = kWaves * kRgBatch * kTileRows;
+
+// 1 / rms of sequence b's row normalised by the last batched RMSNorm step
+// (its column-slice sums of squares, added in slice order).
+__device__ __forceinline__ float rms_r(const StepParams &P, int b) {
+    const int ns = (P.Hp + kGemmChunkK - 1) / kGemmChunkK;
+    float ss = 0.f;
+    for (int s0 = 0; s0 < ns; s0 += 16) {
+        float v[16];
+#pragma unroll
+        for (int j = 0; j < 16; ++j) v[j] = ld_dev(P.ssp + (size_t)b * ns + min(s0 + j, ns - 1));
+#pragma unroll
+        for (int j = 0; j < 16; ++j)
+            if (s0 + j < ns) ss += v[j];
+    }
+    return 1.0f / sqrtf(ss / (float)P.H + P.eps);
+}
+
+// The scales rms_r of sequences below kRScaleTable, in LDS (S.red), for
+// the steps that fold a batched product's partials; ends with a workgroup
+// barrier.
+__device__ __forceinline__ void rms_table(const StepParams &P, const Lds &S) {
+    for (int t = threadIdx.x; t < min(P.B, kRScaleTable); t += kThreads) S.red[t] = rms_r(P, t);
+    __syncthreads();
+}
+__device__ __forceinline__ float rms_of(const StepParams &P, const Lds &S, int b) {
+    return b < kRScaleTable ? S.red[b] : rms_r(P, b);
 }
 
 // Chunk c of the normalised activations (control wave: memory-to-LDS copies).
@@ -1050,17 +1101,17 @@ __device__ __forceinline__ void stage_bf16_chunk(const uint16_t *src, const uint
     ctl_copy_rows(src, src_lo, ld, k0, min(kGemmChunkK, K - k0), b0, nb, buf);
 }
 
-// Chunk c of the merged attention output in columns col0 .. col0 + width - 1
-// (of n_heads d), as two bf16 terms, when there are several chunk results per
-// (sequence, KV head): o_h = sum_c w_ch A_ch / sum_c w_ch L_ch,
-// w_ch = exp(M_ch - M_h).
+// Batched path, several attention chunks per (sequence, KV head): the merged
+// attention output o_h = sum_c w_ch A_ch / sum_c w_ch L_ch, w_ch =
+// exp(M_ch - M_h) (Sec. 2 attention, split over the context), as the two
+// bf16 terms the O projection stages; elements spread over the grid.  Ends
+// with grid barrier k.
 template <int D, int G>
-__device__ __forceinline__ void stage_o_full(const StepParams &P, int col0, int width, int c,
-                                             int b0, int nb, uint16_t *buf) {
-    const int C = P.C, k0 = c * kGemmChunkK, kc = min(kGemmChunkK, width - k0);
-    for (int t = threadIdx.x; t < nb * kc; t += kThreads) {
-        const int b = t / kc, j = col0 + k0 + t % kc, h = j / D, g = h / G, hl = h % G, dd = j % D;
-        const size_t item0 = ((size_t)(b0 + b) * P.nkv + g) * C;
+__device__ __forceinline__ void merge_batched(const StepParams &P, int k) {
+    const int C = P.C, n = P.nq * D, total = P.B * n;
+    for (int e = blockIdx.x * kThreads + threadIdx.x; e < total; e += P.nwg * kThreads) {
+        const int b = e / n, j = e % n, h = j / D, g = h / G, hl = h % G, dd = j % D;
+        const size_t item0 = ((size_t)b * P.nkv + g) * C;
         float M = -INFINITY;
         for (int cc = 0; cc < C; ++cc)
             M = fmaxf(M, ld_dev(P.part_s + ((item0 + cc) * G + hl) * 2));
@@ -1071,9 +1122,13 @@ __device__ __forceinline__ void stage_o_full(const StepParams &P, int col0, int 
             num = fmaf(ld_dev(P.part_o + (item0 + cc) * G * D + hl * D + dd), w, num);
             den = fmaf(ld_dev(P.part_s + ((item0 + cc) * G + hl) * 2 + 1), w, den);
         }
-        const int jl = j - col0 - k0;
-        split_bf16(num / den, buf[b * kActStride + jl], buf[kLoOff + b * kActStride + jl]);
+        uint16_t hi, lo;
+        split_bf16(num / den, hi, lo);
+        st_dev_u16(P.acto + (size_t)b * n + j, hi);
+        st_dev_u16(P.acto_lo + (size_t)b * n + j, lo);
     }
+    bar_arrive(P, k, -1);
+    bar_wait(P, k, -1);
 }
 
 // Embedding block (Sec. 2): x = E[token] (exact in fixed point).  Workgroup 0
@@ -1102,31 +1157,124 @@ __device__ __forceinline__ void phase_embed(KArg ka, int gwait, int garrive, int
     if (garrive >= 0) bar_arrive(P, garrive, ti);
 }
 
+// One rotation pair (rows lr, lr + 1 of KV head g's block, lr even) of the
+// q/k/v projection of sequence b: RoPE (Sec. 2) on query and key rows with
+// cs = (cos, sin) of the pair's angle at the sequence's position, then the
+// query to q, the key and value to the KV cache at that position.
+template <class Rope>
+__device__ __forceinline__ void qkv_store(const StepParams &P, int l, int b, int g, int lr,
+                                          float y0, float y1, Rope &&rope) {
+    const int d = P.d, half = P.d / 2, G = P.group;
+    const int p = eff_pos(P, b);
+    if (lr < (G + 1) * d) {
+        const int i = (lr % d) >> 1;
+        const float2 cs = rope(p, i);
+        const float u0 = y0 * cs.x - y1 * cs.y;
+        const float u1 = y0 * cs.y + y1 * cs.x;
+        if (lr < G * d) {
+            float *qq = P.q + (size_t)b * P.nq * d + (size_t)(g * G + lr / d) * d;
+            st_dev(qq + i, u0);
+            st_dev(qq + i + half, u1);
+        } else {
+            uint16_t *kk = P.kc + (kv_row(P, l, b, g) + p) * d;
+            st_dev_u16(kk + i, f2bf(u0));
+            st_dev_u16(kk + i + half, f2bf(u1));
+        }
+    } else {
+        const int j = lr - (G + 1) * d;
+        uint16_t *vv = P.vc + (kv_row(P, l, b, g) + p) * d;
+        st_dev_u32(reinterpret_cast<unsigned *>(vv + j),
+                   (unsigned)f2bf(y0) | ((unsigned)f2bf(y1) << 16));
+    }
+}
+
+// Batched path: KV head g's q/k/v rows from the K-slice partials (sums in
+// slice order), through qkv_store, by head g's workgroups (part of Sg).
+__device__ __forceinline__ void fold_qkv(const StepParams &P, const Lds &S, int l, int g,
+                                         int part) {
+    const int hrows = P.qkv_rg * kTileRows, rows = P.nkv * hrows, KS = P.KSq;
+    rms_table(P, S);
+    const int npair = hrows / 2, total = P.B * npair, half = P.d / 2;
+    for (int e = part * kThreads + threadIdx.x; e < total; e += P.Sg * kThreads) {
+        const int b = e / npair, lr = 2 * (e % npair);
+        const float *src = P.gpart + (size_t)b * rows + g * hrows + lr;
+        float y0 = 0.f, y1 = 0.f;
+        for (int q0 = 0; q0 < KS; q0 += 4) {
+            // (unconditional loads from in-range addresses, masked when used)
+            unsigned long long v[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                v[j] = ld_dev_u64(src + (size_t)min(q0 + j, KS - 1) * P.qpart_stride);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                if (q0 + j < KS) {
+                    y0 += __uint_as_float((unsigned)v[j]);
+                    y1 += __uint_as_float((unsigned)(v[j] >> 32));
+                }
+            }
+        }
+        const float r = rms_of(P, S, b);   // the deferred RMSNorm scale
+        qkv_store(P, l, b, g, lr, y0 * r, y1 * r,
+                  [&](int p, int i) { return P.rope[(size_t)p * half + i]; });
+    }
+}
+
 // RMSNorm + Q/K/V projection of KV head g + RoPE + KV-cache append.  The rows
 // of head g's block are: its G query heads, then its key, then its value
 // head; query and key rows are packed in rotation pairs (dims i, i + d/2).
+// Batched path: a 2-D partition (KSq K slices x row groups of all heads)
+// writes K-slice partials; after grid barrier qbar head g's workgroups fold
+// them (fold_qkv).
 template <bool BAT>
-__device__ __forceinline__ void phase_qkv(KArg ka, int l, int gwait, int xbar, int ti) {
+__device__ __forceinline__ void phase_qkv(KArg ka, int l, int gwait, int xbar, int qbar,
+                                          int ti) {
     const StepParams P = load_params(ka);
     const Lds S = lds_layout(kl_smem, P);
     const int g = blockIdx.x / P.Sg, part = blockIdx.x % P.Sg;
     const bool member = g < P.nkv;
-    int a0 = 0, a1 = 0;
-    if (member) split_range(P.qkv_rg, P.Sg, part, a0, a1);
     const uint8_t *Lb = P.arena + (size_t)l * P.layer_stride;
     const float *gain = reinterpret_cast<const float *>(Lb + P.off_attn_norm);
-    const int d = P.d, half = P.d / 2, G = P.group;
+    const int half = P.d / 2;
+    if constexpr (BAT) {
+        const int KS = P.KSq, RB = P.nwg / KS, KT = P.Hp / kTileK, KTs = KT / KS;
+        const int ks = blockIdx.x / RB, rb = blockIdx.x % RB, ksc = min(ks, KS - 1);
+        const int nrg = P.nkv * P.qkv_rg, rows = nrg * kTileRows;
+        int a0 = 0, a1 = 0;
+        if (ks < KS) split_range(nrg, RB, rb, a0, a1);
+        const int col0 = ksc * KTs * kTileK;
+        float *pp = P.gpart + (size_t)ksc * P.qpart_stride;
+        weight_phase<true>(
+            P, S, Lb + P.off_qkv + (size_t)ksc * KTs * kTileBytes, KTs, a0, a1 - a0,
+            [&]() { if (gwait >= 0) bar_wait(P, gwait, ti); },
+            // (layer 0 reads the embedding; later layers fold the down
+            // projection's partials, x: xf2 -> xf)
+            [&]() {
+                norm_batched(P, S, gain, xbar, l == 0 ? P.xf : P.xf2, P.xf, l == 0 ? 0 : P.KSd);
+                if (is_ctl_lane0()) trace_stamp(P, ti, 3);
+            },
+            [&](int) {},
+            [&](int c, int b0, int nb, uint16_t *buf) {
+                stage_bf16_chunk(P.act + col0, P.act_lo + col0, P.Hp, KTs * kTileK, c, b0, nb, buf);
+            },
+            [&](int b, int r, float y0, float y1) {
+                st_dev(pp + (size_t)b * rows + r, y0);
+                st_dev(pp + (size_t)b * rows + r + 1, y1);
+            },
+            KT, 0);
+        bar_arrive(P, qbar, -1);
+        bar_wait(P, qbar, -1);
+        if (member) {
+            fold_qkv(P, S, l, g, part);
+            local_arrive(P, P.cnt + g, ti);
+        }
+        return;
+    }
+    int a0 = 0, a1 = 0;
+    if (member) split_range(P.qkv_rg, P.Sg, part, a0, a1);
     const int row0 = g * P.qkv_rg * kTileRows;   // first packed row of head g's block
-    constexpr bool batched = BAT;
-    weight_phase<BAT>(
+    weight_phase<false>(
         P, S, Lb + P.off_qkv, P.Hp / kTileK, g * P.qkv_rg + a0, a1 - a0,
-        [&]() { if (gwait >= 0) bar_wait(P, gwait, ti); },
-        // (layer 0 reads the embedding; later layers fold the down projection's
-        // partials, x: xf2 -> xf)
-        [&]() {
-            norm_batched(P, S, gain, xbar, l == 0 ? P.xf : P.xf2, P.xf, l == 0 ? 0 : P.KSd);
-            if (is_ctl_lane0()) trace_stamp(P, ti, 3);
-        },
+        [&]() { if (gwait >= 0) bar_wait(P, gwait, ti); }, [&]() {},
         [&](int b) {
             // the RoPE row of this sequence's position rides along (a + 2 Hp)
             stage_rms_deferred(P.xf + (size_t)b * P.Hp, gain, P.H, P.Hp, S.a, S.sm,
@@ -1134,36 +1282,12 @@ __device__ __forceinline__ void phase_qkv(KArg ka, int l, int gwait, int xbar, i
                                S.a + 2 * P.Hp, 2 * half);
             if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 3);
         },
-        true, [&](int c, int b0, int nb, uint16_t *buf) { stage_act_chunk(P, c, b0, nb, buf); },
+        [&](int, int, int, uint16_t *) {},
         [&](int b, int r, float y0, float y1) {
-            if (!batched) {   // the deferred RMSNorm scale
-                const float rs = rms_scale(S.sm, P.H, P.eps);
-                y0 *= rs;
-                y1 *= rs;
-            }
-            const int p = eff_pos(P, b);
-            const int lr = r - row0;
-            if (lr < (G + 1) * d) {
-                const int i = (lr % d) >> 1;
-                const float2 cs = batched ? P.rope[(size_t)p * half + i]
-                                          : reinterpret_cast<const float2 *>(S.a + 2 * P.Hp)[i];
-                const float u0 = y0 * cs.x - y1 * cs.y;
-                const float u1 = y0 * cs.y + y1 * cs.x;
-                if (lr < G * d) {
-                    float *qq = P.q + (size_t)b * P.nq * d + (size_t)(g * G + lr / d) * d;
-                    st_dev(qq + i, u0);
-                    st_dev(qq + i + half, u1);
-                } else {
-                    uint16_t *kk = P.kc + (kv_row(P, l, b, g) + p) * d;
-                    st_dev_u16(kk + i, f2bf(u0));
-                    st_dev_u16(kk + i + half, f2bf(u1));
-                }
-            } else {
-                const int j = lr - (G + 1) * d;
-                uint16_t *vv = P.vc + (kv_row(P, l, b, g) + p) * d;
-                st_dev_u32(reinterpret_cast<unsigned *>(vv + j),
-                           (unsigned)f2bf(y0) | ((unsigned)f2bf(y1) << 16));
-            }
+            const float rs = rms_scale(S.sm, P.H, P.eps);   // the deferred RMSNorm scale
+            qkv_store(P, l, b, g, r - row0, y0 * rs, y1 * rs, [&](int, int i) {
+                return reinterpret_cast<const float2 *>(S.a + 2 * P.Hp)[i];
+            });
         });
     if (member) local_arrive(P, P.cnt + g, ti);
 }
@@ -1501,7 +1625,8 @@ __device__ __forceinline__ void phase_attn(KArg ka, int l, int garrive, int ti) 
 // residual.  GEMV path: the staged input is head g's merged attention output,
 // published by the attention phase.
 template <int D, int G, bool BAT>
-__device__ __forceinline__ void phase_oproj(KArg ka, int l, int gwait, int garrive, int ti) {
+__device__ __forceinline__ void phase_oproj(KArg ka, int l, int gwait, int mbar, int garrive,
+                                            int ti) {
     const StepParams P = load_params(ka);
     const Lds S = lds_layout(kl_smem, P);
     const int KTO = G * D / kTileK;
@@ -1525,12 +1650,10 @@ __device__ __forceinline__ void phase_oproj(KArg ka, int l, int gwait, int garri
         float *part = P.xpart + (size_t)ksc * P.xpart_stride;
         weight_phase<true>(
             P, S, Wo + (size_t)ksc * gps * P.o_rg * KTO * kTileBytes, gps * KTO, a0, a1 - a0,
-            [&]() { if (gwait >= 0) bar_wait(P, gwait, ti); }, [&]() {}, [&](int) {}, P.C == 1,
+            [&]() { if (gwait >= 0) bar_wait(P, gwait, ti); },
+            [&]() { if (mbar >= 0) merge_batched<D, G>(P, mbar); }, [&](int) {},
             [&](int c, int b0, int nb, uint16_t *buf) {
-                if (P.C == 1)
-                    stage_bf16_chunk(P.acto + col0, P.acto_lo + col0, P.nq * D, width, c, b0, nb,
-                                     buf);
-                else stage_o_full<D, G>(P, col0, width, c, b0, nb, buf);
+                stage_bf16_chunk(P.acto + col0, P.acto_lo + col0, P.nq * D, width, c, b0, nb, buf);
             },
             [&](int b, int r, float y0, float y1) {
                 st_dev(part + (size_t)b * P.Hp + r, y0);
@@ -1556,7 +1679,7 @@ __device__ __forceinline__ void phase_oproj(KArg ka, int l, int gwait, int garri
                         merge_chunks<D, G>(P, b, g, S.a, S.a + G * D);
                     if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 3);
                 },
-                false, [&](int, int, int, uint16_t *) {}, epi);
+                [&](int, int, int, uint16_t *) {}, epi);
         }
     }
     if (garrive >= 0) bar_arrive(P, garrive, ti);
@@ -1569,6 +1692,41 @@ __device__ __forceinline__ void phase_gateup(KArg ka, int l, int gwait, int xbar
                                              int ti) {
     const StepParams P = load_params(ka);
     const Lds S = lds_layout(kl_smem, P);
+    const uint8_t *Lb = P.arena + (size_t)l * P.layer_stride;
+    const float *gain = reinterpret_cast<const float *>(Lb + P.off_ffn_norm);
+    if constexpr (BAT) {
+        // 2-D partition: KSg K slices (of Hp / KSg columns, one chunk or a
+        // few) x row groups, so a workgroup's load ring streams through all
+        // of its blocks within few chunks; the gate and up partial sums go
+        // to the slice's partial buffer, and the SwiGLU is applied when the
+        // down phase folds them (fold_swiglu)
+        const int KS = P.KSg, RB = P.nwg / KS, KT = P.Hp / kTileK, KTs = KT / KS;
+        const int ks = blockIdx.x / RB, rb = blockIdx.x % RB, ksc = min(ks, KS - 1);
+        int a0 = 0, a1 = 0;
+        if (ks < KS) split_range(P.gu_rg, RB, rb, a0, a1);
+        const int col0 = ksc * KTs * kTileK;
+        float *part = P.gpart + (size_t)ksc * P.gpart_stride;
+        const int grow = P.gu_rg * kTileRows;
+        weight_phase<true>(
+            P, S, Lb + P.off_gu + (size_t)ksc * KTs * kTileBytes, KTs, a0, a1 - a0,
+            [&]() { if (gwait >= 0) bar_wait(P, gwait, ti); },
+            // (folds the O projection's partials, x: xf -> xf2)
+            [&]() {
+                norm_batched(P, S, gain, xbar, P.xf, P.xf2, P.KSo);
+                if (is_ctl_lane0()) trace_stamp(P, ti, 3);
+            },
+            [&](int) {},
+            [&](int c, int b0, int nb, uint16_t *buf) {
+                stage_bf16_chunk(P.act + col0, P.act_lo + col0, P.Hp, KTs * kTileK, c, b0, nb, buf);
+            },
+            [&](int b, int r, float gt, float up) {
+                st_dev(part + (size_t)b * grow + r, gt);
+                st_dev(part + (size_t)b * grow + r + 1, up);
+            },
+            KT, 0);
+        if (garrive >= 0) bar_arrive(P, garrive, ti);
+        return;
+    }
     const int j = blockIdx.x / P.Rc, part = blockIdx.x % P.Rc;
     const bool member = j < P.Sc;
     int first = 0, count = 0;
@@ -1581,48 +1739,69 @@ __device__ __forceinline__ void phase_gateup(KArg ka, int l, int gwait, int xbar
         first = r0 + a0;
         count = a1 - a0;
     }
-    const uint8_t *Lb = P.arena + (size_t)l * P.layer_stride;
-    const float *gain = reinterpret_cast<const float *>(Lb + P.off_ffn_norm);
-    weight_phase<BAT>(
+    weight_phase<false>(
         P, S, Lb + P.off_gu, P.Hp / kTileK, first, count,
-        [&]() { if (gwait >= 0) bar_wait(P, gwait, ti); },
-        // (folds the O projection's partials, x: xf -> xf2)
-        [&]() {
-            norm_batched(P, S, gain, xbar, P.xf, P.xf2, P.KSo);
-            if (is_ctl_lane0()) trace_stamp(P, ti, 3);
-        },
+        [&]() { if (gwait >= 0) bar_wait(P, gwait, ti); }, [&]() {},
         [&](int b) {
             stage_rms_deferred(P.xf + (size_t)b * P.Hp, gain, P.H, P.Hp, S.a, S.sm);
             if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 3);
         },
-        true, [&](int c, int b0, int nb, uint16_t *buf) { stage_act_chunk(P, c, b0, nb, buf); },
+        [&](int, int, int, uint16_t *) {},
         [&](int b, int r, float gt, float up) {
-            if constexpr (!BAT) {   // the deferred RMSNorm scale
-                const float rs = rms_scale(S.sm, P.H, P.eps);
-                gt *= rs;
-                up *= rs;
-            }
-            const float mv = gt / (1.0f + expf(-gt)) * up;
-            if constexpr (BAT) {
-                uint16_t hi, lo;
-                split_bf16(mv, hi, lo);
-                st_dev_u16(P.actm + (size_t)b * P.Fp + (r >> 1), hi);
-                st_dev_u16(P.actm_lo + (size_t)b * P.Fp + (r >> 1), lo);
-            } else {
-                st_dev(P.m + (size_t)b * P.Fp + (r >> 1), mv);
-            }
+            const float rs = rms_scale(S.sm, P.H, P.eps);   // the deferred RMSNorm scale
+            gt *= rs;
+            up *= rs;
+            st_dev(P.m + (size_t)b * P.Fp + (r >> 1), gt / (1.0f + expf(-gt)) * up);
         });
-    if constexpr (BAT) {
-        if (garrive >= 0) bar_arrive(P, garrive, ti);
-    } else {
-        if (member) local_arrive(P, P.cnt + 2 * P.nkv + j, ti);
+    if (member) local_arrive(P, P.cnt + 2 * P.nkv + j, ti);
+}
+
+// Batched path: the SwiGLU of the gate/up K-slice partials, m = silu(g) u with
+// g, u the fixed-order sums over the slices, as the two bf16 terms the down
+// projection stages; the (sequence, FFN column) elements are spread over the
+// grid.  Ends with grid barrier k.
+__device__ __forceinline__ void fold_swiglu(const StepParams &P, const Lds &S, int k) {
+    const int F = P.F, grow = P.gu_rg * kTileRows, KS = P.KSg;
+    rms_table(P, S);
+    const int total = P.B * F;
+    for (int e = blockIdx.x * kThreads + threadIdx.x; e - (int)threadIdx.x < total;
+         e += P.nwg * kThreads) {
+        const int ec = min(e, total - 1), b = ec / F, f = ec % F;
+        const float *src = P.gpart + (size_t)b * grow + 2 * f;
+        float gs = 0.f, us = 0.f;
+        for (int q0 = 0; q0 < KS; q0 += 4) {
+            // (unconditional loads from in-range addresses, masked when used)
+            unsigned long long v[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                v[j] = ld_dev_u64(src + (size_t)min(q0 + j, KS - 1) * P.gpart_stride);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                if (q0 + j < KS) {
+                    gs += __uint_as_float((unsigned)v[j]);
+                    us += __uint_as_float((unsigned)(v[j] >> 32));
+                }
+            }
+        }
+        const float r = rms_of(P, S, b);   // the deferred RMSNorm scale
+        gs *= r;
+        us *= r;
+        if (e < total) {
+            uint16_t hi, lo;
+            split_bf16(gs / (1.0f + expf(-gs)) * us, hi, lo);
+            st_dev_u16(P.actm + (size_t)b * P.Fp + f, hi);
+            st_dev_u16(P.actm_lo + (size_t)b * P.Fp + f, lo);
+        }
     }
+    bar_arrive(P, k, -1);
+    bar_wait(P, k, -1);
 }
 
 // Down projection of FFN column block j: x += Wd[:, block j] m[block j], for
 // the rows this workgroup owns among block j's workgroups.
 template <bool BAT>
-__device__ __forceinline__ void phase_down(KArg ka, int l, int gwait, int garrive, int ti) {
+__device__ __forceinline__ void phase_down(KArg ka, int l, int gwait, int xbar, int garrive,
+                                           int ti) {
     const StepParams P = load_params(ka);
     const Lds S = lds_layout(kl_smem, P);
     const uint8_t *Wd = P.arena + (size_t)l * P.layer_stride + P.off_down;
@@ -1644,8 +1823,12 @@ __device__ __forceinline__ void phase_down(KArg ka, int l, int gwait, int garriv
         float *part = P.xpart + (size_t)ksc * P.xpart_stride;
         weight_phase<true>(
             P, S, Wd + (size_t)ksc * gps * P.down_rg * P.KTc * kTileBytes, gps * P.KTc, a0,
-            a1 - a0, [&]() { if (gwait >= 0) bar_wait(P, gwait, ti); }, [&]() {}, [&](int) {},
-            true,
+            a1 - a0, [&]() { if (gwait >= 0) bar_wait(P, gwait, ti); },
+            [&]() {
+                fold_swiglu(P, S, xbar);
+                if (is_ctl_lane0()) trace_stamp(P, ti, 3);
+            },
+            [&](int) {},
             [&](int c, int b0, int nb, uint16_t *buf) {
                 stage_bf16_chunk(P.actm + col0, P.actm_lo + col0, P.Fp, width, c, b0, nb, buf);
             },
@@ -1670,7 +1853,7 @@ __device__ __forceinline__ void phase_down(KArg ka, int l, int gwait, int garriv
                     stage_vec(P.m + (size_t)b * P.Fp + (size_t)j * kw, kw, kw, S.a);
                     if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 3);
                 },
-                false, [&](int, int, int, uint16_t *) {}, epi);
+                [&](int, int, int, uint16_t *) {}, epi);
         }
     }
     if (garrive >= 0) bar_arrive(P, garrive, ti);
@@ -1696,8 +1879,10 @@ __device__ __forceinline__ void phase_head(KArg ka, int gwait, int xbar, int ti)
             if (!BAT && blockIdx.x == 0 && P.hidden_out) copy_hidden(P);
         },
         [&]() {
-            // (folds the last down projection's partials, x: xf2 -> xf)
+            // (folds the last down projection's partials, x: xf2 -> xf), and
+            // the sequences' RMSNorm scales for the epilogue
             norm_batched(P, S, P.final_norm, xbar, P.xf2, P.xf, P.KSd);
+            rms_table(P, S);
             if (is_ctl_lane0()) trace_stamp(P, ti, 3);
             if (blockIdx.x == 0 && P.hidden_out) copy_hidden(P);
         },
@@ -1705,13 +1890,12 @@ __device__ __forceinline__ void phase_head(KArg ka, int gwait, int xbar, int ti)
             stage_rms_deferred(P.xf + (size_t)b * P.Hp, P.final_norm, P.H, P.Hp, S.a, S.sm);
             if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 3);
         },
-        true, [&](int c, int b0, int nb, uint16_t *buf) { stage_act_chunk(P, c, b0, nb, buf); },
+        [&](int c, int b0, int nb, uint16_t *buf) { stage_act_chunk(P, c, b0, nb, buf); },
         [&](int b, int r, float y0, float y1) {
-            if constexpr (!BAT) {   // the deferred RMSNorm scale
-                const float rs = rms_scale(S.sm, P.H, P.eps);
-                y0 *= rs;
-                y1 *= rs;
-            }
+            // the deferred RMSNorm scale
+            const float rs = !BAT ? rms_scale(S.sm, P.H, P.eps) : rms_of(P, S, b);
+            y0 *= rs;
+            y1 *= rs;
             float *lg = P.logits + (size_t)b * V;
             if (r < V) lg[r] = y0;
             if (r + 1 < V) lg[r + 1] = y1;
@@ -1749,21 +1933,25 @@ __global__ __launch_bounds__(kThreads) void kl_step_kernel(StepParams P, int l0,
         // batched steps: attn -> oproj and gateup -> down are grid barriers
         // too (full-K products with one writer per output)
         if (phases & kPhQkv) {
-            const int w = gw(), x = xb();
-            phase_qkv<BAT>(ka, l, w, x, ti++);
+            const int w = gw(), x = xb(), q = xb();
+            phase_qkv<BAT>(ka, l, w, x, q, ti++);
         }
         if (phases & kPhAttn) phase_attn<D, G, BAT>(ka, l, BAT ? ga(has_op) : -1, ti++);
         if (phases & kPhOproj) {
-            const int w = BAT && has_attn ? gw() : -1, a = ga(has_gu);
-            phase_oproj<D, G, BAT>(ka, l, w, a, ti++);
+            // (batched, several attention chunks: the merge step's own barrier)
+            const int w = BAT && has_attn ? gw() : -1;
+            const int m = BAT && load_params(ka).C > 1 ? na++ : -1, a = ga(has_gu);
+            phase_oproj<D, G, BAT>(ka, l, w, m, a, ti++);
         }
         if (phases & kPhGateUp) {
             const int w = gw(), x = xb(), a = BAT ? ga(has_down) : -1;
             phase_gateup<BAT>(ka, l, w, x, a, ti++);
         }
         if (phases & kPhDown) {
-            const int w = BAT && has_gu ? gw() : -1;
-            phase_down<BAT>(ka, l, w, ga((has_qkv && l + 1 < l1) || has_head), ti++);
+            // (batched: the SwiGLU fold of the gate/up partials ends with a
+            // grid barrier of its own)
+            const int w = BAT && has_gu ? gw() : -1, x = xb();
+            phase_down<BAT>(ka, l, w, x, ga((has_qkv && l + 1 < l1) || has_head), ti++);
         }
     }
     if (has_head) {
