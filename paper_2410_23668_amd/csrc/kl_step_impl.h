@@ -29,6 +29,8 @@
 
 #pragma once
 
+#include <type_traits>
+
 #include "kl_internal.h"
 #include "kl.h"
 
@@ -1359,12 +1361,14 @@ __device__ __forceinline__ void merge_chunks(const StepParams &P, int b, int g, 
 // of (b, g) to finish merges all chunks in chunk order and writes o.  The
 // first sub-chunk's K/V vectors are loaded before the barrier wait, except
 // the new slot, which the QKV phase writes and which is read after the wait
-// with device-coherent loads.  Loads are unconditional (spare ones target a
+// with device-coherent loads (into registers of its own).  Loads are unconditional (spare ones target a
 // shared 16-byte line) and masked when consumed.
 template <int D>
 constexpr int attn_sub() { return kWaves * kAttnLoads * (64 / (D / 8)); }
 
-template <int D, int G, bool LAST>
+// PEEL (batched path, up to 4 query heads per KV head, where the chunks are
+// long): the last sub-chunk is a copy of its own, see below.
+template <int D, int G, bool LAST, bool PEEL>
 __device__ __forceinline__ void attn_item(KArg ka, int l, int b, int g, int c, bool first,
                                           int ti) {
     const StepParams P = load_params(ka);
@@ -1398,7 +1402,6 @@ __device__ __forceinline__ void attn_item(KArg ka, int l, int b, int g, int c, b
     // the scores have used this one's, and its V once the values have (the
     // loop is software-pipelined over sub-chunks)
     auto issue_one = [&](u32x4 *r, const uint16_t *base, int js, int len) {
-        if (!compute) return;   // the control wave keeps its load queue empty for the barrier
 #pragma unroll
         for (int t = 0; t < NG; ++t) {
             const int jl = jloc(t), pos = js + jl;
@@ -1406,20 +1409,24 @@ __device__ __forceinline__ void attn_item(KArg ka, int l, int b, int g, int c, b
             r[t] = ld_stream_16B(real ? (const void *)(base + (size_t)pos * D + ds) : P.dummy);
         }
     };
-    // the new slot (written during this step by another workgroup) is read
-    // with device-coherent loads, after the wait
-    auto fetch_new = [&](u32x4 *r, const uint16_t *base, int js, int len) {
-        if (compute && pnew >= js && pnew < js + len) {
-#pragma unroll
-            for (int t = 0; t < NG; ++t)
-                if (js + jloc(t) == pnew) r[t] = ld_dev_16B(base + (size_t)pnew * D + ds);
-        }
-    };
-    issue_one(kr, Kb, j0, min(SUB, j1 - j0));
-    issue_one(vr, Vb, j0, min(SUB, j1 - j0));
+    if (compute) {   // (the control wave keeps its load queue empty for the barrier)
+        issue_one(kr, Kb, j0, min(SUB, j1 - j0));
+        issue_one(vr, Vb, j0, min(SUB, j1 - j0));
+    }
     if (first) local_wait(P, P.cnt + g, (unsigned)(l + 1) * (unsigned)P.Sg, ti);
-    fetch_new(kr, Kb, j0, min(SUB, j1 - j0));
-    fetch_new(vr, Vb, j0, min(SUB, j1 - j0));
+    // the new slot (written during this step by another workgroup) is read
+    // once, by the lanes that hold it, with device-coherent loads after the
+    // wait into registers of their own; a lane takes it in place of its ring
+    // value where its slab holds the new position (no ring load is
+    // conditional, so the compiler's waits for the ring stay exact)
+    u32x4 knew = {0u, 0u, 0u, 0u}, vnew = {0u, 0u, 0u, 0u};
+    {
+        const int pl = (pnew - j0) % SUB;   // its place in its sub-chunk
+        if (compute && pnew >= j0 && pnew < j1 && (pl / PP) % kWaves == wid && pl % PP == pi) {
+            knew = ld_dev_16B(Kb + (size_t)pnew * D + ds);
+            vnew = ld_dev_16B(Vb + (size_t)pnew * D + ds);
+        }
+    }
     for (int t = threadIdx.x; t < G * D; t += kThreads)
         qs[t] = ld_dev(P.q + (size_t)b * P.nq * D + (size_t)g * G * D + t);
     if (threadIdx.x < G) {
@@ -1433,91 +1440,117 @@ __device__ __forceinline__ void attn_item(KArg ka, int l, int b, int g, int c, b
 #pragma unroll
         for (int e = 0; e < 8; ++e) acc[h][e] = 0.f;
 
-    for (int js = j0; js < j1; js += SUB) {
-        const int len = min(SUB, j1 - js);
-        const int jn = js + SUB, lenn = min(SUB, j1 - jn);   // the next sub-chunk
-        // scores (q is read from LDS; all lanes take part in the lane sums)
-        if (compute) {
-#pragma unroll
-            for (int t = 0; t < NG; ++t) {
-                const int jl = jloc(t);
-                const float kf[8] = {bf_lo(kr[t].x), bf_hi(kr[t].x), bf_lo(kr[t].y),
-                                     bf_hi(kr[t].y), bf_lo(kr[t].z), bf_hi(kr[t].z),
-                                     bf_lo(kr[t].w), bf_hi(kr[t].w)};
-#pragma unroll
-                for (int h = 0; h < G; ++h) {
-                    const float4 q0 = *reinterpret_cast<const float4 *>(qs + h * D + ds);
-                    const float4 q1 = *reinterpret_cast<const float4 *>(qs + h * D + ds + 4);
-                    float s = 0.f;
-                    s = fmaf(q0.x, kf[0], s);
-                    s = fmaf(q0.y, kf[1], s);
-                    s = fmaf(q0.z, kf[2], s);
-                    s = fmaf(q0.w, kf[3], s);
-                    s = fmaf(q1.x, kf[4], s);
-                    s = fmaf(q1.y, kf[5], s);
-                    s = fmaf(q1.z, kf[6], s);
-                    s = fmaf(q1.w, kf[7], s);
-                    s = sum_lanes<LP>(s);
-                    if (jl < len && (lane % LP) == 0) sp[h * SUB + jl] = s * scale;
-                }
-            }
+    // (the loop is split by role: in the compute waves' copy every ring load
+    // is consumed on every path, so the compiler's waits stay exact; the
+    // control wave takes part in the barriers only)
+    if (!compute) {
+        for (int js = j0; js < j1; js += SUB) {
+            __syncthreads();
+            __syncthreads();
+            __syncthreads();
         }
-        if (jn < j1) {
-            issue_one(kr, Kb, jn, lenn);
-            fetch_new(kr, Kb, jn, lenn);
-        }
-        __syncthreads();
-        // softmax statistics: wave h owns head h
-        if (wid < G) {
-            const int h = wid;
-            float mx = -INFINITY;
-            for (int j = lane; j < len; j += 64) mx = fmaxf(mx, sp[h * SUB + j]);
-            mx = wave_max(mx);
-            const float mold = st[h * 4], mnew = fmaxf(mold, mx);
-            const float resc = (mold == -INFINITY) ? 0.f : expf(mold - mnew);
-            float sum = 0.f;
-            for (int j = lane; j < len; j += 64) {
-                const float e = expf(sp[h * SUB + j] - mnew);
-                sp[h * SUB + j] = e;
-                sum += e;
-            }
-            sum = wave_sum(sum);
-            if (lane == 0) {
-                st[h * 4 + 0] = mnew;
-                st[h * 4 + 1] = st[h * 4 + 1] * resc + sum;
-                st[h * 4 + 2] = resc;
-            }
-        }
-        __syncthreads();
-        // values
-        if (compute) {
+    } else {
+        // one sub-chunk; refill: issue the next sub-chunk's loads (every
+        // sub-chunk but the last; a refill that is conditional at run time
+        // makes the compiler assume on every path the fewest loads
+        // outstanding, and wait for all of them, so with PEEL the last
+        // sub-chunk is a copy of its own)
+        auto sub_chunk = [&](int js, auto refill) {
+            const int len = min(SUB, j1 - js);
+            const int jn = js + SUB, lenn = min(SUB, j1 - jn);   // the next sub-chunk
+            // scores (q is read from LDS; all lanes take part in the lane sums)
+            {
 #pragma unroll
-            for (int h = 0; h < G; ++h) {
-                const float r = st[h * 4 + 2];
-#pragma unroll
-                for (int e = 0; e < 8; ++e) acc[h][e] *= r;
-            }
-#pragma unroll
-            for (int t = 0; t < NG; ++t) {
-                const int jl = jloc(t);
-                if (jl < len) {
-                    const float vf[8] = {bf_lo(vr[t].x), bf_hi(vr[t].x), bf_lo(vr[t].y),
-                                         bf_hi(vr[t].y), bf_lo(vr[t].z), bf_hi(vr[t].z),
-                                         bf_lo(vr[t].w), bf_hi(vr[t].w)};
+                for (int t = 0; t < NG; ++t) {
+                    const int jl = jloc(t);
+                    const u32x4 kv = js + jl == pnew ? knew : kr[t];
+                    const float kf[8] = {bf_lo(kv.x), bf_hi(kv.x), bf_lo(kv.y), bf_hi(kv.y),
+                                         bf_lo(kv.z), bf_hi(kv.z), bf_lo(kv.w), bf_hi(kv.w)};
 #pragma unroll
                     for (int h = 0; h < G; ++h) {
-                        const float pr = sp[h * SUB + jl];
-#pragma unroll
-                        for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(pr, vf[e], acc[h][e]);
+                        const float4 q0 = *reinterpret_cast<const float4 *>(qs + h * D + ds);
+                        const float4 q1 = *reinterpret_cast<const float4 *>(qs + h * D + ds + 4);
+                        float s = 0.f;
+                        s = fmaf(q0.x, kf[0], s);
+                        s = fmaf(q0.y, kf[1], s);
+                        s = fmaf(q0.z, kf[2], s);
+                        s = fmaf(q0.w, kf[3], s);
+                        s = fmaf(q1.x, kf[4], s);
+                        s = fmaf(q1.y, kf[5], s);
+                        s = fmaf(q1.z, kf[6], s);
+                        s = fmaf(q1.w, kf[7], s);
+                        s = sum_lanes<LP>(s);
+                        if (jl < len && (lane % LP) == 0) sp[h * SUB + jl] = s * scale;
                     }
                 }
             }
+            if (bool(refill)) issue_one(kr, Kb, jn, lenn);
+            __syncthreads();
+            // softmax statistics: wave h owns head h
+            if (wid < G) {
+                const int h = wid;
+                float mx = -INFINITY;
+                for (int j = lane; j < len; j += 64) mx = fmaxf(mx, sp[h * SUB + j]);
+                mx = wave_max(mx);
+                const float mold = st[h * 4], mnew = fmaxf(mold, mx);
+                const float resc = (mold == -INFINITY) ? 0.f : expf(mold - mnew);
+                float sum = 0.f;
+                for (int j = lane; j < len; j += 64) {
+                    const float e = expf(sp[h * SUB + j] - mnew);
+                    sp[h * SUB + j] = e;
+                    sum += e;
+                }
+                sum = wave_sum(sum);
+                if (lane == 0) {
+                    st[h * 4 + 0] = mnew;
+                    st[h * 4 + 1] = st[h * 4 + 1] * resc + sum;
+                    st[h * 4 + 2] = resc;
+                }
+            }
+            __syncthreads();
+            // values
+            {
+#pragma unroll
+                for (int h = 0; h < G; ++h) {
+                    const float r = st[h * 4 + 2];
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) acc[h][e] *= r;
+                }
+#pragma unroll
+                for (int t = 0; t < NG; ++t) {
+                    const int jl = jloc(t);
+                    if (jl < len) {
+                        const u32x4 vv = js + jl == pnew ? vnew : vr[t];
+                        const float vf[8] = {bf_lo(vv.x), bf_hi(vv.x), bf_lo(vv.y), bf_hi(vv.y),
+                                             bf_lo(vv.z), bf_hi(vv.z), bf_lo(vv.w), bf_hi(vv.w)};
+#pragma unroll
+                        for (int h = 0; h < G; ++h) {
+                            const float pr = sp[h * SUB + jl];
+#pragma unroll
+                            for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(pr, vf[e], acc[h][e]);
+                        }
+                    } else if constexpr (PEEL) {
+                        // (a slot past the sub-chunk is still marked as read, so that
+                        // no ring register is left pending on one path, which would
+                        // make the compiler wait for all loads before refilling it)
+                        asm volatile("" ::"v"(vr[t].x), "v"(vr[t].y), "v"(vr[t].z), "v"(vr[t].w));
+                    }
+                }
+            }
+            if (bool(refill)) issue_one(vr, Vb, jn, lenn);
+            __syncthreads();
+        };
+        if constexpr (PEEL) {
+            int js = j0;
+            for (; js + SUB < j1; js += SUB) sub_chunk(js, std::true_type{});
+            if (js < j1) sub_chunk(js, std::false_type{});
+        } else {
+            // (a single copy of the body, with the refill decided at run time:
+            // 8 query heads per KV head need every register, and at batch 1 a
+            // chunk is mostly one sub-chunk, where the larger code costs more
+            // than the exact waits gain)
+            for (int js = j0; js < j1; js += SUB) sub_chunk(js, js + SUB < j1);
         }
-        if (jn < j1) {
-            issue_one(vr, Vb, jn, lenn);
-            fetch_new(vr, Vb, jn, lenn);
-        }
-        __syncthreads();
     }
     // reduce the PP position slots of each wave, then the waves in order
     if (compute) {
@@ -1596,7 +1629,8 @@ __device__ __forceinline__ void phase_attn(KArg ka, int l, int garrive, int ti) 
         const int items = P.B * P.C;
         bool last = false;
         for (int it = part; it < items; it += P.Sg) {
-            attn_item<D, G, merge_last<D, G, BAT>()>(ka, l, it / P.C, g, it % P.C, it == part, ti);
+            attn_item<D, G, merge_last<D, G, BAT>(), BAT && G <= 4>(ka, l, it / P.C, g, it % P.C,
+                                                                   it == part, ti);
             if (merge_last<D, G, BAT>()) {
                 __syncthreads();
                 last = last || S.sm[kSmLastFlag] != 0.f;
