@@ -17,6 +17,7 @@ constexpr int kTileK = 64;                // columns of one packed weight tile
 constexpr int kTileBytes = kTileRows * kTileK * 2;   // 1 KiB: one 16-byte load per lane
 constexpr int kRgBatch = 16;              // row groups reduced per LDS round
 constexpr int kAttnLoads = 5;             // K (and V) loads per lane per attention sub-chunk
+constexpr int kAttnLoadsPeel = 4;         // the same, batched kernel with up to 4 query heads per KV head
 constexpr int kCombBatch = 32;            // chunk partials loaded together when merging
 // Batched steps (batch >= kMfmaBatch) run the weight products on the matrix
 // cores.  An activation x enters them as two bf16 terms, hi = bf16(x) and

@@ -690,14 +690,12 @@ __device__ __forceinline__ void gemv_phase(const uint8_t *__restrict__ W, int KT
 // bf16 terms of X (hi, then lo, into the same accumulators).  Operand layouts:
 // A lane l holds A[l % 16][8 (l / 16) .. +7], B lane l holds
 // B[8 (l / 16) .. +7][l % 16], D lane l holds D[4 (l / 16) + v][l % 16].
-// Weight tiles arrive through the same ring of 16-byte loads as the GEMV path
-// and are re-laid out through a per-wave LDS slot (2 KiB: the two tiles of a
-// block at one k-tile).  X is staged in LDS in chunks of kGemmChunkK columns
-// (kActStride bf16 per row; the hi rows, then kLoOff elements further the lo
-// rows), double-buffered: stage(c, buf) fills chunk c.  Waves share blocks and
-// k-tiles: with nblk >= 8 blocks each wave takes whole blocks, else
-// ksplit = 8 / nblk waves share a block's k-tiles and their partial products
-// are added in wave order.
+// Weight tiles arrive through the same kind of ring of 16-byte loads as the
+// GEMV path and are re-laid out through a per-wave LDS slot (2 KiB: the two
+// tiles of a block at one k-tile; the slots follow the two activation chunk
+// buffers).  X is staged in LDS in chunks of kGemmChunkK columns (kActStride
+// bf16 per row; the hi rows, then kLoOff elements further the lo rows), in
+// two chunk buffers: stage(c, buf) fills chunk c.
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
@@ -705,14 +703,12 @@ constexpr int kLoOff = kGemmBatch * kActStride;   // elements from a chunk's hi 
 
 struct GemmLds {
     uint16_t *act[2];   // [2 terms][kGemmBatch][kActStride] bf16
-    uint8_t *wslot;     // [kWaves][2048]
 };
 
 __device__ __forceinline__ GemmLds gemm_lds(char *smem) {
     GemmLds g;
     g.act[0] = reinterpret_cast<uint16_t *>(smem);
     g.act[1] = reinterpret_cast<uint16_t *>(smem + 2 * kGemmActBytes);
-    g.wslot = reinterpret_cast<uint8_t *>(smem + 4 * kGemmActBytes);
     return g;
 }
 
@@ -1361,10 +1357,11 @@ __device__ __forceinline__ void merge_chunks(const StepParams &P, int b, int g, 
 // of (b, g) to finish merges all chunks in chunk order and writes o.  The
 // first sub-chunk's K/V vectors are loaded before the barrier wait, except
 // the new slot, which the QKV phase writes and which is read after the wait
-// with device-coherent loads (into registers of its own).  Loads are unconditional (spare ones target a
-// shared 16-byte line) and masked when consumed.
-template <int D>
-constexpr int attn_sub() { return kWaves * kAttnLoads * (64 / (D / 8)); }
+// with device-coherent loads (into registers of its own).  Loads are
+// unconditional (spare ones target a shared 16-byte line) and masked when
+// consumed.
+template <int D, int NG>
+constexpr int attn_sub() { return kWaves * NG * (64 / (D / 8)); }
 
 // PEEL (batched path, up to 4 query heads per KV head, where the chunks are
 // long): the last sub-chunk is a copy of its own, see below.
@@ -1375,8 +1372,10 @@ __device__ __forceinline__ void attn_item(KArg ka, int l, int b, int g, int c, b
     const Lds S = lds_layout(kl_smem, P);
     constexpr int LP = D / 8;                       // lanes per position
     constexpr int PP = 64 / LP;                     // positions per slab
-    constexpr int NG = kAttnLoads;                  // slabs per wave per sub-chunk
-    constexpr int SUB = attn_sub<D>();              // positions per sub-chunk
+    // slabs per wave per sub-chunk (the batched kernel's long chunks: fewer,
+    // measured faster there; never more than kAttnLoads, which sizes the LDS)
+    constexpr int NG = PEEL ? kAttnLoadsPeel : kAttnLoads;
+    constexpr int SUB = attn_sub<D, NG>();          // positions per sub-chunk
     const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
     const int pi = lane / LP, ds = (lane % LP) * 8;
