@@ -36,6 +36,7 @@ constexpr int kGemmResidentK = 2 * kGemmChunkK;   // K columns a workgroup keeps
 // per-wave weight re-layout slots (2 KiB)
 constexpr int kGemmActBytes = kGemmBatch * kActStride * 2;   // one term of one chunk
 constexpr int kGemmLdsBytes = 4 * kGemmActBytes + kWaves * 2048;
+constexpr int kNormCntStride = 64;        // words between batched RMSNorm slice counters
 constexpr int kMaxGroup = 8;              // max query heads per KV head
 constexpr int kBarGroups = 16;            // first level of the grid barrier
 constexpr int kBarBytes = 8192;           // barrier counters: kBarGroups lines of 256 B
@@ -99,7 +100,8 @@ struct StepParams {
     uint16_t *actm, *actm_lo;  // [max_batch][Fp] SwiGLU output
     uint16_t *acto, *acto_lo;  // [max_batch][nq*d] attention output, when C == 1
     unsigned long long *bar;   // grid barrier counters (monotonic): group g at [32 (g + 1)]
-    unsigned *cnt;             // local counters: [nkv] qkv, [nkv] attention, [Sc] gate/up
+    unsigned *cnt;             // local counters: [nkv] qkv, [nkv] attention, [Sc] gate/up,
+                               // then the batched RMSNorm slices (256 bytes apart)
     int *err;                  // device error word
     const uint8_t *dummy;      // 16 readable bytes: target of the GEMV ring's spare loads
     int nwg;                   // grid size

@@ -977,9 +977,17 @@ __device__ __forceinline__ void weight_phase(const StepParams &P, const Lds &S,
 // of x gain, and the row's sum of squares goes to P.ssp per kGemmChunkK
 // columns.  The consumers apply r = 1 / rms(x) to the products (rms_r).
 // Items (sequence, kGemmChunkK-column slice) are spread over the grid, one
-// column per thread.  Ends with grid barrier k.
+// column per thread.  Each item arrives on its slice's counter (norm_cnt,
+// B arrivals per slice per RMSNorm step); a product waits only for the
+// slices it stages (norm_wait) instead of on a grid barrier.  The counters
+// sit kNormCntStride words apart: on one shared line, the polls of every
+// control wave and the items' atomics contend (measured slower than the
+// grid barrier).
+__device__ __forceinline__ unsigned *norm_cnt(const StepParams &P) {
+    return P.cnt + 2 * P.nkv + P.Sc;
+}
 __device__ __forceinline__ void norm_batched(const StepParams &P, const Lds &S,
-                                             const float *gain, int k, const long long *xin,
+                                             const float *gain, const long long *xin,
                                              long long *xout, int nparts) {
     static_assert(kGemmChunkK <= kThreads, "one column per thread");
     const int ns = (P.Hp + kGemmChunkK - 1) / kGemmChunkK;
@@ -1013,10 +1021,27 @@ __device__ __forceinline__ void norm_batched(const StepParams &P, const Lds &S,
         }
         ss = block_sum(ss, S.sm);
         if (threadIdx.x == 0) st_dev(P.ssp + (size_t)b * ns + sl, ss);
-        __syncthreads();   // (S.sm is reused by the next item)
+        drain_all();   // (also: S.sm is reused by the next item)
+        if (is_ctl_lane0())
+            __hip_atomic_fetch_add(norm_cnt(P) + kNormCntStride * sl, 1u, __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
     }
-    bar_arrive(P, k, -1);
-    bar_wait(P, k, -1);
+}
+
+// The control wave waits until the slices [c0, c1) of RMSNorm step inst
+// (numbered within the step: 2 l for layer l's attention norm, 2 l + 1 for
+// its FFN norm, 2 L for the final norm) are complete.  No workgroup barrier:
+// the control wave then copies those slices (the other waves meet it at the
+// barrier after the copies).
+__device__ __forceinline__ void norm_wait(const StepParams &P, int inst, int c0, int c1) {
+    if (is_ctl_lane0()) {
+        const unsigned target = (unsigned)(inst + 1) * (unsigned)P.B;
+        for (int c = c0; c < c1; ++c)
+            spin_until(P, [&]() {
+                return (int)(__hip_atomic_load(norm_cnt(P) + kNormCntStride * c, __ATOMIC_RELAXED,
+                                               __HIP_MEMORY_SCOPE_AGENT) - target) >= 0;
+            });
+    }
 }
 
 // (the steps that apply the scales keep those of sequences below
@@ -1142,7 +1167,8 @@ __device__ __forceinline__ void phase_embed(KArg ka, int gwait, int garrive, int
             if (p < 0 || p >= P.cap || p >= P.max_seq) bits |= KL_DEVERR_POSITION;
             if (bits) atomicOr(P.err, bits);
         }
-        for (int i = threadIdx.x; i < 2 * P.nkv + P.Sc; i += kThreads)
+        const int nc = 2 * P.nkv + P.Sc + kNormCntStride * ((P.Hp + kGemmChunkK - 1) / kGemmChunkK);
+        for (int i = threadIdx.x; i < nc; i += kThreads)
             __hip_atomic_store(P.cnt + i, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
     const int total = P.B * P.Hp;
@@ -1224,8 +1250,7 @@ __device__ __forceinline__ void fold_qkv(const StepParams &P, const Lds &S, int 
 // writes K-slice partials; after grid barrier qbar head g's workgroups fold
 // them (fold_qkv).
 template <bool BAT>
-__device__ __forceinline__ void phase_qkv(KArg ka, int l, int gwait, int xbar, int qbar,
-                                          int ti) {
+__device__ __forceinline__ void phase_qkv(KArg ka, int l, int gwait, int qbar, int ti) {
     const StepParams P = load_params(ka);
     const Lds S = lds_layout(kl_smem, P);
     const int g = blockIdx.x / P.Sg, part = blockIdx.x % P.Sg;
@@ -1247,11 +1272,13 @@ __device__ __forceinline__ void phase_qkv(KArg ka, int l, int gwait, int xbar, i
             // (layer 0 reads the embedding; later layers fold the down
             // projection's partials, x: xf2 -> xf)
             [&]() {
-                norm_batched(P, S, gain, xbar, l == 0 ? P.xf : P.xf2, P.xf, l == 0 ? 0 : P.KSd);
+                norm_batched(P, S, gain, l == 0 ? P.xf : P.xf2, P.xf, l == 0 ? 0 : P.KSd);
                 if (is_ctl_lane0()) trace_stamp(P, ti, 3);
             },
             [&](int) {},
             [&](int c, int b0, int nb, uint16_t *buf) {
+                const int sl = col0 / kGemmChunkK + c;
+                if (b0 == 0) norm_wait(P, 2 * l, sl, sl + 1);
                 stage_bf16_chunk(P.act + col0, P.act_lo + col0, P.Hp, KTs * kTileK, c, b0, nb, buf);
             },
             [&](int b, int r, float y0, float y1) {
@@ -1721,8 +1748,7 @@ __device__ __forceinline__ void phase_oproj(KArg ka, int l, int gwait, int mbar,
 // RMSNorm + gate/up projection + SwiGLU for FFN column block j = w / Rc:
 // m = silu(Wg u) * (Wu u).  Packed rows alternate gate i, up i.
 template <bool BAT>
-__device__ __forceinline__ void phase_gateup(KArg ka, int l, int gwait, int xbar, int garrive,
-                                             int ti) {
+__device__ __forceinline__ void phase_gateup(KArg ka, int l, int gwait, int garrive, int ti) {
     const StepParams P = load_params(ka);
     const Lds S = lds_layout(kl_smem, P);
     const uint8_t *Lb = P.arena + (size_t)l * P.layer_stride;
@@ -1745,11 +1771,13 @@ __device__ __forceinline__ void phase_gateup(KArg ka, int l, int gwait, int xbar
             [&]() { if (gwait >= 0) bar_wait(P, gwait, ti); },
             // (folds the O projection's partials, x: xf -> xf2)
             [&]() {
-                norm_batched(P, S, gain, xbar, P.xf, P.xf2, P.KSo);
+                norm_batched(P, S, gain, P.xf, P.xf2, P.KSo);
                 if (is_ctl_lane0()) trace_stamp(P, ti, 3);
             },
             [&](int) {},
             [&](int c, int b0, int nb, uint16_t *buf) {
+                const int sl = col0 / kGemmChunkK + c;
+                if (b0 == 0) norm_wait(P, 2 * l + 1, sl, sl + 1);
                 stage_bf16_chunk(P.act + col0, P.act_lo + col0, P.Hp, KTs * kTileK, c, b0, nb, buf);
             },
             [&](int b, int r, float gt, float up) {
@@ -1914,7 +1942,7 @@ __device__ __forceinline__ void copy_hidden(const StepParams &P) {
 
 // Classifier block (Sec. 2): final RMSNorm + LM head -> fp32 logits.
 template <bool BAT>
-__device__ __forceinline__ void phase_head(KArg ka, int gwait, int xbar, int ti) {
+__device__ __forceinline__ void phase_head(KArg ka, int gwait, int ti) {
     const StepParams P = load_params(ka);
     const Lds S = lds_layout(kl_smem, P);
     const RgRange R = own_rgs(P.head_rg, P);
@@ -1928,7 +1956,9 @@ __device__ __forceinline__ void phase_head(KArg ka, int gwait, int xbar, int ti)
         [&]() {
             // (folds the last down projection's partials, x: xf2 -> xf), and
             // the sequences' RMSNorm scales for the epilogue
-            norm_batched(P, S, P.final_norm, xbar, P.xf2, P.xf, P.KSd);
+            norm_batched(P, S, P.final_norm, P.xf2, P.xf, P.KSd);
+            norm_wait(P, 2 * P.L, 0, (P.Hp + kGemmChunkK - 1) / kGemmChunkK);
+            __syncthreads();
             rms_table(P, S);
             if (is_ctl_lane0()) trace_stamp(P, ti, 3);
             if (blockIdx.x == 0 && P.hidden_out) copy_hidden(P);
@@ -1964,7 +1994,9 @@ __global__ __launch_bounds__(kThreads) void kl_step_kernel(StepParams P, int l0,
     const KArg ka = kernarg_address();
     const bool has_qkv = phases & kPhQkv, has_gu = phases & kPhGateUp, has_head = phases & kPhHead;
     const int nlay = (phases & kPhLayer) ? l1 - l0 : 0;
-    // batched steps add a grid barrier inside each RMSNorm phase (norm_batched)
+    // batched steps add grid barriers of their own: after the q/k/v product
+    // (its fold), in the SwiGLU fold, and before a merge of several attention
+    // chunks (their RMSNorm steps hand over through slice counters instead)
     constexpr bool batched = BAT;
     bar_init(load_params(ka));
     int na = 0, ti = 0;   // grid arrivals so far; phase index (for the trace)
@@ -1980,8 +2012,8 @@ __global__ __launch_bounds__(kThreads) void kl_step_kernel(StepParams P, int l0,
         // batched steps: attn -> oproj and gateup -> down are grid barriers
         // too (full-K products with one writer per output)
         if (phases & kPhQkv) {
-            const int w = gw(), x = xb(), q = xb();
-            phase_qkv<BAT>(ka, l, w, x, q, ti++);
+            const int w = gw(), q = xb();
+            phase_qkv<BAT>(ka, l, w, q, ti++);
         }
         if (phases & kPhAttn) phase_attn<D, G, BAT>(ka, l, BAT ? ga(has_op) : -1, ti++);
         if (phases & kPhOproj) {
@@ -1991,8 +2023,8 @@ __global__ __launch_bounds__(kThreads) void kl_step_kernel(StepParams P, int l0,
             phase_oproj<D, G, BAT>(ka, l, w, m, a, ti++);
         }
         if (phases & kPhGateUp) {
-            const int w = gw(), x = xb(), a = BAT ? ga(has_down) : -1;
-            phase_gateup<BAT>(ka, l, w, x, a, ti++);
+            const int w = gw(), a = BAT ? ga(has_down) : -1;
+            phase_gateup<BAT>(ka, l, w, a, ti++);
         }
         if (phases & kPhDown) {
             // (batched: the SwiGLU fold of the gate/up partials ends with a
@@ -2002,8 +2034,7 @@ __global__ __launch_bounds__(kThreads) void kl_step_kernel(StepParams P, int l0,
         }
     }
     if (has_head) {
-        const int w = gw(), x = xb();
-        phase_head<BAT>(ka, w, x, ti++);
+        phase_head<BAT>(ka, gw(), ti++);
     }
 }
 
