@@ -336,11 +336,11 @@ kl_status kl_model_create(const kl_config *cfg, kl_state **out) {
     const size_t off_acto = so; so = align_up(so + (size_t)B * S->Ap * 2 * 2, 256);
     const size_t off_bar = so;  so = align_up(so + kBarBytes, 256);
     // local counters: qkv and attention per KV head, gate/up per FFN column
-    // block, batched RMSNorm per 512-column slice (256 bytes apart)
+    // block, batched RMSNorm per 512-column slice (256 bytes apart; batched
+    // path only)
+    const int norm_cnts = B >= kMfmaBatch ? kNormCntStride * ((S->Hp + kGemmChunkK - 1) / kGemmChunkK) : 0;
     const size_t off_cnt = so;
-    so = align_up(so + (size_t)(2 * nkv + S->Sc +
-                                kNormCntStride * ((S->Hp + kGemmChunkK - 1) / kGemmChunkK)) * 4,
-                  256);
+    so = align_up(so + (size_t)(2 * nkv + S->Sc + norm_cnts) * 4, 256);
     const size_t off_err = so;  so = align_up(so + 256, 256);
     const size_t off_dummy = so; so = align_up(so + kTileBytes, 256);
     // batched path: the second residual buffer and the K-slice partial sums

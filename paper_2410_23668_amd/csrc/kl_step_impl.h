@@ -1167,7 +1167,9 @@ __device__ __forceinline__ void phase_embed(KArg ka, int gwait, int garrive, int
             if (p < 0 || p >= P.cap || p >= P.max_seq) bits |= KL_DEVERR_POSITION;
             if (bits) atomicOr(P.err, bits);
         }
-        const int nc = 2 * P.nkv + P.Sc + kNormCntStride * ((P.Hp + kGemmChunkK - 1) / kGemmChunkK);
+        // (the batched RMSNorm counters exist, and are used, in batched steps only)
+        const int nc = 2 * P.nkv + P.Sc +
+                       (P.B >= kMfmaBatch ? kNormCntStride * ((P.Hp + kGemmChunkK - 1) / kGemmChunkK) : 0);
         for (int i = threadIdx.x; i < nc; i += kThreads)
             __hip_atomic_store(P.cnt + i, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
