@@ -171,10 +171,12 @@ kl_status kl_get_info(const kl_state *st, kl_info *info);
  * every later launch writes, for phase i < max_phases of the launch (in the
  * order embed, then qkv, attn, oproj, gateup, down per layer, then head) and
  * workgroup w, s_memrealtime stamps (100 MHz ticks) into
- *   dev_buffer[(i * n_workgroups + w) * 4 + {0: phase end, 1: start of the
- *   wait for its inputs, 2: end of that wait, 3: inputs staged (in LDS on
- *   the per-sequence path; batches of 8 or more: the grid-wide RMSNorm done;
- *   an attention phase: its chunk result published)}]
+ *   dev_buffer[(i * n_workgroups + w) * 4 + {0: phase end (every wave of the
+ *   workgroup done, its writes complete), 1: start of the wait for its
+ *   inputs, 2: end of that wait, 3: inputs staged (in LDS on the
+ *   per-sequence path; batches of 8 or more: the workgroup's share of the
+ *   grid-wide step before the product, RMSNorm or SwiGLU fold, done; an
+ *   attention phase: its chunk result published)}]
  * (slots a workgroup does not reach keep their old contents; a launch
  * overwrites the previous launch's entries).  The buffer (dev, uint64,
  * max_phases * n_workgroups * 4 entries) stays owned by the caller; pass NULL
