@@ -33,6 +33,20 @@ DEVICE_SRC = sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC)
                     if f.endswith((".hip", ".h", ".cpp")))
 
 
+PEAK_BF16_FLOPS = 2.5e15   # dense bf16 matrix-core peak of MI355X
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
@@ -155,14 +169,15 @@ def main():
     kv = KvCache(cfg, B, cap, k_host=K0, v_host=V0)
     toks = torch.from_numpy(tokens).cuda()
     pos = torch.full((B,), P, dtype=torch.int32, device="cuda")
-    logits = torch.empty((B, cfg["vocab"]), dtype=torch.float32, device="cuda")
     info = model.info()
 
     modes = [m.strip() for m in args.modes.split(",") if m.strip()]
     res = {}
+    outs = {}   # each schedule writes logits of its own
     for m in modes:
+        outs[m] = torch.full((B, cfg["vocab"]), float("nan"), dtype=torch.float32, device="cuda")
         log(f"timing mode {m}: {args.warmup} warmup + {args.steps} steps")
-        res[m] = time_mode(model, toks, pos, kv, logits, kb.MODES[m], args.steps, args.warmup)
+        res[m] = time_mode(model, toks, pos, kv, outs[m], kb.MODES[m], args.steps, args.warmup)
         log(f"  {m}: mean {res[m]['mean_ms']:.3f} ms/step")
     err = model.device_error()
     if err:
@@ -201,24 +216,49 @@ def main():
     }
     if "per_layer" in res and head != "per_layer":
         out["speedup_vs_per_layer"] = res["per_layer"]["mean_ms"] / step_ms
+    # every schedule computes the same bits (the timed launches' own outputs)
+    for m in modes[1:]:
+        out[f"bit_exact_{head}_vs_{m}"] = bool(torch.equal(outs[head].view(torch.int32),
+                                                           outs[m].view(torch.int32)))
+    if B >= info.mfma_min_batch:
+        # the weight products run on the matrix cores, each activation as two
+        # bf16 terms (two products per weight element)
+        flops = bytemodel.step_flops(cfg, B, P)
+        mflops = 2 * bytemodel.weight_macs(cfg) * 2 * B
+        out["mfma"] = {"algorithmic_tflops": flops / (step_ms * 1e-3) / 1e12,
+                       "utilisation": flops / (step_ms * 1e-3) / PEAK_BF16_FLOPS,
+                       "issued_tflops": mflops / (step_ms * 1e-3) / 1e12,
+                       "issued_utilisation": mflops / (step_ms * 1e-3) / PEAK_BF16_FLOPS,
+                       "peak_tflops": PEAK_BF16_FLOPS / 1e12,
+                       "note": "algorithmic = 2 flops per weight MAC and sequence plus attention; "
+                               "issued = the matrix-core products actually run (hi and lo "
+                               "activation terms), against the dense bf16 peak"}
 
     # parity of the timed output, and the oracle's own time on the host
     if not args.no_cpu_baseline and weights is not None:
         import oracle
-        log("oracle (1 thread) on the same inputs")
-        Kr, Vr = K0.copy(), V0.copy()
+        # a bounded sample: one sequence of the batch (sequences are independent)
+        nb = 1
+        log(f"oracle (1 thread) on {nb} sequence(s) of the same inputs")
+        Kr, Vr = K0[:, :nb].copy(), V0[:, :nb].copy()
         t = time.perf_counter()
-        ref_logits, _ = oracle.decode_step(cfg, weights, tokens, [P] * B, Kr, Vr, nthreads=1)
+        ref_logits, _ = oracle.decode_step(cfg, weights, tokens[:nb], [P] * nb, Kr, Vr,
+                                           nthreads=1)
         cpu_s = time.perf_counter() - t
-        got = logits.cpu().numpy()
-        out["parity_rel_l2_logits"] = max(oracle.rel_l2(got[b], ref_logits[b]) for b in range(B))
-        out["cpu_baseline"] = {"value": B / cpu_s, "unit": "tok/s", "cores": 1, "kind": "oracle",
-                               "sample": f"one full decode step of {args.workload}, fp64 oracle, "
+        got = outs[head][:nb].cpu().numpy()
+        out["parity_rel_l2_logits"] = max(oracle.rel_l2(got[b], ref_logits[b]) for b in range(nb))
+        out["parity_elem_logits"] = max(
+            float(abs(got[b] - ref_logits[b]).max() / abs(ref_logits[b]).max()) for b in range(nb))
+        out["parity_of"] = f"{head} schedule, the timed launches' logits, sequence(s) 0..{nb - 1}"
+        out["cpu_baseline"] = {"value": nb / cpu_s, "unit": "tok/s", "cores": 1, "kind": "oracle",
+                               "nproc": os.cpu_count(), "cpu_model": cpu_model(),
+                               "sample": f"one decode step of {nb} sequence(s) of "
+                                         f"{args.workload} (all layers), fp64 oracle, "
                                          f"1 thread, {cpu_s:.1f} s"}
     print(json.dumps(out), flush=True)
     # release device memory before interpreter shutdown
     model.close()
-    del kv, toks, pos, logits
+    del kv, toks, pos, outs
     torch.cuda.synchronize()
 
 

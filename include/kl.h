@@ -55,9 +55,12 @@ typedef enum {
     KL_MODE_PER_OP = 2
 } kl_mode;
 
-/* Bits of the device error word (kl_get_device_error). */
-#define KL_DEVERR_TOKEN    1   /* a token id outside [0, vocab): row 0 was used instead      */
-#define KL_DEVERR_POSITION 2   /* a position outside [0, capacity) or >= max_seq: clamped    */
+/* Bits of the device error word (kl_get_device_error).  A sequence with a bad
+ * token or position is skipped: none of its K/V slots is written and its
+ * logits (and hidden state) are NaN; the other sequences of the step are
+ * computed normally. */
+#define KL_DEVERR_TOKEN    1   /* a token id outside [0, vocab)                              */
+#define KL_DEVERR_POSITION 2   /* a position outside [0, capacity) or >= max_seq             */
 #define KL_DEVERR_BARRIER  4   /* a grid barrier waited longer than its watchdog allows      */
 
 /* Model shape.  Supported: head_dim 64 or 128, n_heads a multiple of
@@ -103,6 +106,8 @@ typedef struct {
     int32_t threads_per_group;
     int32_t lds_bytes;          /* dynamic LDS per workgroup                       */
     int32_t attn_chunks_b1;     /* KV chunks per (sequence, KV head) at batch 1    */
+    int32_t mfma_min_batch;     /* steps with batch >= this run the weight products
+                                   on the matrix cores                             */
     int64_t arena_bytes;        /* packed weights + gains                          */
     int64_t scratch_bytes;      /* activations, partials, counters                 */
 } kl_info;
@@ -137,7 +142,13 @@ kl_status kl_model_set_layer(kl_state *st, int32_t layer, const kl_layer_ptrs *w
 kl_status kl_model_set_globals(kl_state *st, const void *embed, const void *final_norm,
                                const void *lm_head, void *stream);
 
-/* Enqueue one decode step on 'stream' (asynchronous).
+/* Enqueue one decode step on 'stream' (asynchronous): the token step of the
+ * paper's Sec. 2 and Fig. 3 (Embedding -> L x Decoder -> Classifier), for
+ * every sequence of the batch.  In KL_MODE_LOOPED the L decoder-layer calls
+ * are collapsed into one call of the looped kernel (Sec. 3.2: the grouped
+ * per-layer arguments become one linearly laid-out argument, the call sites
+ * collapse into one); the other modes issue one launch per layer or per
+ * operator group.  Every mode computes the same bits.
  *   token_ids  dev int32 [batch]   token of each sequence
  *   positions  dev int32 [batch]   position p of the new token; the step writes
  *                                  K/V slot p of every layer and attends over
@@ -148,10 +159,13 @@ kl_status kl_model_set_globals(kl_state *st, const void *embed, const void *fina
  *   hidden_out dev fp32 [batch][hidden] or NULL: the residual stream after the
  *              last layer (before the final norm)
  *   mode       a kl_mode
- * Out-of-range token ids or positions cannot be checked on the host; they set
- * bits in the device error word and are replaced by in-range values.  One step
- * may be in flight per state; the caller's buffers are borrowed until the step
- * completes in stream order. */
+ * Host-checkable errors (NULL or misaligned pointers, batch or capacity out
+ * of range, an unknown mode, the wrong current device) return a negative
+ * status with nothing enqueued.  Out-of-range token ids or positions can only
+ * be seen on the device: they set bits in the device error word, and that
+ * sequence is skipped as described with the bits.  One step may be in flight
+ * per state; the caller's buffers are borrowed until the step completes in
+ * stream order. */
 kl_status kl_decode_step(kl_state *st, const int32_t *token_ids, const int32_t *positions,
                          int32_t batch, const kl_kv_cache *kv, float *logits_out,
                          float *hidden_out, void *stream, int32_t mode);

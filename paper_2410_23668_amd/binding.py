@@ -63,6 +63,7 @@ class kl_kv_cache(ctypes.Structure):
 class kl_info(ctypes.Structure):
     _fields_ = [("n_workgroups", ctypes.c_int32), ("threads_per_group", ctypes.c_int32),
                 ("lds_bytes", ctypes.c_int32), ("attn_chunks_b1", ctypes.c_int32),
+                ("mfma_min_batch", ctypes.c_int32),
                 ("arena_bytes", ctypes.c_int64), ("scratch_bytes", ctypes.c_int64)]
 
 

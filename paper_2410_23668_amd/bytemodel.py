@@ -47,10 +47,15 @@ def step_bytes(cfg, batch: int, context: int) -> int:
     return weights + embed_rows + kv_read + kv_write + logits
 
 
-def step_flops(cfg, batch: int, context: int) -> int:
-    """2 FLOPs per weight MAC per sequence plus 4 * n_heads * d * (context + 1) per layer."""
+def weight_macs(cfg) -> int:
+    """Multiply-adds of the weight products of one step, per sequence."""
     L, H, nq, nkv, d, F, V = (cfg[k] for k in ("n_layers", "hidden", "n_heads", "n_kv_heads",
                                                  "head_dim", "ffn_dim", "vocab"))
-    macs = L * (H * nq * d + 2 * H * nkv * d + nq * d * H + 3 * H * F) + V * H
+    return L * (H * nq * d + 2 * H * nkv * d + nq * d * H + 3 * H * F) + V * H
+
+
+def step_flops(cfg, batch: int, context: int) -> int:
+    """2 FLOPs per weight MAC per sequence plus 4 * n_heads * d * (context + 1) per layer."""
+    L, nq, d = cfg["n_layers"], cfg["n_heads"], cfg["head_dim"]
     attn = L * 4 * nq * d * (context + 1)
-    return batch * (2 * macs + attn)
+    return batch * (2 * weight_macs(cfg) + attn)

@@ -189,6 +189,31 @@ void free_state(kl_state *s) {
     delete s;
 }
 
+// Whether the workgroups of one launch running 'phases' (a single phase, or
+// several) wait for each other inside it; such a launch must be cooperative,
+// so that the whole grid is resident.  Waits on work of an earlier launch are
+// already satisfied when the launch starts (stream order), so only in-launch
+// hand-offs count:
+//   several phases in one launch      grid barriers and local counters;
+//   batch >= kMfmaBatch (matrix-core path), single phases:
+//     qkv       its product's grid barrier before the fold, and the RMSNorm
+//               slice counters;
+//     oproj     with several attention chunks, the merge's grid barrier;
+//     gateup    the RMSNorm slice counters;
+//     down      the SwiGLU fold's grid barrier;
+//     head      the final RMSNorm's slice counters;
+//     attn      none (its counters were completed by the qkv launch);
+//   batch < kMfmaBatch, single phases: none (every counter a phase waits on
+//   belongs to an earlier phase).
+bool launch_waits_inside(int phases, bool batched, int C) {
+    if (phases & kPhEmbed) return phases != kPhEmbed;
+    if (__builtin_popcount((unsigned)phases) > 1) return true;
+    if (!batched) return false;
+    if (phases == kPhAttn) return false;
+    if (phases == kPhOproj) return C > 1;
+    return true;
+}
+
 StepParams base_params(const kl_state &s) {
     const kl_config &c = s.cfg;
     StepParams P{};
@@ -575,24 +600,22 @@ kl_status kl_decode_step(kl_state *st, const int32_t *token_ids, const int32_t *
 
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     const int L = c.n_layers, lds = st->lds_bytes;
-    // a launch whose workgroups wait for each other must be cooperative (all
-    // resident): every multi-phase launch, and at batch >= kMfmaBatch also
-    // the single RMSNorm phases (their batched normalisation has a barrier)
     const bool bat = batch >= kMfmaBatch;
     if (mode == KL_MODE_LOOPED) {
         HIP_TRY(launch_step(P, 0, L, kPhEmbed | kPhLayer | kPhHead, true, lds, s));
     } else if (mode == KL_MODE_PER_LAYER) {
         HIP_TRY(launch_step(P, 0, 0, kPhEmbed, false, lds, s));
-        for (int l = 0; l < L; ++l) HIP_TRY(launch_step(P, l, l + 1, kPhLayer, true, lds, s));
-        HIP_TRY(launch_step(P, 0, 0, kPhHead, bat, lds, s));
+        for (int l = 0; l < L; ++l)
+            HIP_TRY(launch_step(P, l, l + 1, kPhLayer, launch_waits_inside(kPhLayer, bat, P.C),
+                                lds, s));
+        HIP_TRY(launch_step(P, 0, 0, kPhHead, launch_waits_inside(kPhHead, bat, P.C), lds, s));
     } else {
         HIP_TRY(launch_step(P, 0, 0, kPhEmbed, false, lds, s));
         const int ops[] = {kPhQkv, kPhAttn, kPhOproj, kPhGateUp, kPhDown};
         for (int l = 0; l < L; ++l)
             for (int ph : ops)
-                HIP_TRY(launch_step(P, l, l + 1, ph, bat && (ph == kPhQkv || ph == kPhGateUp),
-                                    lds, s));
-        HIP_TRY(launch_step(P, 0, 0, kPhHead, bat, lds, s));
+                HIP_TRY(launch_step(P, l, l + 1, ph, launch_waits_inside(ph, bat, P.C), lds, s));
+        HIP_TRY(launch_step(P, 0, 0, kPhHead, launch_waits_inside(kPhHead, bat, P.C), lds, s));
     }
     return KL_OK;
 }
@@ -630,6 +653,7 @@ kl_status kl_get_info(const kl_state *st, kl_info *info) {
     info->threads_per_group = kThreads;
     info->lds_bytes = st->lds_bytes;
     info->attn_chunks_b1 = std::max(1, st->Sg);
+    info->mfma_min_batch = kMfmaBatch;
     info->arena_bytes = (int64_t)st->arena_bytes;
     info->scratch_bytes = (int64_t)st->scratch_bytes;
     return KL_OK;

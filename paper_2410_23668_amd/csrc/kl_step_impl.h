@@ -116,6 +116,10 @@ __device__ __forceinline__ void split_range(int n, int parts, int i, int &a, int
     b = (int)((long long)n * (i + 1) / parts);
 }
 
+// A sequence whose token or position is out of range still runs through the
+// step with clamped values (every read stays in bounds), but writes nothing
+// the caller owns except NaN logits and hidden state: its K/V slots are left
+// untouched.  The embedding phase raises the matching error bits.
 __device__ __forceinline__ int eff_pos(const StepParams &P, int b) {
     const int p = P.positions[b];
     const int lim = min(P.cap, P.max_seq);
@@ -124,6 +128,10 @@ __device__ __forceinline__ int eff_pos(const StepParams &P, int b) {
 __device__ __forceinline__ int eff_tok(const StepParams &P, int b) {
     const int t = P.tokens[b];
     return (t < 0 || t >= P.V) ? 0 : t;
+}
+__device__ __forceinline__ bool seq_ok(const StepParams &P, int b) {
+    const int t = P.tokens[b], p = P.positions[b];
+    return t >= 0 && t < P.V && p >= 0 && p < min(P.cap, P.max_seq);
 }
 
 __device__ __forceinline__ size_t kv_row(const StepParams &P, int l, int b, int g) {
@@ -1201,12 +1209,12 @@ __device__ __forceinline__ void qkv_store(const StepParams &P, int l, int b, int
             float *qq = P.q + (size_t)b * P.nq * d + (size_t)(g * G + lr / d) * d;
             st_dev(qq + i, u0);
             st_dev(qq + i + half, u1);
-        } else {
+        } else if (seq_ok(P, b)) {
             uint16_t *kk = P.kc + (kv_row(P, l, b, g) + p) * d;
             st_dev_u16(kk + i, f2bf(u0));
             st_dev_u16(kk + i + half, f2bf(u1));
         }
-    } else {
+    } else if (seq_ok(P, b)) {
         const int j = lr - (G + 1) * d;
         uint16_t *vv = P.vc + (kv_row(P, l, b, g) + p) * d;
         st_dev_u32(reinterpret_cast<unsigned *>(vv + j),
@@ -1938,8 +1946,11 @@ __device__ __forceinline__ void phase_down(KArg ka, int l, int gwait, int xbar, 
 
 // The final residual stream -> hidden_out (fp32).
 __device__ __forceinline__ void copy_hidden(const StepParams &P) {
-    for (int idx = threadIdx.x; idx < P.B * P.H; idx += kThreads)
-        P.hidden_out[idx] = from_fix((long long)ld_dev_u64(P.xf + (size_t)(idx / P.H) * P.Hp + idx % P.H));
+    for (int idx = threadIdx.x; idx < P.B * P.H; idx += kThreads) {
+        const int b = idx / P.H;
+        const float x = from_fix((long long)ld_dev_u64(P.xf + (size_t)b * P.Hp + idx % P.H));
+        P.hidden_out[idx] = seq_ok(P, b) ? x : __builtin_nanf("");
+    }
 }
 
 // Classifier block (Sec. 2): final RMSNorm + LM head -> fp32 logits.
@@ -1975,6 +1986,7 @@ __device__ __forceinline__ void phase_head(KArg ka, int gwait, int ti) {
             const float rs = !BAT ? rms_scale(S.sm, P.H, P.eps) : rms_of(P, S, b);
             y0 *= rs;
             y1 *= rs;
+            if (!seq_ok(P, b)) y0 = y1 = __builtin_nanf("");
             float *lg = P.logits + (size_t)b * V;
             if (r < V) lg[r] = y0;
             if (r + 1 < V) lg[r + 1] = y1;

@@ -3,7 +3,9 @@ batch 1 with a 4096- and a 65536-position cache, and at batch 32, against the
 oracle.  At batch 32 the oracle evaluates a sample of the sequences (the
 sequences of a step are independent, so the oracle runs them on their own:
 their tokens, positions and caches), in the launch configuration the bench
-times (looped schedule, one launch per step)."""
+times (looped schedule, one launch per step).  At batch 1 with 4096 cached
+positions, the per-layer and per-op schedules run too and must reproduce the
+looped schedule's logits, hidden state and K/V slot writes bit for bit."""
 import numpy as np
 import pytest
 import torch
@@ -13,12 +15,12 @@ import synth
 from paper_2410_23668_amd import binding as kb
 from paper_2410_23668_amd.device import GpuModel, KvCache
 from synth.workloads import WORKLOADS
-from tests.gpu_cases import REL_L2_TOL, bf16_rel_l2, say
+from tests.gpu_cases import check_vectors, compare_sequence, say
 
 pytestmark = pytest.mark.gpu
 
 
-def run_workload(name, sample):
+def run_workload(name, sample, modes=("looped",)):
     wl = WORKLOADS[name]
     cfg, B, P, cap = wl["model"], wl["batch"], wl["context"], wl["capacity"]
     say(f"[{name}] generating inputs")
@@ -30,33 +32,42 @@ def run_workload(name, sample):
     kv = KvCache(cfg, B, cap, k_host=K0, v_host=V0)
     toks = torch.from_numpy(tokens).cuda()
     pos = torch.full((B,), P, dtype=torch.int32, device="cuda")
-    logits = torch.empty((B, cfg["vocab"]), device="cuda")
-    hidden = torch.empty((B, cfg["hidden"]), device="cuda")
-    say(f"[{name}] GPU step (looped)")
-    model.step(toks, pos, kv, logits, hidden, kb.KL_MODE_LOOPED)
-    torch.cuda.synchronize()
-    assert model.device_error() == 0
-    lg, hd = logits.cpu().numpy(), hidden.cpu().numpy()
-    K, V = kv.host()
+    outs = {}
+    for m in modes:
+        logits = torch.full((B, cfg["vocab"]), float("nan"), device="cuda")
+        hidden = torch.full((B, cfg["hidden"]), float("nan"), device="cuda")
+        # (slot P of every layer is reset before each schedule, so each one's
+        # writes are seen on their own)
+        kv.k[:, :, :, P].zero_()
+        kv.v[:, :, :, P].zero_()
+        say(f"[{name}] GPU step ({m})")
+        model.step(toks, pos, kv, logits, hidden, kb.MODES[m])
+        torch.cuda.synchronize()
+        assert model.device_error() == 0
+        outs[m] = (logits.cpu().numpy(), hidden.cpu().numpy(),
+                   kv.k[:, :, :, P].cpu().numpy().view(np.uint16),
+                   kv.v[:, :, :, P].cpu().numpy().view(np.uint16))
     model.close()
     del kv
     torch.cuda.empty_cache()
-    errs = {}
+    for m in modes[1:]:
+        for x, y, what in zip(outs[modes[0]], outs[m], ("logits", "hidden", "K slot", "V slot")):
+            assert np.array_equal(x.view(np.uint8), y.view(np.uint8)), \
+                f"{what}: {m} differs from {modes[0]}"
+        say(f"[{name}] {m} == {modes[0]} bit for bit")
+    lg, hd, Kp, Vp = outs[modes[0]]
+    errs, elem = {}, {}
     for b in sample:
         say(f"[{name}] oracle, sequence {b}")
         Kb, Vb = K0[:, b:b + 1].copy(), V0[:, b:b + 1].copy()
         rl, rh = oracle.decode_step(cfg, weights, tokens[b:b + 1], [P], Kb, Vb, nthreads=16)
-        errs[f"logits[{b}]"] = oracle.rel_l2(lg[b], rl[0])
-        errs[f"hidden[{b}]"] = oracle.rel_l2(hd[b], rh[0])
-        errs[f"k_slot[{b}]"] = bf16_rel_l2(K[:, b, :, P], Kb[:, 0, :, P])
-        errs[f"v_slot[{b}]"] = bf16_rel_l2(V[:, b, :, P], Vb[:, 0, :, P])
-    say("  errors: " + ", ".join(f"{k}={v:.2e}" for k, v in errs.items()))
-    for k, v in errs.items():
-        assert v <= REL_L2_TOL, f"{k}: rel L2 {v:.3e} > {REL_L2_TOL}"
+        compare_sequence(errs, elem, f"[{b}]", lg[b], rl[0], hd[b], rh[0], Kp[:, b], Kb[:, 0, :, P],
+                         Vp[:, b], Vb[:, 0, :, P])
+    check_vectors(errs, elem)
 
 
-def test_llama8b_batch1_ctx4096_full_model():
-    run_workload("llama8b-b1-ctx4096", [0])
+def test_llama8b_batch1_ctx4096_full_model_all_schedules():
+    run_workload("llama8b-b1-ctx4096", [0], modes=("looped", "per_layer", "per_op"))
 
 
 def test_llama8b_batch1_ctx65536_full_model():

@@ -109,7 +109,46 @@ def test_rope_identity_at_position_zero(d, theta):
 def test_rope_is_complex_rotation(d, theta, pos):
     y = RNG.standard_normal(d)
     ref = bruteforce.rotate(y[None, :], pos, theta)[0]
-    np.testing.assert_allclose(oracle.rope(y, theta, pos), ref, rtol=1e-12, atol=1e-12)
+    # the angle pos * omega carries a rounding error of up to a few pos 2^-53
+    # radians (two ways of forming omega in double), so the bound grows with pos
+    atol = 1e-12 + 8.0 * pos * 2.0 ** -53 * np.abs(y).max()
+    np.testing.assert_allclose(oracle.rope(y, theta, pos), ref, rtol=1e-12, atol=atol)
+
+
+# cos 1 and sin 1 (radians), printed constants
+COS1, SIN1 = 0.5403023058681398, 0.8414709848078965
+
+
+@pytest.mark.parametrize("i", [0, 1, 2, 3])
+def test_rope_closed_form_frequencies_and_pairing(i):
+    # d = 8, theta = 10^4: pair i has frequency theta^(-2i/d) = 10^-i, so the
+    # unit vector e_i at position 10^i turns by exactly 1 radian into the
+    # plane of its partner e_(i + d/2) (half-split pairing):
+    #   e_i -> cos 1 e_i + sin 1 e_(i+4),   e_(i+4) -> -sin 1 e_i + cos 1 e_(i+4).
+    # An interleaved pairing, another exponent or a flipped sign fails this.
+    d, p = 8, 10 ** i
+    e = np.zeros(d)
+    e[i] = 1.0
+    want = np.zeros(d)
+    want[i], want[i + 4] = COS1, SIN1
+    np.testing.assert_allclose(oracle.rope(e, 1e4, p), want, rtol=0, atol=1e-12)
+    e = np.zeros(d)
+    e[i + 4] = 1.0
+    want = np.zeros(d)
+    want[i], want[i + 4] = -SIN1, COS1
+    np.testing.assert_allclose(oracle.rope(e, 1e4, p), want, rtol=0, atol=1e-12)
+
+
+def test_rope_first_pair_turns_by_the_position_at_any_theta():
+    # pair 0 has frequency theta^0 = 1 whatever theta and d are:
+    # e_0 at position 3 -> cos 3 e_0 + sin 3 e_(d/2) (printed constants)
+    for d, theta in ((64, 10000.0), (128, 500000.0)):
+        e = np.zeros(d)
+        e[0] = 1.0
+        got = oracle.rope(e, theta, 3)
+        assert got[0] == pytest.approx(-0.9899924966004454, abs=1e-13)
+        assert got[d // 2] == pytest.approx(0.1411200080598672, abs=1e-13)
+        assert np.count_nonzero(got) == 2
 
 
 def test_rope_preserves_norm_and_relative_position():
