@@ -110,6 +110,9 @@ typedef struct {
                                    on the matrix cores                             */
     int64_t arena_bytes;        /* packed weights + gains                          */
     int64_t scratch_bytes;      /* activations, partials, counters                 */
+    int64_t noalloc_scratch_bytes;  /* scratch a kl_decode_step_noalloc call at
+                                       max_batch needs                             */
+    int64_t noalloc_scratch_limit;  /* bytes of the static scratch                  */
 } kl_info;
 
 /* Load a model: validates cfg, allocates the packed weight arena, the RoPE
@@ -169,6 +172,24 @@ kl_status kl_model_set_globals(kl_state *st, const void *embed, const void *fina
 kl_status kl_decode_step(kl_state *st, const int32_t *token_ids, const int32_t *positions,
                          int32_t batch, const kl_kv_cache *kv, float *logits_out,
                          float *hidden_out, void *stream, int32_t mode);
+
+/* kl_decode_step for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation):
+ * the same arguments, results and errors, bit-identical outputs, and it calls
+ * no allocating routine.  Its step scratch is not the state's but a static
+ * array of the library, one per device, of kl_info.noalloc_scratch_limit bytes
+ * (32 MiB), held until the process ends; a step that needs more (see
+ * kl_info.noalloc_scratch_bytes: e.g. the 70B shape at batch >= 8) returns
+ * KL_ERR_UNSUPPORTED with nothing enqueued.  Each call first clears the
+ * scratch it uses with a fill kernel on 'stream' (one extra launch), so no
+ * state carries over from an earlier call.  Every call on a device shares
+ * that device's array: calls that may overlap in time on one device (other
+ * streams, other threads, other states) race and must be serialized by the
+ * caller. */
+kl_status kl_decode_step_noalloc(kl_state *st, const int32_t *token_ids,
+                                 const int32_t *positions, int32_t batch, const kl_kv_cache *kv,
+                                 float *logits_out, float *hidden_out, void *stream,
+                                 int32_t mode);
 
 /* Bytes of ONE of the K or V buffers for the given batch and capacity
  * (0 if cfg is invalid). */

@@ -30,7 +30,8 @@ KL_DEVERR_POSITION = 2
 KL_DEVERR_BARRIER = 4
 
 EXPORTED = ["kl_load_model", "kl_model_create", "kl_model_set_layer", "kl_model_set_globals",
-            "kl_decode_step", "kl_kv_cache_bytes", "kl_get_device_error",
+            "kl_decode_step", "kl_decode_step_noalloc", "kl_kv_cache_bytes",
+            "kl_get_device_error",
             "kl_get_info", "kl_set_trace", "kl_free_model", "kl_last_error"]
 
 
@@ -64,7 +65,9 @@ class kl_info(ctypes.Structure):
     _fields_ = [("n_workgroups", ctypes.c_int32), ("threads_per_group", ctypes.c_int32),
                 ("lds_bytes", ctypes.c_int32), ("attn_chunks_b1", ctypes.c_int32),
                 ("mfma_min_batch", ctypes.c_int32),
-                ("arena_bytes", ctypes.c_int64), ("scratch_bytes", ctypes.c_int64)]
+                ("arena_bytes", ctypes.c_int64), ("scratch_bytes", ctypes.c_int64),
+                ("noalloc_scratch_bytes", ctypes.c_int64),
+                ("noalloc_scratch_limit", ctypes.c_int64)]
 
 
 class KlError(RuntimeError):
@@ -97,6 +100,9 @@ def lib():
     L.kl_model_set_globals.restype = i32
     L.kl_decode_step.argtypes = [vp, vp, vp, i32, ctypes.POINTER(kl_kv_cache), vp, vp, vp, i32]
     L.kl_decode_step.restype = i32
+    L.kl_decode_step_noalloc.argtypes = [vp, vp, vp, i32, ctypes.POINTER(kl_kv_cache), vp, vp, vp,
+                                         i32]
+    L.kl_decode_step_noalloc.restype = i32
     L.kl_kv_cache_bytes.argtypes = [ctypes.POINTER(kl_config), i32, i32]
     L.kl_kv_cache_bytes.restype = ctypes.c_size_t
     L.kl_get_device_error.argtypes = [vp, ctypes.POINTER(i32)]
@@ -164,6 +170,14 @@ def kl_decode_step(state: int, token_ids: int, positions: int, batch: int, k: in
     kv = kl_kv_cache(k, v, kv_batch, capacity)
     _check(lib().kl_decode_step(state, token_ids, positions, batch, ctypes.byref(kv), logits_out,
                                 hidden_out, stream, mode))
+
+
+def kl_decode_step_noalloc(state: int, token_ids: int, positions: int, batch: int, k: int,
+                           v: int, kv_batch: int, capacity: int, logits_out: int,
+                           hidden_out: int | None, stream: int, mode: int) -> None:
+    kv = kl_kv_cache(k, v, kv_batch, capacity)
+    _check(lib().kl_decode_step_noalloc(state, token_ids, positions, batch, ctypes.byref(kv),
+                                        logits_out, hidden_out, stream, mode))
 
 
 def kl_kv_cache_bytes(cfg: kl_config, batch: int, capacity: int) -> int:

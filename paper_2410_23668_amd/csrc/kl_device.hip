@@ -2,10 +2,55 @@
 // launchers, and the load-time packing kernels.
 
 #include <algorithm>
+#include <mutex>
+#include <unordered_map>
 
 #include "kl_step_impl.h"
 
 namespace kl {
+
+// The scratch of the entry point that allocates nothing
+// (kl_decode_step_noalloc): a file-scope device array, one copy per device
+// that loads this library, kept until the process ends.  In host code its name
+// stands for no device address: host code uses only the address
+// static_scratch_address returns.
+static __device__ __align__(256) uint8_t scratch[kStaticScratchBytes];
+
+hipError_t static_scratch_address(int device, uint8_t **out) {
+    static std::mutex mu;
+    static std::unordered_map<int, uint8_t *> addr;   // device -> its copy's address
+    std::lock_guard<std::mutex> lock(mu);
+    const auto it = addr.find(device);
+    if (it != addr.end()) {
+        *out = it->second;
+        return hipSuccess;
+    }
+    int cur = -1;
+    hipError_t e = hipGetDevice(&cur);
+    if (e != hipSuccess) return e;
+    if (cur != device) return hipErrorInvalidDevice;
+    void *p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    addr[device] = static_cast<uint8_t *>(p);
+    *out = static_cast<uint8_t *>(p);
+    return hipSuccess;
+}
+
+__global__ void kl_zero_kernel(u32x4 *p, size_t n) {
+    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+         i += (size_t)gridDim.x * blockDim.x)
+        p[i] = u32x4{0u, 0u, 0u, 0u};
+}
+
+hipError_t launch_zero(void *p, size_t bytes, hipStream_t stream) {
+    const size_t n = bytes / 16;
+    if (n == 0) return hipSuccess;
+    const int blocks = (int)std::min<size_t>((n + 255) / 256, 4096);
+    hipLaunchKernelGGL(kl_zero_kernel, dim3(blocks), dim3(256), 0, stream,
+                       reinterpret_cast<u32x4 *>(p), n);
+    return hipGetLastError();
+}
 
 // The instance for a model's head_dim, query heads per KV head (the host has
 // validated both) and the batch regime (matrix cores at batch >= kMfmaBatch);

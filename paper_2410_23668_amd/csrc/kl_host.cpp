@@ -26,17 +26,13 @@ struct kl_state {
     uint8_t *arena;
     size_t arena_bytes;
     float2 *rope;
-    uint8_t *scratch;
+    uint8_t *scratch;                 // step scratch laid out by plan_scratch(max_batch)
     size_t scratch_bytes;
-    long long *xf, *xf2;
-    float *q, *m, *part_o, *part_s, *xpart, *gpart, *ssp;
+    uint8_t *static_scratch;          // this device's address of the library's static scratch
     int KSo, KSd, KSg, KSq;           // K slices of the batched O, down, gate/up, q/k/v products
-    uint16_t *act, *act_lo, *actm, *actm_lo, *acto, *acto_lo;
     int Sg, Sc, Rc, KTc;
-    unsigned long long *bar;
-    unsigned *cnt;
-    int *err;
-    uint8_t *dummy;
+    int *err;                         // device error word (its own allocation)
+    size_t off_dummy;                 // arena offset of a zero tile (the load rings' spare loads)
     unsigned long long *trace;
     int trace_max;
     int32_t *rowmaps;                 // device row maps used by set_layer / set_globals
@@ -180,11 +176,100 @@ void lds_layout_for(kl_state &s) {
     s.lds_bytes = (s.lds_bar + 2 * kBarGroups) * (int)sizeof(float);
 }
 
+// Step scratch for a batch of B sequences (byte offsets from its base; every
+// region 256-byte aligned):
+//   grid barrier counters (16 groups, 256 B apart) and the local counters:
+//     qkv and attention per KV head, gate/up per FFN column block, and at
+//     B >= kMfmaBatch the batched RMSNorm slice counters (256 bytes apart);
+//   the residual stream, int64 fixed point [B][Hp];
+//   rotated queries [B][nq d] (GEMV path: reused for the merged attention
+//     output);
+//   the SwiGLU output [B][Fp] (padding columns read as zero);
+//   attention chunk partials: outputs [B nkv C][group][d], (max, sum) pairs;
+//   the matrix-core path's two-term bf16 activations (both terms, [B][Hp],
+//     [B][Fp], [B][nq d]);
+//   at B >= kMfmaBatch also: the second residual buffer, the fp32 K-slice
+//     partials of the O and down projections [slices][B][Hp] and of the
+//     gate/up or q/k/v product (never live at the same time), and the
+//     RMSNorm sums of squares per kGemmChunkK columns [B][slices].
+struct ScratchPlan {
+    int B;
+    bool batched;
+    size_t off_bar, off_cnt, off_cnt_end;
+    size_t off_x, off_q, off_m, off_po, off_ps, off_act, off_actm, off_acto;
+    size_t off_x2, off_xp, off_gp, off_ss;
+    size_t total;
+};
+
+ScratchPlan plan_scratch(const kl_state &S, int B) {
+    const kl_config &c = S.cfg;
+    const int d = c.head_dim, g = c.n_heads / c.n_kv_heads, nkv = c.n_kv_heads;
+    ScratchPlan p{};
+    p.B = B;
+    p.batched = B >= kMfmaBatch;
+    size_t so = 0;
+    auto take = [&](size_t bytes) {
+        const size_t o = so;
+        so = align_up(so + bytes, 256);
+        return o;
+    };
+    const int nslices = (S.Hp + kGemmChunkK - 1) / kGemmChunkK;
+    const int norm_cnts = p.batched ? kNormCntStride * nslices : 0;
+    p.off_bar = take(kBarBytes);
+    p.off_cnt = take((size_t)(2 * nkv + S.Sc + norm_cnts) * 4);
+    p.off_cnt_end = so;
+    const size_t items = (size_t)nkv * std::max(B, S.Sg);   // >= B * nkv * C for this batch
+    p.off_x = take((size_t)B * S.Hp * 8);
+    p.off_q = take((size_t)B * c.n_heads * d * 4);
+    p.off_m = take((size_t)B * S.Fp * 4);
+    p.off_po = take(items * g * d * 4);
+    p.off_ps = take(items * g * 2 * 4);
+    p.off_act = take((size_t)B * S.Hp * 2 * 2);
+    p.off_actm = take((size_t)B * S.Fp * 2 * 2);
+    p.off_acto = take((size_t)B * S.Ap * 2 * 2);
+    if (p.batched) {
+        const size_t qkv_rows = (size_t)nkv * S.qkv_rg * kTileRows;
+        p.off_x2 = take((size_t)B * S.Hp * 8);
+        p.off_xp = take((size_t)std::max(S.KSo, S.KSd) * B * S.Hp * 4);
+        p.off_gp = take(std::max((size_t)S.KSg * B * S.gu_rg * kTileRows,
+                                 (size_t)S.KSq * B * qkv_rows) * 4);
+        p.off_ss = take((size_t)B * nslices * 4);
+    }
+    p.total = so;
+    return p;
+}
+
+// Points the step's scratch fields at the regions of 'plan' inside 'base'.
+void bind_scratch(StepParams &P, uint8_t *base, const ScratchPlan &p, const kl_state &S) {
+    const int B = p.B;
+    P.bar = reinterpret_cast<unsigned long long *>(base + p.off_bar);
+    P.cnt = reinterpret_cast<unsigned *>(base + p.off_cnt);
+    P.xf = reinterpret_cast<long long *>(base + p.off_x);
+    P.q = reinterpret_cast<float *>(base + p.off_q);
+    P.m = reinterpret_cast<float *>(base + p.off_m);
+    P.part_o = reinterpret_cast<float *>(base + p.off_po);
+    P.part_s = reinterpret_cast<float *>(base + p.off_ps);
+    P.act = reinterpret_cast<uint16_t *>(base + p.off_act);
+    P.act_lo = P.act + (size_t)B * S.Hp;
+    P.actm = reinterpret_cast<uint16_t *>(base + p.off_actm);
+    P.actm_lo = P.actm + (size_t)B * S.Fp;
+    P.acto = reinterpret_cast<uint16_t *>(base + p.off_acto);
+    P.acto_lo = P.acto + (size_t)B * S.Ap;
+    P.xf2 = p.batched ? reinterpret_cast<long long *>(base + p.off_x2) : nullptr;
+    P.xpart = p.batched ? reinterpret_cast<float *>(base + p.off_xp) : nullptr;
+    P.gpart = p.batched ? reinterpret_cast<float *>(base + p.off_gp) : nullptr;
+    P.ssp = p.batched ? reinterpret_cast<float *>(base + p.off_ss) : nullptr;
+    P.xpart_stride = B * S.Hp;
+    P.gpart_stride = B * S.gu_rg * kTileRows;
+    P.qpart_stride = B * S.cfg.n_kv_heads * S.qkv_rg * kTileRows;
+}
+
 void free_state(kl_state *s) {
     if (!s) return;
     if (s->arena) (void)hipFree(s->arena);
     if (s->rope) (void)hipFree(s->rope);
     if (s->scratch) (void)hipFree(s->scratch);
+    if (s->err) (void)hipFree(s->err);
     if (s->rowmaps) (void)hipFree(s->rowmaps);
     delete s;
 }
@@ -231,15 +316,9 @@ StepParams base_params(const kl_state &s) {
     P.final_norm = reinterpret_cast<const float *>(s.arena + s.off_final_norm);
     P.lm_head = reinterpret_cast<const uint16_t *>(s.arena + s.off_lm_head);
     P.rope = s.rope;
-    P.xf = s.xf; P.xf2 = s.xf2; P.xpart = s.xpart; P.xpart_stride = c.max_batch * s.Hp;
     P.KSo = s.KSo; P.KSd = s.KSd; P.KSg = s.KSg; P.KSq = s.KSq;
-    P.gpart = s.gpart; P.gpart_stride = c.max_batch * s.gu_rg * kTileRows;
-    P.qpart_stride = c.max_batch * c.n_kv_heads * s.qkv_rg * kTileRows;
-    P.ssp = s.ssp;
-    P.q = s.q; P.m = s.m; P.part_o = s.part_o; P.part_s = s.part_s; P.act = s.act;
-    P.act_lo = s.act_lo; P.actm = s.actm; P.actm_lo = s.actm_lo; P.acto = s.acto;
-    P.acto_lo = s.acto_lo;
-    P.bar = s.bar; P.cnt = s.cnt; P.err = s.err; P.dummy = s.dummy;
+    P.err = s.err;
+    P.dummy = s.arena + s.off_dummy;
     P.nwg = s.nwg;
     P.lds_red = s.lds_red; P.lds_sm = s.lds_sm; P.lds_bar = s.lds_bar;
     P.trace = s.trace;
@@ -336,6 +415,7 @@ kl_status kl_model_create(const kl_config *cfg, kl_state **out) {
     S->off_final_norm = off; off = align_up(off + S->Hp * 4, A);
     S->off_lm_head = off;    off = align_up(off + (size_t)S->head_rg * KTH * kTileBytes, A);
     S->off_embed = off;      off = align_up(off + (size_t)c.vocab * c.hidden * 2, A);
+    S->off_dummy = off;      off = align_up(off + kTileBytes, A);
     S->arena_bytes = off;
     TRY(hipMalloc(&S->arena, S->arena_bytes));
 
@@ -347,70 +427,23 @@ kl_status kl_model_create(const kl_config *cfg, kl_state **out) {
     TRY(step_kernel_setup(c.head_dim, c.n_heads / c.n_kv_heads, S->lds_bytes, &per_cu));
     if (per_cu < 1) return bail(fail(KL_ERR_UNSUPPORTED, "step kernel does not fit on a CU"));
 
-    // scratch
-    const int B = c.max_batch, nkv = c.n_kv_heads;
-    const size_t items = (size_t)nkv * std::max(B, S->Sg);   // >= B * nkv * C for every batch
-    size_t so = 0;
-    const size_t off_x = so;    so = align_up(so + (size_t)B * S->Hp * 8, 256);
-    const size_t off_q = so;    so = align_up(so + (size_t)B * c.n_heads * d * 4, 256);
-    const size_t off_m = so;    so = align_up(so + (size_t)B * S->Fp * 4, 256);
-    const size_t off_po = so;   so = align_up(so + items * g * d * 4, 256);
-    const size_t off_ps = so;   so = align_up(so + items * g * 2 * 4, 256);
-    const size_t off_act = so;  so = align_up(so + (size_t)B * S->Hp * 2 * 2, 256);
-    const size_t off_actm = so; so = align_up(so + (size_t)B * S->Fp * 2 * 2, 256);
-    const size_t off_acto = so; so = align_up(so + (size_t)B * S->Ap * 2 * 2, 256);
-    const size_t off_bar = so;  so = align_up(so + kBarBytes, 256);
-    // local counters: qkv and attention per KV head, gate/up per FFN column
-    // block, batched RMSNorm per 512-column slice (256 bytes apart; batched
-    // path only)
-    const int norm_cnts = B >= kMfmaBatch ? kNormCntStride * ((S->Hp + kGemmChunkK - 1) / kGemmChunkK) : 0;
-    const size_t off_cnt = so;
-    so = align_up(so + (size_t)(2 * nkv + S->Sc + norm_cnts) * 4, 256);
-    const size_t off_err = so;  so = align_up(so + 256, 256);
-    const size_t off_dummy = so; so = align_up(so + kTileBytes, 256);
-    // batched path: the second residual buffer and the K-slice partial sums
-    // of the O and down projections (folded by the next RMSNorm step), of the
-    // gate/up product (folded by the SwiGLU step) and of the q/k/v product
-    // (folded with the RoPE and the KV-cache append)
+    // K slices of the batched products (they depend on the grid, not on the batch)
+    const int nkv = c.n_kv_heads;
     const int qkv_rows = nkv * S->qkv_rg * kTileRows;
     S->KSo = batched_k_slices(nkv, KTO, S->o_rg / 2, S->nwg);
     S->KSd = batched_k_slices(S->Sc, S->KTc, S->down_rg / 2, S->nwg);
     S->KSg = batched_k_slices(KTH, 1, S->gu_rg / 2, S->nwg);
     S->KSq = batched_k_slices(KTH, 1, qkv_rows / 16, S->nwg);
-    const bool batched = B >= kMfmaBatch;
-    const size_t off_x2 = so;
-    if (batched) so = align_up(so + (size_t)B * S->Hp * 8, 256);
-    const size_t off_xp = so;
-    if (batched) so = align_up(so + (size_t)std::max(S->KSo, S->KSd) * B * S->Hp * 4, 256);
-    const size_t off_gp = so;
-    if (batched)
-        so = align_up(so + std::max((size_t)S->KSg * B * S->gu_rg * kTileRows,
-                                    (size_t)S->KSq * B * qkv_rows) * 4, 256);
-    const size_t off_ss = so;
-    if (batched)
-        so = align_up(so + (size_t)B * ((S->Hp + kGemmChunkK - 1) / kGemmChunkK) * 4, 256);
-    S->scratch_bytes = so;
+
+    // step scratch for the largest batch, zeroed; the device error word
+    S->scratch_bytes = plan_scratch(*S, c.max_batch).total;
     TRY(hipMalloc(&S->scratch, S->scratch_bytes));
     TRY(hipMemsetAsync(S->scratch, 0, S->scratch_bytes, s));
-    S->xf = reinterpret_cast<long long *>(S->scratch + off_x);
-    S->q = reinterpret_cast<float *>(S->scratch + off_q);
-    S->m = reinterpret_cast<float *>(S->scratch + off_m);
-    S->part_o = reinterpret_cast<float *>(S->scratch + off_po);
-    S->part_s = reinterpret_cast<float *>(S->scratch + off_ps);
-    S->act = reinterpret_cast<uint16_t *>(S->scratch + off_act);
-    S->act_lo = S->act + (size_t)B * S->Hp;
-    S->actm = reinterpret_cast<uint16_t *>(S->scratch + off_actm);
-    S->actm_lo = S->actm + (size_t)B * S->Fp;
-    S->acto = reinterpret_cast<uint16_t *>(S->scratch + off_acto);
-    S->acto_lo = S->acto + (size_t)B * S->Ap;
-    S->bar = reinterpret_cast<unsigned long long *>(S->scratch + off_bar);
-    S->cnt = reinterpret_cast<unsigned *>(S->scratch + off_cnt);
-    S->err = reinterpret_cast<int *>(S->scratch + off_err);
-    S->dummy = S->scratch + off_dummy;
-    S->xf2 = batched ? reinterpret_cast<long long *>(S->scratch + off_x2) : nullptr;
-    S->xpart = batched ? reinterpret_cast<float *>(S->scratch + off_xp) : nullptr;
-    S->gpart = batched ? reinterpret_cast<float *>(S->scratch + off_gp) : nullptr;
-    S->ssp = batched ? reinterpret_cast<float *>(S->scratch + off_ss) : nullptr;
+    TRY(hipMalloc(&S->err, 256));
+    TRY(hipMemsetAsync(S->err, 0, 256, s));
+    // this device's copy of the library's static scratch (the entry point
+    // that allocates nothing), resolved once per device
+    TRY(static_scratch_address(S->device, &S->static_scratch));
 
     // RoPE table (cos, sin) of pos * theta^(-2i/d), computed in double
     {
@@ -561,9 +594,12 @@ kl_status kl_load_model(const kl_config *cfg, const kl_weight_ptrs *w, void *str
     return KL_OK;
 }
 
-kl_status kl_decode_step(kl_state *st, const int32_t *token_ids, const int32_t *positions,
-                         int32_t batch, const kl_kv_cache *kv, float *logits_out,
-                         float *hidden_out, void *stream, int32_t mode) {
+// One decode step: validation, the scratch binding, the launches of 'mode'.
+// With no_alloc the step's scratch is the library's static scratch of this
+// device (cleared first by a fill kernel on the stream), else the state's.
+static kl_status enqueue_step(kl_state *st, const int32_t *token_ids, const int32_t *positions,
+                              int32_t batch, const kl_kv_cache *kv, float *logits_out,
+                              float *hidden_out, void *stream, int32_t mode, bool no_alloc) {
     g_last_error.clear();
     if (!st) return fail(KL_ERR_INVALID_ARGUMENT, "state is NULL");
     if (!token_ids || !positions || !logits_out || !kv || !kv->k || !kv->v)
@@ -591,7 +627,23 @@ kl_status kl_decode_step(kl_state *st, const int32_t *token_ids, const int32_t *
         return fail(KL_ERR_INVALID_ARGUMENT, "current device %d is not the model's device %d",
                     dev, st->device);
 
+    ScratchPlan plan;
+    uint8_t *base;
+    if (no_alloc) {
+        plan = plan_scratch(*st, batch);
+        if (plan.total > kStaticScratchBytes)
+            return fail(KL_ERR_UNSUPPORTED,
+                        "this step needs %zu bytes of scratch; the static scratch holds %zu "
+                        "(use kl_decode_step)", plan.total, kStaticScratchBytes);
+        if (!st->static_scratch)
+            return fail(KL_ERR_HIP, "the static scratch of device %d is not resolved", st->device);
+        base = st->static_scratch;
+    } else {
+        plan = plan_scratch(*st, c.max_batch);
+        base = st->scratch;
+    }
     StepParams P = base_params(*st);
+    bind_scratch(P, base, plan, *st);
     P.tokens = token_ids; P.positions = positions; P.B = batch;
     P.kc = reinterpret_cast<uint16_t *>(kv->k); P.vc = reinterpret_cast<uint16_t *>(kv->v);
     P.kv_batch = kv->batch; P.cap = kv->capacity;
@@ -601,6 +653,9 @@ kl_status kl_decode_step(kl_state *st, const int32_t *token_ids, const int32_t *
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     const int L = c.n_layers, lds = st->lds_bytes;
     const bool bat = batch >= kMfmaBatch;
+    // (the static scratch holds whatever the last call on this device left:
+    // it starts from zero like a fresh allocation)
+    if (no_alloc) HIP_TRY(launch_zero(base, plan.total, s));
     if (mode == KL_MODE_LOOPED) {
         HIP_TRY(launch_step(P, 0, L, kPhEmbed | kPhLayer | kPhHead, true, lds, s));
     } else if (mode == KL_MODE_PER_LAYER) {
@@ -620,6 +675,21 @@ kl_status kl_decode_step(kl_state *st, const int32_t *token_ids, const int32_t *
     return KL_OK;
 }
 
+kl_status kl_decode_step(kl_state *st, const int32_t *token_ids, const int32_t *positions,
+                         int32_t batch, const kl_kv_cache *kv, float *logits_out,
+                         float *hidden_out, void *stream, int32_t mode) {
+    return enqueue_step(st, token_ids, positions, batch, kv, logits_out, hidden_out, stream, mode,
+                        false);
+}
+
+kl_status kl_decode_step_noalloc(kl_state *st, const int32_t *token_ids,
+                                 const int32_t *positions, int32_t batch, const kl_kv_cache *kv,
+                                 float *logits_out, float *hidden_out, void *stream,
+                                 int32_t mode) {
+    return enqueue_step(st, token_ids, positions, batch, kv, logits_out, hidden_out, stream, mode,
+                        true);
+}
+
 kl_status kl_get_device_error(kl_state *st, int32_t *code) {
     g_last_error.clear();
     if (!st || !code) return fail(KL_ERR_INVALID_ARGUMENT, "state and code must not be NULL");
@@ -631,8 +701,9 @@ kl_status kl_get_device_error(kl_state *st, int32_t *code) {
     HIP_TRY(hipMemset(st->err, 0, sizeof(int32_t)));
     if (v & KL_DEVERR_BARRIER) {
         // a timed-out barrier leaves its counters mid-count: start them afresh
-        HIP_TRY(hipMemset(st->bar, 0, kBarBytes));
-        HIP_TRY(hipMemset(st->cnt, 0, (size_t)(2 * st->cfg.n_kv_heads + st->Sc) * 4));
+        // (the static scratch is cleared by every call that uses it)
+        const ScratchPlan pl = plan_scratch(*st, st->cfg.max_batch);
+        HIP_TRY(hipMemset(st->scratch + pl.off_bar, 0, pl.off_cnt_end - pl.off_bar));
     }
     return fail(KL_ERR_DEVICE_FAULT, "device error word 0x%x", v);
 }
@@ -656,6 +727,8 @@ kl_status kl_get_info(const kl_state *st, kl_info *info) {
     info->mfma_min_batch = kMfmaBatch;
     info->arena_bytes = (int64_t)st->arena_bytes;
     info->scratch_bytes = (int64_t)st->scratch_bytes;
+    info->noalloc_scratch_bytes = (int64_t)plan_scratch(*st, st->cfg.max_batch).total;
+    info->noalloc_scratch_limit = (int64_t)kStaticScratchBytes;
     return KL_OK;
 }
 

@@ -121,6 +121,15 @@ hipError_t launch_step(const StepParams &p, int first_layer, int last_layer, int
                        bool cooperative, int lds_bytes, hipStream_t stream);
 hipError_t step_kernel_setup(int d, int group, int lds_bytes, int *max_blocks_per_cu);
 
+// The static scratch of kl_decode_step_noalloc: one array per device, of
+// this many bytes, held until the process ends.
+constexpr size_t kStaticScratchBytes = size_t(32) << 20;
+// This device's address of the static scratch ('device' must be current);
+// resolved with hipGetSymbolAddress once per device, then cached.
+hipError_t static_scratch_address(int device, uint8_t **out);
+// Zero 'bytes' (a multiple of 16, 16-byte aligned) at p with a fill kernel.
+hipError_t launch_zero(void *p, size_t bytes, hipStream_t stream);
+
 hipError_t launch_pack_rows(uint16_t *dst, int n_rg, int kt, int K, int ld, const int32_t *rowmap,
                             const uint16_t *src0, const uint16_t *src1, const uint16_t *src2,
                             hipStream_t stream);
