@@ -207,8 +207,9 @@ kl_status kl_get_info(const kl_state *st, kl_info *info);
  * order embed, then qkv, attn, oproj, gateup, down per layer, then head) and
  * workgroup w, s_memrealtime stamps (100 MHz ticks) into
  *   dev_buffer[(i * n_workgroups + w) * 4 + {0: phase end (every wave of the
- *   workgroup done, its writes complete), 1: start of the wait for its
- *   inputs, 2: end of that wait, 3: inputs staged (in LDS on the
+ *   workgroup done; its writes complete where the phase ends on a barrier,
+ *   issued where it hands tagged words to the next phase), 1: start of the
+ *   wait for its inputs, 2: end of that wait, 3: inputs staged (in LDS on the
  *   per-sequence path; batches of 8 or more: the workgroup's share of the
  *   grid-wide step before the product, RMSNorm or SwiGLU fold, done; an
  *   attention phase: its chunk result published)}]

@@ -62,31 +62,19 @@ StepKernel step_kernel_for(int d, int group, bool batched) {
 }
 
 // Repack row-major bf16 matrices (row stride ld elements) into 8x64 tiles of
-// their first K columns.  rowmap[packed row] = (source id << 28) | source
-// row, or -1 for a zero row; columns >= K are zero.
+// their first K columns, one 16-byte chunk per thread (pack_chunk: the row
+// map gives each packed row's source and row, columns >= K are zero).
 __global__ void kl_pack_rows_kernel(uint16_t *__restrict__ dst, int n_rg, int KT, int K, int ld,
                                     const int32_t *__restrict__ rowmap,
                                     const uint16_t *__restrict__ s0,
                                     const uint16_t *__restrict__ s1,
                                     const uint16_t *__restrict__ s2) {
     const size_t chunks = (size_t)n_rg * KT * 64;
+    const uint16_t *const src[3] = {s0, s1, s2};
     for (size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x; idx < chunks;
          idx += (size_t)gridDim.x * blockDim.x) {
-        const int lane = (int)(idx % 64);
-        const size_t tile = idx / 64;
-        const int kt = (int)(tile % KT), rg = (int)(tile / KT);
-        const int pr = rg * kTileRows + lane / 8, k = kt * kTileK + (lane % 8) * 8;
-        const int m = rowmap[pr];
-        unsigned w[4] = {0u, 0u, 0u, 0u};
-        if (m >= 0) {
-            const int sid = m >> 28, row = m & 0x0fffffff;
-            const uint16_t *src = (sid == 0 ? s0 : (sid == 1 ? s1 : s2)) + (size_t)row * ld;
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const unsigned v = (k + e < K) ? src[k + e] : 0u;
-                w[e >> 1] |= v << (16 * (e & 1));
-            }
-        }
+        uint32_t w[4];
+        pack_chunk(idx, KT, K, ld, rowmap, src, w);
         reinterpret_cast<u32x4 *>(dst)[idx] = u32x4{w[0], w[1], w[2], w[3]};
     }
 }

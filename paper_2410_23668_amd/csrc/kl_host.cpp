@@ -31,12 +31,13 @@ struct kl_state {
     uint8_t *static_scratch;          // this device's address of the library's static scratch
     int KSo, KSd, KSg, KSq;           // K slices of the batched O, down, gate/up, q/k/v products
     int Sg, Sc, Rc, KTc;
-    int *err;                         // device error word (its own allocation)
+    int *err;                         // device error word (its own allocation, 256 B)
+    unsigned *epoch;                  // first tag of the next step (in the same allocation)
     size_t off_dummy;                 // arena offset of a zero tile (the load rings' spare loads)
     unsigned long long *trace;
     int trace_max;
     int32_t *rowmaps;                 // device row maps used by set_layer / set_globals
-    const int32_t *map_qkv, *map_h, *map_gu, *map_head;
+    const int32_t *maps[4];           // by RowMap
     int nwg, lds_bytes;
     int lds_red, lds_sm, lds_bar;
 };
@@ -64,7 +65,6 @@ kl_status fail(kl_status s, const char *fmt, ...) {
     } while (0)
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
-int pad_k(int v) { return (v + kTileK - 1) / kTileK * kTileK; }
 
 bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
@@ -93,23 +93,6 @@ kl_status validate_config(const kl_config *c) {
     return KL_OK;
 }
 
-// Packed-row -> source-row maps, encoded (source id << 28) | row, -1 = zero row.
-// Q/K/V rows grouped by KV head g: the G query heads of g, then key head g,
-// then value head g; query and key rows in rotation pairs (i, i + d/2).
-std::vector<int32_t> qkv_rowmap(const kl_config &c) {
-    const int d = c.head_dim, half = d / 2, G = c.n_heads / c.n_kv_heads;
-    const auto pair = [&](int j) { return j / 2 + (j % 2) * half; };
-    std::vector<int32_t> m;
-    m.reserve((size_t)(c.n_heads + 2 * c.n_kv_heads) * d);
-    for (int g = 0; g < c.n_kv_heads; ++g) {
-        for (int h = g * G; h < (g + 1) * G; ++h)
-            for (int j = 0; j < d; ++j) m.push_back((0 << 28) | (h * d + pair(j)));
-        for (int j = 0; j < d; ++j) m.push_back((1 << 28) | (g * d + pair(j)));
-        for (int j = 0; j < d; ++j) m.push_back((2 << 28) | (g * d + j));
-    }
-    return m;
-}
-
 // FFN column blocks: the largest divisor of the k-tile count of ffn_dim that
 // is at most 32 (and at most the grid).
 int largest_divisor_at_most(int n, int cap) {
@@ -134,46 +117,26 @@ int batched_k_slices(int n, int t, int nblk, int nwg) {
     return best > 0 ? best : largest_divisor_at_most(n, kMaxKSlices);
 }
 
-int ffn_column_blocks(int ktf, int nwg) {
-    int best = 1;
-    for (int s = 1; s <= std::min(32, std::min(ktf, nwg)); ++s)
-        if (ktf % s == 0) best = s;
-    return best;
-}
-
-std::vector<int32_t> identity_rowmap(int rows, int padded_rows) {
-    std::vector<int32_t> m(padded_rows, -1);
-    for (int r = 0; r < rows; ++r) m[r] = r;
-    return m;
-}
-
-std::vector<int32_t> gateup_rowmap(int F) {
-    std::vector<int32_t> m(2 * F);
-    for (int i = 0; i < F; ++i) {
-        m[2 * i] = i;                  // gate row i
-        m[2 * i + 1] = (1 << 28) | i;  // up row i
-    }
-    return m;
-}
-
 // Dynamic LDS layout of the step kernel (offsets in floats): the activation
 // vector / attention area, the GEMV wave partials, 64 floats of small
 // reductions and flags, then the barrier bases.
 void lds_layout_for(kl_state &s) {
     const kl_config &c = s.cfg;
     const int g = c.n_heads / c.n_kv_heads, d = c.head_dim;
-    const int cmax = std::max(1, s.Sg);                        // chunks at batch 1
     const int sub = kWaves * kAttnLoads * (64 / (d / 8));      // positions per sub-chunk
-    const int attn_main = g * d + g * sub + g * 4 + kWaves * g * d;
-    const int oproj_stage = g * d + 3 * cmax * g + g;          // o + merge statistics
+    const int attn_main = g * d + g * sub + g * 4 + kWaves * g * d + d;   // + new key, value
+    // O projection: o, chunk weights, running sums, the chunk results
+    const int oproj_stage = d + kMergeChunks + 4 + kMergeChunks * (d + 2);
     int amax = std::max(2 * s.Hp + d, s.KTc * kTileK);   // activations, gain, RoPE row
+
     amax = std::max(amax, std::max(attn_main, oproj_stage));
     if (c.max_batch >= kMfmaBatch) amax = std::max(amax, kGemmLdsBytes / 4);   // batched path
     amax = (amax + 63) & ~63;
     s.lds_red = amax;
     s.lds_sm = s.lds_red + kWaves * kRgBatch * kTileRows;
     s.lds_bar = s.lds_sm + 64;
-    s.lds_bytes = (s.lds_bar + 2 * kBarGroups) * (int)sizeof(float);
+    // + the step's epoch, and position and validity per sequence
+    s.lds_bytes = (s.lds_bar + 2 * kBarGroups + 4 + 2 * kMfmaBatch) * (int)sizeof(float);
 }
 
 // Step scratch for a batch of B sequences (byte offsets from its base; every
@@ -182,10 +145,12 @@ void lds_layout_for(kl_state &s) {
 //     qkv and attention per KV head, gate/up per FFN column block, and at
 //     B >= kMfmaBatch the batched RMSNorm slice counters (256 bytes apart);
 //   the residual stream, int64 fixed point [B][Hp];
-//   rotated queries [B][nq d] (GEMV path: reused for the merged attention
-//     output);
-//   the SwiGLU output [B][Fp] (padding columns read as zero);
-//   attention chunk partials: outputs [B nkv C][group][d], (max, sum) pairs;
+//   the per-sequence path's tagged words (8 bytes each, for up to
+//     kMfmaBatch - 1 sequences): rotated queries [B][nq d], the new key and
+//     value [B][nkv][d], chunk results [B][nkv][group][C][d + 2], the SwiGLU
+//     output [B][Fp];
+//   the matrix-core path's rotated queries [B][nq d] and attention chunk
+//     partials: outputs [B nkv C][group][d], (max, sum) pairs;
 //   the matrix-core path's two-term bf16 activations (both terms, [B][Hp],
 //     [B][Fp], [B][nq d]);
 //   at B >= kMfmaBatch also: the second residual buffer, the fp32 K-slice
@@ -196,7 +161,8 @@ struct ScratchPlan {
     int B;
     bool batched;
     size_t off_bar, off_cnt, off_cnt_end;
-    size_t off_x, off_q, off_m, off_po, off_ps, off_act, off_actm, off_acto;
+    size_t off_x, off_q, off_po, off_ps, off_act, off_actm, off_acto;
+    size_t off_qll, off_kvll, off_poll, off_mll;
     size_t off_x2, off_xp, off_gp, off_ss;
     size_t total;
 };
@@ -220,8 +186,13 @@ ScratchPlan plan_scratch(const kl_state &S, int B) {
     p.off_cnt_end = so;
     const size_t items = (size_t)nkv * std::max(B, S.Sg);   // >= B * nkv * C for this batch
     p.off_x = take((size_t)B * S.Hp * 8);
+    const int bl = std::min(B, kMfmaBatch - 1);               // per-sequence steps
+    const size_t items_ll = (size_t)nkv * std::max(bl, S.Sg);
+    p.off_qll = take((size_t)bl * c.n_heads * d * 8);
+    p.off_kvll = take((size_t)bl * nkv * d * 8);
+    p.off_poll = take(items_ll * g * (d + 2) * 8);
+    p.off_mll = take((size_t)bl * S.Fp * 8);
     p.off_q = take((size_t)B * c.n_heads * d * 4);
-    p.off_m = take((size_t)B * S.Fp * 4);
     p.off_po = take(items * g * d * 4);
     p.off_ps = take(items * g * 2 * 4);
     p.off_act = take((size_t)B * S.Hp * 2 * 2);
@@ -246,7 +217,10 @@ void bind_scratch(StepParams &P, uint8_t *base, const ScratchPlan &p, const kl_s
     P.cnt = reinterpret_cast<unsigned *>(base + p.off_cnt);
     P.xf = reinterpret_cast<long long *>(base + p.off_x);
     P.q = reinterpret_cast<float *>(base + p.off_q);
-    P.m = reinterpret_cast<float *>(base + p.off_m);
+    P.q_ll = reinterpret_cast<unsigned long long *>(base + p.off_qll);
+    P.kv_ll = reinterpret_cast<unsigned long long *>(base + p.off_kvll);
+    P.po_ll = reinterpret_cast<unsigned long long *>(base + p.off_poll);
+    P.m_ll = reinterpret_cast<unsigned long long *>(base + p.off_mll);
     P.part_o = reinterpret_cast<float *>(base + p.off_po);
     P.part_s = reinterpret_cast<float *>(base + p.off_ps);
     P.act = reinterpret_cast<uint16_t *>(base + p.off_act);
@@ -318,6 +292,7 @@ StepParams base_params(const kl_state &s) {
     P.rope = s.rope;
     P.KSo = s.KSo; P.KSd = s.KSd; P.KSg = s.KSg; P.KSq = s.KSq;
     P.err = s.err;
+    P.epoch_ptr = s.epoch;
     P.dummy = s.arena + s.off_dummy;
     P.nwg = s.nwg;
     P.lds_red = s.lds_red; P.lds_sm = s.lds_sm; P.lds_bar = s.lds_bar;
@@ -377,46 +352,24 @@ kl_status kl_model_create(const kl_config *cfg, kl_state **out) {
     if (!coop) return bail(fail(KL_ERR_UNSUPPORTED, "device lacks cooperative launch"));
 
     const int d = c.head_dim, g = c.n_heads / c.n_kv_heads;
-    if (ncu < c.n_kv_heads)
-        return bail(fail(KL_ERR_UNSUPPORTED, "n_kv_heads %d exceeds the %d compute units",
-                         c.n_kv_heads, ncu));
+    // (the per-sequence O projection gives every query head workgroups of its own)
+    if (ncu < c.n_heads)
+        return bail(fail(KL_ERR_UNSUPPORTED, "n_heads %d exceeds the %d compute units",
+                         c.n_heads, ncu));
+    // the packed layout's geometry for this grid (one persistent workgroup per CU)
+    const Geometry Gm = layout_geometry(c, ncu);
     S->nwg = ncu;
-    S->Hp = pad_k(c.hidden);
-    S->Ap = pad_k(c.n_heads * d);
-    S->Fp = pad_k(c.ffn_dim);
-    const int vrows = (c.vocab + kTileRows - 1) / kTileRows * kTileRows;
-    const int KTH = S->Hp / kTileK, KTF = S->Fp / kTileK, KTO = g * d / kTileK;
-    S->Sg = S->nwg / c.n_kv_heads;
-    S->Sc = ffn_column_blocks(KTF, S->nwg);
-    S->Rc = S->nwg / S->Sc;
-    S->KTc = KTF / S->Sc;
-    S->qkv_rg = (g + 2) * d / kTileRows;
-    S->o_rg = c.hidden / kTileRows;
-    S->gu_rg = 2 * c.ffn_dim / kTileRows;
-    S->down_rg = c.hidden / kTileRows;
-    S->head_rg = vrows / kTileRows;
-
-    // arena: [layer 0 .. L-1][final_norm][lm_head][embed]; per layer the O
-    // projection is stored per KV head (its columns) and the down projection
-    // per FFN column block
-    const size_t A = 4096;
-    size_t off = 0;
-    S->off_attn_norm = off; off = align_up(off + S->Hp * 4, A);
-    S->off_ffn_norm = off;  off = align_up(off + S->Hp * 4, A);
-    S->off_qkv = off;
-    off = align_up(off + (size_t)c.n_kv_heads * S->qkv_rg * KTH * kTileBytes, A);
-    S->off_o = off;
-    off = align_up(off + (size_t)c.n_kv_heads * S->o_rg * KTO * kTileBytes, A);
-    S->off_gu = off;   off = align_up(off + (size_t)S->gu_rg * KTH * kTileBytes, A);
-    S->off_down = off;
-    off = align_up(off + (size_t)S->Sc * S->down_rg * S->KTc * kTileBytes, A);
-    S->layer_stride = off;
-    off = S->layer_stride * c.n_layers;
-    S->off_final_norm = off; off = align_up(off + S->Hp * 4, A);
-    S->off_lm_head = off;    off = align_up(off + (size_t)S->head_rg * KTH * kTileBytes, A);
-    S->off_embed = off;      off = align_up(off + (size_t)c.vocab * c.hidden * 2, A);
-    S->off_dummy = off;      off = align_up(off + kTileBytes, A);
-    S->arena_bytes = off;
+    S->Hp = Gm.Hp; S->Ap = Gm.Ap; S->Fp = Gm.Fp;
+    const int KTH = Gm.KTH, KTO = g * Gm.KTq;
+    S->Sg = Gm.Sg; S->Sc = Gm.Sc; S->Rc = Gm.Rc; S->KTc = Gm.KTc;
+    S->qkv_rg = Gm.qkv_rg; S->o_rg = Gm.o_rg; S->gu_rg = Gm.gu_rg; S->down_rg = Gm.down_rg;
+    S->head_rg = Gm.head_rg;
+    S->off_attn_norm = Gm.off_attn_norm; S->off_ffn_norm = Gm.off_ffn_norm;
+    S->off_qkv = Gm.off_qkv; S->off_o = Gm.off_o; S->off_gu = Gm.off_gu;
+    S->off_down = Gm.off_down; S->layer_stride = Gm.layer_stride;
+    S->off_final_norm = Gm.off_final_norm; S->off_lm_head = Gm.off_lm_head;
+    S->off_embed = Gm.off_embed; S->off_dummy = Gm.off_dummy;
+    S->arena_bytes = Gm.arena_bytes;
     TRY(hipMalloc(&S->arena, S->arena_bytes));
 
     // grid: one persistent workgroup per CU
@@ -441,6 +394,12 @@ kl_status kl_model_create(const kl_config *cfg, kl_state **out) {
     TRY(hipMemsetAsync(S->scratch, 0, S->scratch_bytes, s));
     TRY(hipMalloc(&S->err, 256));
     TRY(hipMemsetAsync(S->err, 0, 256, s));
+    S->epoch = reinterpret_cast<unsigned *>(reinterpret_cast<uint8_t *>(S->err) + 128);
+    {
+        const unsigned first_tag = 1;
+        TRY(hipMemcpyAsync(S->epoch, &first_tag, sizeof first_tag, hipMemcpyHostToDevice, s));
+        TRY(hipStreamSynchronize(s));
+    }
     // this device's copy of the library's static scratch (the entry point
     // that allocates nothing), resolved once per device
     TRY(static_scratch_address(S->device, &S->static_scratch));
@@ -466,24 +425,17 @@ kl_status kl_model_create(const kl_config *cfg, kl_state **out) {
 
     // row maps (the same for every layer), kept on the device for set_layer
     {
-        const int vrows = (c.vocab + kTileRows - 1) / kTileRows * kTileRows;
-        const std::vector<int32_t> m_qkv = qkv_rowmap(c),
-                                   m_h = identity_rowmap(c.hidden, c.hidden),
-                                   m_gu = gateup_rowmap(c.ffn_dim),
-                                   m_head = identity_rowmap(c.vocab, vrows);
-        const size_t nmap = m_qkv.size() + m_h.size() + m_gu.size() + m_head.size();
-        TRY(hipMalloc(&S->rowmaps, nmap * sizeof(int32_t)));
         std::vector<int32_t> all;
-        all.reserve(nmap);
-        all.insert(all.end(), m_qkv.begin(), m_qkv.end());
-        all.insert(all.end(), m_h.begin(), m_h.end());
-        all.insert(all.end(), m_gu.begin(), m_gu.end());
-        all.insert(all.end(), m_head.begin(), m_head.end());
-        TRY(hipMemcpy(S->rowmaps, all.data(), nmap * sizeof(int32_t), hipMemcpyHostToDevice));
-        S->map_qkv = S->rowmaps;
-        S->map_h = S->map_qkv + m_qkv.size();
-        S->map_gu = S->map_h + m_h.size();
-        S->map_head = S->map_gu + m_gu.size();
+        size_t at[4];
+        for (int m = 0; m < 4; ++m) {
+            const std::vector<int32_t> v = row_map(c, (RowMap)m);
+            at[m] = all.size();
+            all.insert(all.end(), v.begin(), v.end());
+        }
+        TRY(hipMalloc(&S->rowmaps, all.size() * sizeof(int32_t)));
+        TRY(hipMemcpy(S->rowmaps, all.data(), all.size() * sizeof(int32_t),
+                      hipMemcpyHostToDevice));
+        for (int m = 0; m < 4; ++m) S->maps[m] = S->rowmaps + at[m];
     }
     TRY(hipDeviceSynchronize());
 #undef TRY
@@ -500,8 +452,6 @@ kl_status kl_model_set_layer(kl_state *S, int32_t l, const kl_layer_ptrs *w, voi
     kl_status st = check_layer_ptrs(*w, l);
     if (st != KL_OK) return st;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    const int d = c.head_dim, g = c.n_heads / c.n_kv_heads;
-    const int KTH = S->Hp / kTileK, KTO = g * d / kTileK;
     const kl_layer_ptrs &Lw = *w;
     uint8_t *Lb = S->arena + (size_t)l * S->layer_stride;
     const auto u16 = [](const void *p) { return reinterpret_cast<const uint16_t *>(p); };
@@ -510,26 +460,15 @@ kl_status kl_model_set_layer(kl_state *S, int32_t l, const kl_layer_ptrs *w, voi
     if (pe == hipSuccess)
         pe = launch_gain_to_f32(reinterpret_cast<float *>(Lb + S->off_ffn_norm),
                                 u16(Lw.ffn_norm), c.hidden, S->Hp, s);
-    if (pe == hipSuccess)
-        pe = launch_pack_rows(reinterpret_cast<uint16_t *>(Lb + S->off_qkv),
-                              c.n_kv_heads * S->qkv_rg, KTH, c.hidden, c.hidden, S->map_qkv,
-                              u16(Lw.wq), u16(Lw.wk), u16(Lw.wv), s);
-    for (int kv = 0; kv < c.n_kv_heads && pe == hipSuccess; ++kv)   // Wo[:, head kv]
-        pe = launch_pack_rows(reinterpret_cast<uint16_t *>(Lb + S->off_o) +
-                                  (size_t)kv * S->o_rg * KTO * kTileBytes / 2,
-                              S->o_rg, KTO, g * d, c.n_heads * d, S->map_h,
-                              u16(Lw.wo) + (size_t)kv * g * d, nullptr, nullptr, s);
-    if (pe == hipSuccess)
-        pe = launch_pack_rows(reinterpret_cast<uint16_t *>(Lb + S->off_gu), S->gu_rg, KTH,
-                              c.hidden, c.hidden, S->map_gu, u16(Lw.w_gate), u16(Lw.w_up),
-                              nullptr, s);
-    for (int j = 0; j < S->Sc && pe == hipSuccess; ++j) {   // Wd[:, column block j]
-        const int c0 = j * S->KTc * kTileK;
-        pe = launch_pack_rows(reinterpret_cast<uint16_t *>(Lb + S->off_down) +
-                                  (size_t)j * S->down_rg * S->KTc * kTileBytes / 2,
-                              S->down_rg, S->KTc,
-                              std::max(0, std::min(c.ffn_dim - c0, S->KTc * kTileK)), c.ffn_dim,
-                              S->map_h, u16(Lw.w_down) + c0, nullptr, nullptr, s);
+    // the packed matrices of the layer (kl_layout.h: layer_pack_jobs)
+    const uint16_t *srcs[] = {u16(Lw.wq), u16(Lw.wk), u16(Lw.wv), u16(Lw.wo),
+                              u16(Lw.w_gate), u16(Lw.w_up), u16(Lw.w_down)};
+    for (const PackJob &J : layer_pack_jobs(c, layout_geometry(c, S->nwg))) {
+        if (pe != hipSuccess) break;
+        const uint16_t *p[3];
+        for (int k = 0; k < 3; ++k) p[k] = J.src[k] == kSrcNone ? nullptr : srcs[J.src[k]] + J.col0;
+        pe = launch_pack_rows(reinterpret_cast<uint16_t *>(Lb + J.dst), J.n_rg, J.KT, J.K, J.ld,
+                              S->maps[J.map], p[0], p[1], p[2], s);
     }
     if (pe != hipSuccess)
         return fail(KL_ERR_HIP, "packing layer %d failed: %s", l, hipGetErrorString(pe));
@@ -546,14 +485,16 @@ kl_status kl_model_set_globals(kl_state *S, const void *embed, const void *final
         return fail(KL_ERR_INVALID_ARGUMENT, "weight pointers must be 2-byte aligned");
     const kl_config &c = S->cfg;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    const int KTH = S->Hp / kTileK;
     hipError_t pe = launch_gain_to_f32(reinterpret_cast<float *>(S->arena + S->off_final_norm),
                                        reinterpret_cast<const uint16_t *>(final_norm), c.hidden,
                                        S->Hp, s);
-    if (pe == hipSuccess)
-        pe = launch_pack_rows(reinterpret_cast<uint16_t *>(S->arena + S->off_lm_head),
-                              S->head_rg, KTH, c.hidden, c.hidden, S->map_head,
-                              reinterpret_cast<const uint16_t *>(lm_head), nullptr, nullptr, s);
+    if (pe == hipSuccess) {
+        const PackJob J = head_pack_job(c, layout_geometry(c, S->nwg));
+        pe = launch_pack_rows(reinterpret_cast<uint16_t *>(S->arena + J.dst), J.n_rg, J.KT, J.K,
+                              J.ld, S->maps[J.map],
+                              reinterpret_cast<const uint16_t *>(lm_head) + J.col0, nullptr,
+                              nullptr, s);
+    }
     if (pe == hipSuccess)
         pe = hipMemcpyAsync(S->arena + S->off_embed, embed, (size_t)c.vocab * c.hidden * 2,
                             hipMemcpyDeviceToDevice, s);

@@ -3,6 +3,9 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+
+#include "kl_layout.h"
+#include "kl_sync.h"
 #include <stddef.h>
 #include <stdint.h>
 
@@ -12,9 +15,6 @@ namespace kl {
 constexpr int kWaves = 8;                 // compute waves per workgroup
 constexpr int kCtlWave = kWaves;          // the control wave: barriers and counters only
 constexpr int kThreads = (kWaves + 1) * 64;   // threads per workgroup
-constexpr int kTileRows = 8;              // rows of one packed weight tile
-constexpr int kTileK = 64;                // columns of one packed weight tile
-constexpr int kTileBytes = kTileRows * kTileK * 2;   // 1 KiB: one 16-byte load per lane
 constexpr int kRgBatch = 16;              // row groups reduced per LDS round
 constexpr int kAttnLoads = 5;             // K (and V) loads per lane per attention sub-chunk
 constexpr int kAttnLoadsPeel = 4;         // the same, batched kernel with up to 4 query heads per KV head
@@ -38,7 +38,9 @@ constexpr int kGemmActBytes = kGemmBatch * kActStride * 2;   // one term of one 
 constexpr int kGemmLdsBytes = 4 * kGemmActBytes + kWaves * 2048;
 constexpr int kNormCntStride = 64;        // words between batched RMSNorm slice counters
 constexpr int kMaxGroup = 8;              // max query heads per KV head
-constexpr int kBarGroups = 16;            // first level of the grid barrier
+constexpr int kMergeChunks = 32;          // attention chunk results merged per LDS round
+constexpr int kDownGather = 8;            // tagged words per control-wave lane per gather round
+constexpr int kBarGroups = kSyncBarGroups;   // first level of the grid barrier
 constexpr int kBarBytes = 8192;           // barrier counters: kBarGroups lines of 256 B
 
 // Phase selection bits of one launch of the step kernel.
@@ -91,10 +93,19 @@ struct StepParams {
     int KSg, KSq;              // K slices of the batched gate/up and q/k/v products
     float *ssp;                // batched path: sums of squares of the last RMSNorm step's
                                // rows per kGemmChunkK columns [max_batch][ceil(Hp / chunk)]
-    float *q;                  // [max_batch][nq*d] rotated queries
-    float *m;                  // [max_batch][Fp] SwiGLU output (padding stays 0)
-    float *part_o;             // attention chunk outputs [B*nkv*C][group*d]
-    float *part_s;             // attention chunk (max, sum) [B*nkv*C][group][2]
+    float *q;                  // batched path: [B][nq*d] rotated queries
+    float *part_o;             // batched path: attention chunk outputs [B*nkv*C][group*d]
+    float *part_s;             // batched path: attention chunk (max, sum) [B*nkv*C][group][2]
+    // per-sequence path (batch < kMfmaBatch): values handed between
+    // workgroups as tagged words (value in the low 32 bits, the tag of the
+    // writing step and layer in the high 32 bits)
+    unsigned *epoch_ptr;       // device word: the current step's first tag (layer l's tag
+                               // is *epoch_ptr + l; the step's last phase advances it)
+    unsigned long long *q_ll;  // [B][nq*d] rotated queries (fp32)
+    unsigned long long *kv_ll; // [B][nkv][d]: new key (d/2 words: bf16 dims i, i + d/2),
+                               // then new value (d/2 words: bf16 dims 2j, 2j + 1)
+    unsigned long long *po_ll; // [B][nkv][group][C][d + 2]: chunk outputs, then max and sum
+    unsigned long long *m_ll;  // [B][Fp] SwiGLU output (fp32)
     // batched path: activations as bf16 hi and lo terms (hi + lo ~ the fp32 value)
     uint16_t *act, *act_lo;    // [max_batch][Hp] normalised activations
     uint16_t *actm, *actm_lo;  // [max_batch][Fp] SwiGLU output

@@ -40,6 +40,15 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 // ---------------------------------------------------------------- helpers
 
+// The thread's index in its workgroup, opaque to the compiler at each use:
+// values derived from it are formed where they are used instead of being
+// hoisted out of the layer loop and kept live (or spilled) across the kernel.
+__device__ __forceinline__ unsigned kl_tid() {
+    unsigned t = __builtin_amdgcn_workitem_id_x();
+    asm volatile("" : "+v"(t));
+    return t;
+}
+
 __device__ __forceinline__ float bf_lo(unsigned u) { return __uint_as_float(u << 16); }
 __device__ __forceinline__ float bf_hi(unsigned u) { return __uint_as_float(u & 0xffff0000u); }
 __device__ __forceinline__ float bf2f(uint16_t h) { return __uint_as_float((unsigned)h << 16); }
@@ -101,8 +110,8 @@ __device__ __forceinline__ float wave_max(float v) {
 // Sum over the workgroup; every thread gets the same value (fixed order).
 __device__ __forceinline__ float block_sum(float v, float *sm) {
     v = wave_sum(v);
-    const int wid = threadIdx.x >> 6;
-    if ((threadIdx.x & 63) == 0) sm[wid] = v;
+    const int wid = kl_tid() >> 6;
+    if ((kl_tid() & 63) == 0) sm[wid] = v;
     __syncthreads();
     float t = 0.f;
 #pragma unroll
@@ -132,6 +141,20 @@ __device__ __forceinline__ int eff_tok(const StepParams &P, int b) {
 __device__ __forceinline__ bool seq_ok(const StepParams &P, int b) {
     const int t = P.tokens[b], p = P.positions[b];
     return t >= 0 && t < P.V && p >= 0 && p < min(P.cap, P.max_seq);
+}
+// On the per-sequence path (batch < kMfmaBatch) both are read once per launch
+// into LDS (bar_init), so that no phase starts with a dependent memory round
+// trip for them.
+__device__ __forceinline__ int *seq_table(const StepParams &P);
+template <bool PS>
+__device__ __forceinline__ int pos_of(const StepParams &P, int b) {
+    if constexpr (PS) return seq_table(P)[b];
+    else return eff_pos(P, b);
+}
+template <bool PS>
+__device__ __forceinline__ bool ok_of(const StepParams &P, int b) {
+    if constexpr (PS) return seq_table(P)[kMfmaBatch + b] != 0;
+    else return seq_ok(P, b);
 }
 
 __device__ __forceinline__ size_t kv_row(const StepParams &P, int l, int b, int g) {
@@ -215,14 +238,17 @@ constexpr int kSpinLimit = 1 << 22;   // polls before a wait gives up (well over
 extern __shared__ __align__(16) char kl_smem[];
 __device__ __forceinline__ unsigned long long *bar_bases(const StepParams &P);
 
-__device__ __forceinline__ int bar_groups(const StepParams &P) { return min(kBarGroups, P.nwg); }
+__device__ __forceinline__ int bar_groups(const StepParams &P) { return bar_group_count(P.nwg); }
 __device__ __forceinline__ unsigned bar_gsize(const StepParams &P, int ng, int g) {
-    return (unsigned)(P.nwg / ng + (g < P.nwg % ng ? 1 : 0));
+    return bar_group_size(P.nwg, ng, g);
 }
 __device__ __forceinline__ unsigned long long *bar_counter(const StepParams &P, int g) {
     return P.bar + 32 * (g + 1);   // 256 bytes apart
 }
 
+// At launch start: the barrier bases of this launch and the step's first tag
+// of the tagged hand-offs, into LDS (before any wait; any wave may do it).
+__device__ __forceinline__ unsigned *launch_epoch(const StepParams &P);
 __device__ __forceinline__ void bar_init(const StepParams &P) {
     // Only this workgroup's own group counter is read: that group cannot
     // complete barrier 0 before this workgroup arrives, so the value rounds
@@ -230,11 +256,20 @@ __device__ __forceinline__ void bar_init(const StepParams &P) {
     // other group may already be one barrier further, so its base is E times
     // its size, not its current value rounded down.
     const int ng = bar_groups(P);
-    if (threadIdx.x < ng) {   // (before any wait; any wave may do it)
+    const unsigned t = kl_tid();
+    if (t < (unsigned)ng) {
         const int own = blockIdx.x % ng;
         const unsigned long long c = ld_dev_u64(bar_counter(P, own));
-        const unsigned long long epoch = c / bar_gsize(P, ng, own);
-        bar_bases(P)[threadIdx.x] = epoch * bar_gsize(P, ng, threadIdx.x);
+        bar_bases(P)[t] = bar_launch_base(c, P.nwg, ng, own, (int)t);
+    } else if (t == 64) {
+        *launch_epoch(P) = __hip_atomic_load(P.epoch_ptr, __ATOMIC_RELAXED,
+                                             __HIP_MEMORY_SCOPE_AGENT);
+    } else if (t >= 96 && t < 96 + kMfmaBatch && P.B < kMfmaBatch) {
+        const int b = (int)t - 96;
+        if (b < P.B) {
+            seq_table(P)[b] = eff_pos(P, b);
+            seq_table(P)[kMfmaBatch + b] = seq_ok(P, b) ? 1 : 0;
+        }
     }
     __syncthreads();
 }
@@ -253,7 +288,7 @@ __device__ __forceinline__ void trace_stamp(const StepParams &P, int i, int what
 // The control wave (kCtlWave) does all of a workgroup's barrier traffic.  It
 // never has weight or KV loads in flight, so its polls are not queued behind
 // the compute waves' prefetches (a wave's loads complete in issue order).
-__device__ __forceinline__ bool is_ctl_lane0() { return threadIdx.x == kCtlWave * 64; }
+__device__ __forceinline__ bool is_ctl_lane0() { return kl_tid() == kCtlWave * 64; }
 
 // Every wave drains its stores (they must be visible before the signal),
 // then the control wave signals.
@@ -293,7 +328,7 @@ __device__ __forceinline__ void spin_until(const StepParams &P, Done &&done) {
              KL_DEVERR_BARRIER))
             return;
         if (spins >= kSpinLimit) {
-            if ((threadIdx.x & 63) == 0)
+            if ((kl_tid() & 63) == 0)
                 __hip_atomic_fetch_or(P.err, KL_DEVERR_BARRIER, __ATOMIC_RELAXED,
                                       __HIP_MEMORY_SCOPE_AGENT);
             return;
@@ -302,14 +337,14 @@ __device__ __forceinline__ void spin_until(const StepParams &P, Done &&done) {
 }
 
 __device__ __forceinline__ void bar_wait(const StepParams &P, int k, int ti) {
-    if ((threadIdx.x >> 6) == kCtlWave) {
-        const int lane = threadIdx.x & 63, ng = bar_groups(P);
+    if ((kl_tid() >> 6) == kCtlWave) {
+        const int lane = kl_tid() & 63, ng = bar_groups(P);
         const bool mine = lane < ng;
         const unsigned long long target =
-            mine ? bar_bases(P)[lane] + (unsigned long long)(k + 1) * bar_gsize(P, ng, lane) : 0ull;
+            mine ? bar_target(bar_bases(P)[lane], k, P.nwg, ng, lane) : 0ull;
         if (lane == 0) trace_stamp(P, ti, 1);
         spin_until(P, [&]() {
-            const bool d = !mine || (long long)(ld_dev_u64(bar_counter(P, lane)) - target) >= 0;
+            const bool d = !mine || bar_reached(ld_dev_u64(bar_counter(P, lane)), target);
             return __all(d) != 0;
         });
         if (lane == 0) trace_stamp(P, ti, 2);
@@ -330,6 +365,66 @@ __device__ __forceinline__ void local_wait(const StepParams &P, const unsigned *
         trace_stamp(P, ti, 2);
     }
     __syncthreads();
+}
+
+// ---------------------------------------------------------------- tagged hand-offs
+//
+// On the per-sequence path, values that cross workgroups inside a layer (the
+// rotated queries and the new key and value for the attention, the chunk
+// results for the O projection, the SwiGLU output for the down projection)
+// travel as tagged words: one 8-byte word holds the 32-bit value and the tag
+// of the step and layer that wrote it, written and read as one
+// device-coherent access.  A reader polls the words themselves and takes a
+// value once its tag is the current one.  The writer therefore needs no
+// drain of its stores and no counter, and the reader no separate wait before
+// loading: a hand-off costs the time for the stores to land plus one load
+// round trip, instead of store drain, counter atomic, counter poll and data
+// load one after the other.  Tags are epoch + layer, each step using a fresh
+// range of tags that never includes 0 (cleared memory); the epoch is read at
+// launch start and advanced by the step's last phase (ll_next_epoch).
+__device__ __forceinline__ unsigned ll_tag(const StepParams &P, int l) {
+    return *launch_epoch(P) + (unsigned)l;
+}
+__device__ __forceinline__ void st_ll(unsigned long long *p, unsigned v, unsigned tag) {
+    st_dev_u64(p, ll_word(v, tag));
+}
+__device__ __forceinline__ void st_ll_f(unsigned long long *p, float v, unsigned tag) {
+    st_ll(p, __float_as_uint(v), tag);
+}
+
+// Threads tid = 0 .. nt - 1 (the caller's numbering) gather n tagged words:
+// word i (address addr(i)) goes to put(i, value) once it carries 'tag'.  Each
+// thread takes words tid, tid + nt, ... in rounds of W, issuing a round's
+// loads together (from in-range addresses, masked when used) and reloading
+// the round until every word of it is current.  A round gives up after
+// kSpinLimit polls, raising KL_DEVERR_BARRIER, so a missing writer ends the
+// kernel instead of hanging it.
+template <int W, class Addr, class Put>
+__device__ __forceinline__ void ll_gather(const StepParams &P, int n, unsigned tag, int tid,
+                                          int nt, Addr &&addr, Put &&put) {
+    for (int base = 0; base < n; base += W * nt) {
+        unsigned long long v[W];
+        for (int spins = 1;; ++spins) {
+#pragma unroll
+            for (int k = 0; k < W; ++k) v[k] = ld_dev_u64(addr(min(base + tid + k * nt, n - 1)));
+            bool ok = true;
+#pragma unroll
+            for (int k = 0; k < W; ++k) ok = ok && (base + tid + k * nt >= n || ll_current(v[k], tag));
+            if (ok) break;
+            if ((spins & 63) == 0 &&
+                (__hip_atomic_load(P.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) &
+                 KL_DEVERR_BARRIER))
+                break;
+            if (spins >= kSpinLimit) {
+                __hip_atomic_fetch_or(P.err, KL_DEVERR_BARRIER, __ATOMIC_RELAXED,
+                                      __HIP_MEMORY_SCOPE_AGENT);
+                break;
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < W; ++k)
+            if (base + tid + k * nt < n) put(base + tid + k * nt, ll_value(v[k]));
+    }
 }
 
 // ---------------------------------------------------------------- params
@@ -368,7 +463,6 @@ __device__ __forceinline__ StepParams load_params(KArg ka) {
 // ---------------------------------------------------------------- LDS layout
 
 // Offsets (in floats) come from the host, which sizes the allocation.
-constexpr int kSmLastFlag = 32;   // sm slot: this workgroup's attention result arrived last
 
 struct Lds {
     float *a;     // activation vector (max K extent); aliased by the attention area
@@ -392,6 +486,14 @@ __device__ __forceinline__ Lds lds_layout(char *smem, const StepParams &P) {
 __device__ __forceinline__ unsigned long long *bar_bases(const StepParams &P) {
     return lds_layout(kl_smem, P).bar;
 }
+// (after the barrier bases)
+__device__ __forceinline__ unsigned *launch_epoch(const StepParams &P) {
+    return reinterpret_cast<unsigned *>(lds_layout(kl_smem, P).bar + kBarGroups);
+}
+// (after the epoch: position and validity of each sequence, per-sequence path)
+__device__ __forceinline__ int *seq_table(const StepParams &P) {
+    return reinterpret_cast<int *>(lds_layout(kl_smem, P).bar + kBarGroups) + 4;
+}
 
 // ---------------------------------------------------------------- activations
 
@@ -402,7 +504,7 @@ __device__ __forceinline__ unsigned long long *bar_bases(const StepParams &P) {
 // behind them.
 constexpr int kLdsCoherent = 16;
 __device__ __forceinline__ void ctl_copy_to_lds(const void *src, void *dst, int bytes) {
-    const int lane = threadIdx.x & 63;
+    const int lane = kl_tid() & 63;
     const char *s = static_cast<const char *>(src);
     char *d = static_cast<char *>(dst);
     for (int off = 0; off < bytes; off += 64 * 16) {
@@ -417,7 +519,7 @@ __device__ __forceinline__ void ctl_copy_wait() { __builtin_amdgcn_s_waitcnt(0x0
 constexpr int kStageBatch = 8;
 __device__ __forceinline__ void stage_vec(const float *__restrict__ src, int n, int npad,
                                           float *a) {
-    for (int i0 = threadIdx.x; i0 < npad; i0 += kStageBatch * kThreads) {
+    for (int i0 = kl_tid(); i0 < npad; i0 += kStageBatch * kThreads) {
         float v[kStageBatch];
 #pragma unroll
         for (int k = 0; k < kStageBatch; ++k) {
@@ -450,18 +552,18 @@ __device__ __forceinline__ void stage_rms_deferred(const long long *__restrict__
                                                    const float *esrc = nullptr,
                                                    float *edst = nullptr, int ne = 0) {
     float ss = 0.f;
-    for (int i0 = threadIdx.x; i0 < npad; i0 += kStageBatch * kThreads) {
+    for (int i0 = kl_tid(); i0 < npad; i0 += kStageBatch * kThreads) {
         long long v[kStageBatch];
         float gv[kStageBatch];
         float ev = 0.f;
-        const bool first = i0 == (int)threadIdx.x;
+        const bool first = i0 == (int)kl_tid();
 #pragma unroll
         for (int k = 0; k < kStageBatch; ++k) {
             const int i = i0 + k * kThreads;
             v[k] = i < n ? (long long)ld_dev_u64(xf + i) : 0ll;
             gv[k] = i < n ? gain[i] : 0.f;
         }
-        if (first && (int)threadIdx.x < ne) ev = esrc[threadIdx.x];
+        if (first && (int)kl_tid() < ne) ev = esrc[kl_tid()];
 #pragma unroll
         for (int k = 0; k < kStageBatch; ++k) {
             const int i = i0 + k * kThreads;
@@ -472,10 +574,10 @@ __device__ __forceinline__ void stage_rms_deferred(const long long *__restrict__
                 a[npad + i] = gv[k];
             }
         }
-        if (first && (int)threadIdx.x < ne) edst[threadIdx.x] = ev;
+        if (first && (int)kl_tid() < ne) edst[kl_tid()] = ev;
     }
     ss = wave_sum(ss);
-    if ((threadIdx.x & 63) == 0) sm[threadIdx.x >> 6] = ss;
+    if ((kl_tid() & 63) == 0) sm[kl_tid() >> 6] = ss;
     __syncthreads();
 }
 // The scale r of the sequence staged last by stage_rms_deferred (the wave
@@ -492,18 +594,18 @@ __device__ __forceinline__ void stage_rmsnorm(const long long *__restrict__ xf,
                                               float eps, float *a, float *sm,
                                               const float *esrc = nullptr, float *edst = nullptr,
                                               int ne = 0) {
-    for (int i0 = threadIdx.x; i0 < npad; i0 += kStageBatch * kThreads) {
+    for (int i0 = kl_tid(); i0 < npad; i0 += kStageBatch * kThreads) {
         long long v[kStageBatch];
         float gv[kStageBatch];
         float ev = 0.f;
-        const bool first = i0 == (int)threadIdx.x;
+        const bool first = i0 == (int)kl_tid();
 #pragma unroll
         for (int k = 0; k < kStageBatch; ++k) {
             const int i = i0 + k * kThreads;
             v[k] = i < n ? (long long)ld_dev_u64(xf + i) : 0ll;
             gv[k] = i < n ? gain[i] : 0.f;
         }
-        if (first && (int)threadIdx.x < ne) ev = esrc[threadIdx.x];
+        if (first && (int)kl_tid() < ne) ev = esrc[kl_tid()];
 #pragma unroll
         for (int k = 0; k < kStageBatch; ++k) {
             const int i = i0 + k * kThreads;
@@ -512,14 +614,14 @@ __device__ __forceinline__ void stage_rmsnorm(const long long *__restrict__ xf,
                 a[npad + i] = gv[k];
             }
         }
-        if (first && (int)threadIdx.x < ne) edst[threadIdx.x] = ev;
+        if (first && (int)kl_tid() < ne) edst[kl_tid()] = ev;
     }
     __syncthreads();
     float ss = 0.f;
-    for (int i = threadIdx.x; i < n; i += kThreads) ss = fmaf(a[i], a[i], ss);
+    for (int i = kl_tid(); i < n; i += kThreads) ss = fmaf(a[i], a[i], ss);
     ss = block_sum(ss, sm);
     const float r = 1.0f / sqrtf(ss / (float)n + eps);
-    for (int i = threadIdx.x; i < n; i += kThreads) a[i] = a[i] * r * a[npad + i];
+    for (int i = kl_tid(); i < n; i += kThreads) a[i] = a[i] * r * a[npad + i];
     __syncthreads();
 }
 
@@ -562,7 +664,11 @@ __device__ __forceinline__ RgRange own_rgs(int nrg, const StepParams &P) {
 //   row-split (short rows): wave w takes whole row groups w, w + kWaves, ...
 //             of the batch and needs no cross-wave sum.
 // Both orders are fixed by the partition alone.
-template <bool RowSplit, class Wait, class Stage, class Epi>
+// Early (the usual case): the first ring of loads is issued before wait() and
+// stage(0), overlapping their latency; otherwise after stage(0), so that the
+// loads stage(0) makes are not queued behind them (a wave's loads complete in
+// order).
+template <bool RowSplit, bool Early, class Wait, class Stage, class Epi>
 __device__ __forceinline__ void gemv_rows(const uint8_t *__restrict__ W, int KT, int first,
                                           int count, int stride, int B,
                                           const float *__restrict__ a, float *red,
@@ -572,8 +678,8 @@ __device__ __forceinline__ void gemv_rows(const uint8_t *__restrict__ W, int KT,
     constexpr int BATCH = RowSplit ? kWaves * kRgBatch : kRgBatch;   // row groups per LDS round
     // wave-uniform values live in scalar registers, so every branch below is
     // a scalar branch
-    const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int lane = threadIdx.x & 63;
+    const int wid = __builtin_amdgcn_readfirstlane(kl_tid() >> 6);
+    const int lane = kl_tid() & 63;
     const int row = lane >> 3, sub = lane & 7;
     const int kt0 = RowSplit ? 0 : (wid * KT) / kWaves;
     const int nk = RowSplit ? KT : ((wid + 1) * KT) / kWaves - kt0;
@@ -610,13 +716,18 @@ __device__ __forceinline__ void gemv_rows(const uint8_t *__restrict__ W, int KT,
     // the control wave takes part in the staging and the epilogue only
     const bool compute = wid < kWaves;
     const bool has_rows = count > 0;
-    if (has_rows && compute) start(0);
+    if (Early && has_rows && compute) start(0);
     wait();
     if (!has_rows) return;
     for (int b = 0; b < B; ++b) {
         for (int ib = 0; ib < count; ib += BATCH) {
-            if ((b > 0 || ib > 0) && compute) start(ib);
-            if (ib == 0) stage(b);
+            if (Early) {
+                if ((b > 0 || ib > 0) && compute) start(ib);
+                if (ib == 0) stage(b);
+            } else {
+                if (ib == 0) stage(b);
+                if (compute) start(ib);
+            }
             const int nrg = min(BATCH, count - ib);
             int cr = RowSplit ? wid : 0, ck = 0;   // batch item of the row group in progress
             float acc = 0.f;
@@ -654,7 +765,7 @@ __device__ __forceinline__ void gemv_rows(const uint8_t *__restrict__ W, int KT,
                 }
             }
             __syncthreads();
-            for (int t = threadIdx.x; t < nrg * (kTileRows / 2); t += kThreads) {
+            for (int t = kl_tid(); t < nrg * (kTileRows / 2); t += kThreads) {
                 const int rgi = t / (kTileRows / 2), pr = (t % (kTileRows / 2)) * 2;
                 float y0 = 0.f, y1 = 0.f;
                 if (RowSplit) {
@@ -676,16 +787,16 @@ __device__ __forceinline__ void gemv_rows(const uint8_t *__restrict__ W, int KT,
 
 // Row groups are shared split-K when they are long enough for every wave to
 // hold two or more tiles, else row-split.
-template <class Wait, class Stage, class Epi>
+template <bool Early, class Wait, class Stage, class Epi>
 __device__ __forceinline__ void gemv_phase(const uint8_t *__restrict__ W, int KT, int first,
                                            int count, int stride, int B,
                                            const float *__restrict__ a, float *red,
                                            const uint8_t *dummy, Wait &&wait, Stage &&stage,
                                            Epi &&epi) {
     if (KT >= 2 * kWaves)
-        gemv_rows<false>(W, KT, first, count, stride, B, a, red, dummy, wait, stage, epi);
+        gemv_rows<false, Early>(W, KT, first, count, stride, B, a, red, dummy, wait, stage, epi);
     else
-        gemv_rows<true>(W, KT, first, count, stride, B, a, red, dummy, wait, stage, epi);
+        gemv_rows<true, Early>(W, KT, first, count, stride, B, a, red, dummy, wait, stage, epi);
 }
 
 // ---------------------------------------------------------------- batched engine
@@ -765,8 +876,8 @@ __device__ __forceinline__ void gemm_rows_mode(const uint8_t *__restrict__ W, in
     constexpr int CT = kGemmChunkK / kTileK;   // k-tiles per chunk
     constexpr int MB = kGemmMaxBlk;
     static_assert(U == 2 * CT, "a ring pass is one chunk of one 16-row block");
-    const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int lane = threadIdx.x & 63;
+    const int wid = __builtin_amdgcn_readfirstlane(kl_tid() >> 6);
+    const int lane = kl_tid() & 63;
     const bool compute = wid < kWaves;
     const int nkc = resident ? min((KT + CT - 1) / CT, 2) : (KT + CT - 1) / CT;
     const int nblk = (count + 1) / 2;
@@ -954,14 +1065,15 @@ __device__ __forceinline__ void gemm_rows(const uint8_t *__restrict__ W, int KT,
 // as bf16 chunks: prep() runs once after wait(), both once the first weight
 // loads are in flight; stageb(c, b0, nb, buf) fills chunk c for sequences
 // b0 .. b0 + nb - 1 (the control wave's memory-to-LDS copies).
-template <bool BAT, class Wait, class Prep, class Stage1, class StageB, class Epi>
+template <bool BAT, bool Early = true, class Wait, class Prep, class Stage1, class StageB,
+          class Epi>
 __device__ __forceinline__ void weight_phase(const StepParams &P, const Lds &S,
                                              const uint8_t *W, int KT, int first, int count,
                                              Wait &&wait, Prep &&prep, Stage1 &&stage1,
                                              StageB &&stageb, Epi &&epi, int ktg = 0,
                                              size_t gstride = 0) {
     if constexpr (!BAT) {
-        gemv_phase(W, KT, first, count, 1, P.B, S.a, S.red, P.dummy, wait, stage1, epi);
+        gemv_phase<Early>(W, KT, first, count, 1, P.B, S.a, S.red, P.dummy, wait, stage1, epi);
         return;
     }
     const GemmLds L = gemm_lds(kl_smem);
@@ -1002,8 +1114,8 @@ __device__ __forceinline__ void norm_batched(const StepParams &P, const Lds &S,
     const int plast = max(nparts - 1, 0);
     for (int it = blockIdx.x; it < P.B * ns; it += P.nwg) {
         const int b = it / ns, sl = it % ns;
-        const int i = sl * kGemmChunkK + (int)threadIdx.x;
-        const bool live = (int)threadIdx.x < kGemmChunkK && i < P.Hp;
+        const int i = sl * kGemmChunkK + (int)kl_tid();
+        const bool live = (int)kl_tid() < kGemmChunkK && i < P.Hp;
         const int ic = min(i, P.Hp - 1);
         // (unconditional loads from in-range addresses, masked when used)
         long long x = (long long)ld_dev_u64(xin + (size_t)b * P.Hp + ic);
@@ -1028,7 +1140,7 @@ __device__ __forceinline__ void norm_batched(const StepParams &P, const Lds &S,
             st_dev_u16(P.act_lo + (size_t)b * P.Hp + i, lo);
         }
         ss = block_sum(ss, S.sm);
-        if (threadIdx.x == 0) st_dev(P.ssp + (size_t)b * ns + sl, ss);
+        if (kl_tid() == 0) st_dev(P.ssp + (size_t)b * ns + sl, ss);
         drain_all();   // (also: S.sm is reused by the next item)
         if (is_ctl_lane0())
             __hip_atomic_fetch_add(norm_cnt(P) + kNormCntStride * sl, 1u, __ATOMIC_RELAXED,
@@ -1077,7 +1189,7 @@ __device__ __forceinline__ float rms_r(const StepParams &P, int b) {
 // the steps that fold a batched product's partials; ends with a workgroup
 // barrier.
 __device__ __forceinline__ void rms_table(const StepParams &P, const Lds &S) {
-    for (int t = threadIdx.x; t < min(P.B, kRScaleTable); t += kThreads) S.red[t] = rms_r(P, t);
+    for (int t = kl_tid(); t < min(P.B, kRScaleTable); t += kThreads) S.red[t] = rms_r(P, t);
     __syncthreads();
 }
 __device__ __forceinline__ float rms_of(const StepParams &P, const Lds &S, int b) {
@@ -1097,8 +1209,8 @@ __device__ __forceinline__ float rms_of(const StepParams &P, const Lds &S, int b
 // kc are never consumed).
 __device__ __forceinline__ void ctl_copy_rows(const uint16_t *hi, const uint16_t *lo, int ld,
                                               int k0, int kc, int b0, int nb, uint16_t *buf) {
-    if ((threadIdx.x >> 6) != kCtlWave) return;
-    const int lane = threadIdx.x & 63;
+    if ((kl_tid() >> 6) != kCtlWave) return;
+    const int lane = kl_tid() & 63;
     const uint64_t col = (uint64_t)(k0 + min(lane * 8, kc - 8));
     // (the row offset is opaque to the compiler at each step, so that the
     // addresses are formed right before their copies instead of all at once)
@@ -1140,7 +1252,7 @@ __device__ __forceinline__ void stage_bf16_chunk(const uint16_t *src, const uint
 template <int D, int G>
 __device__ __forceinline__ void merge_batched(const StepParams &P, int k) {
     const int C = P.C, n = P.nq * D, total = P.B * n;
-    for (int e = blockIdx.x * kThreads + threadIdx.x; e < total; e += P.nwg * kThreads) {
+    for (int e = blockIdx.x * kThreads + kl_tid(); e < total; e += P.nwg * kThreads) {
         const int b = e / n, j = e % n, h = j / D, g = h / G, hl = h % G, dd = j % D;
         const size_t item0 = ((size_t)b * P.nkv + g) * C;
         float M = -INFINITY;
@@ -1168,7 +1280,7 @@ __device__ __forceinline__ void phase_embed(KArg ka, int gwait, int garrive, int
     const StepParams P = load_params(ka);
     if (gwait >= 0) bar_wait(P, gwait, ti);
     if (blockIdx.x == 0) {
-        for (int b = threadIdx.x; b < P.B; b += kThreads) {
+        for (int b = kl_tid(); b < P.B; b += kThreads) {
             const int t = P.tokens[b], p = P.positions[b];
             int bits = 0;
             if (t < 0 || t >= P.V) bits |= KL_DEVERR_TOKEN;
@@ -1178,11 +1290,11 @@ __device__ __forceinline__ void phase_embed(KArg ka, int gwait, int garrive, int
         // (the batched RMSNorm counters exist, and are used, in batched steps only)
         const int nc = 2 * P.nkv + P.Sc +
                        (P.B >= kMfmaBatch ? kNormCntStride * ((P.Hp + kGemmChunkK - 1) / kGemmChunkK) : 0);
-        for (int i = threadIdx.x; i < nc; i += kThreads)
+        for (int i = kl_tid(); i < nc; i += kThreads)
             __hip_atomic_store(P.cnt + i, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
     const int total = P.B * P.Hp;
-    for (int idx = blockIdx.x * kThreads + threadIdx.x; idx < total; idx += P.nwg * kThreads) {
+    for (int idx = blockIdx.x * kThreads + kl_tid(); idx < total; idx += P.nwg * kThreads) {
         const int b = idx / P.Hp, i = idx % P.Hp;
         const float e = (i < P.H) ? bf2f(P.embed[(size_t)eff_tok(P, b) * P.H + i]) : 0.f;
         st_dev_u64(reinterpret_cast<unsigned long long *>(P.xf + idx),
@@ -1194,31 +1306,47 @@ __device__ __forceinline__ void phase_embed(KArg ka, int gwait, int garrive, int
 // One rotation pair (rows lr, lr + 1 of KV head g's block, lr even) of the
 // q/k/v projection of sequence b: RoPE (Sec. 2) on query and key rows with
 // cs = (cos, sin) of the pair's angle at the sequence's position, then the
-// query to q, the key and value to the KV cache at that position.
-template <class Rope>
+// key and value to the KV cache at that position, and the query (and the new
+// key and value, for the attention) to the attention's inputs: tagged words
+// (LL, the per-sequence path, tag 'tag') or plain device-coherent stores.
+template <bool LL, class Rope>
 __device__ __forceinline__ void qkv_store(const StepParams &P, int l, int b, int g, int lr,
-                                          float y0, float y1, Rope &&rope) {
+                                          float y0, float y1, Rope &&rope, unsigned tag = 0) {
     const int d = P.d, half = P.d / 2, G = P.group;
-    const int p = eff_pos(P, b);
+    const int p = pos_of<LL>(P, b);
+    const bool ok = ok_of<LL>(P, b);
+    unsigned long long *kvl = LL ? P.kv_ll + ((size_t)b * P.nkv + g) * d : nullptr;
     if (lr < (G + 1) * d) {
         const int i = (lr % d) >> 1;
         const float2 cs = rope(p, i);
         const float u0 = y0 * cs.x - y1 * cs.y;
         const float u1 = y0 * cs.y + y1 * cs.x;
         if (lr < G * d) {
-            float *qq = P.q + (size_t)b * P.nq * d + (size_t)(g * G + lr / d) * d;
-            st_dev(qq + i, u0);
-            st_dev(qq + i + half, u1);
-        } else if (seq_ok(P, b)) {
-            uint16_t *kk = P.kc + (kv_row(P, l, b, g) + p) * d;
-            st_dev_u16(kk + i, f2bf(u0));
-            st_dev_u16(kk + i + half, f2bf(u1));
+            const size_t qo = (size_t)b * P.nq * d + (size_t)(g * G + lr / d) * d;
+            if (LL) {
+                st_ll_f(P.q_ll + qo + i, u0, tag);
+                st_ll_f(P.q_ll + qo + i + half, u1, tag);
+            } else {
+                st_dev(P.q + qo + i, u0);
+                st_dev(P.q + qo + i + half, u1);
+            }
+        } else {
+            const uint16_t k0 = f2bf(u0), k1 = f2bf(u1);
+            if (ok) {
+                uint16_t *kk = P.kc + (kv_row(P, l, b, g) + p) * d;
+                st_dev_u16(kk + i, k0);
+                st_dev_u16(kk + i + half, k1);
+            }
+            if (LL) st_ll(kvl + i, (unsigned)k0 | ((unsigned)k1 << 16), tag);
         }
-    } else if (seq_ok(P, b)) {
+    } else {
         const int j = lr - (G + 1) * d;
-        uint16_t *vv = P.vc + (kv_row(P, l, b, g) + p) * d;
-        st_dev_u32(reinterpret_cast<unsigned *>(vv + j),
-                   (unsigned)f2bf(y0) | ((unsigned)f2bf(y1) << 16));
+        const unsigned v01 = (unsigned)f2bf(y0) | ((unsigned)f2bf(y1) << 16);
+        if (ok) {
+            uint16_t *vv = P.vc + (kv_row(P, l, b, g) + p) * d;
+            st_dev_u32(reinterpret_cast<unsigned *>(vv + j), v01);
+        }
+        if (LL) st_ll(kvl + half + j / 2, v01, tag);
     }
 }
 
@@ -1229,7 +1357,7 @@ __device__ __forceinline__ void fold_qkv(const StepParams &P, const Lds &S, int 
     const int hrows = P.qkv_rg * kTileRows, rows = P.nkv * hrows, KS = P.KSq;
     rms_table(P, S);
     const int npair = hrows / 2, total = P.B * npair, half = P.d / 2;
-    for (int e = part * kThreads + threadIdx.x; e < total; e += P.Sg * kThreads) {
+    for (int e = part * kThreads + kl_tid(); e < total; e += P.Sg * kThreads) {
         const int b = e / npair, lr = 2 * (e % npair);
         const float *src = P.gpart + (size_t)b * rows + g * hrows + lr;
         float y0 = 0.f, y1 = 0.f;
@@ -1248,8 +1376,8 @@ __device__ __forceinline__ void fold_qkv(const StepParams &P, const Lds &S, int 
             }
         }
         const float r = rms_of(P, S, b);   // the deferred RMSNorm scale
-        qkv_store(P, l, b, g, lr, y0 * r, y1 * r,
-                  [&](int p, int i) { return P.rope[(size_t)p * half + i]; });
+        qkv_store<false>(P, l, b, g, lr, y0 * r, y1 * r,
+                         [&](int p, int i) { return P.rope[(size_t)p * half + i]; });
     }
 }
 
@@ -1313,74 +1441,79 @@ __device__ __forceinline__ void phase_qkv(KArg ka, int l, int gwait, int qbar, i
         [&](int b) {
             // the RoPE row of this sequence's position rides along (a + 2 Hp)
             stage_rms_deferred(P.xf + (size_t)b * P.Hp, gain, P.H, P.Hp, S.a, S.sm,
-                               reinterpret_cast<const float *>(P.rope + (size_t)eff_pos(P, b) * half),
+                               reinterpret_cast<const float *>(P.rope + (size_t)pos_of<true>(P, b) * half),
                                S.a + 2 * P.Hp, 2 * half);
             if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 3);
         },
         [&](int, int, int, uint16_t *) {},
         [&](int b, int r, float y0, float y1) {
             const float rs = rms_scale(S.sm, P.H, P.eps);   // the deferred RMSNorm scale
-            qkv_store(P, l, b, g, r - row0, y0 * rs, y1 * rs, [&](int, int i) {
+            qkv_store<true>(P, l, b, g, r - row0, y0 * rs, y1 * rs, [&](int, int i) {
                 return reinterpret_cast<const float2 *>(S.a + 2 * P.Hp)[i];
-            });
+            }, ll_tag(P, l));
         });
-    if (member) local_arrive(P, P.cnt + g, ti);
+    // (the attention polls the tagged words: no drain, no counter)
+    if (is_ctl_lane0()) trace_stamp(P, ti, 0);
 }
 
-// Merge the C chunk results of (sequence b, KV head g) in chunk order into
-// o[G * D] (LDS): o_h = sum_c w_ch A_ch / sum_c w_ch L_ch, w_ch = exp(M_ch - M_h).
-// Every thread owns outputs j; its loads of all chunks' values for j are
-// issued together (batches of kCombBatch) with the statistics loads.
+// The merged attention output of query head hq of KV head g for sequence b
+// (Sec. 2 attention, split over the context): o = sum_c w_c A_c / sum_c w_c
+// L_c with w_c = exp(M_c - M), M the largest chunk maximum, over the C chunk
+// results (A_c the unnormalised output, M_c the maximum, L_c the sum of the
+// chunk).  The results arrive as tagged words, kMergeChunks chunks per round;
+// a later round rescales the running sums to its new maximum.  Chunks are
+// taken in order, so the sums are the same in every schedule.  Leaves o in
+// S.a[0 .. D).
 template <int D, int G>
-__device__ __forceinline__ void merge_chunks(const StepParams &P, int b, int g, float *o,
-                                             float *scratch) {
+__device__ __forceinline__ void merge_ll(const StepParams &P, int l, int b, int g, int hq,
+                                         const Lds &S) {
+    constexpr int WD = D + 2;                       // words per chunk and head
+    float *o = S.a;                                 // [D]
+    float *wts = S.a + D;                           // [kMergeChunks]
+    float *run = wts + kMergeChunks;                // running max, running sum, rescale
+    float *raw = run + 4;                           // [kMergeChunks][D + 2] values
+    const unsigned tag = ll_tag(P, l);
     const int C = P.C;
-    const size_t item0 = ((size_t)b * P.nkv + g) * C;
-    const float *po = P.part_o + item0 * G * D;
-    const float *ps = P.part_s + item0 * G * 2;
-    float *cM = scratch, *cL = cM + C * G, *cW = cL + C * G, *cT = cW + C * G;
-    for (int j = threadIdx.x; j - (int)threadIdx.x < G * D; j += kThreads) {
-        const bool jv = j < G * D;
-        const int h = jv ? j / D : 0;
-        float num = 0.f;
-        for (int c0 = 0; c0 < C; c0 += kCombBatch) {
-            float av[kCombBatch];
-#pragma unroll
-            for (int k = 0; k < kCombBatch; ++k)
-                av[k] = (jv && c0 + k < C) ? ld_dev(po + (size_t)(c0 + k) * G * D + j) : 0.f;
-            if (j == (int)threadIdx.x && c0 == 0) {
-                // (first pass only, uniform across the block) statistics:
-                // wave h takes head h, lane c chunk c (strided): the chunk
-                // weights w_ch = exp(M_ch - M_h) and their sum, by wave
-                // reductions instead of a per-thread pass over the chunks
-                const int wid = threadIdx.x >> 6, lane = threadIdx.x & 63;
-                if (wid < G) {
-                    float mx = -INFINITY;
-                    for (int cc = lane; cc < C; cc += 64) {
-                        const unsigned long long v = ld_dev_u64(ps + ((size_t)cc * G + wid) * 2);
-                        cM[cc * G + wid] = __uint_as_float((unsigned)v);
-                        cL[cc * G + wid] = __uint_as_float((unsigned)(v >> 32));
-                        mx = fmaxf(mx, __uint_as_float((unsigned)v));
-                    }
-                    mx = wave_max(mx);
-                    float tot = 0.f;
-                    for (int cc = lane; cc < C; cc += 64) {
-                        const float m = cM[cc * G + wid];
-                        const float w = (m == -INFINITY) ? 0.f : expf(m - mx);
-                        cW[cc * G + wid] = w;
-                        tot = fmaf(cL[cc * G + wid], w, tot);
-                    }
-                    tot = wave_sum(tot);
-                    if (lane == 0) cT[wid] = tot;
-                }
-                __syncthreads();
+    // chunk c's words of query head hq: src + c (D + 2) + j (contiguous)
+    const unsigned long long *src = P.po_ll + (((size_t)b * P.nkv + g) * G + hq) * C * WD;
+    auto val = [&](int i) { return raw[i]; };
+    for (int c0 = 0; c0 < C; c0 += kMergeChunks) {
+        const int nc = min(kMergeChunks, C - c0);
+        ll_gather<(kMergeChunks * WD + kThreads - 1) / kThreads>(
+            P, nc * WD, tag, kl_tid(), kThreads, [&](int i) { return src + (size_t)c0 * WD + i; },
+            [&](int i, unsigned v) { raw[i] = __uint_as_float(v); });
+        __syncthreads();
+        if (kl_tid() < 64) {   // wave 0: this round's chunk weights and sum
+            const int lane = kl_tid();
+            float mx = -INFINITY;
+            for (int c = lane; c < nc; c += 64) mx = fmaxf(mx, val(c * WD + D));
+            mx = wave_max(mx);
+            const float mold = c0 == 0 ? -INFINITY : run[0];
+            const float mnew = fmaxf(mold, mx);
+            float den = 0.f;
+            for (int c = lane; c < nc; c += 64) {
+                const float m = val(c * WD + D);
+                const float w = (m == -INFINITY) ? 0.f : expf(m - mnew);
+                wts[c] = w;
+                den = fmaf(val(c * WD + D + 1), w, den);
             }
-#pragma unroll
-            for (int k = 0; k < kCombBatch; ++k)
-                if (c0 + k < C) num = fmaf(av[k], cW[(c0 + k) * G + h], num);
+            den = wave_sum(den);
+            if (lane == 0) {
+                const float resc = (mold == -INFINITY) ? 0.f : expf(mold - mnew);
+                run[1] = (c0 == 0 ? 0.f : run[1] * resc) + den;
+                run[2] = resc;
+                run[0] = mnew;
+            }
         }
-        if (jv) o[j] = num / cT[h];
+        __syncthreads();
+        for (int t = kl_tid(); t < D; t += kThreads) {
+            float acc = c0 == 0 ? 0.f : o[t] * run[2];
+            for (int c = 0; c < nc; ++c) acc = fmaf(wts[c], val(c * WD + t), acc);
+            o[t] = acc;
+        }
+        __syncthreads();
     }
+    for (int t = kl_tid(); t < D; t += kThreads) o[t] = o[t] / run[1];
     __syncthreads();
 }
 
@@ -1401,8 +1534,10 @@ template <int D, int NG>
 constexpr int attn_sub() { return kWaves * NG * (64 / (D / 8)); }
 
 // PEEL (batched path, up to 4 query heads per KV head, where the chunks are
-// long): the last sub-chunk is a copy of its own, see below.
-template <int D, int G, bool LAST, bool PEEL>
+// long): the last sub-chunk is a copy of its own, see below.  LL (the
+// per-sequence path): the queries and the new key and value arrive as tagged
+// words, and the chunk result leaves as tagged words.
+template <int D, int G, bool LL, bool PEEL>
 __device__ __forceinline__ void attn_item(KArg ka, int l, int b, int g, int c, bool first,
                                           int ti) {
     const StepParams P = load_params(ka);
@@ -1413,10 +1548,10 @@ __device__ __forceinline__ void attn_item(KArg ka, int l, int b, int g, int c, b
     // measured faster there; never more than kAttnLoads, which sizes the LDS)
     constexpr int NG = PEEL ? kAttnLoadsPeel : kAttnLoads;
     constexpr int SUB = attn_sub<D, NG>();          // positions per sub-chunk
-    const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int lane = threadIdx.x & 63;
+    const int wid = __builtin_amdgcn_readfirstlane(kl_tid() >> 6);
+    const int lane = kl_tid() & 63;
     const int pi = lane / LP, ds = (lane % LP) * 8;
-    const int pnew = eff_pos(P, b), n = pnew + 1;
+    const int pnew = pos_of<LL>(P, b), n = pnew + 1;
     int s0, s1;
     split_range((n + PP - 1) / PP, P.C, c, s0, s1);
     const int j0 = min(n, s0 * PP), j1 = min(n, s1 * PP);
@@ -1426,6 +1561,8 @@ __device__ __forceinline__ void attn_item(KArg ka, int l, int b, int g, int c, b
     float *sp = qs + G * D;             // [G][SUB]
     float *st = sp + G * SUB;           // [G][4]: max, sum, rescale
     float *red = st + G * 4;            // [kWaves][G][D]
+    uint16_t *kn = reinterpret_cast<uint16_t *>(red + kWaves * G * D);   // [D] new key (LL)
+    uint16_t *vn = kn + D;                                               // [D] new value (LL)
     const size_t row0 = kv_row(P, l, b, g);
     const uint16_t *Kb = P.kc + row0 * D;
     const uint16_t *Vb = P.vc + row0 * D;
@@ -1449,27 +1586,56 @@ __device__ __forceinline__ void attn_item(KArg ka, int l, int b, int g, int c, b
         issue_one(kr, Kb, j0, min(SUB, j1 - j0));
         issue_one(vr, Vb, j0, min(SUB, j1 - j0));
     }
-    if (first) local_wait(P, P.cnt + g, (unsigned)(l + 1) * (unsigned)P.Sg, ti);
     // the new slot (written during this step by another workgroup) is read
-    // once, by the lanes that hold it, with device-coherent loads after the
-    // wait into registers of their own; a lane takes it in place of its ring
-    // value where its slab holds the new position (no ring load is
-    // conditional, so the compiler's waits for the ring stay exact)
+    // once, by the lanes that hold it, after the wait into registers of their
+    // own; a lane takes it in place of its ring value where its slab holds
+    // the new position (no ring load is conditional, so the compiler's waits
+    // for the ring stay exact)
     u32x4 knew = {0u, 0u, 0u, 0u}, vnew = {0u, 0u, 0u, 0u};
-    {
-        const int pl = (pnew - j0) % SUB;   // its place in its sub-chunk
-        if (compute && pnew >= j0 && pnew < j1 && (pl / PP) % kWaves == wid && pl % PP == pi) {
+    const int pl = (pnew - j0) % SUB;   // its place in its sub-chunk
+    const bool holds_new =
+        compute && pnew >= j0 && pnew < j1 && (pl / PP) % kWaves == wid && pl % PP == pi;
+    if constexpr (LL) {
+        // the queries of head g's query heads and the new key and value, as
+        // tagged words (every thread takes a few), into LDS
+        if (is_ctl_lane0()) trace_stamp(P, ti, 1);
+        const size_t qo = (size_t)b * P.nq * D + (size_t)g * G * D;
+        const unsigned long long *kvl = P.kv_ll + ((size_t)b * P.nkv + g) * D;
+        ll_gather<(G * D + D + kThreads - 1) / kThreads>(
+            P, G * D + D, ll_tag(P, l), kl_tid(), kThreads,
+            [&](int i) { return i < G * D ? P.q_ll + qo + i : kvl + (i - G * D); },
+            [&](int i, unsigned v) {
+                if (i < G * D) {
+                    qs[i] = __uint_as_float(v);
+                } else if (i < G * D + D / 2) {   // key dims j and j + D/2
+                    const int j = i - G * D;
+                    kn[j] = (uint16_t)v;
+                    kn[j + D / 2] = (uint16_t)(v >> 16);
+                } else {                           // value dims 2j and 2j + 1
+                    reinterpret_cast<unsigned *>(vn)[i - G * D - D / 2] = v;
+                }
+            });
+    } else {
+        if (first) local_wait(P, P.cnt + g, (unsigned)(l + 1) * (unsigned)P.Sg, ti);
+        if (holds_new) {   // (device-coherent loads)
             knew = ld_dev_16B(Kb + (size_t)pnew * D + ds);
             vnew = ld_dev_16B(Vb + (size_t)pnew * D + ds);
         }
+        for (int t = kl_tid(); t < G * D; t += kThreads)
+            qs[t] = ld_dev(P.q + (size_t)b * P.nq * D + (size_t)g * G * D + t);
     }
-    for (int t = threadIdx.x; t < G * D; t += kThreads)
-        qs[t] = ld_dev(P.q + (size_t)b * P.nq * D + (size_t)g * G * D + t);
-    if (threadIdx.x < G) {
-        st[threadIdx.x * 4 + 0] = -INFINITY;
-        st[threadIdx.x * 4 + 1] = 0.f;
+    if (kl_tid() < G) {
+        st[kl_tid() * 4 + 0] = -INFINITY;
+        st[kl_tid() * 4 + 1] = 0.f;
     }
     __syncthreads();
+    if constexpr (LL) {
+        if (is_ctl_lane0()) trace_stamp(P, ti, 2);
+        if (holds_new) {
+            knew = *reinterpret_cast<const u32x4 *>(kn + ds);
+            vnew = *reinterpret_cast<const u32x4 *>(vn + ds);
+        }
+    }
     float acc[G][8];
 #pragma unroll
     for (int h = 0; h < G; ++h)
@@ -1609,83 +1775,61 @@ __device__ __forceinline__ void attn_item(KArg ka, int l, int b, int g, int c, b
     __syncthreads();
     // publish: unnormalised outputs [G][D] and (max, sum) per head
     const size_t item = ((size_t)b * P.nkv + g) * P.C + c;
-    float *out = P.part_o + item * G * D;
-    float *sts = P.part_s + item * G * 2;
-    for (int t = threadIdx.x; t < G * D; t += kThreads) {
-        const int h = t / D, dd = t % D;
-        float s = 0.f;
-        for (int w = 0; w < kWaves; ++w) s += red[(w * G + h) * D + dd];
-        st_dev(out + t, s);
-        if (P.C == 1) {   // (one chunk: the merged output is final; the batched O projection copies it)
-            uint16_t hi, lo;
-            split_bf16(s / st[h * 4 + 1], hi, lo);
-            const size_t o = (size_t)b * P.nq * D + (size_t)g * G * D + t;
-            st_dev_u16(P.acto + o, hi);
-            st_dev_u16(P.acto_lo + o, lo);
+    if constexpr (LL) {
+        // tagged words, per query head h: outputs, max, sum (D + 2 words at
+        // [b][g][h][c]: the chunks of one query head are contiguous for the
+        // O projection, which polls them; no drain, no counter)
+        const unsigned tag = ll_tag(P, l);
+        unsigned long long *out = P.po_ll + (((size_t)b * P.nkv + g) * G * P.C + c) * (D + 2);
+        const size_t hstride = (size_t)P.C * (D + 2);
+        for (int t = kl_tid(); t < G * D; t += kThreads) {
+            const int h = t / D, dd = t % D;
+            float s = 0.f;
+            for (int w = 0; w < kWaves; ++w) s += red[(w * G + h) * D + dd];
+            st_ll_f(out + h * hstride + dd, s, tag);
         }
-    }
-    if (threadIdx.x < G) {
-        st_dev(sts + threadIdx.x * 2, st[threadIdx.x * 4 + 0]);
-        st_dev(sts + threadIdx.x * 2 + 1, st[threadIdx.x * 4 + 1]);
+        if (kl_tid() < G) {
+            st_ll_f(out + kl_tid() * hstride + D, st[kl_tid() * 4 + 0], tag);
+            st_ll_f(out + kl_tid() * hstride + D + 1, st[kl_tid() * 4 + 1], tag);
+        }
+    } else {
+        float *out = P.part_o + item * G * D;
+        float *sts = P.part_s + item * G * 2;
+        for (int t = kl_tid(); t < G * D; t += kThreads) {
+            const int h = t / D, dd = t % D;
+            float s = 0.f;
+            for (int w = 0; w < kWaves; ++w) s += red[(w * G + h) * D + dd];
+            st_dev(out + t, s);
+            if (P.C == 1) {   // (one chunk: the merged output is final; the O projection copies it)
+                uint16_t hi, lo;
+                split_bf16(s / st[h * 4 + 1], hi, lo);
+                const size_t o = (size_t)b * P.nq * D + (size_t)g * G * D + t;
+                st_dev_u16(P.acto + o, hi);
+                st_dev_u16(P.acto_lo + o, lo);
+            }
+        }
+        if (kl_tid() < G) {
+            st_dev(sts + kl_tid() * 2, st[kl_tid() * 4 + 0]);
+            st_dev(sts + kl_tid() * 2 + 1, st[kl_tid() * 4 + 1]);
+        }
     }
     if (is_ctl_lane0()) trace_stamp(P, ti, 3);
-    drain_all();
-    if (is_ctl_lane0()) {
-        if (LAST) {
-            const unsigned old = __hip_atomic_fetch_add(P.cnt + P.nkv + g, 1u, __ATOMIC_RELAXED,
-                                                        __HIP_MEMORY_SCOPE_AGENT);
-            // the last chunk result of head g in layer l (per layer: B C
-            // results, then the merged output)
-            const unsigned per_layer = (unsigned)(P.B * P.C) + 1u;
-            S.sm[kSmLastFlag] = (old == (unsigned)l * per_layer + per_layer - 2u) ? 1.f : 0.f;
-        } else {
-            __hip_atomic_fetch_add(P.cnt + P.nkv + g, 1u, __ATOMIC_RELAXED,
-                                   __HIP_MEMORY_SCOPE_AGENT);
-        }
-    }
+    __syncthreads();   // (the attention area is the next item's)
 }
 
-// Attention of KV head g: the workgroups of head g take its items (sequence b,
-// chunk c) round-robin.  GEMV path with up to 4 query heads per KV head: the
-// workgroup whose chunk result of head g arrives last merges the chunk
-// results of every sequence (in chunk order) and publishes o_g in place of
-// the queries (no longer needed in this layer); the O projection then stages
-// G d values instead of merging C chunks in each of its workgroups.  (With 8
-// query heads per KV head the attention already needs every register, and
-// the merge is left to the O projection's workgroups.)
-template <int D, int G, bool BAT>
-constexpr bool merge_last() { return !BAT && G <= 4; }
-
+// Attention of KV head g: the workgroups of head g take its items (sequence
+// b, chunk c) round-robin.  The per-sequence path hands the chunk results to
+// the O projection as tagged words; the batched path publishes them before a
+// grid barrier.
 template <int D, int G, bool BAT>
 __device__ __forceinline__ void phase_attn(KArg ka, int l, int garrive, int ti) {
     const StepParams P = load_params(ka);
-    const Lds S = lds_layout(kl_smem, P);
     const int g = blockIdx.x / P.Sg, part = blockIdx.x % P.Sg;
     if (g < P.nkv) {
         const int items = P.B * P.C;
-        bool last = false;
-        for (int it = part; it < items; it += P.Sg) {
-            attn_item<D, G, merge_last<D, G, BAT>(), BAT && G <= 4>(ka, l, it / P.C, g, it % P.C,
-                                                                   it == part, ti);
-            if (merge_last<D, G, BAT>()) {
-                __syncthreads();
-                last = last || S.sm[kSmLastFlag] != 0.f;
-            }
-        }
-        if (merge_last<D, G, BAT>() && last) {
-            for (int b = 0; b < P.B; ++b) {
-                merge_chunks<D, G>(P, b, g, S.a, S.a + G * D);
-                float *o = P.q + (size_t)b * P.nq * D + (size_t)g * G * D;
-                for (int t = threadIdx.x; t < G * D; t += kThreads) st_dev(o + t, S.a[t]);
-                __syncthreads();   // (S.a is the next sequence's merge area)
-            }
-            drain_all();
-            if (is_ctl_lane0())
-                __hip_atomic_fetch_add(P.cnt + P.nkv + g, 1u, __ATOMIC_RELAXED,
-                                       __HIP_MEMORY_SCOPE_AGENT);
-        }
+        for (int it = part; it < items; it += P.Sg)
+            attn_item<D, G, !BAT, BAT && G <= 4>(ka, l, it / P.C, g, it % P.C, it == part, ti);
     }
-    // (batched steps: the O projection takes all heads and waits on the grid)
     if (garrive >= 0) bar_arrive(P, garrive, ti);
     else if (is_ctl_lane0()) trace_stamp(P, ti, 0);
 }
@@ -1711,6 +1855,8 @@ __device__ __forceinline__ void phase_oproj(KArg ka, int l, int gwait, int mbar,
         // each) x row groups; a workgroup writes its slice's partial sums,
         // which the next RMSNorm step folds into the residual.  Every wave
         // gets whole 16-row blocks and the activation staging is one slice.
+        // (The O projection is packed per query head, D / kTileK k-tiles per
+        // row group: a slice spans gps G packed matrices.)
         const int KS = P.KSo, RB = P.nwg / KS;
         const int ks = blockIdx.x / RB, rb = blockIdx.x % RB, ksc = min(ks, KS - 1);
         const int gps = P.nkv / KS, width = gps * G * D;   // KV heads and columns per slice
@@ -1729,25 +1875,32 @@ __device__ __forceinline__ void phase_oproj(KArg ka, int l, int gwait, int mbar,
                 st_dev(part + (size_t)b * P.Hp + r, y0);
                 st_dev(part + (size_t)b * P.Hp + r + 1, y1);
             },
-            KTO, (size_t)P.o_rg * KTO);
+            D / kTileK, (size_t)P.o_rg * (D / kTileK));
     } else {
+        // per query head: the Sg workgroups of KV head g split into G
+        // groups, group hq applying the O-projection columns of query head
+        // g G + hq to its merged attention output, each workgroup for a
+        // range of rows
         const int g = blockIdx.x / P.Sg, part = blockIdx.x % P.Sg;
         if (g < P.nkv) {
+            int hq = 0;
+            while (hq + 1 < G && part >= (P.Sg * (hq + 1)) / G) ++hq;
+            const int p0 = (P.Sg * hq) / G, np = (P.Sg * (hq + 1)) / G - p0;
             int a0, a1;
-            split_range(P.o_rg, P.Sg, part, a0, a1);
-            // head g's chunk results (and, when the attention phase merges
-            // them, the merged output: one more arrival per layer)
-            constexpr bool merged = merge_last<D, G, false>();
-            const unsigned target = (unsigned)(l + 1) * (unsigned)(P.B * P.C + (merged ? 1 : 0));
-            weight_phase<false>(
-                P, S, Wo + (size_t)g * P.o_rg * KTO * kTileBytes, KTO, a0, a1 - a0,
-                [&]() { local_wait(P, P.cnt + P.nkv + g, target, ti); }, [&]() {},
+            split_range(P.o_rg, np, part - p0, a0, a1);
+            constexpr int KTq = D / kTileK;
+            // (the weight ring starts after the merge: its gather is then
+            // not queued behind the ring's loads)
+            weight_phase<false, false>(
+                P, S, Wo + (size_t)(g * G + hq) * P.o_rg * KTq * kTileBytes, KTq, a0, a1 - a0,
+                [&]() {}, [&]() {},
                 [&](int b) {
-                    if (merged)
-                        stage_vec(P.q + (size_t)b * P.nq * D + (size_t)g * G * D, G * D, G * D, S.a);
-                    else
-                        merge_chunks<D, G>(P, b, g, S.a, S.a + G * D);
-                    if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 3);
+                    if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 1);
+                    merge_ll<D, G>(P, l, b, g, hq, S);
+                    if (b == 0 && is_ctl_lane0()) {
+                        trace_stamp(P, ti, 2);
+                        trace_stamp(P, ti, 3);
+                    }
                 },
                 [&](int, int, int, uint16_t *) {}, epi);
         }
@@ -1822,9 +1975,11 @@ __device__ __forceinline__ void phase_gateup(KArg ka, int l, int gwait, int garr
             const float rs = rms_scale(S.sm, P.H, P.eps);   // the deferred RMSNorm scale
             gt *= rs;
             up *= rs;
-            st_dev(P.m + (size_t)b * P.Fp + (r >> 1), gt / (1.0f + expf(-gt)) * up);
+            st_ll_f(P.m_ll + (size_t)b * P.Fp + (r >> 1), gt / (1.0f + expf(-gt)) * up,
+                    ll_tag(P, l));
         });
-    if (member) local_arrive(P, P.cnt + 2 * P.nkv + j, ti);
+    // (the down projection polls the tagged words: no drain, no counter)
+    if (is_ctl_lane0()) trace_stamp(P, ti, 0);
 }
 
 // Batched path: the SwiGLU of the gate/up K-slice partials, m = silu(g) u with
@@ -1838,7 +1993,7 @@ __device__ __forceinline__ void fold_swiglu(const StepParams &P, const Lds &S, i
     // a thread's elements e0 + k stride, k < FE, are loaded together (one
     // memory round trip per KS / 4 slices instead of one per element)
     constexpr int FE = 4;
-    for (int e0 = blockIdx.x * kThreads + threadIdx.x; e0 - (int)threadIdx.x < total;
+    for (int e0 = blockIdx.x * kThreads + kl_tid(); e0 - (int)kl_tid() < total;
          e0 += FE * stride) {
         float gs[FE], us[FE];
 #pragma unroll
@@ -1927,16 +2082,26 @@ __device__ __forceinline__ void phase_down(KArg ka, int l, int gwait, int xbar, 
         if (j < P.Sc) {
             int a0, a1;
             split_range(P.down_rg, P.Rc, part, a0, a1);
-            const int kw = P.KTc * kTileK;
+            const int kw = P.KTc * kTileK, c0 = j * kw, nreal = max(0, min(kw, P.F - c0));
             weight_phase<false>(
                 P, S, Wd + (size_t)j * P.down_rg * P.KTc * kTileBytes, P.KTc, a0, a1 - a0,
-                [&]() {
-                    local_wait(P, P.cnt + 2 * P.nkv + j, (unsigned)(l + 1) * (unsigned)P.Rc, ti);
-                },
-                [&]() {},
+                [&]() {}, [&]() {},
                 [&](int b) {
-                    stage_vec(P.m + (size_t)b * P.Fp + (size_t)j * kw, kw, kw, S.a);
-                    if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 3);
+                    // block j of the SwiGLU output as tagged words, gathered
+                    // by the control wave (its loads are not queued behind
+                    // the weight ring); padding columns are zero
+                    if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 1);
+                    if ((kl_tid() >> 6) == kCtlWave)
+                        ll_gather<kDownGather>(
+                            P, nreal, ll_tag(P, l), kl_tid() & 63, 64,
+                            [&](int i) { return P.m_ll + (size_t)b * P.Fp + c0 + i; },
+                            [&](int i, unsigned v) { S.a[i] = __uint_as_float(v); });
+                    for (int i = nreal + kl_tid(); i < kw; i += kThreads) S.a[i] = 0.f;
+                    __syncthreads();
+                    if (b == 0 && is_ctl_lane0()) {
+                        trace_stamp(P, ti, 2);
+                        trace_stamp(P, ti, 3);
+                    }
                 },
                 [&](int, int, int, uint16_t *) {}, epi);
         }
@@ -1945,11 +2110,12 @@ __device__ __forceinline__ void phase_down(KArg ka, int l, int gwait, int xbar, 
 }
 
 // The final residual stream -> hidden_out (fp32).
+template <bool PS>
 __device__ __forceinline__ void copy_hidden(const StepParams &P) {
-    for (int idx = threadIdx.x; idx < P.B * P.H; idx += kThreads) {
+    for (int idx = kl_tid(); idx < P.B * P.H; idx += kThreads) {
         const int b = idx / P.H;
         const float x = from_fix((long long)ld_dev_u64(P.xf + (size_t)b * P.Hp + idx % P.H));
-        P.hidden_out[idx] = seq_ok(P, b) ? x : __builtin_nanf("");
+        P.hidden_out[idx] = ok_of<PS>(P, b) ? x : __builtin_nanf("");
     }
 }
 
@@ -1964,7 +2130,7 @@ __device__ __forceinline__ void phase_head(KArg ka, int gwait, int ti) {
         P, S, reinterpret_cast<const uint8_t *>(P.lm_head), P.Hp / kTileK, R.first, R.count,
         [&]() {
             if (gwait >= 0) bar_wait(P, gwait, ti);
-            if (!BAT && blockIdx.x == 0 && P.hidden_out) copy_hidden(P);
+            if (!BAT && blockIdx.x == 0 && P.hidden_out) copy_hidden<!BAT>(P);
         },
         [&]() {
             // (folds the last down projection's partials, x: xf2 -> xf), and
@@ -1974,7 +2140,7 @@ __device__ __forceinline__ void phase_head(KArg ka, int gwait, int ti) {
             __syncthreads();
             rms_table(P, S);
             if (is_ctl_lane0()) trace_stamp(P, ti, 3);
-            if (blockIdx.x == 0 && P.hidden_out) copy_hidden(P);
+            if (blockIdx.x == 0 && P.hidden_out) copy_hidden<!BAT>(P);
         },
         [&](int b) {
             stage_rms_deferred(P.xf + (size_t)b * P.Hp, P.final_norm, P.H, P.Hp, S.a, S.sm);
@@ -1986,11 +2152,16 @@ __device__ __forceinline__ void phase_head(KArg ka, int gwait, int ti) {
             const float rs = !BAT ? rms_scale(S.sm, P.H, P.eps) : rms_of(P, S, b);
             y0 *= rs;
             y1 *= rs;
-            if (!seq_ok(P, b)) y0 = y1 = __builtin_nanf("");
+            if (!ok_of<!BAT>(P, b)) y0 = y1 = __builtin_nanf("");
             float *lg = P.logits + (size_t)b * V;
             if (r < V) lg[r] = y0;
             if (r + 1 < V) lg[r + 1] = y1;
         });
+    // the step's last phase: the next step's tags (every workgroup of every
+    // launch of this step read the epoch at its start)
+    if (blockIdx.x == 0 && kl_tid() == 0)
+        __hip_atomic_store(P.epoch_ptr, ll_next_epoch(*launch_epoch(P), P.L), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
     if (is_ctl_lane0()) trace_stamp(P, ti, 0);
 }
 
