@@ -117,9 +117,13 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="llama8b-b1-ctx4096")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--modes", default="looped,per_layer",
+    ap.add_argument("--modes", default="looped,per_layer,per_layer_graph",
                     help="schedules to time; the first is the headline")
     ap.add_argument("--threads", type=int, default=0, help="host threads for input generation")
+    ap.add_argument("--loop-tokens", type=int, default=-1,
+                    help="tokens of the greedy token loop timed after the steps (its steady-state "
+                         "time per output token); -1: 128 unless the model is loaded layer by "
+                         "layer, 0: skip")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run the copy kernel used to scale HBM counters, then exit")
     args = ap.parse_args()
@@ -150,14 +154,20 @@ def main():
     # models whose weights would not fit twice in device memory (the 70B
     # shape) are generated and loaded one layer at a time
     big = bytemodel.step_bytes(cfg, 1, 0) > 40e9
+    # the token loop (below) needs room for its tokens: the model's positions
+    # reach that far
+    n_loop = args.loop_tokens if args.loop_tokens >= 0 else (0 if big else 128)
+    cap_loop = (P + n_loop + 63) // 64 * 64
+    max_seq = max(cap, cap_loop)
     weights = None
     if big:
         log(f"workload {args.workload}: generating and loading layer by layer ({nthr} threads)")
         seed = wl["seed_weights"]
         model = GpuModel.from_layers(
-            cfg, lambda l: {k: synth.layer_tensor(cfg, seed, l, k, nthr) for k in kb.LAYER_FIELDS},
+            cfg, lambda l: {k: synth.layer_tensor(cfg, seed, l, k, nthr)
+                            for k in synth.layer_names(cfg)},
             lambda: {k: synth.global_tensor(cfg, seed, k, nthr)
-                     for k in ("embed", "final_norm", "lm_head")}, B, cap)
+                     for k in ("embed", "final_norm", "lm_head")}, B, max_seq)
     else:
         log(f"workload {args.workload}: generating weights ({nthr} threads)")
         weights = synth.model_host(cfg, wl["seed_weights"], nthr)
@@ -165,7 +175,7 @@ def main():
     tokens = synth.tokens(cfg, wl["seed_tokens"], B)
     log(f"inputs ready in {time.perf_counter() - t:.1f}s; loading model")
     if not big:
-        model = GpuModel(cfg, weights, B, cap)
+        model = GpuModel(cfg, weights, B, max_seq)
     kv = KvCache(cfg, B, cap, k_host=K0, v_host=V0)
     toks = torch.from_numpy(tokens).cuda()
     pos = torch.full((B,), P, dtype=torch.int32, device="cuda")
@@ -210,12 +220,39 @@ def main():
                      "kernel": "kl_step_kernel (one launch per step)"},
         "modes": {m: r for m, r in res.items()},
         "dispatches_per_step": {"looped": 1, "per_layer": cfg["n_layers"] + 2,
-                                "per_op": 5 * cfg["n_layers"] + 2},
+                                "per_op": 5 * cfg["n_layers"] + 2,
+                                "per_layer_graph": cfg["n_layers"] + 2},
         "grid": {"workgroups": info.n_workgroups, "threads": info.threads_per_group,
                  "lds_bytes": info.lds_bytes},
     }
     if "per_layer" in res and head != "per_layer":
         out["speedup_vs_per_layer"] = res["per_layer"]["mean_ms"] / step_ms
+    # the greedy token loop (sampling fused into the LM head, each token fed to
+    # the next step on the device): steady-state time per output token over
+    # n tokens, in a cache with room for them
+    if n_loop > 0:
+        log(f"token loop: {n_loop} tokens from position {P} ({head})")
+        K1, V1 = synth.kv_cache_host(cfg, wl["seed_kv"], B, cap_loop, [P] * B, nthr)
+        kv_loop = KvCache(cfg, B, cap_loop, k_host=K1, v_host=V1)
+        del K1, V1
+        lg = torch.empty((B, cfg["vocab"]), dtype=torch.float32, device="cuda")
+        toks_out = torch.empty((n_loop, B), dtype=torch.int32, device="cuda")
+        model.greedy(toks, pos, kv_loop, n_loop, toks_out, lg, kb.MODES[head])   # warm-up
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        model.greedy(toks, pos, kv_loop, n_loop, toks_out, lg, kb.MODES[head])
+        e1.record()
+        torch.cuda.synchronize()
+        loop_ms = e0.elapsed_time(e1)
+        if model.device_error():
+            log("device error in the token loop")
+            sys.exit(1)
+        out["token_loop"] = {"tokens": n_loop, "mode": head, "ms_per_token": loop_ms / n_loop,
+                             "tok_s": B * n_loop / (loop_ms * 1e-3),
+                             "context": f"{P}..{P + n_loop - 1}",
+                             "first_tokens": toks_out[:4, 0].tolist()}
+        del kv_loop
     # every schedule computes the same bits (the timed launches' own outputs)
     for m in modes[1:]:
         out[f"bit_exact_{head}_vs_{m}"] = bool(torch.equal(outs[head].view(torch.int32),

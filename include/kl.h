@@ -19,6 +19,14 @@
  *   KL_MODE_PER_OP     one launch per operator group of a layer (the many-
  *                      kernels-per-layer GPU schedule of Sec. 2, Fig. 3 (i)):
  *                      5 L + 2 dispatches.
+ *   KL_MODE_PER_LAYER_GRAPH
+ *                      the per-layer schedule's L + 2 launches recorded once as
+ *                      a HIP graph and replayed (the graph alternative of the
+ *                      related work, Sec. 5): rebuilt when the caller's
+ *                      buffers (tokens, positions, batch, cache, outputs,
+ *                      trace) differ from the last call's; one graph per
+ *                      state.  Not available to kl_decode_step_noalloc or
+ *                      kl_decode_greedy.
  *
  * All modes run the same device code with the same work partition, so for the
  * same inputs they produce bit-identical logits, hidden states and KV writes.
@@ -52,7 +60,8 @@ typedef enum {
 typedef enum {
     KL_MODE_PER_LAYER = 0,
     KL_MODE_LOOPED = 1,
-    KL_MODE_PER_OP = 2
+    KL_MODE_PER_OP = 2,
+    KL_MODE_PER_LAYER_GRAPH = 3
 } kl_mode;
 
 /* Bits of the device error word (kl_get_device_error).  A sequence with a bad
@@ -64,22 +73,30 @@ typedef enum {
 #define KL_DEVERR_BARRIER  4   /* a grid barrier waited longer than its watchdog allows      */
 
 /* Model shape.  Supported: head_dim 64 or 128, n_heads a multiple of
- * n_kv_heads with n_heads / n_kv_heads <= 8, every dimension >= 1 and
- * hidden, ffn_dim multiples of 8.  max_batch bounds the batch of a step;
- * max_seq bounds positions (the RoPE table covers [0, max_seq)). */
+ * n_kv_heads with n_heads / n_kv_heads one of 1, 2, 4, 8 (and 3 with
+ * head_dim 128), n_heads at most the GPU's compute units, every dimension
+ * >= 1 and hidden, ffn_dim multiples of 8.  max_batch bounds the batch of a
+ * step; max_seq bounds positions (the RoPE table covers [0, max_seq)).
+ * qkv_bias: 1 if the Q/K/V projections carry biases (the Qwen2.5 variant of
+ * Table 2), else 0.  Tied embeddings (Llama 3.2) need no flag: pass the
+ * embedding table as the LM head. */
 typedef struct {
     int32_t n_layers, hidden, n_heads, n_kv_heads, head_dim, ffn_dim, vocab;
     float rope_theta, rms_eps;
     int32_t max_batch, max_seq;
+    int32_t qkv_bias;
 } kl_config;
 
 /* One decoder layer's weights: dev bf16, nn.Linear layout [out][in].
  *   attn_norm, ffn_norm [hidden]
  *   wq [n_heads*head_dim][hidden], wk, wv [n_kv_heads*head_dim][hidden]
  *   wo [hidden][n_heads*head_dim]
- *   w_gate, w_up [ffn_dim][hidden], w_down [hidden][ffn_dim]            */
+ *   w_gate, w_up [ffn_dim][hidden], w_down [hidden][ffn_dim]
+ *   bq [n_heads*head_dim], bk, bv [n_kv_heads*head_dim]: the Q/K/V biases,
+ *   required with cfg.qkv_bias and ignored (may be NULL) without         */
 typedef struct {
     const void *attn_norm, *wq, *wk, *wv, *wo, *ffn_norm, *w_gate, *w_up, *w_down;
+    const void *bq, *bk, *bv;
 } kl_layer_ptrs;
 
 /* Whole model: dev bf16 embed [vocab][hidden], final_norm [hidden],
@@ -172,6 +189,26 @@ kl_status kl_model_set_globals(kl_state *st, const void *embed, const void *fina
 kl_status kl_decode_step(kl_state *st, const int32_t *token_ids, const int32_t *positions,
                          int32_t batch, const kl_kv_cache *kv, float *logits_out,
                          float *hidden_out, void *stream, int32_t mode);
+
+/* Greedy token loop: n_steps decode steps in a row on 'stream', each one's
+ * sampled tokens feeding the next on the device (the Sampling block, executed
+ * once per output token, Sec. 2 and Fig. 3; the paper does not fix the
+ * sampler: greedy, the largest logit, the lowest index on ties).  Step n runs
+ * at positions[b] + n on the tokens step n - 1 sampled (step 0 on token_ids),
+ * writes K/V slot positions[b] + n of every layer, and samples in the LM
+ * head's epilogue (no separate kernel, no host round trip).
+ *   token_ids, positions, batch, kv, mode   as for kl_decode_step
+ *   n_steps     >= 1
+ *   tokens_out  dev int32 [n_steps][batch]: the token sampled at each step
+ *   logits_out  dev fp32 [batch][vocab]: every step's logits in turn (the last
+ *               step's remain)
+ * A sequence whose token or position is out of range at some step is skipped
+ * from then on (error bits as for kl_decode_step; it samples token -1).  Same
+ * host-side errors as kl_decode_step, plus n_steps < 1 or a NULL or
+ * misaligned tokens_out; nothing is enqueued then. */
+kl_status kl_decode_greedy(kl_state *st, const int32_t *token_ids, const int32_t *positions,
+                           int32_t batch, int32_t n_steps, const kl_kv_cache *kv,
+                           int32_t *tokens_out, float *logits_out, void *stream, int32_t mode);
 
 /* kl_decode_step for callers that cannot allocate device memory (code under
  * HIP graph capture, tight serving loops, harnesses that forbid allocation):

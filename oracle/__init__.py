@@ -31,10 +31,11 @@ class KloConfig(ctypes.Structure):
 
 
 LAYER_FIELDS = ["attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "w_gate", "w_up", "w_down"]
+BIAS_FIELDS = ["bq", "bk", "bv"]   # optional (absent: no bias)
 
 
 class KloLayer(ctypes.Structure):
-    _fields_ = [(n, ctypes.c_void_p) for n in LAYER_FIELDS]
+    _fields_ = [(n, ctypes.c_void_p) for n in LAYER_FIELDS + BIAS_FIELDS]
 
 
 def build() -> str:
@@ -168,7 +169,9 @@ def decode_step(cfg: dict, model: dict, tokens, positions, kcache: np.ndarray,
     layers = (KloLayer * L)()
     keep = []
     for l in range(L):
-        for n in LAYER_FIELDS:
+        for n in LAYER_FIELDS + BIAS_FIELDS:
+            if n not in model["layers"][l]:
+                continue
             a = np.ascontiguousarray(model["layers"][l][n], dtype=np.uint16)
             keep.append(a)
             setattr(layers[l], n, _p(a))
@@ -182,6 +185,38 @@ def decode_step(cfg: dict, model: dict, tokens, positions, kcache: np.ndarray,
     if rc != 0:
         raise ValueError("oracle: token or position out of range")
     return logits, hidden
+
+
+def argmax(logits) -> int:
+    """Greedy sampling, the Sampling block executed once per output token
+    (Sec. 2, Fig. 3).  The paper does not fix the sampler; the reading is
+    greedy: the index of the largest logit, the lowest such index on ties
+    (numpy's argmax returns the first maximum)."""
+    x = np.asarray(logits, dtype=np.float64)
+    assert x.ndim == 1 and x.size > 0 and not np.isnan(x).any()
+    return int(np.argmax(x))
+
+
+def greedy_decode(cfg: dict, model: dict, tokens, positions, kcache: np.ndarray,
+                  vcache: np.ndarray, n_steps: int, nthreads: int = 1, forced=None):
+    """n_steps decode steps in a row, each feeding its sampled token to the
+    next (the token loop around the step, Sec. 2, Fig. 3): step s runs at
+    positions + s on the previous step's argmax (the first step on 'tokens').
+    With 'forced' ([n_steps][B] tokens), step s >= 1 runs on forced[s - 1]
+    instead (to follow another implementation's choices); the argmax of every
+    step is still returned.  The caches are updated in place.  Returns
+    (sampled [n_steps][B] int32, logits of every step [n_steps][B][V])."""
+    toks = np.asarray(tokens, dtype=np.int32).copy()
+    pos = np.asarray(positions, dtype=np.int32)
+    B = toks.size
+    sampled = np.zeros((n_steps, B), dtype=np.int32)
+    all_logits = []
+    for s in range(n_steps):
+        lg, _ = decode_step(cfg, model, toks, pos + s, kcache, vcache, nthreads=nthreads)
+        all_logits.append(lg)
+        sampled[s] = [argmax(lg[b]) for b in range(B)]
+        toks = (sampled[s] if forced is None else np.asarray(forced[s], dtype=np.int32)).copy()
+    return sampled, np.stack(all_logits)
 
 
 def rel_l2(a, ref) -> float:

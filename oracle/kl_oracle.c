@@ -214,6 +214,13 @@ int32_t klo_decode_step(const klo_config *cfg, const uint16_t *embed,
             klo_gemv(nq * d, H, W->wq, u, q, nthreads);
             klo_gemv(nkv * d, H, W->wk, u, k, nthreads);
             klo_gemv(nkv * d, H, W->wv, u, v, nthreads);
+            /* Q/K/V biases where the model has them, before RoPE */
+            if (W->bq)
+                for (int32_t i = 0; i < nq * d; ++i) q[i] += klo_bf16_to_f64(W->bq[i]);
+            if (W->bk)
+                for (int32_t i = 0; i < nkv * d; ++i) k[i] += klo_bf16_to_f64(W->bk[i]);
+            if (W->bv)
+                for (int32_t i = 0; i < nkv * d; ++i) v[i] += klo_bf16_to_f64(W->bv[i]);
             for (int32_t h = 0; h < nq; ++h) klo_rope(d, cfg->rope_theta, p, q + (int64_t)h * d);
             for (int32_t g = 0; g < nkv; ++g) klo_rope(d, cfg->rope_theta, p, k + (int64_t)g * d);
 

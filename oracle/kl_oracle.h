@@ -23,6 +23,9 @@ typedef struct {
 
 typedef struct {   /* bf16, nn.Linear layout [out][in], row-major */
     const uint16_t *attn_norm, *wq, *wk, *wv, *wo, *ffn_norm, *w_gate, *w_up, *w_down;
+    /* optional Q/K/V biases (NULL: none), [n_heads*head_dim], [n_kv_heads*head_dim] x 2:
+     * the Qwen2.5 variant of the decoder (its Table 2 entry) adds them to the projections */
+    const uint16_t *bq, *bk, *bv;
 } klo_layer;
 
 double   klo_bf16_to_f64(uint16_t h);

@@ -23,14 +23,16 @@ KL_ERR_DEVICE_FAULT = -5
 KL_MODE_PER_LAYER = 0
 KL_MODE_LOOPED = 1
 KL_MODE_PER_OP = 2
-MODES = {"per_layer": KL_MODE_PER_LAYER, "looped": KL_MODE_LOOPED, "per_op": KL_MODE_PER_OP}
+KL_MODE_PER_LAYER_GRAPH = 3
+MODES = {"per_layer": KL_MODE_PER_LAYER, "looped": KL_MODE_LOOPED, "per_op": KL_MODE_PER_OP,
+         "per_layer_graph": KL_MODE_PER_LAYER_GRAPH}
 
 KL_DEVERR_TOKEN = 1
 KL_DEVERR_POSITION = 2
 KL_DEVERR_BARRIER = 4
 
 EXPORTED = ["kl_load_model", "kl_model_create", "kl_model_set_layer", "kl_model_set_globals",
-            "kl_decode_step", "kl_decode_step_noalloc", "kl_kv_cache_bytes",
+            "kl_decode_step", "kl_decode_step_noalloc", "kl_decode_greedy", "kl_kv_cache_bytes",
             "kl_get_device_error",
             "kl_get_info", "kl_set_trace", "kl_free_model", "kl_last_error"]
 
@@ -41,14 +43,15 @@ class kl_config(ctypes.Structure):
                 ("head_dim", ctypes.c_int32), ("ffn_dim", ctypes.c_int32),
                 ("vocab", ctypes.c_int32), ("rope_theta", ctypes.c_float),
                 ("rms_eps", ctypes.c_float), ("max_batch", ctypes.c_int32),
-                ("max_seq", ctypes.c_int32)]
+                ("max_seq", ctypes.c_int32), ("qkv_bias", ctypes.c_int32)]
 
 
 LAYER_FIELDS = ["attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "w_gate", "w_up", "w_down"]
+BIAS_FIELDS = ["bq", "bk", "bv"]   # only for models with Q/K/V biases
 
 
 class kl_layer_ptrs(ctypes.Structure):
-    _fields_ = [(n, ctypes.c_void_p) for n in LAYER_FIELDS]
+    _fields_ = [(n, ctypes.c_void_p) for n in LAYER_FIELDS + BIAS_FIELDS]
 
 
 class kl_weight_ptrs(ctypes.Structure):
@@ -103,6 +106,9 @@ def lib():
     L.kl_decode_step_noalloc.argtypes = [vp, vp, vp, i32, ctypes.POINTER(kl_kv_cache), vp, vp, vp,
                                          i32]
     L.kl_decode_step_noalloc.restype = i32
+    L.kl_decode_greedy.argtypes = [vp, vp, vp, i32, i32, ctypes.POINTER(kl_kv_cache), vp, vp, vp,
+                                   i32]
+    L.kl_decode_greedy.restype = i32
     L.kl_kv_cache_bytes.argtypes = [ctypes.POINTER(kl_config), i32, i32]
     L.kl_kv_cache_bytes.restype = ctypes.c_size_t
     L.kl_get_device_error.argtypes = [vp, ctypes.POINTER(i32)]
@@ -132,7 +138,8 @@ def _check(status: int) -> int:
 def make_config(model: dict, max_batch: int, max_seq: int) -> kl_config:
     return kl_config(model["n_layers"], model["hidden"], model["n_heads"], model["n_kv_heads"],
                      model["head_dim"], model["ffn_dim"], model["vocab"],
-                     float(model["rope_theta"]), float(model["rms_eps"]), max_batch, max_seq)
+                     float(model["rope_theta"]), float(model["rms_eps"]), max_batch, max_seq,
+                     1 if model.get("qkv_bias") else 0)
 
 
 def kl_load_model(cfg: kl_config, embed: int, final_norm: int, lm_head: int, layers: list,
@@ -140,8 +147,8 @@ def kl_load_model(cfg: kl_config, embed: int, final_norm: int, lm_head: int, lay
     """layers: list of dicts name -> device address.  Returns the state handle."""
     arr = (kl_layer_ptrs * len(layers))()
     for i, lay in enumerate(layers):
-        for n in LAYER_FIELDS:
-            setattr(arr[i], n, lay[n])
+        for n in LAYER_FIELDS + BIAS_FIELDS:
+            setattr(arr[i], n, lay.get(n))
     w = kl_weight_ptrs(embed, final_norm, lm_head, arr)
     out = ctypes.c_void_p()
     _check(lib().kl_load_model(ctypes.byref(cfg), ctypes.byref(w), stream, ctypes.byref(out)))
@@ -155,7 +162,7 @@ def kl_model_create(cfg: kl_config) -> int:
 
 
 def kl_model_set_layer(state: int, layer: int, ptrs: dict, stream: int = 0) -> None:
-    lp = kl_layer_ptrs(*[ptrs[n] for n in LAYER_FIELDS])
+    lp = kl_layer_ptrs(*[ptrs.get(n) for n in LAYER_FIELDS + BIAS_FIELDS])
     _check(lib().kl_model_set_layer(state, layer, ctypes.byref(lp), stream))
 
 
@@ -178,6 +185,14 @@ def kl_decode_step_noalloc(state: int, token_ids: int, positions: int, batch: in
     kv = kl_kv_cache(k, v, kv_batch, capacity)
     _check(lib().kl_decode_step_noalloc(state, token_ids, positions, batch, ctypes.byref(kv),
                                         logits_out, hidden_out, stream, mode))
+
+
+def kl_decode_greedy(state: int, token_ids: int, positions: int, batch: int, n_steps: int,
+                     k: int, v: int, kv_batch: int, capacity: int, tokens_out: int,
+                     logits_out: int, stream: int, mode: int) -> None:
+    kv = kl_kv_cache(k, v, kv_batch, capacity)
+    _check(lib().kl_decode_greedy(state, token_ids, positions, batch, n_steps, ctypes.byref(kv),
+                                  tokens_out, logits_out, stream, mode))
 
 
 def kl_kv_cache_bytes(cfg: kl_config, batch: int, capacity: int) -> int:

@@ -33,7 +33,8 @@ def paper_table1(n_params: float, n_layers: int, n_kv_heads: int, head_dim: int,
 
 def layer_weight_bytes(cfg) -> int:
     H, nq, nkv, d, F = (cfg[k] for k in ("hidden", "n_heads", "n_kv_heads", "head_dim", "ffn_dim"))
-    return 2 * (H * nq * d + 2 * H * nkv * d + nq * d * H + 3 * H * F + 2 * H)
+    bias = (nq + 2 * nkv) * d if cfg.get("qkv_bias") else 0   # Q/K/V biases (Qwen2.5)
+    return 2 * (H * nq * d + 2 * H * nkv * d + nq * d * H + 3 * H * F + 2 * H + bias)
 
 
 def step_bytes(cfg, batch: int, context: int) -> int:

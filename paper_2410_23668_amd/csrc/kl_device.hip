@@ -79,6 +79,33 @@ __global__ void kl_pack_rows_kernel(uint16_t *__restrict__ dst, int n_rg, int KT
     }
 }
 
+__global__ void kl_emit_tokens_kernel(int32_t *tokens, const unsigned long long *keys, int n) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) tokens[i] = key_token(keys[i]);
+}
+
+hipError_t launch_emit_tokens(int32_t *tokens, const unsigned long long *keys, int n,
+                              hipStream_t stream) {
+    hipLaunchKernelGGL(kl_emit_tokens_kernel, dim3((n + 255) / 256), dim3(256), 0, stream, tokens,
+                       keys, n);
+    return hipGetLastError();
+}
+
+__global__ void kl_pack_bias_kernel(float *dst, int rows, const int32_t *__restrict__ rowmap,
+                                    const uint16_t *b0, const uint16_t *b1, const uint16_t *b2) {
+    const int r = blockIdx.x * blockDim.x + threadIdx.x;
+    if (r >= rows) return;
+    const uint16_t *const src[3] = {b0, b1, b2};
+    dst[r] = pack_bias_row(r, rowmap, src);
+}
+
+hipError_t launch_pack_bias(float *dst, int rows, const int32_t *rowmap, const uint16_t *bq,
+                            const uint16_t *bk, const uint16_t *bv, hipStream_t stream) {
+    hipLaunchKernelGGL(kl_pack_bias_kernel, dim3((rows + 255) / 256), dim3(256), 0, stream, dst,
+                       rows, rowmap, bq, bk, bv);
+    return hipGetLastError();
+}
+
 __global__ void kl_gain_to_f32_kernel(float *dst, const uint16_t *src, int n, int npad) {
     for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < npad; i += gridDim.x * blockDim.x)
         dst[i] = (i < n) ? bf2f(src[i]) : 0.f;
@@ -115,6 +142,26 @@ hipError_t launch_step(const StepParams &p, int first_layer, int last_layer, int
     hipLaunchKernelGGL(k, dim3(p.nwg), dim3(kThreads), lds_bytes, stream, pc, first_layer,
                        last_layer, phases);
     return hipGetLastError();
+}
+
+hipError_t add_step_node(hipGraph_t g, hipGraphNode_t *node, const hipGraphNode_t *dep,
+                         const StepParams &p, int first_layer, int last_layer, int phases,
+                         bool cooperative, int lds_bytes) {
+    const StepKernel k = step_kernel_for(p.d, p.group, p.B >= kMfmaBatch);
+    if (!k) return hipErrorInvalidValue;
+    StepParams pc = p;   // (the node copies its arguments when it is added)
+    void *args[] = {&pc, &first_layer, &last_layer, &phases};
+    hipKernelNodeParams kp{};
+    kp.func = reinterpret_cast<void *>(k);
+    kp.gridDim = dim3(p.nwg);
+    kp.blockDim = dim3(kThreads);
+    kp.sharedMemBytes = (unsigned)lds_bytes;
+    kp.kernelParams = args;
+    hipError_t e = hipGraphAddKernelNode(node, g, dep, dep ? 1 : 0, &kp);
+    if (e != hipSuccess || !cooperative) return e;
+    hipKernelNodeAttrValue v{};
+    v.cooperative = 1;
+    return hipGraphKernelNodeSetAttribute(*node, hipKernelNodeAttributeCooperative, &v);
 }
 
 hipError_t launch_pack_rows(uint16_t *dst, int n_rg, int kt, int K, int ld, const int32_t *rowmap,

@@ -22,6 +22,7 @@ struct kl_state {
     int device;
     int Hp, Ap, Fp, qkv_rg, o_rg, gu_rg, down_rg, head_rg;
     size_t layer_stride, off_attn_norm, off_ffn_norm, off_qkv, off_o, off_gu, off_down;
+    size_t off_qkv_bias;
     size_t off_final_norm, off_lm_head, off_embed;
     uint8_t *arena;
     size_t arena_bytes;
@@ -33,6 +34,11 @@ struct kl_state {
     int Sg, Sc, Rc, KTc;
     int *err;                         // device error word (its own allocation, 256 B)
     unsigned *epoch;                  // first tag of the next step (in the same allocation)
+    unsigned long long *keys;         // argmax keys of the token loop: [2][max_batch]
+    // the per-layer schedule as a graph, for the caller buffers it was built on
+    hipGraph_t graph;
+    hipGraphExec_t graph_exec;
+    const void *graph_key[10];
     size_t off_dummy;                 // arena offset of a zero tile (the load rings' spare loads)
     unsigned long long *trace;
     int trace_max;
@@ -83,8 +89,11 @@ kl_status validate_config(const kl_config *c) {
         return fail(KL_ERR_UNSUPPORTED, "n_heads %d is not a multiple of n_kv_heads %d",
                     c->n_heads, c->n_kv_heads);
     const int g = c->n_heads / c->n_kv_heads;
-    if (g != 1 && g != 2 && g != 4 && g != 8)
-        return fail(KL_ERR_UNSUPPORTED, "query heads per KV head must be 1, 2, 4 or 8 (got %d)", g);
+    if (g != 1 && g != 2 && g != 4 && g != 8 && !(g == 3 && c->head_dim == 128))
+        return fail(KL_ERR_UNSUPPORTED, "query heads per KV head must be 1, 2, 4 or 8, or 3 with "
+                                        "head_dim 128 (got %d)", g);
+    if (c->qkv_bias != 0 && c->qkv_bias != 1)
+        return fail(KL_ERR_INVALID_ARGUMENT, "qkv_bias must be 0 or 1");
     if (c->hidden % 8 != 0 || c->ffn_dim % 8 != 0)
         return fail(KL_ERR_UNSUPPORTED, "hidden and ffn_dim must be multiples of 8");
     if (c->max_batch > 4096) return fail(KL_ERR_UNSUPPORTED, "max_batch above 4096");
@@ -135,8 +144,10 @@ void lds_layout_for(kl_state &s) {
     s.lds_red = amax;
     s.lds_sm = s.lds_red + kWaves * kRgBatch * kTileRows;
     s.lds_bar = s.lds_sm + 64;
-    // + the step's epoch, and position and validity per sequence
-    s.lds_bytes = (s.lds_bar + 2 * kBarGroups + 4 + 2 * kMfmaBatch) * (int)sizeof(float);
+    // + the step's epoch, position and validity per sequence, the head's
+    // argmax keys of a group of sequences
+    s.lds_bytes = (s.lds_bar + 2 * kBarGroups + 4 + 2 * kMfmaBatch + 2 * kGemmBatch) *
+                  (int)sizeof(float);
 }
 
 // Step scratch for a batch of B sequences (byte offsets from its base; every
@@ -244,6 +255,9 @@ void free_state(kl_state *s) {
     if (s->rope) (void)hipFree(s->rope);
     if (s->scratch) (void)hipFree(s->scratch);
     if (s->err) (void)hipFree(s->err);
+    if (s->keys) (void)hipFree(s->keys);
+    if (s->graph_exec) (void)hipGraphExecDestroy(s->graph_exec);
+    if (s->graph) (void)hipGraphDestroy(s->graph);
     if (s->rowmaps) (void)hipFree(s->rowmaps);
     delete s;
 }
@@ -285,6 +299,7 @@ StepParams base_params(const kl_state &s) {
     P.eps = c.rms_eps; P.max_seq = c.max_seq;
     P.arena = s.arena; P.layer_stride = s.layer_stride;
     P.off_attn_norm = s.off_attn_norm; P.off_ffn_norm = s.off_ffn_norm; P.off_qkv = s.off_qkv;
+    P.off_qkv_bias = s.off_qkv_bias; P.qkv_bias = c.qkv_bias ? 1 : 0;
     P.off_o = s.off_o; P.off_gu = s.off_gu; P.off_down = s.off_down;
     P.embed = reinterpret_cast<const uint16_t *>(s.arena + s.off_embed);
     P.final_norm = reinterpret_cast<const float *>(s.arena + s.off_final_norm);
@@ -314,12 +329,14 @@ size_t kl_kv_cache_bytes(const kl_config *cfg, int32_t batch, int32_t capacity) 
 }
 
 // Validates one layer's pointers.
-kl_status check_layer_ptrs(const kl_layer_ptrs &L, int l) {
+kl_status check_layer_ptrs(const kl_layer_ptrs &L, int l, bool bias) {
     const void *ps[] = {L.attn_norm, L.wq, L.wk, L.wv, L.wo, L.ffn_norm, L.w_gate, L.w_up,
-                        L.w_down};
-    for (const void *p : ps) {
-        if (!p) return fail(KL_ERR_INVALID_ARGUMENT, "layer %d has a NULL weight pointer", l);
-        if (!aligned(p, 2))
+                        L.w_down, L.bq, L.bk, L.bv};
+    for (int i = 0; i < (bias ? 12 : 9); ++i) {
+        if (!ps[i])
+            return fail(KL_ERR_INVALID_ARGUMENT, "layer %d has a NULL weight%s pointer", l,
+                        i >= 9 ? " (bias)" : "");
+        if (!aligned(ps[i], 2))
             return fail(KL_ERR_INVALID_ARGUMENT, "layer %d weight not 2-byte aligned", l);
     }
     return KL_OK;
@@ -365,6 +382,7 @@ kl_status kl_model_create(const kl_config *cfg, kl_state **out) {
     S->qkv_rg = Gm.qkv_rg; S->o_rg = Gm.o_rg; S->gu_rg = Gm.gu_rg; S->down_rg = Gm.down_rg;
     S->head_rg = Gm.head_rg;
     S->off_attn_norm = Gm.off_attn_norm; S->off_ffn_norm = Gm.off_ffn_norm;
+    S->off_qkv_bias = Gm.off_qkv_bias;
     S->off_qkv = Gm.off_qkv; S->off_o = Gm.off_o; S->off_gu = Gm.off_gu;
     S->off_down = Gm.off_down; S->layer_stride = Gm.layer_stride;
     S->off_final_norm = Gm.off_final_norm; S->off_lm_head = Gm.off_lm_head;
@@ -395,6 +413,8 @@ kl_status kl_model_create(const kl_config *cfg, kl_state **out) {
     TRY(hipMalloc(&S->err, 256));
     TRY(hipMemsetAsync(S->err, 0, 256, s));
     S->epoch = reinterpret_cast<unsigned *>(reinterpret_cast<uint8_t *>(S->err) + 128);
+    TRY(hipMalloc(&S->keys, (size_t)2 * c.max_batch * sizeof(unsigned long long)));
+    TRY(hipMemsetAsync(S->keys, 0, (size_t)2 * c.max_batch * sizeof(unsigned long long), s));
     {
         const unsigned first_tag = 1;
         TRY(hipMemcpyAsync(S->epoch, &first_tag, sizeof first_tag, hipMemcpyHostToDevice, s));
@@ -449,7 +469,7 @@ kl_status kl_model_set_layer(kl_state *S, int32_t l, const kl_layer_ptrs *w, voi
     const kl_config &c = S->cfg;
     if (l < 0 || l >= c.n_layers)
         return fail(KL_ERR_INVALID_ARGUMENT, "layer %d outside [0, %d)", l, c.n_layers);
-    kl_status st = check_layer_ptrs(*w, l);
+    kl_status st = check_layer_ptrs(*w, l, c.qkv_bias != 0);
     if (st != KL_OK) return st;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     const kl_layer_ptrs &Lw = *w;
@@ -460,6 +480,10 @@ kl_status kl_model_set_layer(kl_state *S, int32_t l, const kl_layer_ptrs *w, voi
     if (pe == hipSuccess)
         pe = launch_gain_to_f32(reinterpret_cast<float *>(Lb + S->off_ffn_norm),
                                 u16(Lw.ffn_norm), c.hidden, S->Hp, s);
+    if (pe == hipSuccess && c.qkv_bias)
+        pe = launch_pack_bias(reinterpret_cast<float *>(Lb + S->off_qkv_bias),
+                              c.n_kv_heads * S->qkv_rg * kTileRows, S->maps[kMapQkv], u16(Lw.bq),
+                              u16(Lw.bk), u16(Lw.bv), s);
     // the packed matrices of the layer (kl_layout.h: layer_pack_jobs)
     const uint16_t *srcs[] = {u16(Lw.wq), u16(Lw.wk), u16(Lw.wv), u16(Lw.wo),
                               u16(Lw.w_gate), u16(Lw.w_up), u16(Lw.w_down)};
@@ -516,7 +540,7 @@ kl_status kl_load_model(const kl_config *cfg, const kl_weight_ptrs *w, void *str
     if (!aligned(w->embed, 2) || !aligned(w->final_norm, 2) || !aligned(w->lm_head, 2))
         return fail(KL_ERR_INVALID_ARGUMENT, "weight pointers must be 2-byte aligned");
     for (int l = 0; l < cfg->n_layers; ++l) {
-        st = check_layer_ptrs(w->layers[l], l);
+        st = check_layer_ptrs(w->layers[l], l, cfg->qkv_bias != 0);
         if (st != KL_OK) return st;
     }
     kl_state *S = nullptr;
@@ -535,13 +559,11 @@ kl_status kl_load_model(const kl_config *cfg, const kl_weight_ptrs *w, void *str
     return KL_OK;
 }
 
-// One decode step: validation, the scratch binding, the launches of 'mode'.
-// With no_alloc the step's scratch is the library's static scratch of this
-// device (cleared first by a fill kernel on the stream), else the state's.
-static kl_status enqueue_step(kl_state *st, const int32_t *token_ids, const int32_t *positions,
-                              int32_t batch, const kl_kv_cache *kv, float *logits_out,
-                              float *hidden_out, void *stream, int32_t mode, bool no_alloc) {
-    g_last_error.clear();
+// Host-side checks shared by the step entry points (nothing is enqueued on
+// failure).
+static kl_status check_step_args(kl_state *st, const int32_t *token_ids,
+                                 const int32_t *positions, int32_t batch, const kl_kv_cache *kv,
+                                 const float *logits_out, const float *hidden_out, int32_t mode) {
     if (!st) return fail(KL_ERR_INVALID_ARGUMENT, "state is NULL");
     if (!token_ids || !positions || !logits_out || !kv || !kv->k || !kv->v)
         return fail(KL_ERR_INVALID_ARGUMENT, "token_ids, positions, kv, kv->k, kv->v and "
@@ -560,14 +582,102 @@ static kl_status enqueue_step(kl_state *st, const int32_t *token_ids, const int3
     if (kv->capacity < 1 || kv->capacity > c.max_seq)
         return fail(KL_ERR_INVALID_ARGUMENT, "kv capacity %d outside [1, max_seq=%d]",
                     kv->capacity, c.max_seq);
-    if (mode != KL_MODE_PER_LAYER && mode != KL_MODE_LOOPED && mode != KL_MODE_PER_OP)
+    if (mode != KL_MODE_PER_LAYER && mode != KL_MODE_LOOPED && mode != KL_MODE_PER_OP &&
+        mode != KL_MODE_PER_LAYER_GRAPH)
         return fail(KL_ERR_INVALID_ARGUMENT, "unknown mode %d", mode);
     int dev = -1;
     HIP_TRY(hipGetDevice(&dev));
     if (dev != st->device)
         return fail(KL_ERR_INVALID_ARGUMENT, "current device %d is not the model's device %d",
                     dev, st->device);
+    return KL_OK;
+}
 
+// The step's parameters with its scratch in 'base' (laid out by 'plan').
+static StepParams step_params(const kl_state &st, uint8_t *base, const ScratchPlan &plan,
+                              const int32_t *token_ids, const int32_t *positions, int32_t batch,
+                              const kl_kv_cache *kv, float *logits_out, float *hidden_out) {
+    StepParams P = base_params(st);
+    bind_scratch(P, base, plan, st);
+    P.tokens = token_ids; P.positions = positions; P.B = batch;
+    P.kc = reinterpret_cast<uint16_t *>(kv->k); P.vc = reinterpret_cast<uint16_t *>(kv->v);
+    P.kv_batch = kv->batch; P.cap = kv->capacity;
+    P.logits = logits_out; P.hidden_out = hidden_out;
+    P.C = std::max(1, st.Sg / batch);
+    return P;
+}
+
+// The launches of one step in schedule 'mode'.
+static hipError_t launch_schedule(const StepParams &P, int32_t mode, int lds, hipStream_t s) {
+    const int L = P.L;
+    const bool bat = P.B >= kMfmaBatch;
+    hipError_t e = hipSuccess;
+    if (mode == KL_MODE_LOOPED)
+        return launch_step(P, 0, L, kPhEmbed | kPhLayer | kPhHead, true, lds, s);
+    e = launch_step(P, 0, 0, kPhEmbed, false, lds, s);
+    if (mode == KL_MODE_PER_LAYER) {
+        for (int l = 0; l < L && e == hipSuccess; ++l)
+            e = launch_step(P, l, l + 1, kPhLayer, launch_waits_inside(kPhLayer, bat, P.C), lds, s);
+    } else {
+        const int ops[] = {kPhQkv, kPhAttn, kPhOproj, kPhGateUp, kPhDown};
+        for (int l = 0; l < L && e == hipSuccess; ++l)
+            for (int ph : ops)
+                if (e == hipSuccess)
+                    e = launch_step(P, l, l + 1, ph, launch_waits_inside(ph, bat, P.C), lds, s);
+    }
+    if (e == hipSuccess)
+        e = launch_step(P, 0, 0, kPhHead, launch_waits_inside(kPhHead, bat, P.C), lds, s);
+    return e;
+}
+
+// KL_MODE_PER_LAYER_GRAPH: the per-layer schedule's L + 2 launches as one
+// graph (kernel nodes in a chain; the nodes whose workgroups wait on each
+// other cooperative), built for the caller's buffers on first use and
+// replayed while they stay the same.  Every step of a model computes with the
+// same arguments apart from those buffers: the tags of the hand-offs are read
+// from device memory.
+static kl_status launch_layer_graph(kl_state *st, const StepParams &P, hipStream_t s) {
+    const void *key[10] = {P.tokens, P.positions, (const void *)(intptr_t)P.B, P.kc, P.vc,
+                           (const void *)(intptr_t)P.kv_batch, (const void *)(intptr_t)P.cap,
+                           P.logits, P.hidden_out, P.trace};
+    bool same = st->graph_exec != nullptr;
+    for (int i = 0; i < 10 && same; ++i) same = st->graph_key[i] == key[i];
+    if (!same) {
+        if (st->graph_exec) HIP_TRY(hipGraphExecDestroy(st->graph_exec));
+        if (st->graph) HIP_TRY(hipGraphDestroy(st->graph));
+        st->graph_exec = nullptr;
+        st->graph = nullptr;
+        HIP_TRY(hipGraphCreate(&st->graph, 0));
+        const bool bat = P.B >= kMfmaBatch;
+        const int lds = st->lds_bytes;
+        hipGraphNode_t prev = nullptr, node = nullptr;
+        HIP_TRY(add_step_node(st->graph, &node, nullptr, P, 0, 0, kPhEmbed, false, lds));
+        for (int l = 0; l < P.L; ++l) {
+            prev = node;
+            HIP_TRY(add_step_node(st->graph, &node, &prev, P, l, l + 1, kPhLayer,
+                                  launch_waits_inside(kPhLayer, bat, P.C), lds));
+        }
+        prev = node;
+        HIP_TRY(add_step_node(st->graph, &node, &prev, P, 0, 0, kPhHead,
+                              launch_waits_inside(kPhHead, bat, P.C), lds));
+        HIP_TRY(hipGraphInstantiate(&st->graph_exec, st->graph, nullptr, nullptr, 0));
+        for (int i = 0; i < 10; ++i) st->graph_key[i] = key[i];
+    }
+    HIP_TRY(hipGraphLaunch(st->graph_exec, s));
+    return KL_OK;
+}
+
+// One decode step: validation, the scratch binding, the launches of 'mode'.
+// With no_alloc the step's scratch is the library's static scratch of this
+// device (cleared first by a fill kernel on the stream), else the state's.
+static kl_status enqueue_step(kl_state *st, const int32_t *token_ids, const int32_t *positions,
+                              int32_t batch, const kl_kv_cache *kv, float *logits_out,
+                              float *hidden_out, void *stream, int32_t mode, bool no_alloc) {
+    g_last_error.clear();
+    kl_status stt = check_step_args(st, token_ids, positions, batch, kv, logits_out, hidden_out,
+                                    mode);
+    if (stt != KL_OK) return stt;
+    const kl_config &c = st->cfg;
     ScratchPlan plan;
     uint8_t *base;
     if (no_alloc) {
@@ -583,36 +693,19 @@ static kl_status enqueue_step(kl_state *st, const int32_t *token_ids, const int3
         plan = plan_scratch(*st, c.max_batch);
         base = st->scratch;
     }
-    StepParams P = base_params(*st);
-    bind_scratch(P, base, plan, *st);
-    P.tokens = token_ids; P.positions = positions; P.B = batch;
-    P.kc = reinterpret_cast<uint16_t *>(kv->k); P.vc = reinterpret_cast<uint16_t *>(kv->v);
-    P.kv_batch = kv->batch; P.cap = kv->capacity;
-    P.logits = logits_out; P.hidden_out = hidden_out;
-    P.C = std::max(1, st->Sg / batch);
-
+    const StepParams P = step_params(*st, base, plan, token_ids, positions, batch, kv, logits_out,
+                                     hidden_out);
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    const int L = c.n_layers, lds = st->lds_bytes;
-    const bool bat = batch >= kMfmaBatch;
     // (the static scratch holds whatever the last call on this device left:
     // it starts from zero like a fresh allocation)
-    if (no_alloc) HIP_TRY(launch_zero(base, plan.total, s));
-    if (mode == KL_MODE_LOOPED) {
-        HIP_TRY(launch_step(P, 0, L, kPhEmbed | kPhLayer | kPhHead, true, lds, s));
-    } else if (mode == KL_MODE_PER_LAYER) {
-        HIP_TRY(launch_step(P, 0, 0, kPhEmbed, false, lds, s));
-        for (int l = 0; l < L; ++l)
-            HIP_TRY(launch_step(P, l, l + 1, kPhLayer, launch_waits_inside(kPhLayer, bat, P.C),
-                                lds, s));
-        HIP_TRY(launch_step(P, 0, 0, kPhHead, launch_waits_inside(kPhHead, bat, P.C), lds, s));
-    } else {
-        HIP_TRY(launch_step(P, 0, 0, kPhEmbed, false, lds, s));
-        const int ops[] = {kPhQkv, kPhAttn, kPhOproj, kPhGateUp, kPhDown};
-        for (int l = 0; l < L; ++l)
-            for (int ph : ops)
-                HIP_TRY(launch_step(P, l, l + 1, ph, launch_waits_inside(ph, bat, P.C), lds, s));
-        HIP_TRY(launch_step(P, 0, 0, kPhHead, launch_waits_inside(kPhHead, bat, P.C), lds, s));
+    if (mode == KL_MODE_PER_LAYER_GRAPH) {
+        if (no_alloc)
+            return fail(KL_ERR_INVALID_ARGUMENT, "the graph schedule is not available without "
+                                                 "allocation (building a graph allocates)");
+        return launch_layer_graph(st, P, s);
     }
+    if (no_alloc) HIP_TRY(launch_zero(base, plan.total, s));
+    HIP_TRY(launch_schedule(P, mode, st->lds_bytes, s));
     return KL_OK;
 }
 
@@ -629,6 +722,37 @@ kl_status kl_decode_step_noalloc(kl_state *st, const int32_t *token_ids,
                                  int32_t mode) {
     return enqueue_step(st, token_ids, positions, batch, kv, logits_out, hidden_out, stream, mode,
                         true);
+}
+
+kl_status kl_decode_greedy(kl_state *st, const int32_t *token_ids, const int32_t *positions,
+                           int32_t batch, int32_t n_steps, const kl_kv_cache *kv,
+                           int32_t *tokens_out, float *logits_out, void *stream, int32_t mode) {
+    g_last_error.clear();
+    kl_status stt = check_step_args(st, token_ids, positions, batch, kv, logits_out, nullptr, mode);
+    if (stt != KL_OK) return stt;
+    if (n_steps < 1) return fail(KL_ERR_INVALID_ARGUMENT, "n_steps %d < 1", n_steps);
+    if (mode == KL_MODE_PER_LAYER_GRAPH)
+        return fail(KL_ERR_INVALID_ARGUMENT, "the token loop runs the looped, per-layer or "
+                                             "per-op schedule");
+    if (!tokens_out || !aligned(tokens_out, 4))
+        return fail(KL_ERR_INVALID_ARGUMENT, "tokens_out must be a 4-byte aligned pointer");
+    const kl_config &c = st->cfg;
+    StepParams P = step_params(*st, st->scratch, plan_scratch(*st, c.max_batch), token_ids,
+                               positions, batch, kv, logits_out, nullptr);
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    // step n: positions + n; its head leaves the argmax keys in keys[n % 2],
+    // from which step n + 1's embedding takes its tokens (recording them as
+    // tokens_out[n])
+    for (int32_t n = 0; n < n_steps; ++n) {
+        P.pos_add = n;
+        P.amax = st->keys + (size_t)(n % 2) * c.max_batch;
+        P.tok_keys = n == 0 ? nullptr : st->keys + (size_t)((n - 1) % 2) * c.max_batch;
+        P.tok_emit = n == 0 ? nullptr : tokens_out + (size_t)(n - 1) * batch;
+        HIP_TRY(launch_schedule(P, mode, st->lds_bytes, s));
+    }
+    HIP_TRY(launch_emit_tokens(tokens_out + (size_t)(n_steps - 1) * batch,
+                               st->keys + (size_t)((n_steps - 1) % 2) * c.max_batch, batch, s));
+    return KL_OK;
 }
 
 kl_status kl_get_device_error(kl_state *st, int32_t *code) {

@@ -69,12 +69,19 @@ struct StepParams {
     const uint8_t *arena;      // layer 0 base
     size_t layer_stride;       // bytes between consecutive layers
     size_t off_attn_norm, off_ffn_norm, off_qkv, off_o, off_gu, off_down;
+    size_t off_qkv_bias;       // fp32 Q/K/V biases in packed row order (qkv_bias models)
+    int qkv_bias;
     const uint16_t *embed;     // [V][H] bf16, row-major
     const float *final_norm;   // [Hp]
     const uint16_t *lm_head;   // packed tiles
     const float2 *rope;        // [max_seq][d/2] (cos, sin)
     // step arguments
     const int32_t *tokens, *positions;
+    // token loop (greedy sampling, one step per launch sequence):
+    int pos_add;               // added to every position (step s of a loop: s)
+    const unsigned long long *tok_keys;   // non-null: token b is the previous step's argmax
+    int32_t *tok_emit;         // non-null: the embedding phase records the tokens it takes
+    unsigned long long *amax;  // non-null: the head leaves each sequence's argmax key here
     int B;
     uint16_t *kc, *vc;         // [L][kv_batch][nkv][cap][d]
     int kv_batch, cap;
@@ -130,6 +137,11 @@ StepKernel step_kernel_d128_batched(int group);
 
 hipError_t launch_step(const StepParams &p, int first_layer, int last_layer, int phases,
                        bool cooperative, int lds_bytes, hipStream_t stream);
+// Adds the same launch as a kernel node of graph g after 'dep' (null: none);
+// cooperative nodes carry the graph's cooperative attribute.
+hipError_t add_step_node(hipGraph_t g, hipGraphNode_t *node, const hipGraphNode_t *dep,
+                         const StepParams &p, int first_layer, int last_layer, int phases,
+                         bool cooperative, int lds_bytes);
 hipError_t step_kernel_setup(int d, int group, int lds_bytes, int *max_blocks_per_cu);
 
 // The static scratch of kl_decode_step_noalloc: one array per device, of
@@ -141,9 +153,17 @@ hipError_t static_scratch_address(int device, uint8_t **out);
 // Zero 'bytes' (a multiple of 16, 16-byte aligned) at p with a fill kernel.
 hipError_t launch_zero(void *p, size_t bytes, hipStream_t stream);
 
+// tokens[b] = the token of argmax key keys[b] (-1 where there is none), b < n.
+hipError_t launch_emit_tokens(int32_t *tokens, const unsigned long long *keys, int n,
+                              hipStream_t stream);
+
 hipError_t launch_pack_rows(uint16_t *dst, int n_rg, int kt, int K, int ld, const int32_t *rowmap,
                             const uint16_t *src0, const uint16_t *src1, const uint16_t *src2,
                             hipStream_t stream);
+// dst[r] = fp32 bias of packed q/k/v row r (rowmap as for the matrix; the
+// sources bq, bk, bv are source ids 0, 1, 2).
+hipError_t launch_pack_bias(float *dst, int rows, const int32_t *rowmap, const uint16_t *bq,
+                            const uint16_t *bk, const uint16_t *bv, hipStream_t stream);
 hipError_t launch_gain_to_f32(float *dst, const uint16_t *src, int n, int npad,
                               hipStream_t stream);
 

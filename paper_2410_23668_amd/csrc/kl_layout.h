@@ -57,6 +57,17 @@ KL_HD inline void pack_chunk(size_t idx, int KT, int K, int ld, const int32_t *r
     }
 }
 
+// Packed bias row r (fp32): the q/k/v bias of the source row the q/k/v row
+// map gives r, zero for a padding row.
+KL_HD inline float pack_bias_row(int r, const int32_t *rowmap, const uint16_t *const src[3]) {
+    const int m = rowmap[r];
+    if (m < 0) return 0.f;
+    const uint32_t bits = (uint32_t)src[m >> 28][m & 0x0fffffff] << 16;
+    float f;
+    __builtin_memcpy(&f, &bits, 4);
+    return f;
+}
+
 inline size_t layout_align(size_t v, size_t a) { return (v + a - 1) / a * a; }
 inline int layout_pad_k(int v) { return (v + kTileK - 1) / kTileK * kTileK; }
 
@@ -78,11 +89,13 @@ struct Geometry {
     int qkv_rg;                // row groups of one KV head's q/k/v block
     int o_rg, gu_rg, down_rg, head_rg;
     // arena: [layer 0 .. L-1][final norm][LM head][embedding][zero tile]
-    size_t off_attn_norm, off_ffn_norm, off_qkv, off_o, off_gu, off_down, layer_stride;
+    size_t off_attn_norm, off_ffn_norm, off_qkv_bias, off_qkv, off_o, off_gu, off_down,
+        layer_stride;
     size_t off_final_norm, off_lm_head, off_embed, off_dummy, arena_bytes;
 };
 
-// Per layer: the two norm gains (fp32, padded to Hp), the q/k/v matrix
+// Per layer: the two norm gains (fp32, padded to Hp), the Q/K/V biases if
+// the model has them (fp32, packed row order), the q/k/v matrix
 // grouped per KV head (its G query heads, its key, its value; query and key
 // rows in rotation pairs (i, i + d/2)), the O projection per query head (its
 // d columns), gate/up with rows interleaved (gate i, up i), the down
@@ -110,6 +123,9 @@ inline Geometry layout_geometry(const kl_config &c, int nwg) {
     size_t off = 0;
     G.off_attn_norm = off; off = layout_align(off + (size_t)G.Hp * 4, A);
     G.off_ffn_norm = off;  off = layout_align(off + (size_t)G.Hp * 4, A);
+    // Q/K/V biases (fp32, in the packed row order of the q/k/v matrix)
+    G.off_qkv_bias = off;
+    if (c.qkv_bias) off = layout_align(off + (size_t)c.n_kv_heads * G.qkv_rg * kTileRows * 4, A);
     G.off_qkv = off;
     off = layout_align(off + (size_t)c.n_kv_heads * G.qkv_rg * G.KTH * kTileBytes, A);
     G.off_o = off;

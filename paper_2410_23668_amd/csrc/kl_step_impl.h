@@ -129,17 +129,40 @@ __device__ __forceinline__ void split_range(int n, int parts, int i, int &a, int
 // step with clamped values (every read stays in bounds), but writes nothing
 // the caller owns except NaN logits and hidden state: its K/V slots are left
 // untouched.  The embedding phase raises the matching error bits.
+// Greedy sampling (the Sampling block, Sec. 2, Fig. 3) reduces each
+// candidate logit to a 64-bit key, (order-preserving bits of the logit << 32)
+// | (0xFFFFFFFF - index): the largest key is the largest logit and, among equal
+// logits, the lowest index.  NaN logits (a skipped sequence) are no
+// candidates; key 0 means none and decodes to token -1 (out of range).
+__device__ __forceinline__ unsigned long long argmax_key(float v, int idx) {
+    const unsigned u = __float_as_uint(v);
+    const unsigned ord = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+    return ((unsigned long long)ord << 32) | (0xFFFFFFFFu - (unsigned)idx);
+}
+__device__ __forceinline__ int key_token(unsigned long long k) {
+    return k ? (int)(0xFFFFFFFFu - (unsigned)k) : -1;
+}
+__device__ __forceinline__ int raw_tok(const StepParams &P, int b) {
+    if (P.tok_keys)
+        return key_token(__hip_atomic_load(const_cast<unsigned long long *>(P.tok_keys + b),
+                                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+    return P.tokens[b];
+}
+__device__ __forceinline__ int raw_pos(const StepParams &P, int b) {
+    return P.positions[b] + P.pos_add;
+}
+
 __device__ __forceinline__ int eff_pos(const StepParams &P, int b) {
-    const int p = P.positions[b];
+    const int p = raw_pos(P, b);
     const int lim = min(P.cap, P.max_seq);
     return p < 0 ? 0 : (p >= lim ? lim - 1 : p);
 }
 __device__ __forceinline__ int eff_tok(const StepParams &P, int b) {
-    const int t = P.tokens[b];
+    const int t = raw_tok(P, b);
     return (t < 0 || t >= P.V) ? 0 : t;
 }
 __device__ __forceinline__ bool seq_ok(const StepParams &P, int b) {
-    const int t = P.tokens[b], p = P.positions[b];
+    const int t = raw_tok(P, b), p = raw_pos(P, b);
     return t >= 0 && t < P.V && p >= 0 && p < min(P.cap, P.max_seq);
 }
 // On the per-sequence path (batch < kMfmaBatch) both are read once per launch
@@ -493,6 +516,10 @@ __device__ __forceinline__ unsigned *launch_epoch(const StepParams &P) {
 // (after the epoch: position and validity of each sequence, per-sequence path)
 __device__ __forceinline__ int *seq_table(const StepParams &P) {
     return reinterpret_cast<int *>(lds_layout(kl_smem, P).bar + kBarGroups) + 4;
+}
+// (then: the head's argmax keys of up to kGemmBatch sequences)
+__device__ __forceinline__ unsigned long long *amax_slots(const StepParams &P) {
+    return reinterpret_cast<unsigned long long *>(seq_table(P) + 2 * kMfmaBatch);
 }
 
 // ---------------------------------------------------------------- activations
@@ -1065,13 +1092,18 @@ __device__ __forceinline__ void gemm_rows(const uint8_t *__restrict__ W, int KT,
 // as bf16 chunks: prep() runs once after wait(), both once the first weight
 // loads are in flight; stageb(c, b0, nb, buf) fills chunk c for sequences
 // b0 .. b0 + nb - 1 (the control wave's memory-to-LDS copies).
+// (done(b0, nb) runs in every thread after the matrix-core path's group of
+// sequences b0 .. b0 + nb - 1)
+struct NoGroupDone {
+    __device__ void operator()(int, int) const {}
+};
 template <bool BAT, bool Early = true, class Wait, class Prep, class Stage1, class StageB,
-          class Epi>
+          class Epi, class Done = NoGroupDone>
 __device__ __forceinline__ void weight_phase(const StepParams &P, const Lds &S,
                                              const uint8_t *W, int KT, int first, int count,
                                              Wait &&wait, Prep &&prep, Stage1 &&stage1,
                                              StageB &&stageb, Epi &&epi, int ktg = 0,
-                                             size_t gstride = 0) {
+                                             size_t gstride = 0, Done done = Done()) {
     if constexpr (!BAT) {
         gemv_phase<Early>(W, KT, first, count, 1, P.B, S.a, S.red, P.dummy, wait, stage1, epi);
         return;
@@ -1087,6 +1119,7 @@ __device__ __forceinline__ void weight_phase(const StepParams &P, const Lds &S,
                       }
                   },
                   [&](int c, uint16_t *buf) { stageb(c, b0, nb, buf); }, epi);
+        done(b0, nb);
     }
 }
 
@@ -1281,11 +1314,14 @@ __device__ __forceinline__ void phase_embed(KArg ka, int gwait, int garrive, int
     if (gwait >= 0) bar_wait(P, gwait, ti);
     if (blockIdx.x == 0) {
         for (int b = kl_tid(); b < P.B; b += kThreads) {
-            const int t = P.tokens[b], p = P.positions[b];
+            const int t = raw_tok(P, b), p = raw_pos(P, b);
             int bits = 0;
             if (t < 0 || t >= P.V) bits |= KL_DEVERR_TOKEN;
             if (p < 0 || p >= P.cap || p >= P.max_seq) bits |= KL_DEVERR_POSITION;
             if (bits) atomicOr(P.err, bits);
+            // token loop: record the token taken, clear this step's argmax
+            if (P.tok_emit) P.tok_emit[b] = t;
+            if (P.amax) st_dev_u64(P.amax + b, 0ull);
         }
         // (the batched RMSNorm counters exist, and are used, in batched steps only)
         const int nc = 2 * P.nkv + P.Sc +
@@ -1376,7 +1412,15 @@ __device__ __forceinline__ void fold_qkv(const StepParams &P, const Lds &S, int 
             }
         }
         const float r = rms_of(P, S, b);   // the deferred RMSNorm scale
-        qkv_store<false>(P, l, b, g, lr, y0 * r, y1 * r,
+        y0 *= r;
+        y1 *= r;
+        if (P.qkv_bias) {   // (packed row order)
+            const float *bias = reinterpret_cast<const float *>(
+                P.arena + (size_t)l * P.layer_stride + P.off_qkv_bias);
+            y0 += bias[g * hrows + lr];
+            y1 += bias[g * hrows + lr + 1];
+        }
+        qkv_store<false>(P, l, b, g, lr, y0, y1,
                          [&](int p, int i) { return P.rope[(size_t)p * half + i]; });
     }
 }
@@ -1448,7 +1492,14 @@ __device__ __forceinline__ void phase_qkv(KArg ka, int l, int gwait, int qbar, i
         [&](int, int, int, uint16_t *) {},
         [&](int b, int r, float y0, float y1) {
             const float rs = rms_scale(S.sm, P.H, P.eps);   // the deferred RMSNorm scale
-            qkv_store<true>(P, l, b, g, r - row0, y0 * rs, y1 * rs, [&](int, int i) {
+            y0 *= rs;
+            y1 *= rs;
+            if (P.qkv_bias) {   // (packed row order)
+                const float *bias = reinterpret_cast<const float *>(Lb + P.off_qkv_bias);
+                y0 += bias[r];
+                y1 += bias[r + 1];
+            }
+            qkv_store<true>(P, l, b, g, r - row0, y0, y1, [&](int, int i) {
                 return reinterpret_cast<const float2 *>(S.a + 2 * P.Hp)[i];
             }, ll_tag(P, l));
         });
@@ -2126,6 +2177,23 @@ __device__ __forceinline__ void phase_head(KArg ka, int gwait, int ti) {
     const Lds S = lds_layout(kl_smem, P);
     const RgRange R = own_rgs(P.head_rg, P);
     const int V = P.V;
+    // greedy sampling: this workgroup's best key per sequence (LDS atomics),
+    // then one device-scope atomic per sequence into P.amax
+    unsigned long long *best = amax_slots(P);
+    const bool sample = P.amax != nullptr;
+    if (sample && kl_tid() < kGemmBatch) best[kl_tid()] = 0ull;   // (staging barriers follow)
+    auto flush = [&](int b0, int nb) {
+        if (!sample) return;
+        __syncthreads();
+        const int t = kl_tid();
+        if (t < nb) {
+            const unsigned long long k = best[t];
+            if (k) __hip_atomic_fetch_max(P.amax + b0 + t, k, __ATOMIC_RELAXED,
+                                          __HIP_MEMORY_SCOPE_AGENT);
+            best[t] = 0ull;
+        }
+        __syncthreads();
+    };
     weight_phase<BAT>(
         P, S, reinterpret_cast<const uint8_t *>(P.lm_head), P.Hp / kTileK, R.first, R.count,
         [&]() {
@@ -2152,11 +2220,20 @@ __device__ __forceinline__ void phase_head(KArg ka, int gwait, int ti) {
             const float rs = !BAT ? rms_scale(S.sm, P.H, P.eps) : rms_of(P, S, b);
             y0 *= rs;
             y1 *= rs;
-            if (!ok_of<!BAT>(P, b)) y0 = y1 = __builtin_nanf("");
+            const bool ok = ok_of<!BAT>(P, b);
+            if (!ok) y0 = y1 = __builtin_nanf("");
             float *lg = P.logits + (size_t)b * V;
             if (r < V) lg[r] = y0;
             if (r + 1 < V) lg[r + 1] = y1;
-        });
+            if (sample && ok) {
+                unsigned long long k = (r < V) ? argmax_key(y0, r) : 0ull;
+                if (r + 1 < V) k = max(k, argmax_key(y1, r + 1));
+                __hip_atomic_fetch_max(best + (BAT ? b % kGemmBatch : b), k, __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_WORKGROUP);
+            }
+        },
+        0, 0, [&](int b0, int nb) { flush(b0, nb); });
+    if (!BAT) flush(0, P.B);
     // the step's last phase: the next step's tags (every workgroup of every
     // launch of this step read the epoch at its start)
     if (blockIdx.x == 0 && kl_tid() == 0)

@@ -34,7 +34,9 @@ class GpuModel:
         layers = []
         for l, lay in enumerate(weights["layers"]):
             ptrs = {}
-            for n in kb.LAYER_FIELDS:
+            for n in kb.LAYER_FIELDS + kb.BIAS_FIELDS:
+                if n not in lay:
+                    continue
                 t = _dev_u16(lay[n], self.device)
                 src[(l, n)] = t
                 ptrs[n] = t.data_ptr()
@@ -62,7 +64,8 @@ class GpuModel:
         h = stream_handle(stream)
         for l in range(model_cfg["n_layers"]):
             lay = layer_fn(l)
-            src = {n: _dev_u16(lay[n], self.device) for n in kb.LAYER_FIELDS}
+            src = {n: _dev_u16(lay[n], self.device)
+                   for n in kb.LAYER_FIELDS + kb.BIAS_FIELDS if n in lay}
             torch.cuda.synchronize(self.device)
             kb.kl_model_set_layer(self.state, l, {n: t.data_ptr() for n, t in src.items()}, h)
             del src, lay
@@ -93,6 +96,17 @@ class GpuModel:
                           kv.k.data_ptr(), kv.v.data_ptr(), kv.batch, kv.capacity,
                           logits.data_ptr(), hidden.data_ptr() if hidden is not None else None,
                           stream_handle(stream), mode)
+
+    def greedy(self, tokens: torch.Tensor, positions: torch.Tensor, kv: "KvCache", n_steps: int,
+               tokens_out: torch.Tensor, logits: torch.Tensor, mode: int,
+               stream: torch.cuda.Stream | None = None) -> None:
+        assert tokens.dtype == torch.int32 and positions.dtype == torch.int32
+        B = tokens.numel()
+        assert tokens_out.dtype == torch.int32 and tokens_out.shape == (n_steps, B)
+        assert logits.dtype == torch.float32 and logits.shape == (B, self.model_cfg["vocab"])
+        kb.kl_decode_greedy(self.state, tokens.data_ptr(), positions.data_ptr(), B, n_steps,
+                            kv.k.data_ptr(), kv.v.data_ptr(), kv.batch, kv.capacity,
+                            tokens_out.data_ptr(), logits.data_ptr(), stream_handle(stream), mode)
 
     def close(self):
         if getattr(self, "state", None):

@@ -27,8 +27,10 @@ _lib = None
 KIND = {"attn_norm": 0, "wq": 1, "wk": 2, "wv": 3, "wo": 4,
         "ffn_norm": 5, "w_gate": 6, "w_up": 7, "w_down": 8}
 GLOBAL = {"embed": 0, "final_norm": 1, "lm_head": 2}
+BIAS_KIND = {"bq": 9, "bk": 10, "bv": 11}   # models with Q/K/V biases (cfg["qkv_bias"])
 WEIGHT_STD = 0.02
 NORM_STD = 0.01
+BIAS_STD = 0.5     # of the order of the projections themselves, so a dropped bias shows
 
 
 def build() -> str:
@@ -106,9 +108,17 @@ def word(seed: int, stream_id: int, i: int) -> int:
 
 def layer_shapes(cfg) -> dict:
     H, d, nq, nkv, F = cfg["hidden"], cfg["head_dim"], cfg["n_heads"], cfg["n_kv_heads"], cfg["ffn_dim"]
-    return {"attn_norm": (H,), "wq": (nq * d, H), "wk": (nkv * d, H), "wv": (nkv * d, H),
-            "wo": (H, nq * d), "ffn_norm": (H,), "w_gate": (F, H), "w_up": (F, H),
-            "w_down": (H, F)}
+    shapes = {"attn_norm": (H,), "wq": (nq * d, H), "wk": (nkv * d, H), "wv": (nkv * d, H),
+              "wo": (H, nq * d), "ffn_norm": (H,), "w_gate": (F, H), "w_up": (F, H),
+              "w_down": (H, F)}
+    if cfg.get("qkv_bias"):
+        shapes.update(bq=(nq * d,), bk=(nkv * d,), bv=(nkv * d,))
+    return shapes
+
+
+def layer_names(cfg) -> list:
+    """The layer tensors of this model (the biases only where it has them)."""
+    return list(KIND) + (list(BIAS_KIND) if cfg.get("qkv_bias") else [])
 
 
 def global_shapes(cfg) -> dict:
@@ -118,14 +128,18 @@ def global_shapes(cfg) -> dict:
 
 def layer_tensor(cfg, seed: int, layer: int, name: str, nthreads=None, out=None) -> np.ndarray:
     shape = layer_shapes(cfg)[name]
-    sid = 16 * layer + KIND[name]
+    sid = 16 * layer + (KIND[name] if name in KIND else BIAS_KIND[name])
     if name.endswith("norm"):
         return normal_bf16(shape, seed, sid, 1.0, NORM_STD, nthreads, out)
+    if name in BIAS_KIND:
+        return normal_bf16(shape, seed, sid, 0.0, BIAS_STD, nthreads, out)
     return normal_bf16(shape, seed, sid, 0.0, WEIGHT_STD, nthreads, out)
 
 
 def global_tensor(cfg, seed: int, name: str, nthreads=None, out=None) -> np.ndarray:
     shape = global_shapes(cfg)[name]
+    if name == "lm_head" and cfg.get("tie_embeddings"):
+        name = "embed"   # tied: the LM head is the embedding table
     sid = 1_000_000 + GLOBAL[name]
     if name == "final_norm":
         return normal_bf16(shape, seed, sid, 1.0, NORM_STD, nthreads, out)
@@ -134,9 +148,12 @@ def global_tensor(cfg, seed: int, name: str, nthreads=None, out=None) -> np.ndar
 
 def model_host(cfg, seed: int, nthreads=None) -> dict:
     """All weights of a model as numpy uint16 (bf16 bits)."""
-    layers = [{k: layer_tensor(cfg, seed, l, k, nthreads) for k in KIND}
+    layers = [{k: layer_tensor(cfg, seed, l, k, nthreads) for k in layer_names(cfg)}
               for l in range(cfg["n_layers"])]
-    g = {k: global_tensor(cfg, seed, k, nthreads) for k in GLOBAL}
+    g = {k: global_tensor(cfg, seed, k, nthreads) for k in GLOBAL if k != "lm_head"}
+    # (tied: the very same array)
+    g["lm_head"] = g["embed"] if cfg.get("tie_embeddings") else global_tensor(
+        cfg, seed, "lm_head", nthreads)
     g["layers"] = layers
     return g
 

@@ -12,6 +12,12 @@ LLAMA8B = dict(n_layers=32, hidden=4096, n_heads=32, n_kv_heads=8, head_dim=128,
                vocab=128256, rope_theta=500000.0, rms_eps=1e-5)
 LLAMA70B = dict(n_layers=80, hidden=8192, n_heads=64, n_kv_heads=8, head_dim=128, ffn_dim=28672,
                 vocab=128256, rope_theta=500000.0, rms_eps=1e-5)
+# Table 2's other architectures: Llama 3.2 3B (tied embeddings, 3 query heads
+# per KV head) and Qwen2.5-72B (Q/K/V biases)
+LLAMA3B = dict(n_layers=28, hidden=3072, n_heads=24, n_kv_heads=8, head_dim=128, ffn_dim=8192,
+               vocab=128256, rope_theta=500000.0, rms_eps=1e-5, tie_embeddings=True)
+QWEN72B = dict(n_layers=80, hidden=8192, n_heads=64, n_kv_heads=8, head_dim=128, ffn_dim=29568,
+               vocab=152064, rope_theta=1000000.0, rms_eps=1e-6, qkv_bias=True)
 
 
 def _wl(name, model, batch, context, index):
@@ -29,4 +35,9 @@ WORKLOADS = {
     "llama8b-b1-ctx65536": _wl("llama8b-b1-ctx65536", LLAMA8B, 1, 65536, 3),
     "llama70b-b1-ctx4096": _wl("llama70b-b1-ctx4096", LLAMA70B, 1, 4096, 4),
     "llama70b-b32-ctx4096": _wl("llama70b-b32-ctx4096", LLAMA70B, 32, 4096, 4),
+    # Table 2 variants: other architectures, batch 8 / 16, contexts 8K / 16K
+    "llama3b-b1-ctx4096": _wl("llama3b-b1-ctx4096", LLAMA3B, 1, 4096, 5),
+    "qwen72b-b1-ctx4096": _wl("qwen72b-b1-ctx4096", QWEN72B, 1, 4096, 6),
+    "llama8b-b8-ctx16384": _wl("llama8b-b8-ctx16384", LLAMA8B, 8, 16384, 7),
+    "llama8b-b16-ctx8192": _wl("llama8b-b16-ctx8192", LLAMA8B, 16, 8192, 8),
 }

@@ -58,9 +58,11 @@ def decode_step(cfg, model, tokens, positions, K, V):
         x = bf16_decode(model["embed"])[t].copy()
         for l in range(L):
             u = rms_normalise(x, W(l, "attn_norm"), eps)
-            q = rotate((W(l, "wq") @ u).reshape(nq, d), p, theta)
-            k = rotate((W(l, "wk") @ u).reshape(nkv, d), p, theta)
-            v = (W(l, "wv") @ u).reshape(nkv, d)
+            lay = model["layers"][l]
+            bias = {n: (W(l, n) if n in lay else 0.0) for n in ("bq", "bk", "bv")}
+            q = rotate((W(l, "wq") @ u + bias["bq"]).reshape(nq, d), p, theta)
+            k = rotate((W(l, "wk") @ u + bias["bk"]).reshape(nkv, d), p, theta)
+            v = (W(l, "wv") @ u + bias["bv"]).reshape(nkv, d)
             K[l, b, :, p, :] = bf16_encode(k)
             V[l, b, :, p, :] = bf16_encode(v)
             Kd = np.repeat(bf16_decode(K[l, b, :, : p + 1, :]), nq // nkv, axis=0)  # [nq, p+1, d]

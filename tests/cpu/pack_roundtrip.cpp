@@ -11,6 +11,7 @@
 //   gate/up: packed row 2i is gate row i, 2i + 1 up row i;
 //   down projection, per FFN column block j: columns j KTc 64 ..;
 //   LM head: rows are vocabulary rows, padding rows zero;
+//   Q/K/V biases (fp32): in the q/k/v matrix's packed row order;
 // and every column past a matrix's K is zero.  Also: the jobs' regions lie
 // inside the layer (or the arena) and do not overlap.
 // Prints "pack round trip OK" and exits 0, else prints the failures, exit 1.
@@ -69,6 +70,12 @@ void run(const char *name, kl_config c, int nwg) {
     fill(kSrcUp, F, H);
     fill(kSrcDown, H, F);
     fill(kSrcLmHead, V, H);
+    // Q/K/V biases (ids 8..10, one row of nq d, nkv d, nkv d values)
+    std::vector<std::vector<uint16_t>> bias(3);
+    for (int k = 0; k < 3; ++k) {
+        bias[k].resize((size_t)(k == 0 ? nq : nkv) * d);
+        for (size_t i = 0; i < bias[k].size(); ++i) bias[k][i] = val(8 + k, 0, (int)i);
+    }
 
     // pack layer 0 and the classifier into an arena, as the loader does
     std::vector<uint16_t> arena(G.arena_bytes / 2, 0);
@@ -90,6 +97,15 @@ void run(const char *name, kl_config c, int nwg) {
     };
     for (const PackJob &J : layer_pack_jobs(c, G)) pack(J, 0);
     pack(head_pack_job(c, G), 0);
+    // the bias vector, as the bias packing kernel writes it
+    std::vector<float> packed_bias;
+    if (c.qkv_bias) {
+        const std::vector<int32_t> map = row_map(c, kMapQkv);
+        const uint16_t *s[3] = {bias[0].data(), bias[1].data(), bias[2].data()};
+        const int rows = nkv * G.qkv_rg * kTileRows;
+        for (int r = 0; r < rows; ++r) packed_bias.push_back(pack_bias_row(r, map.data(), s));
+        regions.push_back({G.off_qkv_bias, G.off_qkv_bias + (size_t)rows * 4});
+    }
 
     // regions: inside their homes, no overlap
     for (size_t i = 0; i < regions.size(); ++i) {
@@ -125,6 +141,24 @@ void run(const char *name, kl_config c, int nwg) {
                 }
                 expect("qkv", got, want, kv * hrows + lr, k);
             }
+    // biases: packed row kv hrows + lr is the bias of the same source row as above
+    if (c.qkv_bias)
+        for (int kv = 0; kv < nkv; ++kv)
+            for (int lr = 0; lr < hrows; ++lr) {
+                uint16_t want;
+                if (lr < (g + 1) * d) {
+                    const int i = (lr % d) / 2, dim = (lr % 2 == 0) ? i : i + d / 2;
+                    want = lr < g * d ? bias[0][(size_t)(kv * g + lr / d) * d + dim]
+                                      : bias[1][(size_t)kv * d + dim];
+                } else {
+                    want = bias[2][(size_t)kv * d + (lr - (g + 1) * d)];
+                }
+                const float f = packed_bias[(size_t)kv * hrows + lr];
+                uint32_t bits;
+                __builtin_memcpy(&bits, &f, 4);
+                if ((bits & 0xffffu) != 0 || (bits >> 16) != want)
+                    fail(std::string(name) + ": bias row " + std::to_string(kv * hrows + lr));
+            }
     // O projection per query head
     for (int h = 0; h < nq; ++h)
         for (int r = 0; r < H; ++r)
@@ -157,11 +191,13 @@ void run(const char *name, kl_config c, int nwg) {
 }  // namespace
 
 int main() {
-    //            L  H    nq nkv d    F    V    theta  eps    max_batch max_seq
-    run("d64 padded", {1, 136, 4, 2, 64, 200, 37, 1e4f, 1e-5f, 1, 64}, 16);
-    run("d64 group 8", {1, 128, 8, 1, 64, 96, 20, 1e4f, 1e-5f, 1, 64}, 32);
-    run("d128 group 4", {1, 256, 8, 2, 128, 320, 50, 5e5f, 1e-5f, 1, 64}, 256);
-    run("d128 group 1", {1, 192, 2, 2, 128, 136, 9, 5e5f, 1e-5f, 1, 64}, 7);
+    //            L  H    nq nkv d    F    V    theta  eps    max_batch max_seq  qkv_bias
+    run("d64 padded", {1, 136, 4, 2, 64, 200, 37, 1e4f, 1e-5f, 1, 64, 0}, 16);
+    run("d64 group 8", {1, 128, 8, 1, 64, 96, 20, 1e4f, 1e-5f, 1, 64, 0}, 32);
+    run("d128 group 4", {1, 256, 8, 2, 128, 320, 50, 5e5f, 1e-5f, 1, 64, 0}, 256);
+    run("d128 group 1", {1, 192, 2, 2, 128, 136, 9, 5e5f, 1e-5f, 1, 64, 0}, 7);
+    run("d128 group 3 bias", {1, 192, 6, 2, 128, 200, 11, 1e6f, 1e-6f, 1, 64, 1}, 24);
+    run("d64 group 2 bias", {1, 136, 4, 2, 64, 200, 37, 1e4f, 1e-5f, 1, 64, 1}, 16);
     if (g_fail) {
         std::fprintf(stderr, "%d failures\n", g_fail);
         return 1;

@@ -67,7 +67,8 @@ def run_workload(name, sample, modes=("looped",)):
 
 
 def test_llama8b_batch1_ctx4096_full_model_all_schedules():
-    run_workload("llama8b-b1-ctx4096", [0], modes=("looped", "per_layer", "per_op"))
+    run_workload("llama8b-b1-ctx4096", [0],
+                 modes=("looped", "per_layer", "per_op", "per_layer_graph"))
 
 
 def test_llama8b_batch1_ctx65536_full_model():

@@ -235,3 +235,45 @@ def test_llama70b_width_two_layers(batch):
     assert_bit_exact(c.gpu_step(kb.KL_MODE_LOOPED), outs[1], "incremental vs whole load")
     c.model = full
     inc.close()
+
+
+@pytest.mark.parametrize("shape", ["tiny-b1", "tiny-b8", "8b-width-b1"])
+def test_per_layer_graph_replays_match_looped(shape):
+    # the per-layer schedule recorded as a graph: built on the first call with
+    # a set of buffers, replayed on the next ones; every replay (with eager
+    # steps of the other schedules and synchronizations in between) computes
+    # the looped schedule's bits
+    say(f"[graph] {shape}")
+    if shape == "tiny-b1":
+        c = Case(TINY, 1, 192, [150], seed=241)
+    elif shape == "tiny-b8":
+        c = Case(TINY, 8, 192, (np.arange(8, dtype=np.int32) * 23) % 180, seed=243)
+    else:
+        cfg = dict(WORKLOADS["llama8b-b1-ctx4096"]["model"], n_layers=2)
+        c = Case(cfg, 1, 320, [300], seed=245)
+    B, V = c.batch, c.cfg["vocab"]
+    kv = KvCache(c.cfg, B, c.capacity, k_host=c.K0, v_host=c.V0)
+    toks = torch.from_numpy(c.tokens).cuda()
+    pos = torch.from_numpy(c.positions).cuda()
+    eager = torch.empty((B, V), device="cuda")
+    c.model.step(toks, pos, kv, eager, None, kb.KL_MODE_LOOPED)
+    torch.cuda.synchronize()
+    want = eager.cpu().numpy()
+    graph_out = torch.full((B, V), float("nan"), device="cuda")
+    for rep in range(3):
+        graph_out.fill_(float("nan"))
+        c.model.step(toks, pos, kv, graph_out, None, kb.KL_MODE_PER_LAYER_GRAPH)
+        torch.cuda.synchronize()
+        assert np.array_equal(graph_out.cpu().numpy().view(np.uint32), want.view(np.uint32)), \
+            f"replay {rep} differs from the looped schedule"
+        # eager work of the program between the replays
+        c.model.step(toks, pos, kv, eager, None, kb.KL_MODE_PER_OP if rep % 2 else kb.KL_MODE_LOOPED)
+        torch.cuda.synchronize()
+        assert np.array_equal(eager.cpu().numpy().view(np.uint32), want.view(np.uint32))
+    assert c.model.device_error() == 0
+    # other buffers: the graph is rebuilt for them
+    other = torch.empty((B, V), device="cuda")
+    c.model.step(toks, pos, kv, other, None, kb.KL_MODE_PER_LAYER_GRAPH)
+    torch.cuda.synchronize()
+    assert np.array_equal(other.cpu().numpy().view(np.uint32), want.view(np.uint32))
+    c.model.close()

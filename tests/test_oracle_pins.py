@@ -273,6 +273,8 @@ def test_step_with_zero_updates_keeps_embedding_and_closed_form_logits():
 
 @pytest.mark.parametrize("cfg_over,positions,cap", [
     ({}, [3, 5], 8),
+    ({"qkv_bias": True}, [2, 6], 8),
+    ({"tie_embeddings": True, "n_heads": 6, "n_kv_heads": 2}, [4, 1], 8),
     ({"n_heads": 4, "n_kv_heads": 4}, [0, 7], 8),
     ({"n_heads": 6, "n_kv_heads": 2, "head_dim": 8, "hidden": 24, "n_layers": 3}, [1, 2], 4),
 ])
@@ -313,3 +315,62 @@ def test_step_is_idempotent_and_rejects_bad_token():
         oracle.decode_step(cfg, model, np.array([cfg["vocab"]]), [4], K, V)
     with pytest.raises(ValueError):
         oracle.decode_step(cfg, model, toks, [8], K, V)
+
+
+# ---------------------------------------------------------------- sampling
+
+def test_argmax_lowest_index_on_ties_and_brute_force():
+    # ties resolve to the lowest index; -inf and negative values order normally
+    assert oracle.argmax([1.0, 3.0, 3.0, 2.0]) == 1
+    assert oracle.argmax([-np.inf, -5.0, -5.0]) == 1
+    assert oracle.argmax([7.0]) == 0
+    assert oracle.argmax([0.0, -0.0]) == 0          # +0 == -0: a tie
+    for _ in range(50):                              # brute force on small vectors
+        x = RNG.integers(-3, 4, size=int(RNG.integers(1, 12))).astype(np.float64)
+        best = max(range(x.size), key=lambda i: (x[i], -i))
+        assert oracle.argmax(x) == best
+
+
+def test_greedy_loop_feeds_each_token_to_the_next_step():
+    # a 1-layer toy: step s of the loop equals a single decode step at
+    # position p + s on the previous step's argmax, caches carried over
+    cfg = dict(n_layers=1, hidden=8, n_heads=2, n_kv_heads=1, head_dim=4, ffn_dim=12, vocab=16,
+               rope_theta=10000.0, rms_eps=1e-5)
+    import synth
+    w = synth.model_host(cfg, 5)
+    K0, V0 = synth.kv_cache_host(cfg, 6, 1, 8, [3])
+    K, V = K0.copy(), V0.copy()
+    sampled, logits = oracle.greedy_decode(cfg, w, [2], [3], K, V, 3)
+    Kr, Vr = K0.copy(), V0.copy()
+    tok = 2
+    for s in range(3):
+        lg, _ = oracle.decode_step(cfg, w, [tok], [3 + s], Kr, Vr)
+        assert np.array_equal(lg, logits[s])
+        tok = oracle.argmax(lg[0])
+        assert sampled[s, 0] == tok
+    assert np.array_equal(K, Kr) and np.array_equal(V, Vr)
+
+
+def test_qkv_bias_with_zero_weights_is_the_bias():
+    # Q/K/V weights zero: q = bq, k = RoPE(bk) and v = bv exactly; at position 0
+    # the single key's softmax weight is 1, so the attention output of every
+    # query head is bf16(bv) of its KV head, and with W_o the identity-like
+    # one-hot map the residual picks it up exactly
+    cfg = dict(SMALL, qkv_bias=True, n_layers=1)
+    model, K, V, toks = _small_inputs(cfg, 1, 4, [0])
+    lay = model["layers"][0]
+    for n in ("wq", "wk", "wv", "w_down"):
+        lay[n][:] = 0
+    d, nq, nkv, H = cfg["head_dim"], cfg["n_heads"], cfg["n_kv_heads"], cfg["hidden"]
+    wo = np.zeros((H, nq * d))
+    wo[np.arange(nq * d), np.arange(nq * d)] = 1.0          # x[i] += o[i] for i < nq d
+    lay["wo"][:] = oracle.f64_to_bf16(wo)
+    _, hidden = oracle.decode_step(cfg, model, toks, [0], K, V)
+    E = bruteforce.bf16_decode(model["embed"])[toks[0]]
+    bv = oracle.bf16_to_f64(oracle.f64_to_bf16(bruteforce.bf16_decode(lay["bv"])))
+    o = np.repeat(bv.reshape(nkv, d), nq // nkv, axis=0).reshape(-1)
+    want = E.copy()
+    want[: nq * d] += o
+    np.testing.assert_array_equal(hidden[0], want)
+    # the new key slot holds bf16(RoPE at 0 of bk) = bf16(bk)
+    np.testing.assert_array_equal(K[0, 0, :, 0, :], lay["bk"].reshape(nkv, d))
