@@ -89,6 +89,83 @@ def copy_probe(mib: int, reps: int = 3):
                                      "kernel": "torch.neg fp32 (elementwise)"}}), flush=True)
 
 
+def read_stream_ceiling(gib: int = 4, reps: int = 5):
+    """GB/s of kl_read_stream (the step kernel's load pattern, one pass over a
+    buffer) for a few grid sizes: the practical read ceiling, for context."""
+    import torch
+    from paper_2410_23668_amd import binding as kb
+    from paper_2410_23668_amd.device import stream_handle
+    n = gib << 30
+    buf = torch.zeros(n, dtype=torch.uint8, device="cuda")
+    out = torch.zeros(1, dtype=torch.int32, device="cuda")
+    h = stream_handle()
+    rates = {}
+    for wg in (256, 512, 1024, 2048, 4096):
+        kb.kl_read_stream(buf.data_ptr(), n, wg, out.data_ptr(), h)   # warm-up
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            kb.kl_read_stream(buf.data_ptr(), n, wg, out.data_ptr(), h)
+        e1.record()
+        torch.cuda.synchronize()
+        rates[wg] = n * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del buf, out
+    best = max(rates, key=rates.get)
+    return {"bytes": n, "GBps_by_workgroups": {str(k): round(v, 1) for k, v in rates.items()},
+            "best_GBps": rates[best], "best_frac_of_peak": rates[best] / PEAK_HBM_GBS,
+            "step_grid_GBps": rates[256],
+            "kernel": "kl_read_stream: 16-byte non-temporal loads, 16 in flight per lane, 512 "
+                      "lanes per workgroup"}
+
+
+PHASES = ("qkv", "attn", "oproj", "gateup", "down")
+
+
+def phase_table(model, toks, pos, kv, logits, mode, cfg, B, P):
+    """One traced step (kl_set_trace): per phase, the mean over layers of the
+    span from the previous phase's last finishing workgroup to this phase's
+    last finishing workgroup, with the phase's algorithmic bytes and the rate
+    they imply.  The spans of all phases add up to the traced step."""
+    import numpy as np
+    import torch
+    from paper_2410_23668_amd import binding as kb
+    from paper_2410_23668_amd import bytemodel
+    L = cfg["n_layers"]
+    nwg = model.info().n_workgroups
+    nph = 5 * L + 2     # embed, 5 per layer, head
+    tr = torch.zeros(nph * nwg * 4, dtype=torch.int64, device="cuda")
+    kb.kl_set_trace(model.state, tr.data_ptr(), nph)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    model.step(toks, pos, kv, logits, None, mode)
+    e1.record()
+    torch.cuda.synchronize()
+    kb.kl_set_trace(model.state, None, 0)
+    traced_ms = e0.elapsed_time(e1)
+    a = tr.cpu().numpy().reshape(nph, nwg, 4) * 10      # 100 MHz ticks -> ns
+    end = a[:, :, 0]
+    last = [int(end[i][end[i] > 0].max()) for i in range(nph)]
+    first = int(end[0][end[0] > 0].min())
+    nb = bytemodel.phase_bytes(cfg, B, P)
+    rows = {}
+    for k, name in enumerate(PHASES):
+        spans = [last[1 + 5 * l + k] - last[5 * l + k] for l in range(L)]
+        rows[name] = float(np.mean(spans)) / 1e3
+    rows["head"] = (last[nph - 1] - last[nph - 2]) / 1e3
+    table = {}
+    for name, us in rows.items():
+        table[name] = {"us": round(us, 2), "bytes": nb[name],
+                       "GBps": round(nb[name] / (us * 1e-6) / 1e9, 1),
+                       "frac_of_peak": round(nb[name] / (us * 1e-6) / 1e9 / PEAK_HBM_GBS, 3)}
+    layer_us = sum(rows[n] for n in PHASES)
+    return {"per_layer_phase_mean": table, "layer_us": round(layer_us, 2),
+            "embed_us": round((last[0] - first) / 1e3, 2),
+            "traced_span_us": round((last[-1] - first) / 1e3, 1),
+            "traced_step_ms": traced_ms,
+            "note": "span of a phase = its last workgroup's end minus the previous phase's "
+                    "(s_memrealtime stamps); bytes = the phase's algorithmic bytes"}
+
+
 def time_mode(model, toks, pos, kv, logits, mode, steps, warmup):
     import torch
     for _ in range(warmup):
@@ -124,6 +201,10 @@ def main():
                     help="tokens of the greedy token loop timed after the steps (its steady-state "
                          "time per output token); -1: 128 unless the model is loaded layer by "
                          "layer, 0: skip")
+    ap.add_argument("--phases", action="store_true",
+                    help="trace one step of the headline schedule and report per-phase times")
+    ap.add_argument("--no-read-stream", action="store_true",
+                    help="skip the read-stream ceiling measurement")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run the copy kernel used to scale HBM counters, then exit")
     args = ap.parse_args()
@@ -163,9 +244,12 @@ def main():
     if big:
         log(f"workload {args.workload}: generating and loading layer by layer ({nthr} threads)")
         seed = wl["seed_weights"]
+        def layer(l):
+            if l % 8 == 0:
+                log(f"  layer {l}/{cfg['n_layers']} ({time.perf_counter() - t:.0f}s)")
+            return {k: synth.layer_tensor(cfg, seed, l, k, nthr) for k in synth.layer_names(cfg)}
         model = GpuModel.from_layers(
-            cfg, lambda l: {k: synth.layer_tensor(cfg, seed, l, k, nthr)
-                            for k in synth.layer_names(cfg)},
+            cfg, layer,
             lambda: {k: synth.global_tensor(cfg, seed, k, nthr)
                      for k in ("embed", "final_norm", "lm_head")}, B, max_seq)
     else:
@@ -270,6 +354,14 @@ def main():
                        "note": "algorithmic = 2 flops per weight MAC and sequence plus attention; "
                                "issued = the matrix-core products actually run (hi and lo "
                                "activation terms), against the dense bf16 peak"}
+
+    if args.phases:
+        log("phase timeline of one traced step")
+        out["phases"] = phase_table(model, toks, pos, kv, outs[head], kb.MODES[head], cfg, B, P)
+
+    if not args.no_read_stream:
+        log("read-stream ceiling")
+        out["read_stream"] = read_stream_ceiling()
 
     # parity of the timed output, and the oracle's own time on the host
     if not args.no_cpu_baseline and weights is not None:

@@ -256,6 +256,19 @@ kl_status kl_get_info(const kl_state *st, kl_info *info);
  * to stop tracing. */
 kl_status kl_set_trace(kl_state *st, uint64_t *dev_buffer, int32_t max_phases);
 
+/* Measurement helper (no model involved): reads every byte of the device
+ * buffer buf (bytes, both 16-byte aligned) once with the step kernel's
+ * 16-byte non-temporal loads, 16 in flight per lane, on a grid of workgroups
+ * x 512 lanes (1..65536 workgroups), and writes nothing the caller relies on
+ * (dev_out, one device uint32, is at most written with an unspecified value).
+ * Timed by the caller, it gives the read-stream rate this load pattern
+ * reaches: the practical ceiling of a kernel whose traffic is one pass over
+ * its weights (the roofline of Sec. 4.4's bandwidth comparison is the
+ * nominal peak).  Asynchronous on stream; invalid arguments return
+ * KL_ERR_INVALID_ARGUMENT with nothing enqueued. */
+kl_status kl_read_stream(const void *buf, size_t bytes, int32_t workgroups, uint32_t *dev_out,
+                         void *stream);
+
 /* Frees everything the state owns (synchronizes the device first). NULL is a no-op. */
 void kl_free_model(kl_state *st);
 

@@ -34,7 +34,7 @@ KL_DEVERR_BARRIER = 4
 EXPORTED = ["kl_load_model", "kl_model_create", "kl_model_set_layer", "kl_model_set_globals",
             "kl_decode_step", "kl_decode_step_noalloc", "kl_decode_greedy", "kl_kv_cache_bytes",
             "kl_get_device_error",
-            "kl_get_info", "kl_set_trace", "kl_free_model", "kl_last_error"]
+            "kl_get_info", "kl_set_trace", "kl_read_stream", "kl_free_model", "kl_last_error"]
 
 
 class kl_config(ctypes.Structure):
@@ -117,6 +117,8 @@ def lib():
     L.kl_get_info.restype = i32
     L.kl_set_trace.argtypes = [vp, vp, i32]
     L.kl_set_trace.restype = i32
+    L.kl_read_stream.argtypes = [vp, ctypes.c_size_t, i32, vp, vp]
+    L.kl_read_stream.restype = i32
     L.kl_free_model.argtypes = [vp]
     L.kl_free_model.restype = None
     L.kl_last_error.argtypes = []
@@ -216,6 +218,10 @@ def kl_get_info(state: int) -> kl_info:
 
 def kl_set_trace(state: int, dev_buffer: int | None, max_phases: int) -> None:
     _check(lib().kl_set_trace(state, dev_buffer, max_phases))
+
+
+def kl_read_stream(buf: int, nbytes: int, workgroups: int, dev_out: int, stream: int) -> None:
+    _check(lib().kl_read_stream(buf, nbytes, workgroups, dev_out, stream))
 
 
 def kl_free_model(state: int) -> None:

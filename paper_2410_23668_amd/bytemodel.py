@@ -60,3 +60,21 @@ def step_flops(cfg, batch: int, context: int) -> int:
     L, nq, d = cfg["n_layers"], cfg["n_heads"], cfg["head_dim"]
     attn = L * 4 * nq * d * (context + 1)
     return batch * (2 * weight_macs(cfg) + attn)
+
+
+def phase_bytes(cfg, batch: int, context: int) -> dict:
+    """Algorithmic bytes of each phase of one layer (and of the classifier
+    phase), as the step kernel splits the layer: q/k/v (with the attention
+    norm gain), attention (the cached K/V read plus the new slot's write), O
+    projection, gate/up (with the FFN norm gain), down projection."""
+    H, nq, nkv, d, F, V = (cfg[k] for k in ("hidden", "n_heads", "n_kv_heads", "head_dim",
+                                            "ffn_dim", "vocab"))
+    bias = (nq + 2 * nkv) * d if cfg.get("qkv_bias") else 0
+    return {
+        "qkv": 2 * (H * (nq + 2 * nkv) * d + H + bias),
+        "attn": batch * 2 * nkv * d * 2 * (context + 1),
+        "oproj": 2 * nq * d * H,
+        "gateup": 2 * (2 * H * F + H),
+        "down": 2 * F * H,
+        "head": 2 * (V * H + H) + batch * V * 4,
+    }

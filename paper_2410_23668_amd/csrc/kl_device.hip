@@ -52,6 +52,37 @@ hipError_t launch_zero(void *p, size_t bytes, hipStream_t stream) {
     return hipGetLastError();
 }
 
+// Read stream: every 16-byte chunk of the buffer is loaded once with the
+// step kernel's load (non-temporal, 16 B per lane), 16 loads in flight per
+// lane; in round r, lane t of the grid's T lanes loads chunks (16 r + j) T + t,
+// j < 16, so a wave reads 1 KiB runs.  The loaded words are folded into one
+// value that is stored only if it equals a constant the data never produce
+// (the loads cannot be dropped, and nothing is written).
+__global__ void __launch_bounds__(512) kl_read_stream_kernel(const u32x4 *__restrict__ p,
+                                                             size_t n, uint32_t *out) {
+    const size_t T = (size_t)gridDim.x * blockDim.x;
+    const size_t t = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    uint32_t acc = 0;
+    for (size_t base = 0; base < n; base += 16 * T) {
+        u32x4 v[16];
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            const size_t i = base + j * T + t;
+            v[j] = i < n ? ld_stream_16B(p + i) : u32x4{0u, 0u, 0u, 0u};
+        }
+#pragma unroll
+        for (int j = 0; j < 16; ++j) acc ^= v[j][0] ^ v[j][1] ^ v[j][2] ^ v[j][3];
+    }
+    if (acc == 0x9E3779B9u) out[0] = acc;
+}
+
+hipError_t launch_read_stream(const void *p, size_t bytes, int workgroups, uint32_t *out,
+                              hipStream_t stream) {
+    hipLaunchKernelGGL(kl_read_stream_kernel, dim3(workgroups), dim3(512), 0, stream,
+                       reinterpret_cast<const u32x4 *>(p), bytes / 16, out);
+    return hipGetLastError();
+}
+
 // The instance for a model's head_dim, query heads per KV head (the host has
 // validated both) and the batch regime (matrix cores at batch >= kMfmaBatch);
 // the instances are compiled in separate translation units (kl_step_*.hip).

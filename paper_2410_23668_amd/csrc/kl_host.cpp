@@ -783,6 +783,22 @@ kl_status kl_set_trace(kl_state *st, uint64_t *dev_buffer, int32_t max_phases) {
     return KL_OK;
 }
 
+kl_status kl_read_stream(const void *buf, size_t bytes, int32_t workgroups, uint32_t *dev_out,
+                         void *stream) {
+    if (buf == nullptr || dev_out == nullptr)
+        return fail(KL_ERR_INVALID_ARGUMENT, "kl_read_stream: null pointer");
+    if ((reinterpret_cast<uintptr_t>(buf) & 15) != 0 || bytes % 16 != 0)
+        return fail(KL_ERR_INVALID_ARGUMENT,
+                    "kl_read_stream: buffer and size must be multiples of 16 bytes");
+    if (workgroups < 1 || workgroups > 65536)
+        return fail(KL_ERR_INVALID_ARGUMENT, "kl_read_stream: workgroups %d outside [1, 65536]",
+                    workgroups);
+    if (bytes == 0) return KL_OK;
+    const hipError_t e = launch_read_stream(buf, bytes, workgroups, dev_out,
+                                            reinterpret_cast<hipStream_t>(stream));
+    return e == hipSuccess ? KL_OK : fail(KL_ERR_HIP, "kl_read_stream: %s", hipGetErrorString(e));
+}
+
 kl_status kl_get_info(const kl_state *st, kl_info *info) {
     if (!st || !info) return fail(KL_ERR_INVALID_ARGUMENT, "state and info must not be NULL");
     info->n_workgroups = st->nwg;

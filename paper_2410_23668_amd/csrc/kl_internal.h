@@ -152,6 +152,8 @@ constexpr size_t kStaticScratchBytes = size_t(32) << 20;
 hipError_t static_scratch_address(int device, uint8_t **out);
 // Zero 'bytes' (a multiple of 16, 16-byte aligned) at p with a fill kernel.
 hipError_t launch_zero(void *p, size_t bytes, hipStream_t stream);
+hipError_t launch_read_stream(const void *p, size_t bytes, int workgroups, uint32_t *out,
+                              hipStream_t stream);
 
 // tokens[b] = the token of argmax key keys[b] (-1 where there is none), b < n.
 hipError_t launch_emit_tokens(int32_t *tokens, const unsigned long long *keys, int n,

@@ -100,3 +100,17 @@ def test_get_info_and_error_reject_null():
     code = ctypes.c_int32()
     assert kb.lib().kl_get_device_error(None, ctypes.byref(code)) == kb.KL_ERR_INVALID_ARGUMENT
     kb.lib().kl_free_model(None)   # no-op
+
+
+@pytest.mark.parametrize("buf,nbytes,wg,out,msg", [
+    (None, 1024, 256, 64, "null"),
+    (4096, 1024, 256, None, "null"),
+    (4100, 1024, 256, 64, "multiples of 16"),
+    (4096, 1000, 256, 64, "multiples of 16"),
+    (4096, 1024, 0, 64, "workgroups"),
+    (4096, 1024, 65537, 64, "workgroups"),
+])
+def test_read_stream_rejects_bad_arguments_before_any_hip_call(buf, nbytes, wg, out, msg):
+    st = kb.lib().kl_read_stream(buf, nbytes, wg, out, None)
+    assert st == kb.KL_ERR_INVALID_ARGUMENT
+    assert msg in kb.lib().kl_last_error().decode()

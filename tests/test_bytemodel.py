@@ -52,3 +52,14 @@ def test_step_flops_counts_two_per_mac():
     macs = 2 * 2 + 2 * 2 * 2 + 2 * 2 + 3 * 2 * 3 + 5 * 2
     assert bm.step_flops(cfg, 1, 0) == 2 * macs + 4 * 2 * 1
     assert bm.step_flops(cfg, 3, 4) == 3 * (2 * macs + 4 * 2 * 5)
+
+
+@pytest.mark.parametrize("name,batch,ctx", [("LLAMA8B", 1, 4096), ("LLAMA8B", 32, 4096),
+                                            ("LLAMA70B", 32, 4096), ("QWEN72B", 1, 4096)])
+def test_phase_bytes_add_up_to_the_step(name, batch, ctx):
+    import synth.workloads as W
+    cfg = getattr(W, name)
+    pb = bm.phase_bytes(cfg, batch, ctx)
+    layer = sum(pb[k] for k in ("qkv", "attn", "oproj", "gateup", "down"))
+    total = cfg["n_layers"] * layer + pb["head"] + batch * 2 * cfg["hidden"]
+    assert total == bm.step_bytes(cfg, batch, ctx)
