@@ -1,4 +1,5 @@
-"""Build libkl.so (the HIP library behind include/kl.h) for gfx950, in place."""
+"""Build libkl.so (the HIP library behind include/kl.h) for gfx950, and the
+host library of the kernel-looping pass (looping/libklloop.so), in place."""
 from __future__ import annotations
 
 import os
@@ -49,5 +50,23 @@ def build(verbose: bool = False, jobs: int = 0) -> str:
     return LIB
 
 
+LOOPING = os.path.join(HERE, "looping")
+LOOPING_LIB = os.path.join(LOOPING, "libklloop.so")
+
+
+def build_looping(verbose: bool = False) -> str:
+    """Compile the kernel-looping pass (host C++17) into libklloop.so."""
+    cxx = os.environ.get("CXX", "g++")
+    tmp = LOOPING_LIB + ".tmp"
+    cmd = [cxx, "-std=c++17", "-O2", "-fPIC", "-shared", "-Wall", "-Wextra", "-o", tmp,
+           os.path.join(LOOPING, "kl_looping.cpp")]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, LOOPING_LIB)
+    return LOOPING_LIB
+
+
 if __name__ == "__main__":
     print(build(verbose=True))
+    print(build_looping(verbose=True))

@@ -77,10 +77,12 @@ struct Stmt {
     std::vector<Stmt> body;
 };
 
+// Calls pass distinct tensors to a kernel's parameters (no aliasing within a
+// call), and a body assigns a local before reading it.
 struct Kernel {
     std::string name;
     std::vector<Tensor> params;
-    std::vector<int> group;     // per parameter: N when grouped ([N x S]), 0 otherwise
+    std::vector<int> group;     // looped kernels: per parameter, N when grouped ([N x S]), else 0
     std::vector<Tensor> locals; // kernel-private tensors (off-chip temporaries)
     std::vector<Tensor> buffers;// on-chip buffers introduced by the rewrite
     std::vector<Stmt> body;
