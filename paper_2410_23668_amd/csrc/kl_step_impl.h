@@ -1868,6 +1868,213 @@ __device__ __forceinline__ void attn_item(KArg ka, int l, int b, int g, int c, b
     __syncthreads();   // (the attention area is the next item's)
 }
 
+// Streaming attention item (batched path, up to 4 query heads per KV head,
+// where an item is a whole sequence or a long chunk of one): each compute
+// wave streams its own slabs of the chunk (slabs w, w + kWaves, ...; a slab
+// is PP positions, one 16-byte load per lane) through a ring of kAttnRing K
+// and kAttnRing V loads that is refilled as it is consumed, and each lane
+// group (the LP lanes of one position) keeps its own running softmax per
+// query head: max m, sum l and the unnormalised output over its 8 dims,
+// updated once per kAttnRing slabs (their scores first, one rescale by
+// 2^(m_old - m_new) when the max grows, then their values; scores are kept
+// in log2 units, so every weight is one hardware exp2).  No block barrier in
+// the loop: the PP lane groups of a wave are merged by shuffles, the waves in
+// order through LDS.  The queries are held in registers.  The new slot
+// (written this step by another workgroup) is read after the wait with
+// device-coherent loads into LDS and taken from there; its ring load targets
+// a shared dummy line.  Outputs as attn_item's batched path: the chunk's
+// (max, sum, unnormalised output), and the normalised output when the item is
+// the whole sequence.
+template <int D, int G>
+__device__ __forceinline__ void attn_item_stream(KArg ka, int l, int b, int g, int c, bool first,
+                                                 int ti) {
+    const StepParams P = load_params(ka);
+    const Lds S = lds_layout(kl_smem, P);
+    constexpr int LP = D / 8;                       // lanes per position
+    constexpr int PP = 64 / LP;                     // positions per slab
+    constexpr int R = kAttnRing;
+    const int wid = __builtin_amdgcn_readfirstlane(kl_tid() >> 6);
+    const int lane = kl_tid() & 63;
+    const int pi = lane / LP, ds = (lane % LP) * 8;
+    const int pnew = pos_of<false>(P, b), n = pnew + 1;
+    int s0, s1;
+    split_range((n + PP - 1) / PP, P.C, c, s0, s1);
+    const bool compute = wid < kWaves;
+    // this wave's slabs: s0 + wid, s0 + wid + kWaves, ... < s1
+    const int mine = compute && s0 + wid < s1 ? (s1 - s0 - wid + kWaves - 1) / kWaves : 0;
+
+    float *qs = S.attn;                                  // [G][D]
+    float *wm = qs + G * D;                              // [kWaves][G] wave maxima (log2 units)
+    float *wl = wm + kWaves * G;                         // [kWaves][G] wave sums
+    float *wacc = wl + kWaves * G;                       // [kWaves][G][D] wave outputs
+    uint16_t *kn = reinterpret_cast<uint16_t *>(wacc + kWaves * G * D);   // [D] new key
+    uint16_t *vn = kn + D;                                                // [D] new value
+    const size_t row0 = kv_row(P, l, b, g);
+    const uint16_t *Kb = P.kc + row0 * D + ds;
+    const uint16_t *Vb = P.vc + row0 * D + ds;
+    // scores in log2 units: softmax weights are 2^(s log2(e) - max)
+    const float scale = 1.4426950408889634f / sqrtf((float)D);
+
+    // the ring: item i of this wave (slab s0 + wid + i kWaves) sits in slot
+    // i % R; a slot past the wave's slabs, past the context or holding the
+    // new position loads the dummy line (zeros)
+    u32x4 kr[R], vr[R];
+    auto pos_of_item = [&](int i) { return (s0 + wid + i * kWaves) * PP + pi; };
+    auto addr = [&](const uint16_t *base, int i) -> const void * {
+        const int pos = pos_of_item(i);
+        return (i < mine && pos < n && pos != pnew) ? (const void *)(base + (size_t)pos * D)
+                                                    : (const void *)P.dummy;
+    };
+    if (compute) {
+#pragma unroll
+        for (int s = 0; s < R; ++s) kr[s] = ld_stream_16B(addr(Kb, s));
+#pragma unroll
+        for (int s = 0; s < R; ++s) vr[s] = ld_stream_16B(addr(Vb, s));
+    }
+    if (is_ctl_lane0()) trace_stamp(P, ti, 1);
+    if (first) local_wait(P, P.cnt + g, (unsigned)(l + 1) * (unsigned)P.Sg, ti);
+    for (int t = kl_tid(); t < G * D; t += kThreads)
+        qs[t] = ld_dev(P.q + (size_t)b * P.nq * D + (size_t)g * G * D + t);
+    if (kl_tid() < D / 4) {   // the new key and value (device-coherent loads)
+        const size_t o = (size_t)pnew * D + kl_tid() * 4;
+        reinterpret_cast<unsigned long long *>(kn)[kl_tid()] = ld_dev_u64(P.kc + row0 * D + o);
+        reinterpret_cast<unsigned long long *>(vn)[kl_tid()] = ld_dev_u64(P.vc + row0 * D + o);
+    }
+    __syncthreads();
+    if (is_ctl_lane0()) trace_stamp(P, ti, 2);
+
+    float acc[G][8], m[G], lsum[G];
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+        m[h] = -INFINITY;
+        lsum[h] = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[h][e] = 0.f;
+    }
+    if (compute) {
+        float q[G][8];
+#pragma unroll
+        for (int h = 0; h < G; ++h) {
+            const float4 q0 = *reinterpret_cast<const float4 *>(qs + h * D + ds);
+            const float4 q1 = *reinterpret_cast<const float4 *>(qs + h * D + ds + 4);
+            q[h][0] = q0.x; q[h][1] = q0.y; q[h][2] = q0.z; q[h][3] = q0.w;
+            q[h][4] = q1.x; q[h][5] = q1.y; q[h][6] = q1.z; q[h][7] = q1.w;
+        }
+        // R slabs at a time: their scores, one rescale per head, their values
+        for (int i0 = 0; i0 < mine; i0 += R) {
+            float sc[R][G];
+#pragma unroll
+            for (int s = 0; s < R; ++s) {
+                const int pos = pos_of_item(i0 + s);
+                const bool valid = i0 + s < mine && pos < n;
+                const u32x4 kv = pos == pnew ? *reinterpret_cast<const u32x4 *>(kn + ds) : kr[s];
+                kr[s] = ld_stream_16B(addr(Kb, i0 + s + R));
+                const float kf[8] = {bf_lo(kv.x), bf_hi(kv.x), bf_lo(kv.y), bf_hi(kv.y),
+                                     bf_lo(kv.z), bf_hi(kv.z), bf_lo(kv.w), bf_hi(kv.w)};
+#pragma unroll
+                for (int h = 0; h < G; ++h) {
+                    float d = 0.f;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) d = fmaf(q[h][e], kf[e], d);
+                    d = sum_lanes<LP>(d) * scale;
+                    sc[s][h] = valid ? d : -INFINITY;
+                }
+            }
+#pragma unroll
+            for (int h = 0; h < G; ++h) {
+                float mx = m[h];
+#pragma unroll
+                for (int s = 0; s < R; ++s) mx = fmaxf(mx, sc[s][h]);
+                const float al = m[h] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m[h] - mx);
+                float sum = 0.f;
+#pragma unroll
+                for (int s = 0; s < R; ++s) {
+                    sc[s][h] = sc[s][h] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(sc[s][h] - mx);
+                    sum += sc[s][h];
+                }
+                lsum[h] = fmaf(lsum[h], al, sum);
+                m[h] = mx;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) acc[h][e] *= al;
+            }
+#pragma unroll
+            for (int s = 0; s < R; ++s) {
+                const int pos = pos_of_item(i0 + s);
+                const u32x4 vv = pos == pnew ? *reinterpret_cast<const u32x4 *>(vn + ds) : vr[s];
+                vr[s] = ld_stream_16B(addr(Vb, i0 + s + R));
+                const float vf[8] = {bf_lo(vv.x), bf_hi(vv.x), bf_lo(vv.y), bf_hi(vv.y),
+                                     bf_lo(vv.z), bf_hi(vv.z), bf_lo(vv.w), bf_hi(vv.w)};
+#pragma unroll
+                for (int h = 0; h < G; ++h)
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(sc[s][h], vf[e], acc[h][e]);
+            }
+        }
+        // merge the PP lane groups of the wave (lanes ds apart by LP, 2 LP, ...)
+#pragma unroll
+        for (int off = LP; off < 64; off <<= 1) {
+#pragma unroll
+            for (int h = 0; h < G; ++h) {
+                const float m2 = __shfl_xor(m[h], off), l2 = __shfl_xor(lsum[h], off);
+                const float mn = fmaxf(m[h], m2);
+                const float a1 = m[h] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m[h] - mn);
+                const float a2 = m2 == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m2 - mn);
+                lsum[h] = lsum[h] * a1 + l2 * a2;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const float o2 = __shfl_xor(acc[h][e], off);
+                    acc[h][e] = acc[h][e] * a1 + o2 * a2;
+                }
+                m[h] = mn;
+            }
+        }
+        if (pi == 0) {
+#pragma unroll
+            for (int h = 0; h < G; ++h) {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) wacc[(wid * G + h) * D + ds + e] = acc[h][e];
+                if (ds == 0) {
+                    wm[wid * G + h] = m[h];
+                    wl[wid * G + h] = lsum[h];
+                }
+            }
+        }
+    }
+    __syncthreads();
+    // the waves in order: (max, sum, unnormalised output) of the chunk, the
+    // max published in natural-log units like every chunk's
+    const size_t item = ((size_t)b * P.nkv + g) * P.C + c;
+    float *out = P.part_o + item * G * D;
+    float *sts = P.part_s + item * G * 2;
+    for (int t = kl_tid(); t < G * D + G; t += kThreads) {
+        const int h = t < G * D ? t / D : t - G * D, dd = t % D;
+        float M = -INFINITY;
+        for (int w = 0; w < kWaves; ++w) M = fmaxf(M, wm[w * G + h]);
+        float O = 0.f, L = 0.f;
+        for (int w = 0; w < kWaves; ++w) {
+            const float mw = wm[w * G + h];
+            const float a = mw == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mw - M);
+            L = fmaf(wl[w * G + h], a, L);
+            if (t < G * D) O = fmaf(wacc[(w * G + h) * D + dd], a, O);
+        }
+        if (t < G * D) {
+            st_dev(out + t, O);
+            if (P.C == 1) {   // (one chunk: the merged output is final)
+                uint16_t hi, lo;
+                split_bf16(O / L, hi, lo);
+                const size_t o = (size_t)b * P.nq * D + (size_t)g * G * D + t;
+                st_dev_u16(P.acto + o, hi);
+                st_dev_u16(P.acto_lo + o, lo);
+            }
+        } else {
+            st_dev(sts + h * 2, M * 0.6931471805599453f);
+            st_dev(sts + h * 2 + 1, L);
+        }
+    }
+    if (is_ctl_lane0()) trace_stamp(P, ti, 3);
+    __syncthreads();   // (the attention area is the next item's)
+}
+
 // Attention of KV head g: the workgroups of head g take its items (sequence
 // b, chunk c) round-robin.  The per-sequence path hands the chunk results to
 // the O projection as tagged words; the batched path publishes them before a
@@ -1879,7 +2086,10 @@ __device__ __forceinline__ void phase_attn(KArg ka, int l, int garrive, int ti) 
     if (g < P.nkv) {
         const int items = P.B * P.C;
         for (int it = part; it < items; it += P.Sg)
-            attn_item<D, G, !BAT, BAT && G <= 4>(ka, l, it / P.C, g, it % P.C, it == part, ti);
+            if constexpr (BAT && G <= 4)
+                attn_item_stream<D, G>(ka, l, it / P.C, g, it % P.C, it == part, ti);
+            else
+                attn_item<D, G, !BAT, false>(ka, l, it / P.C, g, it % P.C, it == part, ti);
     }
     if (garrive >= 0) bar_arrive(P, garrive, ti);
     else if (is_ctl_lane0()) trace_stamp(P, ti, 0);
