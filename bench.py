@@ -241,26 +241,60 @@ def main():
     cap_loop = (P + n_loop + 63) // 64 * 64
     max_seq = max(cap, cap_loop)
     weights = None
+    data = "synthetic (seeded N(0,0.02) weights, N(0,1) KV)"
     if big:
-        log(f"workload {args.workload}: generating and loading layer by layer ({nthr} threads)")
-        seed = wl["seed_weights"]
+        # generated on the device with torch's seeded normal generator (the
+        # host generator's distributions, not its values: decode cost does not
+        # depend on them), loaded one layer at a time
+        log(f"workload {args.workload}: generating on the device, loading layer by layer")
+        data = ("synthetic, generated on the device (torch seeded normal: N(0,0.02) weights, "
+                "N(1,0.01) norm gains, N(0,1) KV)")
+        gen = torch.Generator(device="cuda")
+        gen.manual_seed(wl["seed_weights"])
+
+        def dev_normal(shape, mean, std):
+            x = torch.empty(shape, dtype=torch.float32, device="cuda")
+            x.normal_(mean, std, generator=gen)
+            return x.to(torch.bfloat16).view(torch.int16)
+
+        def dev_tensor(name, shape):
+            if name.endswith("norm"):
+                return dev_normal(shape, 1.0, synth.NORM_STD)
+            if name in synth.BIAS_KIND:
+                return dev_normal(shape, 0.0, synth.BIAS_STD)
+            return dev_normal(shape, 0.0, synth.WEIGHT_STD)
+
         def layer(l):
             if l % 8 == 0:
                 log(f"  layer {l}/{cfg['n_layers']} ({time.perf_counter() - t:.0f}s)")
-            return {k: synth.layer_tensor(cfg, seed, l, k, nthr) for k in synth.layer_names(cfg)}
-        model = GpuModel.from_layers(
-            cfg, layer,
-            lambda: {k: synth.global_tensor(cfg, seed, k, nthr)
-                     for k in ("embed", "final_norm", "lm_head")}, B, max_seq)
+            shapes = synth.layer_shapes(cfg)
+            return {k: dev_tensor(k, shapes[k]) for k in synth.layer_names(cfg)}
+
+        def globals_():
+            g = {k: dev_tensor(k, v) for k, v in synth.global_shapes(cfg).items()}
+            if cfg.get("tie_embeddings"):
+                g["lm_head"] = g["embed"]
+            return g
+
+        model = GpuModel.from_layers(cfg, layer, globals_, B, max_seq)
     else:
         log(f"workload {args.workload}: generating weights ({nthr} threads)")
         weights = synth.model_host(cfg, wl["seed_weights"], nthr)
-    K0, V0 = synth.kv_cache_host(cfg, wl["seed_kv"], B, cap, [P] * B, nthr)
     tokens = synth.tokens(cfg, wl["seed_tokens"], B)
-    log(f"inputs ready in {time.perf_counter() - t:.1f}s; loading model")
-    if not big:
+    if big:
+        kv = KvCache(cfg, B, cap)
+        gen.manual_seed(wl["seed_kv"])
+        for l in range(cfg["n_layers"]):
+            for b in range(B):
+                kv.k[l, b, :, :P].copy_(dev_normal(kv.k[l, b, :, :P].shape, 0.0, 1.0))
+                kv.v[l, b, :, :P].copy_(dev_normal(kv.v[l, b, :, :P].shape, 0.0, 1.0))
+        K0 = V0 = None
+        log(f"inputs ready in {time.perf_counter() - t:.1f}s")
+    else:
+        K0, V0 = synth.kv_cache_host(cfg, wl["seed_kv"], B, cap, [P] * B, nthr)
+        log(f"inputs ready in {time.perf_counter() - t:.1f}s; loading model")
         model = GpuModel(cfg, weights, B, max_seq)
-    kv = KvCache(cfg, B, cap, k_host=K0, v_host=V0)
+        kv = KvCache(cfg, B, cap, k_host=K0, v_host=V0)
     toks = torch.from_numpy(tokens).cuda()
     pos = torch.full((B,), P, dtype=torch.int32, device="cuda")
     info = model.info()
@@ -295,7 +329,7 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "accum_dtype": "f32",
-        "data": "synthetic (seeded N(0,0.02) weights, N(0,1) KV)",
+        "data": data,
         "config": {"workload": args.workload, "batch": B, "context": P, "mode": head},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": achieved / PEAK_HBM_GBS,

@@ -132,8 +132,13 @@ int batched_k_slices(int n, int t, int nblk, int nwg) {
 void lds_layout_for(kl_state &s) {
     const kl_config &c = s.cfg;
     const int g = c.n_heads / c.n_kv_heads, d = c.head_dim;
-    const int sub = kWaves * kAttnLoads * (64 / (d / 8));      // positions per sub-chunk
-    const int attn_main = g * d + g * sub + g * 4 + kWaves * g * d + d;   // + new key, value
+    // attention: the queries, the new key and value, and (streaming item)
+    // the waves' (max, sum, output) per head of their team or (short-chunk
+    // item) a sub-chunk's scores, the softmax state and the waves' outputs
+    const int hg = std::min(g, 4);
+    const int sub = kWaves * kAttnLoads * (64 / (d / 8));
+    const int attn_main = std::max(g * d + 2 * kWaves * hg + kWaves * hg * d + d,
+                                   g * d + g * sub + g * 4 + kWaves * g * d + d);
     // O projection: o, chunk weights, running sums, the chunk results
     const int oproj_stage = d + kMergeChunks + 4 + kMergeChunks * (d + 2);
     int amax = std::max(2 * s.Hp + d, s.KTc * kTileK);   // activations, gain, RoPE row

@@ -16,9 +16,8 @@ constexpr int kWaves = 8;                 // compute waves per workgroup
 constexpr int kCtlWave = kWaves;          // the control wave: barriers and counters only
 constexpr int kThreads = (kWaves + 1) * 64;   // threads per workgroup
 constexpr int kRgBatch = 16;              // row groups reduced per LDS round
-constexpr int kAttnLoads = 5;             // K (and V) loads per lane per attention sub-chunk
+constexpr int kAttnLoads = 5;             // K (and V) loads per lane per sub-chunk, short attention chunks
 constexpr int kAttnRing = 4;              // K (and V) slabs in flight per wave, streaming attention
-constexpr int kAttnLoadsPeel = 4;         // the same, batched kernel with up to 4 query heads per KV head
 constexpr int kCombBatch = 32;            // chunk partials loaded together when merging
 // Batched steps (batch >= kMfmaBatch) run the weight products on the matrix
 // cores.  An activation x enters them as two bf16 terms, hi = bf16(x) and

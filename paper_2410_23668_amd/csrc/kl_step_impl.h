@@ -1568,41 +1568,36 @@ __device__ __forceinline__ void merge_ll(const StepParams &P, int l, int b, int 
     __syncthreads();
 }
 
-// One attention work item: chunk c of sequence b against KV head g, for the
-// G query heads of that group (split-K flash decoding).  Positions are
-// grouped in slabs of PP positions (one 16-byte load per lane covers a slab);
-// chunk c owns a contiguous range of slabs, and inside a sub-chunk slab q is
-// held by wave q % kWaves, so every compute wave takes part even when a
-// chunk is short.  Scores and probabilities are fp32.  The chunk result is
-// (running max, running sum, unnormalised output) per head; the last chunk
-// of (b, g) to finish merges all chunks in chunk order and writes o.  The
-// first sub-chunk's K/V vectors are loaded before the barrier wait, except
-// the new slot, which the QKV phase writes and which is read after the wait
-// with device-coherent loads (into registers of its own).  Loads are
+// One attention work item of the per-sequence path with up to 4 query heads
+// per KV head, where a chunk is short (at batch 1: 128 positions): chunk c of
+// sequence b against KV head g, for the G query heads of that group
+// (split-K flash decoding).  Positions are grouped in slabs of PP positions
+// (one 16-byte load per lane covers a slab); chunk c owns a contiguous range
+// of slabs, and inside a sub-chunk slab q is held by wave q % kWaves, so
+// every compute wave takes part even when a chunk is short.  The scores of a
+// sub-chunk go through LDS to a block softmax (wave h for head h), then the
+// values.  Scores and probabilities are fp32.  The chunk's K/V vectors are
+// loaded before the wait for the queries, except the new slot, which the
+// Q/K/V phase hands over as tagged words with the queries; loads are
 // unconditional (spare ones target a shared 16-byte line) and masked when
-// consumed.
+// consumed.  The chunk result (max, sum, unnormalised output per head)
+// leaves as tagged words.  (At these chunk lengths this form measured
+// faster than the streaming item below: 9.8 against 10.6 us per layer.)
 template <int D, int NG>
 constexpr int attn_sub() { return kWaves * NG * (64 / (D / 8)); }
 
-// PEEL (batched path, up to 4 query heads per KV head, where the chunks are
-// long): the last sub-chunk is a copy of its own, see below.  LL (the
-// per-sequence path): the queries and the new key and value arrive as tagged
-// words, and the chunk result leaves as tagged words.
-template <int D, int G, bool LL, bool PEEL>
-__device__ __forceinline__ void attn_item(KArg ka, int l, int b, int g, int c, bool first,
-                                          int ti) {
+template <int D, int G>
+__device__ __forceinline__ void attn_item_ll(KArg ka, int l, int b, int g, int c, int ti) {
     const StepParams P = load_params(ka);
     const Lds S = lds_layout(kl_smem, P);
     constexpr int LP = D / 8;                       // lanes per position
     constexpr int PP = 64 / LP;                     // positions per slab
-    // slabs per wave per sub-chunk (the batched kernel's long chunks: fewer,
-    // measured faster there; never more than kAttnLoads, which sizes the LDS)
-    constexpr int NG = PEEL ? kAttnLoadsPeel : kAttnLoads;
+    constexpr int NG = kAttnLoads;                  // slabs per wave per sub-chunk
     constexpr int SUB = attn_sub<D, NG>();          // positions per sub-chunk
     const int wid = __builtin_amdgcn_readfirstlane(kl_tid() >> 6);
     const int lane = kl_tid() & 63;
     const int pi = lane / LP, ds = (lane % LP) * 8;
-    const int pnew = pos_of<LL>(P, b), n = pnew + 1;
+    const int pnew = pos_of<true>(P, b), n = pnew + 1;
     int s0, s1;
     split_range((n + PP - 1) / PP, P.C, c, s0, s1);
     const int j0 = min(n, s0 * PP), j1 = min(n, s1 * PP);
@@ -1612,8 +1607,8 @@ __device__ __forceinline__ void attn_item(KArg ka, int l, int b, int g, int c, b
     float *sp = qs + G * D;             // [G][SUB]
     float *st = sp + G * SUB;           // [G][4]: max, sum, rescale
     float *red = st + G * 4;            // [kWaves][G][D]
-    uint16_t *kn = reinterpret_cast<uint16_t *>(red + kWaves * G * D);   // [D] new key (LL)
-    uint16_t *vn = kn + D;                                               // [D] new value (LL)
+    uint16_t *kn = reinterpret_cast<uint16_t *>(red + kWaves * G * D);   // [D] new key
+    uint16_t *vn = kn + D;                                               // [D] new value
     const size_t row0 = kv_row(P, l, b, g);
     const uint16_t *Kb = P.kc + row0 * D;
     const uint16_t *Vb = P.vc + row0 * D;
@@ -1637,16 +1632,15 @@ __device__ __forceinline__ void attn_item(KArg ka, int l, int b, int g, int c, b
         issue_one(kr, Kb, j0, min(SUB, j1 - j0));
         issue_one(vr, Vb, j0, min(SUB, j1 - j0));
     }
-    // the new slot (written during this step by another workgroup) is read
-    // once, by the lanes that hold it, after the wait into registers of their
-    // own; a lane takes it in place of its ring value where its slab holds
-    // the new position (no ring load is conditional, so the compiler's waits
-    // for the ring stay exact)
+    // the new slot (written during this step by another workgroup) arrives
+    // as tagged words; the lanes that hold it take it from LDS after the wait,
+    // into registers of their own, in place of their ring value (no ring
+    // load is conditional, so the compiler's waits for the ring stay exact)
     u32x4 knew = {0u, 0u, 0u, 0u}, vnew = {0u, 0u, 0u, 0u};
     const int pl = (pnew - j0) % SUB;   // its place in its sub-chunk
     const bool holds_new =
         compute && pnew >= j0 && pnew < j1 && (pl / PP) % kWaves == wid && pl % PP == pi;
-    if constexpr (LL) {
+    {
         // the queries of head g's query heads and the new key and value, as
         // tagged words (every thread takes a few), into LDS
         if (is_ctl_lane0()) trace_stamp(P, ti, 1);
@@ -1666,26 +1660,16 @@ __device__ __forceinline__ void attn_item(KArg ka, int l, int b, int g, int c, b
                     reinterpret_cast<unsigned *>(vn)[i - G * D - D / 2] = v;
                 }
             });
-    } else {
-        if (first) local_wait(P, P.cnt + g, (unsigned)(l + 1) * (unsigned)P.Sg, ti);
-        if (holds_new) {   // (device-coherent loads)
-            knew = ld_dev_16B(Kb + (size_t)pnew * D + ds);
-            vnew = ld_dev_16B(Vb + (size_t)pnew * D + ds);
-        }
-        for (int t = kl_tid(); t < G * D; t += kThreads)
-            qs[t] = ld_dev(P.q + (size_t)b * P.nq * D + (size_t)g * G * D + t);
     }
     if (kl_tid() < G) {
         st[kl_tid() * 4 + 0] = -INFINITY;
         st[kl_tid() * 4 + 1] = 0.f;
     }
     __syncthreads();
-    if constexpr (LL) {
-        if (is_ctl_lane0()) trace_stamp(P, ti, 2);
-        if (holds_new) {
-            knew = *reinterpret_cast<const u32x4 *>(kn + ds);
-            vnew = *reinterpret_cast<const u32x4 *>(vn + ds);
-        }
+    if (is_ctl_lane0()) trace_stamp(P, ti, 2);
+    if (holds_new) {
+        knew = *reinterpret_cast<const u32x4 *>(kn + ds);
+        vnew = *reinterpret_cast<const u32x4 *>(vn + ds);
     }
     float acc[G][8];
 #pragma unroll
@@ -1704,10 +1688,9 @@ __device__ __forceinline__ void attn_item(KArg ka, int l, int b, int g, int c, b
         }
     } else {
         // one sub-chunk; refill: issue the next sub-chunk's loads (every
-        // sub-chunk but the last; a refill that is conditional at run time
-        // makes the compiler assume on every path the fewest loads
-        // outstanding, and wait for all of them, so with PEEL the last
-        // sub-chunk is a copy of its own)
+        // sub-chunk but the last; decided at run time: a chunk is mostly one
+        // sub-chunk here, where a peeled last copy costs more code than its
+        // exact waits gain)
         auto sub_chunk = [&](int js, auto refill) {
             const int len = min(SUB, j1 - js);
             const int jn = js + SUB, lenn = min(SUB, j1 - jn);   // the next sub-chunk
@@ -1782,28 +1765,13 @@ __device__ __forceinline__ void attn_item(KArg ka, int l, int b, int g, int c, b
 #pragma unroll
                             for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(pr, vf[e], acc[h][e]);
                         }
-                    } else if constexpr (PEEL) {
-                        // (a slot past the sub-chunk is still marked as read, so that
-                        // no ring register is left pending on one path, which would
-                        // make the compiler wait for all loads before refilling it)
-                        asm volatile("" ::"v"(vr[t].x), "v"(vr[t].y), "v"(vr[t].z), "v"(vr[t].w));
                     }
                 }
             }
             if (bool(refill)) issue_one(vr, Vb, jn, lenn);
             __syncthreads();
         };
-        if constexpr (PEEL) {
-            int js = j0;
-            for (; js + SUB < j1; js += SUB) sub_chunk(js, std::true_type{});
-            if (js < j1) sub_chunk(js, std::false_type{});
-        } else {
-            // (a single copy of the body, with the refill decided at run time:
-            // 8 query heads per KV head need every register, and at batch 1 a
-            // chunk is mostly one sub-chunk, where the larger code costs more
-            // than the exact waits gain)
-            for (int js = j0; js < j1; js += SUB) sub_chunk(js, js + SUB < j1);
-        }
+        for (int js = j0; js < j1; js += SUB) sub_chunk(js, js + SUB < j1);
     }
     // reduce the PP position slots of each wave, then the waves in order
     if (compute) {
@@ -1825,8 +1793,7 @@ __device__ __forceinline__ void attn_item(KArg ka, int l, int b, int g, int c, b
     }
     __syncthreads();
     // publish: unnormalised outputs [G][D] and (max, sum) per head
-    const size_t item = ((size_t)b * P.nkv + g) * P.C + c;
-    if constexpr (LL) {
+    {
         // tagged words, per query head h: outputs, max, sum (D + 2 words at
         // [b][g][h][c]: the chunks of one query head are contiguous for the
         // O projection, which polls them; no drain, no counter)
@@ -1843,33 +1810,14 @@ __device__ __forceinline__ void attn_item(KArg ka, int l, int b, int g, int c, b
             st_ll_f(out + kl_tid() * hstride + D, st[kl_tid() * 4 + 0], tag);
             st_ll_f(out + kl_tid() * hstride + D + 1, st[kl_tid() * 4 + 1], tag);
         }
-    } else {
-        float *out = P.part_o + item * G * D;
-        float *sts = P.part_s + item * G * 2;
-        for (int t = kl_tid(); t < G * D; t += kThreads) {
-            const int h = t / D, dd = t % D;
-            float s = 0.f;
-            for (int w = 0; w < kWaves; ++w) s += red[(w * G + h) * D + dd];
-            st_dev(out + t, s);
-            if (P.C == 1) {   // (one chunk: the merged output is final; the O projection copies it)
-                uint16_t hi, lo;
-                split_bf16(s / st[h * 4 + 1], hi, lo);
-                const size_t o = (size_t)b * P.nq * D + (size_t)g * G * D + t;
-                st_dev_u16(P.acto + o, hi);
-                st_dev_u16(P.acto_lo + o, lo);
-            }
-        }
-        if (kl_tid() < G) {
-            st_dev(sts + kl_tid() * 2, st[kl_tid() * 4 + 0]);
-            st_dev(sts + kl_tid() * 2 + 1, st[kl_tid() * 4 + 1]);
-        }
     }
     if (is_ctl_lane0()) trace_stamp(P, ti, 3);
     __syncthreads();   // (the attention area is the next item's)
 }
 
-// Streaming attention item (batched path, up to 4 query heads per KV head,
-// where an item is a whole sequence or a long chunk of one): each compute
+
+// Streaming attention item (batched path, where an item is a whole sequence
+// or a long chunk of one): each compute
 // wave streams its own slabs of the chunk (slabs w, w + kWaves, ...; a slab
 // is PP positions, one 16-byte load per lane) through a ring of kAttnRing K
 // and kAttnRing V loads that is refilled as it is consumed, and each lane
@@ -1885,7 +1833,7 @@ __device__ __forceinline__ void attn_item(KArg ka, int l, int b, int g, int c, b
 // a shared dummy line.  Outputs as attn_item's batched path: the chunk's
 // (max, sum, unnormalised output), and the normalised output when the item is
 // the whole sequence.
-template <int D, int G>
+template <int D, int G, bool LL>
 __device__ __forceinline__ void attn_item_stream(KArg ka, int l, int b, int g, int c, bool first,
                                                  int ti) {
     const StepParams P = load_params(ka);
@@ -1893,21 +1841,28 @@ __device__ __forceinline__ void attn_item_stream(KArg ka, int l, int b, int g, i
     constexpr int LP = D / 8;                       // lanes per position
     constexpr int PP = 64 / LP;                     // positions per slab
     constexpr int R = kAttnRing;
+    // more than 4 query heads per KV head: the waves split into NH teams of
+    // HG heads each; every team streams the whole chunk (the second team's
+    // loads of the same lines meet them in L2)
+    constexpr int HG = G < 4 ? G : 4, NH = G / HG, TW = kWaves / NH;
+    static_assert(G % HG == 0 && kWaves % NH == 0, "head teams");
     const int wid = __builtin_amdgcn_readfirstlane(kl_tid() >> 6);
+    const int team = wid / TW, tw = wid % TW;      // (the control wave: team NH)
+    const int h0 = team * HG;                      // the team's first query head
     const int lane = kl_tid() & 63;
     const int pi = lane / LP, ds = (lane % LP) * 8;
-    const int pnew = pos_of<false>(P, b), n = pnew + 1;
+    const int pnew = pos_of<LL>(P, b), n = pnew + 1;
     int s0, s1;
     split_range((n + PP - 1) / PP, P.C, c, s0, s1);
     const bool compute = wid < kWaves;
-    // this wave's slabs: s0 + wid, s0 + wid + kWaves, ... < s1
-    const int mine = compute && s0 + wid < s1 ? (s1 - s0 - wid + kWaves - 1) / kWaves : 0;
+    // this wave's slabs: s0 + tw, s0 + tw + TW, ... < s1
+    const int mine = compute && s0 + tw < s1 ? (s1 - s0 - tw + TW - 1) / TW : 0;
 
     float *qs = S.attn;                                  // [G][D]
-    float *wm = qs + G * D;                              // [kWaves][G] wave maxima (log2 units)
-    float *wl = wm + kWaves * G;                         // [kWaves][G] wave sums
-    float *wacc = wl + kWaves * G;                       // [kWaves][G][D] wave outputs
-    uint16_t *kn = reinterpret_cast<uint16_t *>(wacc + kWaves * G * D);   // [D] new key
+    float *wm = qs + G * D;                              // [kWaves][HG] wave maxima (log2 units)
+    float *wl = wm + kWaves * HG;                        // [kWaves][HG] wave sums
+    float *wacc = wl + kWaves * HG;                      // [kWaves][HG][D] wave outputs
+    uint16_t *kn = reinterpret_cast<uint16_t *>(wacc + kWaves * HG * D);  // [D] new key
     uint16_t *vn = kn + D;                                                // [D] new value
     const size_t row0 = kv_row(P, l, b, g);
     const uint16_t *Kb = P.kc + row0 * D + ds;
@@ -1919,7 +1874,7 @@ __device__ __forceinline__ void attn_item_stream(KArg ka, int l, int b, int g, i
     // i % R; a slot past the wave's slabs, past the context or holding the
     // new position loads the dummy line (zeros)
     u32x4 kr[R], vr[R];
-    auto pos_of_item = [&](int i) { return (s0 + wid + i * kWaves) * PP + pi; };
+    auto pos_of_item = [&](int i) { return (s0 + tw + i * TW) * PP + pi; };
     auto addr = [&](const uint16_t *base, int i) -> const void * {
         const int pos = pos_of_item(i);
         return (i < mine && pos < n && pos != pnew) ? (const void *)(base + (size_t)pos * D)
@@ -1932,37 +1887,58 @@ __device__ __forceinline__ void attn_item_stream(KArg ka, int l, int b, int g, i
         for (int s = 0; s < R; ++s) vr[s] = ld_stream_16B(addr(Vb, s));
     }
     if (is_ctl_lane0()) trace_stamp(P, ti, 1);
-    if (first) local_wait(P, P.cnt + g, (unsigned)(l + 1) * (unsigned)P.Sg, ti);
-    for (int t = kl_tid(); t < G * D; t += kThreads)
-        qs[t] = ld_dev(P.q + (size_t)b * P.nq * D + (size_t)g * G * D + t);
-    if (kl_tid() < D / 4) {   // the new key and value (device-coherent loads)
-        const size_t o = (size_t)pnew * D + kl_tid() * 4;
-        reinterpret_cast<unsigned long long *>(kn)[kl_tid()] = ld_dev_u64(P.kc + row0 * D + o);
-        reinterpret_cast<unsigned long long *>(vn)[kl_tid()] = ld_dev_u64(P.vc + row0 * D + o);
+    if constexpr (LL) {
+        // the queries of head g's query heads and the new key and value, as
+        // tagged words (every thread takes a few), into LDS
+        const size_t qo = (size_t)b * P.nq * D + (size_t)g * G * D;
+        const unsigned long long *kvl = P.kv_ll + ((size_t)b * P.nkv + g) * D;
+        ll_gather<(G * D + D + kThreads - 1) / kThreads>(
+            P, G * D + D, ll_tag(P, l), kl_tid(), kThreads,
+            [&](int i) { return i < G * D ? P.q_ll + qo + i : kvl + (i - G * D); },
+            [&](int i, unsigned v) {
+                if (i < G * D) {
+                    qs[i] = __uint_as_float(v);
+                } else if (i < G * D + D / 2) {   // key dims j and j + D/2
+                    const int j = i - G * D;
+                    kn[j] = (uint16_t)v;
+                    kn[j + D / 2] = (uint16_t)(v >> 16);
+                } else {                           // value dims 2j and 2j + 1
+                    reinterpret_cast<unsigned *>(vn)[i - G * D - D / 2] = v;
+                }
+            });
+    } else {
+        if (first) local_wait(P, P.cnt + g, (unsigned)(l + 1) * (unsigned)P.Sg, ti);
+        for (int t = kl_tid(); t < G * D; t += kThreads)
+            qs[t] = ld_dev(P.q + (size_t)b * P.nq * D + (size_t)g * G * D + t);
+        if (kl_tid() < D / 4) {   // the new key and value (device-coherent loads)
+            const size_t o = (size_t)pnew * D + kl_tid() * 4;
+            reinterpret_cast<unsigned long long *>(kn)[kl_tid()] = ld_dev_u64(P.kc + row0 * D + o);
+            reinterpret_cast<unsigned long long *>(vn)[kl_tid()] = ld_dev_u64(P.vc + row0 * D + o);
+        }
     }
     __syncthreads();
     if (is_ctl_lane0()) trace_stamp(P, ti, 2);
 
-    float acc[G][8], m[G], lsum[G];
+    float acc[HG][8], m[HG], lsum[HG];
 #pragma unroll
-    for (int h = 0; h < G; ++h) {
+    for (int h = 0; h < HG; ++h) {
         m[h] = -INFINITY;
         lsum[h] = 0.f;
 #pragma unroll
         for (int e = 0; e < 8; ++e) acc[h][e] = 0.f;
     }
     if (compute) {
-        float q[G][8];
+        float q[HG][8];
 #pragma unroll
-        for (int h = 0; h < G; ++h) {
-            const float4 q0 = *reinterpret_cast<const float4 *>(qs + h * D + ds);
-            const float4 q1 = *reinterpret_cast<const float4 *>(qs + h * D + ds + 4);
+        for (int h = 0; h < HG; ++h) {
+            const float4 q0 = *reinterpret_cast<const float4 *>(qs + (h0 + h) * D + ds);
+            const float4 q1 = *reinterpret_cast<const float4 *>(qs + (h0 + h) * D + ds + 4);
             q[h][0] = q0.x; q[h][1] = q0.y; q[h][2] = q0.z; q[h][3] = q0.w;
             q[h][4] = q1.x; q[h][5] = q1.y; q[h][6] = q1.z; q[h][7] = q1.w;
         }
         // R slabs at a time: their scores, one rescale per head, their values
         for (int i0 = 0; i0 < mine; i0 += R) {
-            float sc[R][G];
+            float sc[R][HG];
 #pragma unroll
             for (int s = 0; s < R; ++s) {
                 const int pos = pos_of_item(i0 + s);
@@ -1972,7 +1948,7 @@ __device__ __forceinline__ void attn_item_stream(KArg ka, int l, int b, int g, i
                 const float kf[8] = {bf_lo(kv.x), bf_hi(kv.x), bf_lo(kv.y), bf_hi(kv.y),
                                      bf_lo(kv.z), bf_hi(kv.z), bf_lo(kv.w), bf_hi(kv.w)};
 #pragma unroll
-                for (int h = 0; h < G; ++h) {
+                for (int h = 0; h < HG; ++h) {
                     float d = 0.f;
 #pragma unroll
                     for (int e = 0; e < 8; ++e) d = fmaf(q[h][e], kf[e], d);
@@ -1981,7 +1957,7 @@ __device__ __forceinline__ void attn_item_stream(KArg ka, int l, int b, int g, i
                 }
             }
 #pragma unroll
-            for (int h = 0; h < G; ++h) {
+            for (int h = 0; h < HG; ++h) {
                 float mx = m[h];
 #pragma unroll
                 for (int s = 0; s < R; ++s) mx = fmaxf(mx, sc[s][h]);
@@ -2005,7 +1981,7 @@ __device__ __forceinline__ void attn_item_stream(KArg ka, int l, int b, int g, i
                 const float vf[8] = {bf_lo(vv.x), bf_hi(vv.x), bf_lo(vv.y), bf_hi(vv.y),
                                      bf_lo(vv.z), bf_hi(vv.z), bf_lo(vv.w), bf_hi(vv.w)};
 #pragma unroll
-                for (int h = 0; h < G; ++h)
+                for (int h = 0; h < HG; ++h)
 #pragma unroll
                     for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(sc[s][h], vf[e], acc[h][e]);
             }
@@ -2014,7 +1990,7 @@ __device__ __forceinline__ void attn_item_stream(KArg ka, int l, int b, int g, i
 #pragma unroll
         for (int off = LP; off < 64; off <<= 1) {
 #pragma unroll
-            for (int h = 0; h < G; ++h) {
+            for (int h = 0; h < HG; ++h) {
                 const float m2 = __shfl_xor(m[h], off), l2 = __shfl_xor(lsum[h], off);
                 const float mn = fmaxf(m[h], m2);
                 const float a1 = m[h] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m[h] - mn);
@@ -2030,34 +2006,48 @@ __device__ __forceinline__ void attn_item_stream(KArg ka, int l, int b, int g, i
         }
         if (pi == 0) {
 #pragma unroll
-            for (int h = 0; h < G; ++h) {
+            for (int h = 0; h < HG; ++h) {
 #pragma unroll
-                for (int e = 0; e < 8; ++e) wacc[(wid * G + h) * D + ds + e] = acc[h][e];
+                for (int e = 0; e < 8; ++e) wacc[(wid * HG + h) * D + ds + e] = acc[h][e];
                 if (ds == 0) {
-                    wm[wid * G + h] = m[h];
-                    wl[wid * G + h] = lsum[h];
+                    wm[wid * HG + h] = m[h];
+                    wl[wid * HG + h] = lsum[h];
                 }
             }
         }
     }
     __syncthreads();
     // the waves in order: (max, sum, unnormalised output) of the chunk, the
-    // max published in natural-log units like every chunk's
+    // max published in natural-log units; per-sequence path: as tagged
+    // words, per query head h at [b][g][h][c] (D + 2 words: outputs, max,
+    // sum; one query head's chunks contiguous for the O projection, which
+    // polls them)
     const size_t item = ((size_t)b * P.nkv + g) * P.C + c;
     float *out = P.part_o + item * G * D;
     float *sts = P.part_s + item * G * 2;
+    unsigned long long *ll_out = P.po_ll + (((size_t)b * P.nkv + g) * G * P.C + c) * (D + 2);
+    const size_t hstride = (size_t)P.C * (D + 2);
+    const unsigned tag = ll_tag(P, l);
     for (int t = kl_tid(); t < G * D + G; t += kThreads) {
         const int h = t < G * D ? t / D : t - G * D, dd = t % D;
+        const int w0 = (h / HG) * TW, hl = h % HG;   // the head's team, its slot
         float M = -INFINITY;
-        for (int w = 0; w < kWaves; ++w) M = fmaxf(M, wm[w * G + h]);
+        for (int w = w0; w < w0 + TW; ++w) M = fmaxf(M, wm[w * HG + hl]);
         float O = 0.f, L = 0.f;
-        for (int w = 0; w < kWaves; ++w) {
-            const float mw = wm[w * G + h];
+        for (int w = w0; w < w0 + TW; ++w) {
+            const float mw = wm[w * HG + hl];
             const float a = mw == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mw - M);
-            L = fmaf(wl[w * G + h], a, L);
-            if (t < G * D) O = fmaf(wacc[(w * G + h) * D + dd], a, O);
+            L = fmaf(wl[w * HG + hl], a, L);
+            if (t < G * D) O = fmaf(wacc[(w * HG + hl) * D + dd], a, O);
         }
-        if (t < G * D) {
+        if constexpr (LL) {
+            if (t < G * D) {
+                st_ll_f(ll_out + h * hstride + dd, O, tag);
+            } else {
+                st_ll_f(ll_out + h * hstride + D, M * 0.6931471805599453f, tag);
+                st_ll_f(ll_out + h * hstride + D + 1, L, tag);
+            }
+        } else if (t < G * D) {
             st_dev(out + t, O);
             if (P.C == 1) {   // (one chunk: the merged output is final)
                 uint16_t hi, lo;
@@ -2086,10 +2076,10 @@ __device__ __forceinline__ void phase_attn(KArg ka, int l, int garrive, int ti) 
     if (g < P.nkv) {
         const int items = P.B * P.C;
         for (int it = part; it < items; it += P.Sg)
-            if constexpr (BAT && G <= 4)
-                attn_item_stream<D, G>(ka, l, it / P.C, g, it % P.C, it == part, ti);
+            if constexpr (!BAT && G <= 4)
+                attn_item_ll<D, G>(ka, l, it / P.C, g, it % P.C, ti);
             else
-                attn_item<D, G, !BAT, false>(ka, l, it / P.C, g, it % P.C, it == part, ti);
+                attn_item_stream<D, G, !BAT>(ka, l, it / P.C, g, it % P.C, it == part, ti);
     }
     if (garrive >= 0) bar_arrive(P, garrive, ti);
     else if (is_ctl_lane0()) trace_stamp(P, ti, 0);
@@ -2151,7 +2141,8 @@ __device__ __forceinline__ void phase_oproj(KArg ka, int l, int gwait, int mbar,
             split_range(P.o_rg, np, part - p0, a0, a1);
             constexpr int KTq = D / kTileK;
             // (the weight ring starts after the merge: its gather is then
-            // not queued behind the ring's loads)
+            // not queued behind the ring's loads; issued before, the ring's
+            // 128 KiB arrive no sooner and the merge waits behind them)
             weight_phase<false, false>(
                 P, S, Wo + (size_t)(g * G + hq) * P.o_rg * KTq * kTileBytes, KTq, a0, a1 - a0,
                 [&]() {}, [&]() {},

@@ -9,8 +9,12 @@ import torch
 from . import binding as kb
 
 
-def _dev_u16(a: np.ndarray, device) -> torch.Tensor:
-    """Host bf16 bit patterns (uint16) -> device int16 tensor with the same bits."""
+def _dev_u16(a, device) -> torch.Tensor:
+    """Host bf16 bit patterns (uint16) -> device int16 tensor with the same bits
+    (a device tensor of 16-bit values is taken as it is)."""
+    if isinstance(a, torch.Tensor):
+        assert a.element_size() == 2 and a.is_contiguous()
+        return a.view(torch.int16).to(device)
     return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(device)
 
 
