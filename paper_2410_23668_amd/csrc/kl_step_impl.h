@@ -236,6 +236,13 @@ __device__ __forceinline__ u32x4 ld_stream_16B(const void *p) {
     return __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
 }
 
+// Block barrier for LDS hand-offs only: the wave's LDS operations complete,
+// then s_barrier; unlike __syncthreads (whose workgroup release fence also
+// waits for every outstanding memory load), loads in flight stay in flight.
+__device__ __forceinline__ void lds_barrier() {
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
 // s_waitcnt vmcnt(0): this wave's stores have completed at their coherence point.
 __device__ __forceinline__ void wait_stores() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
@@ -605,7 +612,7 @@ __device__ __forceinline__ void stage_rms_deferred(const long long *__restrict__
     }
     ss = wave_sum(ss);
     if ((kl_tid() & 63) == 0) sm[kl_tid() >> 6] = ss;
-    __syncthreads();
+    lds_barrier();
 }
 // The scale r of the sequence staged last by stage_rms_deferred (the wave
 // partials are added in wave order: the same value in every thread).
@@ -791,7 +798,7 @@ __device__ __forceinline__ void gemv_rows(const uint8_t *__restrict__ W, int KT,
                     buf[s] = load_next();
                 }
             }
-            __syncthreads();
+            lds_barrier();
             for (int t = kl_tid(); t < nrg * (kTileRows / 2); t += kThreads) {
                 const int rgi = t / (kTileRows / 2), pr = (t % (kTileRows / 2)) * 2;
                 float y0 = 0.f, y1 = 0.f;
@@ -807,7 +814,7 @@ __device__ __forceinline__ void gemv_rows(const uint8_t *__restrict__ W, int KT,
                 }
                 epi(b, (first + (ib + rgi) * stride) * kTileRows + pr, y0, y1);
             }
-            __syncthreads();
+            lds_barrier();
         }
     }
 }
@@ -1533,7 +1540,7 @@ __device__ __forceinline__ void merge_ll(const StepParams &P, int l, int b, int 
         ll_gather<(kMergeChunks * WD + kThreads - 1) / kThreads>(
             P, nc * WD, tag, kl_tid(), kThreads, [&](int i) { return src + (size_t)c0 * WD + i; },
             [&](int i, unsigned v) { raw[i] = __uint_as_float(v); });
-        __syncthreads();
+        lds_barrier();
         if (kl_tid() < 64) {   // wave 0: this round's chunk weights and sum
             const int lane = kl_tid();
             float mx = -INFINITY;
@@ -1556,16 +1563,16 @@ __device__ __forceinline__ void merge_ll(const StepParams &P, int l, int b, int 
                 run[0] = mnew;
             }
         }
-        __syncthreads();
+        lds_barrier();
         for (int t = kl_tid(); t < D; t += kThreads) {
             float acc = c0 == 0 ? 0.f : o[t] * run[2];
             for (int c = 0; c < nc; ++c) acc = fmaf(wts[c], val(c * WD + t), acc);
             o[t] = acc;
         }
-        __syncthreads();
+        lds_barrier();
     }
     for (int t = kl_tid(); t < D; t += kThreads) o[t] = o[t] / run[1];
-    __syncthreads();
+    lds_barrier();
 }
 
 // One attention work item of the per-sequence path with up to 4 query heads
@@ -1665,7 +1672,7 @@ __device__ __forceinline__ void attn_item_ll(KArg ka, int l, int b, int g, int c
         st[kl_tid() * 4 + 0] = -INFINITY;
         st[kl_tid() * 4 + 1] = 0.f;
     }
-    __syncthreads();
+    lds_barrier();
     if (is_ctl_lane0()) trace_stamp(P, ti, 2);
     if (holds_new) {
         knew = *reinterpret_cast<const u32x4 *>(kn + ds);
@@ -1682,9 +1689,9 @@ __device__ __forceinline__ void attn_item_ll(KArg ka, int l, int b, int g, int c
     // control wave takes part in the barriers only)
     if (!compute) {
         for (int js = j0; js < j1; js += SUB) {
-            __syncthreads();
-            __syncthreads();
-            __syncthreads();
+            lds_barrier();
+            lds_barrier();
+            lds_barrier();
         }
     } else {
         // one sub-chunk; refill: issue the next sub-chunk's loads (every
@@ -1721,7 +1728,7 @@ __device__ __forceinline__ void attn_item_ll(KArg ka, int l, int b, int g, int c
                 }
             }
             if (bool(refill)) issue_one(kr, Kb, jn, lenn);
-            __syncthreads();
+            lds_barrier();
             // softmax statistics: wave h owns head h
             if (wid < G) {
                 const int h = wid;
@@ -1743,7 +1750,7 @@ __device__ __forceinline__ void attn_item_ll(KArg ka, int l, int b, int g, int c
                     st[h * 4 + 2] = resc;
                 }
             }
-            __syncthreads();
+            lds_barrier();
             // values
             {
 #pragma unroll
@@ -1769,7 +1776,7 @@ __device__ __forceinline__ void attn_item_ll(KArg ka, int l, int b, int g, int c
                 }
             }
             if (bool(refill)) issue_one(vr, Vb, jn, lenn);
-            __syncthreads();
+            lds_barrier();
         };
         for (int js = j0; js < j1; js += SUB) sub_chunk(js, js + SUB < j1);
     }
@@ -1791,7 +1798,7 @@ __device__ __forceinline__ void attn_item_ll(KArg ka, int l, int b, int g, int c
                 for (int e = 0; e < 8; ++e) red[(wid * G + h) * D + ds + e] = acc[h][e];
         }
     }
-    __syncthreads();
+    lds_barrier();
     // publish: unnormalised outputs [G][D] and (max, sum) per head
     {
         // tagged words, per query head h: outputs, max, sum (D + 2 words at
@@ -1812,7 +1819,7 @@ __device__ __forceinline__ void attn_item_ll(KArg ka, int l, int b, int g, int c
         }
     }
     if (is_ctl_lane0()) trace_stamp(P, ti, 3);
-    __syncthreads();   // (the attention area is the next item's)
+    lds_barrier();   // (the attention area is the next item's)
 }
 
 
@@ -2349,7 +2356,7 @@ __device__ __forceinline__ void phase_down(KArg ka, int l, int gwait, int xbar, 
                             [&](int i) { return P.m_ll + (size_t)b * P.Fp + c0 + i; },
                             [&](int i, unsigned v) { S.a[i] = __uint_as_float(v); });
                     for (int i = nreal + kl_tid(); i < kw; i += kThreads) S.a[i] = 0.f;
-                    __syncthreads();
+                    lds_barrier();
                     if (b == 0 && is_ctl_lane0()) {
                         trace_stamp(P, ti, 2);
                         trace_stamp(P, ti, 3);
