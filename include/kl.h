@@ -79,12 +79,19 @@ typedef enum {
  * step; max_seq bounds positions (the RoPE table covers [0, max_seq)).
  * qkv_bias: 1 if the Q/K/V projections carry biases (the Qwen2.5 variant of
  * Table 2), else 0.  Tied embeddings (Llama 3.2) need no flag: pass the
- * embedding table as the LM head. */
+ * embedding table as the LM head.
+ * n_experts, top_k: a mixture of experts in place of the SwiGLU MLP (the
+ * Mixtral 8x7B variant of Table 2): 2..8 experts per layer, top_k 1 or 2
+ * of them per token, chosen by a router and weighted by the softmax of the
+ * chosen router logits (the lowest index first among equal logits); 0 (or
+ * 1) experts: the dense MLP.  With experts, steps run with batch < 8 and not
+ * in KL_MODE_PER_OP (KL_ERR_UNSUPPORTED otherwise). */
 typedef struct {
     int32_t n_layers, hidden, n_heads, n_kv_heads, head_dim, ffn_dim, vocab;
     float rope_theta, rms_eps;
     int32_t max_batch, max_seq;
     int32_t qkv_bias;
+    int32_t n_experts, top_k;
 } kl_config;
 
 /* One decoder layer's weights: dev bf16, nn.Linear layout [out][in].
@@ -93,10 +100,14 @@ typedef struct {
  *   wo [hidden][n_heads*head_dim]
  *   w_gate, w_up [ffn_dim][hidden], w_down [hidden][ffn_dim]
  *   bq [n_heads*head_dim], bk, bv [n_kv_heads*head_dim]: the Q/K/V biases,
- *   required with cfg.qkv_bias and ignored (may be NULL) without         */
+ *   required with cfg.qkv_bias and ignored (may be NULL) without
+ *   with n_experts > 1: w_gate, w_up [n_experts][ffn_dim][hidden],
+ *   w_down [n_experts][hidden][ffn_dim] (the experts' MLPs, stacked) and
+ *   w_router [n_experts][hidden]; w_router is ignored (may be NULL) without */
 typedef struct {
     const void *attn_norm, *wq, *wk, *wv, *wo, *ffn_norm, *w_gate, *w_up, *w_down;
     const void *bq, *bk, *bv;
+    const void *w_router;
 } kl_layer_ptrs;
 
 /* Whole model: dev bf16 embed [vocab][hidden], final_norm [hidden],

@@ -27,15 +27,17 @@ class KloConfig(ctypes.Structure):
                 ("n_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("ffn_dim", ctypes.c_int32),
                 ("vocab", ctypes.c_int32), ("rope_theta", ctypes.c_double),
-                ("rms_eps", ctypes.c_double)]
+                ("rms_eps", ctypes.c_double), ("n_experts", ctypes.c_int32),
+                ("top_k", ctypes.c_int32)]
 
 
 LAYER_FIELDS = ["attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "w_gate", "w_up", "w_down"]
 BIAS_FIELDS = ["bq", "bk", "bv"]   # optional (absent: no bias)
+MOE_FIELDS = ["w_router"]          # mixture of experts only
 
 
 class KloLayer(ctypes.Structure):
-    _fields_ = [(n, ctypes.c_void_p) for n in LAYER_FIELDS + BIAS_FIELDS]
+    _fields_ = [(n, ctypes.c_void_p) for n in LAYER_FIELDS + BIAS_FIELDS + MOE_FIELDS]
 
 
 def build() -> str:
@@ -67,9 +69,10 @@ def _load():
     lib.klo_softmax.argtypes = [i32, vp, vp]
     lib.klo_attention.argtypes = [i32, i32, i32, i32, i32, vp, vp, vp, vp]
     lib.klo_swiglu.argtypes = [i32, vp, vp, vp]
+    lib.klo_route.argtypes = [i32, i32, vp, vp, vp]
     lib.klo_decode_step.argtypes = [ctypes.POINTER(KloConfig), vp, vp, vp,
                                     ctypes.POINTER(KloLayer), i32, vp, vp, vp, vp, i32, i32,
-                                    vp, vp, i32]
+                                    vp, vp, vp, i32]
     lib.klo_decode_step.restype = i32
     _lib = lib
     return lib
@@ -148,17 +151,29 @@ def swiglu(gate, up):
     return m
 
 
+def route(logits, top_k):
+    """(expert indices, weights) of the top_k largest router logits."""
+    x = np.ascontiguousarray(logits, dtype=np.float64)
+    idx = np.empty(top_k, dtype=np.int32)
+    w = np.empty(top_k, dtype=np.float64)
+    _load().klo_route(x.size, top_k, _p(x), _p(idx), _p(w))
+    return idx, w
+
+
 def config_struct(cfg: dict) -> KloConfig:
     return KloConfig(cfg["n_layers"], cfg["hidden"], cfg["n_heads"], cfg["n_kv_heads"],
                      cfg["head_dim"], cfg["ffn_dim"], cfg["vocab"], float(cfg["rope_theta"]),
-                     float(cfg["rms_eps"]))
+                     float(cfg["rms_eps"]), int(cfg.get("n_experts", 0)),
+                     int(cfg.get("top_k", 0)))
 
 
 def decode_step(cfg: dict, model: dict, tokens, positions, kcache: np.ndarray,
-                vcache: np.ndarray, nthreads: int = 1):
+                vcache: np.ndarray, nthreads: int = 1, router_out: np.ndarray | None = None):
     """One decode step.  ``model`` holds bf16 (uint16) arrays as produced by
     ``synth.model_host``; kcache/vcache ([L][kv_batch][n_kv][capacity][d]) are
-    updated in place.  Returns (logits [B][V], hidden [B][H]) as float64."""
+    updated in place.  Returns (logits [B][V], hidden [B][H]) as float64.
+    router_out ([B][L][n_experts] float64, mixture of experts) receives the
+    router logits."""
     lib = _load()
     tokens = np.ascontiguousarray(tokens, dtype=np.int32)
     positions = np.ascontiguousarray(positions, dtype=np.int32)
@@ -169,7 +184,7 @@ def decode_step(cfg: dict, model: dict, tokens, positions, kcache: np.ndarray,
     layers = (KloLayer * L)()
     keep = []
     for l in range(L):
-        for n in LAYER_FIELDS + BIAS_FIELDS:
+        for n in LAYER_FIELDS + BIAS_FIELDS + MOE_FIELDS:
             if n not in model["layers"][l]:
                 continue
             a = np.ascontiguousarray(model["layers"][l][n], dtype=np.uint16)
@@ -181,7 +196,7 @@ def decode_step(cfg: dict, model: dict, tokens, positions, kcache: np.ndarray,
     rc = lib.klo_decode_step(ctypes.byref(c), _p(model["embed"]), _p(model["final_norm"]),
                              _p(model["lm_head"]), layers, B, _p(tokens), _p(positions),
                              _p(kcache), _p(vcache), kv_batch, cap, _p(logits), _p(hidden),
-                             nthreads)
+                             _p(router_out) if router_out is not None else None, nthreads)
     if rc != 0:
         raise ValueError("oracle: token or position out of range")
     return logits, hidden

@@ -173,6 +173,27 @@ void klo_swiglu(int32_t n, const double *gate, const double *up, double *m) {
     for (int32_t i = 0; i < n; ++i) m[i] = gate[i] / (1.0 + exp(-gate[i])) * up[i];
 }
 
+/* Mixture-of-experts routing (the Mixtral entry of Table 2; the paper does
+ * not describe the layer, the reading follows the model's definition): the
+ * top_k largest router logits, taken one at a time as the largest not yet
+ * taken with the lowest index winning a tie, weighted by the softmax of the
+ * taken logits (equal to the softmax over all logits renormalised over the
+ * taken ones). */
+void klo_route(int32_t n, int32_t top_k, const double *logits, int32_t *idx, double *w) {
+    for (int32_t k = 0; k < top_k; ++k) {
+        int32_t best = -1;
+        for (int32_t e = 0; e < n; ++e) {
+            int32_t taken = 0;
+            for (int32_t j = 0; j < k; ++j) taken |= idx[j] == e;
+            if (!taken && (best < 0 || logits[e] > logits[best])) best = e;
+        }
+        idx[k] = best;
+    }
+    double s[8];
+    for (int32_t k = 0; k < top_k; ++k) s[k] = logits[idx[k]];
+    klo_softmax(top_k, s, w);
+}
+
 /* ---- one decode step ----------------------------------------------------- */
 
 int32_t klo_decode_step(const klo_config *cfg, const uint16_t *embed,
@@ -180,10 +201,12 @@ int32_t klo_decode_step(const klo_config *cfg, const uint16_t *embed,
                         const klo_layer *layers, int32_t batch, const int32_t *tokens,
                         const int32_t *positions, uint16_t *kcache, uint16_t *vcache,
                         int32_t kv_batch, int32_t capacity, double *logits, double *hidden,
-                        int32_t nthreads) {
+                        double *router, int32_t nthreads) {
     const int32_t L = cfg->n_layers, H = cfg->hidden, nq = cfg->n_heads,
                   nkv = cfg->n_kv_heads, d = cfg->head_dim, F = cfg->ffn_dim,
                   Vv = cfg->vocab;
+    const int32_t E = cfg->n_experts > 1 ? cfg->n_experts : 1, K = cfg->top_k;
+    if (E > 1 && (K < 1 || K > E || K > 8)) return -1;
     for (int32_t b = 0; b < batch; ++b) {
         if (tokens[b] < 0 || tokens[b] >= Vv) return -1;
         if (positions[b] < 0 || positions[b] >= capacity) return -1;
@@ -198,6 +221,8 @@ int32_t klo_decode_step(const klo_config *cfg, const uint16_t *embed,
     double *gt = (double *)malloc(sizeof(double) * (size_t)F);
     double *up = (double *)malloc(sizeof(double) * (size_t)F);
     double *m = (double *)malloc(sizeof(double) * (size_t)F);
+    double *acc = (double *)malloc(sizeof(double) * (size_t)H);
+    double *rl = (double *)malloc(sizeof(double) * (size_t)E);
     const int64_t seq_stride = (int64_t)nkv * capacity * d;      /* one (layer, seq) block */
 
     for (int32_t b = 0; b < batch; ++b) {
@@ -237,11 +262,31 @@ int32_t klo_decode_step(const klo_config *cfg, const uint16_t *embed,
             for (int32_t i = 0; i < H; ++i) x[i] += y[i];
 
             klo_rmsnorm(H, x, W->ffn_norm, cfg->rms_eps, u);
-            klo_gemv(F, H, W->w_gate, u, gt, nthreads);
-            klo_gemv(F, H, W->w_up, u, up, nthreads);
-            klo_swiglu(F, gt, up, m);
-            klo_gemv(H, F, W->w_down, m, y, nthreads);
-            for (int32_t i = 0; i < H; ++i) x[i] += y[i];
+            if (E == 1) {
+                klo_gemv(F, H, W->w_gate, u, gt, nthreads);
+                klo_gemv(F, H, W->w_up, u, up, nthreads);
+                klo_swiglu(F, gt, up, m);
+                klo_gemv(H, F, W->w_down, m, y, nthreads);
+                for (int32_t i = 0; i < H; ++i) x[i] += y[i];
+            } else {
+                /* mixture of experts: the router, then the weighted sum of
+                 * the chosen experts' SwiGLU MLPs */
+                int32_t idx[8];
+                double w[8];
+                klo_gemv(E, H, W->w_router, u, rl, nthreads);
+                if (router) memcpy(router + ((int64_t)b * L + l) * E, rl, sizeof(double) * (size_t)E);
+                klo_route(E, K, rl, idx, w);
+                for (int32_t i = 0; i < H; ++i) acc[i] = 0.0;
+                for (int32_t k = 0; k < K; ++k) {
+                    const int64_t e = idx[k];
+                    klo_gemv(F, H, W->w_gate + e * F * H, u, gt, nthreads);
+                    klo_gemv(F, H, W->w_up + e * F * H, u, up, nthreads);
+                    klo_swiglu(F, gt, up, m);
+                    klo_gemv(H, F, W->w_down + e * H * F, m, y, nthreads);
+                    for (int32_t i = 0; i < H; ++i) acc[i] += w[k] * y[i];
+                }
+                for (int32_t i = 0; i < H; ++i) x[i] += acc[i];
+            }
         }
         if (hidden) memcpy(hidden + (int64_t)b * H, x, sizeof(double) * (size_t)H);
         /* Classifier block (Sec. 2): final RMSNorm, then the (untied) LM head. */
@@ -249,5 +294,6 @@ int32_t klo_decode_step(const klo_config *cfg, const uint16_t *embed,
         klo_gemv(Vv, H, lm_head, u, logits + (int64_t)b * Vv, nthreads);
     }
     free(x); free(u); free(q); free(k); free(v); free(o); free(y); free(gt); free(up); free(m);
+    free(acc); free(rl);
     return 0;
 }

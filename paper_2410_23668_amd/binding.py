@@ -43,15 +43,18 @@ class kl_config(ctypes.Structure):
                 ("head_dim", ctypes.c_int32), ("ffn_dim", ctypes.c_int32),
                 ("vocab", ctypes.c_int32), ("rope_theta", ctypes.c_float),
                 ("rms_eps", ctypes.c_float), ("max_batch", ctypes.c_int32),
-                ("max_seq", ctypes.c_int32), ("qkv_bias", ctypes.c_int32)]
+                ("max_seq", ctypes.c_int32), ("qkv_bias", ctypes.c_int32),
+                ("n_experts", ctypes.c_int32), ("top_k", ctypes.c_int32)]
 
 
 LAYER_FIELDS = ["attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "w_gate", "w_up", "w_down"]
 BIAS_FIELDS = ["bq", "bk", "bv"]   # only for models with Q/K/V biases
+MOE_FIELDS = ["w_router"]          # only for mixtures of experts
+PTR_FIELDS = LAYER_FIELDS + BIAS_FIELDS + MOE_FIELDS
 
 
 class kl_layer_ptrs(ctypes.Structure):
-    _fields_ = [(n, ctypes.c_void_p) for n in LAYER_FIELDS + BIAS_FIELDS]
+    _fields_ = [(n, ctypes.c_void_p) for n in PTR_FIELDS]
 
 
 class kl_weight_ptrs(ctypes.Structure):
@@ -141,7 +144,8 @@ def make_config(model: dict, max_batch: int, max_seq: int) -> kl_config:
     return kl_config(model["n_layers"], model["hidden"], model["n_heads"], model["n_kv_heads"],
                      model["head_dim"], model["ffn_dim"], model["vocab"],
                      float(model["rope_theta"]), float(model["rms_eps"]), max_batch, max_seq,
-                     1 if model.get("qkv_bias") else 0)
+                     1 if model.get("qkv_bias") else 0, int(model.get("n_experts", 0)),
+                     int(model.get("top_k", 0)))
 
 
 def kl_load_model(cfg: kl_config, embed: int, final_norm: int, lm_head: int, layers: list,
@@ -149,7 +153,7 @@ def kl_load_model(cfg: kl_config, embed: int, final_norm: int, lm_head: int, lay
     """layers: list of dicts name -> device address.  Returns the state handle."""
     arr = (kl_layer_ptrs * len(layers))()
     for i, lay in enumerate(layers):
-        for n in LAYER_FIELDS + BIAS_FIELDS:
+        for n in PTR_FIELDS:
             setattr(arr[i], n, lay.get(n))
     w = kl_weight_ptrs(embed, final_norm, lm_head, arr)
     out = ctypes.c_void_p()
@@ -164,7 +168,7 @@ def kl_model_create(cfg: kl_config) -> int:
 
 
 def kl_model_set_layer(state: int, layer: int, ptrs: dict, stream: int = 0) -> None:
-    lp = kl_layer_ptrs(*[ptrs.get(n) for n in LAYER_FIELDS + BIAS_FIELDS])
+    lp = kl_layer_ptrs(*[ptrs.get(n) for n in PTR_FIELDS])
     _check(lib().kl_model_set_layer(state, layer, ctypes.byref(lp), stream))
 
 

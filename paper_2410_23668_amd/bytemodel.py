@@ -31,16 +31,26 @@ def paper_table1(n_params: float, n_layers: int, n_kv_heads: int, head_dim: int,
                 flops_per_byte=gflops / gbytes)
 
 
-def layer_weight_bytes(cfg) -> int:
+def active_experts(cfg, batch: int = 1) -> int:
+    """Expert MLPs a step reads per layer: 1 for a dense model; with a
+    mixture of experts, top_k per token, at most all of them (exact at batch
+    1; an upper bound above, where tokens may share experts)."""
+    E = cfg.get("n_experts", 0)
+    return 1 if E <= 1 else min(E, cfg["top_k"] * batch)
+
+
+def layer_weight_bytes(cfg, batch: int = 1) -> int:
     H, nq, nkv, d, F = (cfg[k] for k in ("hidden", "n_heads", "n_kv_heads", "head_dim", "ffn_dim"))
     bias = (nq + 2 * nkv) * d if cfg.get("qkv_bias") else 0   # Q/K/V biases (Qwen2.5)
-    return 2 * (H * nq * d + 2 * H * nkv * d + nq * d * H + 3 * H * F + 2 * H + bias)
+    router = cfg.get("n_experts", 0) * H if cfg.get("n_experts", 0) > 1 else 0
+    mlp = active_experts(cfg, batch) * 3 * H * F
+    return 2 * (H * nq * d + 2 * H * nkv * d + nq * d * H + mlp + 2 * H + bias + router)
 
 
 def step_bytes(cfg, batch: int, context: int) -> int:
     """Algorithmic HBM bytes of one step; ``context`` cached positions per sequence."""
     L, H, nkv, d, V = (cfg[k] for k in ("n_layers", "hidden", "n_kv_heads", "head_dim", "vocab"))
-    weights = L * layer_weight_bytes(cfg) + 2 * (V * H + H)
+    weights = L * layer_weight_bytes(cfg, batch) + 2 * (V * H + H)
     embed_rows = batch * 2 * H
     kv_read = batch * L * 2 * nkv * d * 2 * context
     kv_write = batch * L * 2 * nkv * d * 2
@@ -52,7 +62,9 @@ def weight_macs(cfg) -> int:
     """Multiply-adds of the weight products of one step, per sequence."""
     L, H, nq, nkv, d, F, V = (cfg[k] for k in ("n_layers", "hidden", "n_heads", "n_kv_heads",
                                                  "head_dim", "ffn_dim", "vocab"))
-    return L * (H * nq * d + 2 * H * nkv * d + nq * d * H + 3 * H * F) + V * H
+    E = cfg.get("n_experts", 0)
+    moe = (E * H + active_experts(cfg) * 3 * H * F) if E > 1 else 3 * H * F
+    return L * (H * nq * d + 2 * H * nkv * d + nq * d * H + moe) + V * H
 
 
 def step_flops(cfg, batch: int, context: int) -> int:
@@ -70,11 +82,13 @@ def phase_bytes(cfg, batch: int, context: int) -> dict:
     H, nq, nkv, d, F, V = (cfg[k] for k in ("hidden", "n_heads", "n_kv_heads", "head_dim",
                                             "ffn_dim", "vocab"))
     bias = (nq + 2 * nkv) * d if cfg.get("qkv_bias") else 0
+    ne = active_experts(cfg, batch)
+    router = cfg.get("n_experts", 0) * H if cfg.get("n_experts", 0) > 1 else 0
     return {
         "qkv": 2 * (H * (nq + 2 * nkv) * d + H + bias),
         "attn": batch * 2 * nkv * d * 2 * (context + 1),
         "oproj": 2 * nq * d * H,
-        "gateup": 2 * (2 * H * F + H),
-        "down": 2 * F * H,
+        "gateup": 2 * (ne * 2 * H * F + H + router),
+        "down": 2 * ne * F * H,
         "head": 2 * (V * H + H) + batch * V * 4,
     }

@@ -23,6 +23,7 @@ struct kl_state {
     int Hp, Ap, Fp, qkv_rg, o_rg, gu_rg, down_rg, head_rg;
     size_t layer_stride, off_attn_norm, off_ffn_norm, off_qkv, off_o, off_gu, off_down;
     size_t off_qkv_bias;
+    size_t off_router, gu_estride, down_estride;   // mixture of experts
     size_t off_final_norm, off_lm_head, off_embed;
     uint8_t *arena;
     size_t arena_bytes;
@@ -43,7 +44,7 @@ struct kl_state {
     unsigned long long *trace;
     int trace_max;
     int32_t *rowmaps;                 // device row maps used by set_layer / set_globals
-    const int32_t *maps[4];           // by RowMap
+    const int32_t *maps[5];           // by RowMap
     int nwg, lds_bytes;
     int lds_red, lds_sm, lds_bar;
 };
@@ -94,6 +95,11 @@ kl_status validate_config(const kl_config *c) {
                                         "head_dim 128 (got %d)", g);
     if (c->qkv_bias != 0 && c->qkv_bias != 1)
         return fail(KL_ERR_INVALID_ARGUMENT, "qkv_bias must be 0 or 1");
+    if (c->n_experts < 0 || c->n_experts > 8)   // (the router is one packed row group)
+        return fail(KL_ERR_UNSUPPORTED, "n_experts %d outside [0, 8]", c->n_experts);
+    if (c->n_experts > 1 && (c->top_k < 1 || c->top_k > 2 || c->top_k > c->n_experts))
+        return fail(KL_ERR_UNSUPPORTED, "top_k %d unsupported with %d experts (1 or 2)",
+                    c->top_k, c->n_experts);
     if (c->hidden % 8 != 0 || c->ffn_dim % 8 != 0)
         return fail(KL_ERR_UNSUPPORTED, "hidden and ffn_dim must be multiples of 8");
     if (c->max_batch > 4096) return fail(KL_ERR_UNSUPPORTED, "max_batch above 4096");
@@ -150,9 +156,10 @@ void lds_layout_for(kl_state &s) {
     s.lds_sm = s.lds_red + kWaves * kRgBatch * kTileRows;
     s.lds_bar = s.lds_sm + 64;
     // + the step's epoch, position and validity per sequence, the head's
-    // argmax keys of a group of sequences
-    s.lds_bytes = (s.lds_bar + 2 * kBarGroups + 4 + 2 * kMfmaBatch + 2 * kGemmBatch) *
-                  (int)sizeof(float);
+    // argmax keys of a group of sequences, the experts and their weights per
+    // sequence (two slots)
+    s.lds_bytes = (s.lds_bar + 2 * kBarGroups + 4 + 2 * kMfmaBatch + 2 * kGemmBatch +
+                   4 * kMfmaBatch) * (int)sizeof(float);
 }
 
 // Step scratch for a batch of B sequences (byte offsets from its base; every
@@ -207,7 +214,8 @@ ScratchPlan plan_scratch(const kl_state &S, int B) {
     p.off_qll = take((size_t)bl * c.n_heads * d * 8);
     p.off_kvll = take((size_t)bl * nkv * d * 8);
     p.off_poll = take(items_ll * g * (d + 2) * 8);
-    p.off_mll = take((size_t)bl * S.Fp * 8);
+    const int topk = c.n_experts > 1 ? c.top_k : 1;          // expert slots per token
+    p.off_mll = take((size_t)bl * topk * S.Fp * 8);
     p.off_q = take((size_t)B * c.n_heads * d * 4);
     p.off_po = take(items * g * d * 4);
     p.off_ps = take(items * g * 2 * 4);
@@ -306,6 +314,8 @@ StepParams base_params(const kl_state &s) {
     P.off_attn_norm = s.off_attn_norm; P.off_ffn_norm = s.off_ffn_norm; P.off_qkv = s.off_qkv;
     P.off_qkv_bias = s.off_qkv_bias; P.qkv_bias = c.qkv_bias ? 1 : 0;
     P.off_o = s.off_o; P.off_gu = s.off_gu; P.off_down = s.off_down;
+    P.E = c.n_experts > 1 ? c.n_experts : 1; P.topk = c.n_experts > 1 ? c.top_k : 1;
+    P.off_router = s.off_router; P.gu_estride = s.gu_estride; P.down_estride = s.down_estride;
     P.embed = reinterpret_cast<const uint16_t *>(s.arena + s.off_embed);
     P.final_norm = reinterpret_cast<const float *>(s.arena + s.off_final_norm);
     P.lm_head = reinterpret_cast<const uint16_t *>(s.arena + s.off_lm_head);
@@ -334,13 +344,14 @@ size_t kl_kv_cache_bytes(const kl_config *cfg, int32_t batch, int32_t capacity) 
 }
 
 // Validates one layer's pointers.
-kl_status check_layer_ptrs(const kl_layer_ptrs &L, int l, bool bias) {
+kl_status check_layer_ptrs(const kl_layer_ptrs &L, int l, bool bias, bool moe) {
     const void *ps[] = {L.attn_norm, L.wq, L.wk, L.wv, L.wo, L.ffn_norm, L.w_gate, L.w_up,
-                        L.w_down, L.bq, L.bk, L.bv};
-    for (int i = 0; i < (bias ? 12 : 9); ++i) {
+                        L.w_down, L.bq, L.bk, L.bv, L.w_router};
+    for (int i = 0; i < 13; ++i) {
+        if ((i >= 9 && i < 12 && !bias) || (i == 12 && !moe)) continue;
         if (!ps[i])
             return fail(KL_ERR_INVALID_ARGUMENT, "layer %d has a NULL weight%s pointer", l,
-                        i >= 9 ? " (bias)" : "");
+                        i == 12 ? " (router)" : (i >= 9 ? " (bias)" : ""));
         if (!aligned(ps[i], 2))
             return fail(KL_ERR_INVALID_ARGUMENT, "layer %d weight not 2-byte aligned", l);
     }
@@ -390,6 +401,8 @@ kl_status kl_model_create(const kl_config *cfg, kl_state **out) {
     S->off_qkv_bias = Gm.off_qkv_bias;
     S->off_qkv = Gm.off_qkv; S->off_o = Gm.off_o; S->off_gu = Gm.off_gu;
     S->off_down = Gm.off_down; S->layer_stride = Gm.layer_stride;
+    S->off_router = Gm.off_router; S->gu_estride = Gm.gu_estride;
+    S->down_estride = Gm.down_estride;
     S->off_final_norm = Gm.off_final_norm; S->off_lm_head = Gm.off_lm_head;
     S->off_embed = Gm.off_embed; S->off_dummy = Gm.off_dummy;
     S->arena_bytes = Gm.arena_bytes;
@@ -451,8 +464,8 @@ kl_status kl_model_create(const kl_config *cfg, kl_state **out) {
     // row maps (the same for every layer), kept on the device for set_layer
     {
         std::vector<int32_t> all;
-        size_t at[4];
-        for (int m = 0; m < 4; ++m) {
+        size_t at[5];
+        for (int m = 0; m < 5; ++m) {
             const std::vector<int32_t> v = row_map(c, (RowMap)m);
             at[m] = all.size();
             all.insert(all.end(), v.begin(), v.end());
@@ -460,7 +473,7 @@ kl_status kl_model_create(const kl_config *cfg, kl_state **out) {
         TRY(hipMalloc(&S->rowmaps, all.size() * sizeof(int32_t)));
         TRY(hipMemcpy(S->rowmaps, all.data(), all.size() * sizeof(int32_t),
                       hipMemcpyHostToDevice));
-        for (int m = 0; m < 4; ++m) S->maps[m] = S->rowmaps + at[m];
+        for (int m = 0; m < 5; ++m) S->maps[m] = S->rowmaps + at[m];
     }
     TRY(hipDeviceSynchronize());
 #undef TRY
@@ -474,7 +487,7 @@ kl_status kl_model_set_layer(kl_state *S, int32_t l, const kl_layer_ptrs *w, voi
     const kl_config &c = S->cfg;
     if (l < 0 || l >= c.n_layers)
         return fail(KL_ERR_INVALID_ARGUMENT, "layer %d outside [0, %d)", l, c.n_layers);
-    kl_status st = check_layer_ptrs(*w, l, c.qkv_bias != 0);
+    kl_status st = check_layer_ptrs(*w, l, c.qkv_bias != 0, c.n_experts > 1);
     if (st != KL_OK) return st;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     const kl_layer_ptrs &Lw = *w;
@@ -490,8 +503,9 @@ kl_status kl_model_set_layer(kl_state *S, int32_t l, const kl_layer_ptrs *w, voi
                               c.n_kv_heads * S->qkv_rg * kTileRows, S->maps[kMapQkv], u16(Lw.bq),
                               u16(Lw.bk), u16(Lw.bv), s);
     // the packed matrices of the layer (kl_layout.h: layer_pack_jobs)
-    const uint16_t *srcs[] = {u16(Lw.wq), u16(Lw.wk), u16(Lw.wv), u16(Lw.wo),
-                              u16(Lw.w_gate), u16(Lw.w_up), u16(Lw.w_down)};
+    const uint16_t *srcs[] = {u16(Lw.wq),     u16(Lw.wk),   u16(Lw.wv),     u16(Lw.wo),
+                              u16(Lw.w_gate), u16(Lw.w_up), u16(Lw.w_down), nullptr,
+                              u16(Lw.w_router)};
     for (const PackJob &J : layer_pack_jobs(c, layout_geometry(c, S->nwg))) {
         if (pe != hipSuccess) break;
         const uint16_t *p[3];
@@ -545,7 +559,7 @@ kl_status kl_load_model(const kl_config *cfg, const kl_weight_ptrs *w, void *str
     if (!aligned(w->embed, 2) || !aligned(w->final_norm, 2) || !aligned(w->lm_head, 2))
         return fail(KL_ERR_INVALID_ARGUMENT, "weight pointers must be 2-byte aligned");
     for (int l = 0; l < cfg->n_layers; ++l) {
-        st = check_layer_ptrs(w->layers[l], l, cfg->qkv_bias != 0);
+        st = check_layer_ptrs(w->layers[l], l, cfg->qkv_bias != 0, cfg->n_experts > 1);
         if (st != KL_OK) return st;
     }
     kl_state *S = nullptr;
@@ -590,6 +604,11 @@ static kl_status check_step_args(kl_state *st, const int32_t *token_ids,
     if (mode != KL_MODE_PER_LAYER && mode != KL_MODE_LOOPED && mode != KL_MODE_PER_OP &&
         mode != KL_MODE_PER_LAYER_GRAPH)
         return fail(KL_ERR_INVALID_ARGUMENT, "unknown mode %d", mode);
+    // (a token's experts are chosen in the gate/up phase and kept in LDS
+    // for the down phase of the same launch, on the per-sequence path)
+    if (c.n_experts > 1 && (batch >= kMfmaBatch || mode == KL_MODE_PER_OP))
+        return fail(KL_ERR_UNSUPPORTED, "a mixture of experts runs with batch < %d and not in "
+                                        "the per-op schedule", kMfmaBatch);
     int dev = -1;
     HIP_TRY(hipGetDevice(&dev));
     if (dev != st->device)

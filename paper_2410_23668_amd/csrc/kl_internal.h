@@ -71,6 +71,11 @@ struct StepParams {
     size_t off_attn_norm, off_ffn_norm, off_qkv, off_o, off_gu, off_down;
     size_t off_qkv_bias;       // fp32 Q/K/V biases in packed row order (qkv_bias models)
     int qkv_bias;
+    // mixture of experts (E > 1): E experts per layer, topk per token; the
+    // router (one packed row group) and expert e's gate/up and down matrices
+    // at off_gu + e gu_estride, off_down + e down_estride
+    int E, topk;
+    size_t off_router, gu_estride, down_estride;
     const uint16_t *embed;     // [V][H] bf16, row-major
     const float *final_norm;   // [Hp]
     const uint16_t *lm_head;   // packed tiles

@@ -82,6 +82,7 @@ inline int layout_ffn_blocks(int ktf, int nwg) {
 
 struct Geometry {
     int nwg;
+    int E, topk;               // experts per layer (1: the dense MLP), experts per token
     int Hp, Ap, Fp;            // K extents padded to kTileK: hidden, n_heads d, ffn
     int KTH, KTF, KTq;         // k-tiles of hidden, ffn, one head
     int Sg;                    // workgroups per KV head
@@ -89,8 +90,9 @@ struct Geometry {
     int qkv_rg;                // row groups of one KV head's q/k/v block
     int o_rg, gu_rg, down_rg, head_rg;
     // arena: [layer 0 .. L-1][final norm][LM head][embedding][zero tile]
-    size_t off_attn_norm, off_ffn_norm, off_qkv_bias, off_qkv, off_o, off_gu, off_down,
-        layer_stride;
+    size_t off_attn_norm, off_ffn_norm, off_qkv_bias, off_qkv, off_o, off_router, off_gu,
+        off_down, layer_stride;
+    size_t gu_estride, down_estride;   // bytes from one expert's gate/up (down) to the next
     size_t off_final_norm, off_lm_head, off_embed, off_dummy, arena_bytes;
 };
 
@@ -98,12 +100,17 @@ struct Geometry {
 // the model has them (fp32, packed row order), the q/k/v matrix
 // grouped per KV head (its G query heads, its key, its value; query and key
 // rows in rotation pairs (i, i + d/2)), the O projection per query head (its
-// d columns), gate/up with rows interleaved (gate i, up i), the down
-// projection per FFN column block.
+// d columns), with experts the router (one packed row group), then per
+// expert (or once) gate/up with rows interleaved (gate i, up i) and the down
+// projection per FFN column block.  With experts, each of the top_k expert
+// slots of a token has nwg / top_k workgroups, so the FFN column blocks are
+// counted against that.
 inline Geometry layout_geometry(const kl_config &c, int nwg) {
     Geometry G{};
     const int d = c.head_dim, g = c.n_heads / c.n_kv_heads;
     G.nwg = nwg;
+    G.E = c.n_experts > 1 ? c.n_experts : 1;
+    G.topk = c.n_experts > 1 ? c.top_k : 1;
     G.Hp = layout_pad_k(c.hidden);
     G.Ap = layout_pad_k(c.n_heads * d);
     G.Fp = layout_pad_k(c.ffn_dim);
@@ -111,8 +118,8 @@ inline Geometry layout_geometry(const kl_config &c, int nwg) {
     G.KTF = G.Fp / kTileK;
     G.KTq = d / kTileK;
     G.Sg = nwg / c.n_kv_heads;
-    G.Sc = layout_ffn_blocks(G.KTF, nwg);
-    G.Rc = nwg / G.Sc;
+    G.Sc = layout_ffn_blocks(G.KTF, nwg / G.topk);
+    G.Rc = nwg / G.topk / G.Sc;
     G.KTc = G.KTF / G.Sc;
     G.qkv_rg = (g + 2) * d / kTileRows;
     G.o_rg = c.hidden / kTileRows;
@@ -130,9 +137,12 @@ inline Geometry layout_geometry(const kl_config &c, int nwg) {
     off = layout_align(off + (size_t)c.n_kv_heads * G.qkv_rg * G.KTH * kTileBytes, A);
     G.off_o = off;
     off = layout_align(off + (size_t)c.n_heads * G.o_rg * G.KTq * kTileBytes, A);
-    G.off_gu = off;        off = layout_align(off + (size_t)G.gu_rg * G.KTH * kTileBytes, A);
-    G.off_down = off;
-    off = layout_align(off + (size_t)G.Sc * G.down_rg * G.KTc * kTileBytes, A);
+    G.off_router = off;
+    if (G.E > 1) off = layout_align(off + (size_t)G.KTH * kTileBytes, A);
+    G.gu_estride = layout_align((size_t)G.gu_rg * G.KTH * kTileBytes, A);
+    G.off_gu = off;        off += (size_t)G.E * G.gu_estride;
+    G.down_estride = layout_align((size_t)G.Sc * G.down_rg * G.KTc * kTileBytes, A);
+    G.off_down = off;      off += (size_t)G.E * G.down_estride;
     G.layer_stride = off;
     off = G.layer_stride * c.n_layers;
     G.off_final_norm = off; off = layout_align(off + (size_t)G.Hp * 4, A);
@@ -143,7 +153,7 @@ inline Geometry layout_geometry(const kl_config &c, int nwg) {
     return G;
 }
 
-enum RowMap { kMapQkv = 0, kMapHidden = 1, kMapGateUp = 2, kMapHead = 3 };
+enum RowMap { kMapQkv = 0, kMapHidden = 1, kMapGateUp = 2, kMapHead = 3, kMapRouter = 4 };
 
 inline std::vector<int32_t> row_map(const kl_config &c, RowMap which) {
     std::vector<int32_t> m;
@@ -163,16 +173,18 @@ inline std::vector<int32_t> row_map(const kl_config &c, RowMap which) {
             m.push_back(i);                 // gate row i
             m.push_back((1 << 28) | i);     // up row i
         }
-    } else {
+    } else if (which == kMapHead) {
         const int rows = (c.vocab + kTileRows - 1) / kTileRows * kTileRows;
         for (int r = 0; r < rows; ++r) m.push_back(r < c.vocab ? r : -1);
+    } else {   // the router: one row group of n_experts rows
+        for (int r = 0; r < kTileRows; ++r) m.push_back(r < c.n_experts ? r : -1);
     }
     return m;
 }
 
 // The caller's source matrices (nn.Linear layout [out][in], bf16).
 enum Source { kSrcNone = -1, kSrcWq, kSrcWk, kSrcWv, kSrcWo, kSrcGate, kSrcUp, kSrcDown,
-              kSrcLmHead };
+              kSrcLmHead, kSrcRouter };
 
 // One run of the packing kernel: n_rg row groups x KT k-tiles at byte
 // offset dst (of the layer, or of the arena for the classifier), from the K
@@ -193,13 +205,21 @@ inline std::vector<PackJob> layer_pack_jobs(const kl_config &c, const Geometry &
     for (int h = 0; h < c.n_heads; ++h)   // Wo[:, query head h]
         jobs.push_back({G.off_o + (size_t)h * G.o_rg * G.KTq * kTileBytes, G.o_rg, G.KTq, d,
                         c.n_heads * d, kMapHidden, {kSrcWo, kSrcNone, kSrcNone}, (size_t)h * d});
-    jobs.push_back({G.off_gu, G.gu_rg, G.KTH, c.hidden, c.hidden, kMapGateUp,
-                    {kSrcGate, kSrcUp, kSrcNone}, 0});
-    for (int j = 0; j < G.Sc; ++j) {   // Wd[:, column block j]
-        const int c0 = j * G.KTc * kTileK;
-        jobs.push_back({G.off_down + (size_t)j * G.down_rg * G.KTc * kTileBytes, G.down_rg, G.KTc,
-                        std::max(0, std::min(c.ffn_dim - c0, G.KTc * kTileK)), c.ffn_dim,
-                        kMapHidden, {kSrcDown, kSrcNone, kSrcNone}, (size_t)c0});
+    if (G.E > 1)   // the router [E][H]
+        jobs.push_back({G.off_router, 1, G.KTH, c.hidden, c.hidden, kMapRouter,
+                        {kSrcRouter, kSrcNone, kSrcNone}, 0});
+    for (int e = 0; e < G.E; ++e) {   // (expert e's matrices: source offsets e F H)
+        const size_t eo = (size_t)e * c.ffn_dim * c.hidden;
+        jobs.push_back({G.off_gu + e * G.gu_estride, G.gu_rg, G.KTH, c.hidden, c.hidden,
+                        kMapGateUp, {kSrcGate, kSrcUp, kSrcNone}, eo});
+        for (int j = 0; j < G.Sc; ++j) {   // Wd[:, column block j]
+            const int c0 = j * G.KTc * kTileK;
+            jobs.push_back({G.off_down + e * G.down_estride +
+                                (size_t)j * G.down_rg * G.KTc * kTileBytes,
+                            G.down_rg, G.KTc,
+                            std::max(0, std::min(c.ffn_dim - c0, G.KTc * kTileK)), c.ffn_dim,
+                            kMapHidden, {kSrcDown, kSrcNone, kSrcNone}, eo + (size_t)c0});
+        }
     }
     return jobs;
 }

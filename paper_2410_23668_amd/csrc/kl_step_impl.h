@@ -528,6 +528,11 @@ __device__ __forceinline__ int *seq_table(const StepParams &P) {
 __device__ __forceinline__ unsigned long long *amax_slots(const StepParams &P) {
     return reinterpret_cast<unsigned long long *>(seq_table(P) + 2 * kMfmaBatch);
 }
+// (then, mixture of experts: per sequence, its two experts and their
+// weights (float bits), chosen in the gate/up phase, used by the down phase)
+__device__ __forceinline__ int *route_table(const StepParams &P) {
+    return reinterpret_cast<int *>(amax_slots(P) + kGemmBatch);
+}
 
 // ---------------------------------------------------------------- activations
 
@@ -2167,6 +2172,161 @@ __device__ __forceinline__ void phase_oproj(KArg ka, int l, int gwait, int mbar,
     if (garrive >= 0) bar_arrive(P, garrive, ti);
 }
 
+
+// ---------------------------------------------------------------- mixture of experts
+//
+// Per-sequence path (the Mixtral variant of Table 2).  Each of a token's
+// top_k expert slots has nwg / top_k workgroups, laid out like the dense
+// FFN's (column block j = w / Rc of the slot's expert).  Every workgroup
+// computes the router logits of every sequence itself (same data, same
+// order: the same values everywhere), so no hand-off is needed, and keeps
+// the chosen experts in LDS for the down phase of the same launch.
+
+// Router logits of sequence b from the staged activation (a = x gain, the
+// RMSNorm scale deferred as in the gate/up product): the packed router (one
+// row group of E <= 8 rows) split over the compute waves by k-tiles, the
+// wave partials added in wave order; then the top_k experts (the lowest index
+// first among equal logits) and the softmax of their logits.
+__device__ __forceinline__ void route_experts(const StepParams &P, const Lds &S,
+                                              const uint8_t *Lb, int b) {
+    const int wid = __builtin_amdgcn_readfirstlane(kl_tid() >> 6);
+    const int lane = kl_tid() & 63, row = lane >> 3, sub = lane & 7;
+    const int KT = P.Hp / kTileK;
+    if (wid < kWaves) {
+        const uint8_t *R = Lb + P.off_router + (size_t)lane * 16;
+        float acc = 0.f;
+        for (int kt = (wid * KT) / kWaves; kt < ((wid + 1) * KT) / kWaves; ++kt) {
+            const u32x4 w = *reinterpret_cast<const u32x4 *>(R + (size_t)kt * kTileBytes);
+            const float *ap = S.a + kt * kTileK + sub * 8;
+            const float4 a0 = *reinterpret_cast<const float4 *>(ap);
+            const float4 a1 = *reinterpret_cast<const float4 *>(ap + 4);
+            acc = fmaf(bf_lo(w.x), a0.x, acc);
+            acc = fmaf(bf_hi(w.x), a0.y, acc);
+            acc = fmaf(bf_lo(w.y), a0.z, acc);
+            acc = fmaf(bf_hi(w.y), a0.w, acc);
+            acc = fmaf(bf_lo(w.z), a1.x, acc);
+            acc = fmaf(bf_hi(w.z), a1.y, acc);
+            acc = fmaf(bf_lo(w.w), a1.z, acc);
+            acc = fmaf(bf_hi(w.w), a1.w, acc);
+        }
+        acc = sum8(acc);
+        if (sub == 0) S.red[wid * kTileRows + row] = acc;
+    }
+    lds_barrier();
+    float *logit = S.red + kWaves * kTileRows;
+    if (kl_tid() < kTileRows) {
+        float t = 0.f;
+        for (int w = 0; w < kWaves; ++w) t += S.red[w * kTileRows + kl_tid()];
+        logit[kl_tid()] = t * rms_scale(S.sm, P.H, P.eps);
+    }
+    lds_barrier();
+    if (kl_tid() == 0) {
+        int e0 = 0;
+        for (int e = 1; e < P.E; ++e)
+            if (logit[e] > logit[e0]) e0 = e;
+        int e1 = e0;
+        float w0 = 1.f, w1 = 0.f;
+        if (P.topk == 2) {
+            e1 = -1;
+            for (int e = 0; e < P.E; ++e)
+                if (e != e0 && (e1 < 0 || logit[e] > logit[e1])) e1 = e;
+            const float t = expf(logit[e1] - logit[e0]);   // softmax of the two logits
+            w0 = 1.f / (1.f + t);
+            w1 = t / (1.f + t);
+        }
+        int *rt = route_table(P) + 4 * b;
+        rt[0] = e0;
+        rt[1] = e1;
+        rt[2] = __float_as_int(w0);
+        rt[3] = __float_as_int(w1);
+    }
+    lds_barrier();
+}
+
+// The expert slot, FFN column block and part of this workgroup (slot >= topk
+// or j >= Sc: no FFN rows).
+struct MoeShare { int slot, j, part; };
+__device__ __forceinline__ MoeShare moe_share(const StepParams &P) {
+    const int nwk = P.nwg / P.topk, loc = blockIdx.x % nwk;
+    return MoeShare{(int)blockIdx.x / nwk, loc / P.Rc, loc % P.Rc};
+}
+
+// RMSNorm, router, and the gate/up product + SwiGLU of this workgroup's
+// expert slot for each sequence: m[b][slot] as tagged words.
+__device__ __forceinline__ void moe_gateup(const StepParams &P, const Lds &S, int l, int gwait,
+                                           int ti) {
+    const uint8_t *Lb = P.arena + (size_t)l * P.layer_stride;
+    const float *gain = reinterpret_cast<const float *>(Lb + P.off_ffn_norm);
+    const MoeShare ms = moe_share(P);
+    const bool member = ms.slot < P.topk && ms.j < P.Sc;
+    int first = 0, count = 0;
+    if (member) {   // as the dense FFN: block j covers SwiGLU outputs [j KTc 64, + KTc 64)
+        const int r0 = min(P.gu_rg, ms.j * P.KTc * 2 * kTileK / kTileRows);
+        const int r1 = min(P.gu_rg, (ms.j + 1) * P.KTc * 2 * kTileK / kTileRows);
+        int a0, a1;
+        split_range(r1 - r0, P.Rc, ms.part, a0, a1);
+        first = r0 + a0;
+        count = a1 - a0;
+    }
+    if (gwait >= 0) bar_wait(P, gwait, ti);
+    for (int b = 0; b < P.B; ++b) {
+        stage_rms_deferred(P.xf + (size_t)b * P.Hp, gain, P.H, P.Hp, S.a, S.sm);
+        route_experts(P, S, Lb, b);
+        if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 3);
+        const int e = member ? route_table(P)[4 * b + ms.slot] : 0;
+        gemv_phase<true>(
+            Lb + P.off_gu + (size_t)e * P.gu_estride, P.Hp / kTileK, first, count, 1, 1, S.a,
+            S.red, P.dummy, [&]() {}, [&](int) {},
+            [&](int, int r, float gt, float up) {
+                const float rs = rms_scale(S.sm, P.H, P.eps);
+                gt *= rs;
+                up *= rs;
+                st_ll_f(P.m_ll + ((size_t)b * P.topk + ms.slot) * P.Fp + (r >> 1),
+                        gt / (1.0f + expf(-gt)) * up, ll_tag(P, l));
+            });
+    }
+}
+
+// Down product of this workgroup's expert slot for each sequence, weighted
+// by the slot's router weight, added into the residual.
+__device__ __forceinline__ void moe_down(const StepParams &P, const Lds &S, int l, int ti) {
+    const MoeShare ms = moe_share(P);
+    if (ms.slot >= P.topk || ms.j >= P.Sc) return;
+    int a0, a1;
+    split_range(P.down_rg, P.Rc, ms.part, a0, a1);
+    const int kw = P.KTc * kTileK, c0 = ms.j * kw, nreal = max(0, min(kw, P.F - c0));
+    for (int b = 0; b < P.B; ++b) {
+        const int *rt = route_table(P) + 4 * b;
+        const int e = rt[ms.slot];
+        const float we = __int_as_float(rt[2 + ms.slot]);
+        gemv_phase<true>(
+            P.arena + (size_t)l * P.layer_stride + P.off_down + (size_t)e * P.down_estride +
+                (size_t)ms.j * P.down_rg * P.KTc * kTileBytes,
+            P.KTc, a0, a1 - a0, 1, 1, S.a, S.red, P.dummy, [&]() {},
+            [&](int) {
+                if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 1);
+                if ((kl_tid() >> 6) == kCtlWave)
+                    ll_gather<kDownGather>(
+                        P, nreal, ll_tag(P, l), kl_tid() & 63, 64,
+                        [&](int i) {
+                            return P.m_ll + ((size_t)b * P.topk + ms.slot) * P.Fp + c0 + i;
+                        },
+                        [&](int i, unsigned v) { S.a[i] = __uint_as_float(v); });
+                for (int i = nreal + kl_tid(); i < kw; i += kThreads) S.a[i] = 0.f;
+                lds_barrier();
+                if (b == 0 && is_ctl_lane0()) {
+                    trace_stamp(P, ti, 2);
+                    trace_stamp(P, ti, 3);
+                }
+            },
+            [&](int, int r, float y0, float y1) {
+                long long *x = P.xf + (size_t)b * P.Hp;
+                add_fix(x + r, we * y0);
+                add_fix(x + r + 1, we * y1);
+            });
+    }
+}
+
 // RMSNorm + gate/up projection + SwiGLU for FFN column block j = w / Rc:
 // m = silu(Wg u) * (Wu u).  Packed rows alternate gate i, up i.
 template <bool BAT>
@@ -2208,6 +2368,11 @@ __device__ __forceinline__ void phase_gateup(KArg ka, int l, int gwait, int garr
             },
             KT, 0);
         if (garrive >= 0) bar_arrive(P, garrive, ti);
+        return;
+    }
+    if (P.E > 1) {
+        moe_gateup(P, S, l, gwait, ti);
+        if (is_ctl_lane0()) trace_stamp(P, ti, 0);
         return;
     }
     const int j = blockIdx.x / P.Rc, part = blockIdx.x % P.Rc;
@@ -2336,6 +2501,8 @@ __device__ __forceinline__ void phase_down(KArg ka, int l, int gwait, int xbar, 
                 st_dev(part + (size_t)b * P.Hp + r + 1, y1);
             },
             P.KTc, (size_t)P.down_rg * P.KTc);
+    } else if (P.E > 1) {
+        moe_down(P, S, l, ti);
     } else {
         const int j = blockIdx.x / P.Rc, part = blockIdx.x % P.Rc;
         if (j < P.Sc) {

@@ -38,7 +38,7 @@ class GpuModel:
         layers = []
         for l, lay in enumerate(weights["layers"]):
             ptrs = {}
-            for n in kb.LAYER_FIELDS + kb.BIAS_FIELDS:
+            for n in kb.PTR_FIELDS:
                 if n not in lay:
                     continue
                 t = _dev_u16(lay[n], self.device)
@@ -69,7 +69,7 @@ class GpuModel:
         for l in range(model_cfg["n_layers"]):
             lay = layer_fn(l)
             src = {n: _dev_u16(lay[n], self.device)
-                   for n in kb.LAYER_FIELDS + kb.BIAS_FIELDS if n in lay}
+                   for n in kb.PTR_FIELDS if n in lay}
             torch.cuda.synchronize(self.device)
             kb.kl_model_set_layer(self.state, l, {n: t.data_ptr() for n, t in src.items()}, h)
             del src, lay

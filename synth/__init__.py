@@ -28,6 +28,7 @@ KIND = {"attn_norm": 0, "wq": 1, "wk": 2, "wv": 3, "wo": 4,
         "ffn_norm": 5, "w_gate": 6, "w_up": 7, "w_down": 8}
 GLOBAL = {"embed": 0, "final_norm": 1, "lm_head": 2}
 BIAS_KIND = {"bq": 9, "bk": 10, "bv": 11}   # models with Q/K/V biases (cfg["qkv_bias"])
+MOE_KIND = {"w_router": 12}                 # mixture-of-experts models (cfg["n_experts"] > 1)
 WEIGHT_STD = 0.02
 NORM_STD = 0.01
 BIAS_STD = 0.5     # of the order of the projections themselves, so a dropped bias shows
@@ -113,12 +114,16 @@ def layer_shapes(cfg) -> dict:
               "w_down": (H, F)}
     if cfg.get("qkv_bias"):
         shapes.update(bq=(nq * d,), bk=(nkv * d,), bv=(nkv * d,))
+    E = cfg.get("n_experts", 0)
+    if E > 1:   # E stacked expert matrices, and the router
+        shapes.update(w_gate=(E * F, H), w_up=(E * F, H), w_down=(E * H, F), w_router=(E, H))
     return shapes
 
 
 def layer_names(cfg) -> list:
     """The layer tensors of this model (the biases only where it has them)."""
-    return list(KIND) + (list(BIAS_KIND) if cfg.get("qkv_bias") else [])
+    return (list(KIND) + (list(BIAS_KIND) if cfg.get("qkv_bias") else []) +
+            (list(MOE_KIND) if cfg.get("n_experts", 0) > 1 else []))
 
 
 def global_shapes(cfg) -> dict:
@@ -128,7 +133,7 @@ def global_shapes(cfg) -> dict:
 
 def layer_tensor(cfg, seed: int, layer: int, name: str, nthreads=None, out=None) -> np.ndarray:
     shape = layer_shapes(cfg)[name]
-    sid = 16 * layer + (KIND[name] if name in KIND else BIAS_KIND[name])
+    sid = 16 * layer + {**KIND, **BIAS_KIND, **MOE_KIND}[name]
     if name.endswith("norm"):
         return normal_bf16(shape, seed, sid, 1.0, NORM_STD, nthreads, out)
     if name in BIAS_KIND:

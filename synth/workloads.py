@@ -18,6 +18,9 @@ LLAMA3B = dict(n_layers=28, hidden=3072, n_heads=24, n_kv_heads=8, head_dim=128,
                vocab=128256, rope_theta=500000.0, rms_eps=1e-5, tie_embeddings=True)
 QWEN72B = dict(n_layers=80, hidden=8192, n_heads=64, n_kv_heads=8, head_dim=128, ffn_dim=29568,
                vocab=152064, rope_theta=1000000.0, rms_eps=1e-6, qkv_bias=True)
+# and Mixtral 8x7B: a mixture of 8 SwiGLU experts per layer, 2 per token
+MIXTRAL = dict(n_layers=32, hidden=4096, n_heads=32, n_kv_heads=8, head_dim=128, ffn_dim=14336,
+               vocab=32000, rope_theta=1000000.0, rms_eps=1e-5, n_experts=8, top_k=2)
 
 
 def _wl(name, model, batch, context, index):
@@ -40,4 +43,5 @@ WORKLOADS = {
     "qwen72b-b1-ctx4096": _wl("qwen72b-b1-ctx4096", QWEN72B, 1, 4096, 6),
     "llama8b-b8-ctx16384": _wl("llama8b-b8-ctx16384", LLAMA8B, 8, 16384, 7),
     "llama8b-b16-ctx8192": _wl("llama8b-b16-ctx8192", LLAMA8B, 16, 8192, 8),
+    "mixtral-b1-ctx4096": _wl("mixtral-b1-ctx4096", MIXTRAL, 1, 4096, 9),
 }

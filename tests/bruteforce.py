@@ -71,9 +71,22 @@ def decode_step(cfg, model, tokens, positions, K, V):
             o = np.einsum("hj,hjd->hd", scipy.special.softmax(scores, axis=1), Vd)
             x = x + W(l, "wo") @ o.reshape(-1)
             u = rms_normalise(x, W(l, "ffn_norm"), eps)
-            g = W(l, "w_gate") @ u
-            m = g * scipy.special.expit(g) * (W(l, "w_up") @ u)
-            x = x + W(l, "w_down") @ m
+            E = cfg.get("n_experts", 0)
+            if E > 1:
+                # mixture of experts: the top_k router logits (stable sort: the
+                # lowest index first among equal ones), softmax over them
+                r = W(l, "w_router") @ u
+                top = np.argsort(-r, kind="stable")[: cfg["top_k"]]
+                wts = scipy.special.softmax(r[top])
+                Fd = F
+                for e, we in zip(top, wts):
+                    g = W(l, "w_gate")[e * Fd:(e + 1) * Fd] @ u
+                    m = g * scipy.special.expit(g) * (W(l, "w_up")[e * Fd:(e + 1) * Fd] @ u)
+                    x = x + we * (W(l, "w_down")[e * H:(e + 1) * H] @ m)
+            else:
+                g = W(l, "w_gate") @ u
+                m = g * scipy.special.expit(g) * (W(l, "w_up") @ u)
+                x = x + W(l, "w_down") @ m
         hidden.append(x)
         logits.append(W(None, "lm_head") @ rms_normalise(x, W(None, "final_norm"), eps))
     return np.array(logits), np.array(hidden)

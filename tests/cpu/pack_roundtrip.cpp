@@ -12,6 +12,9 @@
 //   down projection, per FFN column block j: columns j KTc 64 ..;
 //   LM head: rows are vocabulary rows, padding rows zero;
 //   Q/K/V biases (fp32): in the q/k/v matrix's packed row order;
+//   with experts: the router (one row group of the experts' rows, zero
+//   padded), and per expert e its own gate/up and down matrices at the
+//   expert strides, read from the e-th stacked source matrix;
 // and every column past a matrix's K is zero.  Also: the jobs' regions lie
 // inside the layer (or the arena) and do not overlap.
 // Prints "pack round trip OK" and exits 0, else prints the failures, exit 1.
@@ -56,7 +59,8 @@ void run(const char *name, kl_config c, int nwg) {
     const int H = c.hidden, F = c.ffn_dim, V = c.vocab, d = c.head_dim;
     const int nq = c.n_heads, nkv = c.n_kv_heads, g = nq / nkv;
     // sources, nn.Linear layout [out][in]
-    std::vector<std::vector<uint16_t>> src(8);
+    std::vector<std::vector<uint16_t>> src(9);
+    const int E = c.n_experts > 1 ? c.n_experts : 1;
     auto fill = [&](int id, int rows, int cols) {
         src[id].resize((size_t)rows * cols);
         for (int r = 0; r < rows; ++r)
@@ -66,10 +70,11 @@ void run(const char *name, kl_config c, int nwg) {
     fill(kSrcWk, nkv * d, H);
     fill(kSrcWv, nkv * d, H);
     fill(kSrcWo, H, nq * d);
-    fill(kSrcGate, F, H);
-    fill(kSrcUp, F, H);
-    fill(kSrcDown, H, F);
+    fill(kSrcGate, E * F, H);   // (experts stacked)
+    fill(kSrcUp, E * F, H);
+    fill(kSrcDown, E * H, F);
     fill(kSrcLmHead, V, H);
+    if (E > 1) fill(kSrcRouter, E, H);
     // Q/K/V biases (ids 8..10, one row of nq d, nkv d, nkv d values)
     std::vector<std::vector<uint16_t>> bias(3);
     for (int k = 0; k < 3; ++k) {
@@ -166,21 +171,30 @@ void run(const char *name, kl_config c, int nwg) {
                 expect("o", packed_at(arena, G.off_o + (size_t)h * G.o_rg * G.KTq * kTileBytes,
                                       G.KTq, r, k),
                        val(kSrcWo, r, h * d + k), r, k);
-    // gate/up interleaved
-    for (int r = 0; r < 2 * F; ++r)
-        for (int k = 0; k < G.Hp; ++k)
-            expect("gate/up", packed_at(arena, G.off_gu, G.KTH, r, k),
-                   k < H ? val(r % 2 == 0 ? kSrcGate : kSrcUp, r / 2, k) : 0, r, k);
-    // down projection per FFN column block
-    for (int j = 0; j < G.Sc; ++j)
-        for (int r = 0; r < H; ++r)
-            for (int k = 0; k < G.KTc * kTileK; ++k) {
-                const int col = j * G.KTc * kTileK + k;
-                expect("down",
-                       packed_at(arena, G.off_down + (size_t)j * G.down_rg * G.KTc * kTileBytes,
-                                 G.KTc, r, k),
-                       col < F ? val(kSrcDown, r, col) : 0, r, col);
-            }
+    // per expert: gate/up interleaved, down projection per FFN column block
+    for (int e = 0; e < E; ++e) {
+        for (int r = 0; r < 2 * F; ++r)
+            for (int k = 0; k < G.Hp; ++k)
+                expect("gate/up", packed_at(arena, G.off_gu + e * G.gu_estride, G.KTH, r, k),
+                       k < H ? val(r % 2 == 0 ? kSrcGate : kSrcUp, e * F + r / 2, k) : 0, r, k);
+        for (int j = 0; j < G.Sc; ++j)
+            for (int r = 0; r < H; ++r)
+                for (int k = 0; k < G.KTc * kTileK; ++k) {
+                    const int col = j * G.KTc * kTileK + k;
+                    expect("down",
+                           packed_at(arena,
+                                     G.off_down + e * G.down_estride +
+                                         (size_t)j * G.down_rg * G.KTc * kTileBytes,
+                                     G.KTc, r, k),
+                           col < F ? val(kSrcDown, e * H + r, col) : 0, r, col);
+                }
+    }
+    // the router: E rows, zero padding rows
+    if (E > 1)
+        for (int r = 0; r < kTileRows; ++r)
+            for (int k = 0; k < G.Hp; ++k)
+                expect("router", packed_at(arena, G.off_router, G.KTH, r, k),
+                       (r < E && k < H) ? val(kSrcRouter, r, k) : 0, r, k);
     // LM head, padding rows zero
     for (int r = 0; r < G.head_rg * kTileRows; ++r)
         for (int k = 0; k < G.Hp; ++k)
@@ -198,6 +212,9 @@ int main() {
     run("d128 group 1", {1, 192, 2, 2, 128, 136, 9, 5e5f, 1e-5f, 1, 64, 0}, 7);
     run("d128 group 3 bias", {1, 192, 6, 2, 128, 200, 11, 1e6f, 1e-6f, 1, 64, 1}, 24);
     run("d64 group 2 bias", {1, 136, 4, 2, 64, 200, 37, 1e4f, 1e-5f, 1, 64, 1}, 16);
+    //                    L  H    nq nkv d    F    V   theta  eps  mb ms  bias E  k
+    run("d128 experts 4 top 2", {1, 192, 4, 2, 128, 320, 11, 1e6f, 1e-5f, 1, 64, 0, 4, 2}, 16);
+    run("d64 experts 8 top 1", {1, 136, 4, 2, 64, 200, 37, 1e4f, 1e-5f, 1, 64, 0, 8, 1}, 7);
     if (g_fail) {
         std::fprintf(stderr, "%d failures\n", g_fail);
         return 1;

@@ -277,6 +277,8 @@ def test_step_with_zero_updates_keeps_embedding_and_closed_form_logits():
     ({"tie_embeddings": True, "n_heads": 6, "n_kv_heads": 2}, [4, 1], 8),
     ({"n_heads": 4, "n_kv_heads": 4}, [0, 7], 8),
     ({"n_heads": 6, "n_kv_heads": 2, "head_dim": 8, "hidden": 24, "n_layers": 3}, [1, 2], 4),
+    ({"n_experts": 4, "top_k": 2}, [3, 5], 8),
+    ({"n_experts": 3, "top_k": 1}, [2, 6], 8),
 ])
 def test_step_matches_independent_brute_force(cfg_over, positions, cap):
     cfg = dict(SMALL, **cfg_over)
@@ -374,3 +376,56 @@ def test_qkv_bias_with_zero_weights_is_the_bias():
     np.testing.assert_array_equal(hidden[0], want)
     # the new key slot holds bf16(RoPE at 0 of bk) = bf16(bk)
     np.testing.assert_array_equal(K[0, 0, :, 0, :], lay["bk"].reshape(nkv, d))
+
+
+def test_route_top_k_ties_and_softmax():
+    # the largest logits, the lowest index first among equal ones, weighted
+    # by the softmax of the chosen logits
+    idx, w = oracle.route([0.5, 2.0, -1.0, 2.0, 1.0], 2)
+    assert list(idx) == [1, 3]
+    np.testing.assert_allclose(w, [0.5, 0.5], rtol=0, atol=1e-15)
+    idx, w = oracle.route([0.0, 1.0, 3.0, 2.0], 2)
+    assert list(idx) == [2, 3]
+    np.testing.assert_allclose(w, [1 / (1 + np.exp(-1.0)), 1 / (1 + np.exp(1.0))], rtol=1e-15)
+    idx, w = oracle.route([4.0, 1.0, 3.0], 1)
+    assert list(idx) == [0] and w[0] == 1.0
+
+
+def test_experts_all_equal_reduce_to_the_dense_mlp():
+    # every expert the same MLP: any routing weights summing to 1 give the
+    # dense model's step exactly up to rounding of the weighted sum
+    E = 4
+    cfg_d = dict(SMALL, n_layers=2)
+    cfg_m = dict(cfg_d, n_experts=E, top_k=2)
+    model, K, V, toks = _small_inputs(cfg_d, 2, 8, [3, 5])
+    moe = {k: v for k, v in model.items() if k != "layers"}
+    moe["layers"] = []
+    for l, lay in enumerate(model["layers"]):
+        ml = dict(lay)
+        for n in ("w_gate", "w_up", "w_down"):
+            ml[n] = np.ascontiguousarray(np.concatenate([lay[n]] * E, axis=0))
+        ml["w_router"] = synth.normal_bf16((E, cfg_d["hidden"]), 77, l, 0.0, 0.02)
+        moe["layers"].append(ml)
+    Km, Vm = K.copy(), V.copy()
+    ld, hd = oracle.decode_step(cfg_d, model, toks, [3, 5], K, V)
+    lm, hm = oracle.decode_step(cfg_m, moe, toks, [3, 5], Km, Vm)
+    assert oracle.rel_l2(hm, hd) < 1e-14 and oracle.rel_l2(lm, ld) < 1e-14
+    np.testing.assert_array_equal(K, Km)
+
+
+def test_router_logits_are_reported_and_drive_the_choice():
+    # the reported router logits decide the experts: zeroing every expert's
+    # down projection except the two chosen ones leaves the step unchanged
+    cfg = dict(SMALL, n_layers=1, n_experts=4, top_k=2)
+    model, K, V, toks = _small_inputs(cfg, 1, 8, [3])
+    router = np.zeros((1, 1, 4))
+    K2, V2 = K.copy(), V.copy()
+    l1, h1 = oracle.decode_step(cfg, model, toks, [3], K, V, router_out=router)
+    chosen, _ = oracle.route(router[0, 0], 2)
+    H, F = cfg["hidden"], cfg["ffn_dim"]
+    lay = model["layers"][0]
+    for e in range(4):
+        if e not in chosen:
+            lay["w_down"][e * H:(e + 1) * H] = 0
+    l2, h2 = oracle.decode_step(cfg, model, toks, [3], K2, V2)
+    np.testing.assert_array_equal(h1, h2)
