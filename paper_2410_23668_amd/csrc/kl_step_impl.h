@@ -553,27 +553,9 @@ __device__ __forceinline__ void ctl_copy_to_lds(const void *src, void *dst, int 
 }
 __device__ __forceinline__ void ctl_copy_wait() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
-// Copy a device-coherent fp32 vector of n values into LDS, zero up to npad
-// (loads are issued in batches of kStageBatch per thread before any is used).
+// Activation staging: loads are issued in batches of kStageBatch per thread
+// before any is used.
 constexpr int kStageBatch = 8;
-__device__ __forceinline__ void stage_vec(const float *__restrict__ src, int n, int npad,
-                                          float *a) {
-    for (int i0 = kl_tid(); i0 < npad; i0 += kStageBatch * kThreads) {
-        float v[kStageBatch];
-#pragma unroll
-        for (int k = 0; k < kStageBatch; ++k) {
-            const int i = i0 + k * kThreads;
-            v[k] = i < n ? ld_dev(src + i) : 0.f;
-        }
-#pragma unroll
-        for (int k = 0; k < kStageBatch; ++k) {
-            const int i = i0 + k * kThreads;
-            if (i < npad) a[i] = v[k];
-        }
-    }
-    __syncthreads();
-}
-
 // a[i] = x[i] * rsqrt(mean(x^2) + eps) * gain[i] for i < n, 0 up to npad,
 // x read from the fixed-point residual stream.  The gain is loaded in the
 // same batch as x (a dependent second batch would cost a second memory round
@@ -596,11 +578,16 @@ __device__ __forceinline__ void stage_rms_deferred(const long long *__restrict__
         float gv[kStageBatch];
         float ev = 0.f;
         const bool first = i0 == (int)kl_tid();
+        // (every load is unconditional, from a clamped address, and masked
+        // when used: a conditional device-coherent load becomes a branch that
+        // waits for its load before the next one is issued)
 #pragma unroll
         for (int k = 0; k < kStageBatch; ++k) {
-            const int i = i0 + k * kThreads;
-            v[k] = i < n ? (long long)ld_dev_u64(xf + i) : 0ll;
-            gv[k] = i < n ? gain[i] : 0.f;
+            const int i = i0 + k * kThreads, ic = min(i, n - 1);
+            const long long xv = (long long)ld_dev_u64(xf + ic);
+            const float g = gain[ic];
+            v[k] = i < n ? xv : 0ll;
+            gv[k] = i < n ? g : 0.f;
         }
         if (first && (int)kl_tid() < ne) ev = esrc[kl_tid()];
 #pragma unroll
@@ -626,42 +613,6 @@ __device__ __forceinline__ float rms_scale(const float *sm, int n, float eps) {
 #pragma unroll
     for (int w = 0; w < kThreads / 64; ++w) ss += sm[w];
     return 1.0f / sqrtf(ss / (float)n + eps);
-}
-
-__device__ __forceinline__ void stage_rmsnorm(const long long *__restrict__ xf,
-                                              const float *__restrict__ gain, int n, int npad,
-                                              float eps, float *a, float *sm,
-                                              const float *esrc = nullptr, float *edst = nullptr,
-                                              int ne = 0) {
-    for (int i0 = kl_tid(); i0 < npad; i0 += kStageBatch * kThreads) {
-        long long v[kStageBatch];
-        float gv[kStageBatch];
-        float ev = 0.f;
-        const bool first = i0 == (int)kl_tid();
-#pragma unroll
-        for (int k = 0; k < kStageBatch; ++k) {
-            const int i = i0 + k * kThreads;
-            v[k] = i < n ? (long long)ld_dev_u64(xf + i) : 0ll;
-            gv[k] = i < n ? gain[i] : 0.f;
-        }
-        if (first && (int)kl_tid() < ne) ev = esrc[kl_tid()];
-#pragma unroll
-        for (int k = 0; k < kStageBatch; ++k) {
-            const int i = i0 + k * kThreads;
-            if (i < npad) {
-                a[i] = from_fix(v[k]);
-                a[npad + i] = gv[k];
-            }
-        }
-        if (first && (int)kl_tid() < ne) edst[kl_tid()] = ev;
-    }
-    __syncthreads();
-    float ss = 0.f;
-    for (int i = kl_tid(); i < n; i += kThreads) ss = fmaf(a[i], a[i], ss);
-    ss = block_sum(ss, sm);
-    const float r = 1.0f / sqrtf(ss / (float)n + eps);
-    for (int i = kl_tid(); i < n; i += kThreads) a[i] = a[i] * r * a[npad + i];
-    __syncthreads();
 }
 
 // ---------------------------------------------------------------- GEMV engine
@@ -1920,12 +1871,23 @@ __device__ __forceinline__ void attn_item_stream(KArg ka, int l, int b, int g, i
             });
     } else {
         if (first) local_wait(P, P.cnt + g, (unsigned)(l + 1) * (unsigned)P.Sg, ti);
-        for (int t = kl_tid(); t < G * D; t += kThreads)
-            qs[t] = ld_dev(P.q + (size_t)b * P.nq * D + (size_t)g * G * D + t);
-        if (kl_tid() < D / 4) {   // the new key and value (device-coherent loads)
-            const size_t o = (size_t)pnew * D + kl_tid() * 4;
-            reinterpret_cast<unsigned long long *>(kn)[kl_tid()] = ld_dev_u64(P.kc + row0 * D + o);
-            reinterpret_cast<unsigned long long *>(vn)[kl_tid()] = ld_dev_u64(P.vc + row0 * D + o);
+        // the queries and the new key and value (device-coherent loads, all
+        // unconditional from clamped addresses and issued together; masked
+        // when stored)
+        constexpr int NQ = (G * D + kThreads - 1) / kThreads;
+        float qv[NQ];
+        const float *qsrc = P.q + (size_t)b * P.nq * D + (size_t)g * G * D;
+#pragma unroll
+        for (int k = 0; k < NQ; ++k) qv[k] = ld_dev(qsrc + min((int)kl_tid() + k * kThreads, G * D - 1));
+        const size_t o = (size_t)pnew * D + min((int)kl_tid(), D / 4 - 1) * 4;
+        const unsigned long long kw = ld_dev_u64(P.kc + row0 * D + o);
+        const unsigned long long vw = ld_dev_u64(P.vc + row0 * D + o);
+#pragma unroll
+        for (int k = 0; k < NQ; ++k)
+            if ((int)kl_tid() + k * kThreads < G * D) qs[kl_tid() + k * kThreads] = qv[k];
+        if (kl_tid() < D / 4) {
+            reinterpret_cast<unsigned long long *>(kn)[kl_tid()] = kw;
+            reinterpret_cast<unsigned long long *>(vn)[kl_tid()] = vw;
         }
     }
     __syncthreads();
