@@ -15,6 +15,7 @@ namespace kl {
 constexpr int kWaves = 8;                 // compute waves per workgroup
 constexpr int kCtlWave = kWaves;          // the control wave: barriers and counters only
 constexpr int kThreads = (kWaves + 1) * 64;   // threads per workgroup
+constexpr int kOEarly = 4;               // O projection: waves that gather the merge (the rest load early)
 constexpr int kRgBatch = 16;              // row groups reduced per LDS round
 constexpr int kAttnLoads = 5;             // K (and V) loads per lane per sub-chunk, short attention chunks
 constexpr int kAttnRing = 4;              // K (and V) slabs in flight per wave, streaming attention

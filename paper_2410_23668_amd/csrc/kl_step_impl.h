@@ -657,13 +657,14 @@ __device__ __forceinline__ RgRange own_rgs(int nrg, const StepParams &P) {
 // Early (the usual case): the first ring of loads is issued before wait() and
 // stage(0), overlapping their latency; otherwise after stage(0), so that the
 // loads stage(0) makes are not queued behind them (a wave's loads complete in
-// order).
-template <bool RowSplit, bool Early, class Wait, class Stage, class Epi>
+// order).  Waves from early_from on issue theirs early in either case (they
+// must then take no part in stage's loads).
+template <bool RowSplit, bool Early, bool Split, class Wait, class Stage, class Epi>
 __device__ __forceinline__ void gemv_rows(const uint8_t *__restrict__ W, int KT, int first,
                                           int count, int stride, int B,
                                           const float *__restrict__ a, float *red,
                                           const uint8_t *dummy, Wait &&wait, Stage &&stage,
-                                          Epi &&epi) {
+                                          Epi &&epi, int early_from = kWaves + 1) {
     constexpr int U = kGemvDepth;
     constexpr int BATCH = RowSplit ? kWaves * kRgBatch : kRgBatch;   // row groups per LDS round
     // wave-uniform values live in scalar registers, so every branch below is
@@ -706,12 +707,14 @@ __device__ __forceinline__ void gemv_rows(const uint8_t *__restrict__ W, int KT,
     // the control wave takes part in the staging and the epilogue only
     const bool compute = wid < kWaves;
     const bool has_rows = count > 0;
-    if (Early && has_rows && compute) start(0);
+    // (waves from early_from on issue their first loads early too)
+    const bool early = Early || (Split && wid >= early_from);
+    if (early && has_rows && compute) start(0);
     wait();
     if (!has_rows) return;
     for (int b = 0; b < B; ++b) {
         for (int ib = 0; ib < count; ib += BATCH) {
-            if (Early) {
+            if (early) {
                 if ((b > 0 || ib > 0) && compute) start(ib);
                 if (ib == 0) stage(b);
             } else {
@@ -777,16 +780,18 @@ __device__ __forceinline__ void gemv_rows(const uint8_t *__restrict__ W, int KT,
 
 // Row groups are shared split-K when they are long enough for every wave to
 // hold two or more tiles, else row-split.
-template <bool Early, class Wait, class Stage, class Epi>
+template <bool Early, bool Split = false, class Wait, class Stage, class Epi>
 __device__ __forceinline__ void gemv_phase(const uint8_t *__restrict__ W, int KT, int first,
                                            int count, int stride, int B,
                                            const float *__restrict__ a, float *red,
                                            const uint8_t *dummy, Wait &&wait, Stage &&stage,
-                                           Epi &&epi) {
+                                           Epi &&epi, int early_from = kWaves + 1) {
     if (KT >= 2 * kWaves)
-        gemv_rows<false, Early>(W, KT, first, count, stride, B, a, red, dummy, wait, stage, epi);
+        gemv_rows<false, Early, Split>(W, KT, first, count, stride, B, a, red, dummy, wait,
+                                       stage, epi, early_from);
     else
-        gemv_rows<true, Early>(W, KT, first, count, stride, B, a, red, dummy, wait, stage, epi);
+        gemv_rows<true, Early, Split>(W, KT, first, count, stride, B, a, red, dummy, wait, stage,
+                                      epi, early_from);
 }
 
 // ---------------------------------------------------------------- batched engine
@@ -1476,9 +1481,9 @@ __device__ __forceinline__ void phase_qkv(KArg ka, int l, int gwait, int qbar, i
 // results (A_c the unnormalised output, M_c the maximum, L_c the sum of the
 // chunk).  The results arrive as tagged words, kMergeChunks chunks per round;
 // a later round rescales the running sums to its new maximum.  Chunks are
-// taken in order, so the sums are the same in every schedule.  Leaves o in
-// S.a[0 .. D).
-template <int D, int G>
+// taken in order, so the sums are the same in every schedule.  Threads
+// 0 .. NT - 1 gather the results; leaves o in S.a[0 .. D).
+template <int D, int G, int NT = kThreads>
 __device__ __forceinline__ void merge_ll(const StepParams &P, int l, int b, int g, int hq,
                                          const Lds &S) {
     constexpr int WD = D + 2;                       // words per chunk and head
@@ -1493,9 +1498,10 @@ __device__ __forceinline__ void merge_ll(const StepParams &P, int l, int b, int 
     auto val = [&](int i) { return raw[i]; };
     for (int c0 = 0; c0 < C; c0 += kMergeChunks) {
         const int nc = min(kMergeChunks, C - c0);
-        ll_gather<(kMergeChunks * WD + kThreads - 1) / kThreads>(
-            P, nc * WD, tag, kl_tid(), kThreads, [&](int i) { return src + (size_t)c0 * WD + i; },
-            [&](int i, unsigned v) { raw[i] = __uint_as_float(v); });
+        if (NT == kThreads || kl_tid() < NT)
+            ll_gather<(kMergeChunks * WD + NT - 1) / NT>(
+                P, nc * WD, tag, kl_tid(), NT, [&](int i) { return src + (size_t)c0 * WD + i; },
+                [&](int i, unsigned v) { raw[i] = __uint_as_float(v); });
         lds_barrier();
         if (kl_tid() < 64) {   // wave 0: this round's chunk weights and sum
             const int lane = kl_tid();
@@ -2114,21 +2120,32 @@ __device__ __forceinline__ void phase_oproj(KArg ka, int l, int gwait, int mbar,
             int a0, a1;
             split_range(P.o_rg, np, part - p0, a0, a1);
             constexpr int KTq = D / kTileK;
-            // (the weight ring starts after the merge: its gather is then
-            // not queued behind the ring's loads; issued before, the ring's
-            // 128 KiB arrive no sooner and the merge waits behind them)
-            weight_phase<false, false>(
-                P, S, Wo + (size_t)(g * G + hq) * P.o_rg * KTq * kTileBytes, KTq, a0, a1 - a0,
-                [&]() {}, [&]() {},
+            // With up to 4 query heads per KV head the waves split: waves
+            // kOEarly .. kWaves - 1 issue their loads before the merge and take
+            // no part in its gather, so half the matrix streams while the merge
+            // waits for the attention's chunks; waves 0 .. kOEarly - 1 gather
+            // the chunks and issue their loads after the merge.  (Every wave
+            // issuing its loads first makes the merge's gather queue behind
+            // them; the control wave in the gather slows it.)  The early waves
+            // go early only when one ring holds their whole share (at 8 query
+            // heads per KV head the share is several rings, and the split was
+            // measured slower).
+            constexpr bool SPLIT = G <= 4;
+            constexpr int NTM = SPLIT ? kOEarly * 64 : kThreads;
+            const int mine = ((a1 - a0) + kWaves - 1) / kWaves * KTq;   // tiles per wave, at most
+            const int EW = SPLIT && mine <= kGemvDepth ? kOEarly : kWaves + 1;
+            gemv_phase<false, SPLIT>(
+                Wo + (size_t)(g * G + hq) * P.o_rg * KTq * kTileBytes, KTq, a0, a1 - a0, 1, P.B,
+                S.a, S.red, P.dummy, [&]() {},
                 [&](int b) {
                     if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 1);
-                    merge_ll<D, G>(P, l, b, g, hq, S);
+                    merge_ll<D, G, NTM>(P, l, b, g, hq, S);
                     if (b == 0 && is_ctl_lane0()) {
                         trace_stamp(P, ti, 2);
                         trace_stamp(P, ti, 3);
                     }
                 },
-                [&](int, int, int, uint16_t *) {}, epi);
+                epi, EW);
         }
     }
     if (garrive >= 0) bar_arrive(P, garrive, ti);
