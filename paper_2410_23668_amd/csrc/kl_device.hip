@@ -84,7 +84,7 @@ hipError_t launch_read_stream(const void *p, size_t bytes, int workgroups, uint3
 }
 
 // The instance for a model's head_dim, query heads per KV head (the host has
-// validated both) and the batch regime (matrix cores at batch >= kMfmaBatch);
+// validated both) and the batch regime (the matrix cores when p.batched);
 // the instances are compiled in separate translation units (kl_step_*.hip).
 StepKernel step_kernel_for(int d, int group, bool batched) {
     if (d == 64) return batched ? step_kernel_d64_batched(group) : step_kernel_d64(group);
@@ -162,7 +162,7 @@ hipError_t step_kernel_setup(int d, int group, int lds_bytes, int *max_blocks_pe
 
 hipError_t launch_step(const StepParams &p, int first_layer, int last_layer, int phases,
                        bool cooperative, int lds_bytes, hipStream_t stream) {
-    const StepKernel k = step_kernel_for(p.d, p.group, p.B >= kMfmaBatch);
+    const StepKernel k = step_kernel_for(p.d, p.group, p.batched != 0);
     if (!k) return hipErrorInvalidValue;
     StepParams pc = p;
     if (cooperative) {
@@ -178,7 +178,7 @@ hipError_t launch_step(const StepParams &p, int first_layer, int last_layer, int
 hipError_t add_step_node(hipGraph_t g, hipGraphNode_t *node, const hipGraphNode_t *dep,
                          const StepParams &p, int first_layer, int last_layer, int phases,
                          bool cooperative, int lds_bytes) {
-    const StepKernel k = step_kernel_for(p.d, p.group, p.B >= kMfmaBatch);
+    const StepKernel k = step_kernel_for(p.d, p.group, p.batched != 0);
     if (!k) return hipErrorInvalidValue;
     StepParams pc = p;   // (the node copies its arguments when it is added)
     void *args[] = {&pc, &first_layer, &last_layer, &phases};

@@ -53,6 +53,10 @@ namespace {
 
 thread_local std::string g_last_error;
 
+// First batch size of the matrix-core path for this model (kBatchedFrom, or
+// kMfmaBatch for a mixture of experts, whose routing needs the GEMV path).
+int batched_from(const kl_config &c) { return c.n_experts > 1 ? kMfmaBatch : kBatchedFrom; }
+
 kl_status fail(kl_status s, const char *fmt, ...) {
     char buf[512];
     va_list ap;
@@ -150,7 +154,7 @@ void lds_layout_for(kl_state &s) {
     int amax = std::max(2 * s.Hp + d, s.KTc * kTileK);   // activations, gain, RoPE row
 
     amax = std::max(amax, std::max(attn_main, oproj_stage));
-    if (c.max_batch >= kMfmaBatch) amax = std::max(amax, kGemmLdsBytes / 4);   // batched path
+    if (c.max_batch >= batched_from(c)) amax = std::max(amax, kGemmLdsBytes / 4);   // batched path
     amax = (amax + 63) & ~63;
     s.lds_red = amax;
     s.lds_sm = s.lds_red + kWaves * kRgBatch * kTileRows;
@@ -195,7 +199,7 @@ ScratchPlan plan_scratch(const kl_state &S, int B) {
     const int d = c.head_dim, g = c.n_heads / c.n_kv_heads, nkv = c.n_kv_heads;
     ScratchPlan p{};
     p.B = B;
-    p.batched = B >= kMfmaBatch;
+    p.batched = B >= batched_from(c);
     size_t so = 0;
     auto take = [&](size_t bytes) {
         const size_t o = so;
@@ -209,7 +213,7 @@ ScratchPlan plan_scratch(const kl_state &S, int B) {
     p.off_cnt_end = so;
     const size_t items = (size_t)nkv * std::max(B, S.Sg);   // >= B * nkv * C for this batch
     p.off_x = take((size_t)B * S.Hp * 8);
-    const int bl = std::min(B, kMfmaBatch - 1);               // per-sequence steps
+    const int bl = std::min(B, batched_from(c) - 1);          // per-sequence steps
     const size_t items_ll = (size_t)nkv * std::max(bl, S.Sg);
     p.off_qll = take((size_t)bl * c.n_heads * d * 8);
     p.off_kvll = take((size_t)bl * nkv * d * 8);
@@ -628,13 +632,14 @@ static StepParams step_params(const kl_state &st, uint8_t *base, const ScratchPl
     P.kv_batch = kv->batch; P.cap = kv->capacity;
     P.logits = logits_out; P.hidden_out = hidden_out;
     P.C = std::max(1, st.Sg / batch);
+    P.batched = batch >= batched_from(st.cfg) ? 1 : 0;
     return P;
 }
 
 // The launches of one step in schedule 'mode'.
 static hipError_t launch_schedule(const StepParams &P, int32_t mode, int lds, hipStream_t s) {
     const int L = P.L;
-    const bool bat = P.B >= kMfmaBatch;
+    const bool bat = P.batched != 0;
     hipError_t e = hipSuccess;
     if (mode == KL_MODE_LOOPED)
         return launch_step(P, 0, L, kPhEmbed | kPhLayer | kPhHead, true, lds, s);
@@ -672,7 +677,7 @@ static kl_status launch_layer_graph(kl_state *st, const StepParams &P, hipStream
         st->graph_exec = nullptr;
         st->graph = nullptr;
         HIP_TRY(hipGraphCreate(&st->graph, 0));
-        const bool bat = P.B >= kMfmaBatch;
+        const bool bat = P.batched != 0;
         const int lds = st->lds_bytes;
         hipGraphNode_t prev = nullptr, node = nullptr;
         HIP_TRY(add_step_node(st->graph, &node, nullptr, P, 0, 0, kPhEmbed, false, lds));
@@ -829,7 +834,7 @@ kl_status kl_get_info(const kl_state *st, kl_info *info) {
     info->threads_per_group = kThreads;
     info->lds_bytes = st->lds_bytes;
     info->attn_chunks_b1 = std::max(1, st->Sg);
-    info->mfma_min_batch = kMfmaBatch;
+    info->mfma_min_batch = batched_from(st->cfg);
     info->arena_bytes = (int64_t)st->arena_bytes;
     info->scratch_bytes = (int64_t)st->scratch_bytes;
     info->noalloc_scratch_bytes = (int64_t)plan_scratch(*st, st->cfg.max_batch).total;

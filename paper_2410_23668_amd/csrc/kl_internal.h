@@ -27,6 +27,13 @@ constexpr int kCombBatch = 32;            // chunk partials loaded together when
 // chunks of kGemmChunkK columns for up to kGemmBatch sequences at a time,
 // weight rows in blocks of 16.
 constexpr int kMfmaBatch = 8;
+// Dense models take the matrix-core path from batch kBatchedFrom on.  The GEMV
+// path streams the weights once per sequence, so its step time grows with the
+// batch (8B shape, 4096 cached positions: 3.06, 5.61, 10.6, 18.0 ms at batch
+// 1, 2, 4, 7), while the matrix-core path streams them once (5.44 ms at
+// batch 8).  A mixture of experts keeps the GEMV path below kMfmaBatch (its
+// experts are chosen per token on that path).
+constexpr int kBatchedFrom = 2;
 constexpr int kGemmBatch = 32;
 constexpr int kGemmChunkK = 512;
 constexpr int kActStride = kGemmChunkK + 8;   // bf16 per staged activation row (bank spread)
@@ -130,6 +137,7 @@ struct StepParams {
     const uint8_t *dummy;      // 16 readable bytes: target of the GEMV ring's spare loads
     int nwg;                   // grid size
     int lds_red, lds_sm, lds_bar;   // dynamic LDS layout (float offsets)
+    int batched;               // this step runs the matrix-core path (set by the host)
     int C;                     // attention chunks per (sequence, KV head)
     unsigned long long *trace; // optional phase timestamps (see kl_set_trace), or null
     int trace_max;             // phases recorded per launch

@@ -294,7 +294,7 @@ __device__ __forceinline__ void bar_init(const StepParams &P) {
     } else if (t == 64) {
         *launch_epoch(P) = __hip_atomic_load(P.epoch_ptr, __ATOMIC_RELAXED,
                                              __HIP_MEMORY_SCOPE_AGENT);
-    } else if (t >= 96 && t < 96 + kMfmaBatch && P.B < kMfmaBatch) {
+    } else if (t >= 96 && t < 96 + kMfmaBatch && !P.batched) {
         const int b = (int)t - 96;
         if (b < P.B) {
             seq_table(P)[b] = eff_pos(P, b);
@@ -1293,7 +1293,7 @@ __device__ __forceinline__ void phase_embed(KArg ka, int gwait, int garrive, int
         }
         // (the batched RMSNorm counters exist, and are used, in batched steps only)
         const int nc = 2 * P.nkv + P.Sc +
-                       (P.B >= kMfmaBatch ? kNormCntStride * ((P.Hp + kGemmChunkK - 1) / kGemmChunkK) : 0);
+                       (P.batched ? kNormCntStride * ((P.Hp + kGemmChunkK - 1) / kGemmChunkK) : 0);
         for (int i = kl_tid(); i < nc; i += kThreads)
             __hip_atomic_store(P.cnt + i, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }

@@ -163,9 +163,9 @@ def test_llama8b_width_two_layers_long_cache():
     assert_bit_exact(outs[2], outs[1], "per_op vs looped")
 
 
-@pytest.mark.parametrize("batch", [8, 16, 32])
+@pytest.mark.parametrize("batch", [2, 3, 8, 16, 32])
 def test_tiny_batched_matrix_core_path(batch):
-    # batches >= 8 run the weight products on the matrix cores (bf16
+    # batches >= 2 run the weight products on the matrix cores (bf16
     # activations); ragged positions, all schedules bit-identical
     say(f"[tiny-batched] batch={batch}")
     rng = np.random.default_rng(batch)
@@ -187,11 +187,12 @@ def test_batched_path_with_batch_above_one_group():
     check_against_oracle(c, c.gpu_step(kb.KL_MODE_LOOPED), ref)
 
 
-@pytest.mark.parametrize("batch", [8, 16, 32])
+@pytest.mark.parametrize("batch", [2, 5, 8, 16, 32])
 def test_llama8b_width_two_layers_batched(batch):
-    # the 8B layer shapes on the matrix-core path, 256-position caches: at
-    # batch 8 and 16 several attention chunks per (sequence, KV head) with
-    # the grid-wide merge (4 and 2 chunks), at batch 32 one chunk
+    # the 8B layer shapes on the matrix-core path (every batch from 2 on for
+    # a dense model), 256-position caches: below 32 several attention chunks
+    # per (sequence, KV head) with the grid-wide merge (16, 6, 4 and 2
+    # chunks), at batch 32 one chunk
     cfg = dict(WORKLOADS["llama8b-b32-ctx4096"]["model"], n_layers=2)
     say(f"[8b-width L=2 B={batch}] building")
     filled = (np.arange(batch, dtype=np.int32) * 37) % 250
