@@ -227,7 +227,7 @@ kl_status kl_decode_greedy(kl_state *st, const int32_t *token_ids, const int32_t
  * no allocating routine.  Its step scratch is not the state's but a static
  * array of the library, one per device, of kl_info.noalloc_scratch_limit bytes
  * (32 MiB), held until the process ends; a step that needs more (see
- * kl_info.noalloc_scratch_bytes: e.g. the 70B shape at batch >= 8) returns
+ * kl_info.noalloc_scratch_bytes: e.g. the 70B shape on the matrix-core path) returns
  * KL_ERR_UNSUPPORTED with nothing enqueued.  Each call first clears the
  * scratch it uses with a fill kernel on 'stream' (one extra launch), so no
  * state carries over from an earlier call.  Every call on a device shares
@@ -258,7 +258,7 @@ kl_status kl_get_info(const kl_state *st, kl_info *info);
  *   workgroup done; its writes complete where the phase ends on a barrier,
  *   issued where it hands tagged words to the next phase), 1: start of the
  *   wait for its inputs, 2: end of that wait, 3: inputs staged (in LDS on the
- *   per-sequence path; batches of 8 or more: the workgroup's share of the
+ *   per-sequence path; matrix-core path: the workgroup's share of the
  *   grid-wide step before the product, RMSNorm or SwiGLU fold, done; an
  *   attention phase: its chunk result published)}]
  * (slots a workgroup does not reach keep their old contents; a launch

@@ -170,7 +170,7 @@ void lds_layout_for(kl_state &s) {
 // region 256-byte aligned):
 //   grid barrier counters (16 groups, 256 B apart) and the local counters:
 //     qkv and attention per KV head, gate/up per FFN column block, and at
-//     B >= kMfmaBatch the batched RMSNorm slice counters (256 bytes apart);
+//     matrix-core steps the batched RMSNorm slice counters (256 bytes apart);
 //   the residual stream, int64 fixed point [B][Hp];
 //   the per-sequence path's tagged words (8 bytes each, for up to
 //     kMfmaBatch - 1 sequences): rotated queries [B][nq d], the new key and
@@ -180,7 +180,7 @@ void lds_layout_for(kl_state &s) {
 //     partials: outputs [B nkv C][group][d], (max, sum) pairs;
 //   the matrix-core path's two-term bf16 activations (both terms, [B][Hp],
 //     [B][Fp], [B][nq d]);
-//   at B >= kMfmaBatch also: the second residual buffer, the fp32 K-slice
+//   on the matrix-core path also: the second residual buffer, the fp32 K-slice
 //     partials of the O and down projections [slices][B][Hp] and of the
 //     gate/up or q/k/v product (never live at the same time), and the
 //     RMSNorm sums of squares per kGemmChunkK columns [B][slices].
@@ -285,7 +285,7 @@ void free_state(kl_state *s) {
 // already satisfied when the launch starts (stream order), so only in-launch
 // hand-offs count:
 //   several phases in one launch      grid barriers and local counters;
-//   batch >= kMfmaBatch (matrix-core path), single phases:
+//   matrix-core path, single phases:
 //     qkv       its product's grid barrier before the fold, and the RMSNorm
 //               slice counters;
 //     oproj     with several attention chunks, the merge's grid barrier;
@@ -293,7 +293,7 @@ void free_state(kl_state *s) {
 //     down      the SwiGLU fold's grid barrier;
 //     head      the final RMSNorm's slice counters;
 //     attn      none (its counters were completed by the qkv launch);
-//   batch < kMfmaBatch, single phases: none (every counter a phase waits on
+//   per-sequence path, single phases: none (every counter a phase waits on
 //   belongs to an earlier phase).
 bool launch_waits_inside(int phases, bool batched, int C) {
     if (phases & kPhEmbed) return phases != kPhEmbed;

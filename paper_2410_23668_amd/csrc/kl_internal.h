@@ -20,7 +20,7 @@ constexpr int kRgBatch = 16;              // row groups reduced per LDS round
 constexpr int kAttnLoads = 5;             // K (and V) loads per lane per sub-chunk, short attention chunks
 constexpr int kAttnRing = 4;              // K (and V) slabs in flight per wave, streaming attention
 constexpr int kCombBatch = 32;            // chunk partials loaded together when merging
-// Batched steps (batch >= kMfmaBatch) run the weight products on the matrix
+// Batched steps (the matrix-core path) run the weight products on the matrix
 // cores.  An activation x enters them as two bf16 terms, hi = bf16(x) and
 // lo = bf16(x - hi), both multiplied into the same fp32 accumulators (about
 // 16 significant bits of x instead of 8).  Activations are staged in LDS in
@@ -116,7 +116,7 @@ struct StepParams {
     float *q;                  // batched path: [B][nq*d] rotated queries
     float *part_o;             // batched path: attention chunk outputs [B*nkv*C][group*d]
     float *part_s;             // batched path: attention chunk (max, sum) [B*nkv*C][group][2]
-    // per-sequence path (batch < kMfmaBatch): values handed between
+    // per-sequence path (batch below the model's matrix-core batch): values handed between
     // workgroups as tagged words (value in the low 32 bits, the tag of the
     // writing step and layer in the high 32 bits)
     unsigned *epoch_ptr;       // device word: the current step's first tag (layer l's tag

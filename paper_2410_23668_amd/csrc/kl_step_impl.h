@@ -165,7 +165,7 @@ __device__ __forceinline__ bool seq_ok(const StepParams &P, int b) {
     const int t = raw_tok(P, b), p = raw_pos(P, b);
     return t >= 0 && t < P.V && p >= 0 && p < min(P.cap, P.max_seq);
 }
-// On the per-sequence path (batch < kMfmaBatch) both are read once per launch
+// On the per-sequence path (at most kMfmaBatch - 1 sequences) both are read once per launch
 // into LDS (bar_init), so that no phase starts with a dependent memory round
 // trip for them.
 __device__ __forceinline__ int *seq_table(const StepParams &P);
@@ -1054,7 +1054,7 @@ __device__ __forceinline__ void gemm_rows(const uint8_t *__restrict__ W, int KT,
 
 // ---------------------------------------------------------------- batched phases
 //
-// A weight phase runs the GEMV engine for batches below kMfmaBatch and the
+// A weight phase runs the GEMV engine on the per-sequence path and the
 // matrix-core engine otherwise (sequences in groups of kGemmBatch; the
 // weights stream once per group).  In the batched path every input is staged
 // as bf16 chunks: prep() runs once after wait(), both once the first weight
