@@ -8,8 +8,9 @@ import numpy as np
 import pytest
 import torch
 
+import synth
 from paper_2410_23668_amd import binding as kb
-from paper_2410_23668_amd.device import KvCache
+from paper_2410_23668_amd.device import GpuModel, KvCache
 from synth.workloads import TINY, WORKLOADS
 from tests.gpu_cases import MODES, Case, assert_bit_exact, check_against_oracle, say
 
@@ -278,3 +279,15 @@ def test_per_layer_graph_replays_match_looped(shape):
     torch.cuda.synchronize()
     assert np.array_equal(other.cpu().numpy().view(np.uint32), want.view(np.uint32))
     c.model.close()
+
+
+def test_matrix_core_batch_per_model():
+    """kl_info.mfma_min_batch: a dense model takes the matrix-core path from
+    batch 2 (the GEMV path streams the weights once per sequence); with
+    experts, the GEMV path (per-token routing) runs below batch 8."""
+    for cfg, want in ((dict(TINY, n_layers=1), 2),
+                      (dict(TINY, n_layers=1, n_experts=4, top_k=2), 8)):
+        weights = synth.model_host(cfg, 5, 4)
+        m = GpuModel(cfg, weights, 8, 64)
+        assert m.info().mfma_min_batch == want, (cfg, m.info().mfma_min_batch)
+        m.close()
