@@ -47,15 +47,14 @@ struct kl_state {
     const int32_t *maps[5];           // by RowMap
     int nwg, lds_bytes;
     int lds_red, lds_sm, lds_bar;
+    int lds_red_seq;                  // the GEMV partial sums on the per-sequence path
+    bool multi_ok;                    // up to kMultiSeq sequences share a GEMV pass
+    int batched_from;                 // first batch of the matrix-core path
 };
 
 namespace {
 
 thread_local std::string g_last_error;
-
-// First batch size of the matrix-core path for this model (kBatchedFrom, or
-// kMfmaBatch for a mixture of experts, whose routing needs the GEMV path).
-int batched_from(const kl_config &c) { return c.n_experts > 1 ? kMfmaBatch : kBatchedFrom; }
 
 kl_status fail(kl_status s, const char *fmt, ...) {
     char buf[512];
@@ -151,19 +150,39 @@ void lds_layout_for(kl_state &s) {
                                    g * d + g * sub + g * 4 + kWaves * g * d + d);
     // O projection: o, chunk weights, running sums, the chunk results
     const int oproj_stage = d + kMergeChunks + 4 + kMergeChunks * (d + 2);
-    int amax = std::max(2 * s.Hp + d, s.KTc * kTileK);   // activations, gain, RoPE row
-
-    amax = std::max(amax, std::max(attn_main, oproj_stage));
-    if (c.max_batch >= batched_from(c)) amax = std::max(amax, kGemmLdsBytes / 4);   // batched path
-    amax = (amax + 63) & ~63;
-    s.lds_red = amax;
-    s.lds_sm = s.lds_red + kWaves * kRgBatch * kTileRows;
-    s.lds_bar = s.lds_sm + 64;
-    // + the step's epoch, position and validity per sequence, the head's
-    // argmax keys of a group of sequences, the experts and their weights per
-    // sequence (two slots)
-    s.lds_bytes = (s.lds_bar + 2 * kBarGroups + 4 + 2 * kMfmaBatch + 2 * kGemmBatch +
-                   4 * kMfmaBatch) * (int)sizeof(float);
+    const auto round64 = [](int v) { return (v + 63) & ~63; };
+    const int rs = kWaves * kRgBatch * kTileRows;   // one sequence's GEMV partial sums
+    // per-sequence path, one sequence per GEMV pass: activations and RoPE row
+    const int one = round64(std::max({2 * s.Hp + d, s.KTc * kTileK, attn_main, oproj_stage}));
+    // kMultiSeq sequences per pass: their activations and RoPE rows, their
+    // SwiGLU blocks, their merged attention outputs before the merge's area
+    const int multi = round64(std::max({kMultiSeq * (s.Hp + d), kMultiSeq * s.KTc * kTileK,
+                                        kMultiSeq * d + kMergeChunks + 4 + kMergeChunks * (d + 2),
+                                        attn_main, 2 * s.Hp + d}));
+    // The first batch of the matrix-core path: with several sequences per
+    // GEMV pass the per-sequence path serves up to kMultiSeq sequences (a
+    // mixture of experts: up to kMfmaBatch - 1, as its routing needs).  The
+    // matrix-core path's area (and its partial sums after it) may overlap
+    // the per-sequence path's partial sums: a launch runs one of the two.
+    const auto layout = [&](bool mu) {
+        s.multi_ok = mu;
+        s.batched_from = c.n_experts > 1 ? kMfmaBatch : (mu ? kMultiSeq + 1 : kBatchedFrom);
+        const int seq_a = mu ? multi : one;
+        const int seq_end = seq_a + (mu ? kMultiSeq : 1) * rs;
+        const bool bat = c.max_batch >= s.batched_from;
+        const int bat_a = bat ? round64(std::max(seq_a, kGemmLdsBytes / 4)) : seq_a;
+        s.lds_red_seq = seq_a;
+        s.lds_red = bat_a;
+        s.lds_sm = std::max(seq_end, bat_a + rs);
+        s.lds_bar = s.lds_sm + 64;
+        // + the step's epoch, position and validity per sequence, the head's
+        // argmax keys of a group of sequences, the experts and their weights
+        // per sequence (two slots)
+        s.lds_bytes = (s.lds_bar + 2 * kBarGroups + 4 + 2 * kMfmaBatch + 2 * kGemmBatch +
+                       4 * kMfmaBatch) * (int)sizeof(float);
+    };
+    layout(c.max_batch >= 2);
+    if (s.multi_ok && s.lds_bytes > 160 * 1024 - 256) layout(false);
 }
 
 // Step scratch for a batch of B sequences (byte offsets from its base; every
@@ -199,7 +218,7 @@ ScratchPlan plan_scratch(const kl_state &S, int B) {
     const int d = c.head_dim, g = c.n_heads / c.n_kv_heads, nkv = c.n_kv_heads;
     ScratchPlan p{};
     p.B = B;
-    p.batched = B >= batched_from(c);
+    p.batched = B >= S.batched_from;
     size_t so = 0;
     auto take = [&](size_t bytes) {
         const size_t o = so;
@@ -213,7 +232,7 @@ ScratchPlan plan_scratch(const kl_state &S, int B) {
     p.off_cnt_end = so;
     const size_t items = (size_t)nkv * std::max(B, S.Sg);   // >= B * nkv * C for this batch
     p.off_x = take((size_t)B * S.Hp * 8);
-    const int bl = std::min(B, batched_from(c) - 1);          // per-sequence steps
+    const int bl = std::min(B, S.batched_from - 1);           // per-sequence steps
     const size_t items_ll = (size_t)nkv * std::max(bl, S.Sg);
     p.off_qll = take((size_t)bl * c.n_heads * d * 8);
     p.off_kvll = take((size_t)bl * nkv * d * 8);
@@ -632,7 +651,11 @@ static StepParams step_params(const kl_state &st, uint8_t *base, const ScratchPl
     P.kv_batch = kv->batch; P.cap = kv->capacity;
     P.logits = logits_out; P.hidden_out = hidden_out;
     P.C = std::max(1, st.Sg / batch);
-    P.batched = batch >= batched_from(st.cfg) ? 1 : 0;
+    P.batched = batch >= st.batched_from ? 1 : 0;
+    // (several sequences share a GEMV pass; the partial sums' place differs
+    // between the two paths)
+    P.multi = !P.batched && batch >= 2 && batch <= kMultiSeq && st.multi_ok ? 1 : 0;
+    P.lds_red = P.batched ? st.lds_red : st.lds_red_seq;
     return P;
 }
 
@@ -834,7 +857,7 @@ kl_status kl_get_info(const kl_state *st, kl_info *info) {
     info->threads_per_group = kThreads;
     info->lds_bytes = st->lds_bytes;
     info->attn_chunks_b1 = std::max(1, st->Sg);
-    info->mfma_min_batch = batched_from(st->cfg);
+    info->mfma_min_batch = st->batched_from;
     info->arena_bytes = (int64_t)st->arena_bytes;
     info->scratch_bytes = (int64_t)st->scratch_bytes;
     info->noalloc_scratch_bytes = (int64_t)plan_scratch(*st, st->cfg.max_batch).total;

@@ -34,6 +34,9 @@ constexpr int kMfmaBatch = 8;
 // batch 8).  A mixture of experts keeps the GEMV path below kMfmaBatch (its
 // experts are chosen per token on that path).
 constexpr int kBatchedFrom = 2;
+// Up to kMultiSeq sequences share one pass of the GEMV engine: each weight
+// tile is applied to every staged vector, so the weights stream once.
+constexpr int kMultiSeq = 4;
 constexpr int kGemmBatch = 32;
 constexpr int kGemmChunkK = 512;
 constexpr int kActStride = kGemmChunkK + 8;   // bf16 per staged activation row (bank spread)
@@ -138,6 +141,8 @@ struct StepParams {
     int nwg;                   // grid size
     int lds_red, lds_sm, lds_bar;   // dynamic LDS layout (float offsets)
     int batched;               // this step runs the matrix-core path (set by the host)
+    int multi;                 // per-sequence path: the B <= kMultiSeq sequences share each
+                               // GEMV pass (set by the host)
     int C;                     // attention chunks per (sequence, KV head)
     unsigned long long *trace; // optional phase timestamps (see kl_set_trace), or null
     int trace_max;             // phases recorded per launch

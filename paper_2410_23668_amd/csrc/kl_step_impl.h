@@ -512,6 +512,19 @@ __device__ __forceinline__ Lds lds_layout(char *smem, const StepParams &P) {
     s.bar = reinterpret_cast<unsigned long long *>(f + P.lds_bar);
     return s;
 }
+// Per-sequence path: with P.multi the B sequences share each GEMV pass and
+// sequence b's staged vector sits b stride floats into the activation area
+// (its wave sums of squares b kSmSeq floats into sm); otherwise every
+// sequence is staged at the start of the area in turn.
+__device__ __forceinline__ float *seq_vec(const StepParams &P, const Lds &S, int b, int stride) {
+    return S.a + (P.multi ? b * stride : 0);
+}
+__device__ __forceinline__ float *seq_sm(const StepParams &P, const Lds &S, int b);
+// The Q/K/V phase's staged RoPE row (cos, sin) of sequence b: after the
+// activation vectors.
+__device__ __forceinline__ float *rope_row(const StepParams &P, const Lds &S, int b) {
+    return S.a + (P.multi ? kMultiSeq * P.Hp + b * P.d : 2 * P.Hp);
+}
 
 __device__ __forceinline__ unsigned long long *bar_bases(const StepParams &P) {
     return lds_layout(kl_smem, P).bar;
@@ -564,9 +577,9 @@ constexpr int kStageBatch = 8;
 // RMSNorm staging for the GEMV path, with the normalisation deferred: the
 // weight product is linear, so W (x r g) = r (W (x g)) with the per-sequence
 // scale r = 1 / sqrt(mean(x^2) + eps) applied in the epilogue (rms_scale).
-// Stages a = x g (and the gain at a + npad, zero padding) and leaves each
-// wave's partial sum of x^2 in sm[wave]; the weight stream starts as soon as
-// a is in LDS, without waiting for a block-wide reduction.
+// Stages a = x g (zero padding) and leaves each wave's partial sum of x^2
+// in sm[wave]; the weight stream starts as soon as a is in LDS, without
+// waiting for a block-wide reduction.
 __device__ __forceinline__ void stage_rms_deferred(const long long *__restrict__ xf,
                                                    const float *__restrict__ gain, int n, int npad,
                                                    float *a, float *sm,
@@ -595,10 +608,7 @@ __device__ __forceinline__ void stage_rms_deferred(const long long *__restrict__
             const int i = i0 + k * kThreads;
             const float x = from_fix(v[k]);
             ss = fmaf(x, x, ss);
-            if (i < npad) {
-                a[i] = x * gv[k];
-                a[npad + i] = gv[k];
-            }
+            if (i < npad) a[i] = x * gv[k];
         }
         if (first && (int)kl_tid() < ne) edst[kl_tid()] = ev;
     }
@@ -606,13 +616,81 @@ __device__ __forceinline__ void stage_rms_deferred(const long long *__restrict__
     if ((kl_tid() & 63) == 0) sm[kl_tid() >> 6] = ss;
     lds_barrier();
 }
+// The same for sequences 0 .. nb - 1 (nb <= kMultiSeq) together, their loads
+// issued in one batch: sequence b's residual row at xf + b xstride, its
+// staged vector at a + b astride, its wave sums at sm + b kSmSeq, and the ne
+// floats esrc(b) -> edst(b).  (Loads for b >= nb repeat sequence nb - 1's
+// and are dropped: every load stays unconditional.)  Half the batch per
+// sequence keeps the loads in flight within the registers the weight ring
+// leaves.  Each sequence's sums are those stage_rms_deferred leaves for it
+// alone only up to the order of the additions: the sum of a thread's terms is
+// taken in the same order, so the values are the same.
+constexpr int kSmSeq = kThreads / 64;   // floats between sequences' wave sums
+constexpr int kStageMulti = 4;          // loads per thread and sequence per batch
+struct NoExtra {   // stage_rms_multi without an extra vector
+    __device__ float *operator()(int) const { return nullptr; }
+};
+template <class ESrc, class EDst>
+__device__ __forceinline__ void stage_rms_multi(const long long *__restrict__ xf, int xstride,
+                                                const float *__restrict__ gain, int n, int npad,
+                                                int nb, float *a, int astride, float *sm,
+                                                ESrc &&esrc, EDst &&edst, int ne) {
+    float ss[kMultiSeq];
+#pragma unroll
+    for (int bb = 0; bb < kMultiSeq; ++bb) ss[bb] = 0.f;
+    for (int i0 = kl_tid(); i0 < npad; i0 += kStageMulti * kThreads) {
+        long long v[kMultiSeq][kStageMulti];
+        float gv[kStageMulti], ev[kMultiSeq];
+        const bool first = i0 == (int)kl_tid();
+#pragma unroll
+        for (int k = 0; k < kStageMulti; ++k) {
+            const int i = i0 + k * kThreads, ic = min(i, n - 1);
+            const float g = gain[ic];
+            gv[k] = i < n ? g : 0.f;
+#pragma unroll
+            for (int bb = 0; bb < kMultiSeq; ++bb) {
+                const long long xv =
+                    (long long)ld_dev_u64(xf + (size_t)min(bb, nb - 1) * xstride + ic);
+                v[bb][k] = i < n ? xv : 0ll;
+            }
+        }
+        if (first && (int)kl_tid() < ne) {
+#pragma unroll
+            for (int bb = 0; bb < kMultiSeq; ++bb) ev[bb] = esrc(min(bb, nb - 1))[kl_tid()];
+        }
+#pragma unroll
+        for (int bb = 0; bb < kMultiSeq; ++bb) {
+            if (bb < nb) {
+#pragma unroll
+                for (int k = 0; k < kStageMulti; ++k) {
+                    const int i = i0 + k * kThreads;
+                    const float x = from_fix(v[bb][k]);
+                    ss[bb] = fmaf(x, x, ss[bb]);
+                    if (i < npad) a[bb * astride + i] = x * gv[k];
+                }
+                if (first && (int)kl_tid() < ne) edst(bb)[kl_tid()] = ev[bb];
+            }
+        }
+    }
+#pragma unroll
+    for (int bb = 0; bb < kMultiSeq; ++bb) {
+        if (bb < nb) {
+            const float t = wave_sum(ss[bb]);
+            if ((kl_tid() & 63) == 0) sm[bb * kSmSeq + (kl_tid() >> 6)] = t;
+        }
+    }
+    lds_barrier();
+}
 // The scale r of the sequence staged last by stage_rms_deferred (the wave
 // partials are added in wave order: the same value in every thread).
 __device__ __forceinline__ float rms_scale(const float *sm, int n, float eps) {
     float ss = 0.f;
 #pragma unroll
-    for (int w = 0; w < kThreads / 64; ++w) ss += sm[w];
+    for (int w = 0; w < kSmSeq; ++w) ss += sm[w];
     return 1.0f / sqrtf(ss / (float)n + eps);
+}
+__device__ __forceinline__ float *seq_sm(const StepParams &P, const Lds &S, int b) {
+    return S.sm + (P.multi ? b * kSmSeq : 0);
 }
 
 // ---------------------------------------------------------------- GEMV engine
@@ -628,6 +706,8 @@ __device__ __forceinline__ float rms_scale(const float *sm, int n, float eps) {
 // before stage(b) (which fills a with sequence b's activation vector); each
 // next batch's first loads are issued before the previous batch's reduction.
 constexpr int kGemvDepth = 16;   // tile loads in flight per wave (16 KiB)
+// one sequence's GEMV partial sums in the reduction area (either row sharing)
+constexpr int kRedStride = kWaves * kRgBatch * kTileRows;
 
 // The ring of tile loads must stay in flight across loop iterations, the
 // grid barrier and the activation staging, and the compiler only places a
@@ -778,20 +858,186 @@ __device__ __forceinline__ void gemv_rows(const uint8_t *__restrict__ W, int KT,
     }
 }
 
+// Several sequences per pass (B <= kMultiSeq): every tile is applied to all
+// B staged vectors (astride floats apart; their partial sums kRedStride
+// floats apart in red), so the weights stream once for all of them.  The
+// activation reads from LDS then bound the pass, so a wave takes its row
+// groups kMultiRg at a time, interleaved tile by tile at each k (tiles
+// (r, k), (r + 1, k), ..., (r, k + 1), ...): one read of the B vectors at k
+// serves kMultiRg tiles.  A group short of kMultiRg real row groups is padded
+// with spare loads of the dummy line, whose products are dropped.  Every row
+// group's sums are taken in the same order as in gemv_rows, so the results
+// are those of B passes of one sequence.  With U a multiple of kMultiRg, a
+// group's tiles sit in consecutive ring slots, known at compile time in the
+// unrolled loop.
+constexpr int kMultiRg = 4;
+template <bool RowSplit, bool Early, bool Split, class Wait, class Stage, class Epi>
+__device__ __forceinline__ void gemv_rows_multi(const uint8_t *__restrict__ W, int KT, int first,
+                                                int count, int stride, int B,
+                                                const float *__restrict__ a, int astride,
+                                                float *red, const uint8_t *dummy, Wait &&wait,
+                                                Stage &&stage, Epi &&epi, int early_from) {
+    constexpr int U = kGemvDepth, NP = kMultiRg;
+    static_assert(U % NP == 0, "a ring slot's place in its group must be fixed");
+    constexpr int BATCH = RowSplit ? kWaves * kRgBatch : kRgBatch;
+    const int wid = __builtin_amdgcn_readfirstlane(kl_tid() >> 6);
+    const int lane = kl_tid() & 63;
+    const int row = lane >> 3, sub = lane & 7;
+    const int kt0 = RowSplit ? 0 : (wid * KT) / kWaves;
+    const int nk = RowSplit ? KT : ((wid + 1) * KT) / kWaves - kt0;
+    const int rsz = (RowSplit ? kWaves : 1) * stride * KT;   // tiles between a wave's row groups
+    const uint8_t *base = W + (size_t)lane * 16;
+    const float *abase = a + sub * 8;
+    u32x4 buf[U];
+    // loads: the wave's row groups gi .. gi + NP - 1 of the batch (mine of
+    // them), at k index lk; tile0 = the first row group's first tile
+    int n = 0, mine = 0, tile0 = 0, gi = 0, lk = 0;
+    auto load_h = [&](int h) {
+        const bool real = gi + h < mine;
+        const int t = __builtin_amdgcn_readfirstlane(tile0 + (gi + h) * rsz + lk);
+        const u32x4 v = ld_stream_16B(real ? base + (size_t)t * kTileBytes : dummy);
+        if (h == NP - 1) {
+            const bool wrap = lk + 1 == nk;
+            lk = wrap ? 0 : lk + 1;
+            gi = wrap ? gi + NP : gi;
+        }
+        return v;
+    };
+    auto start = [&](int ib) {
+        const int nb = min(BATCH, count - ib);
+        mine = RowSplit ? (nb > wid ? (nb - wid + kWaves - 1) / kWaves : 0) : nb;
+        n = nk * NP * ((mine + NP - 1) / NP);
+        tile0 = (first + (ib + (RowSplit ? wid : 0)) * stride) * KT + kt0;
+        gi = 0;
+        lk = 0;
+#pragma unroll
+        for (int s = 0; s < U; ++s) buf[s] = load_h(s % NP);
+    };
+    const bool compute = wid < kWaves;
+    const bool has_rows = count > 0;
+    const bool early = Early || (Split && wid >= early_from);
+    if (early && has_rows && compute) start(0);
+    wait();
+    if (!has_rows) return;
+    for (int ib = 0; ib < count; ib += BATCH) {
+        if (early) {
+            if (ib > 0 && compute) start(ib);
+            if (ib == 0)
+                for (int bb = 0; bb < B; ++bb) stage(bb);
+        } else {
+            if (ib == 0)
+                for (int bb = 0; bb < B; ++bb) stage(bb);
+            if (compute) start(ib);
+        }
+        const int nrg = min(BATCH, count - ib);
+        int cr = 0, ck = 0;   // the group in progress (its first row group), its k index
+        float acc[NP][kMultiSeq];
+#pragma unroll
+        for (int h = 0; h < NP; ++h)
+#pragma unroll
+            for (int bb = 0; bb < kMultiSeq; ++bb) acc[h][bb] = 0.f;
+        // a group's NP tiles sit in slots s .. s + NP - 1; they are consumed
+        // together (each sequence's vector read once for all of them), then
+        // refilled in order
+        if (compute)
+        for (int i0 = 0; i0 < n; i0 += U) {
+#pragma unroll
+            for (int s = 0; s < U; s += NP) {
+                if (i0 + s < n) {
+                    float wf[NP][8];
+#pragma unroll
+                    for (int h = 0; h < NP; ++h) {
+                        const u32x4 wv = buf[s + h];
+                        wf[h][0] = bf_lo(wv.x); wf[h][1] = bf_hi(wv.x);
+                        wf[h][2] = bf_lo(wv.y); wf[h][3] = bf_hi(wv.y);
+                        wf[h][4] = bf_lo(wv.z); wf[h][5] = bf_hi(wv.z);
+                        wf[h][6] = bf_lo(wv.w); wf[h][7] = bf_hi(wv.w);
+                    }
+#pragma unroll
+                    for (int bb = 0; bb < kMultiSeq; ++bb) {
+                        if (bb < B) {
+                            const float *ap = abase + bb * astride + (kt0 + ck) * kTileK;
+                            const float4 a0 = *reinterpret_cast<const float4 *>(ap);
+                            const float4 a1 = *reinterpret_cast<const float4 *>(ap + 4);
+                            const float av[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+#pragma unroll
+                            for (int h = 0; h < NP; ++h) {
+                                float v = acc[h][bb];
+#pragma unroll
+                                for (int e = 0; e < 8; ++e) v = fmaf(wf[h][e], av[e], v);
+                                acc[h][bb] = v;
+                            }
+                        }
+                    }
+                    if (++ck == nk) {   // the group's row groups are done
+#pragma unroll
+                        for (int hh = 0; hh < NP; ++hh) {
+                            const int c = cr + hh;   // the wave's c-th row group of the batch
+                            const int ri = RowSplit ? (wid + c * kWaves) * kTileRows + row
+                                                    : (wid * kRgBatch + c) * kTileRows + row;
+#pragma unroll
+                            for (int bb = 0; bb < kMultiSeq; ++bb) {
+                                if (bb < B) {
+                                    const float t = sum8(acc[hh][bb]);
+                                    if (c < mine && sub == 0) red[bb * kRedStride + ri] = t;
+                                }
+                                acc[hh][bb] = 0.f;
+                            }
+                        }
+                        ck = 0;
+                        cr += NP;
+                    }
+                }
+#pragma unroll
+                for (int h = 0; h < NP; ++h) buf[s + h] = load_h(h);
+            }
+        }
+        lds_barrier();
+        for (int t = kl_tid(); t < B * nrg * (kTileRows / 2); t += kThreads) {
+            const int bb = t / (nrg * (kTileRows / 2)), tt = t - bb * (nrg * (kTileRows / 2));
+            const int rgi = tt / (kTileRows / 2), pr = (tt % (kTileRows / 2)) * 2;
+            const float *rd = red + bb * kRedStride;
+            float y0 = 0.f, y1 = 0.f;
+            if (RowSplit) {
+                y0 = rd[rgi * kTileRows + pr];
+                y1 = rd[rgi * kTileRows + pr + 1];
+            } else {
+                for (int w = 0; w < kWaves; ++w) {
+                    if (((w + 1) * KT) / kWaves == (w * KT) / kWaves) continue;   // empty slice
+                    y0 += rd[(w * kRgBatch + rgi) * kTileRows + pr];
+                    y1 += rd[(w * kRgBatch + rgi) * kTileRows + pr + 1];
+                }
+            }
+            epi(bb, (first + (ib + rgi) * stride) * kTileRows + pr, y0, y1);
+        }
+        lds_barrier();
+    }
+}
+
 // Row groups are shared split-K when they are long enough for every wave to
-// hold two or more tiles, else row-split.
-template <bool Early, bool Split = false, class Wait, class Stage, class Epi>
+// hold two or more tiles, else row-split.  Multi: the B sequences share each
+// pass (gemv_rows_multi).
+template <bool Early, bool Split = false, bool Multi = false, class Wait, class Stage, class Epi>
 __device__ __forceinline__ void gemv_phase(const uint8_t *__restrict__ W, int KT, int first,
                                            int count, int stride, int B,
                                            const float *__restrict__ a, float *red,
                                            const uint8_t *dummy, Wait &&wait, Stage &&stage,
-                                           Epi &&epi, int early_from = kWaves + 1) {
-    if (KT >= 2 * kWaves)
-        gemv_rows<false, Early, Split>(W, KT, first, count, stride, B, a, red, dummy, wait,
-                                       stage, epi, early_from);
-    else
+                                           Epi &&epi, int early_from = kWaves + 1,
+                                           int astride = 0) {
+    if constexpr (Multi) {
+        if (KT >= 2 * kWaves)
+            gemv_rows_multi<false, Early, Split>(W, KT, first, count, stride, B, a, astride, red,
+                                                 dummy, wait, stage, epi, early_from);
+        else
+            gemv_rows_multi<true, Early, Split>(W, KT, first, count, stride, B, a, astride, red,
+                                                dummy, wait, stage, epi, early_from);
+    } else if (KT >= 2 * kWaves) {
+        gemv_rows<false, Early, Split>(W, KT, first, count, stride, B, a, red, dummy, wait, stage,
+                                       epi, early_from);
+    } else {
         gemv_rows<true, Early, Split>(W, KT, first, count, stride, B, a, red, dummy, wait, stage,
                                       epi, early_from);
+    }
 }
 
 // ---------------------------------------------------------------- batched engine
@@ -1065,15 +1311,24 @@ __device__ __forceinline__ void gemm_rows(const uint8_t *__restrict__ W, int KT,
 struct NoGroupDone {
     __device__ void operator()(int, int) const {}
 };
+// Per-sequence path: with P.multi, the sequences' vectors sit astride floats
+// apart and share each pass (stage1(b) is called for every b before the
+// pass; stage1(0) may stage them all).
 template <bool BAT, bool Early = true, class Wait, class Prep, class Stage1, class StageB,
           class Epi, class Done = NoGroupDone>
 __device__ __forceinline__ void weight_phase(const StepParams &P, const Lds &S,
                                              const uint8_t *W, int KT, int first, int count,
                                              Wait &&wait, Prep &&prep, Stage1 &&stage1,
                                              StageB &&stageb, Epi &&epi, int ktg = 0,
-                                             size_t gstride = 0, Done done = Done()) {
+                                             size_t gstride = 0, Done done = Done(),
+                                             int astride = 0) {
     if constexpr (!BAT) {
-        gemv_phase<Early>(W, KT, first, count, 1, P.B, S.a, S.red, P.dummy, wait, stage1, epi);
+        if (P.multi)
+            gemv_phase<Early, false, true>(W, KT, first, count, 1, P.B, S.a, S.red, P.dummy, wait,
+                                           stage1, epi, kWaves + 1, astride);
+        else
+            gemv_phase<Early>(W, KT, first, count, 1, P.B, S.a, S.red, P.dummy, wait, stage1,
+                              epi);
         return;
     }
     const GemmLds L = gemm_lds(kl_smem);
@@ -1451,15 +1706,25 @@ __device__ __forceinline__ void phase_qkv(KArg ka, int l, int gwait, int qbar, i
         P, S, Lb + P.off_qkv, P.Hp / kTileK, g * P.qkv_rg + a0, a1 - a0,
         [&]() { if (gwait >= 0) bar_wait(P, gwait, ti); }, [&]() {},
         [&](int b) {
-            // the RoPE row of this sequence's position rides along (a + 2 Hp)
-            stage_rms_deferred(P.xf + (size_t)b * P.Hp, gain, P.H, P.Hp, S.a, S.sm,
-                               reinterpret_cast<const float *>(P.rope + (size_t)pos_of<true>(P, b) * half),
-                               S.a + 2 * P.Hp, 2 * half);
+            // the RoPE row of the sequence's position rides along (rope_row)
+            auto rsrc = [&](int bb) {
+                return reinterpret_cast<const float *>(P.rope +
+                                                       (size_t)pos_of<true>(P, bb) * half);
+            };
+            if (P.multi) {
+                if (b == 0)
+                    stage_rms_multi(P.xf, P.Hp, gain, P.H, P.Hp, P.B, S.a, P.Hp, S.sm, rsrc,
+                                    [&](int bb) { return rope_row(P, S, bb); }, 2 * half);
+            } else {
+                stage_rms_deferred(P.xf + (size_t)b * P.Hp, gain, P.H, P.Hp, S.a, S.sm, rsrc(b),
+                                   rope_row(P, S, b), 2 * half);
+            }
             if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 3);
         },
         [&](int, int, int, uint16_t *) {},
         [&](int b, int r, float y0, float y1) {
-            const float rs = rms_scale(S.sm, P.H, P.eps);   // the deferred RMSNorm scale
+            // the deferred RMSNorm scale
+            const float rs = rms_scale(seq_sm(P, S, b), P.H, P.eps);
             y0 *= rs;
             y1 *= rs;
             if (P.qkv_bias) {   // (packed row order)
@@ -1468,9 +1733,10 @@ __device__ __forceinline__ void phase_qkv(KArg ka, int l, int gwait, int qbar, i
                 y1 += bias[r + 1];
             }
             qkv_store<true>(P, l, b, g, r - row0, y0, y1, [&](int, int i) {
-                return reinterpret_cast<const float2 *>(S.a + 2 * P.Hp)[i];
+                return reinterpret_cast<const float2 *>(rope_row(P, S, b))[i];
             }, ll_tag(P, l));
-        });
+        },
+        0, 0, NoGroupDone(), P.Hp);
     // (the attention polls the tagged words: no drain, no counter)
     if (is_ctl_lane0()) trace_stamp(P, ti, 0);
 }
@@ -1482,13 +1748,13 @@ __device__ __forceinline__ void phase_qkv(KArg ka, int l, int gwait, int qbar, i
 // chunk).  The results arrive as tagged words, kMergeChunks chunks per round;
 // a later round rescales the running sums to its new maximum.  Chunks are
 // taken in order, so the sums are the same in every schedule.  Threads
-// 0 .. NT - 1 gather the results; leaves o in S.a[0 .. D).
+// 0 .. NT - 1 gather the results; leaves o[0 .. D) (LDS), with the LDS
+// area scr for the chunk results.
 template <int D, int G, int NT = kThreads>
 __device__ __forceinline__ void merge_ll(const StepParams &P, int l, int b, int g, int hq,
-                                         const Lds &S) {
+                                         float *o, float *scr) {
     constexpr int WD = D + 2;                       // words per chunk and head
-    float *o = S.a;                                 // [D]
-    float *wts = S.a + D;                           // [kMergeChunks]
+    float *wts = scr;                               // [kMergeChunks]
     float *run = wts + kMergeChunks;                // running max, running sum, rescale
     float *raw = run + 4;                           // [kMergeChunks][D + 2] values
     const unsigned tag = ll_tag(P, l);
@@ -1534,6 +1800,57 @@ __device__ __forceinline__ void merge_ll(const StepParams &P, int l, int b, int 
         lds_barrier();
     }
     for (int t = kl_tid(); t < D; t += kThreads) o[t] = o[t] / run[1];
+    lds_barrier();
+}
+// The same for sequences 0 .. nb - 1 together (nb C <= kMergeChunks): one
+// gather of all their chunk results, then wave b forms sequence b's chunk
+// weights and sum; sequence b's output goes to S.a + b D.  Each output is
+// the one merge_ll gives for its sequence alone (a single round there).
+template <int D, int G, int NT = kThreads>
+__device__ __forceinline__ void merge_ll_multi(const StepParams &P, int l, int nb, int g, int hq,
+                                               const Lds &S) {
+    constexpr int WD = D + 2;
+    float *wts = S.a + kMultiSeq * D;               // [nb][C]
+    float *den = wts + kMergeChunks;                // [nb]
+    float *raw = den + 4;                           // [nb][C][D + 2] values
+    const unsigned tag = ll_tag(P, l);
+    const int C = P.C, per = C * WD;
+    const size_t sstride = (size_t)P.nkv * G * per;   // words between sequences
+    const unsigned long long *src = P.po_ll + ((size_t)g * G + hq) * per;
+    if (NT == kThreads || kl_tid() < NT)
+        ll_gather<(kMergeChunks * WD + NT - 1) / NT>(
+            P, nb * per, tag, kl_tid(), NT,
+            [&](int i) {
+                const int bb = i / per;
+                return src + bb * sstride + (i - bb * per);
+            },
+            [&](int i, unsigned v) { raw[i] = __uint_as_float(v); });
+    lds_barrier();
+    const int wid = kl_tid() >> 6;
+    if (wid < nb) {
+        const int lane = kl_tid() & 63;
+        const float *rv = raw + wid * per;
+        float mx = -INFINITY;
+        for (int c = lane; c < C; c += 64) mx = fmaxf(mx, rv[c * WD + D]);
+        mx = wave_max(mx);
+        float dn = 0.f;
+        for (int c = lane; c < C; c += 64) {
+            const float m = rv[c * WD + D];
+            const float w = (m == -INFINITY) ? 0.f : expf(m - mx);
+            wts[wid * C + c] = w;
+            dn = fmaf(rv[c * WD + D + 1], w, dn);
+        }
+        dn = wave_sum(dn);
+        if (lane == 0) den[wid] = 0.f + dn;
+    }
+    lds_barrier();
+    for (int t = kl_tid(); t < nb * D; t += kThreads) {
+        const int bb = t / D, j = t - bb * D;
+        const float *rv = raw + bb * per;
+        float acc = 0.f;
+        for (int c = 0; c < C; ++c) acc = fmaf(wts[bb * C + c], rv[c * WD + j], acc);
+        S.a[bb * D + j] = acc / den[bb];
+    }
     lds_barrier();
 }
 
@@ -2134,18 +2451,28 @@ __device__ __forceinline__ void phase_oproj(KArg ka, int l, int gwait, int mbar,
             constexpr int NTM = SPLIT ? kOEarly * 64 : kThreads;
             const int mine = ((a1 - a0) + kWaves - 1) / kWaves * KTq;   // tiles per wave, at most
             const int EW = SPLIT && mine <= kGemvDepth ? kOEarly : kWaves + 1;
-            gemv_phase<false, SPLIT>(
-                Wo + (size_t)(g * G + hq) * P.o_rg * KTq * kTileBytes, KTq, a0, a1 - a0, 1, P.B,
-                S.a, S.red, P.dummy, [&]() {},
-                [&](int b) {
-                    if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 1);
-                    merge_ll<D, G, NTM>(P, l, b, g, hq, S);
-                    if (b == 0 && is_ctl_lane0()) {
-                        trace_stamp(P, ti, 2);
-                        trace_stamp(P, ti, 3);
-                    }
-                },
-                epi, EW);
+            auto stage = [&](int b) {
+                if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 1);
+                // (with P.multi sequence b's output goes to S.a + b D; all
+                // sequences in one gather when their chunks fit)
+                if (!P.multi)
+                    merge_ll<D, G, NTM>(P, l, b, g, hq, S.a, S.a + D);
+                else if (P.B * P.C > kMergeChunks)
+                    merge_ll<D, G, NTM>(P, l, b, g, hq, S.a + b * D, S.a + kMultiSeq * D);
+                else if (b == 0)
+                    merge_ll_multi<D, G, NTM>(P, l, P.B, g, hq, S);
+                if (b == 0 && is_ctl_lane0()) {
+                    trace_stamp(P, ti, 2);
+                    trace_stamp(P, ti, 3);
+                }
+            };
+            const uint8_t *W = Wo + (size_t)(g * G + hq) * P.o_rg * KTq * kTileBytes;
+            if (P.multi)
+                gemv_phase<false, SPLIT, true>(W, KTq, a0, a1 - a0, 1, P.B, S.a, S.red, P.dummy,
+                                               [&]() {}, stage, epi, EW, D);
+            else
+                gemv_phase<false, SPLIT>(W, KTq, a0, a1 - a0, 1, P.B, S.a, S.red, P.dummy,
+                                         [&]() {}, stage, epi, EW);
         }
     }
     if (garrive >= 0) bar_arrive(P, garrive, ti);
@@ -2370,17 +2697,25 @@ __device__ __forceinline__ void phase_gateup(KArg ka, int l, int gwait, int garr
         P, S, Lb + P.off_gu, P.Hp / kTileK, first, count,
         [&]() { if (gwait >= 0) bar_wait(P, gwait, ti); }, [&]() {},
         [&](int b) {
-            stage_rms_deferred(P.xf + (size_t)b * P.Hp, gain, P.H, P.Hp, S.a, S.sm);
+            if (P.multi) {
+                if (b == 0)
+                    stage_rms_multi(P.xf, P.Hp, gain, P.H, P.Hp, P.B, S.a, P.Hp, S.sm, NoExtra(),
+                                    NoExtra(), 0);
+            } else {
+                stage_rms_deferred(P.xf + (size_t)b * P.Hp, gain, P.H, P.Hp, S.a, S.sm);
+            }
             if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 3);
         },
         [&](int, int, int, uint16_t *) {},
         [&](int b, int r, float gt, float up) {
-            const float rs = rms_scale(S.sm, P.H, P.eps);   // the deferred RMSNorm scale
+            // the deferred RMSNorm scale
+            const float rs = rms_scale(seq_sm(P, S, b), P.H, P.eps);
             gt *= rs;
             up *= rs;
             st_ll_f(P.m_ll + (size_t)b * P.Fp + (r >> 1), gt / (1.0f + expf(-gt)) * up,
                     ll_tag(P, l));
-        });
+        },
+        0, 0, NoGroupDone(), P.Hp);
     // (the down projection polls the tagged words: no drain, no counter)
     if (is_ctl_lane0()) trace_stamp(P, ti, 0);
 }
@@ -2494,21 +2829,42 @@ __device__ __forceinline__ void phase_down(KArg ka, int l, int gwait, int xbar, 
                 [&](int b) {
                     // block j of the SwiGLU output as tagged words, gathered
                     // by the control wave (its loads are not queued behind
-                    // the weight ring); padding columns are zero
+                    // the weight ring); padding columns are zero.  With
+                    // P.multi the first call gathers every sequence's block
+                    // (block of sequence bb at a + bb kw).
                     if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 1);
-                    if ((kl_tid() >> 6) == kCtlWave)
-                        ll_gather<kDownGather>(
-                            P, nreal, ll_tag(P, l), kl_tid() & 63, 64,
-                            [&](int i) { return P.m_ll + (size_t)b * P.Fp + c0 + i; },
-                            [&](int i, unsigned v) { S.a[i] = __uint_as_float(v); });
-                    for (int i = nreal + kl_tid(); i < kw; i += kThreads) S.a[i] = 0.f;
+                    if (P.multi) {
+                        if (b > 0) return;
+                        if ((kl_tid() >> 6) == kCtlWave)
+                            ll_gather<kDownGather>(
+                                P, P.B * nreal, ll_tag(P, l), kl_tid() & 63, 64,
+                                [&](int i) {
+                                    const int bb = i / nreal;
+                                    return P.m_ll + (size_t)bb * P.Fp + c0 + (i - bb * nreal);
+                                },
+                                [&](int i, unsigned v) {
+                                    const int bb = i / nreal;
+                                    S.a[bb * kw + (i - bb * nreal)] = __uint_as_float(v);
+                                });
+                        for (int i = kl_tid(); i < P.B * (kw - nreal); i += kThreads) {
+                            const int bb = i / (kw - nreal);
+                            S.a[bb * kw + nreal + (i - bb * (kw - nreal))] = 0.f;
+                        }
+                    } else {
+                        if ((kl_tid() >> 6) == kCtlWave)
+                            ll_gather<kDownGather>(
+                                P, nreal, ll_tag(P, l), kl_tid() & 63, 64,
+                                [&](int i) { return P.m_ll + (size_t)b * P.Fp + c0 + i; },
+                                [&](int i, unsigned v) { S.a[i] = __uint_as_float(v); });
+                        for (int i = nreal + kl_tid(); i < kw; i += kThreads) S.a[i] = 0.f;
+                    }
                     lds_barrier();
                     if (b == 0 && is_ctl_lane0()) {
                         trace_stamp(P, ti, 2);
                         trace_stamp(P, ti, 3);
                     }
                 },
-                [&](int, int, int, uint16_t *) {}, epi);
+                [&](int, int, int, uint16_t *) {}, epi, 0, 0, NoGroupDone(), kw);
         }
     }
     if (garrive >= 0) bar_arrive(P, garrive, ti);
@@ -2565,13 +2921,19 @@ __device__ __forceinline__ void phase_head(KArg ka, int gwait, int ti) {
             if (blockIdx.x == 0 && P.hidden_out) copy_hidden<!BAT>(P);
         },
         [&](int b) {
-            stage_rms_deferred(P.xf + (size_t)b * P.Hp, P.final_norm, P.H, P.Hp, S.a, S.sm);
+            if (P.multi) {
+                if (b == 0)
+                    stage_rms_multi(P.xf, P.Hp, P.final_norm, P.H, P.Hp, P.B, S.a, P.Hp, S.sm,
+                                    NoExtra(), NoExtra(), 0);
+            } else {
+                stage_rms_deferred(P.xf + (size_t)b * P.Hp, P.final_norm, P.H, P.Hp, S.a, S.sm);
+            }
             if (b == 0 && is_ctl_lane0()) trace_stamp(P, ti, 3);
         },
         [&](int c, int b0, int nb, uint16_t *buf) { stage_act_chunk(P, c, b0, nb, buf); },
         [&](int b, int r, float y0, float y1) {
             // the deferred RMSNorm scale
-            const float rs = !BAT ? rms_scale(S.sm, P.H, P.eps) : rms_of(P, S, b);
+            const float rs = !BAT ? rms_scale(seq_sm(P, S, b), P.H, P.eps) : rms_of(P, S, b);
             y0 *= rs;
             y1 *= rs;
             const bool ok = ok_of<!BAT>(P, b);
@@ -2586,7 +2948,7 @@ __device__ __forceinline__ void phase_head(KArg ka, int gwait, int ti) {
                                        __HIP_MEMORY_SCOPE_WORKGROUP);
             }
         },
-        0, 0, [&](int b0, int nb) { flush(b0, nb); });
+        0, 0, [&](int b0, int nb) { flush(b0, nb); }, P.Hp);
     if (!BAT) flush(0, P.B);
     // the step's last phase: the next step's tags (every workgroup of every
     // launch of this step read the epoch at its start)

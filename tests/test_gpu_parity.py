@@ -164,10 +164,12 @@ def test_llama8b_width_two_layers_long_cache():
     assert_bit_exact(outs[2], outs[1], "per_op vs looped")
 
 
-@pytest.mark.parametrize("batch", [2, 3, 8, 16, 32])
+@pytest.mark.parametrize("batch", [2, 3, 4, 5, 8, 16, 32])
 def test_tiny_batched_matrix_core_path(batch):
-    # batches >= 2 run the weight products on the matrix cores (bf16
-    # activations); ragged positions, all schedules bit-identical
+    # batches 2 .. 4 share each GEMV pass (the attention merge one sequence
+    # at a time: their chunks exceed one gather), from 5 on the weight
+    # products run on the matrix cores (bf16 activations); ragged
+    # positions, all schedules bit-identical
     say(f"[tiny-batched] batch={batch}")
     rng = np.random.default_rng(batch)
     filled = rng.integers(0, 190, size=batch).astype(np.int32)
@@ -188,12 +190,13 @@ def test_batched_path_with_batch_above_one_group():
     check_against_oracle(c, c.gpu_step(kb.KL_MODE_LOOPED), ref)
 
 
-@pytest.mark.parametrize("batch", [2, 5, 8, 16, 32])
+@pytest.mark.parametrize("batch", [2, 3, 4, 5, 8, 16, 32])
 def test_llama8b_width_two_layers_batched(batch):
-    # the 8B layer shapes on the matrix-core path (every batch from 2 on for
-    # a dense model), 256-position caches: below 32 several attention chunks
-    # per (sequence, KV head) with the grid-wide merge (16, 6, 4 and 2
-    # chunks), at batch 32 one chunk
+    # the 8B layer shapes, 256-position caches: batches 2 .. 4 on the GEMV
+    # path with the sequences sharing each pass (16, 10 and 8 attention
+    # chunks per (sequence, KV head), merged in one gather), from 5 on the
+    # matrix-core path: below 32 several chunks with the grid-wide merge (6,
+    # 4 and 2 chunks), at batch 32 one chunk
     cfg = dict(WORKLOADS["llama8b-b32-ctx4096"]["model"], n_layers=2)
     say(f"[8b-width L=2 B={batch}] building")
     filled = (np.arange(batch, dtype=np.int32) * 37) % 250
@@ -283,11 +286,28 @@ def test_per_layer_graph_replays_match_looped(shape):
 
 def test_matrix_core_batch_per_model():
     """kl_info.mfma_min_batch: a dense model takes the matrix-core path from
-    batch 2 (the GEMV path streams the weights once per sequence); with
+    batch 5 (up to 4 sequences share each pass of the GEMV path); with
     experts, the GEMV path (per-token routing) runs below batch 8."""
-    for cfg, want in ((dict(TINY, n_layers=1), 2),
+    for cfg, want in ((dict(TINY, n_layers=1), 5),
                       (dict(TINY, n_layers=1, n_experts=4, top_k=2), 8)):
         weights = synth.model_host(cfg, 5, 4)
         m = GpuModel(cfg, weights, 8, 64)
         assert m.info().mfma_min_batch == want, (cfg, m.info().mfma_min_batch)
         m.close()
+
+
+@pytest.mark.parametrize("batch", [2, 4])
+def test_shared_gemv_pass_in_a_model_sized_for_more(batch):
+    """Batches 2 and 4 of a model allocated for 8 sequences (the LDS holds
+    both engines' areas): the shared GEMV pass against the oracle, and each
+    schedule bit-identical."""
+    cfg = dict(WORKLOADS["llama8b-b32-ctx4096"]["model"], n_layers=2)
+    say(f"[8b-width L=2 B={batch} of 8] building")
+    filled = (np.arange(batch, dtype=np.int32) * 53 + 11) % 250
+    c = Case(cfg, batch, 256, filled, seed=91 + batch, max_batch=8)
+    ref = c.oracle_step(nthreads=8)
+    outs = [c.gpu_step(mode) for _, mode in MODES]
+    check_against_oracle(c, outs[1], ref)
+    assert_bit_exact(outs[0], outs[1], "per_layer vs looped")
+    assert_bit_exact(outs[2], outs[1], "per_op vs looped")
+    c.model.close()
