@@ -27,16 +27,17 @@ constexpr int kCombBatch = 32;            // chunk partials loaded together when
 // chunks of kGemmChunkK columns for up to kGemmBatch sequences at a time,
 // weight rows in blocks of 16.
 constexpr int kMfmaBatch = 8;
-// Dense models take the matrix-core path from batch kBatchedFrom on.  The GEMV
-// path streams the weights once per sequence, so its step time grows with the
-// batch (8B shape, 4096 cached positions: 3.06, 5.61, 10.6, 18.0 ms at batch
-// 1, 2, 4, 7), while the matrix-core path streams them once (5.44 ms at
-// batch 8).  A mixture of experts keeps the GEMV path below kMfmaBatch (its
-// experts are chosen per token on that path).
-constexpr int kBatchedFrom = 2;
 // Up to kMultiSeq sequences share one pass of the GEMV engine: each weight
-// tile is applied to every staged vector, so the weights stream once.
+// tile is applied to every staged vector, so the weights stream once (8B
+// shape, 4096 cached positions: 3.06, 3.52, 3.91, 4.35 ms at batch 1-4,
+// against 5.0 ms on the matrix-core path).  Dense models take the
+// matrix-core path from batch kMultiSeq + 1 on, or from kBatchedFrom where
+// the LDS cannot hold the shared pass's vectors beside the matrix-core
+// engine's area (one sequence per pass: 5.61 ms at batch 2).  A mixture of
+// experts keeps the GEMV path below kMfmaBatch (its experts are chosen per
+// token on that path).
 constexpr int kMultiSeq = 4;
+constexpr int kBatchedFrom = 2;
 constexpr int kGemmBatch = 32;
 constexpr int kGemmChunkK = 512;
 constexpr int kActStride = kGemmChunkK + 8;   // bf16 per staged activation row (bank spread)

@@ -1,6 +1,7 @@
 """Parity at the benchmarked sizes: the full 8B-shape model (32 layers) at
-batch 1 with a 4096- and a 65536-position cache, and at batch 32, against the
-oracle.  At batch 32 the oracle evaluates a sample of the sequences (the
+batch 1 with a 4096- and a 65536-position cache, at batch 4 (the sequences
+sharing each GEMV pass) and at batch 32, against the oracle.  At batches 4
+and 32 the oracle evaluates a sample of the sequences (the
 sequences of a step are independent, so the oracle runs them on their own:
 their tokens, positions and caches), in the launch configuration the bench
 times (looped schedule, one launch per step).  At batch 1 with 4096 cached
@@ -73,6 +74,10 @@ def test_llama8b_batch1_ctx4096_full_model_all_schedules():
 
 def test_llama8b_batch1_ctx65536_full_model():
     run_workload("llama8b-b1-ctx65536", [0])
+
+
+def test_llama8b_batch4_full_model_sampled_two_schedules():
+    run_workload("llama8b-b4-ctx4096", [0, 3], modes=("looped", "per_layer"))
 
 
 def test_llama8b_batch32_full_model_sampled():
