@@ -212,12 +212,14 @@ def test_llama8b_width_two_layers_batched(batch):
     assert_bit_exact(outs[2], outs[1], "per_op vs looped")
 
 
-@pytest.mark.parametrize("batch", [1, 8, 32])
+@pytest.mark.parametrize("batch", [1, 3, 8, 32])
 def test_llama70b_width_two_layers(batch):
     # the 70B layer shapes (hidden 8192, 64 query / 8 KV heads: 8 query heads
     # per KV head, FFN 28672) with 2 layers, loaded one layer at a time; at
-    # batch 32 one attention chunk per (sequence, KV head) with 8 query heads
-    # per KV head (the oracle evaluates a sample of the sequences)
+    # batch 3 the sequences share each GEMV pass (the O projection without
+    # its wave split); at batch 32 one attention chunk per (sequence, KV
+    # head) with 8 query heads per KV head (the oracle evaluates a sample of
+    # the sequences)
     from paper_2410_23668_amd.device import GpuModel
     cfg = dict(WORKLOADS["llama70b-b1-ctx4096"]["model"], n_layers=2)
     say(f"[70b-width L=2 B={batch}] building")

@@ -31,20 +31,20 @@ def run_case(tag, cfg, batch, capacity, seed, sample=None):
     c.model.close()
 
 
-@pytest.mark.parametrize("batch", [1, 8])
+@pytest.mark.parametrize("batch", [1, 2, 8])
 def test_tiny_with_qkv_bias(batch):
     run_case(f"tiny+bias B={batch}", dict(TINY, qkv_bias=True), batch, 192, 301 + batch)
 
 
-@pytest.mark.parametrize("batch", [1, 8])
+@pytest.mark.parametrize("batch", [1, 4, 8])
 def test_llama3b_width_tied_embeddings_group3(batch):
     run_case(f"3b-width L=2 B={batch}", dict(LLAMA3B, n_layers=2), batch, 256, 311 + batch)
 
 
-@pytest.mark.parametrize("batch", [1, 16])
+@pytest.mark.parametrize("batch", [1, 2, 16])
 def test_qwen72b_width_qkv_bias(batch):
     run_case(f"qwen72b-width L=2 B={batch}", dict(QWEN72B, n_layers=2), batch, 256, 321 + batch,
-             sample=None if batch == 1 else [0, 9, 15])
+             sample=None if batch <= 2 else [0, 9, 15])
 
 
 def test_llama8b_width_batch16_ctx8192():
