@@ -44,7 +44,7 @@ WORKLOADS = {
     "llama8b-b8-ctx16384": _wl("llama8b-b8-ctx16384", LLAMA8B, 8, 16384, 7),
     "llama8b-b16-ctx8192": _wl("llama8b-b16-ctx8192", LLAMA8B, 16, 8192, 8),
     "mixtral-b1-ctx4096": _wl("mixtral-b1-ctx4096", MIXTRAL, 1, 4096, 9),
-    # small batches (the matrix-core path from batch 2)
+    # small batches (the sequences share each GEMV pass)
     "llama8b-b2-ctx4096": _wl("llama8b-b2-ctx4096", LLAMA8B, 2, 4096, 10),
     "llama8b-b4-ctx4096": _wl("llama8b-b4-ctx4096", LLAMA8B, 4, 4096, 11),
 }
