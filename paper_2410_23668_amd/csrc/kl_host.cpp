@@ -146,7 +146,8 @@ void lds_layout_for(kl_state &s) {
     // item) a sub-chunk's scores, the softmax state and the waves' outputs
     const int hg = std::min(g, 4);
     const int sub = kWaves * kAttnLoads * (64 / (d / 8));
-    const int attn_main = std::max(g * d + 2 * kWaves * hg + kWaves * hg * d + d,
+    // (+ the streaming item's per-wave score tiles, 16 x 16 floats)
+    const int attn_main = std::max(g * d + 2 * kWaves * hg + kWaves * hg * d + d + kWaves * 256,
                                    g * d + g * sub + g * 4 + kWaves * g * d + d);
     // O projection: o, chunk weights, running sums, the chunk results
     const int oproj_stage = d + kMergeChunks + 4 + kMergeChunks * (d + 2);
