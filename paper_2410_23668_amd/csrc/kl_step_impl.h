@@ -2134,10 +2134,11 @@ __device__ __forceinline__ void attn_item_stream(KArg ka, int l, int b, int g, i
     // round is columns 32 ks + 8 (l / 16) .. + 7 of tile row l % 16 (slab
     // (l % 16) / PP, position (l % 16) % PP).  The tile goes through a
     // per-wave LDS slot to the lanes of its positions; the softmax and the
-    // values stay on the vector units.  (8B shape, batch 32: attention 112 ->
-    // 95 us per layer.  The per-sequence path's chunks are a few rounds long,
-    // where the vector-unit scores measured faster: 70B shape, batch 1,
-    // 23.8 against 24.2 ms per step.)
+    // values stay on the vector units.  (Step time, same device: 8B shape,
+    // batch 32, 8.07 -> 7.97 ms; 70B shape, batch 32, 47.1-47.8 -> 46.3-46.7
+    // ms.  The per-sequence path's chunks are a few rounds long, where the
+    // vector-unit scores measured faster: 70B shape, batch 1, 23.8 against
+    // 24.2 ms.)
     constexpr bool MC = D == 128 && !LL;
     static_assert(!MC || (R * PP == 16 && R * 32 == D), "one 16-row tile per ring round");
     // more than 4 query heads per KV head: the waves split into NH teams of
