@@ -141,7 +141,7 @@ int batched_k_slices(int n, int t, int nblk, int nwg) {
 // every workgroup kWaves / 2 blocks or more; failing that, batched_k_slices.
 // Fewer slices halve what the fold reads.  (8B shape, batch 32: 7.95 ms with
 // 4 gate/up and 8 q/k/v slices, 7.48 with 2 and 4; the same for the O and
-// down products, whose partials the next RMSNorm folds, measured slower.)
+// down products, whose partials the next RMSNorm folds, gained nothing.)
 int folded_k_slices(int n, int t, int nblk, int nwg) {
     for (int s = 1; s <= std::min(n, kMaxKSlices); ++s) {
         if (n % s || (n / s) * t * kTileK > 2 * kGemmResidentK) continue;
